@@ -1,0 +1,206 @@
+"""Benchmark: fwd+bwd of the segmented gated linear recurrence layer on one MI355X.
+
+One step = chain_fwd + chain_bwd over the whole sequence of the workload
+(every kernel of the hot path: prep, state scan, output walk, and the
+backward's replay, scans, dq walk and dk/dv/dg walk), inputs resident in HBM.
+Default workload: B=1, H=40, d=128, L=262144 in 8 nonuniform segments
+(the 256K-context layer of a hidden-5120 model), bf16 I/O, fp32 state.
+
+Prints one JSON line ("Measurement").
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15   # dense bf16 MFMA, FLOP/s
+PEAK_HBM = 8.0e12    # HBM3E, B/s
+METRIC = "fwd+bwd tokens/s per layer (H=40,d=128, 256K ctx); % bf16 MFMA peak"
+
+# interface bytes per token-head that each kernel must move (io = element bytes, D = head dim):
+#   fwd_prep: k, v, g            fwd_out: q, k, v, g in; o out
+#   bwd_prep: q, k, v, dO, g     bwd_dq: dO, v, k, q, g in; dq, dg out
+#   bwd_dkv:  q, k, v, dO, g, dg in; dk, dv, dg out
+KERNEL_BYTES = {
+    "fwd_prep": lambda D, io: 2 * D * io + 4,
+    "fwd_out": lambda D, io: 4 * D * io + 4,
+    "bwd_prep": lambda D, io: 4 * D * io + 4,
+    "bwd_dq": lambda D, io: 5 * D * io + 8,
+    "bwd_dkv": lambda D, io: 6 * D * io + 12,
+}
+
+
+def alg_flops_per_token_head(D, C=64):
+    """Causal-tile algorithmic flops of one fwd+bwd per token and head (see
+    the design doc): fwd (C+1)(2D) + 4 D^2; bwd incl. the state replay
+    (C+1)(5D) + 10 D^2."""
+    return (C + 1) * 2 * D + 4 * D * D + (C + 1) * 5 * D + 10 * D * D
+
+
+def alg_bytes_per_token_head(D, io):
+    """Every interface tensor touched once: fwd q,k,v in, o out, g in;
+    bwd q,k,v,dO,g in, dq,dk,dv,dg out."""
+    return (4 * D * io + 4) + (7 * D * io + 8)
+
+
+def kernel_src_hash():
+    h = hashlib.sha256()
+    for f in ("sf_kernels.hip", "sf_device.hpp"):
+        with open(os.path.join(ROOT, "paper_2608_06838_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(kernel):
+    """HBM bytes per launch for `kernel` from the committed rocprofv3 counter
+    summary, or None when absent or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_ctx256k_h40.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for ln in f:
+            if "=" in ln and not ln.startswith("#"):
+                a, b = ln.split("=", 1)
+                kv[a.strip()] = b.strip()
+    if kv.get("src_sha") != kernel_src_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, inp, budget_s=15.0):
+    """Time the fp64 oracle (fwd + bwd) on the host cores on a bounded sample of
+    the same workload: the first n_h heads of batch 0 over the first L_s tokens."""
+    import numpy as np
+    import oracle
+
+    cores = len(os.sched_getaffinity(0))
+    nh = min(w["H"], cores)
+
+    def sample(L_s):
+        sl = {k: inp[k][:1, :L_s, :nh] for k in ("q", "k", "v", "g", "dO")}
+        return {k: v.detach().cpu().double().numpy() for k, v in sl.items()}
+
+    def run(s):
+        t0 = time.perf_counter()
+        _, _, _ = oracle.forward(s["q"], s["k"], s["v"], s["g"], None, threads=nh)
+        oracle.backward(s["q"], s["k"], s["v"], s["g"], None, s["dO"], None, threads=nh)
+        return time.perf_counter() - t0
+
+    L0 = 1024
+    t_cal = run(sample(L0))
+    L_s = int(min(w["L"], max(L0, (budget_s / max(t_cal, 1e-6)) * L0)) // 64 * 64)
+    s = sample(L_s)
+    t = run(s)
+    value = nh * L_s / w["H"] / t  # layer tokens/s: a layer token is H token-heads
+    return {"value": value, "unit": "tokens/s", "cores": nh, "kind": "oracle",
+            "sample": f"batch 0, heads 0..{nh - 1}, first {L_s} tokens, fwd+bwd fp64, "
+                      f"{t:.1f} s wall; value scaled to a {w['H']}-head layer"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="ctx256k_h40")
+    ap.add_argument("--ts", type=int, default=0)
+    ap.add_argument("--no-overlap", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernel-times", action="store_true", help="print per-kernel times to stderr")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the recurrence shards over "
+              "heads with no exchange, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_06838_amd as sf
+    from paper_2608_06838_amd import synth
+
+    w = synth.workload(args.workload)
+    w["L"] = sum(w["seg_lens"])
+    dev = torch.device("cuda:0")
+    inp = synth.make_inputs(w, device=dev, seed=1002)
+    B, L, H, D = inp["q"].shape
+    io = inp["q"].element_size()
+    seg = w["seg_lens"]
+    overlap = not args.no_overlap
+
+    # preallocated outputs and workspaces: the timed region does no allocation
+    o = torch.empty_like(inp["q"])
+    S_bnd = torch.empty((len(seg) + 1, B, H, D, D), dtype=torch.float32, device=dev)
+    nws = sf.chain_workspace_bytes(inp["q"], inp["g"], seg, ts=args.ts)
+    ws_f = torch.empty(nws, dtype=torch.uint8, device=dev)
+    ws_b = torch.empty(nws, dtype=torch.uint8, device=dev)
+    dq, dk, dv = (torch.empty_like(inp["q"]) for _ in range(3))
+    dg = torch.empty_like(inp["g"])
+    dS0 = torch.empty((B, H, D, D), dtype=torch.float32, device=dev)
+
+    def step():
+        sf.chain_fwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, inp["S_in"], ts=args.ts, overlap=overlap,
+                     out=(o, S_bnd, ws_f))
+        sf.chain_bwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, S_bnd, inp["dO"], inp["dS_out"],
+                     ts=args.ts, overlap=overlap, out=(dq, dk, dv, dg, dS0, ws_b))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    kernels = list(sf.KERNELS)
+    for kname in kernels:
+        sf.prof_read(kname)  # drop anything recorded before
+        sf.prof_enable(kname, True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ktime = {}
+    for kname in kernels:
+        sf.prof_enable(kname, False)
+        ktime[kname] = sf.prof_read(kname)
+    ms = (t1 - t0) * 1e3 / args.steps
+    tokens = B * L
+    value = tokens / (ms / 1e3)
+
+    # dominant kernel and its roofline
+    dom = max((k for k in KERNEL_BYTES), key=lambda k: ktime[k][0])
+    tot_ms, nlaunch = ktime[dom]
+    avg_s = tot_ms / 1e3 / max(nlaunch, 1)
+    bytes_per_launch = KERNEL_BYTES[dom](D, io) * B * H * L * args.steps / max(nlaunch, 1)
+    achieved = bytes_per_launch / avg_s / 1e9
+    traffic = read_traffic(dom)
+    flops = alg_flops_per_token_head(D) * B * H * L
+    if args.kernel_times:
+        for k in kernels:
+            msk, n = ktime[k]
+            print(f"# {k:9s} {msk / args.steps:8.3f} ms/step  {n // args.steps:4d} launches/step",
+                  file=sys.stderr)
+    out = {
+        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if io == 2 else "f32", "data": "synthetic",
+        "config": {"workload": w["name"], "B": B, "H": H, "Dk": D, "Dv": D, "L": L, "segments": seg,
+                   "chunk": 64, "io": "bf16" if io == 2 else "f32", "state": "f32",
+                   "overlap": overlap, "ts": args.ts or "auto"},
+        "mfma_frac_of_bf16_peak": flops / (ms / 1e3) / PEAK_BF16,
+        "hbm_frac_alg": alg_bytes_per_token_head(D, io) * B * H * L / (ms / 1e3) / PEAK_HBM,
+        "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM / 1e9,
+                     "unit": "GB/s", "frac": achieved * 1e9 / PEAK_HBM, "traffic": traffic},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, inp)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,200 @@
+/*
+ * stateflow.h -- C ABI of libstateflow, the MI355X (gfx950) hot path of
+ * StateFlow's sequence-pipelined training for a gated linear recurrence layer.
+ *
+ * Operation (paper Sec. 2.1, Eq. 1, scalar-identity transition F_t = a_t I,
+ * and the per-key-channel diagonal transition read for GLA; the state is
+ * stored as S in R^{Dk x Dv}, the transpose of the paper's S):
+ *
+ *     S_t = a_t o S_{t-1} + k_t v_t^T,    o_t = S_t^T q_t,    a_t = exp(g_t)
+ *
+ * evaluated per (batch b, head h) in the chunkwise-parallel form of Sec. 2.2
+ * (Eq. 2: Pre / ST / Out over kernel-level chunks of `chunk` tokens).  There is
+ * no 1/sqrt(Dk) scaling (callers pre-scale q).  A segment ("chunk C_i" in
+ * Sec. 3.1) enters with a boundary state S_in and leaves with S_out (Fwd
+ * equation of Sec. 3.1); its backward consumes dS_out and produces dS_in (Bwd
+ * equation of Sec. 3.1) for the loss  sum_t <dO_t, o_t> + <dS_out, S_out>.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Device pointers.  q, k, v, o, dO, dq, dk, dv, g, dg, states and the
+ *    workspace are device (HBM) pointers on the current HIP device; the
+ *    caller allocates and owns all of them.  The library never allocates or
+ *    frees device memory and never synchronises the host; every call only
+ *    enqueues work on the given stream(s) and returns.  Device faults surface
+ *    at the caller's next synchronisation.
+ *  - Layout.  q, k, dq, dk: [B][L][H][Dk];  v, o, dO, dv: [B][L][H][Dv], with
+ *    element strides (sx_b, sx_l, sx_h) and the channel dim contiguous; all
+ *    eight share the strides in sf_shape.  g, dg are float32: [B][L][H]
+ *    (scalar gate, strides sg_b, sg_l, sg_h) or [B][L][H][Dk] (vector gate,
+ *    channel dim contiguous).  g is the natural-log decay, dg its gradient.
+ *    States (S_in, S_out, dS_out, dS_in, boundary slots) are float32
+ *    [B][H][Dk][Dv], contiguous.
+ *  - dtype.  io_dtype selects the element type of q, k, v, o, dO, dq, dk, dv:
+ *    SF_F32 (fp32 arithmetic throughout, fp32 matrix cores) or SF_BF16
+ *    (bf16 MFMA operands, fp32 accumulation and fp32 state).
+ *  - Supported (v1): Dk == Dv in {64, 128}; chunk == 64 (0 selects 64);
+ *    L % 64 == 0; SF_F32 needs Dk <= 64; pointers 16-byte aligned, strides a
+ *    multiple of 16 bytes.  Anything else is rejected before any launch.
+ *  - Errors.  Validation failures return a status synchronously and launch
+ *    nothing.  A failed HIP call returns SF_E_HIP.  sf_last_error() gives a
+ *    thread-local message for the last failure on the calling thread.  No C++
+ *    exception crosses this boundary.
+ *  - Aliasing.  No output may overlap any input or another output
+ *    (SF_E_ALIAS).
+ *  - Determinism.  Results are bitwise reproducible run to run and do not
+ *    depend on the overlap mode.
+ */
+#ifndef STATEFLOW_H
+#define STATEFLOW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SF_ABI_VERSION 1
+
+typedef enum {
+    SF_OK = 0,
+    SF_E_NULL = 1,        /* a required pointer is NULL */
+    SF_E_SHAPE = 2,       /* inconsistent sizes or strides */
+    SF_E_DTYPE = 3,       /* unknown io_dtype or gate kind */
+    SF_E_ALIGN = 4,       /* pointer or stride not 16-byte aligned */
+    SF_E_ALIAS = 5,       /* an output overlaps an input or another output */
+    SF_E_WORKSPACE = 6,   /* workspace smaller than required */
+    SF_E_UNSUPPORTED = 7, /* valid but not implemented in this version */
+    SF_E_HIP = 8          /* a HIP runtime call failed */
+} sf_status;
+
+typedef enum { SF_F32 = 0, SF_BF16 = 1 } sf_dtype;
+typedef enum { SF_GATE_SCALAR = 0, SF_GATE_VECTOR = 1 } sf_gate;
+
+/* hipStream_t passed as an opaque pointer (NULL = the null stream). */
+typedef void *sf_stream;
+
+typedef struct sf_shape {
+    int32_t B, H, Dk, Dv;
+    int64_t L;        /* tokens: of the segment (segment calls) or of the whole
+                         sequence (chain calls) */
+    int32_t chunk;    /* kernel-level chunk length T_C (Sec. 2.2); 0 or 64 */
+    int32_t io_dtype; /* sf_dtype */
+    int32_t gate;     /* sf_gate */
+    int32_t reserved; /* must be 0 */
+    int64_t sx_b, sx_l, sx_h; /* element strides of the token tensors; all
+                                 three 0 selects the packed [B][L][H][D] */
+    int64_t sg_b, sg_l, sg_h; /* element strides of g / dg; all three 0
+                                 selects the packed layout */
+} sf_shape;
+
+/* Tuning knobs; a NULL pointer selects the defaults for every field. */
+typedef struct sf_tuning {
+    int32_t ts;       /* state-materialisation stride in tokens (superchunk):
+                         a multiple of 64, or 0 for automatic.  The state scan
+                         (ST) runs over L/ts summaries per segment. */
+    int32_t overlap;  /* chain calls: 1 (default when aux != NULL) runs the
+                         state scans on the aux stream overlapped with the
+                         neighbouring segment's dense kernels (Sec. 3.4
+                         "Split and Overlap"); 0 serialises on main. */
+    int32_t reserved[6];
+} sf_tuning;
+
+/* ABI version (SF_ABI_VERSION). */
+int sf_abi_version(void);
+
+/* Static text for a status code. */
+const char *sf_status_str(int status);
+
+/* Thread-local description of the most recent failure ("" if none). */
+const char *sf_last_error(void);
+
+/* Workspace bytes needed by sf_segment_fwd / sf_segment_bwd for this shape
+ * (0 if the shape is invalid; the segment calls then report why). */
+size_t sf_fwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning);
+size_t sf_bwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning);
+
+/*
+ * One segment forward: (o, S_out) = Fwd(q, k, v, g; S_in)  (Sec. 3.1, Fwd).
+ *   S_in   [B][H][Dk][Dv] f32, may be NULL (zero state, the paper's S_0 = 0).
+ *   o      written for all L tokens; S_out written.
+ *   ws     device scratch of at least sf_fwd_workspace_bytes(); contents on
+ *          entry are ignored, on return unspecified.
+ * L == 0 copies S_in (or zeros) to S_out.
+ */
+sf_status sf_segment_fwd(const sf_shape *shape, const void *q, const void *k, const void *v,
+                         const float *g, const float *S_in, void *o, float *S_out, void *ws,
+                         size_t ws_bytes, const sf_tuning *tuning, sf_stream stream);
+
+/*
+ * One segment backward (Sec. 3.1, Bwd): given the forward inputs, S_in, the
+ * output gradient dO and the boundary gradient dS_out (NULL = zero), writes
+ * dq, dk, dv, dg and dS_in.  Nothing from the forward is reused: the states
+ * are replayed from S_in (state replay "SR" of Sec. 3.4).
+ */
+sf_status sf_segment_bwd(const sf_shape *shape, const void *q, const void *k, const void *v,
+                         const float *g, const float *S_in, const void *dO,
+                         const float *dS_out, void *dq, void *dk, void *dv, float *dg,
+                         float *dS_in, void *ws, size_t ws_bytes, const sf_tuning *tuning,
+                         sf_stream stream);
+
+/* Workspace bytes for the chain calls (covers both directions). */
+size_t sf_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
+                                const sf_tuning *tuning);
+
+/*
+ * Segment driver, forward (Sec. 3.1 chaining: S_0^in = S_init,
+ * S_{i+1}^in = S_i^out).  shape->L is the whole sequence; seg_len[0..n_seg-1]
+ * (host array, each > 0 and a multiple of 64) sums to it.  The token tensors
+ * are the whole sequence; segment i covers tokens [sum_{j<i} seg_len[j], ...).
+ *   S_bnd  [n_seg+1][B][H][Dk][Dv] f32: slot 0 is the input S_init (read);
+ *          slots 1..n_seg receive S_out of each segment (slot n_seg = the
+ *          final state).
+ * With aux != NULL and overlap enabled, each segment's state scan runs on aux
+ * concurrently with the next segment's preparation and the previous
+ * segment's output kernels (Sec. 3.4, fwd split-and-overlap schedule); both
+ * streams must belong to the current device.  On return the work is
+ * enqueued on main and aux, and main carries a dependency on all of it.
+ */
+sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
+                       const void *q, const void *k, const void *v, const float *g, void *o,
+                       float *S_bnd, void *ws, size_t ws_bytes, const sf_tuning *tuning,
+                       sf_stream main, sf_stream aux);
+
+/*
+ * Segment driver, backward (Sec. 3.1 reverse chaining dS_i^out = dS_{i+1}^in),
+ * segments processed last to first.  S_bnd is the forward's boundary array
+ * (slot i = S_in of segment i; slot n_seg is not read).  dS_final is the
+ * gradient of the final state (NULL = zero); dS_init receives the gradient
+ * of S_init.  Overlap as in sf_chain_fwd (Sec. 3.4, bwd schedule).
+ */
+sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
+                       const void *q, const void *k, const void *v, const float *g,
+                       const float *S_bnd, const void *dO, const float *dS_final, void *dq,
+                       void *dk, void *dv, float *dg, float *dS_init, void *ws, size_t ws_bytes,
+                       const sf_tuning *tuning, sf_stream main, sf_stream aux);
+
+/*
+ * Kernel timing for measurement: while enabled, the library brackets every
+ * launch of kernel `kernel_id` (an sf_kernel_id) with HIP events on the
+ * stream that launch uses.  sf_prof_read() synchronises those events and
+ * returns the summed milliseconds and launch count since the last reset.
+ */
+typedef enum {
+    SF_K_FWD_PREP = 0, /* per-superchunk state contribution (Pre) */
+    SF_K_SCAN = 1,     /* fp32 state scan (ST / STB) */
+    SF_K_FWD_OUT = 2,  /* intra-chunk attention + inter-chunk output (Out) */
+    SF_K_BWD_PREP = 3, /* per-superchunk state and state-gradient contributions */
+    SF_K_BWD_DQ = 4,   /* dq by a forward state walk (OG) */
+    SF_K_BWD_DKV = 5,  /* dk, dv, dg by a reverse state-gradient walk (PG) */
+    SF_K_COUNT = 6
+} sf_kernel_id;
+
+sf_status sf_prof_enable(int32_t kernel_id, int32_t on);
+sf_status sf_prof_read(int32_t kernel_id, double *total_ms, int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* STATEFLOW_H */

@@ -1,0 +1,249 @@
+"""libstateflow for MI355X: the segmented gated linear recurrence of StateFlow
+(arXiv 2608.06838) as hand-written gfx950 HIP kernels behind a C ABI.
+
+Python surface (torch tensors in, torch tensors out; PyTorch supplies device
+memory and streams only, every arithmetic step runs in libstateflow.so):
+
+    o, S_out                 = segment_fwd(q, k, v, g, S_in)
+    dq, dk, dv, dg, dS_in    = segment_bwd(q, k, v, g, S_in, dO, dS_out)
+    o, S_bnd                 = chain_fwd(q, k, v, g, seg_lens, S_init)
+    dq, dk, dv, dg, dS_init  = chain_bwd(q, k, v, g, seg_lens, S_bnd, dO, dS_final)
+
+Shapes: q, k, v, dO: [B, L, H, D] (bf16 or fp32, channel dim contiguous, all
+with the same strides); g: [B, L, H] fp32 natural-log decay; states:
+[B, H, D, D] fp32 (S stored as Dk x Dv).  See include/stateflow.h.
+"""
+import ctypes
+
+import torch
+
+from . import _lib
+from ._lib import KERNELS, StateflowError  # noqa: F401
+
+__all__ = ["segment_fwd", "segment_bwd", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
+           "bwd_workspace_bytes", "chain_workspace_bytes", "prof_enable", "prof_read",
+           "StateflowError", "abi_version"]
+
+_IO = {torch.bfloat16: _lib.SF_BF16, torch.float32: _lib.SF_F32}
+_aux_streams = {}
+
+
+def abi_version():
+    return _lib.lib().sf_abi_version()
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_handle(s):
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _tuning(ts=0, overlap=True):
+    t = _lib.SfTuning()
+    t.ts = int(ts)
+    t.overlap = 1 if overlap else 0
+    return t
+
+
+def _shape(q, g):
+    if q.dim() != 4:
+        raise ValueError("q must be [B, L, H, D]")
+    if q.dtype not in _IO:
+        raise TypeError(f"unsupported I/O dtype {q.dtype}")
+    if g.dtype != torch.float32:
+        raise TypeError("g must be float32")
+    B, L, H, D = q.shape
+    vec = g.dim() == 4
+    if (vec and tuple(g.shape) != (B, L, H, D)) or (not vec and tuple(g.shape) != (B, L, H)):
+        raise ValueError(f"g has shape {tuple(g.shape)}, expected {(B, L, H)} or {(B, L, H, D)}")
+    if q.stride(3) != 1 or (vec and g.stride(3) != 1):
+        raise ValueError("the channel dim must be contiguous")
+    sh = _lib.SfShape()
+    sh.B, sh.H, sh.Dk, sh.Dv, sh.L = B, H, D, D, L
+    sh.chunk = 64
+    sh.io_dtype = _IO[q.dtype]
+    sh.gate = _lib.SF_GATE_VECTOR if vec else _lib.SF_GATE_SCALAR
+    sh.reserved = 0
+    sh.sx_b, sh.sx_l, sh.sx_h = q.stride(0), q.stride(1), q.stride(2)
+    sh.sg_b, sh.sg_l, sh.sg_h = g.stride(0), g.stride(1), g.stride(2)
+    return sh
+
+
+def _same_layout(ref, *ts):
+    for t in ts:
+        if t is None:
+            continue
+        if t.shape != ref.shape or t.stride() != ref.stride() or t.dtype != ref.dtype:
+            raise ValueError("q, k, v, dO must share shape, strides and dtype")
+        if t.device != ref.device:
+            raise ValueError("all tensors must be on one device")
+
+
+def _state(t, B, H, D, name, n=None):
+    if t is None:
+        return None
+    want = (B, H, D, D) if n is None else (n, B, H, D, D)
+    if tuple(t.shape) != want or t.dtype != torch.float32 or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous float32 tensor of shape {want}")
+    return t
+
+
+def _like(x):
+    return torch.empty_strided(x.size(), x.stride(), dtype=x.dtype, device=x.device)
+
+
+def _ws(nbytes, device):
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def fwd_workspace_bytes(q, g, ts=0):
+    return _lib.lib().sf_fwd_workspace_bytes(ctypes.byref(_shape(q, g)), ctypes.byref(_tuning(ts)))
+
+
+def bwd_workspace_bytes(q, g, ts=0):
+    return _lib.lib().sf_bwd_workspace_bytes(ctypes.byref(_shape(q, g)), ctypes.byref(_tuning(ts)))
+
+
+def chain_workspace_bytes(q, g, seg_lens, ts=0):
+    sl = (ctypes.c_int64 * len(seg_lens))(*[int(x) for x in seg_lens])
+    return _lib.lib().sf_chain_workspace_bytes(ctypes.byref(_shape(q, g)), len(seg_lens), sl,
+                                               ctypes.byref(_tuning(ts)))
+
+
+def segment_fwd(q, k, v, g, S_in=None, *, ts=0, stream=None):
+    """(o, S_out) = Fwd(q, k, v, g; S_in) for one segment."""
+    _same_layout(q, k, v)
+    sh = _shape(q, g)
+    B, L, H, D = q.shape
+    _state(S_in, B, H, D, "S_in")
+    stream = stream or torch.cuda.current_stream(q.device)
+    L_ = _lib.lib()
+    tun = _tuning(ts)
+    with torch.cuda.stream(stream):
+        o = _like(q)
+        S_out = torch.empty((B, H, D, D), dtype=torch.float32, device=q.device)
+        nbytes = L_.sf_fwd_workspace_bytes(ctypes.byref(sh), ctypes.byref(tun))
+        ws = _ws(nbytes, q.device)
+    rc = L_.sf_segment_fwd(ctypes.byref(sh), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(S_in), _ptr(o),
+                           _ptr(S_out), _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream))
+    _lib.check("sf_segment_fwd", rc)
+    return o, S_out
+
+
+def segment_bwd(q, k, v, g, S_in, dO, dS_out=None, *, ts=0, stream=None):
+    """(dq, dk, dv, dg, dS_in) = Bwd(q, k, v, g, S_in; dO, dS_out) for one segment."""
+    _same_layout(q, k, v, dO)
+    sh = _shape(q, g)
+    B, L, H, D = q.shape
+    _state(S_in, B, H, D, "S_in")
+    _state(dS_out, B, H, D, "dS_out")
+    stream = stream or torch.cuda.current_stream(q.device)
+    L_ = _lib.lib()
+    tun = _tuning(ts)
+    with torch.cuda.stream(stream):
+        dq, dk, dv = _like(q), _like(q), _like(q)
+        dg = _like(g)
+        dS_in = torch.empty((B, H, D, D), dtype=torch.float32, device=q.device)
+        nbytes = L_.sf_bwd_workspace_bytes(ctypes.byref(sh), ctypes.byref(tun))
+        ws = _ws(nbytes, q.device)
+    rc = L_.sf_segment_bwd(ctypes.byref(sh), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(S_in), _ptr(dO),
+                           _ptr(dS_out), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg), _ptr(dS_in), _ptr(ws),
+                           ws.numel(), ctypes.byref(tun), _stream_handle(stream))
+    _lib.check("sf_segment_bwd", rc)
+    return dq, dk, dv, dg, dS_in
+
+
+def _aux_for(device, aux_stream, overlap):
+    if not overlap:
+        return None
+    if aux_stream is not None:
+        return aux_stream
+    key = torch.device(device).index
+    if key not in _aux_streams:
+        _aux_streams[key] = torch.cuda.Stream(device=device)  # default priority
+    return _aux_streams[key]
+
+
+def chain_fwd(q, k, v, g, seg_lens, S_init=None, *, ts=0, overlap=True, stream=None, aux_stream=None,
+              out=None):
+    """Forward over consecutive segments with S_in(i+1) = S_out(i).
+
+    Returns (o, S_bnd) with S_bnd[i] the state entering segment i
+    (S_bnd[0] = S_init or zero, S_bnd[-1] the final state).  `out` may supply
+    preallocated (o, S_bnd, workspace) buffers.
+    """
+    _same_layout(q, k, v)
+    sh = _shape(q, g)
+    B, L, H, D = q.shape
+    n = len(seg_lens)
+    _state(S_init, B, H, D, "S_init")
+    stream = stream or torch.cuda.current_stream(q.device)
+    aux = _aux_for(q.device, aux_stream, overlap)
+    L_ = _lib.lib()
+    tun = _tuning(ts, overlap)
+    sl = (ctypes.c_int64 * n)(*[int(x) for x in seg_lens])
+    with torch.cuda.stream(stream):
+        if out is None:
+            o = _like(q)
+            S_bnd = torch.empty((n + 1, B, H, D, D), dtype=torch.float32, device=q.device)
+            ws = _ws(L_.sf_chain_workspace_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun)), q.device)
+        else:
+            o, S_bnd, ws = out
+        if S_init is None:
+            S_bnd[0].zero_()
+        else:
+            S_bnd[0].copy_(S_init)
+    rc = L_.sf_chain_fwd(ctypes.byref(sh), n, sl, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(o), _ptr(S_bnd),
+                         _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream),
+                         _stream_handle(aux) if aux is not None else None)
+    _lib.check("sf_chain_fwd", rc)
+    return o, S_bnd
+
+
+def chain_bwd(q, k, v, g, seg_lens, S_bnd, dO, dS_final=None, *, ts=0, overlap=True, stream=None,
+              aux_stream=None, out=None):
+    """Backward over the segments in reverse with dS_out(i) = dS_in(i+1).
+
+    Returns (dq, dk, dv, dg, dS_init).  `out` may supply preallocated
+    (dq, dk, dv, dg, dS_init, workspace) buffers.
+    """
+    _same_layout(q, k, v, dO)
+    sh = _shape(q, g)
+    B, L, H, D = q.shape
+    n = len(seg_lens)
+    if (S_bnd.dim() != 5 or S_bnd.shape[0] < n or tuple(S_bnd.shape[1:]) != (B, H, D, D)
+            or S_bnd.dtype != torch.float32 or not S_bnd.is_contiguous()):
+        raise ValueError("S_bnd must be a contiguous float32 [n_seg(+1), B, H, D, D] tensor")
+    _state(dS_final, B, H, D, "dS_final")
+    stream = stream or torch.cuda.current_stream(q.device)
+    aux = _aux_for(q.device, aux_stream, overlap)
+    L_ = _lib.lib()
+    tun = _tuning(ts, overlap)
+    sl = (ctypes.c_int64 * n)(*[int(x) for x in seg_lens])
+    with torch.cuda.stream(stream):
+        if out is None:
+            dq, dk, dv = _like(q), _like(q), _like(q)
+            dg = _like(g)
+            dS_init = torch.empty((B, H, D, D), dtype=torch.float32, device=q.device)
+            ws = _ws(L_.sf_chain_workspace_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun)), q.device)
+        else:
+            dq, dk, dv, dg, dS_init, ws = out
+    rc = L_.sf_chain_bwd(ctypes.byref(sh), n, sl, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(S_bnd), _ptr(dO),
+                         _ptr(dS_final), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg), _ptr(dS_init), _ptr(ws),
+                         ws.numel(), ctypes.byref(tun), _stream_handle(stream),
+                         _stream_handle(aux) if aux is not None else None)
+    _lib.check("sf_chain_bwd", rc)
+    return dq, dk, dv, dg, dS_init
+
+
+def prof_enable(kernel, on=True):
+    _lib.check("sf_prof_enable", _lib.lib().sf_prof_enable(KERNELS[kernel], 1 if on else 0))
+
+
+def prof_read(kernel):
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    _lib.check("sf_prof_read", _lib.lib().sf_prof_read(KERNELS[kernel], ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value

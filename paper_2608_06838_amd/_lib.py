@@ -1,0 +1,93 @@
+"""ctypes binding of libstateflow (include/stateflow.h).
+
+Argument marshalling only: every step of the recurrence runs in the HIP
+kernels of libstateflow.so.  Importing this module fails loudly when the
+library has not been built; there is no fallback path.
+"""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libstateflow.so")
+
+SF_OK, SF_E_NULL, SF_E_SHAPE, SF_E_DTYPE, SF_E_ALIGN, SF_E_ALIAS, SF_E_WORKSPACE, \
+    SF_E_UNSUPPORTED, SF_E_HIP = range(9)
+SF_F32, SF_BF16 = 0, 1
+SF_GATE_SCALAR, SF_GATE_VECTOR = 0, 1
+KERNELS = {"fwd_prep": 0, "scan": 1, "fwd_out": 2, "bwd_prep": 3, "bwd_dq": 4, "bwd_dkv": 5}
+
+# every symbol include/stateflow.h declares
+EXPORTS = ["sf_abi_version", "sf_status_str", "sf_last_error", "sf_fwd_workspace_bytes",
+           "sf_bwd_workspace_bytes", "sf_segment_fwd", "sf_segment_bwd", "sf_chain_workspace_bytes",
+           "sf_chain_fwd", "sf_chain_bwd", "sf_prof_enable", "sf_prof_read"]
+
+
+class SfShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("Dk", ctypes.c_int32),
+                ("Dv", ctypes.c_int32), ("L", ctypes.c_int64), ("chunk", ctypes.c_int32),
+                ("io_dtype", ctypes.c_int32), ("gate", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("sx_b", ctypes.c_int64), ("sx_l", ctypes.c_int64), ("sx_h", ctypes.c_int64),
+                ("sg_b", ctypes.c_int64), ("sg_l", ctypes.c_int64), ("sg_h", ctypes.c_int64)]
+
+
+class SfTuning(ctypes.Structure):
+    _fields_ = [("ts", ctypes.c_int32), ("overlap", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 6)]
+
+
+class StateflowError(RuntimeError):
+    def __init__(self, fn, status, msg):
+        super().__init__(f"{fn} failed: {STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+STATUS = {SF_OK: "SF_OK", SF_E_NULL: "SF_E_NULL", SF_E_SHAPE: "SF_E_SHAPE",
+          SF_E_DTYPE: "SF_E_DTYPE", SF_E_ALIGN: "SF_E_ALIGN", SF_E_ALIAS: "SF_E_ALIAS",
+          SF_E_WORKSPACE: "SF_E_WORKSPACE", SF_E_UNSUPPORTED: "SF_E_UNSUPPORTED",
+          SF_E_HIP: "SF_E_HIP"}
+
+_lib = None
+
+
+def lib():
+    """Load libstateflow.so (raises if it was not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with paper_2608_06838_amd/build.py "
+                          "(or __graft_entry__.build()); there is no non-HIP fallback")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, sp, tp = ctypes.c_void_p, ctypes.POINTER(SfShape), ctypes.POINTER(SfTuning)
+    i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    L.sf_abi_version.restype = ctypes.c_int
+    L.sf_abi_version.argtypes = []
+    L.sf_status_str.restype = ctypes.c_char_p
+    L.sf_status_str.argtypes = [ctypes.c_int]
+    L.sf_last_error.restype = ctypes.c_char_p
+    L.sf_last_error.argtypes = []
+    for f in (L.sf_fwd_workspace_bytes, L.sf_bwd_workspace_bytes):
+        f.restype = sz
+        f.argtypes = [sp, tp]
+    L.sf_segment_fwd.restype = ctypes.c_int
+    L.sf_segment_fwd.argtypes = [sp] + [vp] * 8 + [sz, tp, vp]
+    L.sf_segment_bwd.restype = ctypes.c_int
+    L.sf_segment_bwd.argtypes = [sp] + [vp] * 13 + [sz, tp, vp]
+    L.sf_chain_workspace_bytes.restype = sz
+    L.sf_chain_workspace_bytes.argtypes = [sp, i32, i64p, tp]
+    L.sf_chain_fwd.restype = ctypes.c_int
+    L.sf_chain_fwd.argtypes = [sp, i32, i64p] + [vp] * 7 + [sz, tp, vp, vp]
+    L.sf_chain_bwd.restype = ctypes.c_int
+    L.sf_chain_bwd.argtypes = [sp, i32, i64p] + [vp] * 13 + [sz, tp, vp, vp]
+    L.sf_prof_enable.restype = ctypes.c_int
+    L.sf_prof_enable.argtypes = [i32, i32]
+    L.sf_prof_read.restype = ctypes.c_int
+    L.sf_prof_read.argtypes = [i32, ctypes.POINTER(ctypes.c_double), i64p]
+    _lib = L
+    return L
+
+
+def check(fn, status):
+    if status != SF_OK:
+        raise StateflowError(fn, status, lib().sf_last_error().decode())

@@ -1,0 +1,687 @@
+// sf_abi.hip -- host side of libstateflow: argument validation, workspace
+// layout, the per-segment phase sequence and the two-stream segment driver.
+//
+// Segment forward (paper Sec. 3.1 Fwd; phases of Sec. 2.2 Eq. 2):
+//   Pre  (k_prep)  per superchunk J: D_J, Gamma_J            -- dense, MFMA
+//   ST   (k_scan)  S_{J+1} = Gamma_J S_J + D_J, S_out         -- fp32 scan
+//   Out  (k_walk)  walk the chunks of J from S_J, write o     -- dense, MFMA
+// Segment backward (Sec. 3.1 Bwd; SR/OG/STB/PG of Sec. 3.4):
+//   prep  (SR + the dO part of OG) D_J, E_J
+//   scan  (ST replay + STB) S_J, G_{J+1}, dS_in
+//   dq    forward walk from S_J;  dkv  reverse walk from G_{J+1}
+// Chain driver (Sec. 3.1 chaining, Sec. 3.4 split-and-overlap): the scan of
+// segment i runs on the aux stream while the main stream runs the prep of
+// segment i+1 and the output phase of segment i-1, i.e. the schedule
+// Pre(1) -> (ST(1) || Pre(2)) -> (ST(2) || Out(1)) -> Out(2) applied across
+// consecutive segments; the backward mirrors it in reverse segment order.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "sf_launch.hpp"
+#include "stateflow.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+sf_status fail(sf_status s, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+sf_status hip_fail(hipError_t e, const char *what) {
+    return fail(SF_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ------------------------------------------------------------- validation
+struct Shape {
+    int B, H, D;
+    int64_t L;
+    int io, gate;
+    size_t esz;
+    int64_t sx_b, sx_l, sx_h, sg_b, sg_l, sg_h;
+};
+
+struct Dim {
+    int64_t size, stride;
+};
+
+// Strided tensor with a contiguous innermost dim of `inner` elements: the index
+// map is injective iff, sorted by stride, each stride covers the previous extent.
+bool non_overlapping(std::vector<Dim> dims, int64_t inner) {
+    std::vector<Dim> d;
+    for (auto &x : dims)
+        if (x.size > 1) d.push_back(x);
+    std::sort(d.begin(), d.end(), [](const Dim &a, const Dim &b) { return a.stride < b.stride; });
+    int64_t extent = inner;
+    for (auto &x : d) {
+        if (x.stride < extent) return false;
+        extent = x.stride * x.size;
+    }
+    return true;
+}
+
+sf_status resolve(const sf_shape *sh, Shape &r) {
+    if (!sh) return fail(SF_E_NULL, "shape is NULL");
+    if (sh->B < 1 || sh->H < 1 || sh->L < 0)
+        return fail(SF_E_SHAPE, "need B >= 1, H >= 1, L >= 0 (got B=%d H=%d L=%lld)", sh->B, sh->H,
+                    (long long)sh->L);
+    if (sh->io_dtype != SF_F32 && sh->io_dtype != SF_BF16)
+        return fail(SF_E_DTYPE, "unknown io_dtype %d", sh->io_dtype);
+    if (sh->gate != SF_GATE_SCALAR && sh->gate != SF_GATE_VECTOR)
+        return fail(SF_E_DTYPE, "unknown gate kind %d", sh->gate);
+    if (sh->reserved != 0) return fail(SF_E_SHAPE, "shape.reserved must be 0");
+    if (sh->Dk != sh->Dv || (sh->Dk != 64 && sh->Dk != 128))
+        return fail(SF_E_UNSUPPORTED, "supported head dims: Dk == Dv in {64, 128} (got %d, %d)", sh->Dk,
+                    sh->Dv);
+    if (sh->chunk != 0 && sh->chunk != 64)
+        return fail(SF_E_UNSUPPORTED, "chunk must be 64 (got %d)", sh->chunk);
+    if (sh->L % 64 != 0) return fail(SF_E_SHAPE, "L must be a multiple of 64 (got %lld)", (long long)sh->L);
+    if (sh->gate == SF_GATE_VECTOR)
+        return fail(SF_E_UNSUPPORTED, "the vector (per-key-channel) gate is not implemented yet");
+    if (sh->io_dtype == SF_F32 && sh->Dk > 64)
+        return fail(SF_E_UNSUPPORTED, "fp32 I/O supports Dk <= 64 (got %d)", sh->Dk);
+    r.B = sh->B;
+    r.H = sh->H;
+    r.D = sh->Dk;
+    r.L = sh->L;
+    r.io = sh->io_dtype;
+    r.gate = sh->gate;
+    r.esz = sh->io_dtype == SF_BF16 ? 2 : 4;
+    if (sh->sx_b == 0 && sh->sx_l == 0 && sh->sx_h == 0) {
+        r.sx_h = r.D;
+        r.sx_l = (int64_t)r.H * r.D;
+        r.sx_b = r.L * r.H * r.D;
+    } else {
+        r.sx_b = sh->sx_b;
+        r.sx_l = sh->sx_l;
+        r.sx_h = sh->sx_h;
+    }
+    const int64_t gin = r.gate == SF_GATE_VECTOR ? r.D : 1;
+    if (sh->sg_b == 0 && sh->sg_l == 0 && sh->sg_h == 0) {
+        r.sg_h = gin;
+        r.sg_l = (int64_t)r.H * gin;
+        r.sg_b = r.L * r.H * gin;
+    } else {
+        r.sg_b = sh->sg_b;
+        r.sg_l = sh->sg_l;
+        r.sg_h = sh->sg_h;
+    }
+    if (r.sx_b <= 0 || r.sx_l <= 0 || r.sx_h <= 0 || r.sg_b <= 0 || r.sg_l <= 0 || r.sg_h <= 0)
+        return fail(SF_E_SHAPE, "strides must be positive");
+    if (!non_overlapping({{r.B, r.sx_b}, {r.L, r.sx_l}, {r.H, r.sx_h}}, r.D))
+        return fail(SF_E_SHAPE, "token-tensor strides make elements overlap");
+    if (!non_overlapping({{r.B, r.sg_b}, {r.L, r.sg_l}, {r.H, r.sg_h}}, gin))
+        return fail(SF_E_SHAPE, "gate strides make elements overlap");
+    if ((r.sx_b * (int64_t)r.esz) % 16 || (r.sx_l * (int64_t)r.esz) % 16 || (r.sx_h * (int64_t)r.esz) % 16)
+        return fail(SF_E_ALIGN, "token-tensor strides must be multiples of 16 bytes");
+    return SF_OK;
+}
+
+// byte extent of a tensor
+struct Range {
+    const char *lo, *hi;
+    const char *name;
+};
+Range xrange(const Shape &r, const void *p, int64_t L, const char *name) {
+    const char *b = (const char *)p;
+    int64_t last = (r.B - 1) * r.sx_b + (L - 1) * r.sx_l + (r.H - 1) * r.sx_h + r.D;
+    return {b, b + (L > 0 ? last * (int64_t)r.esz : 0), name};
+}
+Range grange(const Shape &r, const float *p, int64_t L, const char *name) {
+    const char *b = (const char *)p;
+    const int64_t gin = r.gate == SF_GATE_VECTOR ? r.D : 1;
+    int64_t last = (r.B - 1) * r.sg_b + (L - 1) * r.sg_l + (r.H - 1) * r.sg_h + gin;
+    return {b, b + (L > 0 ? last * 4 : 0), name};
+}
+Range srange(const Shape &r, const float *p, int64_t nstates, const char *name) {
+    const char *b = (const char *)p;
+    return {b, b + (p ? nstates * r.B * r.H * (int64_t)r.D * r.D * 4 : 0), name};
+}
+bool overlap(const Range &a, const Range &b) {
+    return a.lo && b.lo && a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi;
+}
+sf_status check_alias(const std::vector<Range> &ins, const std::vector<Range> &outs) {
+    for (size_t i = 0; i < outs.size(); ++i) {
+        for (auto &in : ins)
+            if (overlap(outs[i], in)) return fail(SF_E_ALIAS, "output %s overlaps input %s", outs[i].name, in.name);
+        for (size_t j = i + 1; j < outs.size(); ++j)
+            if (overlap(outs[i], outs[j]))
+                return fail(SF_E_ALIAS, "output %s overlaps output %s", outs[i].name, outs[j].name);
+    }
+    return SF_OK;
+}
+sf_status check_align(std::initializer_list<std::pair<const void *, const char *>> ps) {
+    for (auto &p : ps)
+        if (p.first && ((uintptr_t)p.first % 16))
+            return fail(SF_E_ALIGN, "%s is not 16-byte aligned", p.second);
+    return SF_OK;
+}
+
+// --------------------------------------------------------- plan / workspace
+constexpr size_t ALIGN = 256;
+size_t al(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+sf_status pick_ts(const Shape &r, int64_t L, const sf_tuning *t, int &ts) {
+    if (t && t->ts != 0) {
+        if (t->ts < 64 || t->ts % 64) return fail(SF_E_SHAPE, "tuning.ts must be a positive multiple of 64");
+        ts = t->ts;
+        return SF_OK;
+    }
+    // Largest power-of-two multiple of 64 (<= 2048) that still gives at least
+    // 512 workgroups (two per CU on 256 CUs) to the dense kernels.
+    const int64_t bh = (int64_t)r.B * r.H;
+    ts = 64;
+    for (int cand = 2048; cand >= 64; cand /= 2)
+        if (bh * ((L + cand - 1) / cand) >= 512) {
+            ts = cand;
+            break;
+        }
+    if (ts >= L && L > 0) ts = (int)std::min<int64_t>(L, 1 << 30);
+    return SF_OK;
+}
+
+int n_super_of(int64_t L, int ts) { return L > 0 ? (int)((L + ts - 1) / ts) : 0; }
+
+struct WsLayout {
+    size_t S = 0, E = 0, Lg = 0, Dot = 0, total = 0;
+};
+WsLayout ws_layout(const Shape &r, int64_t L, int ts, bool bwd) {
+    WsLayout w;
+    const int n = n_super_of(L, ts);
+    const size_t bh = (size_t)r.B * r.H, SS = (size_t)r.D * r.D;
+    size_t off = 0;
+    if (n > 1) {
+        w.S = off;
+        off += al(bh * n * SS * 4);
+        if (bwd) {
+            w.E = off;
+            off += al(bh * n * SS * 4);
+        }
+        w.Lg = off;
+        off += al(bh * n * 4);
+    }
+    if (bwd && n >= 1) {
+        w.Dot = off;
+        off += al(bh * n * (SS / 256) * 4);
+    }
+    w.total = off;
+    return w;
+}
+
+// ------------------------------------------------------------- profiling
+std::mutex g_prof_mu;
+bool g_prof_on[SF_K_COUNT] = {};
+std::vector<std::pair<hipEvent_t, hipEvent_t>> g_prof_ev[SF_K_COUNT];
+
+sf_status launch(int kind, const Shape &r, const sf::SegArgs &a, hipStream_t s) {
+    bool on;
+    {
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        on = g_prof_on[kind];
+    }
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (on) {
+        if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess ||
+            hipEventRecord(e0, s) != hipSuccess)
+            return hip_fail(hipGetLastError(), "profiling event");
+    }
+    hipError_t e = sf::launch_kernel(kind, r.io, r.D, a, s);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    if (on) {
+        if (hipEventRecord(e1, s) != hipSuccess) return hip_fail(hipGetLastError(), "profiling event");
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        g_prof_ev[kind].push_back({e0, e1});
+    }
+    return SF_OK;
+}
+
+// ----------------------------------------------------------- segment plans
+struct Seg {
+    sf::SegArgs a;
+    int n;  // superchunks
+};
+
+Seg make_seg(const Shape &r, int64_t L, int ts, char *ws, bool bwd) {
+    Seg s{};
+    sf::SegArgs &a = s.a;
+    a.sx_b = r.sx_b;
+    a.sx_l = r.sx_l;
+    a.sx_h = r.sx_h;
+    a.sg_b = r.sg_b;
+    a.sg_l = r.sg_l;
+    a.sg_h = r.sg_h;
+    a.B = r.B;
+    a.H = r.H;
+    a.L = L;
+    a.ts = ts;
+    a.n_super = n_super_of(L, ts);
+    s.n = a.n_super;
+    WsLayout w = ws_layout(r, L, ts, bwd);
+    if (s.n > 1) {
+        a.wsS = (float *)(ws + w.S);
+        a.wsE = bwd ? (float *)(ws + w.E) : nullptr;
+        a.wsLg = (float *)(ws + w.Lg);
+    }
+    if (bwd && s.n >= 1) a.wsDot = (float *)(ws + w.Dot);
+    return s;
+}
+
+const char *offset_x(const Shape &r, const void *p, int64_t tok) {
+    return p ? (const char *)p + tok * r.sx_l * (int64_t)r.esz : nullptr;
+}
+const float *offset_g(const Shape &r, const float *p, int64_t tok) { return p ? p + tok * r.sg_l : nullptr; }
+
+// forward phases of one segment
+sf_status fwd_prep(const Shape &r, const Seg &s, hipStream_t st) {
+    return s.n > 1 ? launch(SF_K_FWD_PREP, r, s.a, st) : SF_OK;
+}
+sf_status fwd_scan(const Shape &r, const Seg &s, hipStream_t st) {
+    if (s.n > 1) return launch(SF_K_SCAN, r, s.a, st);
+    return SF_OK;
+}
+sf_status fwd_out(const Shape &r, const Seg &s, hipStream_t st) {
+    if (s.n == 0) {
+        hipError_t e = sf::launch_state_copy(s.a.S_in, s.a.S_out, (int64_t)r.B * r.H * r.D * r.D, st);
+        return e == hipSuccess ? SF_OK : hip_fail(e, "state copy");
+    }
+    sf::SegArgs a = s.a;
+    if (s.n > 1) a.S_out = nullptr;  // the scan wrote S_out
+    return launch(SF_K_FWD_OUT, r, a, st);
+}
+// backward phases
+sf_status bwd_prep(const Shape &r, const Seg &s, hipStream_t st) {
+    return s.n > 1 ? launch(SF_K_BWD_PREP, r, s.a, st) : SF_OK;
+}
+sf_status bwd_scan(const Shape &r, const Seg &s, hipStream_t st) {
+    return s.n > 1 ? launch(SF_K_SCAN, r, s.a, st) : SF_OK;
+}
+sf_status bwd_grad(const Shape &r, const Seg &s, hipStream_t st) {
+    if (s.n == 0) {
+        hipError_t e = sf::launch_state_copy(s.a.dS_out, s.a.dS_in, (int64_t)r.B * r.H * r.D * r.D, st);
+        return e == hipSuccess ? SF_OK : hip_fail(e, "state copy");
+    }
+    sf_status rc = launch(SF_K_BWD_DQ, r, s.a, st);
+    if (rc != SF_OK) return rc;
+    return launch(SF_K_BWD_DKV, r, s.a, st);
+}
+
+// ------------------------------------------------------------ stream events
+struct EventPool {
+    int dev = -1;
+    hipEvent_t ev[2] = {nullptr, nullptr};
+};
+thread_local EventPool g_events;
+
+sf_status events(hipEvent_t &e0, hipEvent_t &e1) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (g_events.dev != dev) {
+        for (auto &x : g_events.ev) {
+            x = nullptr;
+            e = hipEventCreateWithFlags(&x, hipEventDisableTiming);
+            if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
+        }
+        g_events.dev = dev;
+    }
+    e0 = g_events.ev[0];
+    e1 = g_events.ev[1];
+    return SF_OK;
+}
+sf_status dep(hipStream_t from, hipStream_t to, hipEvent_t ev) {
+    if (from == to) return SF_OK;
+    hipError_t e = hipEventRecord(ev, from);
+    if (e == hipSuccess) e = hipStreamWaitEvent(to, ev, 0);
+    return e == hipSuccess ? SF_OK : hip_fail(e, "stream dependency");
+}
+
+#define TRY(x)                          \
+    do {                                \
+        sf_status _rc = (x);            \
+        if (_rc != SF_OK) return _rc;   \
+    } while (0)
+
+sf_status check_segments(const Shape &r, int32_t n_seg, const int64_t *seg_len) {
+    if (n_seg < 1) return fail(SF_E_SHAPE, "n_seg must be >= 1");
+    if (!seg_len) return fail(SF_E_NULL, "seg_len is NULL");
+    int64_t sum = 0;
+    for (int i = 0; i < n_seg; ++i) {
+        if (seg_len[i] <= 0 || seg_len[i] % 64)
+            return fail(SF_E_SHAPE, "seg_len[%d] = %lld must be a positive multiple of 64", i,
+                        (long long)seg_len[i]);
+        sum += seg_len[i];
+    }
+    if (sum != r.L) return fail(SF_E_SHAPE, "segment lengths sum to %lld, shape.L is %lld", (long long)sum,
+                                (long long)r.L);
+    return SF_OK;
+}
+
+size_t chain_ws(const Shape &r, int32_t n_seg, const int64_t *seg_len, const sf_tuning *t) {
+    size_t slot = 0;
+    for (int i = 0; i < n_seg; ++i) {
+        int ts;
+        if (pick_ts(r, seg_len[i], t, ts) != SF_OK) return 0;
+        slot = std::max(slot, std::max(ws_layout(r, seg_len[i], ts, true).total,
+                                       ws_layout(r, seg_len[i], ts, false).total));
+    }
+    const size_t gbnd = al((size_t)r.B * r.H * r.D * r.D * 4);
+    return 2 * al(slot) + 2 * gbnd;
+}
+
+}  // namespace
+
+// ===================================================================== ABI
+extern "C" {
+
+int sf_abi_version(void) { return SF_ABI_VERSION; }
+
+const char *sf_status_str(int s) {
+    switch (s) {
+    case SF_OK: return "SF_OK";
+    case SF_E_NULL: return "SF_E_NULL";
+    case SF_E_SHAPE: return "SF_E_SHAPE";
+    case SF_E_DTYPE: return "SF_E_DTYPE";
+    case SF_E_ALIGN: return "SF_E_ALIGN";
+    case SF_E_ALIAS: return "SF_E_ALIAS";
+    case SF_E_WORKSPACE: return "SF_E_WORKSPACE";
+    case SF_E_UNSUPPORTED: return "SF_E_UNSUPPORTED";
+    case SF_E_HIP: return "SF_E_HIP";
+    default: return "SF_E_UNKNOWN";
+    }
+}
+
+const char *sf_last_error(void) { return g_err.c_str(); }
+
+size_t sf_fwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning) {
+    Shape r;
+    int ts;
+    if (resolve(shape, r) != SF_OK || pick_ts(r, r.L, tuning, ts) != SF_OK) return 0;
+    return ws_layout(r, r.L, ts, false).total;
+}
+
+size_t sf_bwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning) {
+    Shape r;
+    int ts;
+    if (resolve(shape, r) != SF_OK || pick_ts(r, r.L, tuning, ts) != SF_OK) return 0;
+    return ws_layout(r, r.L, ts, true).total;
+}
+
+sf_status sf_segment_fwd(const sf_shape *shape, const void *q, const void *k, const void *v,
+                         const float *g, const float *S_in, void *o, float *S_out, void *ws,
+                         size_t ws_bytes, const sf_tuning *tuning, sf_stream stream) {
+    g_err.clear();
+    Shape r;
+    TRY(resolve(shape, r));
+    if (!S_out || (r.L > 0 && (!q || !k || !v || !g || !o)))
+        return fail(SF_E_NULL, "q, k, v, g, o and S_out are required");
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_in, "S_in"}, {S_out, "S_out"}, {ws, "ws"}}));
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
+                     grange(r, g, r.L, "g"), srange(r, S_in, 1, "S_in")},
+                    {xrange(r, o, r.L, "o"), srange(r, S_out, 1, "S_out")}));
+    int ts;
+    TRY(pick_ts(r, r.L, tuning, ts));
+    const size_t need = ws_layout(r, r.L, ts, false).total;
+    if (need > 0 && !ws) return fail(SF_E_NULL, "workspace of %zu bytes required", need);
+    if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
+    Seg s = make_seg(r, r.L, ts, (char *)ws, false);
+    s.a.q = q;
+    s.a.k = k;
+    s.a.v = v;
+    s.a.g = g;
+    s.a.o = o;
+    s.a.S_in = S_in;
+    s.a.S_out = S_out;
+    hipStream_t st = (hipStream_t)stream;
+    TRY(fwd_prep(r, s, st));
+    TRY(fwd_scan(r, s, st));
+    TRY(fwd_out(r, s, st));
+    return SF_OK;
+}
+
+sf_status sf_segment_bwd(const sf_shape *shape, const void *q, const void *k, const void *v,
+                         const float *g, const float *S_in, const void *dO, const float *dS_out,
+                         void *dq, void *dk, void *dv, float *dg, float *dS_in, void *ws, size_t ws_bytes,
+                         const sf_tuning *tuning, sf_stream stream) {
+    g_err.clear();
+    Shape r;
+    TRY(resolve(shape, r));
+    if (!dS_in || (r.L > 0 && (!q || !k || !v || !g || !dO || !dq || !dk || !dv || !dg)))
+        return fail(SF_E_NULL, "q, k, v, g, dO, dq, dk, dv, dg and dS_in are required");
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {dO, "dO"}, {dq, "dq"}, {dk, "dk"}, {dv, "dv"},
+                     {S_in, "S_in"}, {dS_out, "dS_out"}, {dS_in, "dS_in"}, {ws, "ws"}}));
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
+                     grange(r, g, r.L, "g"), srange(r, S_in, 1, "S_in"), xrange(r, dO, r.L, "dO"),
+                     srange(r, dS_out, 1, "dS_out")},
+                    {xrange(r, dq, r.L, "dq"), xrange(r, dk, r.L, "dk"), xrange(r, dv, r.L, "dv"),
+                     grange(r, dg, r.L, "dg"), srange(r, dS_in, 1, "dS_in")}));
+    int ts;
+    TRY(pick_ts(r, r.L, tuning, ts));
+    const size_t need = ws_layout(r, r.L, ts, true).total;
+    if (need > 0 && !ws) return fail(SF_E_NULL, "workspace of %zu bytes required", need);
+    if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
+    Seg s = make_seg(r, r.L, ts, (char *)ws, true);
+    s.a.q = q;
+    s.a.k = k;
+    s.a.v = v;
+    s.a.g = g;
+    s.a.dO = dO;
+    s.a.dq = dq;
+    s.a.dk = dk;
+    s.a.dv = dv;
+    s.a.dg = dg;
+    s.a.S_in = S_in;
+    s.a.dS_out = dS_out;
+    s.a.dS_in = dS_in;
+    hipStream_t st = (hipStream_t)stream;
+    TRY(bwd_prep(r, s, st));
+    TRY(bwd_scan(r, s, st));
+    TRY(bwd_grad(r, s, st));
+    return SF_OK;
+}
+
+size_t sf_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
+                                const sf_tuning *tuning) {
+    Shape r;
+    if (resolve(shape, r) != SF_OK || check_segments(r, n_seg, seg_len) != SF_OK) return 0;
+    return chain_ws(r, n_seg, seg_len, tuning);
+}
+
+sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
+                       const void *k, const void *v, const float *g, void *o, float *S_bnd, void *ws,
+                       size_t ws_bytes, const sf_tuning *tuning, sf_stream main_s, sf_stream aux_s) {
+    g_err.clear();
+    Shape r;
+    TRY(resolve(shape, r));
+    TRY(check_segments(r, n_seg, seg_len));
+    if (!q || !k || !v || !g || !o || !S_bnd || !ws)
+        return fail(SF_E_NULL, "q, k, v, g, o, S_bnd and ws are required");
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_bnd, "S_bnd"}, {ws, "ws"}}));
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
+                     grange(r, g, r.L, "g")},
+                    {xrange(r, o, r.L, "o"), srange(r, S_bnd, n_seg + 1, "S_bnd")}));
+    const size_t need = chain_ws(r, n_seg, seg_len, tuning);
+    if (need == 0) return fail(SF_E_SHAPE, "cannot size the chain workspace");
+    if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
+    const size_t slot = (need - 2 * al((size_t)r.B * r.H * r.D * r.D * 4)) / 2;
+    const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
+    hipStream_t mn = (hipStream_t)main_s;
+    hipStream_t ax = (aux_s && (!tuning || tuning->overlap != 0)) ? (hipStream_t)aux_s : mn;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (ax != mn) TRY(events(e0, e1));
+    if (ax != mn) TRY(dep(mn, ax, e0));  // aux sees everything queued on main so far
+
+    std::vector<Seg> segs(n_seg);
+    int64_t tok = 0;
+    for (int i = 0; i < n_seg; ++i) {
+        int ts;
+        TRY(pick_ts(r, seg_len[i], tuning, ts));
+        Seg &s = segs[i];
+        s = make_seg(r, seg_len[i], ts, (char *)ws + (i % 2) * slot, false);
+        s.a.q = offset_x(r, q, tok);
+        s.a.k = offset_x(r, k, tok);
+        s.a.v = offset_x(r, v, tok);
+        s.a.g = offset_g(r, g, tok);
+        s.a.o = (void *)offset_x(r, o, tok);
+        s.a.S_in = S_bnd + i * SSB;
+        s.a.S_out = S_bnd + (i + 1) * SSB;
+        tok += seg_len[i];
+    }
+    // S_bnd[i] is produced by scan(i-1) on aux (multi-superchunk segments) or by
+    // the walk of segment i-1 on main (single-superchunk segments).
+    int pending = -1;
+    bool bnd_on_aux = false;  // producer stream of the current S_bnd[i]
+    for (int i = 0; i < n_seg; ++i) {
+        Seg &s = segs[i];
+        if (s.n > 1) {
+            TRY(fwd_prep(r, s, mn));
+            TRY(dep(mn, ax, e0));  // prep(i) done (and any main-side S_bnd[i] producer)
+            TRY(fwd_scan(r, s, ax));
+            bnd_on_aux = (ax != mn);
+        }
+        if (pending >= 0) {
+            TRY(dep(ax, mn, e1));
+            TRY(fwd_out(r, segs[pending], mn));
+            pending = -1;
+        }
+        if (s.n > 1) {
+            pending = i;
+        } else {
+            if (bnd_on_aux) TRY(dep(ax, mn, e1));
+            TRY(fwd_out(r, s, mn));
+            bnd_on_aux = false;
+        }
+    }
+    if (pending >= 0) {
+        TRY(dep(ax, mn, e1));
+        TRY(fwd_out(r, segs[pending], mn));
+    }
+    if (ax != mn) TRY(dep(ax, mn, e1));
+    return SF_OK;
+}
+
+sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
+                       const void *k, const void *v, const float *g, const float *S_bnd, const void *dO,
+                       const float *dS_final, void *dq, void *dk, void *dv, float *dg, float *dS_init,
+                       void *ws, size_t ws_bytes, const sf_tuning *tuning, sf_stream main_s,
+                       sf_stream aux_s) {
+    g_err.clear();
+    Shape r;
+    TRY(resolve(shape, r));
+    TRY(check_segments(r, n_seg, seg_len));
+    if (!q || !k || !v || !g || !S_bnd || !dO || !dq || !dk || !dv || !dg || !dS_init || !ws)
+        return fail(SF_E_NULL, "q, k, v, g, S_bnd, dO, dq, dk, dv, dg, dS_init and ws are required");
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {dO, "dO"}, {dq, "dq"}, {dk, "dk"}, {dv, "dv"},
+                     {S_bnd, "S_bnd"}, {dS_final, "dS_final"}, {dS_init, "dS_init"}, {ws, "ws"}}));
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
+                     grange(r, g, r.L, "g"), srange(r, S_bnd, n_seg, "S_bnd"), xrange(r, dO, r.L, "dO"),
+                     srange(r, dS_final, 1, "dS_final")},
+                    {xrange(r, dq, r.L, "dq"), xrange(r, dk, r.L, "dk"), xrange(r, dv, r.L, "dv"),
+                     grange(r, dg, r.L, "dg"), srange(r, dS_init, 1, "dS_init")}));
+    const size_t need = chain_ws(r, n_seg, seg_len, tuning);
+    if (need == 0) return fail(SF_E_SHAPE, "cannot size the chain workspace");
+    if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
+    const size_t gb = al((size_t)r.B * r.H * r.D * r.D * 4);
+    const size_t slot = (need - 2 * gb) / 2;
+    float *gbnd[2] = {(float *)((char *)ws + 2 * slot), (float *)((char *)ws + 2 * slot + gb)};
+    const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
+    hipStream_t mn = (hipStream_t)main_s;
+    hipStream_t ax = (aux_s && (!tuning || tuning->overlap != 0)) ? (hipStream_t)aux_s : mn;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (ax != mn) TRY(events(e0, e1));
+    if (ax != mn) TRY(dep(mn, ax, e0));
+
+    std::vector<Seg> segs(n_seg);
+    int64_t tok = 0;
+    for (int i = 0; i < n_seg; ++i) {
+        int ts;
+        TRY(pick_ts(r, seg_len[i], tuning, ts));
+        Seg &s = segs[i];
+        s = make_seg(r, seg_len[i], ts, (char *)ws + (i % 2) * slot, true);
+        s.a.q = offset_x(r, q, tok);
+        s.a.k = offset_x(r, k, tok);
+        s.a.v = offset_x(r, v, tok);
+        s.a.g = offset_g(r, g, tok);
+        s.a.dO = offset_x(r, dO, tok);
+        s.a.dq = (void *)offset_x(r, dq, tok);
+        s.a.dk = (void *)offset_x(r, dk, tok);
+        s.a.dv = (void *)offset_x(r, dv, tok);
+        s.a.dg = (float *)offset_g(r, dg, tok);
+        s.a.S_in = S_bnd + i * SSB;
+        s.a.dS_out = i == n_seg - 1 ? dS_final : gbnd[(i + 1) % 2];
+        s.a.dS_in = i == 0 ? dS_init : gbnd[i % 2];
+        tok += seg_len[i];
+    }
+    int pending = -1;
+    bool bnd_on_aux = false;  // producer stream of the current dS_out
+    for (int i = n_seg - 1; i >= 0; --i) {
+        Seg &s = segs[i];
+        if (s.n > 1) {
+            TRY(bwd_prep(r, s, mn));
+            TRY(dep(mn, ax, e0));
+            TRY(bwd_scan(r, s, ax));
+            bnd_on_aux = (ax != mn);
+        }
+        if (pending >= 0) {
+            TRY(dep(ax, mn, e1));
+            TRY(bwd_grad(r, segs[pending], mn));
+            pending = -1;
+        }
+        if (s.n > 1) {
+            pending = i;
+        } else {
+            if (bnd_on_aux) TRY(dep(ax, mn, e1));
+            TRY(bwd_grad(r, s, mn));
+            bnd_on_aux = false;
+        }
+    }
+    if (pending >= 0) {
+        TRY(dep(ax, mn, e1));
+        TRY(bwd_grad(r, segs[pending], mn));
+    }
+    if (ax != mn) TRY(dep(ax, mn, e1));
+    return SF_OK;
+}
+
+sf_status sf_prof_enable(int32_t kernel_id, int32_t on) {
+    if (kernel_id < 0 || kernel_id >= SF_K_COUNT) return fail(SF_E_SHAPE, "unknown kernel id %d", kernel_id);
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof_on[kernel_id] = on != 0;
+    return SF_OK;
+}
+
+sf_status sf_prof_read(int32_t kernel_id, double *total_ms, int64_t *launches) {
+    if (kernel_id < 0 || kernel_id >= SF_K_COUNT) return fail(SF_E_SHAPE, "unknown kernel id %d", kernel_id);
+    if (!total_ms || !launches) return fail(SF_E_NULL, "total_ms and launches are required");
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> evs;
+    {
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        evs.swap(g_prof_ev[kernel_id]);
+    }
+    double tot = 0.0;
+    sf_status rc = SF_OK;
+    for (auto &p : evs) {
+        float ms = 0.f;
+        hipError_t e = hipEventSynchronize(p.second);
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.first, p.second);
+        if (e != hipSuccess && rc == SF_OK) rc = hip_fail(e, "profiling event");
+        tot += ms;
+        (void)hipEventDestroy(p.first);
+        (void)hipEventDestroy(p.second);
+    }
+    *total_ms = tot;
+    *launches = (int64_t)evs.size();
+    return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,224 @@
+// sf_device.hpp -- device-side building blocks for the gfx950 (CDNA4) kernels:
+// MFMA wrappers, LDS fragment loads, global->LDS tile staging with an in-register
+// transpose, and wave64 scans.
+//
+// MFMA lane maps (measured on gfx950):
+//   v_mfma_f32_16x16x32_bf16: lane l supplies A[l%16][8*(l/16)+j] and
+//     B[8*(l/16)+j][l%16], j = 0..7, and receives D[4*(l/16)+r][l%16], r = 0..3.
+//   v_mfma_f32_16x16x4_f32: lane l supplies A[l%16][l/16], B[l/16][l%16]; same D.
+// Every product below is an "NT" product C[m][n] += sum_k A[m][k] * B[n][k] with
+// both operands stored with the contraction index contiguous, so one fragment
+// loader serves both sides.  An fp32 "k-step of 32" is eight 16x16x4 MFMAs over
+// the same 8-element fragments, so bf16 and fp32 kernels share all index maths.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sf {
+
+constexpr int C = 64;     // kernel-level chunk (tokens)
+constexpr int NT = 256;   // threads per workgroup (4 waves)
+constexpr float LOG2E = 1.4426950408889634f;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+
+template <typename T> struct Frag;
+template <> struct Frag<__bf16> { typedef bf16x8 type; };
+template <> struct Frag<float> { typedef f32x8 type; };
+template <typename T> using frag_t = typename Frag<T>::type;
+
+// Padding of 16 bytes per LDS row keeps the 16-row fragment reads conflict-free.
+template <typename T> constexpr int pad() { return 16 / (int)sizeof(T); }
+
+__device__ __forceinline__ void mma(f32x4 &c, const bf16x8 &a, const bf16x8 &b) {
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ void mma(f32x4 &c, const f32x8 &a, const f32x8 &b) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], c, 0, 0, 0);
+}
+
+template <typename T> __device__ __forceinline__ T cvt(float x) { return (T)x; }
+template <typename T> __device__ __forceinline__ float tof(T x) { return (float)x; }
+
+// Fragment of rows row0..row0+15, contraction columns k0..k0+31 (lane gets
+// row row0 + l%16, columns k0 + 8*(l/16) .. +7).
+template <typename T>
+__device__ __forceinline__ frag_t<T> ldfrag(const T *base, int ld, int row0, int k0, int lane) {
+    const T *p = base + (row0 + (lane & 15)) * ld + k0 + 8 * (lane >> 4);
+    return *reinterpret_cast<const frag_t<T> *>(p);
+}
+
+// Transposed tiles [rows][C tokens] keep their 16-byte token blocks XOR-swizzled
+// by (row >> 4): with this layout both the per-thread transposed stores and the
+// 16-row fragment reads touch every LDS bank at most once per pass.
+template <typename T>
+__device__ __forceinline__ int tswz(int row, int t) {
+    constexpr int TPB = 16 / (int)sizeof(T), NB = C / TPB;
+    return (((t / TPB) ^ ((row >> 4) & (NB - 1))) * TPB) + (t % TPB);
+}
+// ldfrag() for a swizzled transposed tile.
+template <typename T>
+__device__ __forceinline__ frag_t<T> ldfragT(const T *base, int ldt, int row0, int k0, int lane) {
+    const int r = row0 + (lane & 15), t = k0 + 8 * (lane >> 4);
+    const T *p = base + r * ldt;
+    if constexpr (sizeof(T) == 2) {
+        return *reinterpret_cast<const frag_t<T> *>(p + tswz<T>(r, t));
+    } else {
+        f32x4 lo = *reinterpret_cast<const f32x4 *>(p + tswz<T>(r, t));
+        f32x4 hi = *reinterpret_cast<const f32x4 *>(p + tswz<T>(r, t + 4));
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+}
+
+// Same rows, but the contraction slots follow an accumulator pair: slot j < 4 is
+// column k0 + 4*(l/16) + j, slot j >= 4 is column k0 + 16 + 4*(l/16) + (j-4).
+// Pairs with frag_from_acc() on the other operand.
+template <typename T>
+__device__ __forceinline__ frag_t<T> ldfrag_perm(const T *base, int ld, int row0, int k0, int lane);
+template <>
+__device__ __forceinline__ bf16x8 ldfrag_perm<__bf16>(const __bf16 *base, int ld, int row0, int k0,
+                                                      int lane) {
+    const __bf16 *p = base + (row0 + (lane & 15)) * ld + k0 + 4 * (lane >> 4);
+    bf16x4 lo = *reinterpret_cast<const bf16x4 *>(p);
+    bf16x4 hi = *reinterpret_cast<const bf16x4 *>(p + 16);
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+template <>
+__device__ __forceinline__ f32x8 ldfrag_perm<float>(const float *base, int ld, int row0, int k0,
+                                                    int lane) {
+    const float *p = base + (row0 + (lane & 15)) * ld + k0 + 4 * (lane >> 4);
+    f32x4 lo = *reinterpret_cast<const f32x4 *>(p);
+    f32x4 hi = *reinterpret_cast<const f32x4 *>(p + 16);
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Operand fragment built from two accumulator tiles X[m0..m0+15][n] (a0) and
+// X[m0+16..m0+31][n] (a1): as an A operand it is X^T rows n, contraction over m.
+template <typename T>
+__device__ __forceinline__ frag_t<T> frag_from_acc(const f32x4 &a0, const f32x4 &a1) {
+    frag_t<T> f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        f[j] = cvt<T>(a0[j]);
+        f[j + 4] = cvt<T>(a1[j]);
+    }
+    return f;
+}
+
+// Fragment with every element multiplied by a per-slot factor (fp32), re-rounded.
+template <typename T>
+__device__ __forceinline__ frag_t<T> scale_frag(const frag_t<T> &f, const float *s) {
+    frag_t<T> o;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = cvt<T>(tof<T>(f[j]) * s[j]);
+    return o;
+}
+
+// Store 4 consecutive fp32 values as T (8 bytes for bf16, 16 for fp32).
+__device__ __forceinline__ void st4(__bf16 *p, float a, float b, float c, float d) {
+    bf16x4 v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+    *reinterpret_cast<bf16x4 *>(p) = v;
+}
+__device__ __forceinline__ void st4(float *p, float a, float b, float c, float d) {
+    f32x4 v = {a, b, c, d};
+    *reinterpret_cast<f32x4 *>(p) = v;
+}
+__device__ __forceinline__ f32x4 ld4f(const __bf16 *p) {
+    bf16x4 v = *reinterpret_cast<const bf16x4 *>(p);
+    return f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+}
+__device__ __forceinline__ f32x4 ld4f(const float *p) { return *reinterpret_cast<const f32x4 *>(p); }
+
+// A chunk tile of C tokens x D channels moving global -> registers -> LDS.
+// Thread `tid` owns rows (tokens) row0 .. row0+RPT-1 and one 16-byte column
+// block cb (E channels), so 8..16 consecutive lanes read one contiguous row.
+template <typename T, int D>
+struct Tile {
+    static constexpr int E = 16 / (int)sizeof(T);
+    static constexpr int CB = D / E;
+    static constexpr int RPT = C * D / (NT * E);
+    static_assert(NT % CB == 0 && RPT >= 2, "tile shape");
+    typedef T vecE __attribute__((ext_vector_type(E)));
+    typedef T vecR __attribute__((ext_vector_type(RPT)));
+    vecE r[RPT];
+
+    __device__ __forceinline__ int cb(int tid) const { return tid % CB; }
+    __device__ __forceinline__ int row0(int tid) const { return (tid / CB) * RPT; }
+
+    __device__ __forceinline__ void load(const T *base, int64_t row_stride, int tid) {
+        const T *p = base + (int64_t)row0(tid) * row_stride + cb(tid) * E;
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) r[j] = *reinterpret_cast<const vecE *>(p + (int64_t)j * row_stride);
+    }
+    // natural layout [token][channel], row pitch ld
+    __device__ __forceinline__ void store_nat(T *lds, int ld, int tid) const {
+        T *p = lds + row0(tid) * ld + cb(tid) * E;
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) *reinterpret_cast<vecE *>(p + j * ld) = r[j];
+    }
+    // swizzled transposed layout [channel][token] (see tswz), token j scaled by s[j]
+    __device__ __forceinline__ void store_T(T *lds, int ldt, int tid, const float *s) const {
+        const int c0 = cb(tid) * E, t0 = row0(tid);
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+            vecR vals;
+#pragma unroll
+            for (int j = 0; j < RPT; ++j) vals[j] = cvt<T>(tof<T>(r[j][i]) * s[j]);
+            put_T(lds + (c0 + i) * ldt, c0 + i, t0, vals);
+        }
+    }
+    // transposed, unscaled (a pure register transpose)
+    __device__ __forceinline__ void store_T1(T *lds, int ldt, int tid) const {
+        const int c0 = cb(tid) * E, t0 = row0(tid);
+#pragma unroll
+        for (int i = 0; i < E; ++i) {
+            vecR vals;
+#pragma unroll
+            for (int j = 0; j < RPT; ++j) vals[j] = r[j][i];
+            put_T(lds + (c0 + i) * ldt, c0 + i, t0, vals);
+        }
+    }
+    // RPT consecutive tokens of one transposed row; split at 16-byte blocks
+    __device__ __forceinline__ static void put_T(T *row, int c, int t0, const vecR &vals) {
+        if constexpr (RPT * sizeof(T) <= 16) {
+            *reinterpret_cast<vecR *>(row + tswz<T>(c, t0)) = vals;
+        } else {
+            static_assert(RPT * sizeof(T) == 32, "transposed store width");
+            typedef T half_t __attribute__((ext_vector_type(RPT / 2)));
+            const half_t lo = __builtin_shufflevector(vals, vals, 0, 1, 2, 3);
+            const half_t hi = __builtin_shufflevector(vals, vals, 4, 5, 6, 7);
+            *reinterpret_cast<half_t *>(row + tswz<T>(c, t0)) = lo;
+            *reinterpret_cast<half_t *>(row + tswz<T>(c, t0 + RPT / 2)) = hi;
+        }
+    }
+};
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ float wave_incl_scan(float x, int lane) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        float y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+    }
+    return x;
+}
+// Inclusive suffix sum over the 64 lanes of a wave.
+__device__ __forceinline__ float wave_incl_suffix(float x, int lane) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        float y = __shfl_down(x, o, 64);
+        if (lane + o < 64) x += y;
+    }
+    return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+    return x;
+}
+
+}  // namespace sf

@@ -1,0 +1,788 @@
+// sf_kernels.hip -- gfx950 kernels of the segmented gated linear recurrence.
+//
+// Per (batch, head) the recurrence S_t = a_t S_{t-1} + k_t v_t^T, o_t = S_t^T q_t
+// (paper Sec. 2.1, Eq. 1) is evaluated in the chunkwise form of Sec. 2.2 (Eq. 2):
+// a segment of L tokens is cut into kernel-level chunks of C = 64 tokens and
+// into "superchunks" of ts tokens (a multiple of C) at which the state is
+// materialised.  With b_j the chunk-local inclusive cumulative log-decay,
+//   intra:  A = (Q K^T) o M,  M[t][s] = exp(b_t - b_s) [s <= t]
+//   out:    O = diag(exp(b)) Q S_c + A V
+//   state:  S_{c+1} = exp(b_63) S_c + (K o exp(b_63 - b))^T V
+// Every exponent is <= 0 (g <= 0), so no factor can overflow.
+//
+// Kernels (one workgroup of 256 threads per (batch, head, superchunk)):
+//   k_prep<.., BWD=false>  Pre: superchunk state contribution D_J and its decay
+//   k_scan<false>          ST:  S_{J+1} = Gamma_J S_J + D_J (fp32), S_out
+//   k_walk<.., DQ=false>   Out: walk the chunks from S_J, write o
+//   k_prep<.., BWD=true>   replay D_J and the state-gradient contribution E_J
+//   k_scan<true>           ST + STB: S_J forward, G_{J+1} backward, dS_in,
+//                          <G_{J+1}, S_{J+1}> partials for dg
+//   k_walk<.., DQ=true>    dq by a forward walk; also q.dq per token
+//   k_bwd_dkv              dk, dv, dg by a reverse walk of the state gradient
+// A segment that fits in one superchunk skips prep and scan: the walkers start
+// from S_in / dS_out directly and produce S_out / dS_in themselves.
+#include "sf_device.hpp"
+#include "sf_launch.hpp"
+
+namespace sf {
+
+// (t-tile, s-tile) pairs of the causal 64x64 score matrix, s-tile <= t-tile.
+__device__ __forceinline__ void tri_tile(int i, int &tt, int &st) {
+    // 0:(0,0) 1:(1,0) 2:(1,1) 3:(2,0) 4:(2,1) 5:(2,2) 6:(3,0) 7:(3,1) 8:(3,2) 9:(3,3)
+    tt = (i >= 1) + (i >= 3) + (i >= 6);
+    st = i - (tt * (tt + 1)) / 2;
+}
+
+struct Decode {
+    int J, bh, b, h, nch;
+    int64_t tok0;
+};
+__device__ __forceinline__ Decode decode(const SegArgs &a) {
+    Decode d;
+    d.J = blockIdx.x % a.n_super;
+    d.bh = blockIdx.x / a.n_super;
+    d.b = d.bh / a.H;
+    d.h = d.bh % a.H;
+    d.tok0 = (int64_t)d.J * a.ts;
+    int64_t rem = a.L - d.tok0;
+    d.nch = (int)((rem < a.ts ? rem : a.ts) / C);
+    return d;
+}
+
+// ---------------------------------------------------------------------------
+// Pre: per superchunk, D_J = sum_c (decay after c) (K~_c)^T V_c, and for the
+// backward E_J = sum_t exp(B_t) q_t dO_t^T (B superchunk-local, inclusive).
+// State tiles: wave w owns state columns [w*D/4, (w+1)*D/4).
+template <typename T, int D, bool BWD>
+__global__ void __launch_bounds__(NT) k_prep(SegArgs a) {
+    constexpr int LDT = C + pad<T>();
+    constexpr int NK = D / 16, NV = D / 64, DW = D / 4;
+    __shared__ __attribute__((aligned(16))) T sKT[D * LDT];
+    __shared__ __attribute__((aligned(16))) T sVT[D * LDT];
+    __shared__ __attribute__((aligned(16))) T sQT[BWD ? D * LDT : 8];
+    __shared__ __attribute__((aligned(16))) T sOT[BWD ? D * LDT : 8];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
+    const Decode d = decode(a);
+    const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
+    const T *K = (const T *)a.k + xo;
+    const T *V = (const T *)a.v + xo;
+    const T *Q = (const T *)a.q + xo;
+    const T *dO = (const T *)a.dO + xo;
+    const float *gp = a.g + d.b * a.sg_b + d.h * a.sg_h + d.tok0 * a.sg_l;
+    const int c0 = w * DW;
+
+    f32x4 Ds[NK][NV], Es[BWD ? NK : 1][BWD ? NV : 1];
+#pragma unroll
+    for (int i = 0; i < NK; ++i)
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            Ds[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if constexpr (BWD) Es[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+
+    Tile<T, D> tk, tv, tq, to;
+    tk.load(K, a.sx_l, tid);
+    tv.load(V, a.sx_l, tid);
+    if constexpr (BWD) {
+        tq.load(Q, a.sx_l, tid);
+        to.load(dO, a.sx_l, tid);
+    }
+    float gl = gp[lane * a.sg_l];
+    float off = 0.f;  // log2 decay of the superchunk's earlier chunks
+
+    for (int c = 0; c < d.nch; ++c) {
+        const float b2 = wave_incl_scan(gl * LOG2E, lane);
+        const float b63 = __shfl(b2, 63, 64);
+        __syncthreads();
+        {
+            constexpr int R = Tile<T, D>::RPT;
+            float ks[R], qs[R];
+#pragma unroll
+            for (int j = 0; j < R; ++j) {
+                const float bj = __shfl(b2, tk.row0(tid) + j, 64);
+                ks[j] = exp2f(b63 - bj);
+                qs[j] = exp2f(off + bj);
+            }
+            tk.store_T(sKT, LDT, tid, ks);
+            tv.store_T1(sVT, LDT, tid);
+            if constexpr (BWD) {
+                tq.store_T(sQT, LDT, tid, qs);
+                to.store_T1(sOT, LDT, tid);
+            }
+        }
+        if (c + 1 < d.nch) {
+            const int64_t nx = (int64_t)(c + 1) * C * a.sx_l;
+            tk.load(K + nx, a.sx_l, tid);
+            tv.load(V + nx, a.sx_l, tid);
+            if constexpr (BWD) {
+                tq.load(Q + nx, a.sx_l, tid);
+                to.load(dO + nx, a.sx_l, tid);
+            }
+            gl = gp[((c + 1) * C + lane) * a.sg_l];
+        }
+        __syncthreads();
+        const float gam = exp2f(b63);
+#pragma unroll
+        for (int i = 0; i < NK; ++i)
+#pragma unroll
+            for (int j = 0; j < NV; ++j) Ds[i][j] *= gam;
+#pragma unroll
+        for (int ks = 0; ks < C / 32; ++ks) {
+            frag_t<T> fb[NV];
+#pragma unroll
+            for (int j = 0; j < NV; ++j) fb[j] = ldfragT(sVT, LDT, c0 + 16 * j, 32 * ks, lane);
+#pragma unroll
+            for (int i = 0; i < NK; ++i) {
+                const frag_t<T> fa = ldfragT(sKT, LDT, 16 * i, 32 * ks, lane);
+#pragma unroll
+                for (int j = 0; j < NV; ++j) mma(Ds[i][j], fa, fb[j]);
+            }
+            if constexpr (BWD) {
+#pragma unroll
+                for (int j = 0; j < NV; ++j) fb[j] = ldfragT(sOT, LDT, c0 + 16 * j, 32 * ks, lane);
+#pragma unroll
+                for (int i = 0; i < NK; ++i) {
+                    const frag_t<T> fa = ldfragT(sQT, LDT, 16 * i, 32 * ks, lane);
+#pragma unroll
+                    for (int j = 0; j < NV; ++j) mma(Es[i][j], fa, fb[j]);
+                }
+            }
+        }
+        off += b63;
+    }
+    const int64_t so = ((int64_t)d.bh * a.n_super + d.J) * D * D;
+#pragma unroll
+    for (int i = 0; i < NK; ++i)
+#pragma unroll
+        for (int j = 0; j < NV; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t e = so + (int64_t)(16 * i + 4 * q4 + r) * D + c0 + 16 * j + n16;
+                a.wsS[e] = Ds[i][j][r];
+                if constexpr (BWD) a.wsE[e] = Es[i][j][r];
+            }
+    if (tid == 0) a.wsLg[(int64_t)d.bh * a.n_super + d.J] = off;
+}
+
+// ---------------------------------------------------------------------------
+// ST (and STB): fp32 scan over superchunk summaries, 4 state elements per
+// thread; grid = B*H*(D*D/1024).  Forward: slot J of wsS is replaced by S_J
+// (state entering superchunk J).  Backward additionally walks J downwards:
+// slot J of wsE is replaced by G_{J+1} (gradient of the state leaving J) and
+// the wave partials of <G_{J+1}, S_{J+1}> go to wsDot[(bh, J)][part*4 + wave].
+template <bool BWD>
+__global__ void __launch_bounds__(NT) k_scan(SegArgs a, int D) {
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int parts = D * D / 1024;
+    const int part = blockIdx.x % parts;
+    const int64_t bh = blockIdx.x / parts;
+    const int64_t SS = (int64_t)D * D;
+    const int64_t e = (int64_t)(part * NT + tid) * 4;
+    const int n = a.n_super;
+    float *Sb = a.wsS + bh * n * SS + e;
+    const float *lg = a.wsLg + bh * n;
+
+    f32x4 S = a.S_in ? *reinterpret_cast<const f32x4 *>(a.S_in + bh * SS + e) : f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int J = 0; J < n; J += 4) {
+        f32x4 dd[4];
+        float f[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (J + u < n) {
+                dd[u] = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)(J + u) * SS);
+                f[u] = exp2f(lg[J + u]);
+            }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (J + u < n) {
+                *reinterpret_cast<f32x4 *>(Sb + (int64_t)(J + u) * SS) = S;
+                S = f[u] * S + dd[u];
+            }
+    }
+    if constexpr (!BWD) {
+        if (a.S_out) *reinterpret_cast<f32x4 *>(a.S_out + bh * SS + e) = S;
+    } else {
+        const int ndot = D * D / 256;
+        float *Eb = a.wsE + bh * n * SS + e;
+        f32x4 G = a.dS_out ? *reinterpret_cast<const f32x4 *>(a.dS_out + bh * SS + e)
+                           : f32x4{0.f, 0.f, 0.f, 0.f};
+        f32x4 Sn = S;  // S_{J+1} for J = n-1 is S_out
+        for (int J = n - 1; J >= 0; --J) {
+            const f32x4 E = *reinterpret_cast<const f32x4 *>(Eb + (int64_t)J * SS);
+            const f32x4 Sj = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)J * SS);
+            const float f = exp2f(lg[J]);
+            float p = G[0] * Sn[0] + G[1] * Sn[1] + G[2] * Sn[2] + G[3] * Sn[3];
+            p = wave_sum(p);
+            if (lane == 0) a.wsDot[(bh * n + J) * ndot + part * 4 + w] = p;
+            *reinterpret_cast<f32x4 *>(Eb + (int64_t)J * SS) = G;
+            G = f * G + E;
+            Sn = Sj;
+        }
+        if (a.dS_in) *reinterpret_cast<f32x4 *>(a.dS_in + bh * SS + e) = G;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Forward walker over the chunks of one superchunk, state in registers.
+//   DQ == false (Out):  X1 = q, X2 = k, X3 = v, state S[k][v];   writes o.
+//   DQ == true  (OG):   X1 = dO, X2 = v, X3 = k, state S^T[v][k]; writes dq
+//                       and r_t = q_t . dq_t into dg (read back by k_bwd_dkv).
+// The state lives as MFMA accumulators: wave w owns state columns
+// [w*D/4, (w+1)*D/4), tile (kt, vt) lane holds rows 16kt+4*(l/16)+r, column
+// 16vt+l%16, which is exactly an A-operand fragment of the transposed state
+// (frag_from_acc), so Q S needs no LDS round trip for S.
+template <typename T, int D, bool DQ>
+__global__ void __launch_bounds__(NT) k_walk(SegArgs a) {
+    constexpr int LDN = D + pad<T>(), LDT = C + pad<T>();
+    constexpr int NK = D / 16, NV = D / 64, DW = D / 4;
+    constexpr int R = Tile<T, D>::RPT;
+    __shared__ __attribute__((aligned(16))) T sX1[C * LDN];
+    __shared__ __attribute__((aligned(16))) T sX2[C * LDN];
+    __shared__ __attribute__((aligned(16))) T sX2T[D * LDT];  // decayed: X2~^T
+    __shared__ __attribute__((aligned(16))) T sX3T[D * LDT];
+    __shared__ __attribute__((aligned(16))) T sA[C * LDT];    // A[t][s]
+    __shared__ float sb[C];
+    __shared__ float sred[DQ ? 4 * C : 1];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
+    const Decode d = decode(a);
+    const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
+    const T *X1 = (const T *)(DQ ? a.dO : a.q) + xo;
+    const T *X2 = (const T *)(DQ ? a.v : a.k) + xo;
+    const T *X3 = (const T *)(DQ ? a.k : a.v) + xo;
+    const T *Qd = (const T *)(DQ ? a.q : a.v) + xo;  // DQ: q for the q.dq dot
+    T *Y = (T *)(DQ ? a.dq : a.o) + xo;
+    const int64_t go = d.b * a.sg_b + d.h * a.sg_h + d.tok0 * a.sg_l;
+    const float *gp = a.g + go;
+    float *dgp = a.dg + go;
+    const int c0 = w * DW;
+    const int64_t SS = (int64_t)D * D;
+
+    // initial state S_J
+    const float *src = a.n_super == 1 ? (a.S_in ? a.S_in + d.bh * SS : nullptr)
+                                      : a.wsS + ((int64_t)d.bh * a.n_super + d.J) * SS;
+    f32x4 S[NK][NV];
+#pragma unroll
+    for (int i = 0; i < NK; ++i)
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            const int col = c0 + 16 * j + n16, row = 16 * i + 4 * q4;
+            if (!src) {
+                S[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            } else if constexpr (!DQ) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) S[i][j][r] = src[(int64_t)(row + r) * D + col];
+            } else {
+                S[i][j] = *reinterpret_cast<const f32x4 *>(src + (int64_t)col * D + row);
+            }
+        }
+    // A tiles read by the A.V product but above the diagonal stay zero
+    {
+        const int rr = tid >> 4, cc = tid & 15;
+        sA[rr * LDT + 16 + cc] = cvt<T>(0.f);
+        sA[(32 + rr) * LDT + 48 + cc] = cvt<T>(0.f);
+    }
+
+    Tile<T, D> t1, t2, t3;
+    t1.load(X1, a.sx_l, tid);
+    t2.load(X2, a.sx_l, tid);
+    t3.load(X3, a.sx_l, tid);
+    float gl = gp[lane * a.sg_l];
+    // DQ: q values of this lane's dq elements, one chunk ahead
+    typedef T vec4T __attribute__((ext_vector_type(4)));
+    vec4T qn[DQ ? 4 : 1][DQ ? NV : 1];
+    auto load_q = [&](int c) {
+        if constexpr (DQ) {
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+                for (int j = 0; j < NV; ++j)
+                    qn[tt][j] = *reinterpret_cast<const vec4T *>(
+                        Qd + (int64_t)(c * C + 16 * tt + n16) * a.sx_l + c0 + 16 * j + 4 * q4);
+        }
+    };
+    load_q(0);
+
+    for (int c = 0; c < d.nch; ++c) {
+        const float b2 = wave_incl_scan(gl * LOG2E, lane);
+        const float b63 = __shfl(b2, 63, 64);
+        vec4T qc[DQ ? 4 : 1][DQ ? NV : 1];
+        if constexpr (DQ) {
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+                for (int j = 0; j < NV; ++j) qc[tt][j] = qn[tt][j];
+        }
+        __syncthreads();
+        if (w == 0) sb[lane] = b2;
+        {
+            float ks[R];
+#pragma unroll
+            for (int j = 0; j < R; ++j) ks[j] = exp2f(b63 - __shfl(b2, t2.row0(tid) + j, 64));
+            t1.store_nat(sX1, LDN, tid);
+            t2.store_nat(sX2, LDN, tid);
+            t2.store_T(sX2T, LDT, tid, ks);
+            t3.store_T1(sX3T, LDT, tid);
+        }
+        if (c + 1 < d.nch) {
+            const int64_t nx = (int64_t)(c + 1) * C * a.sx_l;
+            t1.load(X1 + nx, a.sx_l, tid);
+            t2.load(X2 + nx, a.sx_l, tid);
+            t3.load(X3 + nx, a.sx_l, tid);
+            gl = gp[((c + 1) * C + lane) * a.sg_l];
+            load_q(c + 1);
+        }
+        __syncthreads();
+
+        // scores P^T[s][t] = sum_ch X2[s][ch] X1[t][ch] on the causal tiles
+        for (int i = w; i < 10; i += 4) {
+            int tt, st;
+            tri_tile(i, tt, st);
+            f32x4 p = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks)
+                mma(p, ldfrag(sX2, LDN, 16 * st, 32 * ks, lane), ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane));
+            const int t = 16 * tt + n16;
+            const float bt = sb[t];
+            float v4[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int s = 16 * st + 4 * q4 + r;
+                v4[r] = s <= t ? p[r] * exp2f(bt - sb[s]) : 0.f;
+            }
+            st4(&sA[t * LDT + 16 * st + 4 * q4], v4[0], v4[1], v4[2], v4[3]);
+        }
+        __syncthreads();
+
+        // Y^T[col][t] = exp(b_t) sum_m S[m][col] X1[t][m] + sum_s X3[s][col] A[t][s]
+        f32x4 O[NV][4];
+#pragma unroll
+        for (int j = 0; j < NV; ++j)
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) O[j][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) {
+            frag_t<T> fs[NV];
+#pragma unroll
+            for (int j = 0; j < NV; ++j) fs[j] = frag_from_acc<T>(S[2 * ks][j], S[2 * ks + 1][j]);
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) {
+                const frag_t<T> fb = ldfrag_perm(sX1, LDN, 16 * tt, 32 * ks, lane);
+#pragma unroll
+                for (int j = 0; j < NV; ++j) mma(O[j][tt], fs[j], fb);
+            }
+        }
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) {
+            const float et = exp2f(sb[16 * tt + n16]);
+#pragma unroll
+            for (int j = 0; j < NV; ++j) O[j][tt] *= et;
+        }
+#pragma unroll
+        for (int ks = 0; ks < C / 32; ++ks) {
+            frag_t<T> fa[NV];
+#pragma unroll
+            for (int j = 0; j < NV; ++j) fa[j] = ldfragT(sX3T, LDT, c0 + 16 * j, 32 * ks, lane);
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) {
+                if (32 * ks > 16 * tt + 15) continue;
+                const frag_t<T> fb = ldfrag(sA, LDT, 16 * tt, 32 * ks, lane);
+#pragma unroll
+                for (int j = 0; j < NV; ++j) mma(O[j][tt], fa[j], fb);
+            }
+        }
+        float part[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) {
+            const int64_t trow = (int64_t)(c * C + 16 * tt + n16) * a.sx_l;
+#pragma unroll
+            for (int j = 0; j < NV; ++j) {
+                const int col = c0 + 16 * j + 4 * q4;
+                st4(Y + trow + col, O[j][tt][0], O[j][tt][1], O[j][tt][2], O[j][tt][3]);
+                if constexpr (DQ) {
+                    const vec4T qv = qc[tt][j];
+                    part[tt] += O[j][tt][0] * tof<T>(qv[0]) + O[j][tt][1] * tof<T>(qv[1]) +
+                                O[j][tt][2] * tof<T>(qv[2]) + O[j][tt][3] * tof<T>(qv[3]);
+                }
+            }
+        }
+        if constexpr (DQ) {
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) {
+                part[tt] += __shfl_xor(part[tt], 16, 64);
+                part[tt] += __shfl_xor(part[tt], 32, 64);
+                if (q4 == 0) sred[w * C + 16 * tt + n16] = part[tt];
+            }
+        }
+
+        // state update S = exp(b_63) S + X2~^T X3
+        const float gam = exp2f(b63);
+#pragma unroll
+        for (int i = 0; i < NK; ++i)
+#pragma unroll
+            for (int j = 0; j < NV; ++j) S[i][j] *= gam;
+#pragma unroll
+        for (int ks = 0; ks < C / 32; ++ks) {
+            frag_t<T> fb[NV];
+#pragma unroll
+            for (int j = 0; j < NV; ++j) fb[j] = ldfragT(sX3T, LDT, c0 + 16 * j, 32 * ks, lane);
+#pragma unroll
+            for (int i = 0; i < NK; ++i) {
+                const frag_t<T> fa = ldfragT(sX2T, LDT, 16 * i, 32 * ks, lane);
+#pragma unroll
+                for (int j = 0; j < NV; ++j) mma(S[i][j], fa, fb[j]);
+            }
+        }
+        if constexpr (DQ) {
+            __syncthreads();
+            if (w == 0)
+                dgp[(int64_t)(c * C + lane) * a.sg_l] =
+                    sred[lane] + sred[C + lane] + sred[2 * C + lane] + sred[3 * C + lane];
+        }
+    }
+
+    if (a.n_super == 1) {
+        if constexpr (!DQ) {
+            if (a.S_out) {
+                float *dst = a.S_out + d.bh * SS;
+#pragma unroll
+                for (int i = 0; i < NK; ++i)
+#pragma unroll
+                    for (int j = 0; j < NV; ++j)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + 16 * j + n16] = S[i][j][r];
+            }
+        } else {
+            // <dS_out, S_out> for dg (state here is S_out^T)
+            float p = 0.f;
+            if (a.dS_out) {
+                const float *ds = a.dS_out + d.bh * SS;
+#pragma unroll
+                for (int i = 0; i < NK; ++i)
+#pragma unroll
+                    for (int j = 0; j < NV; ++j) {
+                        const f32x4 x = *reinterpret_cast<const f32x4 *>(
+                            ds + (int64_t)(c0 + 16 * j + n16) * D + 16 * i + 4 * q4);
+                        p += x[0] * S[i][j][0] + x[1] * S[i][j][1] + x[2] * S[i][j][2] + x[3] * S[i][j][3];
+                    }
+            }
+            p = wave_sum(p);
+            const int ndot = D * D / 256;
+            float *dot = a.wsDot + (int64_t)d.bh * ndot;
+            if (lane == 0) dot[w] = p;
+            if (w == 0 && lane >= 4 && lane < ndot) dot[lane] = 0.f;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// PG: reverse walk over the chunks of a superchunk with the state gradient G
+// (dLoss/dS of the state leaving the chunk) in registers:
+//   dv^T = exp(b_63 - b_s) G^T K^T + dO^T A^T      (A from Q K^T)
+//   dk^T = exp(b_63 - b_s) G V^T   + Q^T dA^T      (dA from dO V^T)
+//   G   <- exp(b_63) G + (Q o exp(b))^T dO
+//   dg_t = sum_{t' >= t in superchunk} (q.dq - k.dk)_{t'} + <G_{J+1}, S_{J+1}>
+// (the last term is the decay gradient carried in from later superchunks).
+template <typename T, int D>
+__global__ void __launch_bounds__(NT) k_bwd_dkv(SegArgs a) {
+    constexpr int LDN = D + pad<T>(), LDT = C + pad<T>();
+    constexpr int NK = D / 16, NV = D / 64, DW = D / 4;
+    __shared__ __attribute__((aligned(16))) T sQ[C * LDN];
+    __shared__ __attribute__((aligned(16))) T sK[C * LDN];
+    __shared__ __attribute__((aligned(16))) T sV[C * LDN];
+    __shared__ __attribute__((aligned(16))) T sO[C * LDN];   // dO
+    __shared__ __attribute__((aligned(16))) T sQT[D * LDT];
+    __shared__ __attribute__((aligned(16))) T sOT[D * LDT];  // dO^T
+    __shared__ __attribute__((aligned(16))) T sAT[C * LDT];  // A^T[s][t]
+    __shared__ __attribute__((aligned(16))) T sdAT[C * LDT]; // dA^T[s][t]
+    __shared__ __attribute__((aligned(16))) T sG[D * LDN];   // G[k][v]
+    __shared__ float sb[C];
+    __shared__ float sred[4 * C];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
+    const Decode d = decode(a);
+    const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
+    const T *Q = (const T *)a.q + xo;
+    const T *K = (const T *)a.k + xo;
+    const T *V = (const T *)a.v + xo;
+    const T *dO = (const T *)a.dO + xo;
+    T *dK = (T *)a.dk + xo;
+    T *dV = (T *)a.dv + xo;
+    const int64_t go = d.b * a.sg_b + d.h * a.sg_h + d.tok0 * a.sg_l;
+    const float *gp = a.g + go;
+    float *dgp = a.dg + go;
+    const int c0 = w * DW;
+    const int64_t SS = (int64_t)D * D;
+    const int ndot = D * D / 256;
+
+    const float *gsrc = a.n_super == 1 ? (a.dS_out ? a.dS_out + d.bh * SS : nullptr)
+                                       : a.wsE + ((int64_t)d.bh * a.n_super + d.J) * SS;
+    f32x4 G[NK][NV];
+#pragma unroll
+    for (int i = 0; i < NK; ++i)
+#pragma unroll
+        for (int j = 0; j < NV; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                G[i][j][r] = gsrc ? gsrc[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + 16 * j + n16] : 0.f;
+    float carry;
+    {
+        const float *dot = a.wsDot + ((int64_t)d.bh * a.n_super + d.J) * ndot;
+        carry = wave_sum(lane < ndot ? dot[lane] : 0.f);
+    }
+    {
+        const int rr = tid >> 4, cc = tid & 15;
+        sAT[(16 + rr) * LDT + cc] = cvt<T>(0.f);
+        sAT[(48 + rr) * LDT + 32 + cc] = cvt<T>(0.f);
+        sdAT[(16 + rr) * LDT + cc] = cvt<T>(0.f);
+        sdAT[(48 + rr) * LDT + 32 + cc] = cvt<T>(0.f);
+    }
+
+    Tile<T, D> tq, tk, tv, to;
+    {
+        const int64_t nx = (int64_t)(d.nch - 1) * C * a.sx_l;
+        tq.load(Q + nx, a.sx_l, tid);
+        tk.load(K + nx, a.sx_l, tid);
+        tv.load(V + nx, a.sx_l, tid);
+        to.load(dO + nx, a.sx_l, tid);
+    }
+    float gl = gp[((d.nch - 1) * C + lane) * a.sg_l];
+    float rn = dgp[((d.nch - 1) * C + lane) * a.sg_l];  // q.dq left in dg by the dq walk
+
+    for (int c = d.nch - 1; c >= 0; --c) {
+        const float b2 = wave_incl_scan(gl * LOG2E, lane);
+        const float b63 = __shfl(b2, 63, 64);
+        const float rc = rn;
+        __syncthreads();
+        if (w == 0) sb[lane] = b2;
+        tq.store_nat(sQ, LDN, tid);
+        tk.store_nat(sK, LDN, tid);
+        tv.store_nat(sV, LDN, tid);
+        to.store_nat(sO, LDN, tid);
+        tq.store_T1(sQT, LDT, tid);
+        to.store_T1(sOT, LDT, tid);
+#pragma unroll
+        for (int i = 0; i < NK; ++i)
+#pragma unroll
+            for (int j = 0; j < NV; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    sG[(16 * i + 4 * q4 + r) * LDN + c0 + 16 * j + n16] = cvt<T>(G[i][j][r]);
+        if (c > 0) {
+            const int64_t nx = (int64_t)(c - 1) * C * a.sx_l;
+            tq.load(Q + nx, a.sx_l, tid);
+            tk.load(K + nx, a.sx_l, tid);
+            tv.load(V + nx, a.sx_l, tid);
+            to.load(dO + nx, a.sx_l, tid);
+            gl = gp[((c - 1) * C + lane) * a.sg_l];
+            rn = dgp[((c - 1) * C + lane) * a.sg_l];
+        }
+        __syncthreads();
+
+        // A^T and dA^T on the causal tiles: P[t][s] = sum X[t][ch] Y[s][ch]
+        for (int i = w; i < 20; i += 4) {
+            const bool isdA = i >= 10;
+            int tt, st;
+            tri_tile(isdA ? i - 10 : i, tt, st);
+            const T *X = isdA ? sO : sQ;
+            const T *Yt = isdA ? sV : sK;
+            T *dst = isdA ? sdAT : sAT;
+            f32x4 p = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks)
+                mma(p, ldfrag(X, LDN, 16 * tt, 32 * ks, lane), ldfrag(Yt, LDN, 16 * st, 32 * ks, lane));
+            const int s = 16 * st + n16;
+            const float bs = sb[s];
+            float v4[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * tt + 4 * q4 + r;
+                v4[r] = s <= t ? p[r] * exp2f(sb[t] - bs) : 0.f;
+            }
+            st4(&dst[s * LDT + 16 * tt + 4 * q4], v4[0], v4[1], v4[2], v4[3]);
+        }
+        __syncthreads();
+
+        const int64_t crow = (int64_t)c * C;
+        // dv^T[v][s], v in this wave's columns
+        {
+            f32x4 DV[NV][4];
+#pragma unroll
+            for (int j = 0; j < NV; ++j)
+#pragma unroll
+                for (int st = 0; st < 4; ++st) DV[j][st] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks) {
+                frag_t<T> fs[NV];
+#pragma unroll
+                for (int j = 0; j < NV; ++j) fs[j] = frag_from_acc<T>(G[2 * ks][j], G[2 * ks + 1][j]);
+#pragma unroll
+                for (int st = 0; st < 4; ++st) {
+                    const frag_t<T> fb = ldfrag_perm(sK, LDN, 16 * st, 32 * ks, lane);
+#pragma unroll
+                    for (int j = 0; j < NV; ++j) mma(DV[j][st], fs[j], fb);
+                }
+            }
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                const float f = exp2f(b63 - sb[16 * st + n16]);
+#pragma unroll
+                for (int j = 0; j < NV; ++j) DV[j][st] *= f;
+            }
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+#pragma unroll
+                for (int ks = st / 2; ks < C / 32; ++ks) {
+                    const frag_t<T> fb = ldfrag(sAT, LDT, 16 * st, 32 * ks, lane);
+#pragma unroll
+                    for (int j = 0; j < NV; ++j)
+                        mma(DV[j][st], ldfragT(sOT, LDT, c0 + 16 * j, 32 * ks, lane), fb);
+                }
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+#pragma unroll
+                for (int j = 0; j < NV; ++j)
+                    st4(dV + (crow + 16 * st + n16) * a.sx_l + c0 + 16 * j + 4 * q4, DV[j][st][0],
+                        DV[j][st][1], DV[j][st][2], DV[j][st][3]);
+        }
+        // dk^T[k][s], k in this wave's rows; k.dk partials
+        {
+            f32x4 DK[NV][4];
+#pragma unroll
+            for (int j = 0; j < NV; ++j)
+#pragma unroll
+                for (int st = 0; st < 4; ++st) DK[j][st] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks) {
+                frag_t<T> fa[NV];
+#pragma unroll
+                for (int j = 0; j < NV; ++j) fa[j] = ldfrag(sG, LDN, c0 + 16 * j, 32 * ks, lane);
+#pragma unroll
+                for (int st = 0; st < 4; ++st) {
+                    const frag_t<T> fb = ldfrag(sV, LDN, 16 * st, 32 * ks, lane);
+#pragma unroll
+                    for (int j = 0; j < NV; ++j) mma(DK[j][st], fa[j], fb);
+                }
+            }
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                const float f = exp2f(b63 - sb[16 * st + n16]);
+#pragma unroll
+                for (int j = 0; j < NV; ++j) DK[j][st] *= f;
+            }
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+#pragma unroll
+                for (int ks = st / 2; ks < C / 32; ++ks) {
+                    const frag_t<T> fb = ldfrag(sdAT, LDT, 16 * st, 32 * ks, lane);
+#pragma unroll
+                    for (int j = 0; j < NV; ++j)
+                        mma(DK[j][st], ldfragT(sQT, LDT, c0 + 16 * j, 32 * ks, lane), fb);
+                }
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                const int s = 16 * st + n16;
+                float part = 0.f;
+#pragma unroll
+                for (int j = 0; j < NV; ++j) {
+                    const int col = c0 + 16 * j + 4 * q4;
+                    st4(dK + (crow + s) * a.sx_l + col, DK[j][st][0], DK[j][st][1], DK[j][st][2],
+                        DK[j][st][3]);
+                    const f32x4 kv = ld4f(&sK[s * LDN + col]);
+                    part += DK[j][st][0] * kv[0] + DK[j][st][1] * kv[1] + DK[j][st][2] * kv[2] +
+                            DK[j][st][3] * kv[3];
+                }
+                part += __shfl_xor(part, 16, 64);
+                part += __shfl_xor(part, 32, 64);
+                if (q4 == 0) sred[w * C + s] = part;
+            }
+        }
+        // G <- exp(b_63) G + (Q o exp(b))^T dO
+        {
+            const float gam = exp2f(b63);
+#pragma unroll
+            for (int i = 0; i < NK; ++i)
+#pragma unroll
+                for (int j = 0; j < NV; ++j) G[i][j] *= gam;
+#pragma unroll
+            for (int ks = 0; ks < C / 32; ++ks) {
+                float qs[8];
+#pragma unroll
+                for (int jj = 0; jj < 8; ++jj) qs[jj] = exp2f(sb[32 * ks + 8 * q4 + jj]);
+                frag_t<T> fb[NV];
+#pragma unroll
+                for (int j = 0; j < NV; ++j) fb[j] = ldfragT(sOT, LDT, c0 + 16 * j, 32 * ks, lane);
+#pragma unroll
+                for (int i = 0; i < NK; ++i) {
+                    const frag_t<T> fa = scale_frag<T>(ldfragT(sQT, LDT, 16 * i, 32 * ks, lane), qs);
+#pragma unroll
+                    for (int j = 0; j < NV; ++j) mma(G[i][j], fa, fb[j]);
+                }
+            }
+        }
+        __syncthreads();
+        if (w == 0) {
+            float *dgt = dgp + (crow + lane) * a.sg_l;
+            const float ell = rc - (sred[lane] + sred[C + lane] + sred[2 * C + lane] + sred[3 * C + lane]);
+            const float suf = wave_incl_suffix(ell, lane);
+            *dgt = carry + suf;
+            carry += __shfl(suf, 0, 64);
+        }
+    }
+    if (a.n_super == 1 && a.dS_in) {
+        float *dst = a.dS_in + d.bh * SS;
+#pragma unroll
+        for (int i = 0; i < NK; ++i)
+#pragma unroll
+            for (int j = 0; j < NV; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + 16 * j + n16] = G[i][j][r];
+    }
+}
+
+// Boundary state of an empty segment: dst = src, or zero when src is NULL.
+__global__ void __launch_bounds__(NT) k_state_copy(const float *src, float *dst, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+    if (i < n) dst[i] = src ? src[i] : 0.f;
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+template <typename T, int D>
+static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s) {
+    const dim3 blk(NT);
+    const dim3 grid((unsigned)((int64_t)a.B * a.H * a.n_super));
+    switch (kind) {
+    case SF_K_FWD_PREP: hipLaunchKernelGGL((k_prep<T, D, false>), grid, blk, 0, s, a); break;
+    case SF_K_FWD_OUT: hipLaunchKernelGGL((k_walk<T, D, false>), grid, blk, 0, s, a); break;
+    case SF_K_BWD_PREP: hipLaunchKernelGGL((k_prep<T, D, true>), grid, blk, 0, s, a); break;
+    case SF_K_BWD_DQ: hipLaunchKernelGGL((k_walk<T, D, true>), grid, blk, 0, s, a); break;
+    case SF_K_BWD_DKV: hipLaunchKernelGGL((k_bwd_dkv<T, D>), grid, blk, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t s) {
+    if (kind == SF_K_SCAN) {
+        const dim3 grid((unsigned)((int64_t)a.B * a.H * (D * D / 1024)));
+        if (a.dS_in || a.wsE) hipLaunchKernelGGL((k_scan<true>), grid, dim3(NT), 0, s, a, D);
+        else hipLaunchKernelGGL((k_scan<false>), grid, dim3(NT), 0, s, a, D);
+        return hipGetLastError();
+    }
+    if (io == SF_BF16 && D == 128) return launch_td<__bf16, 128>(kind, a, s);
+    if (io == SF_BF16 && D == 64) return launch_td<__bf16, 64>(kind, a, s);
+    if (io == SF_F32 && D == 64) return launch_td<float, 64>(kind, a, s);
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_state_copy(const float *src, float *dst, int64_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_state_copy, dim3((unsigned)((n + NT - 1) / NT)), dim3(NT), 0, s, src, dst, n);
+    return hipGetLastError();
+}
+
+}  // namespace sf

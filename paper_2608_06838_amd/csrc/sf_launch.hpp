@@ -1,0 +1,38 @@
+// sf_launch.hpp -- argument block shared by the host driver and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "stateflow.h"
+
+namespace sf {
+
+// One segment (or one superchunk-parallel launch over a segment).  Token
+// tensors point at the segment's first token; strides are in elements.
+struct SegArgs {
+    const void *q, *k, *v, *dO;
+    void *o, *dq, *dk, *dv;
+    const float *g;
+    float *dg;
+    int64_t sx_b, sx_l, sx_h;
+    int64_t sg_b, sg_l, sg_h;
+    int32_t B, H;
+    int64_t L;        // tokens in the segment
+    int32_t ts;       // superchunk length (multiple of 64)
+    int32_t n_super;  // ceil(L / ts)
+    const float *S_in;
+    float *S_out;
+    const float *dS_out;
+    float *dS_in;
+    float *wsS;    // [B][H][n_super][D][D]: D_J, replaced by S_J by the scan
+    float *wsE;    // [B][H][n_super][D][D]: E_J, replaced by G_{J+1} (backward only)
+    float *wsLg;   // [B][H][n_super]: log2 of the superchunk decay
+    float *wsDot;  // [B][H][n_super][D*D/256]: partials of <G_{J+1}, S_{J+1}>
+};
+
+// kind is an sf_kernel_id; io an sf_dtype.  The scan runs its backward form
+// when wsE is set.
+hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t s);
+hipError_t launch_state_copy(const float *src, float *dst, int64_t n, hipStream_t s);
+
+}  // namespace sf

@@ -1,0 +1,131 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, sizes workspaces, and rejects bad arguments before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_06838_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "stateflow.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sf_[a-z_]+)\s*\(", text)))
+
+
+def shape(**kw):
+    s = _lib.SfShape()
+    s.B, s.H, s.Dk, s.Dv, s.L = 1, 2, 128, 128, 1024
+    s.chunk, s.io_dtype, s.gate, s.reserved = 64, _lib.SF_BF16, _lib.SF_GATE_SCALAR, 0
+    for k, v in kw.items():
+        setattr(s, k, v)
+    return s
+
+
+def test_exports_every_declared_symbol():
+    L = _lib.lib()
+    declared = header_functions()
+    assert set(declared) == set(_lib.EXPORTS), (declared, _lib.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+    assert L.sf_abi_version() == 1
+    assert L.sf_status_str(_lib.SF_E_ALIAS) == b"SF_E_ALIAS"
+
+
+def test_workspace_sizes():
+    L = _lib.lib()
+    t = _lib.SfTuning()
+    t.ts = 256
+    s = shape(L=1024)
+    n = 1024 // 256
+    fwd = L.sf_fwd_workspace_bytes(ctypes.byref(s), ctypes.byref(t))
+    bwd = L.sf_bwd_workspace_bytes(ctypes.byref(s), ctypes.byref(t))
+    state = 2 * n * 128 * 128 * 4
+    assert fwd >= state + 2 * n * 4
+    assert bwd >= 2 * state + 2 * n * 4 + 2 * n * 64 * 4
+    t.ts = 1024  # one superchunk: the walkers start from S_in directly
+    assert L.sf_fwd_workspace_bytes(ctypes.byref(s), ctypes.byref(t)) == 0
+    assert 0 < L.sf_bwd_workspace_bytes(ctypes.byref(s), ctypes.byref(t)) <= 4096
+    # invalid shapes size to 0
+    assert L.sf_fwd_workspace_bytes(ctypes.byref(shape(L=100)), None) == 0
+    assert L.sf_fwd_workspace_bytes(None, None) == 0
+    segs = (ctypes.c_int64 * 3)(512, 256, 256)
+    assert L.sf_chain_workspace_bytes(ctypes.byref(s), 3, segs, None) > 0
+    bad = (ctypes.c_int64 * 3)(512, 256, 128)
+    assert L.sf_chain_workspace_bytes(ctypes.byref(s), 3, bad, None) == 0
+
+
+FAKE = 0x7F0000000000  # never dereferenced: every case below fails validation first
+
+
+def p(i):
+    return ctypes.c_void_p(FAKE + i * (1 << 32))
+
+
+def fwd(s, q=1, k=2, v=3, g=4, S_in=None, o=5, S_out=6, ws=7, ws_bytes=1 << 30, tun=None):
+    L = _lib.lib()
+    args = [p(x) if x is not None else None for x in (q, k, v, g, S_in, o, S_out, ws)]
+    return L.sf_segment_fwd(ctypes.byref(s) if s is not None else None, *args, ws_bytes,
+                            ctypes.byref(tun) if tun is not None else None, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(L=100), _lib.SF_E_SHAPE),
+    (dict(B=0), _lib.SF_E_SHAPE),
+    (dict(Dk=96, Dv=96), _lib.SF_E_UNSUPPORTED),
+    (dict(Dk=128, Dv=64), _lib.SF_E_UNSUPPORTED),
+    (dict(chunk=32), _lib.SF_E_UNSUPPORTED),
+    (dict(io_dtype=7), _lib.SF_E_DTYPE),
+    (dict(gate=5), _lib.SF_E_DTYPE),
+    (dict(io_dtype=_lib.SF_F32, Dk=128, Dv=128), _lib.SF_E_UNSUPPORTED),
+    (dict(reserved=1), _lib.SF_E_SHAPE),
+    (dict(sx_b=1024 * 2 * 128, sx_l=100, sx_h=128), _lib.SF_E_SHAPE),   # rows overlap
+    (dict(sx_b=1024 * 2 * 136, sx_l=2 * 136, sx_h=132), _lib.SF_E_ALIGN),  # 264-byte head stride
+])
+def test_shape_validation(kw, status):
+    assert fwd(shape(**kw)) == status
+    assert _lib.lib().sf_last_error() != b""
+
+
+def test_pointer_validation():
+    s = shape()
+    assert fwd(None) == _lib.SF_E_NULL
+    assert fwd(s, q=None) == _lib.SF_E_NULL
+    assert fwd(s, S_out=None) == _lib.SF_E_NULL
+    # misaligned pointer
+    L = _lib.lib()
+    rc = L.sf_segment_fwd(ctypes.byref(s), ctypes.c_void_p(FAKE + 2), p(2), p(3), p(4), None, p(5), p(6),
+                          p(7), 1 << 30, None, None)
+    assert rc == _lib.SF_E_ALIGN
+    # output overlapping an input
+    assert fwd(s, o=1) == _lib.SF_E_ALIAS
+    assert fwd(s, S_out=5) == _lib.SF_E_ALIAS  # S_out inside o
+    # workspace too small
+    t = _lib.SfTuning()
+    t.ts = 128
+    assert fwd(s, ws_bytes=16, tun=t) == _lib.SF_E_WORKSPACE
+    assert fwd(s, ws=None, tun=t) == _lib.SF_E_NULL
+    t.ts = 100
+    assert fwd(s, tun=t) == _lib.SF_E_SHAPE
+
+
+def test_chain_validation():
+    L = _lib.lib()
+    s = shape(L=1024)
+    segs = (ctypes.c_int64 * 2)(512, 448)   # sums to 960
+    rc = L.sf_chain_fwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), p(7), 1 << 30, None,
+                        None, None)
+    assert rc == _lib.SF_E_SHAPE
+    segs = (ctypes.c_int64 * 2)(512, 512)
+    rc = L.sf_chain_fwd(ctypes.byref(s), 0, segs, p(1), p(2), p(3), p(4), p(5), p(6), p(7), 1 << 30, None,
+                        None, None)
+    assert rc == _lib.SF_E_SHAPE
+    rc = L.sf_chain_bwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, p(8), p(9),
+                        p(10), p(11), None, p(13), 1 << 30, None, None, None)
+    assert rc == _lib.SF_E_NULL  # dS_init missing
+    rc = L.sf_prof_enable(99, 1)
+    assert rc == _lib.SF_E_SHAPE

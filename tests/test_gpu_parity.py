@@ -1,0 +1,168 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Sizes span several chunks and superchunks with ragged tails; the workloads of
+the paper's evaluation shapes run at full size, with the oracle on all heads
+where it finishes in seconds and on sampled (batch, head) pairs otherwise.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_06838_amd as sf
+from paper_2608_06838_amd import synth
+from tests._helpers import assert_close, dg_floor, oracle_run, select, select_state, to64
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def on_gpu(inp):
+    out = {}
+    for key, x in inp.items():
+        out[key] = x.to(DEV) if isinstance(x, torch.Tensor) else x
+    return out
+
+
+def check_all(io, got, ref, inp, names=("o", "S_out", "dq", "dk", "dv", "dg", "dS_in")):
+    pairs = ref["pairs"]
+    fl = dg_floor(ref, to64(select(inp["q"], pairs)), to64(select(inp["k"], pairs)))
+    for n in names:
+        X = got[n]
+        X = select_state(X, pairs) if n in ("S_out", "dS_in") else select(X, pairs)
+        assert_close(n, to64(X), ref[n], io, floor=fl if n == "dg" else 0.0)
+
+
+def seg_case(w, L, ts, seed, dS_std=0.1, s_in_std=None):
+    if s_in_std is not None:
+        w = dict(w, s_in_std=s_in_std)
+    inp = synth.make_inputs(w, device="cpu", seed=seed, dS_out_std=dS_std, L=L)
+    g = on_gpu(inp)
+    say(f"[seg] {w['name']} L={L} ts={ts} seed={seed}")
+    o, S_out = sf.segment_fwd(g["q"], g["k"], g["v"], g["g"], g["S_in"], ts=ts)
+    dq, dk, dv, dg, dS_in = sf.segment_bwd(g["q"], g["k"], g["v"], g["g"], g["S_in"], g["dO"], g["dS_out"],
+                                           ts=ts)
+    torch.cuda.synchronize()
+    return inp, dict(o=o, S_out=S_out, dq=dq, dk=dk, dv=dv, dg=dg, dS_in=dS_in)
+
+
+@pytest.mark.parametrize("ts", [1024, 256, 192])
+def test_tiny_fp32_segment(ts):
+    """B=1, H=2, d=64, L=1024, fp32 I/O; one superchunk, four, and a ragged split."""
+    w = synth.workload("tiny_fp32")
+    inp, got = seg_case(w, 1024, ts, seed=1000, dS_std=0.0)
+    check_all("f32", got, oracle_run(inp), inp)
+    inp, got = seg_case(w, 1024, ts, seed=1001, dS_std=0.1, s_in_std=0.1)
+    check_all("f32", got, oracle_run(inp), inp)
+
+
+@pytest.mark.parametrize("D", [128, 64])
+@pytest.mark.parametrize("ts", [4096, 128, 64])
+def test_bf16_segment_paths(D, ts):
+    """B=2, H=3, L=448 (7 chunks): single superchunk, ragged 128-token
+    superchunks (128,128,128,64), and one superchunk per chunk."""
+    w = synth.workload("mid_bf16", B=2, H=3, D=D)
+    inp, got = seg_case(w, 448, ts, seed=7 + D + ts)
+    check_all("bf16", got, oracle_run(inp), inp)
+
+
+def test_fp32_strong_decay_and_memoryless():
+    """Very negative gates (a_t -> 0): each token sees only itself."""
+    w = synth.workload("tiny_fp32", g_mu=-30.0)
+    inp, got = seg_case(w, 256, 128, seed=3)
+    check_all("f32", got, oracle_run(inp), inp)
+
+
+def test_empty_segment():
+    w = synth.workload("mid_bf16", B=1, H=2, D=128)
+    inp = on_gpu(synth.make_inputs(w, device="cpu", seed=5, dS_out_std=0.1, L=64))
+    q0 = inp["q"][:, :0]
+    g0 = inp["g"][:, :0]
+    say("[seg] empty segment")
+    o, S_out = sf.segment_fwd(q0, q0, q0, g0, inp["S_in"])
+    _, _, _, _, dS_in = sf.segment_bwd(q0, q0, q0, g0, inp["S_in"], q0, inp["dS_out"])
+    torch.cuda.synchronize()
+    assert o.numel() == 0
+    assert torch.equal(S_out, inp["S_in"])
+    assert torch.equal(dS_in, inp["dS_out"])
+
+
+def run_chain(g, seg_lens, ts=0, overlap=True):
+    o, S_bnd = sf.chain_fwd(g["q"], g["k"], g["v"], g["g"], seg_lens, g["S_in"], ts=ts, overlap=overlap)
+    dq, dk, dv, dg, dS0 = sf.chain_bwd(g["q"], g["k"], g["v"], g["g"], seg_lens, S_bnd, g["dO"], g["dS_out"],
+                                       ts=ts, overlap=overlap)
+    torch.cuda.synchronize()
+    return dict(o=o, S_bnd=S_bnd, S_out=S_bnd[-1], dq=dq, dk=dk, dv=dv, dg=dg, dS_in=dS0)
+
+
+def check_chain(io, inp, got, seg_lens, pairs=None):
+    pos = np.cumsum([0] + list(seg_lens)).tolist()
+    ref = oracle_run(inp, pairs=pairs, snap_pos=pos)
+    check_all(io, got, ref, inp)
+    for i in range(1, len(pos) - 1):  # interior boundary states
+        X = got["S_bnd"][i]
+        X = select_state(X, ref["pairs"])
+        assert_close(f"S_bnd{i}", to64(X), ref["snaps"][i], io)
+
+
+@pytest.mark.parametrize("ts", [0, 64, 128])
+def test_chain_nonuniform_small(ts):
+    """Four nonuniform segments, chained; overlap on and off agree bitwise."""
+    w = synth.workload("mid_bf16", B=1, H=4, D=128)
+    seg_lens = [192, 64, 320, 128]
+    inp = synth.make_inputs(w, device="cpu", seed=11, dS_out_std=0.1, L=sum(seg_lens))
+    g = on_gpu(inp)
+    say(f"[chain] small nonuniform ts={ts}")
+    a = run_chain(g, seg_lens, ts=ts, overlap=True)
+    b = run_chain(g, seg_lens, ts=ts, overlap=False)
+    for key in a:
+        assert torch.equal(a[key], b[key]), key
+    check_chain("bf16", inp, a, seg_lens)
+
+
+def test_mid_layer_chain():
+    """B=1, H=16, d=128, L=32768 in 8 segments of 4096, bf16 I/O, S_in ~ 0.1 N(0,1)."""
+    w = synth.workload("mid_bf16")
+    say("[chain] mid_bf16 full size")
+    inp = synth.make_inputs(w, device=DEV, seed=1001, dS_out_std=0.1)
+    got = run_chain(inp, w["seg_lens"])
+    check_chain("bf16", inp, got, w["seg_lens"])
+
+
+def test_scan_stress_sampled():
+    """B=4, H=32, L=16384 in 32 segments of 512 with strong decay; oracle on
+    six (batch, head) pairs."""
+    w = synth.workload("scan_stress")
+    say("[chain] scan_stress full size")
+    inp = synth.make_inputs(w, device=DEV, seed=1004, dS_out_std=0.1)
+    got = run_chain(inp, w["seg_lens"])
+    again = run_chain(inp, w["seg_lens"], overlap=False)
+    for key in got:
+        assert torch.equal(got[key], again[key]), key
+    check_chain("bf16", inp, got, w["seg_lens"], pairs=[(0, 0), (1, 7), (2, 31), (3, 16), (0, 20), (3, 3)])
+
+
+def test_ctx256k_sampled():
+    """B=1, H=40, d=128, L=262144 in 8 nonuniform segments (the 256K-context
+    workload).  Full-size run; the oracle checks one head end to end; the run
+    is repeated and must be bitwise identical."""
+    w = synth.workload("ctx256k_h40")
+    say("[chain] ctx256k_h40 full size")
+    inp = synth.make_inputs(w, device=DEV, seed=1002, dS_out_std=0.0)
+    got = run_chain(inp, w["seg_lens"])
+    again = run_chain(inp, w["seg_lens"])
+    for key in ("o", "dq", "dg", "dS_in"):
+        assert torch.equal(got[key], again[key]), key
+    say("[chain] ctx256k_h40 oracle on head 17")
+    check_chain("bf16", inp, got, w["seg_lens"], pairs=[(0, 17)])
+
+
+def test_vector_gate_reports_unsupported():
+    w = synth.workload("vector_gate", B=1, H=2)
+    inp = on_gpu(synth.make_inputs(w, device="cpu", seed=3, L=256))
+    with pytest.raises(sf.StateflowError) as e:
+        sf.segment_fwd(inp["q"], inp["k"], inp["v"], inp["g"])
+    assert "SF_E_UNSUPPORTED" in str(e.value)
