@@ -17,8 +17,15 @@
 namespace sf {
 
 constexpr int C = 64;     // kernel-level chunk (tokens)
-constexpr int NT = 256;   // threads per workgroup (4 waves)
 constexpr float LOG2E = 1.4426950408889634f;
+
+// Computed bf16 MFMA operands (decayed scores, decayed keys/queries, states)
+// are carried as hi + lo bf16 pairs (x = hi + lo to ~2^-17 relative), so the
+// only bf16 rounding left on the dense path is that of the inputs and outputs.
+#ifndef SF_SPLIT_BF16
+#define SF_SPLIT_BF16 1
+#endif
+template <typename T> constexpr bool kSplit = sizeof(T) == 2 && SF_SPLIT_BF16;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
@@ -30,8 +37,20 @@ template <> struct Frag<__bf16> { typedef bf16x8 type; };
 template <> struct Frag<float> { typedef f32x8 type; };
 template <typename T> using frag_t = typename Frag<T>::type;
 
-// Padding of 16 bytes per LDS row keeps the 16-row fragment reads conflict-free.
-template <typename T> constexpr int pad() { return 16 / (int)sizeof(T); }
+// LDS rows are padded by 32 bytes: on gfx950 the 16-row x 16-byte fragment
+// reads are conflict-free when the row pitch is 32 modulo 64 bytes (measured
+// with SQ_LDS_BANK_CONFLICT over pitches 256..576 B).
+template <typename T> constexpr int pad() { return 32 / (int)sizeof(T); }
+
+// Natural tiles [token][channel] keep each 32-channel group permuted so that
+// physical columns 8q..8q+7 hold logical channels {4q..4q+3, 16+4q..16+4q+3}:
+// a plain 16-byte fragment read then returns the slot order of an accumulator
+// pair (frag_from_acc / split_acc).  Products that contract two natural tiles
+// see the same permutation on both sides and are unaffected.
+__device__ __forceinline__ int nat_pos(int l) {
+    const int g = l & ~31, r = l & 31;
+    return g + (r < 16 ? 8 * (r >> 2) + (r & 3) : 8 * ((r - 16) >> 2) + 4 + (r & 3));
+}
 
 __device__ __forceinline__ void mma(f32x4 &c, const bf16x8 &a, const bf16x8 &b) {
     c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -74,28 +93,6 @@ __device__ __forceinline__ frag_t<T> ldfragT(const T *base, int ldt, int row0, i
     }
 }
 
-// Same rows, but the contraction slots follow an accumulator pair: slot j < 4 is
-// column k0 + 4*(l/16) + j, slot j >= 4 is column k0 + 16 + 4*(l/16) + (j-4).
-// Pairs with frag_from_acc() on the other operand.
-template <typename T>
-__device__ __forceinline__ frag_t<T> ldfrag_perm(const T *base, int ld, int row0, int k0, int lane);
-template <>
-__device__ __forceinline__ bf16x8 ldfrag_perm<__bf16>(const __bf16 *base, int ld, int row0, int k0,
-                                                      int lane) {
-    const __bf16 *p = base + (row0 + (lane & 15)) * ld + k0 + 4 * (lane >> 4);
-    bf16x4 lo = *reinterpret_cast<const bf16x4 *>(p);
-    bf16x4 hi = *reinterpret_cast<const bf16x4 *>(p + 16);
-    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-}
-template <>
-__device__ __forceinline__ f32x8 ldfrag_perm<float>(const float *base, int ld, int row0, int k0,
-                                                    int lane) {
-    const float *p = base + (row0 + (lane & 15)) * ld + k0 + 4 * (lane >> 4);
-    f32x4 lo = *reinterpret_cast<const f32x4 *>(p);
-    f32x4 hi = *reinterpret_cast<const f32x4 *>(p + 16);
-    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-}
-
 // Operand fragment built from two accumulator tiles X[m0..m0+15][n] (a0) and
 // X[m0+16..m0+31][n] (a1): as an A operand it is X^T rows n, contraction over m.
 template <typename T>
@@ -133,10 +130,63 @@ __device__ __forceinline__ f32x4 ld4f(const __bf16 *p) {
 }
 __device__ __forceinline__ f32x4 ld4f(const float *p) { return *reinterpret_cast<const f32x4 *>(p); }
 
+// hi/lo split of 8 fp32 values: hi = T(x), lo = T(x - hi)
+template <typename T>
+__device__ __forceinline__ void split8(const float *x, frag_t<T> &hi, frag_t<T> &lo) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const T h = cvt<T>(x[j]);
+        hi[j] = h;
+        lo[j] = cvt<T>(x[j] - tof<T>(h));
+    }
+}
+// split fragment of two accumulator tiles (see frag_from_acc)
+template <typename T>
+__device__ __forceinline__ void split_acc(const f32x4 &a0, const f32x4 &a1, frag_t<T> &hi, frag_t<T> &lo) {
+    float x[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+    split8<T>(x, hi, lo);
+}
+// split fragment of a T fragment scaled per slot by s[] (fp32)
+template <typename T>
+__device__ __forceinline__ void split_scaled(const frag_t<T> &f, const float *s, frag_t<T> &hi, frag_t<T> &lo) {
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = tof<T>(f[j]) * s[j];
+    split8<T>(x, hi, lo);
+}
+// acc += a * b, with a given as a hi/lo pair (lo skipped when not splitting)
+template <typename T>
+__device__ __forceinline__ void mma2(f32x4 &c, const frag_t<T> &ahi, const frag_t<T> &alo, const frag_t<T> &b) {
+    mma(c, ahi, b);
+    if constexpr (kSplit<T>) mma(c, alo, b);
+}
+template <typename T>
+__device__ __forceinline__ void mma2b(f32x4 &c, const frag_t<T> &a, const frag_t<T> &bhi, const frag_t<T> &blo) {
+    mma(c, a, bhi);
+    if constexpr (kSplit<T>) mma(c, a, blo);
+}
+// 4 consecutive fp32 values stored as a hi/lo pair of T vectors
+template <typename T>
+__device__ __forceinline__ void st4_split(T *hi, T *lo, const float *v) {
+    if constexpr (kSplit<T>) {
+        float h[4], l[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const T x = cvt<T>(v[j]);
+            h[j] = tof<T>(x);
+            l[j] = v[j] - h[j];
+        }
+        st4(hi, h[0], h[1], h[2], h[3]);
+        st4(lo, l[0], l[1], l[2], l[3]);
+    } else {
+        st4(hi, v[0], v[1], v[2], v[3]);
+    }
+}
+
 // A chunk tile of C tokens x D channels moving global -> registers -> LDS.
 // Thread `tid` owns rows (tokens) row0 .. row0+RPT-1 and one 16-byte column
 // block cb (E channels), so 8..16 consecutive lanes read one contiguous row.
-template <typename T, int D>
+template <typename T, int D, int NT>
 struct Tile {
     static constexpr int E = 16 / (int)sizeof(T);
     static constexpr int CB = D / E;
@@ -154,11 +204,23 @@ struct Tile {
 #pragma unroll
         for (int j = 0; j < RPT; ++j) r[j] = *reinterpret_cast<const vecE *>(p + (int64_t)j * row_stride);
     }
-    // natural layout [token][channel], row pitch ld
+    // natural layout [token][channel] (channels permuted by nat_pos), row pitch ld
     __device__ __forceinline__ void store_nat(T *lds, int ld, int tid) const {
-        T *p = lds + row0(tid) * ld + cb(tid) * E;
+        T *p = lds + row0(tid) * ld;
+        const int ch = cb(tid) * E;
+        if constexpr (E == 8) {
+            typedef T half_t __attribute__((ext_vector_type(4)));
+            const int p0 = nat_pos(ch), p1 = nat_pos(ch + 4);
 #pragma unroll
-        for (int j = 0; j < RPT; ++j) *reinterpret_cast<vecE *>(p + j * ld) = r[j];
+            for (int j = 0; j < RPT; ++j) {
+                *reinterpret_cast<half_t *>(p + j * ld + p0) = __builtin_shufflevector(r[j], r[j], 0, 1, 2, 3);
+                *reinterpret_cast<half_t *>(p + j * ld + p1) = __builtin_shufflevector(r[j], r[j], 4, 5, 6, 7);
+            }
+        } else {
+            const int p0 = nat_pos(ch);
+#pragma unroll
+            for (int j = 0; j < RPT; ++j) *reinterpret_cast<vecE *>(p + j * ld + p0) = r[j];
+        }
     }
     // swizzled transposed layout [channel][token] (see tswz), token j scaled by s[j]
     __device__ __forceinline__ void store_T(T *lds, int ldt, int tid, const float *s) const {
@@ -180,6 +242,26 @@ struct Tile {
 #pragma unroll
             for (int j = 0; j < RPT; ++j) vals[j] = r[j][i];
             put_T(lds + (c0 + i) * ldt, c0 + i, t0, vals);
+        }
+    }
+    // swizzled transposed layout with each scaled value kept as hi (lds) + lo (lds_lo)
+    __device__ __forceinline__ void store_T2(T *lds, T *lds_lo, int ldt, int tid, const float *s) const {
+        if constexpr (!kSplit<T>) {
+            store_T(lds, ldt, tid, s);
+        } else {
+            const int c0 = cb(tid) * E, t0 = row0(tid);
+#pragma unroll
+            for (int i = 0; i < E; ++i) {
+                vecR hi, lo;
+#pragma unroll
+                for (int j = 0; j < RPT; ++j) {
+                    const float x = tof<T>(r[j][i]) * s[j];
+                    hi[j] = cvt<T>(x);
+                    lo[j] = cvt<T>(x - tof<T>(hi[j]));
+                }
+                put_T(lds + (c0 + i) * ldt, c0 + i, t0, hi);
+                put_T(lds_lo + (c0 + i) * ldt, c0 + i, t0, lo);
+            }
         }
     }
     // RPT consecutive tokens of one transposed row; split at 16-byte blocks

@@ -10,7 +10,8 @@
 //   state:  S_{c+1} = exp(b_63) S_c + (K o exp(b_63 - b))^T V
 // Every exponent is <= 0 (g <= 0), so no factor can overflow.
 //
-// Kernels (one workgroup of 256 threads per (batch, head, superchunk)):
+// Kernels (one workgroup of D/16 waves per (batch, head, superchunk); wave w
+// owns the 16 state columns [16w, 16w+16)):
 //   k_prep<.., BWD=false>  Pre: superchunk state contribution D_J and its decay
 //   k_scan<false>          ST:  S_{J+1} = Gamma_J S_J + D_J (fp32), S_out
 //   k_walk<.., DQ=false>   Out: walk the chunks from S_J, write o
@@ -25,6 +26,18 @@
 #include "sf_launch.hpp"
 
 namespace sf {
+
+template <typename T, int D>
+struct Cfg {
+    static constexpr int NW = D / 16;        // waves; wave w owns state column tile w
+    static constexpr int NT = 64 * NW;       // threads
+    static constexpr int NK = D / 16;        // 16-row tiles of a D x D state
+    static constexpr int LDN = D + pad<T>(); // natural tile [token][channel] pitch
+    static constexpr int LDT = C + pad<T>(); // transposed tile [row][token] pitch
+    static constexpr bool SP = kSplit<T>;
+    static_assert(NT == 4 * D, "kernels declare __launch_bounds__(4 * D)");
+};
+constexpr int SCAN_NT = 256;
 
 // (t-tile, s-tile) pairs of the causal 64x64 score matrix, s-tile <= t-tile.
 __device__ __forceinline__ void tri_tile(int i, int &tt, int &st) {
@@ -52,17 +65,20 @@ __device__ __forceinline__ Decode decode(const SegArgs &a) {
 // ---------------------------------------------------------------------------
 // Pre: per superchunk, D_J = sum_c (decay after c) (K~_c)^T V_c, and for the
 // backward E_J = sum_t exp(B_t) q_t dO_t^T (B superchunk-local, inclusive).
-// State tiles: wave w owns state columns [w*D/4, (w+1)*D/4).
 template <typename T, int D, bool BWD>
-__global__ void __launch_bounds__(NT) k_prep(SegArgs a) {
-    constexpr int LDT = C + pad<T>();
-    constexpr int NK = D / 16, NV = D / 64, DW = D / 4;
+__global__ void __launch_bounds__(4 * D) k_prep(SegArgs a) {
+    using F = Cfg<T, D>;
+    constexpr int LDT = F::LDT, NK = F::NK, NT = F::NT;
+    constexpr bool SP = F::SP;
     __shared__ __attribute__((aligned(16))) T sKT[D * LDT];
+    __shared__ __attribute__((aligned(16))) T sKTl[SP ? D * LDT : 8];
     __shared__ __attribute__((aligned(16))) T sVT[D * LDT];
     __shared__ __attribute__((aligned(16))) T sQT[BWD ? D * LDT : 8];
+    __shared__ __attribute__((aligned(16))) T sQTl[BWD && SP ? D * LDT : 8];
     __shared__ __attribute__((aligned(16))) T sOT[BWD ? D * LDT : 8];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
+    const int c0 = 16 * w;
     const Decode d = decode(a);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *K = (const T *)a.k + xo;
@@ -70,18 +86,15 @@ __global__ void __launch_bounds__(NT) k_prep(SegArgs a) {
     const T *Q = (const T *)a.q + xo;
     const T *dO = (const T *)a.dO + xo;
     const float *gp = a.g + d.b * a.sg_b + d.h * a.sg_h + d.tok0 * a.sg_l;
-    const int c0 = w * DW;
 
-    f32x4 Ds[NK][NV], Es[BWD ? NK : 1][BWD ? NV : 1];
+    f32x4 Ds[NK], Es[BWD ? NK : 1];
 #pragma unroll
-    for (int i = 0; i < NK; ++i)
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            Ds[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if constexpr (BWD) Es[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
+    for (int i = 0; i < NK; ++i) {
+        Ds[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (BWD) Es[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 
-    Tile<T, D> tk, tv, tq, to;
+    Tile<T, D, NT> tk, tv, tq, to;
     tk.load(K, a.sx_l, tid);
     tv.load(V, a.sx_l, tid);
     if constexpr (BWD) {
@@ -96,7 +109,7 @@ __global__ void __launch_bounds__(NT) k_prep(SegArgs a) {
         const float b63 = __shfl(b2, 63, 64);
         __syncthreads();
         {
-            constexpr int R = Tile<T, D>::RPT;
+            constexpr int R = Tile<T, D, NT>::RPT;
             float ks[R], qs[R];
 #pragma unroll
             for (int j = 0; j < R; ++j) {
@@ -104,10 +117,10 @@ __global__ void __launch_bounds__(NT) k_prep(SegArgs a) {
                 ks[j] = exp2f(b63 - bj);
                 qs[j] = exp2f(off + bj);
             }
-            tk.store_T(sKT, LDT, tid, ks);
+            tk.store_T2(sKT, sKTl, LDT, tid, ks);
             tv.store_T1(sVT, LDT, tid);
             if constexpr (BWD) {
-                tq.store_T(sQT, LDT, tid, qs);
+                tq.store_T2(sQT, sQTl, LDT, tid, qs);
                 to.store_T1(sOT, LDT, tid);
             }
         }
@@ -124,28 +137,21 @@ __global__ void __launch_bounds__(NT) k_prep(SegArgs a) {
         __syncthreads();
         const float gam = exp2f(b63);
 #pragma unroll
-        for (int i = 0; i < NK; ++i)
-#pragma unroll
-            for (int j = 0; j < NV; ++j) Ds[i][j] *= gam;
+        for (int i = 0; i < NK; ++i) Ds[i] *= gam;
 #pragma unroll
         for (int ks = 0; ks < C / 32; ++ks) {
-            frag_t<T> fb[NV];
-#pragma unroll
-            for (int j = 0; j < NV; ++j) fb[j] = ldfragT(sVT, LDT, c0 + 16 * j, 32 * ks, lane);
+            const frag_t<T> fv = ldfragT(sVT, LDT, c0, 32 * ks, lane);
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
-                const frag_t<T> fa = ldfragT(sKT, LDT, 16 * i, 32 * ks, lane);
-#pragma unroll
-                for (int j = 0; j < NV; ++j) mma(Ds[i][j], fa, fb[j]);
+                mma(Ds[i], ldfragT(sKT, LDT, 16 * i, 32 * ks, lane), fv);
+                if constexpr (SP) mma(Ds[i], ldfragT(sKTl, LDT, 16 * i, 32 * ks, lane), fv);
             }
             if constexpr (BWD) {
-#pragma unroll
-                for (int j = 0; j < NV; ++j) fb[j] = ldfragT(sOT, LDT, c0 + 16 * j, 32 * ks, lane);
+                const frag_t<T> fo = ldfragT(sOT, LDT, c0, 32 * ks, lane);
 #pragma unroll
                 for (int i = 0; i < NK; ++i) {
-                    const frag_t<T> fa = ldfragT(sQT, LDT, 16 * i, 32 * ks, lane);
-#pragma unroll
-                    for (int j = 0; j < NV; ++j) mma(Es[i][j], fa, fb[j]);
+                    mma(Es[i], ldfragT(sQT, LDT, 16 * i, 32 * ks, lane), fo);
+                    if constexpr (SP) mma(Es[i], ldfragT(sQTl, LDT, 16 * i, 32 * ks, lane), fo);
                 }
             }
         }
@@ -155,13 +161,11 @@ __global__ void __launch_bounds__(NT) k_prep(SegArgs a) {
 #pragma unroll
     for (int i = 0; i < NK; ++i)
 #pragma unroll
-        for (int j = 0; j < NV; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t e = so + (int64_t)(16 * i + 4 * q4 + r) * D + c0 + 16 * j + n16;
-                a.wsS[e] = Ds[i][j][r];
-                if constexpr (BWD) a.wsE[e] = Es[i][j][r];
-            }
+        for (int r = 0; r < 4; ++r) {
+            const int64_t e = so + (int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16;
+            a.wsS[e] = Ds[i][r];
+            if constexpr (BWD) a.wsE[e] = Es[i][r];
+        }
     if (tid == 0) a.wsLg[(int64_t)d.bh * a.n_super + d.J] = off;
 }
 
@@ -172,13 +176,13 @@ __global__ void __launch_bounds__(NT) k_prep(SegArgs a) {
 // slot J of wsE is replaced by G_{J+1} (gradient of the state leaving J) and
 // the wave partials of <G_{J+1}, S_{J+1}> go to wsDot[(bh, J)][part*4 + wave].
 template <bool BWD>
-__global__ void __launch_bounds__(NT) k_scan(SegArgs a, int D) {
+__global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int parts = D * D / 1024;
     const int part = blockIdx.x % parts;
     const int64_t bh = blockIdx.x / parts;
     const int64_t SS = (int64_t)D * D;
-    const int64_t e = (int64_t)(part * NT + tid) * 4;
+    const int64_t e = (int64_t)(part * SCAN_NT + tid) * 4;
     const int n = a.n_super;
     float *Sb = a.wsS + bh * n * SS + e;
     const float *lg = a.wsLg + bh * n;
@@ -228,24 +232,28 @@ __global__ void __launch_bounds__(NT) k_scan(SegArgs a, int D) {
 //   DQ == false (Out):  X1 = q, X2 = k, X3 = v, state S[k][v];   writes o.
 //   DQ == true  (OG):   X1 = dO, X2 = v, X3 = k, state S^T[v][k]; writes dq
 //                       and r_t = q_t . dq_t into dg (read back by k_bwd_dkv).
-// The state lives as MFMA accumulators: wave w owns state columns
-// [w*D/4, (w+1)*D/4), tile (kt, vt) lane holds rows 16kt+4*(l/16)+r, column
-// 16vt+l%16, which is exactly an A-operand fragment of the transposed state
-// (frag_from_acc), so Q S needs no LDS round trip for S.
+// The state lives as MFMA accumulators: wave w owns state column tile w; row
+// tile kt of lane l holds rows 16kt+4*(l/16)+r of column 16w+l%16, which is an
+// A-operand fragment of the transposed state (split_acc), so Q S needs no LDS
+// round trip for S.
 template <typename T, int D, bool DQ>
-__global__ void __launch_bounds__(NT) k_walk(SegArgs a) {
-    constexpr int LDN = D + pad<T>(), LDT = C + pad<T>();
-    constexpr int NK = D / 16, NV = D / 64, DW = D / 4;
-    constexpr int R = Tile<T, D>::RPT;
+__global__ void __launch_bounds__(4 * D) k_walk(SegArgs a) {
+    using F = Cfg<T, D>;
+    constexpr int LDN = F::LDN, LDT = F::LDT, NK = F::NK, NW = F::NW, NT = F::NT;
+    constexpr bool SP = F::SP;
+    constexpr int R = Tile<T, D, NT>::RPT;
     __shared__ __attribute__((aligned(16))) T sX1[C * LDN];
     __shared__ __attribute__((aligned(16))) T sX2[C * LDN];
-    __shared__ __attribute__((aligned(16))) T sX2T[D * LDT];  // decayed: X2~^T
+    __shared__ __attribute__((aligned(16))) T sX2T[D * LDT];  // decayed: X2~^T (hi)
+    __shared__ __attribute__((aligned(16))) T sX2Tl[SP ? D * LDT : 8];
     __shared__ __attribute__((aligned(16))) T sX3T[D * LDT];
-    __shared__ __attribute__((aligned(16))) T sA[C * LDT];    // A[t][s]
+    __shared__ __attribute__((aligned(16))) T sA[C * LDT];    // A[t][s] (hi)
+    __shared__ __attribute__((aligned(16))) T sAl[SP ? C * LDT : 8];
     __shared__ float sb[C];
-    __shared__ float sred[DQ ? 4 * C : 1];
+    __shared__ float sred[DQ ? NW * C : 1];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
+    const int c0 = 16 * w;
     const Decode d = decode(a);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *X1 = (const T *)(DQ ? a.dO : a.q) + xo;
@@ -256,50 +264,46 @@ __global__ void __launch_bounds__(NT) k_walk(SegArgs a) {
     const int64_t go = d.b * a.sg_b + d.h * a.sg_h + d.tok0 * a.sg_l;
     const float *gp = a.g + go;
     float *dgp = a.dg + go;
-    const int c0 = w * DW;
     const int64_t SS = (int64_t)D * D;
 
-    // initial state S_J
+    // initial state S_J (column tile w)
     const float *src = a.n_super == 1 ? (a.S_in ? a.S_in + d.bh * SS : nullptr)
                                       : a.wsS + ((int64_t)d.bh * a.n_super + d.J) * SS;
-    f32x4 S[NK][NV];
+    f32x4 S[NK];
 #pragma unroll
-    for (int i = 0; i < NK; ++i)
+    for (int i = 0; i < NK; ++i) {
+        const int col = c0 + n16, row = 16 * i + 4 * q4;
+        if (!src) {
+            S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        } else if constexpr (!DQ) {
 #pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            const int col = c0 + 16 * j + n16, row = 16 * i + 4 * q4;
-            if (!src) {
-                S[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-            } else if constexpr (!DQ) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) S[i][j][r] = src[(int64_t)(row + r) * D + col];
-            } else {
-                S[i][j] = *reinterpret_cast<const f32x4 *>(src + (int64_t)col * D + row);
-            }
+            for (int r = 0; r < 4; ++r) S[i][r] = src[(int64_t)(row + r) * D + col];
+        } else {
+            S[i] = *reinterpret_cast<const f32x4 *>(src + (int64_t)col * D + row);
         }
+    }
     // A tiles read by the A.V product but above the diagonal stay zero
-    {
-        const int rr = tid >> 4, cc = tid & 15;
-        sA[rr * LDT + 16 + cc] = cvt<T>(0.f);
-        sA[(32 + rr) * LDT + 48 + cc] = cvt<T>(0.f);
+    for (int e = tid; e < 512; e += NT) {
+        const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
+        const int idx = tile ? (32 + rr) * LDT + 48 + cc : rr * LDT + 16 + cc;
+        sA[idx] = cvt<T>(0.f);
+        if constexpr (SP) sAl[idx] = cvt<T>(0.f);
     }
 
-    Tile<T, D> t1, t2, t3;
+    Tile<T, D, NT> t1, t2, t3;
     t1.load(X1, a.sx_l, tid);
     t2.load(X2, a.sx_l, tid);
     t3.load(X3, a.sx_l, tid);
     float gl = gp[lane * a.sg_l];
     // DQ: q values of this lane's dq elements, one chunk ahead
     typedef T vec4T __attribute__((ext_vector_type(4)));
-    vec4T qn[DQ ? 4 : 1][DQ ? NV : 1];
+    vec4T qn[DQ ? 4 : 1];
     auto load_q = [&](int c) {
         if constexpr (DQ) {
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-                for (int j = 0; j < NV; ++j)
-                    qn[tt][j] = *reinterpret_cast<const vec4T *>(
-                        Qd + (int64_t)(c * C + 16 * tt + n16) * a.sx_l + c0 + 16 * j + 4 * q4);
+                qn[tt] = *reinterpret_cast<const vec4T *>(Qd + (int64_t)(c * C + 16 * tt + n16) * a.sx_l +
+                                                           c0 + 4 * q4);
         }
     };
     load_q(0);
@@ -307,12 +311,10 @@ __global__ void __launch_bounds__(NT) k_walk(SegArgs a) {
     for (int c = 0; c < d.nch; ++c) {
         const float b2 = wave_incl_scan(gl * LOG2E, lane);
         const float b63 = __shfl(b2, 63, 64);
-        vec4T qc[DQ ? 4 : 1][DQ ? NV : 1];
+        vec4T qc[DQ ? 4 : 1];
         if constexpr (DQ) {
 #pragma unroll
-            for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-                for (int j = 0; j < NV; ++j) qc[tt][j] = qn[tt][j];
+            for (int tt = 0; tt < 4; ++tt) qc[tt] = qn[tt];
         }
         __syncthreads();
         if (w == 0) sb[lane] = b2;
@@ -322,7 +324,7 @@ __global__ void __launch_bounds__(NT) k_walk(SegArgs a) {
             for (int j = 0; j < R; ++j) ks[j] = exp2f(b63 - __shfl(b2, t2.row0(tid) + j, 64));
             t1.store_nat(sX1, LDN, tid);
             t2.store_nat(sX2, LDN, tid);
-            t2.store_T(sX2T, LDT, tid, ks);
+            t2.store_T2(sX2T, sX2Tl, LDT, tid, ks);
             t3.store_T1(sX3T, LDT, tid);
         }
         if (c + 1 < d.nch) {
@@ -335,8 +337,8 @@ __global__ void __launch_bounds__(NT) k_walk(SegArgs a) {
         }
         __syncthreads();
 
-        // scores P^T[s][t] = sum_ch X2[s][ch] X1[t][ch] on the causal tiles
-        for (int i = w; i < 10; i += 4) {
+        // scores P^T[s][t] = sum_ch X2[s][ch] X1[t][ch] on the causal tiles -> A[t][s]
+        for (int i = w; i < 10; i += NW) {
             int tt, st;
             tri_tile(i, tt, st);
             f32x4 p = {0.f, 0.f, 0.f, 0.f};
@@ -351,60 +353,44 @@ __global__ void __launch_bounds__(NT) k_walk(SegArgs a) {
                 const int s = 16 * st + 4 * q4 + r;
                 v4[r] = s <= t ? p[r] * exp2f(bt - sb[s]) : 0.f;
             }
-            st4(&sA[t * LDT + 16 * st + 4 * q4], v4[0], v4[1], v4[2], v4[3]);
+            const int o = t * LDT + 16 * st + 4 * q4;
+            st4_split<T>(&sA[o], &sAl[SP ? o : 0], v4);
         }
         __syncthreads();
 
         // Y^T[col][t] = exp(b_t) sum_m S[m][col] X1[t][m] + sum_s X3[s][col] A[t][s]
-        f32x4 O[NV][4];
+        f32x4 O[4];
 #pragma unroll
-        for (int j = 0; j < NV; ++j)
-#pragma unroll
-            for (int tt = 0; tt < 4; ++tt) O[j][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int tt = 0; tt < 4; ++tt) O[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < D / 32; ++ks) {
-            frag_t<T> fs[NV];
+            frag_t<T> fh, fl;
+            split_acc<T>(S[2 * ks], S[2 * ks + 1], fh, fl);
 #pragma unroll
-            for (int j = 0; j < NV; ++j) fs[j] = frag_from_acc<T>(S[2 * ks][j], S[2 * ks + 1][j]);
-#pragma unroll
-            for (int tt = 0; tt < 4; ++tt) {
-                const frag_t<T> fb = ldfrag_perm(sX1, LDN, 16 * tt, 32 * ks, lane);
-#pragma unroll
-                for (int j = 0; j < NV; ++j) mma(O[j][tt], fs[j], fb);
-            }
+            for (int tt = 0; tt < 4; ++tt) mma2<T>(O[tt], fh, fl, ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane));
         }
 #pragma unroll
-        for (int tt = 0; tt < 4; ++tt) {
-            const float et = exp2f(sb[16 * tt + n16]);
-#pragma unroll
-            for (int j = 0; j < NV; ++j) O[j][tt] *= et;
-        }
+        for (int tt = 0; tt < 4; ++tt) O[tt] *= exp2f(sb[16 * tt + n16]);
 #pragma unroll
         for (int ks = 0; ks < C / 32; ++ks) {
-            frag_t<T> fa[NV];
-#pragma unroll
-            for (int j = 0; j < NV; ++j) fa[j] = ldfragT(sX3T, LDT, c0 + 16 * j, 32 * ks, lane);
+            const frag_t<T> fa = ldfragT(sX3T, LDT, c0, 32 * ks, lane);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
                 if (32 * ks > 16 * tt + 15) continue;
-                const frag_t<T> fb = ldfrag(sA, LDT, 16 * tt, 32 * ks, lane);
-#pragma unroll
-                for (int j = 0; j < NV; ++j) mma(O[j][tt], fa[j], fb);
+                mma(O[tt], fa, ldfrag(sA, LDT, 16 * tt, 32 * ks, lane));
+                if constexpr (SP) mma(O[tt], fa, ldfrag(sAl, LDT, 16 * tt, 32 * ks, lane));
             }
         }
         float part[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int tt = 0; tt < 4; ++tt) {
             const int64_t trow = (int64_t)(c * C + 16 * tt + n16) * a.sx_l;
-#pragma unroll
-            for (int j = 0; j < NV; ++j) {
-                const int col = c0 + 16 * j + 4 * q4;
-                st4(Y + trow + col, O[j][tt][0], O[j][tt][1], O[j][tt][2], O[j][tt][3]);
-                if constexpr (DQ) {
-                    const vec4T qv = qc[tt][j];
-                    part[tt] += O[j][tt][0] * tof<T>(qv[0]) + O[j][tt][1] * tof<T>(qv[1]) +
-                                O[j][tt][2] * tof<T>(qv[2]) + O[j][tt][3] * tof<T>(qv[3]);
-                }
+            const int col = c0 + 4 * q4;
+            st4(Y + trow + col, O[tt][0], O[tt][1], O[tt][2], O[tt][3]);
+            if constexpr (DQ) {
+                const vec4T qv = qc[tt];
+                part[tt] = O[tt][0] * tof<T>(qv[0]) + O[tt][1] * tof<T>(qv[1]) + O[tt][2] * tof<T>(qv[2]) +
+                           O[tt][3] * tof<T>(qv[3]);
             }
         }
         if constexpr (DQ) {
@@ -419,26 +405,24 @@ __global__ void __launch_bounds__(NT) k_walk(SegArgs a) {
         // state update S = exp(b_63) S + X2~^T X3
         const float gam = exp2f(b63);
 #pragma unroll
-        for (int i = 0; i < NK; ++i)
-#pragma unroll
-            for (int j = 0; j < NV; ++j) S[i][j] *= gam;
+        for (int i = 0; i < NK; ++i) S[i] *= gam;
 #pragma unroll
         for (int ks = 0; ks < C / 32; ++ks) {
-            frag_t<T> fb[NV];
-#pragma unroll
-            for (int j = 0; j < NV; ++j) fb[j] = ldfragT(sX3T, LDT, c0 + 16 * j, 32 * ks, lane);
+            const frag_t<T> fb = ldfragT(sX3T, LDT, c0, 32 * ks, lane);
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
-                const frag_t<T> fa = ldfragT(sX2T, LDT, 16 * i, 32 * ks, lane);
-#pragma unroll
-                for (int j = 0; j < NV; ++j) mma(S[i][j], fa, fb[j]);
+                mma(S[i], ldfragT(sX2T, LDT, 16 * i, 32 * ks, lane), fb);
+                if constexpr (SP) mma(S[i], ldfragT(sX2Tl, LDT, 16 * i, 32 * ks, lane), fb);
             }
         }
         if constexpr (DQ) {
             __syncthreads();
-            if (w == 0)
-                dgp[(int64_t)(c * C + lane) * a.sg_l] =
-                    sred[lane] + sred[C + lane] + sred[2 * C + lane] + sred[3 * C + lane];
+            if (w == 0) {
+                float r = 0.f;
+#pragma unroll
+                for (int ww = 0; ww < NW; ++ww) r += sred[ww * C + lane];
+                dgp[(int64_t)(c * C + lane) * a.sg_l] = r;
+            }
         }
     }
 
@@ -449,59 +433,64 @@ __global__ void __launch_bounds__(NT) k_walk(SegArgs a) {
 #pragma unroll
                 for (int i = 0; i < NK; ++i)
 #pragma unroll
-                    for (int j = 0; j < NV; ++j)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r)
-                            dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + 16 * j + n16] = S[i][j][r];
+                    for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = S[i][r];
             }
         } else {
-            // <dS_out, S_out> for dg (state here is S_out^T)
+            // <dS_out, S_out> for dg (the state here is S_out^T)
             float p = 0.f;
             if (a.dS_out) {
                 const float *ds = a.dS_out + d.bh * SS;
 #pragma unroll
-                for (int i = 0; i < NK; ++i)
-#pragma unroll
-                    for (int j = 0; j < NV; ++j) {
-                        const f32x4 x = *reinterpret_cast<const f32x4 *>(
-                            ds + (int64_t)(c0 + 16 * j + n16) * D + 16 * i + 4 * q4);
-                        p += x[0] * S[i][j][0] + x[1] * S[i][j][1] + x[2] * S[i][j][2] + x[3] * S[i][j][3];
-                    }
+                for (int i = 0; i < NK; ++i) {
+                    const f32x4 x =
+                        *reinterpret_cast<const f32x4 *>(ds + (int64_t)(c0 + n16) * D + 16 * i + 4 * q4);
+                    p += x[0] * S[i][0] + x[1] * S[i][1] + x[2] * S[i][2] + x[3] * S[i][3];
+                }
             }
             p = wave_sum(p);
             const int ndot = D * D / 256;
             float *dot = a.wsDot + (int64_t)d.bh * ndot;
             if (lane == 0) dot[w] = p;
-            if (w == 0 && lane >= 4 && lane < ndot) dot[lane] = 0.f;
+            if (w == 0 && lane >= NW && lane < ndot) dot[lane] = 0.f;
         }
     }
 }
 
 // ---------------------------------------------------------------------------
 // PG: reverse walk over the chunks of a superchunk with the state gradient G
-// (dLoss/dS of the state leaving the chunk) in registers:
+// (dLoss/dS of the state leaving the chunk) in registers, in both
+// orientations: G[k][v] (wave w owns v-tile w) feeds dv, G^T[v][k] (wave w
+// owns k-tile w) feeds dk, so neither needs G through LDS:
 //   dv^T = exp(b_63 - b_s) G^T K^T + dO^T A^T      (A from Q K^T)
 //   dk^T = exp(b_63 - b_s) G V^T   + Q^T dA^T      (dA from dO V^T)
-//   G   <- exp(b_63) G + (Q o exp(b))^T dO
+//   G   <- exp(b_63) G + (Q o exp(b))^T dO          (and its transpose)
 //   dg_t = sum_{t' >= t in superchunk} (q.dq - k.dk)_{t'} + <G_{J+1}, S_{J+1}>
 // (the last term is the decay gradient carried in from later superchunks).
 template <typename T, int D>
-__global__ void __launch_bounds__(NT) k_bwd_dkv(SegArgs a) {
-    constexpr int LDN = D + pad<T>(), LDT = C + pad<T>();
-    constexpr int NK = D / 16, NV = D / 64, DW = D / 4;
+__global__ void __launch_bounds__(4 * D) k_bwd_dkv(SegArgs a) {
+    using F = Cfg<T, D>;
+    constexpr int LDN = F::LDN, LDT = F::LDT, NK = F::NK, NW = F::NW, NT = F::NT;
+    constexpr bool SP = F::SP;
     __shared__ __attribute__((aligned(16))) T sQ[C * LDN];
     __shared__ __attribute__((aligned(16))) T sK[C * LDN];
     __shared__ __attribute__((aligned(16))) T sV[C * LDN];
     __shared__ __attribute__((aligned(16))) T sO[C * LDN];   // dO
     __shared__ __attribute__((aligned(16))) T sQT[D * LDT];
     __shared__ __attribute__((aligned(16))) T sOT[D * LDT];  // dO^T
-    __shared__ __attribute__((aligned(16))) T sAT[C * LDT];  // A^T[s][t]
-    __shared__ __attribute__((aligned(16))) T sdAT[C * LDT]; // dA^T[s][t]
-    __shared__ __attribute__((aligned(16))) T sG[D * LDN];   // G[k][v]
+    // scratch: A^T and dA^T (hi, lo) for the dv/dk products, then (Q o exp(b))^T
+    // (hi, lo) for the state-gradient update
+    constexpr int NS = SP ? 2 : 1;
+    constexpr int SCR = 2 * NS * C * LDT;
+    static_assert(NS * D * LDT <= SCR, "scratch holds the scaled Q^T");
+    __shared__ __attribute__((aligned(16))) T sScr[SCR];
+    T *sAT = sScr, *sATl = sScr + (NS - 1) * C * LDT;            // A^T[s][t]
+    T *sdAT = sScr + NS * C * LDT, *sdATl = sdAT + (NS - 1) * C * LDT;  // dA^T[s][t]
+    T *sQs = sScr, *sQsl = sScr + (NS - 1) * D * LDT;              // (Q o exp(b))^T
     __shared__ float sb[C];
-    __shared__ float sred[4 * C];
+    __shared__ float sred[NW * C];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
+    const int c0 = 16 * w;
     const Decode d = decode(a);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *Q = (const T *)a.q + xo;
@@ -513,34 +502,29 @@ __global__ void __launch_bounds__(NT) k_bwd_dkv(SegArgs a) {
     const int64_t go = d.b * a.sg_b + d.h * a.sg_h + d.tok0 * a.sg_l;
     const float *gp = a.g + go;
     float *dgp = a.dg + go;
-    const int c0 = w * DW;
     const int64_t SS = (int64_t)D * D;
     const int ndot = D * D / 256;
 
     const float *gsrc = a.n_super == 1 ? (a.dS_out ? a.dS_out + d.bh * SS : nullptr)
                                        : a.wsE + ((int64_t)d.bh * a.n_super + d.J) * SS;
-    f32x4 G[NK][NV];
+    f32x4 G[NK], GT[NK];  // G[k][v] (v-tile w) and G^T[v][k] (k-tile w)
 #pragma unroll
-    for (int i = 0; i < NK; ++i)
+    for (int i = 0; i < NK; ++i) {
+        if (!gsrc) {
+            G[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            GT[i] = G[i];
+        } else {
 #pragma unroll
-        for (int j = 0; j < NV; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                G[i][j][r] = gsrc ? gsrc[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + 16 * j + n16] : 0.f;
+            for (int r = 0; r < 4; ++r) G[i][r] = gsrc[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16];
+            GT[i] = *reinterpret_cast<const f32x4 *>(gsrc + (int64_t)(c0 + n16) * D + 16 * i + 4 * q4);
+        }
+    }
     float carry;
     {
         const float *dot = a.wsDot + ((int64_t)d.bh * a.n_super + d.J) * ndot;
         carry = wave_sum(lane < ndot ? dot[lane] : 0.f);
     }
-    {
-        const int rr = tid >> 4, cc = tid & 15;
-        sAT[(16 + rr) * LDT + cc] = cvt<T>(0.f);
-        sAT[(48 + rr) * LDT + 32 + cc] = cvt<T>(0.f);
-        sdAT[(16 + rr) * LDT + cc] = cvt<T>(0.f);
-        sdAT[(48 + rr) * LDT + 32 + cc] = cvt<T>(0.f);
-    }
-
-    Tile<T, D> tq, tk, tv, to;
+    Tile<T, D, NT> tq, tk, tv, to;
     {
         const int64_t nx = (int64_t)(d.nch - 1) * C * a.sx_l;
         tq.load(Q + nx, a.sx_l, tid);
@@ -563,13 +547,18 @@ __global__ void __launch_bounds__(NT) k_bwd_dkv(SegArgs a) {
         to.store_nat(sO, LDN, tid);
         tq.store_T1(sQT, LDT, tid);
         to.store_T1(sOT, LDT, tid);
-#pragma unroll
-        for (int i = 0; i < NK; ++i)
-#pragma unroll
-            for (int j = 0; j < NV; ++j)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    sG[(16 * i + 4 * q4 + r) * LDN + c0 + 16 * j + n16] = cvt<T>(G[i][j][r]);
+        // score tiles read by the dv/dk products but above the diagonal are zero
+        // (rewritten every chunk: the scratch also holds the scaled Q^T)
+        for (int e = tid; e < 512; e += NT) {
+            const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
+            const int idx = tile ? (48 + rr) * LDT + 32 + cc : (16 + rr) * LDT + cc;
+            sAT[idx] = cvt<T>(0.f);
+            sdAT[idx] = cvt<T>(0.f);
+            if constexpr (SP) {
+                sATl[idx] = cvt<T>(0.f);
+                sdATl[idx] = cvt<T>(0.f);
+            }
+        }
         if (c > 0) {
             const int64_t nx = (int64_t)(c - 1) * C * a.sx_l;
             tq.load(Q + nx, a.sx_l, tid);
@@ -582,13 +571,12 @@ __global__ void __launch_bounds__(NT) k_bwd_dkv(SegArgs a) {
         __syncthreads();
 
         // A^T and dA^T on the causal tiles: P[t][s] = sum X[t][ch] Y[s][ch]
-        for (int i = w; i < 20; i += 4) {
+        for (int i = w; i < 20; i += NW) {
             const bool isdA = i >= 10;
             int tt, st;
             tri_tile(isdA ? i - 10 : i, tt, st);
             const T *X = isdA ? sO : sQ;
             const T *Yt = isdA ? sV : sK;
-            T *dst = isdA ? sdAT : sAT;
             f32x4 p = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks)
@@ -601,134 +589,124 @@ __global__ void __launch_bounds__(NT) k_bwd_dkv(SegArgs a) {
                 const int t = 16 * tt + 4 * q4 + r;
                 v4[r] = s <= t ? p[r] * exp2f(sb[t] - bs) : 0.f;
             }
-            st4(&dst[s * LDT + 16 * tt + 4 * q4], v4[0], v4[1], v4[2], v4[3]);
+            const int o = s * LDT + 16 * tt + 4 * q4;
+            if (isdA) st4_split<T>(&sdAT[o], &sdATl[SP ? o : 0], v4);
+            else st4_split<T>(&sAT[o], &sATl[SP ? o : 0], v4);
         }
         __syncthreads();
 
         const int64_t crow = (int64_t)c * C;
-        // dv^T[v][s], v in this wave's columns
+        // dv^T[v][s] for v in tile w
         {
-            f32x4 DV[NV][4];
+            f32x4 DV[4];
 #pragma unroll
-            for (int j = 0; j < NV; ++j)
-#pragma unroll
-                for (int st = 0; st < 4; ++st) DV[j][st] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int st = 0; st < 4; ++st) DV[st] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks) {
-                frag_t<T> fs[NV];
+                frag_t<T> fh, fl;
+                split_acc<T>(G[2 * ks], G[2 * ks + 1], fh, fl);
 #pragma unroll
-                for (int j = 0; j < NV; ++j) fs[j] = frag_from_acc<T>(G[2 * ks][j], G[2 * ks + 1][j]);
-#pragma unroll
-                for (int st = 0; st < 4; ++st) {
-                    const frag_t<T> fb = ldfrag_perm(sK, LDN, 16 * st, 32 * ks, lane);
-#pragma unroll
-                    for (int j = 0; j < NV; ++j) mma(DV[j][st], fs[j], fb);
-                }
+                for (int st = 0; st < 4; ++st) mma2<T>(DV[st], fh, fl, ldfrag(sK, LDN, 16 * st, 32 * ks, lane));
             }
 #pragma unroll
-            for (int st = 0; st < 4; ++st) {
-                const float f = exp2f(b63 - sb[16 * st + n16]);
-#pragma unroll
-                for (int j = 0; j < NV; ++j) DV[j][st] *= f;
-            }
+            for (int st = 0; st < 4; ++st) DV[st] *= exp2f(b63 - sb[16 * st + n16]);
 #pragma unroll
             for (int st = 0; st < 4; ++st)
 #pragma unroll
                 for (int ks = st / 2; ks < C / 32; ++ks) {
-                    const frag_t<T> fb = ldfrag(sAT, LDT, 16 * st, 32 * ks, lane);
-#pragma unroll
-                    for (int j = 0; j < NV; ++j)
-                        mma(DV[j][st], ldfragT(sOT, LDT, c0 + 16 * j, 32 * ks, lane), fb);
+                    const frag_t<T> fa = ldfragT(sOT, LDT, c0, 32 * ks, lane);
+                    mma(DV[st], fa, ldfrag(sAT, LDT, 16 * st, 32 * ks, lane));
+                    if constexpr (SP) mma(DV[st], fa, ldfrag(sATl, LDT, 16 * st, 32 * ks, lane));
                 }
 #pragma unroll
             for (int st = 0; st < 4; ++st)
-#pragma unroll
-                for (int j = 0; j < NV; ++j)
-                    st4(dV + (crow + 16 * st + n16) * a.sx_l + c0 + 16 * j + 4 * q4, DV[j][st][0],
-                        DV[j][st][1], DV[j][st][2], DV[j][st][3]);
+                st4(dV + (crow + 16 * st + n16) * a.sx_l + c0 + 4 * q4, DV[st][0], DV[st][1], DV[st][2], DV[st][3]);
         }
-        // dk^T[k][s], k in this wave's rows; k.dk partials
+        // dk^T[k][s] for k in tile w; k.dk partials
         {
-            f32x4 DK[NV][4];
+            f32x4 DK[4];
 #pragma unroll
-            for (int j = 0; j < NV; ++j)
-#pragma unroll
-                for (int st = 0; st < 4; ++st) DK[j][st] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int st = 0; st < 4; ++st) DK[st] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks) {
-                frag_t<T> fa[NV];
+                frag_t<T> fh, fl;
+                split_acc<T>(GT[2 * ks], GT[2 * ks + 1], fh, fl);
 #pragma unroll
-                for (int j = 0; j < NV; ++j) fa[j] = ldfrag(sG, LDN, c0 + 16 * j, 32 * ks, lane);
-#pragma unroll
-                for (int st = 0; st < 4; ++st) {
-                    const frag_t<T> fb = ldfrag(sV, LDN, 16 * st, 32 * ks, lane);
-#pragma unroll
-                    for (int j = 0; j < NV; ++j) mma(DK[j][st], fa[j], fb);
-                }
+                for (int st = 0; st < 4; ++st) mma2<T>(DK[st], fh, fl, ldfrag(sV, LDN, 16 * st, 32 * ks, lane));
             }
 #pragma unroll
-            for (int st = 0; st < 4; ++st) {
-                const float f = exp2f(b63 - sb[16 * st + n16]);
-#pragma unroll
-                for (int j = 0; j < NV; ++j) DK[j][st] *= f;
-            }
+            for (int st = 0; st < 4; ++st) DK[st] *= exp2f(b63 - sb[16 * st + n16]);
 #pragma unroll
             for (int st = 0; st < 4; ++st)
 #pragma unroll
                 for (int ks = st / 2; ks < C / 32; ++ks) {
-                    const frag_t<T> fb = ldfrag(sdAT, LDT, 16 * st, 32 * ks, lane);
-#pragma unroll
-                    for (int j = 0; j < NV; ++j)
-                        mma(DK[j][st], ldfragT(sQT, LDT, c0 + 16 * j, 32 * ks, lane), fb);
+                    const frag_t<T> fa = ldfragT(sQT, LDT, c0, 32 * ks, lane);
+                    mma(DK[st], fa, ldfrag(sdAT, LDT, 16 * st, 32 * ks, lane));
+                    if constexpr (SP) mma(DK[st], fa, ldfrag(sdATl, LDT, 16 * st, 32 * ks, lane));
                 }
 #pragma unroll
             for (int st = 0; st < 4; ++st) {
                 const int s = 16 * st + n16;
-                float part = 0.f;
-#pragma unroll
-                for (int j = 0; j < NV; ++j) {
-                    const int col = c0 + 16 * j + 4 * q4;
-                    st4(dK + (crow + s) * a.sx_l + col, DK[j][st][0], DK[j][st][1], DK[j][st][2],
-                        DK[j][st][3]);
-                    const f32x4 kv = ld4f(&sK[s * LDN + col]);
-                    part += DK[j][st][0] * kv[0] + DK[j][st][1] * kv[1] + DK[j][st][2] * kv[2] +
-                            DK[j][st][3] * kv[3];
-                }
+                const int col = c0 + 4 * q4;
+                st4(dK + (crow + s) * a.sx_l + col, DK[st][0], DK[st][1], DK[st][2], DK[st][3]);
+                const f32x4 kv = ld4f(&sK[s * LDN + nat_pos(col)]);
+                float part = DK[st][0] * kv[0] + DK[st][1] * kv[1] + DK[st][2] * kv[2] + DK[st][3] * kv[3];
                 part += __shfl_xor(part, 16, 64);
                 part += __shfl_xor(part, 32, 64);
                 if (q4 == 0) sred[w * C + s] = part;
             }
         }
-        // G <- exp(b_63) G + (Q o exp(b))^T dO
+        __syncthreads();  // dv/dk done with the score tiles; k.dk partials complete
+        if (w == 0) {
+            float kd = 0.f;
+#pragma unroll
+            for (int ww = 0; ww < NW; ++ww) kd += sred[ww * C + lane];
+            const float suf = wave_incl_suffix(rc - kd, lane);
+            dgp[(crow + lane) * a.sg_l] = carry + suf;
+            carry += __shfl(suf, 0, 64);
+        }
+        // (Q o exp(b))^T as hi/lo into the scratch, same swizzled layout as sQT
         {
-            const float gam = exp2f(b63);
+            constexpr int TPB = 16 / (int)sizeof(T), NB = C / TPB;
+            typedef T vecB __attribute__((ext_vector_type(TPB)));
+            for (int blk = tid; blk < D * NB; blk += NT) {
+                const int row = blk / NB, pb = blk % NB;
+                const int t0 = (pb ^ ((row >> 4) & (NB - 1))) * TPB;
+                const int o = row * LDT + pb * TPB;
+                const vecB x = *reinterpret_cast<const vecB *>(&sQT[o]);
+                vecB hi, lo;
 #pragma unroll
-            for (int i = 0; i < NK; ++i)
-#pragma unroll
-                for (int j = 0; j < NV; ++j) G[i][j] *= gam;
-#pragma unroll
-            for (int ks = 0; ks < C / 32; ++ks) {
-                float qs[8];
-#pragma unroll
-                for (int jj = 0; jj < 8; ++jj) qs[jj] = exp2f(sb[32 * ks + 8 * q4 + jj]);
-                frag_t<T> fb[NV];
-#pragma unroll
-                for (int j = 0; j < NV; ++j) fb[j] = ldfragT(sOT, LDT, c0 + 16 * j, 32 * ks, lane);
-#pragma unroll
-                for (int i = 0; i < NK; ++i) {
-                    const frag_t<T> fa = scale_frag<T>(ldfragT(sQT, LDT, 16 * i, 32 * ks, lane), qs);
-#pragma unroll
-                    for (int j = 0; j < NV; ++j) mma(G[i][j], fa, fb[j]);
+                for (int j = 0; j < TPB; ++j) {
+                    const float v = tof<T>(x[j]) * exp2f(sb[t0 + j]);
+                    hi[j] = cvt<T>(v);
+                    lo[j] = cvt<T>(v - tof<T>(hi[j]));
                 }
+                *reinterpret_cast<vecB *>(&sQs[o]) = hi;
+                if constexpr (SP) *reinterpret_cast<vecB *>(&sQsl[o]) = lo;
             }
         }
         __syncthreads();
-        if (w == 0) {
-            float *dgt = dgp + (crow + lane) * a.sg_l;
-            const float ell = rc - (sred[lane] + sred[C + lane] + sred[2 * C + lane] + sred[3 * C + lane]);
-            const float suf = wave_incl_suffix(ell, lane);
-            *dgt = carry + suf;
-            carry += __shfl(suf, 0, 64);
+        // G <- exp(b_63) G + (Q o exp(b))^T dO, and the same for G^T
+        {
+            const float gam = exp2f(b63);
+#pragma unroll
+            for (int i = 0; i < NK; ++i) {
+                G[i] *= gam;
+                GT[i] *= gam;
+            }
+#pragma unroll
+            for (int ks = 0; ks < C / 32; ++ks) {
+                const frag_t<T> fo = ldfragT(sOT, LDT, c0, 32 * ks, lane);
+#pragma unroll
+                for (int i = 0; i < NK; ++i) {
+                    mma(G[i], ldfragT(sQs, LDT, 16 * i, 32 * ks, lane), fo);
+                    if constexpr (SP) mma(G[i], ldfragT(sQsl, LDT, 16 * i, 32 * ks, lane), fo);
+                }
+                const frag_t<T> qh = ldfragT(sQs, LDT, c0, 32 * ks, lane);
+                const frag_t<T> ql = ldfragT(sQsl, LDT, SP ? c0 : 0, SP ? 32 * ks : 0, lane);
+#pragma unroll
+                for (int i = 0; i < NK; ++i) mma2b<T>(GT[i], ldfragT(sOT, LDT, 16 * i, 32 * ks, lane), qh, ql);
+            }
         }
     }
     if (a.n_super == 1 && a.dS_in) {
@@ -736,16 +714,13 @@ __global__ void __launch_bounds__(NT) k_bwd_dkv(SegArgs a) {
 #pragma unroll
         for (int i = 0; i < NK; ++i)
 #pragma unroll
-            for (int j = 0; j < NV; ++j)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + 16 * j + n16] = G[i][j][r];
+            for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = G[i][r];
     }
 }
 
 // Boundary state of an empty segment: dst = src, or zero when src is NULL.
-__global__ void __launch_bounds__(NT) k_state_copy(const float *src, float *dst, int64_t n) {
-    const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+__global__ void __launch_bounds__(SCAN_NT) k_state_copy(const float *src, float *dst, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * SCAN_NT + threadIdx.x;
     if (i < n) dst[i] = src ? src[i] : 0.f;
 }
 
@@ -753,7 +728,7 @@ __global__ void __launch_bounds__(NT) k_state_copy(const float *src, float *dst,
 // launchers
 template <typename T, int D>
 static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s) {
-    const dim3 blk(NT);
+    const dim3 blk(Cfg<T, D>::NT);
     const dim3 grid((unsigned)((int64_t)a.B * a.H * a.n_super));
     switch (kind) {
     case SF_K_FWD_PREP: hipLaunchKernelGGL((k_prep<T, D, false>), grid, blk, 0, s, a); break;
@@ -769,8 +744,8 @@ static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s) {
 hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t s) {
     if (kind == SF_K_SCAN) {
         const dim3 grid((unsigned)((int64_t)a.B * a.H * (D * D / 1024)));
-        if (a.dS_in || a.wsE) hipLaunchKernelGGL((k_scan<true>), grid, dim3(NT), 0, s, a, D);
-        else hipLaunchKernelGGL((k_scan<false>), grid, dim3(NT), 0, s, a, D);
+        if (a.wsE) hipLaunchKernelGGL((k_scan<true>), grid, dim3(SCAN_NT), 0, s, a, D);
+        else hipLaunchKernelGGL((k_scan<false>), grid, dim3(SCAN_NT), 0, s, a, D);
         return hipGetLastError();
     }
     if (io == SF_BF16 && D == 128) return launch_td<__bf16, 128>(kind, a, s);
@@ -781,7 +756,8 @@ hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t 
 
 hipError_t launch_state_copy(const float *src, float *dst, int64_t n, hipStream_t s) {
     if (n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_state_copy, dim3((unsigned)((n + NT - 1) / NT)), dim3(NT), 0, s, src, dst, n);
+    hipLaunchKernelGGL(k_state_copy, dim3((unsigned)((n + SCAN_NT - 1) / SCAN_NT)), dim3(SCAN_NT), 0, s, src, dst,
+                       n);
     return hipGetLastError();
 }
 
