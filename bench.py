@@ -116,6 +116,8 @@ def main():
     ap.add_argument("--no-overlap", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-times", action="store_true", help="print per-kernel times to stderr")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after timing, run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the recurrence shards over "
@@ -169,6 +171,14 @@ def main():
         sf.prof_enable(kname, False)
         ktime[kname] = sf.prof_read(kname)
     ms = (t1 - t0) * 1e3 / args.steps
+    if args.copy_mib > 0:  # known-size copy: FETCH_SIZE / WRITE_SIZE calibration under rocprofv3 --pmc
+        n = args.copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     tokens = B * L
     value = tokens / (ms / 1e3)
 
