@@ -15,6 +15,7 @@
 // Pre(1) -> (ST(1) || Pre(2)) -> (ST(2) || Out(1)) -> Out(2) applied across
 // consecutive segments; the backward mirrors it in reverse segment order.
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <mutex>
@@ -172,21 +173,60 @@ sf_status check_align(std::initializer_list<std::pair<const void *, const char *
 constexpr size_t ALIGN = 256;
 size_t al(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
+// Compute units of the current device (256 on MI355X; also the fallback when no
+// device is visible, e.g. for workspace queries on a host without a GPU).
+int device_cus() {
+    static thread_local int cached_dev = -2, cached_cus = 256;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return 256;
+    }
+    if (dev != cached_dev) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+            (void)hipGetLastError();
+            n = 256;
+        }
+        cached_dev = dev;
+        cached_cus = n;
+    }
+    return cached_cus;
+}
+
 sf_status pick_ts(const Shape &r, int64_t L, const sf_tuning *t, int &ts) {
     if (t && t->ts != 0) {
         if (t->ts < 64 || t->ts % 64) return fail(SF_E_SHAPE, "tuning.ts must be a positive multiple of 64");
         ts = t->ts;
         return SF_OK;
     }
-    // Largest power-of-two multiple of 64 (<= 2048) that still gives at least
-    // 512 workgroups (two per CU on 256 CUs) to the dense kernels.
+    // Superchunks of one head run one after another inside a workgroup, and the
+    // workgroups of a launch run in rounds of `slots` (two per CU).  Choose the
+    // superchunk length (a multiple of 64) that minimises
+    //   rounds * chunks_per_superchunk + kState * superchunks,
+    // the walk time in chunk steps plus the cost of materialising, scanning and
+    // re-reading one more boundary state per superchunk (about 0.006 chunk
+    // steps per state at d = 128).
     const int64_t bh = (int64_t)r.B * r.H;
-    ts = 64;
-    for (int cand = 2048; cand >= 64; cand /= 2)
-        if (bh * ((L + cand - 1) / cand) >= 512) {
-            ts = cand;
-            break;
+    const int64_t nc = (L + 63) / 64;
+    if (nc <= 1) {
+        ts = (int)std::max<int64_t>(64, std::min<int64_t>(L, 1 << 30));
+        return SF_OK;
+    }
+    const double slots = 2.0 * device_cus(), kState = 0.006 * (double)r.D * r.D / (128.0 * 128.0);
+    double best = 1e300;
+    int64_t best_m = nc;
+    for (int64_t m = 1; m <= nc; ++m) {  // chunks per superchunk
+        const int64_t ns = (nc + m - 1) / m;
+        if (m > 1 && (nc + m - 2) / (m - 1) == ns) continue;  // same split as a shorter m
+        const double rounds = std::ceil((double)(bh * ns) / slots);
+        const double cost = rounds * (double)m + kState * (double)(bh * ns);
+        if (cost < best - 1e-9) {
+            best = cost;
+            best_m = m;
         }
+    }
+    ts = (int)std::min<int64_t>(best_m * 64, 1 << 30);
     if (ts >= L && L > 0) ts = (int)std::min<int64_t>(L, 1 << 30);
     return SF_OK;
 }

@@ -222,6 +222,16 @@ struct Tile {
             for (int j = 0; j < RPT; ++j) *reinterpret_cast<vecE *>(p + j * ld + p0) = r[j];
         }
     }
+    // natural layout [token][channel] in plain channel order, rows with bit 3 set
+    // XOR-swizzled by swx channels (see swz_col)
+    __device__ __forceinline__ void store_swz(T *lds, int ld, int tid, int swx) const {
+        const int ch = cb(tid) * E, r0 = row0(tid);
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            const int row = r0 + j;
+            *reinterpret_cast<vecE *>(lds + row * ld + (ch ^ (((row >> 3) & 1) * swx))) = r[j];
+        }
+    }
     // swizzled transposed layout [channel][token] (see tswz), token j scaled by s[j]
     __device__ __forceinline__ void store_T(T *lds, int ldt, int tid, const float *s) const {
         const int c0 = cb(tid) * E, t0 = row0(tid);
@@ -278,6 +288,88 @@ struct Tile {
         }
     }
 };
+
+// ---------------------------------------------------------------------------
+// Natural tiles read through transposing loads.
+//
+// A natural tile M[token][channel] (row pitch ld) can serve as an MFMA operand
+// whose rows are channels and whose contraction runs over tokens: on gfx950,
+// ds_read_b64_tr_b16 lets each group of 16 lanes exchange 4x4 blocks of 16-bit
+// elements while reading.  Measured lane map: within a 16-lane group, lane i
+// receives element (i % 4) of the 8-byte words addressed by lanes 4m + i/4,
+// m = 0..3.  The 32-lane halves of the instruction are served together, so the
+// two 16-lane groups of a half (tokens 8q.., 8(q+1)..) must hit different banks:
+// rows with bit 3 set are stored with their channel index XORed by swx (128
+// bytes; 64 for 128-byte rows), which made the pattern conflict-free
+// (SQ_LDS_BANK_CONFLICT = 0 at a 288-byte pitch).
+template <typename T, int D>
+constexpr int swx() { return (D * (int)sizeof(T) >= 256 ? 128 : 64) / (int)sizeof(T); }
+__device__ __forceinline__ int swz_col(int row, int col, int swx) { return col ^ (((row >> 3) & 1) * swx); }
+
+// Lane (q = l/16, n = l%16) receives M[k0 + 8q + j][c0 + n], j = 0..7: an operand
+// fragment with rows = channels c0..c0+15 and contraction = tokens k0..k0+31.
+// c0 must be a multiple of 4 (bf16) / any (fp32, read element by element).
+template <typename T, int LD, int SWX>
+__device__ __forceinline__ frag_t<T> ldfragTR(const T *M, int k0, int c0, int lane) {
+    const int q = lane >> 4, a = lane & 15;
+    if constexpr (sizeof(T) == 2) {
+        typedef short s4 __attribute__((ext_vector_type(4)));
+        const int col = c0 + 4 * (a & 3);
+        const int r0 = k0 + 8 * q + (a >> 2), r1 = r0 + 4;
+        const s4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s4 *)(M + r0 * LD + swz_col(r0, col, SWX)));
+        const s4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s4 *)(M + r1 * LD + swz_col(r1, col, SWX)));
+        const s4 lo = x0, hi = x1;
+        typedef short s8 __attribute__((ext_vector_type(8)));
+        const s8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        return __builtin_bit_cast(frag_t<T>, v);
+    } else {
+        frag_t<T> f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int row = k0 + 8 * q + j;
+            f[j] = M[row * LD + swz_col(row, c0 + a, SWX)];
+        }
+        return f;
+    }
+}
+// ldfrag() on a swizzled natural tile (rows row0.., channels k0 + 8q .. +7).
+template <typename T, int LD, int SWX>
+__device__ __forceinline__ frag_t<T> ldfrag_swz(const T *M, int row0, int k0, int lane) {
+    const int r = row0 + (lane & 15);
+    return *reinterpret_cast<const frag_t<T> *>(M + r * LD + swz_col(r, k0 + 8 * (lane >> 4), SWX));
+}
+// Fragment in plain channel order (channels k0 + 8q .. +7) from a tile stored
+// in nat_pos order: the 8 channels sit in two 4-channel runs 8 apart.
+template <typename T>
+__device__ __forceinline__ frag_t<T> ldfrag_unperm(const T *M, int ld, int row0, int k0, int lane) {
+    const int q = lane >> 4;
+    const T *p = M + (row0 + (lane & 15)) * ld + k0 + 16 * (q & 1) + 4 * (q >> 1);
+    typedef T h4 __attribute__((ext_vector_type(4)));
+    const h4 lo = *reinterpret_cast<const h4 *>(p);
+    const h4 hi = *reinterpret_cast<const h4 *>(p + 8);
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave with DPP row shifts and row
+// broadcasts (no LDS round trips); lanes without a source add 0.
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ float dpp_or0(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROWS, 0xf, true));
+}
+__device__ __forceinline__ float wave_scan_dpp(float x) {
+    x += dpp_or0<0x111>(x);       // row_shr:1
+    x += dpp_or0<0x112>(x);       // row_shr:2
+    x += dpp_or0<0x114>(x);       // row_shr:4
+    x += dpp_or0<0x118>(x);       // row_shr:8
+    x += dpp_or0<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
+    x += dpp_or0<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
+    return x;
+}
+__device__ __forceinline__ float lane_value(float x, int l) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), l));
+}
 
 // Inclusive prefix sum over the 64 lanes of a wave.
 __device__ __forceinline__ float wave_incl_scan(float x, int lane) {

@@ -39,6 +39,24 @@ struct Cfg {
 };
 constexpr int SCAN_NT = 256;
 
+// state column tiles per wave of the prep kernels (forward, backward) and of
+// the chunk walkers: 2 gives D/32 waves per workgroup, twice the reuse of every
+// shared operand fragment and workgroups small enough for two per CU
+#ifndef SF_NCT_PREP
+#define SF_NCT_PREP 2
+#endif
+#ifndef SF_NCT_PREPB
+#define SF_NCT_PREPB 1
+#endif
+#ifndef SF_NCT_WALK
+#define SF_NCT_WALK 2
+#endif
+
+// 2^x with the hardware v_exp_f32 (results below 2^-126 flush to zero, which
+// is what a decay that small means here; no input is ever > 0 except on
+// masked-out causal entries, which are discarded by a select)
+__device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // (t-tile, s-tile) pairs of the causal 64x64 score matrix, s-tile <= t-tile.
 __device__ __forceinline__ void tri_tile(int i, int &tt, int &st) {
     // 0:(0,0) 1:(1,0) 2:(1,1) 3:(2,0) 4:(2,1) 5:(2,2) 6:(3,0) 7:(3,1) 8:(3,2) 9:(3,3)
@@ -65,20 +83,22 @@ __device__ __forceinline__ Decode decode(const SegArgs &a) {
 // ---------------------------------------------------------------------------
 // Pre: per superchunk, D_J = sum_c (decay after c) (K~_c)^T V_c, and for the
 // backward E_J = sum_t exp(B_t) q_t dO_t^T (B superchunk-local, inclusive).
-template <typename T, int D, bool BWD>
-__global__ void __launch_bounds__(4 * D) k_prep(SegArgs a) {
-    using F = Cfg<T, D>;
-    constexpr int LDT = F::LDT, NK = F::NK, NT = F::NT;
-    constexpr bool SP = F::SP;
-    __shared__ __attribute__((aligned(16))) T sKT[D * LDT];
-    __shared__ __attribute__((aligned(16))) T sKTl[SP ? D * LDT : 8];
-    __shared__ __attribute__((aligned(16))) T sVT[D * LDT];
-    __shared__ __attribute__((aligned(16))) T sQT[BWD ? D * LDT : 8];
-    __shared__ __attribute__((aligned(16))) T sQTl[BWD && SP ? D * LDT : 8];
-    __shared__ __attribute__((aligned(16))) T sOT[BWD ? D * LDT : 8];
+// Wave w owns NCT state column tiles.  The key (query) tile is read through
+// transposing loads as the exact shared operand; the per-token decay goes on
+// the wave's own value (dO) columns, split hi/lo:
+//   D[k][col] = gam D[k][col] + sum_s K[s][k] (exp2(b63 - b_s) V[s][col])
+template <typename T, int D, int NCT, bool BWD>
+__global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_prep(SegArgs a) {
+    constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
+    constexpr int LDN = D + pad<T>(), SWX = swx<T, D>();
+    __shared__ __attribute__((aligned(16))) T sK[C * LDN];
+    __shared__ __attribute__((aligned(16))) T sV[C * LDN];
+    __shared__ __attribute__((aligned(16))) T sQ[BWD ? C * LDN : 8];
+    __shared__ __attribute__((aligned(16))) T sO[BWD ? C * LDN : 8];
+    __shared__ __attribute__((aligned(16))) float se[C];   // exp2(b63 - b_s)
+    __shared__ __attribute__((aligned(16))) float sqs[BWD ? C : 4];  // exp2(off + b_t)
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
-    const int c0 = 16 * w;
     const Decode d = decode(a);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *K = (const T *)a.k + xo;
@@ -87,71 +107,80 @@ __global__ void __launch_bounds__(4 * D) k_prep(SegArgs a) {
     const T *dO = (const T *)a.dO + xo;
     const float *gp = a.g + d.b * a.sg_b + d.h * a.sg_h + d.tok0 * a.sg_l;
 
-    f32x4 Ds[NK], Es[BWD ? NK : 1];
+    f32x4 Ds[NCT][NK], Es[BWD ? NCT : 1][NK];
 #pragma unroll
-    for (int i = 0; i < NK; ++i) {
-        Ds[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if constexpr (BWD) Es[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+        for (int i = 0; i < NK; ++i) {
+            Ds[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if constexpr (BWD) Es[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
 
     Tile<T, D, NT> tk, tv, tq, to;
-    tk.load(K, a.sx_l, tid);
-    tv.load(V, a.sx_l, tid);
-    if constexpr (BWD) {
-        tq.load(Q, a.sx_l, tid);
-        to.load(dO, a.sx_l, tid);
-    }
-    float gl = gp[lane * a.sg_l];
+    float gl;
+    auto issue = [&](int c) {
+        const int64_t nx = (int64_t)c * C * a.sx_l;
+        tk.load(K + nx, a.sx_l, tid);
+        tv.load(V + nx, a.sx_l, tid);
+        if constexpr (BWD) {
+            tq.load(Q + nx, a.sx_l, tid);
+            to.load(dO + nx, a.sx_l, tid);
+        }
+        gl = gp[(c * C + lane) * a.sg_l];
+    };
+    issue(0);
     float off = 0.f;  // log2 decay of the superchunk's earlier chunks
 
     for (int c = 0; c < d.nch; ++c) {
-        const float b2 = wave_incl_scan(gl * LOG2E, lane);
-        const float b63 = __shfl(b2, 63, 64);
+        const float b2 = wave_scan_dpp(gl * LOG2E);
+        const float b63 = lane_value(b2, 63);
         __syncthreads();
-        {
-            constexpr int R = Tile<T, D, NT>::RPT;
-            float ks[R], qs[R];
-#pragma unroll
-            for (int j = 0; j < R; ++j) {
-                const float bj = __shfl(b2, tk.row0(tid) + j, 64);
-                ks[j] = exp2f(b63 - bj);
-                qs[j] = exp2f(off + bj);
-            }
-            tk.store_T2(sKT, sKTl, LDT, tid, ks);
-            tv.store_T1(sVT, LDT, tid);
-            if constexpr (BWD) {
-                tq.store_T2(sQT, sQTl, LDT, tid, qs);
-                to.store_T1(sOT, LDT, tid);
-            }
+        if (w == 0) {
+            se[lane] = fexp2(b63 - b2);
+            if constexpr (BWD) sqs[lane] = fexp2(off + b2);
         }
-        if (c + 1 < d.nch) {
-            const int64_t nx = (int64_t)(c + 1) * C * a.sx_l;
-            tk.load(K + nx, a.sx_l, tid);
-            tv.load(V + nx, a.sx_l, tid);
-            if constexpr (BWD) {
-                tq.load(Q + nx, a.sx_l, tid);
-                to.load(dO + nx, a.sx_l, tid);
-            }
-            gl = gp[((c + 1) * C + lane) * a.sg_l];
+        tk.store_swz(sK, LDN, tid, SWX);
+        tv.store_swz(sV, LDN, tid, SWX);
+        if constexpr (BWD) {
+            tq.store_swz(sQ, LDN, tid, SWX);
+            to.store_swz(sO, LDN, tid, SWX);
         }
+        if (c + 1 < d.nch) issue(c + 1);
         __syncthreads();
-        const float gam = exp2f(b63);
+        const float gam = fexp2(b63);
 #pragma unroll
-        for (int i = 0; i < NK; ++i) Ds[i] *= gam;
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int i = 0; i < NK; ++i) Ds[ct][i] *= gam;
 #pragma unroll
         for (int ks = 0; ks < C / 32; ++ks) {
-            const frag_t<T> fv = ldfragT(sVT, LDT, c0, 32 * ks, lane);
+            const int s0 = 32 * ks + 8 * q4;
+            const f32x4 e0 = *reinterpret_cast<const f32x4 *>(&se[s0]);
+            const f32x4 e1 = *reinterpret_cast<const f32x4 *>(&se[s0 + 4]);
+            const float ev[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
+            frag_t<T> vh[NCT], vl[NCT], oh[BWD ? NCT : 1], ol[BWD ? NCT : 1];
+            float qv[8];
+            if constexpr (BWD) {
+                const f32x4 u0 = *reinterpret_cast<const f32x4 *>(&sqs[s0]);
+                const f32x4 u1 = *reinterpret_cast<const f32x4 *>(&sqs[s0 + 4]);
+                qv[0] = u0[0]; qv[1] = u0[1]; qv[2] = u0[2]; qv[3] = u0[3];
+                qv[4] = u1[0]; qv[5] = u1[1]; qv[6] = u1[2]; qv[7] = u1[3];
+            }
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) {
+                const int c0 = 16 * (NCT * w + ct);
+                split_scaled<T>(ldfragTR<T, LDN, SWX>(sV, 32 * ks, c0, lane), ev, vh[ct], vl[ct]);
+                if constexpr (BWD) split_scaled<T>(ldfragTR<T, LDN, SWX>(sO, 32 * ks, c0, lane), qv, oh[ct], ol[ct]);
+            }
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
-                mma(Ds[i], ldfragT(sKT, LDT, 16 * i, 32 * ks, lane), fv);
-                if constexpr (SP) mma(Ds[i], ldfragT(sKTl, LDT, 16 * i, 32 * ks, lane), fv);
-            }
-            if constexpr (BWD) {
-                const frag_t<T> fo = ldfragT(sOT, LDT, c0, 32 * ks, lane);
+                const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sK, 32 * ks, 16 * i, lane);
 #pragma unroll
-                for (int i = 0; i < NK; ++i) {
-                    mma(Es[i], ldfragT(sQT, LDT, 16 * i, 32 * ks, lane), fo);
-                    if constexpr (SP) mma(Es[i], ldfragT(sQTl, LDT, 16 * i, 32 * ks, lane), fo);
+                for (int ct = 0; ct < NCT; ++ct) mma2b<T>(Ds[ct][i], kf, vh[ct], vl[ct]);
+                if constexpr (BWD) {
+                    const frag_t<T> qf = ldfragTR<T, LDN, SWX>(sQ, 32 * ks, 16 * i, lane);
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct) mma2b<T>(Es[ct][i], qf, oh[ct], ol[ct]);
                 }
             }
         }
@@ -159,13 +188,17 @@ __global__ void __launch_bounds__(4 * D) k_prep(SegArgs a) {
     }
     const int64_t so = ((int64_t)d.bh * a.n_super + d.J) * D * D;
 #pragma unroll
-    for (int i = 0; i < NK; ++i)
+    for (int ct = 0; ct < NCT; ++ct) {
+        const int c0 = 16 * (NCT * w + ct);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int64_t e = so + (int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16;
-            a.wsS[e] = Ds[i][r];
-            if constexpr (BWD) a.wsE[e] = Es[i][r];
-        }
+        for (int i = 0; i < NK; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t e = so + (int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16;
+                a.wsS[e] = Ds[ct][i][r];
+                if constexpr (BWD) a.wsE[e] = Es[ct][i][r];
+            }
+    }
     if (tid == 0) a.wsLg[(int64_t)d.bh * a.n_super + d.J] = off;
 }
 
@@ -195,7 +228,7 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
         for (int u = 0; u < 4; ++u)
             if (J + u < n) {
                 dd[u] = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)(J + u) * SS);
-                f[u] = exp2f(lg[J + u]);
+                f[u] = fexp2(lg[J + u]);
             }
 #pragma unroll
         for (int u = 0; u < 4; ++u)
@@ -215,7 +248,7 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
         for (int J = n - 1; J >= 0; --J) {
             const f32x4 E = *reinterpret_cast<const f32x4 *>(Eb + (int64_t)J * SS);
             const f32x4 Sj = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)J * SS);
-            const float f = exp2f(lg[J]);
+            const float f = fexp2(lg[J]);
             float p = G[0] * Sn[0] + G[1] * Sn[1] + G[2] * Sn[2] + G[3] * Sn[3];
             p = wave_sum(p);
             if (lane == 0) a.wsDot[(bh * n + J) * ndot + part * 4 + w] = p;
@@ -232,28 +265,30 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
 //   DQ == false (Out):  X1 = q, X2 = k, X3 = v, state S[k][v];   writes o.
 //   DQ == true  (OG):   X1 = dO, X2 = v, X3 = k, state S^T[v][k]; writes dq
 //                       and r_t = q_t . dq_t into dg (read back by k_bwd_dkv).
-// The state lives as MFMA accumulators: wave w owns state column tile w; row
-// tile kt of lane l holds rows 16kt+4*(l/16)+r of column 16w+l%16, which is an
-// A-operand fragment of the transposed state (split_acc), so Q S needs no LDS
-// round trip for S.
-template <typename T, int D, bool DQ>
-__global__ void __launch_bounds__(4 * D) k_walk(SegArgs a) {
-    using F = Cfg<T, D>;
-    constexpr int LDN = F::LDN, LDT = F::LDT, NK = F::NK, NW = F::NW, NT = F::NT;
-    constexpr bool SP = F::SP;
-    constexpr int R = Tile<T, D, NT>::RPT;
+// Wave w owns NCT state column tiles.  The state lives as MFMA accumulators:
+// row tile i of lane l holds rows 16i+4*(l/16)+r of column c0+l%16, which is an
+// A-operand fragment of the transposed state (split_acc), so X1 S needs no LDS
+// round trip for S.  LDS holds the three input tiles in natural [token][channel]
+// layout only: X1 in nat_pos channel order (the order of an accumulator pair),
+// X2 and X3 plain and swizzled for the transposing loads that feed the state
+// update (X2^T, the exact shared operand) and the value side (X3^T, decayed per
+// token and split hi/lo in registers by the wave that owns those columns).
+template <typename T, int D, int NCT, bool DQ>
+__global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_walk(SegArgs a) {
+    constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
+    constexpr int LDN = D + pad<T>(), LDT = C + pad<T>(), SWX = swx<T, D>();
+    constexpr bool SP = kSplit<T>;
     __shared__ __attribute__((aligned(16))) T sX1[C * LDN];
     __shared__ __attribute__((aligned(16))) T sX2[C * LDN];
-    __shared__ __attribute__((aligned(16))) T sX2T[D * LDT];  // decayed: X2~^T (hi)
-    __shared__ __attribute__((aligned(16))) T sX2Tl[SP ? D * LDT : 8];
-    __shared__ __attribute__((aligned(16))) T sX3T[D * LDT];
+    __shared__ __attribute__((aligned(16))) T sX3[C * LDN];
     __shared__ __attribute__((aligned(16))) T sA[C * LDT];    // A[t][s] (hi)
     __shared__ __attribute__((aligned(16))) T sAl[SP ? C * LDT : 8];
-    __shared__ float sb[C];
+    __shared__ __attribute__((aligned(16))) float sb[C];   // b_t (log2, chunk-local)
+    __shared__ __attribute__((aligned(16))) float sq[C];   // exp2(b_t)
+    __shared__ __attribute__((aligned(16))) float se[C];   // exp2(b63 - b_t)
     __shared__ float sred[DQ ? NW * C : 1];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
-    const int c0 = 16 * w;
     const Decode d = decode(a);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *X1 = (const T *)(DQ ? a.dO : a.q) + xo;
@@ -266,22 +301,24 @@ __global__ void __launch_bounds__(4 * D) k_walk(SegArgs a) {
     float *dgp = a.dg + go;
     const int64_t SS = (int64_t)D * D;
 
-    // initial state S_J (column tile w)
+    // initial state S_J (column tiles NCT*w + ct)
     const float *src = a.n_super == 1 ? (a.S_in ? a.S_in + d.bh * SS : nullptr)
                                       : a.wsS + ((int64_t)d.bh * a.n_super + d.J) * SS;
-    f32x4 S[NK];
+    f32x4 S[NCT][NK];
 #pragma unroll
-    for (int i = 0; i < NK; ++i) {
-        const int col = c0 + n16, row = 16 * i + 4 * q4;
-        if (!src) {
-            S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        } else if constexpr (!DQ) {
+    for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) S[i][r] = src[(int64_t)(row + r) * D + col];
-        } else {
-            S[i] = *reinterpret_cast<const f32x4 *>(src + (int64_t)col * D + row);
+        for (int i = 0; i < NK; ++i) {
+            const int col = 16 * (NCT * w + ct) + n16, row = 16 * i + 4 * q4;
+            if (!src) {
+                S[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            } else if constexpr (!DQ) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) S[ct][i][r] = src[(int64_t)(row + r) * D + col];
+            } else {
+                S[ct][i] = *reinterpret_cast<const f32x4 *>(src + (int64_t)col * D + row);
+            }
         }
-    }
     // A tiles read by the A.V product but above the diagonal stay zero
     for (int e = tid; e < 512; e += NT) {
         const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
@@ -290,51 +327,49 @@ __global__ void __launch_bounds__(4 * D) k_walk(SegArgs a) {
         if constexpr (SP) sAl[idx] = cvt<T>(0.f);
     }
 
-    Tile<T, D, NT> t1, t2, t3;
-    t1.load(X1, a.sx_l, tid);
-    t2.load(X2, a.sx_l, tid);
-    t3.load(X3, a.sx_l, tid);
-    float gl = gp[lane * a.sg_l];
-    // DQ: q values of this lane's dq elements, one chunk ahead
     typedef T vec4T __attribute__((ext_vector_type(4)));
-    vec4T qn[DQ ? 4 : 1];
-    auto load_q = [&](int c) {
-        if constexpr (DQ) {
+    Tile<T, D, NT> t1, t2, t3;
+    float gl;
+    vec4T qn[DQ ? NCT * 4 : 1];  // DQ: q values of this lane's dq elements
+    auto issue = [&](int c) {
+        const int64_t nx = (int64_t)c * C * a.sx_l;
+        t1.load(X1 + nx, a.sx_l, tid);
+        t2.load(X2 + nx, a.sx_l, tid);
+        t3.load(X3 + nx, a.sx_l, tid);
+        gl = gp[(c * C + lane) * a.sg_l];
+    };
+    auto issue_q = [&](int c) {  // DQ: q at this lane's dq elements, read after chunk c-1's dot
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
-                qn[tt] = *reinterpret_cast<const vec4T *>(Qd + (int64_t)(c * C + 16 * tt + n16) * a.sx_l +
-                                                           c0 + 4 * q4);
-        }
+                qn[4 * ct + tt] = *reinterpret_cast<const vec4T *>(
+                    Qd + (int64_t)(c * C + 16 * tt + n16) * a.sx_l + 16 * (NCT * w + ct) + 4 * q4);
     };
-    load_q(0);
+    issue(0);
+    if constexpr (DQ) issue_q(0);
 
     for (int c = 0; c < d.nch; ++c) {
-        const float b2 = wave_incl_scan(gl * LOG2E, lane);
-        const float b63 = __shfl(b2, 63, 64);
-        vec4T qc[DQ ? 4 : 1];
-        if constexpr (DQ) {
-#pragma unroll
-            for (int tt = 0; tt < 4; ++tt) qc[tt] = qn[tt];
-        }
+        const float b2 = wave_scan_dpp(gl * LOG2E);
+        const float b63 = lane_value(b2, 63);
         __syncthreads();
-        if (w == 0) sb[lane] = b2;
-        {
-            float ks[R];
+        if constexpr (DQ) {  // q.dq of the previous chunk
+            if (w == 0 && c > 0) {
+                float r = 0.f;
 #pragma unroll
-            for (int j = 0; j < R; ++j) ks[j] = exp2f(b63 - __shfl(b2, t2.row0(tid) + j, 64));
-            t1.store_nat(sX1, LDN, tid);
-            t2.store_nat(sX2, LDN, tid);
-            t2.store_T2(sX2T, sX2Tl, LDT, tid, ks);
-            t3.store_T1(sX3T, LDT, tid);
+                for (int ww = 0; ww < NW; ++ww) r += sred[ww * C + lane];
+                dgp[(int64_t)((c - 1) * C + lane) * a.sg_l] = r;
+            }
         }
-        if (c + 1 < d.nch) {
-            const int64_t nx = (int64_t)(c + 1) * C * a.sx_l;
-            t1.load(X1 + nx, a.sx_l, tid);
-            t2.load(X2 + nx, a.sx_l, tid);
-            t3.load(X3 + nx, a.sx_l, tid);
-            gl = gp[((c + 1) * C + lane) * a.sg_l];
-            load_q(c + 1);
+        if (w == 0) {
+            sb[lane] = b2;
+            sq[lane] = fexp2(b2);
+            se[lane] = fexp2(b63 - b2);
         }
+        t1.store_nat(sX1, LDN, tid);
+        t2.store_swz(sX2, LDN, tid, SWX);
+        t3.store_swz(sX3, LDN, tid, SWX);
+        if (c + 1 < d.nch) issue(c + 1);
         __syncthreads();
 
         // scores P^T[s][t] = sum_ch X2[s][ch] X1[t][ch] on the causal tiles -> A[t][s]
@@ -344,56 +379,63 @@ __global__ void __launch_bounds__(4 * D) k_walk(SegArgs a) {
             f32x4 p = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks)
-                mma(p, ldfrag(sX2, LDN, 16 * st, 32 * ks, lane), ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane));
+                mma(p, ldfrag_swz<T, LDN, SWX>(sX2, 16 * st, 32 * ks, lane),
+                    ldfrag_unperm<T>(sX1, LDN, 16 * tt, 32 * ks, lane));
             const int t = 16 * tt + n16;
             const float bt = sb[t];
+            const f32x4 bs = *reinterpret_cast<const f32x4 *>(&sb[16 * st + 4 * q4]);
             float v4[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int s = 16 * st + 4 * q4 + r;
-                v4[r] = s <= t ? p[r] * exp2f(bt - sb[s]) : 0.f;
+                v4[r] = s <= t ? p[r] * fexp2(bt - bs[r]) : 0.f;
             }
             const int o = t * LDT + 16 * st + 4 * q4;
             st4_split<T>(&sA[o], &sAl[SP ? o : 0], v4);
         }
         __syncthreads();
 
-        // Y^T[col][t] = exp(b_t) sum_m S[m][col] X1[t][m] + sum_s X3[s][col] A[t][s]
-        f32x4 O[4];
-#pragma unroll
-        for (int tt = 0; tt < 4; ++tt) O[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < D / 32; ++ks) {
-            frag_t<T> fh, fl;
-            split_acc<T>(S[2 * ks], S[2 * ks + 1], fh, fl);
-#pragma unroll
-            for (int tt = 0; tt < 4; ++tt) mma2<T>(O[tt], fh, fl, ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane));
-        }
-#pragma unroll
-        for (int tt = 0; tt < 4; ++tt) O[tt] *= exp2f(sb[16 * tt + n16]);
-#pragma unroll
-        for (int ks = 0; ks < C / 32; ++ks) {
-            const frag_t<T> fa = ldfragT(sX3T, LDT, c0, 32 * ks, lane);
-#pragma unroll
-            for (int tt = 0; tt < 4; ++tt) {
-                if (32 * ks > 16 * tt + 15) continue;
-                mma(O[tt], fa, ldfrag(sA, LDT, 16 * tt, 32 * ks, lane));
-                if constexpr (SP) mma(O[tt], fa, ldfrag(sAl, LDT, 16 * tt, 32 * ks, lane));
-            }
-        }
+        // Y^T[col][t] = exp2(b_t) sum_m S[m][col] X1[t][m] + sum_s X3[s][col] A[t][s]
+        frag_t<T> vf[NCT][C / 32];
         float part[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int tt = 0; tt < 4; ++tt) {
-            const int64_t trow = (int64_t)(c * C + 16 * tt + n16) * a.sx_l;
-            const int col = c0 + 4 * q4;
-            st4(Y + trow + col, O[tt][0], O[tt][1], O[tt][2], O[tt][3]);
-            if constexpr (DQ) {
-                const vec4T qv = qc[tt];
-                part[tt] = O[tt][0] * tof<T>(qv[0]) + O[tt][1] * tof<T>(qv[1]) + O[tt][2] * tof<T>(qv[2]) +
-                           O[tt][3] * tof<T>(qv[3]);
+        for (int ct = 0; ct < NCT; ++ct) {
+            const int c0 = 16 * (NCT * w + ct);
+            f32x4 O[4];
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) O[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks) {
+                frag_t<T> fh, fl;
+                split_acc<T>(S[ct][2 * ks], S[ct][2 * ks + 1], fh, fl);
+#pragma unroll
+                for (int tt = 0; tt < 4; ++tt) mma2<T>(O[tt], fh, fl, ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane));
+            }
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) O[tt] *= sq[16 * tt + n16];
+#pragma unroll
+            for (int ks = 0; ks < C / 32; ++ks) {
+                vf[ct][ks] = ldfragTR<T, LDN, SWX>(sX3, 32 * ks, c0, lane);
+#pragma unroll
+                for (int tt = 0; tt < 4; ++tt) {
+                    if (32 * ks > 16 * tt + 15) continue;
+                    mma(O[tt], vf[ct][ks], ldfrag(sA, LDT, 16 * tt, 32 * ks, lane));
+                    if constexpr (SP) mma(O[tt], vf[ct][ks], ldfrag(sAl, LDT, 16 * tt, 32 * ks, lane));
+                }
+            }
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) {
+                const int64_t trow = (int64_t)(c * C + 16 * tt + n16) * a.sx_l;
+                st4(Y + trow + c0 + 4 * q4, O[tt][0], O[tt][1], O[tt][2], O[tt][3]);
+                if constexpr (DQ) {
+                    const vec4T qv = qn[4 * ct + tt];
+                    part[tt] += O[tt][0] * tof<T>(qv[0]) + O[tt][1] * tof<T>(qv[1]) + O[tt][2] * tof<T>(qv[2]) +
+                                O[tt][3] * tof<T>(qv[3]);
+                }
             }
         }
         if constexpr (DQ) {
+            if (c + 1 < d.nch) issue_q(c + 1);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
                 part[tt] += __shfl_xor(part[tt], 16, 64);
@@ -402,27 +444,36 @@ __global__ void __launch_bounds__(4 * D) k_walk(SegArgs a) {
             }
         }
 
-        // state update S = exp(b_63) S + X2~^T X3
-        const float gam = exp2f(b63);
+        // state update S = exp2(b63) S + X2^T (exp2(b63 - b) o X3)
+        const float gam = fexp2(b63);
 #pragma unroll
-        for (int i = 0; i < NK; ++i) S[i] *= gam;
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int i = 0; i < NK; ++i) S[ct][i] *= gam;
 #pragma unroll
         for (int ks = 0; ks < C / 32; ++ks) {
-            const frag_t<T> fb = ldfragT(sX3T, LDT, c0, 32 * ks, lane);
+            const int s0 = 32 * ks + 8 * q4;
+            const f32x4 e0 = *reinterpret_cast<const f32x4 *>(&se[s0]);
+            const f32x4 e1 = *reinterpret_cast<const f32x4 *>(&se[s0 + 4]);
+            const float ev[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
+            frag_t<T> vh[NCT], vl[NCT];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) split_scaled<T>(vf[ct][ks], ev, vh[ct], vl[ct]);
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
-                mma(S[i], ldfragT(sX2T, LDT, 16 * i, 32 * ks, lane), fb);
-                if constexpr (SP) mma(S[i], ldfragT(sX2Tl, LDT, 16 * i, 32 * ks, lane), fb);
+                const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sX2, 32 * ks, 16 * i, lane);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) mma2b<T>(S[ct][i], kf, vh[ct], vl[ct]);
             }
         }
-        if constexpr (DQ) {
-            __syncthreads();
-            if (w == 0) {
-                float r = 0.f;
+    }
+    if constexpr (DQ) {
+        __syncthreads();
+        if (w == 0 && d.nch > 0) {
+            float r = 0.f;
 #pragma unroll
-                for (int ww = 0; ww < NW; ++ww) r += sred[ww * C + lane];
-                dgp[(int64_t)(c * C + lane) * a.sg_l] = r;
-            }
+            for (int ww = 0; ww < NW; ++ww) r += sred[ww * C + lane];
+            dgp[(int64_t)((d.nch - 1) * C + lane) * a.sg_l] = r;
         }
     }
 
@@ -431,9 +482,12 @@ __global__ void __launch_bounds__(4 * D) k_walk(SegArgs a) {
             if (a.S_out) {
                 float *dst = a.S_out + d.bh * SS;
 #pragma unroll
-                for (int i = 0; i < NK; ++i)
+                for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = S[i][r];
+                    for (int i = 0; i < NK; ++i)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            dst[(int64_t)(16 * i + 4 * q4 + r) * D + 16 * (NCT * w + ct) + n16] = S[ct][i][r];
             }
         } else {
             // <dS_out, S_out> for dg (the state here is S_out^T)
@@ -441,11 +495,13 @@ __global__ void __launch_bounds__(4 * D) k_walk(SegArgs a) {
             if (a.dS_out) {
                 const float *ds = a.dS_out + d.bh * SS;
 #pragma unroll
-                for (int i = 0; i < NK; ++i) {
-                    const f32x4 x =
-                        *reinterpret_cast<const f32x4 *>(ds + (int64_t)(c0 + n16) * D + 16 * i + 4 * q4);
-                    p += x[0] * S[i][0] + x[1] * S[i][1] + x[2] * S[i][2] + x[3] * S[i][3];
-                }
+                for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                    for (int i = 0; i < NK; ++i) {
+                        const f32x4 x = *reinterpret_cast<const f32x4 *>(
+                            ds + (int64_t)(16 * (NCT * w + ct) + n16) * D + 16 * i + 4 * q4);
+                        p += x[0] * S[ct][i][0] + x[1] * S[ct][i][1] + x[2] * S[ct][i][2] + x[3] * S[ct][i][3];
+                    }
             }
             p = wave_sum(p);
             const int ndot = D * D / 256;
@@ -587,7 +643,7 @@ __global__ void __launch_bounds__(4 * D) k_bwd_dkv(SegArgs a) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int t = 16 * tt + 4 * q4 + r;
-                v4[r] = s <= t ? p[r] * exp2f(sb[t] - bs) : 0.f;
+                v4[r] = s <= t ? p[r] * fexp2(sb[t] - bs) : 0.f;
             }
             const int o = s * LDT + 16 * tt + 4 * q4;
             if (isdA) st4_split<T>(&sdAT[o], &sdATl[SP ? o : 0], v4);
@@ -609,7 +665,7 @@ __global__ void __launch_bounds__(4 * D) k_bwd_dkv(SegArgs a) {
                 for (int st = 0; st < 4; ++st) mma2<T>(DV[st], fh, fl, ldfrag(sK, LDN, 16 * st, 32 * ks, lane));
             }
 #pragma unroll
-            for (int st = 0; st < 4; ++st) DV[st] *= exp2f(b63 - sb[16 * st + n16]);
+            for (int st = 0; st < 4; ++st) DV[st] *= fexp2(b63 - sb[16 * st + n16]);
 #pragma unroll
             for (int st = 0; st < 4; ++st)
 #pragma unroll
@@ -635,7 +691,7 @@ __global__ void __launch_bounds__(4 * D) k_bwd_dkv(SegArgs a) {
                 for (int st = 0; st < 4; ++st) mma2<T>(DK[st], fh, fl, ldfrag(sV, LDN, 16 * st, 32 * ks, lane));
             }
 #pragma unroll
-            for (int st = 0; st < 4; ++st) DK[st] *= exp2f(b63 - sb[16 * st + n16]);
+            for (int st = 0; st < 4; ++st) DK[st] *= fexp2(b63 - sb[16 * st + n16]);
 #pragma unroll
             for (int st = 0; st < 4; ++st)
 #pragma unroll
@@ -677,7 +733,7 @@ __global__ void __launch_bounds__(4 * D) k_bwd_dkv(SegArgs a) {
                 vecB hi, lo;
 #pragma unroll
                 for (int j = 0; j < TPB; ++j) {
-                    const float v = tof<T>(x[j]) * exp2f(sb[t0 + j]);
+                    const float v = tof<T>(x[j]) * fexp2(sb[t0 + j]);
                     hi[j] = cvt<T>(v);
                     lo[j] = cvt<T>(v - tof<T>(hi[j]));
                 }
@@ -688,7 +744,7 @@ __global__ void __launch_bounds__(4 * D) k_bwd_dkv(SegArgs a) {
         __syncthreads();
         // G <- exp(b_63) G + (Q o exp(b))^T dO, and the same for G^T
         {
-            const float gam = exp2f(b63);
+            const float gam = fexp2(b63);
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
                 G[i] *= gam;
@@ -728,14 +784,15 @@ __global__ void __launch_bounds__(SCAN_NT) k_state_copy(const float *src, float 
 // launchers
 template <typename T, int D>
 static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s) {
-    const dim3 blk(Cfg<T, D>::NT);
     const dim3 grid((unsigned)((int64_t)a.B * a.H * a.n_super));
+    constexpr int NTP = 64 * D / (16 * SF_NCT_PREP), NTB = 64 * D / (16 * SF_NCT_PREPB);
+    constexpr int NTW = 64 * D / (16 * SF_NCT_WALK);
     switch (kind) {
-    case SF_K_FWD_PREP: hipLaunchKernelGGL((k_prep<T, D, false>), grid, blk, 0, s, a); break;
-    case SF_K_FWD_OUT: hipLaunchKernelGGL((k_walk<T, D, false>), grid, blk, 0, s, a); break;
-    case SF_K_BWD_PREP: hipLaunchKernelGGL((k_prep<T, D, true>), grid, blk, 0, s, a); break;
-    case SF_K_BWD_DQ: hipLaunchKernelGGL((k_walk<T, D, true>), grid, blk, 0, s, a); break;
-    case SF_K_BWD_DKV: hipLaunchKernelGGL((k_bwd_dkv<T, D>), grid, blk, 0, s, a); break;
+    case SF_K_FWD_PREP: hipLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, false>), grid, dim3(NTP), 0, s, a); break;
+    case SF_K_FWD_OUT: hipLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, false>), grid, dim3(NTW), 0, s, a); break;
+    case SF_K_BWD_PREP: hipLaunchKernelGGL((k_prep<T, D, SF_NCT_PREPB, true>), grid, dim3(NTB), 0, s, a); break;
+    case SF_K_BWD_DQ: hipLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, true>), grid, dim3(NTW), 0, s, a); break;
+    case SF_K_BWD_DKV: hipLaunchKernelGGL((k_bwd_dkv<T, D>), grid, dim3(4 * D), 0, s, a); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
