@@ -25,7 +25,22 @@ constexpr float LOG2E = 1.4426950408889634f;
 #ifndef SF_SPLIT_BF16
 #define SF_SPLIT_BF16 1
 #endif
+// per operand class (compile-time switches for accuracy/throughput studies):
+// the state as an MFMA operand (S, G), the decayed per-token operands of the
+// state updates, and the decayed score tiles
+#ifndef SF_SPLIT_STATE
+#define SF_SPLIT_STATE SF_SPLIT_BF16
+#endif
+#ifndef SF_SPLIT_DECAY
+#define SF_SPLIT_DECAY SF_SPLIT_BF16
+#endif
+#ifndef SF_SPLIT_SCORES
+#define SF_SPLIT_SCORES SF_SPLIT_BF16
+#endif
 template <typename T> constexpr bool kSplit = sizeof(T) == 2 && SF_SPLIT_BF16;
+template <typename T> constexpr bool kSplitState = sizeof(T) == 2 && SF_SPLIT_STATE;
+template <typename T> constexpr bool kSplitDecay = sizeof(T) == 2 && SF_SPLIT_DECAY;
+template <typename T> constexpr bool kSplitScores = sizeof(T) == 2 && SF_SPLIT_SCORES;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
@@ -130,45 +145,73 @@ __device__ __forceinline__ f32x4 ld4f(const __bf16 *p) {
 }
 __device__ __forceinline__ f32x4 ld4f(const float *p) { return *reinterpret_cast<const f32x4 *>(p); }
 
-// hi/lo split of 8 fp32 values: hi = T(x), lo = T(x - hi)
+// 4 fp32 values rounded to T (a register-held output vector)
 template <typename T>
+__device__ __forceinline__ auto pack4(const f32x4 &x) {
+    typedef T v4 __attribute__((ext_vector_type(4)));
+    return __builtin_convertvector(x, v4);
+}
+
+// hi/lo split of 8 fp32 values: hi = T(x), lo = T(x - hi)
+template <typename T, bool SP = kSplit<T>>
 __device__ __forceinline__ void split8(const float *x, frag_t<T> &hi, frag_t<T> &lo) {
+    if constexpr (sizeof(T) == 2) {
+        // pairs: one packed conversion for hi, hi back to fp32 by a shift / mask of
+        // the packed word, one packed conversion for lo
+        typedef float f2 __attribute__((ext_vector_type(2)));
+        typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+        typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+        u4 h, l;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const T h = cvt<T>(x[j]);
-        hi[j] = h;
-        lo[j] = cvt<T>(x[j] - tof<T>(h));
+        for (int p = 0; p < 4; ++p) {
+            const f2 xv = {x[2 * p], x[2 * p + 1]};
+            const uint32_t u = __builtin_bit_cast(uint32_t, __builtin_convertvector(xv, b2));
+            h[p] = u;
+            if constexpr (SP) {
+                const f2 r = {x[2 * p] - __builtin_bit_cast(float, u << 16),
+                              x[2 * p + 1] - __builtin_bit_cast(float, u & 0xffff0000u)};
+                l[p] = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, b2));
+            }
+        }
+        hi = __builtin_bit_cast(frag_t<T>, h);
+        if constexpr (SP) lo = __builtin_bit_cast(frag_t<T>, l);
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            hi[j] = cvt<T>(x[j]);
+            lo[j] = cvt<T>(0.f);
+        }
     }
 }
 // split fragment of two accumulator tiles (see frag_from_acc)
-template <typename T>
+template <typename T, bool SP = kSplit<T>>
 __device__ __forceinline__ void split_acc(const f32x4 &a0, const f32x4 &a1, frag_t<T> &hi, frag_t<T> &lo) {
     float x[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
-    split8<T>(x, hi, lo);
+    split8<T, SP>(x, hi, lo);
 }
 // split fragment of a T fragment scaled per slot by s[] (fp32)
-template <typename T>
+template <typename T, bool SP = kSplit<T>>
 __device__ __forceinline__ void split_scaled(const frag_t<T> &f, const float *s, frag_t<T> &hi, frag_t<T> &lo) {
     float x[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) x[j] = tof<T>(f[j]) * s[j];
-    split8<T>(x, hi, lo);
+    split8<T, SP>(x, hi, lo);
 }
 // acc += a * b, with a given as a hi/lo pair (lo skipped when not splitting)
-template <typename T>
+template <typename T, bool SP = kSplit<T>>
 __device__ __forceinline__ void mma2(f32x4 &c, const frag_t<T> &ahi, const frag_t<T> &alo, const frag_t<T> &b) {
     mma(c, ahi, b);
-    if constexpr (kSplit<T>) mma(c, alo, b);
+    if constexpr (SP) mma(c, alo, b);
 }
-template <typename T>
+template <typename T, bool SP = kSplit<T>>
 __device__ __forceinline__ void mma2b(f32x4 &c, const frag_t<T> &a, const frag_t<T> &bhi, const frag_t<T> &blo) {
     mma(c, a, bhi);
-    if constexpr (kSplit<T>) mma(c, a, blo);
+    if constexpr (SP) mma(c, a, blo);
 }
 // 4 consecutive fp32 values stored as a hi/lo pair of T vectors
-template <typename T>
+template <typename T, bool SP = kSplit<T>>
 __device__ __forceinline__ void st4_split(T *hi, T *lo, const float *v) {
-    if constexpr (kSplit<T>) {
+    if constexpr (SP) {
         float h[4], l[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -306,39 +349,53 @@ template <typename T, int D>
 constexpr int swx() { return (D * (int)sizeof(T) >= 256 ? 128 : 64) / (int)sizeof(T); }
 __device__ __forceinline__ int swz_col(int row, int col, int swx) { return col ^ (((row >> 3) & 1) * swx); }
 
-// Lane (q = l/16, n = l%16) receives M[k0 + 8q + j][c0 + n], j = 0..7: an operand
-// fragment with rows = channels c0..c0+15 and contraction = tokens k0..k0+31.
-// c0 must be a multiple of 4 (bf16) / any (fp32, read element by element).
+// Per-lane element offsets into a swizzled natural tile.  Every row a lane
+// touches in a fragment read has the same bit 3, so the swizzle reduces to
+// +swx for channel blocks below swx and -swx above it: two offsets per lane,
+// and each fragment address is one of them plus a compile-time constant.
+struct LaneOff {
+    int lo, hi;
+};
+// for ldfragTR: rows k0 + 8q + (a / 4) (+4), channels c0 + 4 (a % 4) (bf16) or
+// rows k0 + 8q + j, channel c0 + a (fp32), with a = lane % 16
 template <typename T, int LD, int SWX>
-__device__ __forceinline__ frag_t<T> ldfragTR(const T *M, int k0, int c0, int lane) {
-    const int q = lane >> 4, a = lane & 15;
+__device__ __forceinline__ LaneOff tr_off(int lane) {
+    const int q = lane >> 4, a = lane & 15, S = (q & 1) * SWX;
+    const int base = sizeof(T) == 2 ? (8 * q + (a >> 2)) * LD + 4 * (a & 3) : 8 * q * LD + a;
+    return {base + S, base - S};
+}
+// for ldfrag_swz: rows row0 + n, channels k0 + 8q .. +7
+template <typename T, int LD, int SWX>
+__device__ __forceinline__ LaneOff swz_off(int lane) {
+    const int q = lane >> 4, n = lane & 15, S = ((n >> 3) & 1) * SWX;
+    return {n * LD + 8 * q + S, n * LD + 8 * q - S};
+}
+
+// Lane (q = l/16, n = l%16) receives M[k0 + 8q + j][c0 + n], j = 0..7: an operand
+// fragment with rows = channels c0..c0+15 and contraction = tokens k0..k0+31
+// (k0 a multiple of 32, c0 of 16; o = tr_off(lane)).
+template <typename T, int LD, int SWX>
+__device__ __forceinline__ frag_t<T> ldfragTR(const T *M, const LaneOff &o, int k0, int c0) {
+    const int e = (c0 < SWX ? o.lo : o.hi) + k0 * LD + c0;
     if constexpr (sizeof(T) == 2) {
         typedef short s4 __attribute__((ext_vector_type(4)));
-        const int col = c0 + 4 * (a & 3);
-        const int r0 = k0 + 8 * q + (a >> 2), r1 = r0 + 4;
-        const s4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s4 *)(M + r0 * LD + swz_col(r0, col, SWX)));
-        const s4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s4 *)(M + r1 * LD + swz_col(r1, col, SWX)));
-        const s4 lo = x0, hi = x1;
         typedef short s8 __attribute__((ext_vector_type(8)));
-        const s8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        const s4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)(M + e));
+        const s4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)(M + e + 4 * LD));
+        const s8 v = __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7);
         return __builtin_bit_cast(frag_t<T>, v);
     } else {
         frag_t<T> f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int row = k0 + 8 * q + j;
-            f[j] = M[row * LD + swz_col(row, c0 + a, SWX)];
-        }
+        for (int j = 0; j < 8; ++j) f[j] = M[e + j * LD];
         return f;
     }
 }
-// ldfrag() on a swizzled natural tile (rows row0.., channels k0 + 8q .. +7).
+// ldfrag() on a swizzled natural tile (rows row0.., channels k0 + 8q .. +7;
+// row0 a multiple of 16, k0 of 32; o = swz_off(lane)).
 template <typename T, int LD, int SWX>
-__device__ __forceinline__ frag_t<T> ldfrag_swz(const T *M, int row0, int k0, int lane) {
-    const int r = row0 + (lane & 15);
-    return *reinterpret_cast<const frag_t<T> *>(M + r * LD + swz_col(r, k0 + 8 * (lane >> 4), SWX));
+__device__ __forceinline__ frag_t<T> ldfrag_swz(const T *M, const LaneOff &o, int row0, int k0) {
+    return *reinterpret_cast<const frag_t<T> *>(M + (k0 < SWX ? o.lo : o.hi) + row0 * LD + k0);
 }
 // Fragment in plain channel order (channels k0 + 8q .. +7) from a tile stored
 // in nat_pos order: the 8 channels sit in two 4-channel runs 8 apart.
@@ -351,6 +408,19 @@ __device__ __forceinline__ frag_t<T> ldfrag_unperm(const T *M, int ld, int row0,
     const h4 hi = *reinterpret_cast<const h4 *>(p + 8);
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }
+
+// Compiler scheduling fence: no instruction moves across it.  Used to keep a
+// batch of LDS fragment reads ahead of independent VALU work, so that their
+// latency overlaps that work instead of stalling the MFMA that consumes them.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+// Wait for every outstanding vector memory operation of this wave.  Loads and
+// stores share one counter on gfx9-class GPUs, and once both kinds are pending
+// the compiler can only wait for a load by draining everything, stores
+// included.  The chunk loops therefore retire their prefetch loads here, before
+// they issue the chunk's global stores, so that the next chunk's use of the
+// prefetched registers does not wait for those stores.
+__device__ __forceinline__ void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
 // Inclusive prefix sum over the 64 lanes of a wave with DPP row shifts and row
 // broadcasts (no LDS round trips); lanes without a source add 0.

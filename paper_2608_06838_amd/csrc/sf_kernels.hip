@@ -51,6 +51,9 @@ constexpr int SCAN_NT = 256;
 #ifndef SF_NCT_WALK
 #define SF_NCT_WALK 2
 #endif
+#ifndef SF_NCT_DKV
+#define SF_NCT_DKV 1
+#endif
 
 // 2^x with the hardware v_exp_f32 (results below 2^-126 flush to zero, which
 // is what a decay that small means here; no input is ever > 0 except on
@@ -91,6 +94,7 @@ template <typename T, int D, int NCT, bool BWD>
 __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_prep(SegArgs a) {
     constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
     constexpr int LDN = D + pad<T>(), SWX = swx<T, D>();
+    constexpr bool SPD = kSplitDecay<T>;
     __shared__ __attribute__((aligned(16))) T sK[C * LDN];
     __shared__ __attribute__((aligned(16))) T sV[C * LDN];
     __shared__ __attribute__((aligned(16))) T sQ[BWD ? C * LDN : 8];
@@ -100,6 +104,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
     const Decode d = decode(a);
+    const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *K = (const T *)a.k + xo;
     const T *V = (const T *)a.v + xo;
@@ -169,18 +174,18 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
                 const int c0 = 16 * (NCT * w + ct);
-                split_scaled<T>(ldfragTR<T, LDN, SWX>(sV, 32 * ks, c0, lane), ev, vh[ct], vl[ct]);
-                if constexpr (BWD) split_scaled<T>(ldfragTR<T, LDN, SWX>(sO, 32 * ks, c0, lane), qv, oh[ct], ol[ct]);
+                split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sV, tro, 32 * ks, c0), ev, vh[ct], vl[ct]);
+                if constexpr (BWD) split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sO, tro, 32 * ks, c0), qv, oh[ct], ol[ct]);
             }
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
-                const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sK, 32 * ks, 16 * i, lane);
+                const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sK, tro, 32 * ks, 16 * i);
 #pragma unroll
-                for (int ct = 0; ct < NCT; ++ct) mma2b<T>(Ds[ct][i], kf, vh[ct], vl[ct]);
+                for (int ct = 0; ct < NCT; ++ct) mma2b<T, SPD>(Ds[ct][i], kf, vh[ct], vl[ct]);
                 if constexpr (BWD) {
-                    const frag_t<T> qf = ldfragTR<T, LDN, SWX>(sQ, 32 * ks, 16 * i, lane);
+                    const frag_t<T> qf = ldfragTR<T, LDN, SWX>(sQ, tro, 32 * ks, 16 * i);
 #pragma unroll
-                    for (int ct = 0; ct < NCT; ++ct) mma2b<T>(Es[ct][i], qf, oh[ct], ol[ct]);
+                    for (int ct = 0; ct < NCT; ++ct) mma2b<T, SPD>(Es[ct][i], qf, oh[ct], ol[ct]);
                 }
             }
         }
@@ -277,7 +282,7 @@ template <typename T, int D, int NCT, bool DQ>
 __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_walk(SegArgs a) {
     constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
     constexpr int LDN = D + pad<T>(), LDT = C + pad<T>(), SWX = swx<T, D>();
-    constexpr bool SP = kSplit<T>;
+    constexpr bool SP = kSplitScores<T>, SPS = kSplitState<T>, SPD = kSplitDecay<T>;
     __shared__ __attribute__((aligned(16))) T sX1[C * LDN];
     __shared__ __attribute__((aligned(16))) T sX2[C * LDN];
     __shared__ __attribute__((aligned(16))) T sX3[C * LDN];
@@ -290,6 +295,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
     const Decode d = decode(a);
+    const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *X1 = (const T *)(DQ ? a.dO : a.q) + xo;
     const T *X2 = (const T *)(DQ ? a.v : a.k) + xo;
@@ -379,7 +385,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             f32x4 p = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks)
-                mma(p, ldfrag_swz<T, LDN, SWX>(sX2, 16 * st, 32 * ks, lane),
+                mma(p, ldfrag_swz<T, LDN, SWX>(sX2, swo, 16 * st, 32 * ks),
                     ldfrag_unperm<T>(sX1, LDN, 16 * tt, 32 * ks, lane));
             const int t = 16 * tt + n16;
             const float bt = sb[t];
@@ -391,7 +397,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
                 v4[r] = s <= t ? p[r] * fexp2(bt - bs[r]) : 0.f;
             }
             const int o = t * LDT + 16 * st + 4 * q4;
-            st4_split<T>(&sA[o], &sAl[SP ? o : 0], v4);
+            st4_split<T, SP>(&sA[o], &sAl[SP ? o : 0], v4);
         }
         __syncthreads();
 
@@ -407,15 +413,15 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks) {
                 frag_t<T> fh, fl;
-                split_acc<T>(S[ct][2 * ks], S[ct][2 * ks + 1], fh, fl);
+                split_acc<T, SPS>(S[ct][2 * ks], S[ct][2 * ks + 1], fh, fl);
 #pragma unroll
-                for (int tt = 0; tt < 4; ++tt) mma2<T>(O[tt], fh, fl, ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane));
+                for (int tt = 0; tt < 4; ++tt) mma2<T, SPS>(O[tt], fh, fl, ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane));
             }
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) O[tt] *= sq[16 * tt + n16];
 #pragma unroll
             for (int ks = 0; ks < C / 32; ++ks) {
-                vf[ct][ks] = ldfragTR<T, LDN, SWX>(sX3, 32 * ks, c0, lane);
+                vf[ct][ks] = ldfragTR<T, LDN, SWX>(sX3, tro, 32 * ks, c0);
 #pragma unroll
                 for (int tt = 0; tt < 4; ++tt) {
                     if (32 * ks > 16 * tt + 15) continue;
@@ -458,12 +464,12 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             const float ev[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
             frag_t<T> vh[NCT], vl[NCT];
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) split_scaled<T>(vf[ct][ks], ev, vh[ct], vl[ct]);
+            for (int ct = 0; ct < NCT; ++ct) split_scaled<T, SPD>(vf[ct][ks], ev, vh[ct], vl[ct]);
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
-                const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sX2, 32 * ks, 16 * i, lane);
+                const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sX2, tro, 32 * ks, 16 * i);
 #pragma unroll
-                for (int ct = 0; ct < NCT; ++ct) mma2b<T>(S[ct][i], kf, vh[ct], vl[ct]);
+                for (int ct = 0; ct < NCT; ++ct) mma2b<T, SPD>(S[ct][i], kf, vh[ct], vl[ct]);
             }
         }
     }
@@ -515,39 +521,38 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 // ---------------------------------------------------------------------------
 // PG: reverse walk over the chunks of a superchunk with the state gradient G
 // (dLoss/dS of the state leaving the chunk) in registers, in both
-// orientations: G[k][v] (wave w owns v-tile w) feeds dv, G^T[v][k] (wave w
-// owns k-tile w) feeds dk, so neither needs G through LDS:
+// orientations: G[k][v] (wave w owns v-tiles) feeds dv, G^T[v][k] (wave w owns
+// k-tiles) feeds dk, so neither needs G through LDS:
 //   dv^T = exp(b_63 - b_s) G^T K^T + dO^T A^T      (A from Q K^T)
 //   dk^T = exp(b_63 - b_s) G V^T   + Q^T dA^T      (dA from dO V^T)
-//   G   <- exp(b_63) G + (Q o exp(b))^T dO          (and its transpose)
+//   G   <- exp(b_63) G + Q^T (exp(b) o dO)          (and its transpose)
 //   dg_t = sum_{t' >= t in superchunk} (q.dq - k.dk)_{t'} + <G_{J+1}, S_{J+1}>
 // (the last term is the decay gradient carried in from later superchunks).
-template <typename T, int D>
-__global__ void __launch_bounds__(4 * D) k_bwd_dkv(SegArgs a) {
-    using F = Cfg<T, D>;
-    constexpr int LDN = F::LDN, LDT = F::LDT, NK = F::NK, NW = F::NW, NT = F::NT;
-    constexpr bool SP = F::SP;
-    __shared__ __attribute__((aligned(16))) T sQ[C * LDN];
-    __shared__ __attribute__((aligned(16))) T sK[C * LDN];
-    __shared__ __attribute__((aligned(16))) T sV[C * LDN];
-    __shared__ __attribute__((aligned(16))) T sO[C * LDN];   // dO
-    __shared__ __attribute__((aligned(16))) T sQT[D * LDT];
-    __shared__ __attribute__((aligned(16))) T sOT[D * LDT];  // dO^T
-    // scratch: A^T and dA^T (hi, lo) for the dv/dk products, then (Q o exp(b))^T
-    // (hi, lo) for the state-gradient update
-    constexpr int NS = SP ? 2 : 1;
-    constexpr int SCR = 2 * NS * C * LDT;
-    static_assert(NS * D * LDT <= SCR, "scratch holds the scaled Q^T");
-    __shared__ __attribute__((aligned(16))) T sScr[SCR];
-    T *sAT = sScr, *sATl = sScr + (NS - 1) * C * LDT;            // A^T[s][t]
-    T *sdAT = sScr + NS * C * LDT, *sdATl = sdAT + (NS - 1) * C * LDT;  // dA^T[s][t]
-    T *sQs = sScr, *sQsl = sScr + (NS - 1) * D * LDT;              // (Q o exp(b))^T
-    __shared__ float sb[C];
+// LDS holds natural tiles only: K and V in nat_pos channel order (they meet the
+// accumulator-built G fragments), Q and dO plain and swizzled for the
+// transposing loads of the G updates, where the per-token decay goes on the
+// wave's own columns.
+template <typename T, int D, int NCT>
+__global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
+    constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
+    constexpr int LDN = D + pad<T>(), LDT = C + pad<T>(), SWX = swx<T, D>();
+    constexpr bool SP = kSplitScores<T>, SPS = kSplitState<T>, SPD = kSplitDecay<T>;
+    __shared__ __attribute__((aligned(16))) T sQ[C * LDN];   // plain, swizzled
+    __shared__ __attribute__((aligned(16))) T sO[C * LDN];   // dO, plain, swizzled
+    __shared__ __attribute__((aligned(16))) T sK[C * LDN];   // nat_pos order
+    __shared__ __attribute__((aligned(16))) T sV[C * LDN];   // nat_pos order
+    __shared__ __attribute__((aligned(16))) T sAT[C * LDT];  // A^T[s][t] (hi)
+    __shared__ __attribute__((aligned(16))) T sATl[SP ? C * LDT : 8];
+    __shared__ __attribute__((aligned(16))) T sdAT[C * LDT]; // dA^T[s][t] (hi)
+    __shared__ __attribute__((aligned(16))) T sdATl[SP ? C * LDT : 8];
+    __shared__ __attribute__((aligned(16))) float sb[C];   // b_t (log2, chunk-local)
+    __shared__ __attribute__((aligned(16))) float se[C];   // exp2(b63 - b_s)
+    __shared__ __attribute__((aligned(16))) float sq[C];   // exp2(b_t)
     __shared__ float sred[NW * C];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
-    const int c0 = 16 * w;
     const Decode d = decode(a);
+    const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *Q = (const T *)a.q + xo;
     const T *K = (const T *)a.k + xo;
@@ -563,66 +568,79 @@ __global__ void __launch_bounds__(4 * D) k_bwd_dkv(SegArgs a) {
 
     const float *gsrc = a.n_super == 1 ? (a.dS_out ? a.dS_out + d.bh * SS : nullptr)
                                        : a.wsE + ((int64_t)d.bh * a.n_super + d.J) * SS;
-    f32x4 G[NK], GT[NK];  // G[k][v] (v-tile w) and G^T[v][k] (k-tile w)
+    f32x4 G[NCT][NK], GT[NCT][NK];  // G[k][v] (v-tiles) and G^T[v][k] (k-tiles)
 #pragma unroll
-    for (int i = 0; i < NK; ++i) {
-        if (!gsrc) {
-            G[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-            GT[i] = G[i];
-        } else {
+    for (int ct = 0; ct < NCT; ++ct) {
+        const int c0 = 16 * (NCT * w + ct);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) G[i][r] = gsrc[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16];
-            GT[i] = *reinterpret_cast<const f32x4 *>(gsrc + (int64_t)(c0 + n16) * D + 16 * i + 4 * q4);
+        for (int i = 0; i < NK; ++i) {
+            if (!gsrc) {
+                G[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+                GT[ct][i] = G[ct][i];
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) G[ct][i][r] = gsrc[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16];
+                GT[ct][i] = *reinterpret_cast<const f32x4 *>(gsrc + (int64_t)(c0 + n16) * D + 16 * i + 4 * q4);
+            }
         }
     }
-    float carry;
-    {
+    float carry = 0.f;  // wave 0: decay gradient carried in from later tokens
+    if (w == 0) {
         const float *dot = a.wsDot + ((int64_t)d.bh * a.n_super + d.J) * ndot;
         carry = wave_sum(lane < ndot ? dot[lane] : 0.f);
     }
+    // score tiles read by the dv/dk products but above the diagonal stay zero
+    for (int e = tid; e < 512; e += NT) {
+        const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
+        const int idx = tile ? (48 + rr) * LDT + 32 + cc : (16 + rr) * LDT + cc;
+        sAT[idx] = cvt<T>(0.f);
+        sdAT[idx] = cvt<T>(0.f);
+        if constexpr (SP) {
+            sATl[idx] = cvt<T>(0.f);
+            sdATl[idx] = cvt<T>(0.f);
+        }
+    }
+
     Tile<T, D, NT> tq, tk, tv, to;
-    {
-        const int64_t nx = (int64_t)(d.nch - 1) * C * a.sx_l;
+    float gl, rn;
+    auto issue = [&](int c) {
+        const int64_t nx = (int64_t)c * C * a.sx_l;
         tq.load(Q + nx, a.sx_l, tid);
         tk.load(K + nx, a.sx_l, tid);
         tv.load(V + nx, a.sx_l, tid);
         to.load(dO + nx, a.sx_l, tid);
-    }
-    float gl = gp[((d.nch - 1) * C + lane) * a.sg_l];
-    float rn = dgp[((d.nch - 1) * C + lane) * a.sg_l];  // q.dq left in dg by the dq walk
+        gl = gp[(c * C + lane) * a.sg_l];
+        rn = dgp[(c * C + lane) * a.sg_l];  // q.dq left in dg by the dq walk
+    };
+    issue(d.nch - 1);
+    float rprev = 0.f;  // wave 0: q.dq of the chunk whose dg is still pending
+
+    // dg of chunk cp from the k.dk partials in sred (wave 0)
+    auto finish_dg = [&](int cp) {
+        float kd = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) kd += sred[ww * C + lane];
+        const float suf = wave_incl_suffix(rprev - kd, lane);
+        dgp[((int64_t)cp * C + lane) * a.sg_l] = carry + suf;
+        carry += lane_value(suf, 0);
+    };
 
     for (int c = d.nch - 1; c >= 0; --c) {
-        const float b2 = wave_incl_scan(gl * LOG2E, lane);
-        const float b63 = __shfl(b2, 63, 64);
+        const float b2 = wave_scan_dpp(gl * LOG2E);
+        const float b63 = lane_value(b2, 63);
         const float rc = rn;
         __syncthreads();
-        if (w == 0) sb[lane] = b2;
-        tq.store_nat(sQ, LDN, tid);
+        tq.store_swz(sQ, LDN, tid, SWX);
+        to.store_swz(sO, LDN, tid, SWX);
         tk.store_nat(sK, LDN, tid);
         tv.store_nat(sV, LDN, tid);
-        to.store_nat(sO, LDN, tid);
-        tq.store_T1(sQT, LDT, tid);
-        to.store_T1(sOT, LDT, tid);
-        // score tiles read by the dv/dk products but above the diagonal are zero
-        // (rewritten every chunk: the scratch also holds the scaled Q^T)
-        for (int e = tid; e < 512; e += NT) {
-            const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
-            const int idx = tile ? (48 + rr) * LDT + 32 + cc : (16 + rr) * LDT + cc;
-            sAT[idx] = cvt<T>(0.f);
-            sdAT[idx] = cvt<T>(0.f);
-            if constexpr (SP) {
-                sATl[idx] = cvt<T>(0.f);
-                sdATl[idx] = cvt<T>(0.f);
-            }
-        }
-        if (c > 0) {
-            const int64_t nx = (int64_t)(c - 1) * C * a.sx_l;
-            tq.load(Q + nx, a.sx_l, tid);
-            tk.load(K + nx, a.sx_l, tid);
-            tv.load(V + nx, a.sx_l, tid);
-            to.load(dO + nx, a.sx_l, tid);
-            gl = gp[((c - 1) * C + lane) * a.sg_l];
-            rn = dgp[((c - 1) * C + lane) * a.sg_l];
+        if (c > 0) issue(c - 1);
+        if (w == 0) {
+            if (c < d.nch - 1) finish_dg(c + 1);
+            rprev = rc;
+            sb[lane] = b2;
+            se[lane] = fexp2(b63 - b2);
+            sq[lane] = fexp2(b2);
         }
         __syncthreads();
 
@@ -636,141 +654,141 @@ __global__ void __launch_bounds__(4 * D) k_bwd_dkv(SegArgs a) {
             f32x4 p = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks)
-                mma(p, ldfrag(X, LDN, 16 * tt, 32 * ks, lane), ldfrag(Yt, LDN, 16 * st, 32 * ks, lane));
+                mma(p, ldfrag_swz<T, LDN, SWX>(X, swo, 16 * tt, 32 * ks),
+                    ldfrag_unperm<T>(Yt, LDN, 16 * st, 32 * ks, lane));
             const int s = 16 * st + n16;
             const float bs = sb[s];
+            const f32x4 bt = *reinterpret_cast<const f32x4 *>(&sb[16 * tt + 4 * q4]);
             float v4[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int t = 16 * tt + 4 * q4 + r;
-                v4[r] = s <= t ? p[r] * fexp2(sb[t] - bs) : 0.f;
+                v4[r] = s <= t ? p[r] * fexp2(bt[r] - bs) : 0.f;
             }
             const int o = s * LDT + 16 * tt + 4 * q4;
-            if (isdA) st4_split<T>(&sdAT[o], &sdATl[SP ? o : 0], v4);
-            else st4_split<T>(&sAT[o], &sATl[SP ? o : 0], v4);
+            if (isdA) st4_split<T, SP>(&sdAT[o], &sdATl[SP ? o : 0], v4);
+            else st4_split<T, SP>(&sAT[o], &sATl[SP ? o : 0], v4);
         }
         __syncthreads();
 
         const int64_t crow = (int64_t)c * C;
-        // dv^T[v][s] for v in tile w
-        {
-            f32x4 DV[4];
+        float kdp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int st = 0; st < 4; ++st) DV[st] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int ct = 0; ct < NCT; ++ct) {
+            const int c0 = 16 * (NCT * w + ct);
+            // decayed state parts: dv^T[v][s] += G^T K^T, dk^T[k][s] += G V^T (v, k in this tile)
+            f32x4 DV[4], DK[4];
+#pragma unroll
+            for (int st = 0; st < 4; ++st) DV[st] = DK[st] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks) {
-                frag_t<T> fh, fl;
-                split_acc<T>(G[2 * ks], G[2 * ks + 1], fh, fl);
+                frag_t<T> kfr[4], vfr[4];
 #pragma unroll
-                for (int st = 0; st < 4; ++st) mma2<T>(DV[st], fh, fl, ldfrag(sK, LDN, 16 * st, 32 * ks, lane));
-            }
-#pragma unroll
-            for (int st = 0; st < 4; ++st) DV[st] *= fexp2(b63 - sb[16 * st + n16]);
-#pragma unroll
-            for (int st = 0; st < 4; ++st)
-#pragma unroll
-                for (int ks = st / 2; ks < C / 32; ++ks) {
-                    const frag_t<T> fa = ldfragT(sOT, LDT, c0, 32 * ks, lane);
-                    mma(DV[st], fa, ldfrag(sAT, LDT, 16 * st, 32 * ks, lane));
-                    if constexpr (SP) mma(DV[st], fa, ldfrag(sATl, LDT, 16 * st, 32 * ks, lane));
+                for (int st = 0; st < 4; ++st) {
+                    kfr[st] = ldfrag(sK, LDN, 16 * st, 32 * ks, lane);
+                    vfr[st] = ldfrag(sV, LDN, 16 * st, 32 * ks, lane);
                 }
+                sched_fence();  // keep the fragment reads ahead of the split below
+                frag_t<T> gh, gl, th, tl;
+                split_acc<T, SPS>(G[ct][2 * ks], G[ct][2 * ks + 1], gh, gl);
+                split_acc<T, SPS>(GT[ct][2 * ks], GT[ct][2 * ks + 1], th, tl);
+                sched_fence();
 #pragma unroll
-            for (int st = 0; st < 4; ++st)
-                st4(dV + (crow + 16 * st + n16) * a.sx_l + c0 + 4 * q4, DV[st][0], DV[st][1], DV[st][2], DV[st][3]);
-        }
-        // dk^T[k][s] for k in tile w; k.dk partials
-        {
-            f32x4 DK[4];
-#pragma unroll
-            for (int st = 0; st < 4; ++st) DK[st] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int ks = 0; ks < D / 32; ++ks) {
-                frag_t<T> fh, fl;
-                split_acc<T>(GT[2 * ks], GT[2 * ks + 1], fh, fl);
-#pragma unroll
-                for (int st = 0; st < 4; ++st) mma2<T>(DK[st], fh, fl, ldfrag(sV, LDN, 16 * st, 32 * ks, lane));
+                for (int st = 0; st < 4; ++st) {
+                    mma2<T, SPS>(DV[st], gh, gl, kfr[st]);
+                    mma2<T, SPS>(DK[st], th, tl, vfr[st]);
+                }
             }
+            const frag_t<T> of0 = ldfragTR<T, LDN, SWX>(sO, tro, 0, c0), of1 = ldfragTR<T, LDN, SWX>(sO, tro, 32, c0);
+            const frag_t<T> qf0 = ldfragTR<T, LDN, SWX>(sQ, tro, 0, c0), qf1 = ldfragTR<T, LDN, SWX>(sQ, tro, 32, c0);
 #pragma unroll
-            for (int st = 0; st < 4; ++st) DK[st] *= fexp2(b63 - sb[16 * st + n16]);
+            for (int st = 0; st < 4; ++st) {
+                const float f = se[16 * st + n16];
+                DV[st] *= f;
+                DK[st] *= f;
+            }
+            // intra-chunk parts: dv^T += dO^T A^T, dk^T += Q^T dA^T (A^T, dA^T zero above the diagonal)
 #pragma unroll
             for (int st = 0; st < 4; ++st)
 #pragma unroll
                 for (int ks = st / 2; ks < C / 32; ++ks) {
-                    const frag_t<T> fa = ldfragT(sQT, LDT, c0, 32 * ks, lane);
-                    mma(DK[st], fa, ldfrag(sdAT, LDT, 16 * st, 32 * ks, lane));
-                    if constexpr (SP) mma(DK[st], fa, ldfrag(sdATl, LDT, 16 * st, 32 * ks, lane));
+                    const frag_t<T> ah = ldfrag(sAT, LDT, 16 * st, 32 * ks, lane);
+                    const frag_t<T> dh = ldfrag(sdAT, LDT, 16 * st, 32 * ks, lane);
+                    frag_t<T> al, dl;
+                    if constexpr (SP) {
+                        al = ldfrag(sATl, LDT, 16 * st, 32 * ks, lane);
+                        dl = ldfrag(sdATl, LDT, 16 * st, 32 * ks, lane);
+                    }
+                    const frag_t<T> &ofk = ks ? of1 : of0, &qfk = ks ? qf1 : qf0;
+                    mma(DV[st], ofk, ah);
+                    mma(DK[st], qfk, dh);
+                    if constexpr (SP) {
+                        mma(DV[st], ofk, al);
+                        mma(DK[st], qfk, dl);
+                    }
                 }
 #pragma unroll
             for (int st = 0; st < 4; ++st) {
                 const int s = 16 * st + n16;
                 const int col = c0 + 4 * q4;
+                st4(dV + (crow + s) * a.sx_l + col, DV[st][0], DV[st][1], DV[st][2], DV[st][3]);
                 st4(dK + (crow + s) * a.sx_l + col, DK[st][0], DK[st][1], DK[st][2], DK[st][3]);
                 const f32x4 kv = ld4f(&sK[s * LDN + nat_pos(col)]);
-                float part = DK[st][0] * kv[0] + DK[st][1] * kv[1] + DK[st][2] * kv[2] + DK[st][3] * kv[3];
-                part += __shfl_xor(part, 16, 64);
-                part += __shfl_xor(part, 32, 64);
-                if (q4 == 0) sred[w * C + s] = part;
+                kdp[st] += DK[st][0] * kv[0] + DK[st][1] * kv[1] + DK[st][2] * kv[2] + DK[st][3] * kv[3];
             }
         }
-        __syncthreads();  // dv/dk done with the score tiles; k.dk partials complete
-        if (w == 0) {
-            float kd = 0.f;
 #pragma unroll
-            for (int ww = 0; ww < NW; ++ww) kd += sred[ww * C + lane];
-            const float suf = wave_incl_suffix(rc - kd, lane);
-            dgp[(crow + lane) * a.sg_l] = carry + suf;
-            carry += __shfl(suf, 0, 64);
+        for (int st = 0; st < 4; ++st) {
+            kdp[st] += __shfl_xor(kdp[st], 16, 64);
+            kdp[st] += __shfl_xor(kdp[st], 32, 64);
+            if (q4 == 0) sred[w * C + 16 * st + n16] = kdp[st];
         }
-        // (Q o exp(b))^T as hi/lo into the scratch, same swizzled layout as sQT
-        {
-            constexpr int TPB = 16 / (int)sizeof(T), NB = C / TPB;
-            typedef T vecB __attribute__((ext_vector_type(TPB)));
-            for (int blk = tid; blk < D * NB; blk += NT) {
-                const int row = blk / NB, pb = blk % NB;
-                const int t0 = (pb ^ ((row >> 4) & (NB - 1))) * TPB;
-                const int o = row * LDT + pb * TPB;
-                const vecB x = *reinterpret_cast<const vecB *>(&sQT[o]);
-                vecB hi, lo;
+
+        // G <- exp2(b63) G + Q^T (exp2(b) o dO), G^T <- exp2(b63) G^T + dO^T (exp2(b) o Q)
+        const float gam = fexp2(b63);
 #pragma unroll
-                for (int j = 0; j < TPB; ++j) {
-                    const float v = tof<T>(x[j]) * fexp2(sb[t0 + j]);
-                    hi[j] = cvt<T>(v);
-                    lo[j] = cvt<T>(v - tof<T>(hi[j]));
-                }
-                *reinterpret_cast<vecB *>(&sQs[o]) = hi;
-                if constexpr (SP) *reinterpret_cast<vecB *>(&sQsl[o]) = lo;
-            }
-        }
-        __syncthreads();
-        // G <- exp(b_63) G + (Q o exp(b))^T dO, and the same for G^T
-        {
-            const float gam = fexp2(b63);
+        for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
-                G[i] *= gam;
-                GT[i] *= gam;
+                G[ct][i] *= gam;
+                GT[ct][i] *= gam;
             }
 #pragma unroll
-            for (int ks = 0; ks < C / 32; ++ks) {
-                const frag_t<T> fo = ldfragT(sOT, LDT, c0, 32 * ks, lane);
+        for (int ks = 0; ks < C / 32; ++ks) {
+            const int t0 = 32 * ks + 8 * q4;
+            const f32x4 e0 = *reinterpret_cast<const f32x4 *>(&sq[t0]);
+            const f32x4 e1 = *reinterpret_cast<const f32x4 *>(&sq[t0 + 4]);
+            const float ev[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
+            frag_t<T> oh[NCT], ol[NCT], qh[NCT], ql[NCT];
 #pragma unroll
-                for (int i = 0; i < NK; ++i) {
-                    mma(G[i], ldfragT(sQs, LDT, 16 * i, 32 * ks, lane), fo);
-                    if constexpr (SP) mma(G[i], ldfragT(sQsl, LDT, 16 * i, 32 * ks, lane), fo);
+            for (int ct = 0; ct < NCT; ++ct) {
+                const int c0 = 16 * (NCT * w + ct);
+                split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sO, tro, 32 * ks, c0), ev, oh[ct], ol[ct]);
+                split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sQ, tro, 32 * ks, c0), ev, qh[ct], ql[ct]);
+            }
+#pragma unroll
+            for (int i = 0; i < NK; ++i) {
+                const frag_t<T> qa = ldfragTR<T, LDN, SWX>(sQ, tro, 32 * ks, 16 * i);
+                const frag_t<T> oa = ldfragTR<T, LDN, SWX>(sO, tro, 32 * ks, 16 * i);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    mma2b<T, SPD>(G[ct][i], qa, oh[ct], ol[ct]);
+                    mma2b<T, SPD>(GT[ct][i], oa, qh[ct], ql[ct]);
                 }
-                const frag_t<T> qh = ldfragT(sQs, LDT, c0, 32 * ks, lane);
-                const frag_t<T> ql = ldfragT(sQsl, LDT, SP ? c0 : 0, SP ? 32 * ks : 0, lane);
-#pragma unroll
-                for (int i = 0; i < NK; ++i) mma2b<T>(GT[i], ldfragT(sOT, LDT, 16 * i, 32 * ks, lane), qh, ql);
             }
         }
     }
+    __syncthreads();
+    if (w == 0 && d.nch > 0) finish_dg(0);
     if (a.n_super == 1 && a.dS_in) {
         float *dst = a.dS_in + d.bh * SS;
 #pragma unroll
-        for (int i = 0; i < NK; ++i)
+        for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = G[i][r];
+            for (int i = 0; i < NK; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    dst[(int64_t)(16 * i + 4 * q4 + r) * D + 16 * (NCT * w + ct) + n16] = G[ct][i][r];
     }
 }
 
@@ -792,7 +810,9 @@ static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s) {
     case SF_K_FWD_OUT: hipLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, false>), grid, dim3(NTW), 0, s, a); break;
     case SF_K_BWD_PREP: hipLaunchKernelGGL((k_prep<T, D, SF_NCT_PREPB, true>), grid, dim3(NTB), 0, s, a); break;
     case SF_K_BWD_DQ: hipLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, true>), grid, dim3(NTW), 0, s, a); break;
-    case SF_K_BWD_DKV: hipLaunchKernelGGL((k_bwd_dkv<T, D>), grid, dim3(4 * D), 0, s, a); break;
+    case SF_K_BWD_DKV:
+        hipLaunchKernelGGL((k_bwd_dkv<T, D, SF_NCT_DKV>), grid, dim3(64 * D / (16 * SF_NCT_DKV)), 0, s, a);
+        break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
