@@ -26,12 +26,14 @@ METRIC = "fwd+bwd tokens/s per layer (H=40,d=128, 256K ctx); % bf16 MFMA peak"
 #   fwd_prep: k, v, g            fwd_out: q, k, v, g in; o out
 #   bwd_prep: q, k, v, dO, g     bwd_dq: dO, v, k, q, g in; dq, dg out
 #   bwd_dkv:  q, k, v, dO, g, dg in; dk, dv, dg out
+# gb = bytes of one token-head's gate (4 scalar, 4*D per-key-channel); the
+# per-key-channel backward runs dv and dk as two walks
 KERNEL_BYTES = {
-    "fwd_prep": lambda D, io: 2 * D * io + 4,
-    "fwd_out": lambda D, io: 4 * D * io + 4,
-    "bwd_prep": lambda D, io: 4 * D * io + 4,
-    "bwd_dq": lambda D, io: 5 * D * io + 8,
-    "bwd_dkv": lambda D, io: 6 * D * io + 12,
+    "fwd_prep": lambda D, io, gb: 2 * D * io + gb,
+    "fwd_out": lambda D, io, gb: 4 * D * io + gb,
+    "bwd_prep": lambda D, io, gb: 4 * D * io + gb * (1 if gb == 4 else 2),
+    "bwd_dq": lambda D, io, gb: 5 * D * io + 2 * gb,
+    "bwd_dkv": lambda D, io, gb: 6 * D * io + 3 * gb if gb == 4 else 9 * D * io + 4 * gb,
 }
 
 
@@ -42,10 +44,10 @@ def alg_flops_per_token_head(D, C=64):
     return (C + 1) * 2 * D + 4 * D * D + (C + 1) * 5 * D + 10 * D * D
 
 
-def alg_bytes_per_token_head(D, io):
+def alg_bytes_per_token_head(D, io, gb=4):
     """Every interface tensor touched once: fwd q,k,v in, o out, g in;
     bwd q,k,v,dO,g in, dq,dk,dv,dg out."""
-    return (4 * D * io + 4) + (7 * D * io + 8)
+    return (4 * D * io + gb) + (7 * D * io + 2 * gb)
 
 
 def kernel_src_hash():
@@ -134,6 +136,7 @@ def main():
     inp = synth.make_inputs(w, device=dev, seed=1002)
     B, L, H, D = inp["q"].shape
     io = inp["q"].element_size()
+    gb = 4 * (D if inp["g"].dim() == 4 else 1)
     seg = w["seg_lens"]
     overlap = not args.no_overlap
 
@@ -186,9 +189,9 @@ def main():
     dom = max((k for k in KERNEL_BYTES), key=lambda k: ktime[k][0])
     tot_ms, nlaunch = ktime[dom]
     avg_s = tot_ms / 1e3 / max(nlaunch, 1)
-    bytes_per_launch = KERNEL_BYTES[dom](D, io) * B * H * L * args.steps / max(nlaunch, 1)
+    bytes_per_launch = KERNEL_BYTES[dom](D, io, gb) * B * H * L * args.steps / max(nlaunch, 1)
     achieved = bytes_per_launch / avg_s / 1e9
-    traffic = read_traffic(dom)
+    traffic = read_traffic(dom) if w["name"] == "ctx256k_h40" else None
     flops = alg_flops_per_token_head(D) * B * H * L
     if args.kernel_times:
         for k in kernels:
@@ -200,10 +203,11 @@ def main():
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16" if io == 2 else "f32", "data": "synthetic",
         "config": {"workload": w["name"], "B": B, "H": H, "Dk": D, "Dv": D, "L": L, "segments": seg,
+                   "gate": "per-key-channel" if gb > 4 else "scalar",
                    "chunk": 64, "io": "bf16" if io == 2 else "f32", "state": "f32",
                    "overlap": overlap, "ts": args.ts or "auto"},
         "mfma_frac_of_bf16_peak": flops / (ms / 1e3) / PEAK_BF16,
-        "hbm_frac_alg": alg_bytes_per_token_head(D, io) * B * H * L / (ms / 1e3) / PEAK_HBM,
+        "hbm_frac_alg": alg_bytes_per_token_head(D, io, gb) * B * H * L / (ms / 1e3) / PEAK_HBM,
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM / 1e9,
                      "unit": "GB/s", "frac": achieved * 1e9 / PEAK_HBM, "traffic": traffic},
     }

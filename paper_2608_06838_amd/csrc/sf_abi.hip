@@ -88,8 +88,6 @@ sf_status resolve(const sf_shape *sh, Shape &r) {
     if (sh->chunk != 0 && sh->chunk != 64)
         return fail(SF_E_UNSUPPORTED, "chunk must be 64 (got %d)", sh->chunk);
     if (sh->L % 64 != 0) return fail(SF_E_SHAPE, "L must be a multiple of 64 (got %lld)", (long long)sh->L);
-    if (sh->gate == SF_GATE_VECTOR)
-        return fail(SF_E_UNSUPPORTED, "the vector (per-key-channel) gate is not implemented yet");
     if (sh->io_dtype == SF_F32 && sh->Dk > 64)
         return fail(SF_E_UNSUPPORTED, "fp32 I/O supports Dk <= 64 (got %d)", sh->Dk);
     r.B = sh->B;
@@ -249,11 +247,11 @@ WsLayout ws_layout(const Shape &r, int64_t L, int ts, bool bwd) {
             off += al(bh * n * SS * 4);
         }
         w.Lg = off;
-        off += al(bh * n * 4);
+        off += al(bh * n * (r.gate == SF_GATE_VECTOR ? r.D : 1) * 4);
     }
     if (bwd && n >= 1) {
         w.Dot = off;
-        off += al(bh * n * (SS / 256) * 4);
+        off += al(bh * n * (r.gate == SF_GATE_VECTOR ? (size_t)r.D : SS / 256) * 4);
     }
     w.total = off;
     return w;
@@ -303,6 +301,7 @@ Seg make_seg(const Shape &r, int64_t L, int ts, char *ws, bool bwd) {
     a.sg_h = r.sg_h;
     a.B = r.B;
     a.H = r.H;
+    a.vec = r.gate == SF_GATE_VECTOR ? 1 : 0;
     a.L = L;
     a.ts = ts;
     a.n_super = n_super_of(L, ts);

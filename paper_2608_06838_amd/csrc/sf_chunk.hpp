@@ -1,0 +1,37 @@
+// sf_chunk.hpp -- chunk-walk helpers shared by the scalar-gate and vector-gate
+// kernels: workgroup -> (batch, head, superchunk) decode, causal tile order, exp2.
+#pragma once
+#include "sf_device.hpp"
+#include "sf_launch.hpp"
+
+namespace sf {
+
+// 2^x with the hardware v_exp_f32 (results below 2^-126 flush to zero, which
+// is what a decay that small means here; no input is ever > 0 except on
+// masked-out causal entries, which are discarded by a select)
+__device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// (t-tile, s-tile) pairs of the causal 64x64 score matrix, s-tile <= t-tile.
+__device__ __forceinline__ void tri_tile(int i, int &tt, int &st) {
+    // 0:(0,0) 1:(1,0) 2:(1,1) 3:(2,0) 4:(2,1) 5:(2,2) 6:(3,0) 7:(3,1) 8:(3,2) 9:(3,3)
+    tt = (i >= 1) + (i >= 3) + (i >= 6);
+    st = i - (tt * (tt + 1)) / 2;
+}
+
+struct Decode {
+    int J, bh, b, h, nch;
+    int64_t tok0;
+};
+__device__ __forceinline__ Decode decode(const SegArgs &a) {
+    Decode d;
+    d.J = blockIdx.x % a.n_super;
+    d.bh = blockIdx.x / a.n_super;
+    d.b = d.bh / a.H;
+    d.h = d.bh % a.H;
+    d.tok0 = (int64_t)d.J * a.ts;
+    int64_t rem = a.L - d.tok0;
+    d.nch = (int)((rem < a.ts ? rem : a.ts) / C);
+    return d;
+}
+
+}  // namespace sf

@@ -437,6 +437,9 @@ __device__ __forceinline__ float wave_scan_dpp(float x) {
     x += dpp_or0<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
     return x;
 }
+// x from lane + N of the same 16-lane row, 0 past the row's end (DPP row_shl:N)
+template <int N>
+__device__ __forceinline__ float dpp_row_shl(float x) { return dpp_or0<0x100 + N>(x); }
 __device__ __forceinline__ float lane_value(float x, int l) {
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), l));
 }

@@ -22,21 +22,10 @@
 //   k_bwd_dkv              dk, dv, dg by a reverse walk of the state gradient
 // A segment that fits in one superchunk skips prep and scan: the walkers start
 // from S_in / dS_out directly and produce S_out / dS_in themselves.
-#include "sf_device.hpp"
-#include "sf_launch.hpp"
+#include "sf_chunk.hpp"
 
 namespace sf {
 
-template <typename T, int D>
-struct Cfg {
-    static constexpr int NW = D / 16;        // waves; wave w owns state column tile w
-    static constexpr int NT = 64 * NW;       // threads
-    static constexpr int NK = D / 16;        // 16-row tiles of a D x D state
-    static constexpr int LDN = D + pad<T>(); // natural tile [token][channel] pitch
-    static constexpr int LDT = C + pad<T>(); // transposed tile [row][token] pitch
-    static constexpr bool SP = kSplit<T>;
-    static_assert(NT == 4 * D, "kernels declare __launch_bounds__(4 * D)");
-};
 constexpr int SCAN_NT = 256;
 
 // state column tiles per wave of the prep kernels (forward, backward) and of
@@ -54,34 +43,6 @@ constexpr int SCAN_NT = 256;
 #ifndef SF_NCT_DKV
 #define SF_NCT_DKV 1
 #endif
-
-// 2^x with the hardware v_exp_f32 (results below 2^-126 flush to zero, which
-// is what a decay that small means here; no input is ever > 0 except on
-// masked-out causal entries, which are discarded by a select)
-__device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// (t-tile, s-tile) pairs of the causal 64x64 score matrix, s-tile <= t-tile.
-__device__ __forceinline__ void tri_tile(int i, int &tt, int &st) {
-    // 0:(0,0) 1:(1,0) 2:(1,1) 3:(2,0) 4:(2,1) 5:(2,2) 6:(3,0) 7:(3,1) 8:(3,2) 9:(3,3)
-    tt = (i >= 1) + (i >= 3) + (i >= 6);
-    st = i - (tt * (tt + 1)) / 2;
-}
-
-struct Decode {
-    int J, bh, b, h, nch;
-    int64_t tok0;
-};
-__device__ __forceinline__ Decode decode(const SegArgs &a) {
-    Decode d;
-    d.J = blockIdx.x % a.n_super;
-    d.bh = blockIdx.x / a.n_super;
-    d.b = d.bh / a.H;
-    d.h = d.bh % a.H;
-    d.tok0 = (int64_t)d.J * a.ts;
-    int64_t rem = a.L - d.tok0;
-    d.nch = (int)((rem < a.ts ? rem : a.ts) / C);
-    return d;
-}
 
 // ---------------------------------------------------------------------------
 // Pre: per superchunk, D_J = sum_c (decay after c) (K~_c)^T V_c, and for the
@@ -212,8 +173,11 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 // thread; grid = B*H*(D*D/1024).  Forward: slot J of wsS is replaced by S_J
 // (state entering superchunk J).  Backward additionally walks J downwards:
 // slot J of wsE is replaced by G_{J+1} (gradient of the state leaving J) and
-// the wave partials of <G_{J+1}, S_{J+1}> go to wsDot[(bh, J)][part*4 + wave].
-template <bool BWD>
+// <G_{J+1}, S_{J+1}> goes to wsDot: scalar gate as wave partials at
+// [(bh, J)][part*4 + wave], vector gate (VG) per key row at [(bh, J)][row].
+// VG: the superchunk decay is per key row (wsLg[(bh, J)][row]); a thread's 4
+// elements lie in one row.
+template <bool BWD, bool VG>
 __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int parts = D * D / 1024;
@@ -221,9 +185,11 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
     const int64_t bh = blockIdx.x / parts;
     const int64_t SS = (int64_t)D * D;
     const int64_t e = (int64_t)(part * SCAN_NT + tid) * 4;
+    const int row = (int)(e / D);
     const int n = a.n_super;
     float *Sb = a.wsS + bh * n * SS + e;
-    const float *lg = a.wsLg + bh * n;
+    const int LS = VG ? D : 1;  // wsLg entries per superchunk
+    const float *lg = a.wsLg + bh * n * LS + (VG ? row : 0);
 
     f32x4 S = a.S_in ? *reinterpret_cast<const f32x4 *>(a.S_in + bh * SS + e) : f32x4{0.f, 0.f, 0.f, 0.f};
     for (int J = 0; J < n; J += 4) {
@@ -233,7 +199,7 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
         for (int u = 0; u < 4; ++u)
             if (J + u < n) {
                 dd[u] = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)(J + u) * SS);
-                f[u] = fexp2(lg[J + u]);
+                f[u] = fexp2(lg[(J + u) * LS]);
             }
 #pragma unroll
         for (int u = 0; u < 4; ++u)
@@ -245,7 +211,7 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
     if constexpr (!BWD) {
         if (a.S_out) *reinterpret_cast<f32x4 *>(a.S_out + bh * SS + e) = S;
     } else {
-        const int ndot = D * D / 256;
+        const int ndot = VG ? D : D * D / 256;
         float *Eb = a.wsE + bh * n * SS + e;
         f32x4 G = a.dS_out ? *reinterpret_cast<const f32x4 *>(a.dS_out + bh * SS + e)
                            : f32x4{0.f, 0.f, 0.f, 0.f};
@@ -253,10 +219,16 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
         for (int J = n - 1; J >= 0; --J) {
             const f32x4 E = *reinterpret_cast<const f32x4 *>(Eb + (int64_t)J * SS);
             const f32x4 Sj = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)J * SS);
-            const float f = fexp2(lg[J]);
+            const float f = fexp2(lg[J * LS]);
             float p = G[0] * Sn[0] + G[1] * Sn[1] + G[2] * Sn[2] + G[3] * Sn[3];
-            p = wave_sum(p);
-            if (lane == 0) a.wsDot[(bh * n + J) * ndot + part * 4 + w] = p;
+            if constexpr (!VG) {
+                p = wave_sum(p);
+                if (lane == 0) a.wsDot[(bh * n + J) * ndot + part * 4 + w] = p;
+            } else {
+                // the D/4 threads of one row are consecutive lanes
+                for (int o = D / 8; o >= 1; o >>= 1) p += __shfl_xor(p, o, 64);
+                if ((lane & (D / 4 - 1)) == 0) a.wsDot[(bh * n + J) * ndot + row] = p;
+            }
             *reinterpret_cast<f32x4 *>(Eb + (int64_t)J * SS) = G;
             G = f * G + E;
             Sn = Sj;
@@ -821,10 +793,16 @@ static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s) {
 hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t s) {
     if (kind == SF_K_SCAN) {
         const dim3 grid((unsigned)((int64_t)a.B * a.H * (D * D / 1024)));
-        if (a.wsE) hipLaunchKernelGGL((k_scan<true>), grid, dim3(SCAN_NT), 0, s, a, D);
-        else hipLaunchKernelGGL((k_scan<false>), grid, dim3(SCAN_NT), 0, s, a, D);
+        if (a.vec) {
+            if (a.wsE) hipLaunchKernelGGL((k_scan<true, true>), grid, dim3(SCAN_NT), 0, s, a, D);
+            else hipLaunchKernelGGL((k_scan<false, true>), grid, dim3(SCAN_NT), 0, s, a, D);
+        } else {
+            if (a.wsE) hipLaunchKernelGGL((k_scan<true, false>), grid, dim3(SCAN_NT), 0, s, a, D);
+            else hipLaunchKernelGGL((k_scan<false, false>), grid, dim3(SCAN_NT), 0, s, a, D);
+        }
         return hipGetLastError();
     }
+    if (a.vec) return launch_kernel_vg(kind, io, D, a, s);
     if (io == SF_BF16 && D == 128) return launch_td<__bf16, 128>(kind, a, s);
     if (io == SF_BF16 && D == 64) return launch_td<__bf16, 64>(kind, a, s);
     if (io == SF_F32 && D == 64) return launch_td<float, 64>(kind, a, s);

@@ -17,6 +17,7 @@ struct SegArgs {
     int64_t sx_b, sx_l, sx_h;
     int64_t sg_b, sg_l, sg_h;
     int32_t B, H;
+    int32_t vec;      // 1: per-key-channel gate (g, dg are [B][L][H][D])
     int64_t L;        // tokens in the segment
     int32_t ts;       // superchunk length (multiple of 64)
     int32_t n_super;  // ceil(L / ts)
@@ -26,13 +27,15 @@ struct SegArgs {
     float *dS_in;
     float *wsS;    // [B][H][n_super][D][D]: D_J, replaced by S_J by the scan
     float *wsE;    // [B][H][n_super][D][D]: E_J, replaced by G_{J+1} (backward only)
-    float *wsLg;   // [B][H][n_super]: log2 of the superchunk decay
-    float *wsDot;  // [B][H][n_super][D*D/256]: partials of <G_{J+1}, S_{J+1}>
+    float *wsLg;   // [B][H][n_super] (vector gate: [..][D]): log2 of the superchunk decay
+    float *wsDot;  // [B][H][n_super][D*D/256]: partials of <G_{J+1}, S_{J+1}>;
+                   // vector gate: [B][H][n_super][D], the per-key-row sums
 };
 
 // kind is an sf_kernel_id; io an sf_dtype.  The scan runs its backward form
 // when wsE is set.
 hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t s);
+hipError_t launch_kernel_vg(int kind, int io, int D, const SegArgs &a, hipStream_t s);
 hipError_t launch_state_copy(const float *src, float *dst, int64_t n, hipStream_t s);
 
 }  // namespace sf

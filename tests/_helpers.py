@@ -74,12 +74,16 @@ def oracle_run(inp, pairs=None, snap_pos=None):
 
 
 def dg_floor(ref, q, k):
-    """Scale of the per-token terms q_t.dq_t and k_t.dk_t whose telescoping sum
+    """Scale of the per-token terms q_t.dq_t and k_t.dk_t (per channel for the
+    vector gate) whose telescoping sum
     gives the decay gradient (dg_t = sum_{t'>=t} (q.dq - k.dk)_{t'} plus the
     carry from later superchunks).  The kernels evaluate dg through that sum,
     so its absolute error is relative to this scale; when the gate is so
     strong that dg itself is many orders smaller (a_t ~ 0), this floor keeps
     the metric meaningful."""
-    qd = np.sum(q * ref["dq"], axis=-1)
-    kd = np.sum(k * ref["dk"], axis=-1)
+    if ref["dg"].ndim == q.ndim:  # per-key-channel gate: dg per channel
+        qd, kd = q * ref["dq"], k * ref["dk"]
+    else:
+        qd = np.sum(q * ref["dq"], axis=-1)
+        kd = np.sum(k * ref["dk"], axis=-1)
     return float(np.sqrt(np.mean(qd * qd + kd * kd)))

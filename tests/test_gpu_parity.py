@@ -160,9 +160,46 @@ def test_ctx256k_sampled():
     check_chain("bf16", inp, got, w["seg_lens"], pairs=[(0, 17)])
 
 
-def test_vector_gate_reports_unsupported():
-    w = synth.workload("vector_gate", B=1, H=2)
-    inp = on_gpu(synth.make_inputs(w, device="cpu", seed=3, L=256))
-    with pytest.raises(sf.StateflowError) as e:
-        sf.segment_fwd(inp["q"], inp["k"], inp["v"], inp["g"])
-    assert "SF_E_UNSUPPORTED" in str(e.value)
+# ------------------------------------------------------------------ vector gate
+@pytest.mark.parametrize("D,io", [(128, "bf16"), (64, "bf16"), (64, "f32")])
+@pytest.mark.parametrize("ts", [4096, 128, 64])
+def test_vector_gate_segment(D, io, ts):
+    """Per-key-channel gate, B=2, H=3, L=448 (7 chunks): one superchunk, ragged
+    128-token superchunks, one superchunk per chunk."""
+    w = synth.workload("vector_gate", B=2, H=3, D=D, io=io)
+    inp, got = seg_case(w, 448, ts, seed=31 + D + ts, s_in_std=0.1)
+    check_all(io, got, oracle_run(inp), inp)
+
+
+@pytest.mark.parametrize("g_mu", [-0.5, -30.0])
+def test_vector_gate_decay_regimes(g_mu):
+    """Gates strong enough that some chunks (g_mu = -0.5: a mix) or all chunks
+    (g_mu = -30: memoryless) decay below 2^-100 in some channel and are walked
+    token by token; the rest take the tiled path."""
+    w = synth.workload("vector_gate", B=1, H=2, D=128, g_mu=g_mu)
+    inp, got = seg_case(w, 512, 128, seed=41, s_in_std=0.1)
+    check_all("bf16", got, oracle_run(inp), inp)
+
+
+@pytest.mark.parametrize("ts", [0, 64])
+def test_vector_gate_chain_nonuniform(ts):
+    w = synth.workload("vector_gate", B=1, H=3, D=128)
+    seg_lens = [192, 64, 320, 128]
+    inp = synth.make_inputs(w, device="cpu", seed=43, dS_out_std=0.1, L=sum(seg_lens))
+    g = on_gpu(inp)
+    say(f"[chain] vector gate nonuniform ts={ts}")
+    a = run_chain(g, seg_lens, ts=ts, overlap=True)
+    b = run_chain(g, seg_lens, ts=ts, overlap=False)
+    for key in a:
+        assert torch.equal(a[key], b[key]), key
+    check_chain("bf16", inp, a, seg_lens)
+
+
+def test_vector_gate_workload_sampled():
+    """B=2, H=16, d=128, L=65536 in 16 segments of 4096 with the per-key-channel
+    gate; the oracle checks two (batch, head) pairs end to end."""
+    w = synth.workload("vector_gate")
+    say("[chain] vector_gate full size")
+    inp = synth.make_inputs(w, device=DEV, seed=1003, dS_out_std=0.0)
+    got = run_chain(inp, w["seg_lens"])
+    check_chain("bf16", inp, got, w["seg_lens"], pairs=[(0, 5), (1, 12)])
