@@ -118,6 +118,8 @@ def main():
     ap.add_argument("--no-overlap", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-times", action="store_true", help="print per-kernel times to stderr")
+    ap.add_argument("--overlap-study", action="store_true",
+                    help="also time the chain with the scans on the main stream (no overlap)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -211,6 +213,24 @@ def main():
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM / 1e9,
                      "unit": "GB/s", "frac": achieved * 1e9 / PEAK_HBM, "traffic": traffic},
     }
+    # scan overlap (the fp32 superchunk scans run on a second stream): the chain's
+    # time against the summed times of its other kernels, which is the chain time
+    # with the scans taking no time at all
+    t_other = sum(ktime[k][0] for k in kernels if k != "scan") / args.steps
+    out["overlap"] = {"t_e2e_ms": ms, "t_without_scan_ms": t_other, "t_scan_ms": ktime["scan"][0] / args.steps,
+                      "e2e_over_without_scan": ms / t_other if t_other > 0 else None}
+    if args.overlap_study:
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            sf.chain_fwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, inp["S_in"], ts=args.ts, overlap=False,
+                         out=(o, S_bnd, ws_f))
+            sf.chain_bwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, S_bnd, inp["dO"], inp["dS_out"],
+                         ts=args.ts, overlap=False, out=(dq, dk, dv, dg, dS0, ws_b))
+        torch.cuda.synchronize()
+        t_serial = (time.perf_counter() - t0) * 1e3 / args.steps
+        out["overlap"]["t_serial_ms"] = t_serial
+        out["overlap"]["hidden_frac_of_scan"] = ((t_serial - ms) / out["overlap"]["t_scan_ms"]
+                                                 if out["overlap"]["t_scan_ms"] > 0 else None)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, inp)
     print(json.dumps(out), flush=True)
