@@ -124,6 +124,9 @@ sf_status resolve(const sf_shape *sh, Shape &r) {
         return fail(SF_E_SHAPE, "gate strides make elements overlap");
     if ((r.sx_b * (int64_t)r.esz) % 16 || (r.sx_l * (int64_t)r.esz) % 16 || (r.sx_h * (int64_t)r.esz) % 16)
         return fail(SF_E_ALIGN, "token-tensor strides must be multiples of 16 bytes");
+    // the kernels address a 64-token chunk of a tensor with 32-bit byte offsets
+    if ((63 * r.sx_l + r.D) * (int64_t)r.esz >= (int64_t(1) << 31) || (63 * r.sg_l + gin) * 4 >= (int64_t(1) << 31))
+        return fail(SF_E_SHAPE, "token stride too large: a 64-token chunk must span < 2 GiB");
     return SF_OK;
 }
 

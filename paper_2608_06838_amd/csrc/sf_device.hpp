@@ -130,6 +130,49 @@ __device__ __forceinline__ frag_t<T> scale_frag(const frag_t<T> &f, const float 
     return o;
 }
 
+// Buffer addressing.  A resource (four scalar registers) covers `bytes` bytes
+// from `base`; an access names it plus a 32-bit per-lane byte offset and a
+// uniform (scalar) byte offset, so a tile costs one VGPR per row instead of a
+// 64-bit address, and accesses past `bytes` read zero / are dropped.  The
+// third word 0x00020000 selects raw (unswizzled, untyped) 32-bit addressing.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t buf_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+template <typename V>
+__device__ __forceinline__ V buf_ld(rsrc_t r, uint32_t voff, uint32_t soff) {
+    typedef unsigned u2 __attribute__((ext_vector_type(2)));
+    typedef unsigned u4 __attribute__((ext_vector_type(4)));
+    if constexpr (sizeof(V) == 16) return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+    else if constexpr (sizeof(V) == 8) return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+    else {
+        static_assert(sizeof(V) == 4, "buffer load width");
+        return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+    }
+}
+template <typename V>
+__device__ __forceinline__ void buf_st(rsrc_t r, uint32_t voff, uint32_t soff, const V &v) {
+    typedef unsigned u2 __attribute__((ext_vector_type(2)));
+    typedef unsigned u4 __attribute__((ext_vector_type(4)));
+    if constexpr (sizeof(V) == 16) __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), r, voff, soff, 0);
+    else if constexpr (sizeof(V) == 8) __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u2, v), r, voff, soff, 0);
+    else {
+        static_assert(sizeof(V) == 4, "buffer store width");
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, voff, soff, 0);
+    }
+}
+// 4 consecutive fp32 values stored as T through a buffer resource
+template <typename T>
+__device__ __forceinline__ void st4_buf(rsrc_t r, uint32_t voff, uint32_t soff, const f32x4 &v) {
+    if constexpr (sizeof(T) == 2) buf_st(r, voff, soff, bf16x4{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]});
+    else buf_st(r, voff, soff, v);
+}
+// Bytes spanned by C rows of D elements at row stride `ld` (elements).
+template <typename T, int D>
+__host__ __device__ __forceinline__ uint32_t chunk_span(int64_t ld) {
+    return (uint32_t)(((int64_t)(C - 1) * ld + D) * (int64_t)sizeof(T));
+}
+
 // Store 4 consecutive fp32 values as T (8 bytes for bf16, 16 for fp32).
 __device__ __forceinline__ void st4(__bf16 *p, float a, float b, float c, float d) {
     bf16x4 v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
@@ -246,6 +289,17 @@ struct Tile {
         const T *p = base + (int64_t)row0(tid) * row_stride + cb(tid) * E;
 #pragma unroll
         for (int j = 0; j < RPT; ++j) r[j] = *reinterpret_cast<const vecE *>(p + (int64_t)j * row_stride);
+    }
+    // byte offsets of this thread's rows from a chunk's first token (row stride
+    // in elements); one set serves every tile with that stride
+    __device__ __forceinline__ static void offsets(uint32_t (&o)[RPT], int64_t row_stride, int tid) {
+#pragma unroll
+        for (int j = 0; j < RPT; ++j)
+            o[j] = (uint32_t)(((int64_t)((tid / CB) * RPT + j) * row_stride + (tid % CB) * E) * (int64_t)sizeof(T));
+    }
+    __device__ __forceinline__ void load_buf(rsrc_t rs, const uint32_t (&o)[RPT], uint32_t soff) {
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) r[j] = buf_ld<vecE>(rs, o[j], soff);
     }
     // natural layout [token][channel] (channels permuted by nat_pos), row pitch ld
     __device__ __forceinline__ void store_nat(T *lds, int ld, int tid) const {

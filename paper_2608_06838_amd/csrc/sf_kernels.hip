@@ -309,20 +309,30 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     Tile<T, D, NT> t1, t2, t3;
     float gl;
     vec4T qn[DQ ? NCT * 4 : 1];  // DQ: q values of this lane's dq elements
+    // chunk c of a token tensor is a buffer resource over its C rows: tile rows
+    // at per-lane 32-bit offsets, accumulator rows (token 16tt + n16, channels
+    // c0 + 4q4..) at a per-lane offset plus the uniform offset of token tile tt
+    const int64_t cstep = (int64_t)C * a.sx_l;
+    const uint32_t cspan = chunk_span<T, D>(a.sx_l), gspan = (uint32_t)(((C - 1) * a.sg_l + 1) * 4);
+    uint32_t toff[Tile<T, D, NT>::RPT];
+    Tile<T, D, NT>::offsets(toff, a.sx_l, tid);
+    const uint32_t goff = (uint32_t)(lane * a.sg_l * 4);
+    const uint32_t aoff = (uint32_t)((n16 * a.sx_l + 16 * NCT * w + 4 * q4) * (int64_t)sizeof(T));
+    const uint32_t tstep = (uint32_t)(16 * a.sx_l * (int64_t)sizeof(T));
     auto issue = [&](int c) {
-        const int64_t nx = (int64_t)c * C * a.sx_l;
-        t1.load(X1 + nx, a.sx_l, tid);
-        t2.load(X2 + nx, a.sx_l, tid);
-        t3.load(X3 + nx, a.sx_l, tid);
-        gl = gp[(c * C + lane) * a.sg_l];
+        const int64_t nx = c * cstep;
+        t1.load_buf(buf_rsrc(X1 + nx, cspan), toff, 0);
+        t2.load_buf(buf_rsrc(X2 + nx, cspan), toff, 0);
+        t3.load_buf(buf_rsrc(X3 + nx, cspan), toff, 0);
+        gl = buf_ld<float>(buf_rsrc(gp + (int64_t)c * C * a.sg_l, gspan), goff, 0);
     };
     auto issue_q = [&](int c) {  // DQ: q at this lane's dq elements, read after chunk c-1's dot
+        const rsrc_t rq = buf_rsrc(Qd + c * cstep, cspan);
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
-                qn[4 * ct + tt] = *reinterpret_cast<const vec4T *>(
-                    Qd + (int64_t)(c * C + 16 * tt + n16) * a.sx_l + 16 * (NCT * w + ct) + 4 * q4);
+                qn[4 * ct + tt] = buf_ld<vec4T>(rq, aoff + 16 * ct * (uint32_t)sizeof(T), tt * tstep);
     };
     issue(0);
     if constexpr (DQ) issue_q(0);
@@ -401,10 +411,10 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
                     if constexpr (SP) mma(O[tt], vf[ct][ks], ldfrag(sAl, LDT, 16 * tt, 32 * ks, lane));
                 }
             }
+            const rsrc_t ry = buf_rsrc(Y + c * cstep, cspan);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
-                const int64_t trow = (int64_t)(c * C + 16 * tt + n16) * a.sx_l;
-                st4(Y + trow + c0 + 4 * q4, O[tt][0], O[tt][1], O[tt][2], O[tt][3]);
+                st4_buf<T>(ry, aoff + 16 * ct * (uint32_t)sizeof(T), tt * tstep, O[tt]);
                 if constexpr (DQ) {
                     const vec4T qv = qn[4 * ct + tt];
                     part[tt] += O[tt][0] * tof<T>(qv[0]) + O[tt][1] * tof<T>(qv[1]) + O[tt][2] * tof<T>(qv[2]) +
@@ -421,6 +431,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
                 if (q4 == 0) sred[w * C + 16 * tt + n16] = part[tt];
             }
         }
+        // keep the output stores ahead of the state update: loads and stores share
+        // one counter, so the wait for the next tiles also waits for these stores
+        sched_fence();
 
         // state update S = exp2(b63) S + X2^T (exp2(b63 - b) o X3)
         const float gam = fexp2(b63);
