@@ -258,8 +258,12 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     __shared__ __attribute__((aligned(16))) T sX1[C * LDN];
     __shared__ __attribute__((aligned(16))) T sX2[C * LDN];
     __shared__ __attribute__((aligned(16))) T sX3[C * LDN];
-    __shared__ __attribute__((aligned(16))) T sA[C * LDT];    // A[t][s] (hi)
-    __shared__ __attribute__((aligned(16))) T sAl[SP ? C * LDT : 8];
+    // A[t][s] hi/lo; between chunks the same bytes stage the previous chunk's
+    // output tile [token][channel] for row-contiguous global stores
+    constexpr int AB = (SP ? 2 : 1) * C * LDT * (int)sizeof(T), YB = C * LDN * (int)sizeof(T);
+    __shared__ __attribute__((aligned(16))) char sAraw[AB > YB ? AB : YB];
+    T *const sA = reinterpret_cast<T *>(sAraw), *const sAl = SP ? sA + C * LDT : sA;
+    T *const sY = reinterpret_cast<T *>(sAraw);
     __shared__ __attribute__((aligned(16))) float sb[C];   // b_t (log2, chunk-local)
     __shared__ __attribute__((aligned(16))) float sq[C];   // exp2(b_t)
     __shared__ __attribute__((aligned(16))) float se[C];   // exp2(b63 - b_t)
@@ -297,14 +301,6 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
                 S[ct][i] = *reinterpret_cast<const f32x4 *>(src + (int64_t)col * D + row);
             }
         }
-    // A tiles read by the A.V product but above the diagonal stay zero
-    for (int e = tid; e < 512; e += NT) {
-        const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
-        const int idx = tile ? (32 + rr) * LDT + 48 + cc : rr * LDT + 16 + cc;
-        sA[idx] = cvt<T>(0.f);
-        if constexpr (SP) sAl[idx] = cvt<T>(0.f);
-    }
-
     typedef T vec4T __attribute__((ext_vector_type(4)));
     Tile<T, D, NT> t1, t2, t3;
     float gl;
@@ -334,6 +330,24 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             for (int tt = 0; tt < 4; ++tt)
                 qn[4 * ct + tt] = buf_ld<vec4T>(rq, aoff + 16 * ct * (uint32_t)sizeof(T), tt * tstep);
     };
+    vec4T yo[NCT][4];  // this lane's outputs of the chunk, accumulator layout
+    // a chunk's outputs go registers -> LDS tile (once every wave is done with the
+    // score tiles) -> whole-row 16-byte global stores early in the next chunk
+    auto put_y = [&]() {
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt)
+                *reinterpret_cast<vec4T *>(&sY[(16 * tt + n16) * LDN + 16 * (NCT * w + ct) + 4 * q4]) = yo[ct][tt];
+    };
+    auto store_y = [&](int cp) {
+        typedef typename Tile<T, D, NT>::vecE vecE;
+        constexpr int E = Tile<T, D, NT>::E, CB = Tile<T, D, NT>::CB, RPT = Tile<T, D, NT>::RPT;
+        const int r0 = (tid / CB) * RPT, ch = (tid % CB) * E;
+        const rsrc_t ry = buf_rsrc(Y + cp * cstep, cspan);
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) buf_st(ry, toff[j], 0, *reinterpret_cast<const vecE *>(&sY[(r0 + j) * LDN + ch]));
+    };
     issue(0);
     if constexpr (DQ) issue_q(0);
 
@@ -357,6 +371,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         t1.store_nat(sX1, LDN, tid);
         t2.store_swz(sX2, LDN, tid, SWX);
         t3.store_swz(sX3, LDN, tid, SWX);
+        // previous outputs out before the next loads: the wait for those loads
+        // (one counter for loads and stores) then also covers these stores
+        if (c > 0) store_y(c - 1);
         if (c + 1 < d.nch) issue(c + 1);
         __syncthreads();
 
@@ -381,47 +398,72 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             const int o = t * LDT + 16 * st + 4 * q4;
             st4_split<T, SP>(&sA[o], &sAl[SP ? o : 0], v4);
         }
+        // A tiles read by the A.V product but above the diagonal are zero (written
+        // every chunk: the same bytes staged the previous outputs)
+        for (int e = tid; e < 512; e += NT) {
+            const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
+            const int idx = tile ? (32 + rr) * LDT + 48 + cc : rr * LDT + 16 + cc;
+            sA[idx] = cvt<T>(0.f);
+            if constexpr (SP) sAl[idx] = cvt<T>(0.f);
+        }
         __syncthreads();
 
         // Y^T[col][t] = exp2(b_t) sum_m S[m][col] X1[t][m] + sum_s X3[s][col] A[t][s]
-        frag_t<T> vf[NCT][C / 32];
         float part[4] = {0.f, 0.f, 0.f, 0.f};
+        // both column tiles per loaded row fragment: each X1 / A fragment is read
+        // once and feeds NCT accumulators
+        f32x4 O[NCT][4];
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) {
-            const int c0 = 16 * (NCT * w + ct);
-            f32x4 O[4];
+        for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-            for (int tt = 0; tt < 4; ++tt) O[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int tt = 0; tt < 4; ++tt) O[ct][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int ks = 0; ks < D / 32; ++ks) {
-                frag_t<T> fh, fl;
-                split_acc<T, SPS>(S[ct][2 * ks], S[ct][2 * ks + 1], fh, fl);
+        for (int ks = 0; ks < D / 32; ++ks) {
+            frag_t<T> fh[NCT], fl[NCT];
 #pragma unroll
-                for (int tt = 0; tt < 4; ++tt) mma2<T, SPS>(O[tt], fh, fl, ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane));
-            }
-#pragma unroll
-            for (int tt = 0; tt < 4; ++tt) O[tt] *= sq[16 * tt + n16];
-#pragma unroll
-            for (int ks = 0; ks < C / 32; ++ks) {
-                vf[ct][ks] = ldfragTR<T, LDN, SWX>(sX3, tro, 32 * ks, c0);
-#pragma unroll
-                for (int tt = 0; tt < 4; ++tt) {
-                    if (32 * ks > 16 * tt + 15) continue;
-                    mma(O[tt], vf[ct][ks], ldfrag(sA, LDT, 16 * tt, 32 * ks, lane));
-                    if constexpr (SP) mma(O[tt], vf[ct][ks], ldfrag(sAl, LDT, 16 * tt, 32 * ks, lane));
-                }
-            }
-            const rsrc_t ry = buf_rsrc(Y + c * cstep, cspan);
+            for (int ct = 0; ct < NCT; ++ct) split_acc<T, SPS>(S[ct][2 * ks], S[ct][2 * ks + 1], fh[ct], fl[ct]);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
-                st4_buf<T>(ry, aoff + 16 * ct * (uint32_t)sizeof(T), tt * tstep, O[tt]);
-                if constexpr (DQ) {
-                    const vec4T qv = qn[4 * ct + tt];
-                    part[tt] += O[tt][0] * tof<T>(qv[0]) + O[tt][1] * tof<T>(qv[1]) + O[tt][2] * tof<T>(qv[2]) +
-                                O[tt][3] * tof<T>(qv[3]);
+                const frag_t<T> xf = ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) mma2<T, SPS>(O[ct][tt], fh[ct], fl[ct], xf);
+            }
+        }
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) {
+            const float sqt = sq[16 * tt + n16];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) O[ct][tt] *= sqt;
+        }
+#pragma unroll
+        for (int ks = 0; ks < C / 32; ++ks) {
+            frag_t<T> vf[NCT];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) vf[ct] = ldfragTR<T, LDN, SWX>(sX3, tro, 32 * ks, 16 * (NCT * w + ct));
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) {
+                if (32 * ks > 16 * tt + 15) continue;
+                const frag_t<T> ah = ldfrag(sA, LDT, 16 * tt, 32 * ks, lane);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) mma(O[ct][tt], vf[ct], ah);
+                if constexpr (SP) {
+                    const frag_t<T> al = ldfrag(sAl, LDT, 16 * tt, 32 * ks, lane);
+#pragma unroll
+                    for (int ct = 0; ct < NCT; ++ct) mma(O[ct][tt], vf[ct], al);
                 }
             }
         }
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) {
+                yo[ct][tt] = pack4<T>(O[ct][tt]);
+                if constexpr (DQ) {
+                    const vec4T qv = qn[4 * ct + tt];
+                    part[tt] += O[ct][tt][0] * tof<T>(qv[0]) + O[ct][tt][1] * tof<T>(qv[1]) +
+                                O[ct][tt][2] * tof<T>(qv[2]) + O[ct][tt][3] * tof<T>(qv[3]);
+                }
+            }
         if constexpr (DQ) {
             if (c + 1 < d.nch) issue_q(c + 1);
 #pragma unroll
@@ -431,8 +473,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
                 if (q4 == 0) sred[w * C + 16 * tt + n16] = part[tt];
             }
         }
-        // keep the output stores ahead of the state update: loads and stores share
-        // one counter, so the wait for the next tiles also waits for these stores
+        sched_fence();
+        __syncthreads();  // every wave is done with the score tiles
+        put_y();
         sched_fence();
 
         // state update S = exp2(b63) S + X2^T (exp2(b63 - b) o X3)
@@ -449,7 +492,8 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             const float ev[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
             frag_t<T> vh[NCT], vl[NCT];
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) split_scaled<T, SPD>(vf[ct][ks], ev, vh[ct], vl[ct]);
+            for (int ct = 0; ct < NCT; ++ct)
+                split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sX3, tro, 32 * ks, 16 * (NCT * w + ct)), ev, vh[ct], vl[ct]);
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
                 const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sX2, tro, 32 * ks, 16 * i);
@@ -457,6 +501,10 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
                 for (int ct = 0; ct < NCT; ++ct) mma2b<T, SPD>(S[ct][i], kf, vh[ct], vl[ct]);
             }
         }
+    }
+    if (d.nch > 0) {
+        __syncthreads();
+        store_y(d.nch - 1);
     }
     if constexpr (DQ) {
         __syncthreads();
