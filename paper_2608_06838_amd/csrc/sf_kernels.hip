@@ -636,14 +636,22 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
 
     Tile<T, D, NT> tq, tk, tv, to;
     float gl, rn;
+    // chunk c of a tensor is a buffer resource over its C rows (see k_walk)
+    const int64_t cstep = (int64_t)C * a.sx_l;
+    const uint32_t cspan = chunk_span<T, D>(a.sx_l), gspan = (uint32_t)(((C - 1) * a.sg_l + 1) * 4);
+    uint32_t toff[Tile<T, D, NT>::RPT];
+    Tile<T, D, NT>::offsets(toff, a.sx_l, tid);
+    const uint32_t goff = (uint32_t)(lane * a.sg_l * 4);
+    const uint32_t tstep = (uint32_t)(16 * a.sx_l * (int64_t)sizeof(T));
     auto issue = [&](int c) {
-        const int64_t nx = (int64_t)c * C * a.sx_l;
-        tq.load(Q + nx, a.sx_l, tid);
-        tk.load(K + nx, a.sx_l, tid);
-        tv.load(V + nx, a.sx_l, tid);
-        to.load(dO + nx, a.sx_l, tid);
-        gl = gp[(c * C + lane) * a.sg_l];
-        rn = dgp[(c * C + lane) * a.sg_l];  // q.dq left in dg by the dq walk
+        const int64_t nx = c * cstep;
+        tq.load_buf(buf_rsrc(Q + nx, cspan), toff, 0);
+        tk.load_buf(buf_rsrc(K + nx, cspan), toff, 0);
+        tv.load_buf(buf_rsrc(V + nx, cspan), toff, 0);
+        to.load_buf(buf_rsrc(dO + nx, cspan), toff, 0);
+        const int64_t ng = (int64_t)c * C * a.sg_l;
+        gl = buf_ld<float>(buf_rsrc(gp + ng, gspan), goff, 0);
+        rn = buf_ld<float>(buf_rsrc(dgp + ng, gspan), goff, 0);  // q.dq left in dg by the dq walk
     };
     issue(d.nch - 1);
     float rprev = 0.f;  // wave 0: q.dq of the chunk whose dg is still pending
@@ -704,7 +712,6 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
         }
         __syncthreads();
 
-        const int64_t crow = (int64_t)c * C;
         float kdp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
@@ -760,12 +767,14 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
                         mma(DK[st], qfk, dl);
                     }
                 }
+            const rsrc_t rk = buf_rsrc(dK + c * cstep, cspan), rv = buf_rsrc(dV + c * cstep, cspan);
+            const uint32_t voff = (uint32_t)((n16 * a.sx_l + c0 + 4 * q4) * (int64_t)sizeof(T));
 #pragma unroll
             for (int st = 0; st < 4; ++st) {
                 const int s = 16 * st + n16;
                 const int col = c0 + 4 * q4;
-                st4(dV + (crow + s) * a.sx_l + col, DV[st][0], DV[st][1], DV[st][2], DV[st][3]);
-                st4(dK + (crow + s) * a.sx_l + col, DK[st][0], DK[st][1], DK[st][2], DK[st][3]);
+                st4_buf<T>(rv, voff, st * tstep, DV[st]);
+                st4_buf<T>(rk, voff, st * tstep, DK[st]);
                 const f32x4 kv = ld4f(&sK[s * LDN + nat_pos(col)]);
                 kdp[st] += DK[st][0] * kv[0] + DK[st][1] * kv[1] + DK[st][2] * kv[2] + DK[st][3] * kv[3];
             }
