@@ -643,17 +643,24 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
     Tile<T, D, NT>::offsets(toff, a.sx_l, tid);
     const uint32_t goff = (uint32_t)(lane * a.sg_l * 4);
     const uint32_t tstep = (uint32_t)(16 * a.sx_l * (int64_t)sizeof(T));
+    // the next chunk's loads go out in two batches (q, dO, g at staging; k, v at
+    // the start of the dv/dk products) so the vector-memory queue drains behind
+    // compute instead of stalling every wave at one point
+    auto issue_kv = [&](int c) {
+        const int64_t nx = c * cstep;
+        tk.load_buf(buf_rsrc(K + nx, cspan), toff, 0);
+        tv.load_buf(buf_rsrc(V + nx, cspan), toff, 0);
+    };
     auto issue = [&](int c) {
         const int64_t nx = c * cstep;
         tq.load_buf(buf_rsrc(Q + nx, cspan), toff, 0);
-        tk.load_buf(buf_rsrc(K + nx, cspan), toff, 0);
-        tv.load_buf(buf_rsrc(V + nx, cspan), toff, 0);
         to.load_buf(buf_rsrc(dO + nx, cspan), toff, 0);
         const int64_t ng = (int64_t)c * C * a.sg_l;
         gl = buf_ld<float>(buf_rsrc(gp + ng, gspan), goff, 0);
         rn = buf_ld<float>(buf_rsrc(dgp + ng, gspan), goff, 0);  // q.dq left in dg by the dq walk
     };
     issue(d.nch - 1);
+    issue_kv(d.nch - 1);
     float rprev = 0.f;  // wave 0: q.dq of the chunk whose dg is still pending
 
     // dg of chunk cp from the k.dk partials in sred (wave 0)
@@ -712,6 +719,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
         }
         __syncthreads();
 
+        if (c > 0) issue_kv(c - 1);
         float kdp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
