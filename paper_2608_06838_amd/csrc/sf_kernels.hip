@@ -643,9 +643,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
     Tile<T, D, NT>::offsets(toff, a.sx_l, tid);
     const uint32_t goff = (uint32_t)(lane * a.sg_l * 4);
     const uint32_t tstep = (uint32_t)(16 * a.sx_l * (int64_t)sizeof(T));
-    // the next chunk's loads go out in two batches (q, dO, g at staging; k, v at
-    // the start of the dv/dk products) so the vector-memory queue drains behind
-    // compute instead of stalling every wave at one point
+    // the next chunk's loads go out in two batches (q, dO, g at the start of the
+    // score tiles; k, v at the start of the dv/dk products) so the vector-memory
+    // queue drains behind compute instead of stalling every wave at one point
     auto issue_kv = [&](int c) {
         const int64_t nx = c * cstep;
         tk.load_buf(buf_rsrc(K + nx, cspan), toff, 0);
@@ -682,15 +682,17 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
         to.store_swz(sO, LDN, tid, SWX);
         tk.store_nat(sK, LDN, tid);
         tv.store_nat(sV, LDN, tid);
-        if (c > 0) issue(c - 1);
         if (w == 0) {
             if (c < d.nch - 1) finish_dg(c + 1);
             rprev = rc;
+        }
+        if (w == NW - 1) {  // the decay tables, from another wave than the dg finish
             sb[lane] = b2;
             se[lane] = fexp2(b63 - b2);
             sq[lane] = fexp2(b2);
         }
         __syncthreads();
+        if (c > 0) issue(c - 1);
 
         // A^T and dA^T on the causal tiles: P[t][s] = sum X[t][ch] Y[s][ch]
         for (int i = w; i < 20; i += NW) {
