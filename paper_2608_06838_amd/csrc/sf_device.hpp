@@ -232,6 +232,28 @@ __device__ __forceinline__ void split_acc(const f32x4 &a0, const f32x4 &a1, frag
     float x[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
     split8<T, SP>(x, hi, lo);
 }
+// The same fragment in plain channel order: lane row q receives channels
+// 8q .. 8q+7 of the 32-channel block instead of {4q..4q+3, 16+4q..16+4q+3}.
+// A 32-lane swap (rows 2,3 of the first tile with rows 0,1 of the second)
+// then a 16-lane swap (odd rows of the first with even rows of the second)
+// put A_{2r}, A_{2r+1} (or B_{2r-4}, B_{2r-3}) in lane row r, so such a
+// fragment contracts with a tile stored in plain channel order.
+__device__ __forceinline__ void acc_pair_to_plain(float (&x)[8]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        unsigned a = __builtin_bit_cast(unsigned, x[j]), b = __builtin_bit_cast(unsigned, x[4 + j]);
+        const auto s32 = __builtin_amdgcn_permlane32_swap(a, b, false, false);
+        const auto s16 = __builtin_amdgcn_permlane16_swap(s32[0], s32[1], false, false);
+        x[j] = __builtin_bit_cast(float, (unsigned)s16[0]);
+        x[4 + j] = __builtin_bit_cast(float, (unsigned)s16[1]);
+    }
+}
+template <typename T, bool SP = kSplit<T>>
+__device__ __forceinline__ void split_acc_plain(const f32x4 &a0, const f32x4 &a1, frag_t<T> &hi, frag_t<T> &lo) {
+    float x[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+    acc_pair_to_plain(x);
+    split8<T, SP>(x, hi, lo);
+}
 // split fragment of a T fragment scaled per slot by s[] (fp32)
 template <typename T, bool SP = kSplit<T>>
 __device__ __forceinline__ void split_scaled(const frag_t<T> &f, const float *s, frag_t<T> &hi, frag_t<T> &lo) {

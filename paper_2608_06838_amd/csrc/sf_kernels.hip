@@ -244,12 +244,16 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
 //                       and r_t = q_t . dq_t into dg (read back by k_bwd_dkv).
 // Wave w owns NCT state column tiles.  The state lives as MFMA accumulators:
 // row tile i of lane l holds rows 16i+4*(l/16)+r of column c0+l%16, which is an
-// A-operand fragment of the transposed state (split_acc), so X1 S needs no LDS
-// round trip for S.  LDS holds the three input tiles in natural [token][channel]
-// layout only: X1 in nat_pos channel order (the order of an accumulator pair),
+// A-operand fragment of the transposed state once two lane-row swaps put its
+// channels in plain order (split_acc_plain), so X1 S needs no LDS round trip
+// for S.  LDS holds the three input tiles in natural [token][channel] layout
+// only: X1 plain and unswizzled (whole 16-byte fragment reads, conflict-free),
 // X2 and X3 plain and swizzled for the transposing loads that feed the state
 // update (X2^T, the exact shared operand) and the value side (X3^T, decayed per
 // token and split hi/lo in registers by the wave that owns those columns).
+// The score tiles XOR their 16-byte blocks by bit 2 of the row and the output
+// staging tile uses a 16-byte-odd pitch: both halve the bank conflicts of the
+// 8-byte accumulator-row writes.
 template <typename T, int D, int NCT, bool DQ>
 __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_walk(SegArgs a) {
     constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
@@ -260,10 +264,11 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     __shared__ __attribute__((aligned(16))) T sX3[C * LDN];
     // A[t][s] hi/lo; between chunks the same bytes stage the previous chunk's
     // output tile [token][channel] for row-contiguous global stores
-    constexpr int AB = (SP ? 2 : 1) * C * LDT * (int)sizeof(T), YB = C * LDN * (int)sizeof(T);
+    constexpr int AB = (SP ? 2 : 1) * C * LDT * (int)sizeof(T), YB = C * (D + 16 / (int)sizeof(T)) * (int)sizeof(T);
     __shared__ __attribute__((aligned(16))) char sAraw[AB > YB ? AB : YB];
     T *const sA = reinterpret_cast<T *>(sAraw), *const sAl = SP ? sA + C * LDT : sA;
     T *const sY = reinterpret_cast<T *>(sAraw);
+    constexpr int LDY = D + 16 / (int)sizeof(T);
     __shared__ __attribute__((aligned(16))) float sb[C];   // b_t (log2, chunk-local)
     __shared__ __attribute__((aligned(16))) float sq[C];   // exp2(b_t)
     __shared__ __attribute__((aligned(16))) float se[C];   // exp2(b63 - b_t)
@@ -338,7 +343,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
-                *reinterpret_cast<vec4T *>(&sY[(16 * tt + n16) * LDN + 16 * (NCT * w + ct) + 4 * q4]) = yo[ct][tt];
+                *reinterpret_cast<vec4T *>(&sY[(16 * tt + n16) * LDY + 16 * (NCT * w + ct) + 4 * q4]) = yo[ct][tt];
     };
     auto store_y = [&](int cp) {
         typedef typename Tile<T, D, NT>::vecE vecE;
@@ -346,7 +351,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         const int r0 = (tid / CB) * RPT, ch = (tid % CB) * E;
         const rsrc_t ry = buf_rsrc(Y + cp * cstep, cspan);
 #pragma unroll
-        for (int j = 0; j < RPT; ++j) buf_st(ry, toff[j], 0, *reinterpret_cast<const vecE *>(&sY[(r0 + j) * LDN + ch]));
+        for (int j = 0; j < RPT; ++j) buf_st(ry, toff[j], 0, *reinterpret_cast<const vecE *>(&sY[(r0 + j) * LDY + ch]));
     };
     issue(0);
     if constexpr (DQ) issue_q(0);
@@ -368,7 +373,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             sq[lane] = fexp2(b2);
             se[lane] = fexp2(b63 - b2);
         }
-        t1.store_nat(sX1, LDN, tid);
+        t1.store_swz(sX1, LDN, tid, 0);
         t2.store_swz(sX2, LDN, tid, SWX);
         t3.store_swz(sX3, LDN, tid, SWX);
         // previous outputs out before the next loads: the wait for those loads
@@ -385,7 +390,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks)
                 mma(p, ldfrag_swz<T, LDN, SWX>(sX2, swo, 16 * st, 32 * ks),
-                    ldfrag_unperm<T>(sX1, LDN, 16 * tt, 32 * ks, lane));
+                    ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane));
             const int t = 16 * tt + n16;
             const float bt = sb[t];
             const f32x4 bs = *reinterpret_cast<const f32x4 *>(&sb[16 * st + 4 * q4]);
@@ -395,14 +400,14 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
                 const int s = 16 * st + 4 * q4 + r;
                 v4[r] = s <= t ? p[r] * fexp2(bt - bs[r]) : 0.f;
             }
-            const int o = t * LDT + 16 * st + 4 * q4;
+            const int o = t * LDT + ((16 * st + 4 * q4) ^ (sizeof(T) == 2 ? 8 * ((t >> 2) & 1) : 0));
             st4_split<T, SP>(&sA[o], &sAl[SP ? o : 0], v4);
         }
         // A tiles read by the A.V product but above the diagonal are zero (written
         // every chunk: the same bytes staged the previous outputs)
         for (int e = tid; e < 512; e += NT) {
             const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
-            const int idx = tile ? (32 + rr) * LDT + 48 + cc : rr * LDT + 16 + cc;
+            const int idx = (tile ? (32 + rr) * LDT : rr * LDT) + ((tile ? 48 + cc : 16 + cc) ^ (sizeof(T) == 2 ? 8 * ((rr >> 2) & 1) : 0));
             sA[idx] = cvt<T>(0.f);
             if constexpr (SP) sAl[idx] = cvt<T>(0.f);
         }
@@ -421,7 +426,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         for (int ks = 0; ks < D / 32; ++ks) {
             frag_t<T> fh[NCT], fl[NCT];
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) split_acc<T, SPS>(S[ct][2 * ks], S[ct][2 * ks + 1], fh[ct], fl[ct]);
+            for (int ct = 0; ct < NCT; ++ct) split_acc_plain<T, SPS>(S[ct][2 * ks], S[ct][2 * ks + 1], fh[ct], fl[ct]);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
                 const frag_t<T> xf = ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane);
@@ -443,11 +448,12 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
                 if (32 * ks > 16 * tt + 15) continue;
-                const frag_t<T> ah = ldfrag(sA, LDT, 16 * tt, 32 * ks, lane);
+                const int aw = sizeof(T) == 2 ? 8 * ((lane >> 2) & 1) : 0;
+                const frag_t<T> ah = *reinterpret_cast<const frag_t<T> *>(sA + (16 * tt + (lane & 15)) * LDT + ((32 * ks + 8 * (lane >> 4)) ^ aw));
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) mma(O[ct][tt], vf[ct], ah);
                 if constexpr (SP) {
-                    const frag_t<T> al = ldfrag(sAl, LDT, 16 * tt, 32 * ks, lane);
+                    const frag_t<T> al = *reinterpret_cast<const frag_t<T> *>(sAl + (16 * tt + (lane & 15)) * LDT + ((32 * ks + 8 * (lane >> 4)) ^ aw));
 #pragma unroll
                     for (int ct = 0; ct < NCT; ++ct) mma(O[ct][tt], vf[ct], al);
                 }
@@ -561,10 +567,10 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 //   G   <- exp(b_63) G + Q^T (exp(b) o dO)          (and its transpose)
 //   dg_t = sum_{t' >= t in superchunk} (q.dq - k.dk)_{t'} + <G_{J+1}, S_{J+1}>
 // (the last term is the decay gradient carried in from later superchunks).
-// LDS holds natural tiles only: K and V in nat_pos channel order (they meet the
-// accumulator-built G fragments), Q and dO plain and swizzled for the
-// transposing loads of the G updates, where the per-token decay goes on the
-// wave's own columns.
+// LDS holds natural tiles only: K and V plain and unswizzled (they meet the
+// accumulator-built G fragments, reordered by split_acc_plain), Q and dO plain
+// and swizzled for the transposing loads of the G updates, where the per-token
+// decay goes on the wave's own columns.
 template <typename T, int D, int NCT>
 __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
     constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
@@ -572,8 +578,8 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
     constexpr bool SP = kSplitScores<T>, SPS = kSplitState<T>, SPD = kSplitDecay<T>;
     __shared__ __attribute__((aligned(16))) T sQ[C * LDN];   // plain, swizzled
     __shared__ __attribute__((aligned(16))) T sO[C * LDN];   // dO, plain, swizzled
-    __shared__ __attribute__((aligned(16))) T sK[C * LDN];   // nat_pos order
-    __shared__ __attribute__((aligned(16))) T sV[C * LDN];   // nat_pos order
+    __shared__ __attribute__((aligned(16))) T sK[C * LDN];   // plain
+    __shared__ __attribute__((aligned(16))) T sV[C * LDN];   // plain
     __shared__ __attribute__((aligned(16))) T sAT[C * LDT];  // A^T[s][t] (hi)
     __shared__ __attribute__((aligned(16))) T sATl[SP ? C * LDT : 8];
     __shared__ __attribute__((aligned(16))) T sdAT[C * LDT]; // dA^T[s][t] (hi)
@@ -680,8 +686,8 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
         __syncthreads();
         tq.store_swz(sQ, LDN, tid, SWX);
         to.store_swz(sO, LDN, tid, SWX);
-        tk.store_nat(sK, LDN, tid);
-        tv.store_nat(sV, LDN, tid);
+        tk.store_swz(sK, LDN, tid, 0);
+        tv.store_swz(sV, LDN, tid, 0);
         if (w == 0) {
             if (c < d.nch - 1) finish_dg(c + 1);
             rprev = rc;
@@ -705,7 +711,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks)
                 mma(p, ldfrag_swz<T, LDN, SWX>(X, swo, 16 * tt, 32 * ks),
-                    ldfrag_unperm<T>(Yt, LDN, 16 * st, 32 * ks, lane));
+                    ldfrag(Yt, LDN, 16 * st, 32 * ks, lane));
             const int s = 16 * st + n16;
             const float bs = sb[s];
             const f32x4 bt = *reinterpret_cast<const f32x4 *>(&sb[16 * tt + 4 * q4]);
@@ -740,8 +746,8 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
                 }
                 sched_fence();  // keep the fragment reads ahead of the split below
                 frag_t<T> gh, gl, th, tl;
-                split_acc<T, SPS>(G[ct][2 * ks], G[ct][2 * ks + 1], gh, gl);
-                split_acc<T, SPS>(GT[ct][2 * ks], GT[ct][2 * ks + 1], th, tl);
+                split_acc_plain<T, SPS>(G[ct][2 * ks], G[ct][2 * ks + 1], gh, gl);
+                split_acc_plain<T, SPS>(GT[ct][2 * ks], GT[ct][2 * ks + 1], th, tl);
                 sched_fence();
 #pragma unroll
                 for (int st = 0; st < 4; ++st) {
@@ -785,7 +791,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
                 const int col = c0 + 4 * q4;
                 st4_buf<T>(rv, voff, st * tstep, DV[st]);
                 st4_buf<T>(rk, voff, st * tstep, DK[st]);
-                const f32x4 kv = ld4f(&sK[s * LDN + nat_pos(col)]);
+                const f32x4 kv = ld4f(&sK[s * LDN + col]);
                 kdp[st] += DK[st][0] * kv[0] + DK[st][1] * kv[1] + DK[st][2] * kv[2] + DK[st][3] * kv[3];
             }
         }
