@@ -320,13 +320,16 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     const uint32_t goff = (uint32_t)(lane * a.sg_l * 4);
     const uint32_t aoff = (uint32_t)((n16 * a.sx_l + 16 * NCT * w + 4 * q4) * (int64_t)sizeof(T));
     const uint32_t tstep = (uint32_t)(16 * a.sx_l * (int64_t)sizeof(T));
-    auto issue = [&](int c) {
-        const int64_t nx = c * cstep;
-        t1.load_buf(buf_rsrc(X1 + nx, cspan), toff, 0);
-        t2.load_buf(buf_rsrc(X2 + nx, cspan), toff, 0);
-        t3.load_buf(buf_rsrc(X3 + nx, cspan), toff, 0);
+    // the next chunk's tiles go out in three batches (X1 and g at staging, X2 at
+    // the start of the scores, X3 at the start of the output products), so the
+    // vector-memory queue drains behind compute instead of stalling every wave
+    // at one point
+    auto issue1 = [&](int c) {
+        t1.load_buf(buf_rsrc(X1 + c * cstep, cspan), toff, 0);
         gl = buf_ld<float>(buf_rsrc(gp + (int64_t)c * C * a.sg_l, gspan), goff, 0);
     };
+    auto issue2 = [&](int c) { t2.load_buf(buf_rsrc(X2 + c * cstep, cspan), toff, 0); };
+    auto issue3 = [&](int c) { t3.load_buf(buf_rsrc(X3 + c * cstep, cspan), toff, 0); };
     auto issue_q = [&](int c) {  // DQ: q at this lane's dq elements, read after chunk c-1's dot
         const rsrc_t rq = buf_rsrc(Qd + c * cstep, cspan);
 #pragma unroll
@@ -353,7 +356,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 #pragma unroll
         for (int j = 0; j < RPT; ++j) buf_st(ry, toff[j], 0, *reinterpret_cast<const vecE *>(&sY[(r0 + j) * LDY + ch]));
     };
-    issue(0);
+    issue1(0);
+    issue2(0);
+    issue3(0);
     if constexpr (DQ) issue_q(0);
 
     for (int c = 0; c < d.nch; ++c) {
@@ -379,8 +384,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         // previous outputs out before the next loads: the wait for those loads
         // (one counter for loads and stores) then also covers these stores
         if (c > 0) store_y(c - 1);
-        if (c + 1 < d.nch) issue(c + 1);
+        if (c + 1 < d.nch) issue1(c + 1);
         __syncthreads();
+        if (c + 1 < d.nch) issue2(c + 1);
 
         // scores P^T[s][t] = sum_ch X2[s][ch] X1[t][ch] on the causal tiles -> A[t][s]
         for (int i = w; i < 10; i += NW) {
@@ -412,6 +418,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             if constexpr (SP) sAl[idx] = cvt<T>(0.f);
         }
         __syncthreads();
+        if (c + 1 < d.nch) issue3(c + 1);
 
         // Y^T[col][t] = exp2(b_t) sum_m S[m][col] X1[t][m] + sum_s X3[s][col] A[t][s]
         float part[4] = {0.f, 0.f, 0.f, 0.f};
