@@ -485,6 +485,17 @@ __device__ __forceinline__ frag_t<T> ldfrag_unperm(const T *M, int ld, int row0,
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
+// x summed over the four 16-lane rows of the wave (lanes l, l^16, l^32, l^48),
+// returned in every lane: a 32-lane and a 16-lane swap, no LDS round trip.
+__device__ __forceinline__ float sum_rows(float x) {
+    const unsigned u = __builtin_bit_cast(unsigned, x);
+    const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    const float y = __builtin_bit_cast(float, (unsigned)a[0]) + __builtin_bit_cast(float, (unsigned)a[1]);
+    const unsigned v = __builtin_bit_cast(unsigned, y);
+    const auto b = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return __builtin_bit_cast(float, (unsigned)b[0]) + __builtin_bit_cast(float, (unsigned)b[1]);
+}
+
 // Compiler scheduling fence: no instruction moves across it.  Used to keep a
 // batch of LDS fragment reads ahead of independent VALU work, so that their
 // latency overlaps that work instead of stalling the MFMA that consumes them.

@@ -481,8 +481,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             if (c + 1 < d.nch) issue_q(c + 1);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
-                part[tt] += __shfl_xor(part[tt], 16, 64);
-                part[tt] += __shfl_xor(part[tt], 32, 64);
+                part[tt] = sum_rows(part[tt]);
                 if (q4 == 0) sred[w * C + 16 * tt + n16] = part[tt];
             }
         }
@@ -598,6 +597,12 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
     const Decode d = decode(a);
+    // score tiles XOR their 16-byte blocks by bit 2 of the row (bf16): the 8-byte
+    // accumulator-row writes then spread over twice the banks
+    auto asw = [](int row) { return sizeof(T) == 2 ? 8 * ((row >> 2) & 1) : 0; };
+    auto ldfrag_a = [&](const T *M, int row0, int k0) {
+        return *reinterpret_cast<const frag_t<T> *>(M + (row0 + n16) * LDT + ((k0 + 8 * q4) ^ asw(n16)));
+    };
     const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *Q = (const T *)a.q + xo;
@@ -638,7 +643,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
     // score tiles read by the dv/dk products but above the diagonal stay zero
     for (int e = tid; e < 512; e += NT) {
         const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
-        const int idx = tile ? (48 + rr) * LDT + 32 + cc : (16 + rr) * LDT + cc;
+        const int idx = (tile ? (48 + rr) * LDT : (16 + rr) * LDT) + ((tile ? 32 + cc : cc) ^ asw(rr));
         sAT[idx] = cvt<T>(0.f);
         sdAT[idx] = cvt<T>(0.f);
         if constexpr (SP) {
@@ -728,7 +733,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
                 const int t = 16 * tt + 4 * q4 + r;
                 v4[r] = s <= t ? p[r] * fexp2(bt[r] - bs) : 0.f;
             }
-            const int o = s * LDT + 16 * tt + 4 * q4;
+            const int o = s * LDT + ((16 * tt + 4 * q4) ^ asw(s));
             if (isdA) st4_split<T, SP>(&sdAT[o], &sdATl[SP ? o : 0], v4);
             else st4_split<T, SP>(&sAT[o], &sATl[SP ? o : 0], v4);
         }
@@ -770,26 +775,47 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
                 DV[st] *= f;
                 DK[st] *= f;
             }
-            // intra-chunk parts: dv^T += dO^T A^T, dk^T += Q^T dA^T (A^T, dA^T zero above the diagonal)
-#pragma unroll
-            for (int st = 0; st < 4; ++st)
-#pragma unroll
-                for (int ks = st / 2; ks < C / 32; ++ks) {
-                    const frag_t<T> ah = ldfrag(sAT, LDT, 16 * st, 32 * ks, lane);
-                    const frag_t<T> dh = ldfrag(sdAT, LDT, 16 * st, 32 * ks, lane);
-                    frag_t<T> al, dl;
-                    if constexpr (SP) {
-                        al = ldfrag(sATl, LDT, 16 * st, 32 * ks, lane);
-                        dl = ldfrag(sdATl, LDT, 16 * st, 32 * ks, lane);
-                    }
-                    const frag_t<T> &ofk = ks ? of1 : of0, &qfk = ks ? qf1 : qf0;
-                    mma(DV[st], ofk, ah);
-                    mma(DK[st], qfk, dh);
-                    if constexpr (SP) {
-                        mma(DV[st], ofk, al);
-                        mma(DK[st], qfk, dl);
-                    }
+            // intra-chunk parts: dv^T += dO^T A^T, dk^T += Q^T dA^T (A^T, dA^T zero above
+            // the diagonal) over the (st, ks) pairs (0,0) (0,1) (1,0) (1,1) (2,1) (3,1),
+            // each pair's fragments read two pairs ahead of its products
+            struct AF {
+                frag_t<T> ah, dh, al, dl;
+            };
+            auto ld_pair = [&](int st, int ks, AF &f) {
+                f.ah = ldfrag_a(sAT, 16 * st, 32 * ks);
+                f.dh = ldfrag_a(sdAT, 16 * st, 32 * ks);
+                if constexpr (SP) {
+                    f.al = ldfrag_a(sATl, 16 * st, 32 * ks);
+                    f.dl = ldfrag_a(sdATl, 16 * st, 32 * ks);
                 }
+            };
+            auto mma_pair = [&](int st, int ks, const AF &f) {
+                const frag_t<T> &ofk = ks ? of1 : of0, &qfk = ks ? qf1 : qf0;
+                mma(DV[st], ofk, f.ah);
+                mma(DK[st], qfk, f.dh);
+                if constexpr (SP) {
+                    mma(DV[st], ofk, f.al);
+                    mma(DK[st], qfk, f.dl);
+                }
+            };
+            AF f0, f1;
+            ld_pair(0, 0, f0);
+            ld_pair(0, 1, f1);
+            sched_fence();
+            mma_pair(0, 0, f0);
+            ld_pair(1, 0, f0);
+            sched_fence();
+            mma_pair(0, 1, f1);
+            ld_pair(1, 1, f1);
+            sched_fence();
+            mma_pair(1, 0, f0);
+            ld_pair(2, 1, f0);
+            sched_fence();
+            mma_pair(1, 1, f1);
+            ld_pair(3, 1, f1);
+            sched_fence();
+            mma_pair(2, 1, f0);
+            mma_pair(3, 1, f1);
             const rsrc_t rk = buf_rsrc(dK + c * cstep, cspan), rv = buf_rsrc(dV + c * cstep, cspan);
             const uint32_t voff = (uint32_t)((n16 * a.sx_l + c0 + 4 * q4) * (int64_t)sizeof(T));
 #pragma unroll
@@ -804,8 +830,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
         }
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
-            kdp[st] += __shfl_xor(kdp[st], 16, 64);
-            kdp[st] += __shfl_xor(kdp[st], 32, 64);
+            kdp[st] = sum_rows(kdp[st]);
             if (q4 == 0) sred[w * C + 16 * st + n16] = kdp[st];
         }
 

@@ -452,8 +452,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_walk_vg(SegArgs a) {
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
                     float p = part[ct];
-                    p += __shfl_xor(p, 16, 64);
-                    p += __shfl_xor(p, 32, 64);
+                    p = sum_rows(p);
                     if (q4 == 0) Y[tok * a.sx_l + 16 * (NCT * w + ct) + n16] = cvt<T>(p);
                 }
             }
@@ -684,8 +683,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dq_vg(SegArgs a) {
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
                     float p = part[ct];
-                    p += __shfl_xor(p, 16, 64);
-                    p += __shfl_xor(p, 32, 64);
+                    p = sum_rows(p);
                     if (q4 == 0) {
                         const int col = 16 * (NCT * w + ct) + n16;
                         dQ[tok * a.sx_l + col] = cvt<T>(p);
@@ -710,8 +708,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dq_vg(SegArgs a) {
                     p += x[0] * S[ct][i][0] + x[1] * S[ct][i][1] + x[2] * S[ct][i][2] + x[3] * S[ct][i][3];
                 }
             }
-            p += __shfl_xor(p, 16, 64);
-            p += __shfl_xor(p, 32, 64);
+            p = sum_rows(p);
             if (q4 == 0) dot[col] = p;
         }
     }
@@ -927,8 +924,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dv_vg(SegArgs a) {
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
                     float p = part[ct];
-                    p += __shfl_xor(p, 16, 64);
-                    p += __shfl_xor(p, 32, 64);
+                    p = sum_rows(p);
                     if (q4 == 0) dV[tok * a.sx_l + 16 * (NCT * w + ct) + n16] = cvt<T>(p);
                 }
             }
@@ -1214,8 +1210,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dk_vg(SegArgs a) {
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
                     float p = part[ct];
-                    p += __shfl_xor(p, 16, 64);
-                    p += __shfl_xor(p, 32, 64);  // dk_t[col], every lane of the column
+                    p = sum_rows(p);  // dk_t[col], every lane of the column
                     const int col = 16 * (NCT * w + ct) + n16;
                     acc[ct] += dgp[tok * a.sg_l + col] - kk[ct] * p;  // + r_t - k_t dk_t
                     if (q4 == 0) {
