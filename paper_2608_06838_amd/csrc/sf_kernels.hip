@@ -40,9 +40,6 @@ constexpr int SCAN_NT = 256;
 #ifndef SF_NCT_WALK
 #define SF_NCT_WALK 2
 #endif
-#ifndef SF_NCT_DKV
-#define SF_NCT_DKV 1
-#endif
 
 // ---------------------------------------------------------------------------
 // Pre: per superchunk, D_J = sum_c (decay after c) (K~_c)^T V_c, and for the
@@ -565,21 +562,26 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 
 // ---------------------------------------------------------------------------
 // PG: reverse walk over the chunks of a superchunk with the state gradient G
-// (dLoss/dS of the state leaving the chunk) in registers, in both
-// orientations: G[k][v] (wave w owns v-tiles) feeds dv, G^T[v][k] (wave w owns
-// k-tiles) feeds dk, so neither needs G through LDS:
+// (dLoss/dS of the state leaving the chunk) in registers:
 //   dv^T = exp(b_63 - b_s) G^T K^T + dO^T A^T      (A from Q K^T)
 //   dk^T = exp(b_63 - b_s) G V^T   + Q^T dA^T      (dA from dO V^T)
 //   G   <- exp(b_63) G + Q^T (exp(b) o dO)          (and its transpose)
 //   dg_t = sum_{t' >= t in superchunk} (q.dq - k.dk)_{t'} + <G_{J+1}, S_{J+1}>
 // (the last term is the decay gradient carried in from later superchunks).
-// LDS holds natural tiles only: K and V plain and unswizzled (they meet the
-// accumulator-built G fragments, reordered by split_acc_plain), Q and dO plain
-// and swizzled for the transposing loads of the G updates, where the per-token
-// decay goes on the wave's own columns.
-template <typename T, int D, int NCT>
-__global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
-    constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
+// The workgroup has two halves of D/16 waves.  Wave j of the v-side half keeps
+// G[k][v] for v-tile j (an A-operand fragment for dv) and computes dv; wave j
+// of the k-side half keeps G^T[v][k] for k-tile j and computes dk and k.dk.
+// Each half updates only its own orientation, so per wave the products, the
+// hi/lo splits and the registers are half of a both-orientations walk, and the
+// four waves per SIMD (d = 128) hide each other's latency.  The v-side half
+// stages q and dO, the k-side half k and v.  LDS holds natural tiles only: K
+// and V plain and unswizzled (they meet the accumulator-built G fragments,
+// reordered by split_acc_plain), Q and dO plain and swizzled for the
+// transposing loads of the G updates, where the per-token decay goes on the
+// wave's own columns.
+template <typename T, int D>
+__global__ void __launch_bounds__(128 * D / 16) k_bwd_dkv(SegArgs a) {
+    constexpr int NJ = D / 16, NW = 2 * NJ, NT = 64 * NW, NH = NT / 2, NK = D / 16;
     constexpr int LDN = D + pad<T>(), LDT = C + pad<T>(), SWX = swx<T, D>();
     constexpr bool SP = kSplitScores<T>, SPS = kSplitState<T>, SPD = kSplitDecay<T>;
     __shared__ __attribute__((aligned(16))) T sQ[C * LDN];   // plain, swizzled
@@ -593,9 +595,14 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
     __shared__ __attribute__((aligned(16))) float sb[C];   // b_t (log2, chunk-local)
     __shared__ __attribute__((aligned(16))) float se[C];   // exp2(b63 - b_s)
     __shared__ __attribute__((aligned(16))) float sq[C];   // exp2(b_t)
-    __shared__ float sred[NW * C];
+    __shared__ float sred[NJ * C];
 
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
+    // the wave index through readfirstlane: the compiler then keeps the role and
+    // every role-selected pointer in scalar registers
+    const int tid = threadIdx.x, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const bool kside = w >= NJ;
+    const int j = kside ? w - NJ : w, c0 = 16 * j, htid = kside ? tid - NH : tid;
     const Decode d = decode(a);
     // score tiles XOR their 16-byte blocks by bit 2 of the row (bf16): the 8-byte
     // accumulator-row writes then spread over twice the banks
@@ -609,30 +616,33 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
     const T *K = (const T *)a.k + xo;
     const T *V = (const T *)a.v + xo;
     const T *dO = (const T *)a.dO + xo;
-    T *dK = (T *)a.dk + xo;
-    T *dV = (T *)a.dv + xo;
+    T *Out = (T *)(kside ? a.dk : a.dv) + xo;
     const int64_t go = d.b * a.sg_b + d.h * a.sg_h + d.tok0 * a.sg_l;
     const float *gp = a.g + go;
     float *dgp = a.dg + go;
     const int64_t SS = (int64_t)D * D;
     const int ndot = D * D / 256;
+    // role operands: the B side of the decayed-state product, the own-column
+    // transposed tile of the intra-chunk product and of the G update, the score
+    // tile, and the shared operand of the G update
+    const T *Xs = kside ? sV : sK;
+    const T *Own = kside ? sQ : sO;
+    const T *Oth = kside ? sO : sQ;
+    const T *At = kside ? sdAT : sAT;
+    const T *Atl = kside ? sdATl : sATl;
 
     const float *gsrc = a.n_super == 1 ? (a.dS_out ? a.dS_out + d.bh * SS : nullptr)
                                        : a.wsE + ((int64_t)d.bh * a.n_super + d.J) * SS;
-    f32x4 G[NCT][NK], GT[NCT][NK];  // G[k][v] (v-tiles) and G^T[v][k] (k-tiles)
+    f32x4 G[NK];  // v-side: G[k][v] rows 16i.. of v-tile j; k-side: G^T[v][k] rows of k-tile j
 #pragma unroll
-    for (int ct = 0; ct < NCT; ++ct) {
-        const int c0 = 16 * (NCT * w + ct);
+    for (int i = 0; i < NK; ++i) {
+        if (!gsrc) {
+            G[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        } else if (!kside) {
 #pragma unroll
-        for (int i = 0; i < NK; ++i) {
-            if (!gsrc) {
-                G[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-                GT[ct][i] = G[ct][i];
-            } else {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) G[ct][i][r] = gsrc[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16];
-                GT[ct][i] = *reinterpret_cast<const f32x4 *>(gsrc + (int64_t)(c0 + n16) * D + 16 * i + 4 * q4);
-            }
+            for (int r = 0; r < 4; ++r) G[i][r] = gsrc[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16];
+        } else {
+            G[i] = *reinterpret_cast<const f32x4 *>(gsrc + (int64_t)(c0 + n16) * D + 16 * i + 4 * q4);
         }
     }
     float carry = 0.f;  // wave 0: decay gradient carried in from later tokens
@@ -652,40 +662,36 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
         }
     }
 
-    Tile<T, D, NT> tq, tk, tv, to;
+    // each half loads two tiles (v-side q, dO; k-side k, v) one chunk ahead
+    using HT = Tile<T, D, NH>;
+    HT t1, t2;
     float gl, rn;
-    // chunk c of a tensor is a buffer resource over its C rows (see k_walk)
     const int64_t cstep = (int64_t)C * a.sx_l;
     const uint32_t cspan = chunk_span<T, D>(a.sx_l), gspan = (uint32_t)(((C - 1) * a.sg_l + 1) * 4);
-    uint32_t toff[Tile<T, D, NT>::RPT];
-    Tile<T, D, NT>::offsets(toff, a.sx_l, tid);
+    uint32_t toff[HT::RPT];
+    HT::offsets(toff, a.sx_l, htid);
     const uint32_t goff = (uint32_t)(lane * a.sg_l * 4);
     const uint32_t tstep = (uint32_t)(16 * a.sx_l * (int64_t)sizeof(T));
-    // the next chunk's loads go out in two batches (q, dO, g at the start of the
-    // score tiles; k, v at the start of the dv/dk products) so the vector-memory
-    // queue drains behind compute instead of stalling every wave at one point
-    auto issue_kv = [&](int c) {
-        const int64_t nx = c * cstep;
-        tk.load_buf(buf_rsrc(K + nx, cspan), toff, 0);
-        tv.load_buf(buf_rsrc(V + nx, cspan), toff, 0);
-    };
+    const T *L1 = kside ? K : Q, *L2 = kside ? V : dO;
     auto issue = [&](int c) {
         const int64_t nx = c * cstep;
-        tq.load_buf(buf_rsrc(Q + nx, cspan), toff, 0);
-        to.load_buf(buf_rsrc(dO + nx, cspan), toff, 0);
+        t1.load_buf(buf_rsrc(L1 + nx, cspan), toff, 0);
+        t2.load_buf(buf_rsrc(L2 + nx, cspan), toff, 0);
+    };
+    auto issue_g = [&](int c) {
         const int64_t ng = (int64_t)c * C * a.sg_l;
         gl = buf_ld<float>(buf_rsrc(gp + ng, gspan), goff, 0);
         rn = buf_ld<float>(buf_rsrc(dgp + ng, gspan), goff, 0);  // q.dq left in dg by the dq walk
     };
+    issue_g(d.nch - 1);
     issue(d.nch - 1);
-    issue_kv(d.nch - 1);
     float rprev = 0.f;  // wave 0: q.dq of the chunk whose dg is still pending
 
     // dg of chunk cp from the k.dk partials in sred (wave 0)
     auto finish_dg = [&](int cp) {
         float kd = 0.f;
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) kd += sred[ww * C + lane];
+        for (int jj = 0; jj < NJ; ++jj) kd += sred[jj * C + lane];
         const float suf = wave_incl_suffix(rprev - kd, lane);
         dgp[((int64_t)cp * C + lane) * a.sg_l] = carry + suf;
         carry += lane_value(suf, 0);
@@ -696,10 +702,13 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
         const float b63 = lane_value(b2, 63);
         const float rc = rn;
         __syncthreads();
-        tq.store_swz(sQ, LDN, tid, SWX);
-        to.store_swz(sO, LDN, tid, SWX);
-        tk.store_swz(sK, LDN, tid, 0);
-        tv.store_swz(sV, LDN, tid, 0);
+        if (!kside) {
+            t1.store_swz(sQ, LDN, htid, SWX);
+            t2.store_swz(sO, LDN, htid, SWX);
+        } else {
+            t1.store_swz(sK, LDN, htid, 0);
+            t2.store_swz(sV, LDN, htid, 0);
+        }
         if (w == 0) {
             if (c < d.nch - 1) finish_dg(c + 1);
             rprev = rc;
@@ -709,12 +718,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
             se[lane] = fexp2(b63 - b2);
             sq[lane] = fexp2(b2);
         }
+        if (c > 0) issue_g(c - 1);
         __syncthreads();
-        // Waves w and w + NW/2 share a SIMD and the issue arbiter favours the
-        // older one; raising the younger half during the scores and the dv/dk
-        // products lets the pair finish those phases together (measured 2%).
-        if (w >= NW / 2) __builtin_amdgcn_s_setprio(2);
-        if (c > 0) issue(c - 1);
+        if (c > 0 && !kside) issue(c - 1);
 
         // A^T and dA^T on the causal tiles: P[t][s] = sum X[t][ch] Y[s][ch]
         for (int i = w; i < 20; i += NW) {
@@ -726,8 +732,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
             f32x4 p = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < D / 32; ++ks)
-                mma(p, ldfrag_swz<T, LDN, SWX>(X, swo, 16 * tt, 32 * ks),
-                    ldfrag(Yt, LDN, 16 * st, 32 * ks, lane));
+                mma(p, ldfrag_swz<T, LDN, SWX>(X, swo, 16 * tt, 32 * ks), ldfrag(Yt, LDN, 16 * st, 32 * ks, lane));
             const int s = 16 * st + n16;
             const float bs = sb[s];
             const f32x4 bt = *reinterpret_cast<const f32x4 *>(&sb[16 * tt + 4 * q4]);
@@ -742,68 +747,47 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
             else st4_split<T, SP>(&sAT[o], &sATl[SP ? o : 0], v4);
         }
         __syncthreads();
-        __builtin_amdgcn_s_setprio(0);
+        if (c > 0 && kside) issue(c - 1);
+        // the arbiter favours older waves, so the k-side half (younger, with the
+        // k.dk dots on top) finished the products last; it runs them at raised
+        // priority (the step measured 0.8% faster, the walk 7%)
+        if (kside) __builtin_amdgcn_s_setprio(2);
 
-        if (c > 0) issue_kv(c - 1);
-        if (w >= NW / 2) __builtin_amdgcn_s_setprio(2);
-        float kdp[4] = {0.f, 0.f, 0.f, 0.f};
+        // decayed state part: out^T[col][s] += G^T X^T over the wave's 16 columns
+        f32x4 DX[4];
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) {
-            const int c0 = 16 * (NCT * w + ct);
-            // decayed state parts: dv^T[v][s] += G^T K^T, dk^T[k][s] += G V^T (v, k in this tile)
-            f32x4 DV[4], DK[4];
+        for (int st = 0; st < 4; ++st) DX[st] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int st = 0; st < 4; ++st) DV[st] = DK[st] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int ks = 0; ks < D / 32; ++ks) {
+            frag_t<T> xfr[4];
 #pragma unroll
-            for (int ks = 0; ks < D / 32; ++ks) {
-                frag_t<T> kfr[4], vfr[4];
+            for (int st = 0; st < 4; ++st) xfr[st] = ldfrag(Xs, LDN, 16 * st, 32 * ks, lane);
+            sched_fence();  // keep the fragment reads ahead of the split below
+            frag_t<T> gh, glo;
+            split_acc_plain<T, SPS>(G[2 * ks], G[2 * ks + 1], gh, glo);
+            sched_fence();
 #pragma unroll
-                for (int st = 0; st < 4; ++st) {
-                    kfr[st] = ldfrag(sK, LDN, 16 * st, 32 * ks, lane);
-                    vfr[st] = ldfrag(sV, LDN, 16 * st, 32 * ks, lane);
-                }
-                sched_fence();  // keep the fragment reads ahead of the split below
-                frag_t<T> gh, gl, th, tl;
-                split_acc_plain<T, SPS>(G[ct][2 * ks], G[ct][2 * ks + 1], gh, gl);
-                split_acc_plain<T, SPS>(GT[ct][2 * ks], GT[ct][2 * ks + 1], th, tl);
-                sched_fence();
+            for (int st = 0; st < 4; ++st) mma2<T, SPS>(DX[st], gh, glo, xfr[st]);
+        }
+        const frag_t<T> of0 = ldfragTR<T, LDN, SWX>(Own, tro, 0, c0), of1 = ldfragTR<T, LDN, SWX>(Own, tro, 32, c0);
 #pragma unroll
-                for (int st = 0; st < 4; ++st) {
-                    mma2<T, SPS>(DV[st], gh, gl, kfr[st]);
-                    mma2<T, SPS>(DK[st], th, tl, vfr[st]);
-                }
-            }
-            const frag_t<T> of0 = ldfragTR<T, LDN, SWX>(sO, tro, 0, c0), of1 = ldfragTR<T, LDN, SWX>(sO, tro, 32, c0);
-            const frag_t<T> qf0 = ldfragTR<T, LDN, SWX>(sQ, tro, 0, c0), qf1 = ldfragTR<T, LDN, SWX>(sQ, tro, 32, c0);
-#pragma unroll
-            for (int st = 0; st < 4; ++st) {
-                const float f = se[16 * st + n16];
-                DV[st] *= f;
-                DK[st] *= f;
-            }
-            // intra-chunk parts: dv^T += dO^T A^T, dk^T += Q^T dA^T (A^T, dA^T zero above
-            // the diagonal) over the (st, ks) pairs (0,0) (0,1) (1,0) (1,1) (2,1) (3,1),
-            // each pair's fragments read two pairs ahead of its products
-            struct AF {
-                frag_t<T> ah, dh, al, dl;
-            };
-            auto ld_pair = [&](int st, int ks, AF &f) {
-                f.ah = ldfrag_a(sAT, 16 * st, 32 * ks);
-                f.dh = ldfrag_a(sdAT, 16 * st, 32 * ks);
-                if constexpr (SP) {
-                    f.al = ldfrag_a(sATl, 16 * st, 32 * ks);
-                    f.dl = ldfrag_a(sdATl, 16 * st, 32 * ks);
-                }
-            };
-            auto mma_pair = [&](int st, int ks, const AF &f) {
-                const frag_t<T> &ofk = ks ? of1 : of0, &qfk = ks ? qf1 : qf0;
-                mma(DV[st], ofk, f.ah);
-                mma(DK[st], qfk, f.dh);
-                if constexpr (SP) {
-                    mma(DV[st], ofk, f.al);
-                    mma(DK[st], qfk, f.dl);
-                }
-            };
+        for (int st = 0; st < 4; ++st) DX[st] *= se[16 * st + n16];
+        // intra-chunk part: dv^T += dO^T A^T (v side), dk^T += Q^T dA^T (k side), score
+        // tiles zero above the diagonal, over the (st, ks) pairs (0,0) (0,1) (1,0)
+        // (1,1) (2,1) (3,1), each pair's fragments read two pairs ahead of its products
+        struct AF {
+            frag_t<T> h, l;
+        };
+        auto ld_pair = [&](int st, int ks, AF &f) {
+            f.h = ldfrag_a(At, 16 * st, 32 * ks);
+            if constexpr (SP) f.l = ldfrag_a(Atl, 16 * st, 32 * ks);
+        };
+        auto mma_pair = [&](int st, int ks, const AF &f) {
+            const frag_t<T> &ofk = ks ? of1 : of0;
+            mma(DX[st], ofk, f.h);
+            if constexpr (SP) mma(DX[st], ofk, f.l);
+        };
+        {
             AF f0, f1;
             ld_pair(0, 0, f0);
             ld_pair(0, 1, f1);
@@ -822,70 +806,46 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
             sched_fence();
             mma_pair(2, 1, f0);
             mma_pair(3, 1, f1);
-            const rsrc_t rk = buf_rsrc(dK + c * cstep, cspan), rv = buf_rsrc(dV + c * cstep, cspan);
-            const uint32_t voff = (uint32_t)((n16 * a.sx_l + c0 + 4 * q4) * (int64_t)sizeof(T));
+        }
+        const rsrc_t ro = buf_rsrc(Out + c * cstep, cspan);
+        const uint32_t voff = (uint32_t)((n16 * a.sx_l + c0 + 4 * q4) * (int64_t)sizeof(T));
+#pragma unroll
+        for (int st = 0; st < 4; ++st) st4_buf<T>(ro, voff, st * tstep, DX[st]);
+        if (kside) {  // k.dk partials of this wave's 16 channels
 #pragma unroll
             for (int st = 0; st < 4; ++st) {
-                const int s = 16 * st + n16;
-                const int col = c0 + 4 * q4;
-                st4_buf<T>(rv, voff, st * tstep, DV[st]);
-                st4_buf<T>(rk, voff, st * tstep, DK[st]);
-                const f32x4 kv = ld4f(&sK[s * LDN + col]);
-                kdp[st] += DK[st][0] * kv[0] + DK[st][1] * kv[1] + DK[st][2] * kv[2] + DK[st][3] * kv[3];
+                const f32x4 kv = ld4f(&sK[(16 * st + n16) * LDN + c0 + 4 * q4]);
+                float kd = DX[st][0] * kv[0] + DX[st][1] * kv[1] + DX[st][2] * kv[2] + DX[st][3] * kv[3];
+                kd = sum_rows(kd);
+                if (q4 == 0) sred[j * C + 16 * st + n16] = kd;
             }
-        }
-#pragma unroll
-        for (int st = 0; st < 4; ++st) {
-            kdp[st] = sum_rows(kdp[st]);
-            if (q4 == 0) sred[w * C + 16 * st + n16] = kdp[st];
         }
 
-        if (w >= NW / 2) __builtin_amdgcn_s_setprio(0);
-        // G <- exp2(b63) G + Q^T (exp2(b) o dO), G^T <- exp2(b63) G^T + dO^T (exp2(b) o Q)
+        __builtin_amdgcn_s_setprio(0);
+        // G <- exp2(b63) G + Q^T (exp2(b) o dO) (v side), G^T <- exp2(b63) G^T + dO^T (exp2(b) o Q) (k side)
         const float gam = fexp2(b63);
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-            for (int i = 0; i < NK; ++i) {
-                G[ct][i] *= gam;
-                GT[ct][i] *= gam;
-            }
+        for (int i = 0; i < NK; ++i) G[i] *= gam;
 #pragma unroll
         for (int ks = 0; ks < C / 32; ++ks) {
             const int t0 = 32 * ks + 8 * q4;
             const f32x4 e0 = *reinterpret_cast<const f32x4 *>(&sq[t0]);
             const f32x4 e1 = *reinterpret_cast<const f32x4 *>(&sq[t0 + 4]);
             const float ev[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
-            frag_t<T> oh[NCT], ol[NCT], qh[NCT], ql[NCT];
+            frag_t<T> oh, ol;
+            split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(Own, tro, 32 * ks, c0), ev, oh, ol);
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) {
-                const int c0 = 16 * (NCT * w + ct);
-                split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sO, tro, 32 * ks, c0), ev, oh[ct], ol[ct]);
-                split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sQ, tro, 32 * ks, c0), ev, qh[ct], ql[ct]);
-            }
-#pragma unroll
-            for (int i = 0; i < NK; ++i) {
-                const frag_t<T> qa = ldfragTR<T, LDN, SWX>(sQ, tro, 32 * ks, 16 * i);
-                const frag_t<T> oa = ldfragTR<T, LDN, SWX>(sO, tro, 32 * ks, 16 * i);
-#pragma unroll
-                for (int ct = 0; ct < NCT; ++ct) {
-                    mma2b<T, SPD>(G[ct][i], qa, oh[ct], ol[ct]);
-                    mma2b<T, SPD>(GT[ct][i], oa, qh[ct], ql[ct]);
-                }
-            }
+            for (int i = 0; i < NK; ++i) mma2b<T, SPD>(G[i], ldfragTR<T, LDN, SWX>(Oth, tro, 32 * ks, 16 * i), oh, ol);
         }
     }
     __syncthreads();
     if (w == 0 && d.nch > 0) finish_dg(0);
-    if (a.n_super == 1 && a.dS_in) {
+    if (a.n_super == 1 && a.dS_in && !kside) {
         float *dst = a.dS_in + d.bh * SS;
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct)
+        for (int i = 0; i < NK; ++i)
 #pragma unroll
-            for (int i = 0; i < NK; ++i)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    dst[(int64_t)(16 * i + 4 * q4 + r) * D + 16 * (NCT * w + ct) + n16] = G[ct][i][r];
+            for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = G[i][r];
     }
 }
 
@@ -908,7 +868,7 @@ static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s) {
     case SF_K_BWD_PREP: hipLaunchKernelGGL((k_prep<T, D, SF_NCT_PREPB, true>), grid, dim3(NTB), 0, s, a); break;
     case SF_K_BWD_DQ: hipLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, true>), grid, dim3(NTW), 0, s, a); break;
     case SF_K_BWD_DKV:
-        hipLaunchKernelGGL((k_bwd_dkv<T, D, SF_NCT_DKV>), grid, dim3(64 * D / (16 * SF_NCT_DKV)), 0, s, a);
+        hipLaunchKernelGGL((k_bwd_dkv<T, D>), grid, dim3(128 * D / 16), 0, s, a);
         break;
     default: return hipErrorInvalidValue;
     }
