@@ -305,6 +305,7 @@ Seg make_seg(const Shape &r, int64_t L, int ts, char *ws, bool bwd) {
     a.B = r.B;
     a.H = r.H;
     a.vec = r.gate == SF_GATE_VECTOR ? 1 : 0;
+    a.n_cu = device_cus();
     a.L = L;
     a.ts = ts;
     a.n_super = n_super_of(L, ts);

@@ -18,6 +18,18 @@ __device__ __forceinline__ void tri_tile(int i, int &tt, int &st) {
     st = i - (tt * (tt + 1)) / 2;
 }
 
+// Two workgroups that share a CU progress at different rates: the issue
+// arbiter favours older waves, so the workgroup dispatched first finished its
+// superchunk ~25% ahead of its partner (per-workgroup timestamps), and the CU
+// then ran the partner alone.  Workgroups of alternate dispatch rounds take
+// turns at raised priority, in epochs of 2^12 real-time ticks (41 us at the
+// 100 MHz counter), so both members of a pair progress together.
+__device__ __forceinline__ unsigned pair_parity(int n_cu) { return ((int)blockIdx.x / (n_cu > 0 ? n_cu : 1)) & 1; }
+__device__ __forceinline__ void pair_turn(unsigned parity) {
+    if ((((unsigned)(__builtin_amdgcn_s_memrealtime() >> 12)) ^ parity) & 1) __builtin_amdgcn_s_setprio(1);
+    else __builtin_amdgcn_s_setprio(0);
+}
+
 struct Decode {
     int J, bh, b, h, nch;
     int64_t tok0;

@@ -94,7 +94,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     issue(0);
     float off = 0.f;  // log2 decay of the superchunk's earlier chunks
 
+    const unsigned par = pair_parity(a.n_cu);
     for (int c = 0; c < d.nch; ++c) {
+        if constexpr (!BWD) pair_turn(par);  // the backward form runs one workgroup per CU
         const float b2 = wave_scan_dpp(gl * LOG2E);
         const float b63 = lane_value(b2, 63);
         __syncthreads();
@@ -358,7 +360,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     issue3(0);
     if constexpr (DQ) issue_q(0);
 
+    const unsigned par = pair_parity(a.n_cu);
     for (int c = 0; c < d.nch; ++c) {
+        pair_turn(par);
         const float b2 = wave_scan_dpp(gl * LOG2E);
         const float b63 = lane_value(b2, 63);
         __syncthreads();

@@ -18,6 +18,7 @@ struct SegArgs {
     int64_t sg_b, sg_l, sg_h;
     int32_t B, H;
     int32_t vec;      // 1: per-key-channel gate (g, dg are [B][L][H][D])
+    int32_t n_cu;     // compute units of the device
     int64_t L;        // tokens in the segment
     int32_t ts;       // superchunk length (multiple of 64)
     int32_t n_super;  // ceil(L / ts)
