@@ -85,6 +85,8 @@ def fwd(s, q=1, k=2, v=3, g=4, S_in=None, o=5, S_out=6, ws=7, ws_bytes=1 << 30, 
     (dict(reserved=1), _lib.SF_E_SHAPE),
     (dict(sx_b=1024 * 2 * 128, sx_l=100, sx_h=128), _lib.SF_E_SHAPE),   # rows overlap
     (dict(sx_b=1024 * 2 * 136, sx_l=2 * 136, sx_h=132), _lib.SF_E_ALIGN),  # 264-byte head stride
+    # a 64-token chunk spanning >= 2 GiB (the kernels address chunks with 32-bit offsets)
+    (dict(sx_b=1024 * (1 << 25), sx_l=1 << 25, sx_h=128), _lib.SF_E_SHAPE),
 ])
 def test_shape_validation(kw, status):
     assert fwd(shape(**kw)) == status
