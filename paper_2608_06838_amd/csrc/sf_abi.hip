@@ -362,11 +362,11 @@ sf_status bwd_grad(const Shape &r, const Seg &s, hipStream_t st) {
 // ------------------------------------------------------------ stream events
 struct EventPool {
     int dev = -1;
-    hipEvent_t ev[2] = {nullptr, nullptr};
+    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};  // dependency, join, scan done (x2)
 };
 thread_local EventPool g_events;
 
-sf_status events(hipEvent_t &e0, hipEvent_t &e1) {
+sf_status events(hipEvent_t &e0, hipEvent_t &e1, hipEvent_t *scan_done = nullptr) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -380,7 +380,20 @@ sf_status events(hipEvent_t &e0, hipEvent_t &e1) {
     }
     e0 = g_events.ev[0];
     e1 = g_events.ev[1];
+    if (scan_done) {
+        scan_done[0] = g_events.ev[2];
+        scan_done[1] = g_events.ev[3];
+    }
     return SF_OK;
+}
+// the main stream waits for one recorded point of the aux stream
+sf_status record(hipEvent_t ev, hipStream_t s) {
+    const hipError_t e = hipEventRecord(ev, s);
+    return e == hipSuccess ? SF_OK : hip_fail(e, "event record");
+}
+sf_status wait(hipStream_t s, hipEvent_t ev) {
+    const hipError_t e = hipStreamWaitEvent(s, ev, 0);
+    return e == hipSuccess ? SF_OK : hip_fail(e, "stream wait");
 }
 sf_status dep(hipStream_t from, hipStream_t to, hipEvent_t ev) {
     if (from == to) return SF_OK;
@@ -560,8 +573,8 @@ sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
     const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
     hipStream_t mn = (hipStream_t)main_s;
     hipStream_t ax = (aux_s && (!tuning || tuning->overlap != 0)) ? (hipStream_t)aux_s : mn;
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (ax != mn) TRY(events(e0, e1));
+    hipEvent_t e0 = nullptr, e1 = nullptr, sd[2] = {nullptr, nullptr};
+    if (ax != mn) TRY(events(e0, e1, sd));
     if (ax != mn) TRY(dep(mn, ax, e0));  // aux sees everything queued on main so far
 
     std::vector<Seg> segs(n_seg);
@@ -580,33 +593,32 @@ sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
         s.a.S_out = S_bnd + (i + 1) * SSB;
         tok += seg_len[i];
     }
-    // S_bnd[i] is produced by scan(i-1) on aux (multi-superchunk segments) or by
-    // the walk of segment i-1 on main (single-superchunk segments).
+    // Schedule (Sec. 3.4): Pre(i) -> [ST(i) on aux || Out(i-1) on main] -> Pre(i+1) ...
+    // Out(i-1) waits only for ST(i-1) (its own recorded point on aux), so ST(i)
+    // overlaps it.  S_bnd[i] is produced by ST(i-1) on aux (multi-superchunk
+    // segments; waited for before Out(i-1), hence before a single-superchunk
+    // Out(i)) or by the walk of segment i-1 on main (single-superchunk).  Two
+    // workspace slots suffice: Pre(i+1) overwrites slot (i+1)%2 on main after
+    // Out(i-1) has read it.
     int pending = -1;
-    bool bnd_on_aux = false;  // producer stream of the current S_bnd[i]
     for (int i = 0; i < n_seg; ++i) {
         Seg &s = segs[i];
         if (s.n > 1) {
             TRY(fwd_prep(r, s, mn));
             TRY(dep(mn, ax, e0));  // prep(i) done (and any main-side S_bnd[i] producer)
             TRY(fwd_scan(r, s, ax));
-            bnd_on_aux = (ax != mn);
+            if (ax != mn) TRY(record(sd[i % 2], ax));
         }
         if (pending >= 0) {
-            TRY(dep(ax, mn, e1));
+            if (ax != mn) TRY(wait(mn, sd[pending % 2]));
             TRY(fwd_out(r, segs[pending], mn));
             pending = -1;
         }
-        if (s.n > 1) {
-            pending = i;
-        } else {
-            if (bnd_on_aux) TRY(dep(ax, mn, e1));
-            TRY(fwd_out(r, s, mn));
-            bnd_on_aux = false;
-        }
+        if (s.n > 1) pending = i;
+        else TRY(fwd_out(r, s, mn));
     }
     if (pending >= 0) {
-        TRY(dep(ax, mn, e1));
+        if (ax != mn) TRY(wait(mn, sd[pending % 2]));
         TRY(fwd_out(r, segs[pending], mn));
     }
     if (ax != mn) TRY(dep(ax, mn, e1));
@@ -640,8 +652,8 @@ sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
     const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
     hipStream_t mn = (hipStream_t)main_s;
     hipStream_t ax = (aux_s && (!tuning || tuning->overlap != 0)) ? (hipStream_t)aux_s : mn;
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (ax != mn) TRY(events(e0, e1));
+    hipEvent_t e0 = nullptr, e1 = nullptr, sd[2] = {nullptr, nullptr};
+    if (ax != mn) TRY(events(e0, e1, sd));
     if (ax != mn) TRY(dep(mn, ax, e0));
 
     std::vector<Seg> segs(n_seg);
@@ -665,31 +677,31 @@ sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
         s.a.dS_in = i == 0 ? dS_init : gbnd[i % 2];
         tok += seg_len[i];
     }
+    // Mirror of the forward schedule: the gradient kernels of segment i+1 wait
+    // only for STB(i+1) and overlap STB(i).  For a multi-superchunk segment the
+    // gradient kernels read G_J from their own slot, never dS_out, so STB(i)
+    // writing dS_in(i) meanwhile is safe; a single-superchunk segment's
+    // kernels read dS_out, produced by STB(i+1) (waited for just before) or by
+    // the kernels of segment i+1 on main.
     int pending = -1;
-    bool bnd_on_aux = false;  // producer stream of the current dS_out
     for (int i = n_seg - 1; i >= 0; --i) {
         Seg &s = segs[i];
         if (s.n > 1) {
             TRY(bwd_prep(r, s, mn));
             TRY(dep(mn, ax, e0));
             TRY(bwd_scan(r, s, ax));
-            bnd_on_aux = (ax != mn);
+            if (ax != mn) TRY(record(sd[i % 2], ax));
         }
         if (pending >= 0) {
-            TRY(dep(ax, mn, e1));
+            if (ax != mn) TRY(wait(mn, sd[pending % 2]));
             TRY(bwd_grad(r, segs[pending], mn));
             pending = -1;
         }
-        if (s.n > 1) {
-            pending = i;
-        } else {
-            if (bnd_on_aux) TRY(dep(ax, mn, e1));
-            TRY(bwd_grad(r, s, mn));
-            bnd_on_aux = false;
-        }
+        if (s.n > 1) pending = i;
+        else TRY(bwd_grad(r, s, mn));
     }
     if (pending >= 0) {
-        TRY(dep(ax, mn, e1));
+        if (ax != mn) TRY(wait(mn, sd[pending % 2]));
         TRY(bwd_grad(r, segs[pending], mn));
     }
     if (ax != mn) TRY(dep(ax, mn, e1));
