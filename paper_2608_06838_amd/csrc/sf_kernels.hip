@@ -215,22 +215,35 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
         f32x4 G = a.dS_out ? *reinterpret_cast<const f32x4 *>(a.dS_out + bh * SS + e)
                            : f32x4{0.f, 0.f, 0.f, 0.f};
         f32x4 Sn = S;  // S_{J+1} for J = n-1 is S_out
-        for (int J = n - 1; J >= 0; --J) {
-            const f32x4 E = *reinterpret_cast<const f32x4 *>(Eb + (int64_t)J * SS);
-            const f32x4 Sj = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)J * SS);
-            const float f = fexp2(lg[J * LS]);
-            float p = G[0] * Sn[0] + G[1] * Sn[1] + G[2] * Sn[2] + G[3] * Sn[3];
-            if constexpr (!VG) {
-                p = wave_sum(p);
-                if (lane == 0) a.wsDot[(bh * n + J) * ndot + part * 4 + w] = p;
-            } else {
-                // the D/4 threads of one row are consecutive lanes
-                for (int o = D / 8; o >= 1; o >>= 1) p += __shfl_xor(p, o, 64);
-                if ((lane & (D / 4 - 1)) == 0) a.wsDot[(bh * n + J) * ndot + row] = p;
-            }
-            *reinterpret_cast<f32x4 *>(Eb + (int64_t)J * SS) = G;
-            G = f * G + E;
-            Sn = Sj;
+        // four superchunks per step: their loads go out together, ahead of the
+        // dependent chain
+        for (int J0 = n - 1; J0 >= 0; J0 -= 4) {
+            f32x4 E[4], Sj[4];
+            float f[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (J0 - u >= 0) {
+                    E[u] = *reinterpret_cast<const f32x4 *>(Eb + (int64_t)(J0 - u) * SS);
+                    Sj[u] = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)(J0 - u) * SS);
+                    f[u] = fexp2(lg[(J0 - u) * LS]);
+                }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (J0 - u >= 0) {
+                    const int J = J0 - u;
+                    float p = G[0] * Sn[0] + G[1] * Sn[1] + G[2] * Sn[2] + G[3] * Sn[3];
+                    if constexpr (!VG) {
+                        p = lane_value(wave_scan_dpp(p), 63);
+                        if (lane == 0) a.wsDot[(bh * n + J) * ndot + part * 4 + w] = p;
+                    } else {
+                        // the D/4 threads of one row are consecutive lanes
+                        for (int o = D / 8; o >= 1; o >>= 1) p += __shfl_xor(p, o, 64);
+                        if ((lane & (D / 4 - 1)) == 0) a.wsDot[(bh * n + J) * ndot + row] = p;
+                    }
+                    *reinterpret_cast<f32x4 *>(Eb + (int64_t)J * SS) = G;
+                    G = f[u] * G + E[u];
+                    Sn = Sj[u];
+                }
         }
         if (a.dS_in) *reinterpret_cast<f32x4 *>(a.dS_in + bh * SS + e) = G;
     }
