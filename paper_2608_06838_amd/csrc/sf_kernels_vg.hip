@@ -16,8 +16,9 @@
 // the chunk; a chunk that decays faster in some channel is walked token by
 // token instead (exact recurrence, slower), decided per chunk and workgroup.
 //
-// Kernels (wave w of D/32 waves owns NCT = 2 state column tiles, like the
-// scalar walkers):
+// Kernels (wave w of D/(16 NCT) waves owns NCT state column tiles: NCT = 2 for
+// the preps and the dq walk, NCT = 1 for the o, dv and dk walks, whose state
+// then fits in half the registers and two waves share each SIMD):
 //   k_prep_vg<BWD=false>  D_J and the per-channel superchunk decay
 //   k_prep_vg<BWD=true>   E_J = sum_t diag(2^{B_t}) q_t dO_t^T
 //   k_walk_vg             o (and S_out for a one-superchunk segment)
@@ -1232,18 +1233,19 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dk_vg(SegArgs a) {
 template <typename T, int D>
 static hipError_t launch_vg_td(int kind, const SegArgs &a, hipStream_t s) {
     constexpr int NCT = 2, NT = 64 * D / (16 * NCT);
+    constexpr int NC1 = 1, NT1 = 64 * D / 16;  // fwd and dk/dv walks: one 16-column tile per wave
     const dim3 grid((unsigned)((int64_t)a.B * a.H * a.n_super));
     switch (kind) {
     case SF_K_FWD_PREP: hipLaunchKernelGGL((k_prep_vg<T, D, NCT, false>), grid, dim3(NT), 0, s, a); break;
-    case SF_K_FWD_OUT: hipLaunchKernelGGL((k_walk_vg<T, D, NCT>), grid, dim3(NT), 0, s, a); break;
+    case SF_K_FWD_OUT: hipLaunchKernelGGL((k_walk_vg<T, D, NC1>), grid, dim3(NT1), 0, s, a); break;
     case SF_K_BWD_PREP:
         hipLaunchKernelGGL((k_prep_vg<T, D, NCT, false>), grid, dim3(NT), 0, s, a);
         hipLaunchKernelGGL((k_prep_vg<T, D, NCT, true>), grid, dim3(NT), 0, s, a);
         break;
     case SF_K_BWD_DQ: hipLaunchKernelGGL((k_dq_vg<T, D, NCT>), grid, dim3(NT), 0, s, a); break;
     case SF_K_BWD_DKV:
-        hipLaunchKernelGGL((k_dv_vg<T, D, NCT>), grid, dim3(NT), 0, s, a);
-        hipLaunchKernelGGL((k_dk_vg<T, D, NCT>), grid, dim3(NT), 0, s, a);
+        hipLaunchKernelGGL((k_dv_vg<T, D, NC1>), grid, dim3(NT1), 0, s, a);
+        hipLaunchKernelGGL((k_dk_vg<T, D, NC1>), grid, dim3(NT1), 0, s, a);
         break;
     default: return hipErrorInvalidValue;
     }
