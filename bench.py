@@ -52,7 +52,7 @@ def alg_bytes_per_token_head(D, io, gb=4):
 
 def kernel_src_hash():
     h = hashlib.sha256()
-    for f in ("sf_kernels.hip", "sf_device.hpp"):
+    for f in ("sf_kernels.hip", "sf_chunk.hpp", "sf_device.hpp"):
         with open(os.path.join(ROOT, "paper_2608_06838_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -233,7 +233,8 @@ def main():
         "mfma_frac_of_bf16_peak": flops / (ms / 1e3) / PEAK_BF16,
         "hbm_frac_alg": alg_bytes_per_token_head(D, io, gb) * B * H * L / (ms / 1e3) / PEAK_HBM,
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM / 1e9,
-                     "unit": "GB/s", "frac": achieved * 1e9 / PEAK_HBM, "traffic": traffic},
+                     "unit": "GB/s", "frac": achieved * 1e9 / PEAK_HBM, "traffic": traffic,
+                     "launches": nlaunch, "avg_launch_us": avg_s * 1e6},
     }
     # scan overlap (the fp32 superchunk scans run on a second stream): the chain's
     # time against the summed times of its other kernels, which is the chain time
