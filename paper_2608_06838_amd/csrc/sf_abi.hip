@@ -273,14 +273,13 @@ sf_status launch(int kind, const Shape &r, const sf::SegArgs &a, hipStream_t s) 
     }
     hipEvent_t e0 = nullptr, e1 = nullptr;
     if (on) {
-        if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess ||
-            hipEventRecord(e0, s) != hipSuccess)
+        if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess)
             return hip_fail(hipGetLastError(), "profiling event");
     }
-    hipError_t e = sf::launch_kernel(kind, r.io, r.D, a, s);
+    // the events take the dispatch timestamps of the launch itself
+    hipError_t e = sf::launch_kernel(kind, r.io, r.D, a, s, e0, e1);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     if (on) {
-        if (hipEventRecord(e1, s) != hipSuccess) return hip_fail(hipGetLastError(), "profiling event");
         std::lock_guard<std::mutex> lk(g_prof_mu);
         g_prof_ev[kind].push_back({e0, e1});
     }

@@ -875,39 +875,39 @@ __global__ void __launch_bounds__(SCAN_NT) k_state_copy(const float *src, float 
 // ---------------------------------------------------------------------------
 // launchers
 template <typename T, int D>
-static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s) {
+static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     const dim3 grid((unsigned)((int64_t)a.B * a.H * a.n_super));
     constexpr int NTP = 64 * D / (16 * SF_NCT_PREP), NTB = 64 * D / (16 * SF_NCT_PREPB);
     constexpr int NTW = 64 * D / (16 * SF_NCT_WALK);
     switch (kind) {
-    case SF_K_FWD_PREP: hipLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, false>), grid, dim3(NTP), 0, s, a); break;
-    case SF_K_FWD_OUT: hipLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, false>), grid, dim3(NTW), 0, s, a); break;
-    case SF_K_BWD_PREP: hipLaunchKernelGGL((k_prep<T, D, SF_NCT_PREPB, true>), grid, dim3(NTB), 0, s, a); break;
-    case SF_K_BWD_DQ: hipLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, true>), grid, dim3(NTW), 0, s, a); break;
+    case SF_K_FWD_PREP: hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, false>), grid, dim3(NTP), 0, s, e0, e1, 0, a); break;
+    case SF_K_FWD_OUT: hipExtLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, false>), grid, dim3(NTW), 0, s, e0, e1, 0, a); break;
+    case SF_K_BWD_PREP: hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREPB, true>), grid, dim3(NTB), 0, s, e0, e1, 0, a); break;
+    case SF_K_BWD_DQ: hipExtLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, true>), grid, dim3(NTW), 0, s, e0, e1, 0, a); break;
     case SF_K_BWD_DKV:
-        hipLaunchKernelGGL((k_bwd_dkv<T, D>), grid, dim3(128 * D / 16), 0, s, a);
+        hipExtLaunchKernelGGL((k_bwd_dkv<T, D>), grid, dim3(128 * D / 16), 0, s, e0, e1, 0, a);
         break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t s) {
+hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     if (kind == SF_K_SCAN) {
         const dim3 grid((unsigned)((int64_t)a.B * a.H * (D * D / 1024)));
         if (a.vec) {
-            if (a.wsE) hipLaunchKernelGGL((k_scan<true, true>), grid, dim3(SCAN_NT), 0, s, a, D);
-            else hipLaunchKernelGGL((k_scan<false, true>), grid, dim3(SCAN_NT), 0, s, a, D);
+            if (a.wsE) hipExtLaunchKernelGGL((k_scan<true, true>), grid, dim3(SCAN_NT), 0, s, e0, e1, 0, a, D);
+            else hipExtLaunchKernelGGL((k_scan<false, true>), grid, dim3(SCAN_NT), 0, s, e0, e1, 0, a, D);
         } else {
-            if (a.wsE) hipLaunchKernelGGL((k_scan<true, false>), grid, dim3(SCAN_NT), 0, s, a, D);
-            else hipLaunchKernelGGL((k_scan<false, false>), grid, dim3(SCAN_NT), 0, s, a, D);
+            if (a.wsE) hipExtLaunchKernelGGL((k_scan<true, false>), grid, dim3(SCAN_NT), 0, s, e0, e1, 0, a, D);
+            else hipExtLaunchKernelGGL((k_scan<false, false>), grid, dim3(SCAN_NT), 0, s, e0, e1, 0, a, D);
         }
         return hipGetLastError();
     }
-    if (a.vec) return launch_kernel_vg(kind, io, D, a, s);
-    if (io == SF_BF16 && D == 128) return launch_td<__bf16, 128>(kind, a, s);
-    if (io == SF_BF16 && D == 64) return launch_td<__bf16, 64>(kind, a, s);
-    if (io == SF_F32 && D == 64) return launch_td<float, 64>(kind, a, s);
+    if (a.vec) return launch_kernel_vg(kind, io, D, a, s, e0, e1);
+    if (io == SF_BF16 && D == 128) return launch_td<__bf16, 128>(kind, a, s, e0, e1);
+    if (io == SF_BF16 && D == 64) return launch_td<__bf16, 64>(kind, a, s, e0, e1);
+    if (io == SF_F32 && D == 64) return launch_td<float, 64>(kind, a, s, e0, e1);
     return hipErrorInvalidValue;
 }
 

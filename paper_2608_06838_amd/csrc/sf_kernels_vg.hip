@@ -1231,31 +1231,31 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dk_vg(SegArgs a) {
 
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-static hipError_t launch_vg_td(int kind, const SegArgs &a, hipStream_t s) {
+static hipError_t launch_vg_td(int kind, const SegArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     constexpr int NCT = 2, NT = 64 * D / (16 * NCT);
     constexpr int NC1 = 1, NT1 = 64 * D / 16;  // fwd and dk/dv walks: one 16-column tile per wave
     const dim3 grid((unsigned)((int64_t)a.B * a.H * a.n_super));
     switch (kind) {
-    case SF_K_FWD_PREP: hipLaunchKernelGGL((k_prep_vg<T, D, NCT, false>), grid, dim3(NT), 0, s, a); break;
-    case SF_K_FWD_OUT: hipLaunchKernelGGL((k_walk_vg<T, D, NC1>), grid, dim3(NT1), 0, s, a); break;
+    case SF_K_FWD_PREP: hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, false>), grid, dim3(NT), 0, s, e0, e1, 0, a); break;
+    case SF_K_FWD_OUT: hipExtLaunchKernelGGL((k_walk_vg<T, D, NC1>), grid, dim3(NT1), 0, s, e0, e1, 0, a); break;
     case SF_K_BWD_PREP:
-        hipLaunchKernelGGL((k_prep_vg<T, D, NCT, false>), grid, dim3(NT), 0, s, a);
-        hipLaunchKernelGGL((k_prep_vg<T, D, NCT, true>), grid, dim3(NT), 0, s, a);
+        hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, false>), grid, dim3(NT), 0, s, e0, nullptr, 0, a);
+        hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, true>), grid, dim3(NT), 0, s, nullptr, e1, 0, a);
         break;
-    case SF_K_BWD_DQ: hipLaunchKernelGGL((k_dq_vg<T, D, NCT>), grid, dim3(NT), 0, s, a); break;
+    case SF_K_BWD_DQ: hipExtLaunchKernelGGL((k_dq_vg<T, D, NCT>), grid, dim3(NT), 0, s, e0, e1, 0, a); break;
     case SF_K_BWD_DKV:
-        hipLaunchKernelGGL((k_dv_vg<T, D, NC1>), grid, dim3(NT1), 0, s, a);
-        hipLaunchKernelGGL((k_dk_vg<T, D, NC1>), grid, dim3(NT1), 0, s, a);
+        hipExtLaunchKernelGGL((k_dv_vg<T, D, NC1>), grid, dim3(NT1), 0, s, e0, nullptr, 0, a);
+        hipExtLaunchKernelGGL((k_dk_vg<T, D, NC1>), grid, dim3(NT1), 0, s, nullptr, e1, 0, a);
         break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_kernel_vg(int kind, int io, int D, const SegArgs &a, hipStream_t s) {
-    if (io == SF_BF16 && D == 128) return launch_vg_td<__bf16, 128>(kind, a, s);
-    if (io == SF_BF16 && D == 64) return launch_vg_td<__bf16, 64>(kind, a, s);
-    if (io == SF_F32 && D == 64) return launch_vg_td<float, 64>(kind, a, s);
+hipError_t launch_kernel_vg(int kind, int io, int D, const SegArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    if (io == SF_BF16 && D == 128) return launch_vg_td<__bf16, 128>(kind, a, s, e0, e1);
+    if (io == SF_BF16 && D == 64) return launch_vg_td<__bf16, 64>(kind, a, s, e0, e1);
+    if (io == SF_F32 && D == 64) return launch_vg_td<float, 64>(kind, a, s, e0, e1);
     return hipErrorInvalidValue;
 }
 

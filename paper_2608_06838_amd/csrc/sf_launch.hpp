@@ -1,5 +1,6 @@
 // sf_launch.hpp -- argument block shared by the host driver and the kernels.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -34,9 +35,12 @@ struct SegArgs {
 };
 
 // kind is an sf_kernel_id; io an sf_dtype.  The scan runs its backward form
-// when wsE is set.
-hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t s);
-hipError_t launch_kernel_vg(int kind, int io, int D, const SegArgs &a, hipStream_t s);
+// when wsE is set.  Non-null e0/e1 take the begin timestamp of the first
+// kernel the kind launches and the end timestamp of its last (the timing
+// rides on the dispatch packets, no marker packets are added).
+hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t s, hipEvent_t e0 = nullptr,
+                         hipEvent_t e1 = nullptr);
+hipError_t launch_kernel_vg(int kind, int io, int D, const SegArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_state_copy(const float *src, float *dst, int64_t n, hipStream_t s);
 
 }  // namespace sf
