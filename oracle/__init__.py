@@ -110,3 +110,5 @@ def backward(q, k, v, g, S_in, dO, dS_out=None, threads=0):
     if rc != 0:
         raise RuntimeError(f"sfo_backward failed ({rc})")
     return dq, dk, dv, dg, dS_in
+
+from .conv import conv_backward, conv_forward  # noqa: E402,F401
