@@ -177,10 +177,56 @@ sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
                        const sf_tuning *tuning, sf_stream main, sf_stream aux);
 
 /*
- * Kernel timing for measurement: while enabled, the library brackets every
- * launch of kernel `kernel_id` (an sf_kernel_id) with HIP events on the
- * stream that launch uses.  sf_prof_read() synchronises those events and
- * returns the summed milliseconds and launch count since the last reset.
+ * Short convolution with a boundary tail: the auxiliary boundary state that
+ * Sec. 3.1 (footnote to the chunk boundary states) lets a segment carry next
+ * to S.  Per batch b, channel c and token t of a segment, with a causal
+ * depthwise window of W taps:
+ *
+ *     u_t[c] = sum_{j=0}^{W-1} w[c][j] * xh_{t-W+1+j}[c],     y_t[c] = act(u_t[c])
+ *
+ * where xh_s = x_s for s >= 0 and xh_s = tail_in[b][W-1+s][c] for
+ * -(W-1) <= s < 0: the last W-1 inputs of the previous segment, oldest first
+ * (NULL = zeros, the start of a sequence).  tail_out[b][i][c] = xh_{L-W+1+i}
+ * (i = 0..W-2) is the tail the next segment takes, so chaining segments
+ * through their tails equals one call over the whole sequence.
+ *   x, y, dx, dy   [B][L][C] in io_dtype, element strides (sx_b, sx_l),
+ *                  channels contiguous (0, 0 = packed)
+ *   w, dw          [C][W] float32
+ *   tail_in, tail_out, dtail_in, dtail_out   [B][W-1][C] float32, packed
+ *   act            SF_ACT_NONE (identity) or SF_ACT_SILU (u * sigmoid(u))
+ * The backward takes the gradient of the loss sum <dy, y> + <dtail_out,
+ * tail_out> (dtail_out NULL = zero) and writes dx, dtail_in and dw (summed
+ * over batch and tokens, in a fixed order: bitwise reproducible).  dw needs
+ * a workspace of sf_conv_bwd_workspace_bytes().  Supported: 1 <= W <= 4
+ * (W = 1 has no tail; the tail pointers are then ignored), C a multiple of 8,
+ * L >= 0, 16-byte aligned pointers and strides.  Same ownership, error and
+ * aliasing rules as the recurrence entry points.
+ */
+typedef enum { SF_ACT_NONE = 0, SF_ACT_SILU = 1 } sf_act;
+
+typedef struct sf_conv_shape {
+    int32_t B, C;     /* batch, channels */
+    int64_t L;        /* tokens of the segment */
+    int32_t W;        /* taps, 1..4 */
+    int32_t io_dtype; /* sf_dtype of x, y, dx, dy */
+    int32_t act;      /* sf_act */
+    int32_t reserved; /* must be 0 */
+    int64_t sx_b, sx_l; /* element strides of x, y, dx, dy; both 0 = packed */
+} sf_conv_shape;
+
+size_t sf_conv_bwd_workspace_bytes(const sf_conv_shape *shape);
+sf_status sf_conv_fwd(const sf_conv_shape *shape, const void *x, const float *w, const float *tail_in,
+                      void *y, float *tail_out, sf_stream stream);
+sf_status sf_conv_bwd(const sf_conv_shape *shape, const void *x, const float *w, const float *tail_in,
+                      const void *dy, const float *dtail_out, void *dx, float *dw, float *dtail_in,
+                      void *ws, size_t ws_bytes, sf_stream stream);
+
+/*
+ * Kernel timing for measurement: while enabled, every launch of kernel
+ * `kernel_id` (an sf_kernel_id) carries HIP events that take the begin and
+ * end timestamps of its own dispatch.  sf_prof_read() synchronises those
+ * events and returns the summed milliseconds and launch count since the last
+ * reset.
  */
 typedef enum {
     SF_K_FWD_PREP = 0, /* per-superchunk state contribution (Pre) */
@@ -189,7 +235,9 @@ typedef enum {
     SF_K_BWD_PREP = 3, /* per-superchunk state and state-gradient contributions */
     SF_K_BWD_DQ = 4,   /* dq by a forward state walk (OG) */
     SF_K_BWD_DKV = 5,  /* dk, dv, dg by a reverse state-gradient walk (PG) */
-    SF_K_COUNT = 6
+    SF_K_CONV_FWD = 6, /* short convolution, forward */
+    SF_K_CONV_BWD = 7, /* short convolution, backward (dx, dtail_in, dw partials and their sum) */
+    SF_K_COUNT = 8
 } sf_kernel_id;
 
 sf_status sf_prof_enable(int32_t kernel_id, int32_t on);

@@ -12,6 +12,14 @@ memory and streams only, every arithmetic step runs in libstateflow.so):
 Shapes: q, k, v, dO: [B, L, H, D] (bf16 or fp32, channel dim contiguous, all
 with the same strides); g: [B, L, H] fp32 natural-log decay; states:
 [B, H, D, D] fp32 (S stored as Dk x Dv).  See include/stateflow.h.
+
+The short convolution whose tail is the auxiliary boundary state of a segment:
+
+    y, tail_out              = conv_fwd(x, w, tail_in, act="silu")
+    dx, dw, dtail_in         = conv_bwd(x, w, tail_in, dy, dtail_out, act="silu")
+
+x, y: [B, L, C] (bf16 or fp32, channels contiguous); w: [C, W] fp32;
+tails: [B, W-1, C] fp32.
 """
 import ctypes
 
@@ -21,8 +29,8 @@ from . import _lib
 from ._lib import KERNELS, StateflowError  # noqa: F401
 
 __all__ = ["segment_fwd", "segment_bwd", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
-           "bwd_workspace_bytes", "chain_workspace_bytes", "prof_enable", "prof_read",
-           "StateflowError", "abi_version"]
+           "bwd_workspace_bytes", "chain_workspace_bytes", "conv_fwd", "conv_bwd", "conv_bwd_workspace_bytes",
+           "prof_enable", "prof_read", "StateflowError", "abi_version"]
 
 _IO = {torch.bfloat16: _lib.SF_BF16, torch.float32: _lib.SF_F32}
 _aux_streams = {}
@@ -236,6 +244,81 @@ def chain_bwd(q, k, v, g, seg_lens, S_bnd, dO, dS_final=None, *, ts=0, overlap=T
                          _stream_handle(aux) if aux is not None else None)
     _lib.check("sf_chain_bwd", rc)
     return dq, dk, dv, dg, dS_init
+
+
+_ACT = {"none": _lib.SF_ACT_NONE, "silu": _lib.SF_ACT_SILU}
+
+
+def _conv_shape(x, w, act):
+    if x.dim() != 3:
+        raise ValueError("x must be [B, L, C]")
+    if x.dtype not in _IO:
+        raise TypeError(f"unsupported I/O dtype {x.dtype}")
+    if w.dim() != 2 or w.dtype != torch.float32 or not w.is_contiguous():
+        raise ValueError("w must be a contiguous float32 [C, W] tensor")
+    B, L, C = x.shape
+    if w.shape[0] != C:
+        raise ValueError(f"w has {w.shape[0]} channels, x has {C}")
+    if x.stride(2) != 1:
+        raise ValueError("x must have a contiguous channel dim")
+    sh = _lib.SfConvShape()
+    sh.B, sh.C, sh.L, sh.W = B, C, L, w.shape[1]
+    sh.io_dtype = _IO[x.dtype]
+    sh.act = _ACT[act]
+    sh.sx_b, sh.sx_l = x.stride(0), x.stride(1)
+    return sh
+
+
+def _tail(t, B, W, C, name):
+    if t is None or W == 1:
+        return None
+    if t.dtype != torch.float32 or tuple(t.shape) != (B, W - 1, C) or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous float32 [{B}, {W - 1}, {C}] tensor")
+    return t
+
+
+def conv_bwd_workspace_bytes(x, w, act="silu"):
+    return _lib.lib().sf_conv_bwd_workspace_bytes(ctypes.byref(_conv_shape(x, w, act)))
+
+
+def conv_fwd(x, w, tail_in=None, act="silu", *, stream=None):
+    """(y, tail_out) of the short convolution over one segment; tail_out is
+    None for W = 1."""
+    sh = _conv_shape(x, w, act)
+    B, L, C = x.shape
+    W = w.shape[1]
+    tail_in = _tail(tail_in, B, W, C, "tail_in")
+    stream = stream or torch.cuda.current_stream(x.device)
+    with torch.cuda.stream(stream):
+        y = _like(x)
+        tail_out = torch.empty((B, W - 1, C), dtype=torch.float32, device=x.device) if W > 1 else None
+    rc = _lib.lib().sf_conv_fwd(ctypes.byref(sh), _ptr(x), _ptr(w), _ptr(tail_in), _ptr(y), _ptr(tail_out),
+                                _stream_handle(stream))
+    _lib.check("sf_conv_fwd", rc)
+    return y, tail_out
+
+
+def conv_bwd(x, w, tail_in, dy, dtail_out=None, act="silu", *, stream=None):
+    """(dx, dw, dtail_in) for the loss sum <dy, y> + <dtail_out, tail_out>;
+    dtail_in is None for W = 1."""
+    sh = _conv_shape(x, w, act)
+    B, L, C = x.shape
+    W = w.shape[1]
+    if tuple(dy.shape) != tuple(x.shape) or dy.stride() != x.stride() or dy.dtype != x.dtype:
+        raise ValueError("dy must match x in shape, strides and dtype")
+    tail_in = _tail(tail_in, B, W, C, "tail_in")
+    dtail_out = _tail(dtail_out, B, W, C, "dtail_out")
+    stream = stream or torch.cuda.current_stream(x.device)
+    L_ = _lib.lib()
+    with torch.cuda.stream(stream):
+        dx = _like(x)
+        dw = torch.empty((C, W), dtype=torch.float32, device=x.device)
+        dtail_in = torch.empty((B, W - 1, C), dtype=torch.float32, device=x.device) if W > 1 else None
+        ws = _ws(L_.sf_conv_bwd_workspace_bytes(ctypes.byref(sh)), x.device)
+    rc = L_.sf_conv_bwd(ctypes.byref(sh), _ptr(x), _ptr(w), _ptr(tail_in), _ptr(dy), _ptr(dtail_out), _ptr(dx),
+                        _ptr(dw), _ptr(dtail_in), _ptr(ws), ws.numel(), _stream_handle(stream))
+    _lib.check("sf_conv_bwd", rc)
+    return dx, dw, dtail_in
 
 
 def prof_enable(kernel, on=True):

@@ -14,12 +14,15 @@ SF_OK, SF_E_NULL, SF_E_SHAPE, SF_E_DTYPE, SF_E_ALIGN, SF_E_ALIAS, SF_E_WORKSPACE
     SF_E_UNSUPPORTED, SF_E_HIP = range(9)
 SF_F32, SF_BF16 = 0, 1
 SF_GATE_SCALAR, SF_GATE_VECTOR = 0, 1
-KERNELS = {"fwd_prep": 0, "scan": 1, "fwd_out": 2, "bwd_prep": 3, "bwd_dq": 4, "bwd_dkv": 5}
+KERNELS = {"fwd_prep": 0, "scan": 1, "fwd_out": 2, "bwd_prep": 3, "bwd_dq": 4, "bwd_dkv": 5,
+           "conv_fwd": 6, "conv_bwd": 7}
+SF_ACT_NONE, SF_ACT_SILU = 0, 1
 
 # every symbol include/stateflow.h declares
 EXPORTS = ["sf_abi_version", "sf_status_str", "sf_last_error", "sf_fwd_workspace_bytes",
            "sf_bwd_workspace_bytes", "sf_segment_fwd", "sf_segment_bwd", "sf_chain_workspace_bytes",
-           "sf_chain_fwd", "sf_chain_bwd", "sf_prof_enable", "sf_prof_read"]
+           "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd",
+           "sf_prof_enable", "sf_prof_read"]
 
 
 class SfShape(ctypes.Structure):
@@ -28,6 +31,12 @@ class SfShape(ctypes.Structure):
                 ("io_dtype", ctypes.c_int32), ("gate", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("sx_b", ctypes.c_int64), ("sx_l", ctypes.c_int64), ("sx_h", ctypes.c_int64),
                 ("sg_b", ctypes.c_int64), ("sg_l", ctypes.c_int64), ("sg_h", ctypes.c_int64)]
+
+
+class SfConvShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("C", ctypes.c_int32), ("L", ctypes.c_int64), ("W", ctypes.c_int32),
+                ("io_dtype", ctypes.c_int32), ("act", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("sx_b", ctypes.c_int64), ("sx_l", ctypes.c_int64)]
 
 
 class SfTuning(ctypes.Structure):
@@ -80,6 +89,13 @@ def lib():
     L.sf_chain_fwd.argtypes = [sp, i32, i64p] + [vp] * 7 + [sz, tp, vp, vp]
     L.sf_chain_bwd.restype = ctypes.c_int
     L.sf_chain_bwd.argtypes = [sp, i32, i64p] + [vp] * 13 + [sz, tp, vp, vp]
+    cp = ctypes.POINTER(SfConvShape)
+    L.sf_conv_bwd_workspace_bytes.restype = sz
+    L.sf_conv_bwd_workspace_bytes.argtypes = [cp]
+    L.sf_conv_fwd.restype = ctypes.c_int
+    L.sf_conv_fwd.argtypes = [cp] + [vp] * 5 + [vp]
+    L.sf_conv_bwd.restype = ctypes.c_int
+    L.sf_conv_bwd.argtypes = [cp] + [vp] * 9 + [sz, vp]
     L.sf_prof_enable.restype = ctypes.c_int
     L.sf_prof_enable.argtypes = [i32, i32]
     L.sf_prof_read.restype = ctypes.c_int

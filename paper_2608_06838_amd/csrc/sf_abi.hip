@@ -286,6 +286,88 @@ sf_status launch(int kind, const Shape &r, const sf::SegArgs &a, hipStream_t s) 
     return SF_OK;
 }
 
+// ------------------------------------------------------ short convolution
+struct ConvShape {
+    int B, C, W, io, act;
+    int64_t L, sx_b, sx_l;
+    size_t esz;
+};
+
+sf_status conv_resolve(const sf_conv_shape *sh, ConvShape &r) {
+    if (!sh) return fail(SF_E_NULL, "shape is NULL");
+    if (sh->B < 1 || sh->C < 1 || sh->L < 0)
+        return fail(SF_E_SHAPE, "need B >= 1, C >= 1, L >= 0 (got B=%d C=%d L=%lld)", sh->B, sh->C, (long long)sh->L);
+    if (sh->io_dtype != SF_F32 && sh->io_dtype != SF_BF16) return fail(SF_E_DTYPE, "unknown io_dtype %d", sh->io_dtype);
+    if (sh->act != SF_ACT_NONE && sh->act != SF_ACT_SILU) return fail(SF_E_DTYPE, "unknown act %d", sh->act);
+    if (sh->reserved != 0) return fail(SF_E_SHAPE, "shape.reserved must be 0");
+    if (sh->W < 1 || sh->W > 4) return fail(SF_E_UNSUPPORTED, "supported taps: 1 <= W <= 4 (got %d)", sh->W);
+    const int ce = sf::conv_channels_per_thread();
+    if (sh->C % ce) return fail(SF_E_UNSUPPORTED, "C must be a multiple of %d (got %d)", ce, sh->C);
+    r.B = sh->B;
+    r.C = sh->C;
+    r.W = sh->W;
+    r.io = sh->io_dtype;
+    r.act = sh->act;
+    r.L = sh->L;
+    r.esz = sh->io_dtype == SF_BF16 ? 2 : 4;
+    if (sh->sx_b == 0 && sh->sx_l == 0) {
+        r.sx_l = r.C;
+        r.sx_b = r.L * r.C;
+    } else {
+        r.sx_b = sh->sx_b;
+        r.sx_l = sh->sx_l;
+    }
+    if (r.sx_b <= 0 || r.sx_l <= 0) return fail(SF_E_SHAPE, "strides must be positive");
+    if (!non_overlapping({{r.B, r.sx_b}, {r.L, r.sx_l}}, r.C))
+        return fail(SF_E_SHAPE, "strides make elements overlap");
+    if ((r.sx_b * (int64_t)r.esz) % 16 || (r.sx_l * (int64_t)r.esz) % 16)
+        return fail(SF_E_ALIGN, "strides must be multiples of 16 bytes");
+    if (r.B > 65535) return fail(SF_E_UNSUPPORTED, "B must be <= 65535 (got %d)", r.B);
+    return SF_OK;
+}
+
+// tokens per workgroup row: 256 in the forward; the backward grows it with L
+// so that at most 256 dw partials per batch go through the workspace
+int64_t conv_block(const ConvShape &r, bool bwd) {
+    if (!bwd) return 256;
+    const int64_t per = (r.L + 255) / 256;
+    return std::max<int64_t>(256, (per + 63) / 64 * 64);
+}
+int64_t conv_nblocks(const ConvShape &r, bool bwd) { return (r.L + conv_block(r, bwd) - 1) / conv_block(r, bwd); }
+size_t conv_ws_bytes(const ConvShape &r) {
+    return r.L > 0 ? (size_t)r.B * (size_t)conv_nblocks(r, true) * (size_t)r.C * (size_t)r.W * 4 : 0;
+}
+
+Range conv_xrange(const ConvShape &r, const void *p, const char *name) {
+    const char *b = (const char *)p;
+    const int64_t last = (r.B - 1) * r.sx_b + (r.L - 1) * r.sx_l + r.C;
+    return {b, b + (r.L > 0 ? last * (int64_t)r.esz : 0), name};
+}
+Range frange(const void *p, int64_t n, const char *name) {
+    const char *b = (const char *)p;
+    return {b, b + (p ? n * 4 : 0), name};
+}
+
+sf_status conv_run(int kind, bool bwd, const sf::ConvArgs &a, hipStream_t s) {
+    bool on;
+    {
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        on = g_prof_on[kind];
+    }
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (on) {
+        if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess)
+            return hip_fail(hipGetLastError(), "profiling event");
+    }
+    hipError_t e = sf::launch_conv(bwd, a, s, e0, e1);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    if (on) {
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        g_prof_ev[kind].push_back({e0, e1});
+    }
+    return SF_OK;
+}
+
 // ----------------------------------------------------------- segment plans
 struct Seg {
     sf::SegArgs a;
@@ -705,6 +787,88 @@ sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
     }
     if (ax != mn) TRY(dep(ax, mn, e1));
     return SF_OK;
+}
+
+size_t sf_conv_bwd_workspace_bytes(const sf_conv_shape *shape) {
+    ConvShape r;
+    if (conv_resolve(shape, r) != SF_OK) return 0;
+    return conv_ws_bytes(r);
+}
+
+sf_status sf_conv_fwd(const sf_conv_shape *shape, const void *x, const float *w, const float *tail_in, void *y,
+                      float *tail_out, sf_stream stream) {
+    ConvShape r;
+    TRY(conv_resolve(shape, r));
+    const bool tail = r.W > 1;
+    if (!w || (r.L > 0 && (!x || !y))) return fail(SF_E_NULL, "x, w and y are required");
+    TRY(check_align({{x, "x"}, {y, "y"}}));
+    if (((uintptr_t)w | (uintptr_t)(tail ? tail_in : nullptr) | (uintptr_t)(tail ? tail_out : nullptr)) % 4)
+        return fail(SF_E_ALIGN, "w and the tails must be 4-byte aligned");
+    const int64_t nt = (int64_t)r.B * (r.W - 1) * r.C;
+    TRY(check_alias({conv_xrange(r, x, "x"), frange(w, (int64_t)r.C * r.W, "w"),
+                     frange(tail ? tail_in : nullptr, nt, "tail_in")},
+                    {conv_xrange(r, y, "y"), frange(tail ? tail_out : nullptr, nt, "tail_out")}));
+    if (r.L == 0 && (!tail || !tail_out)) return SF_OK;  // nothing to write
+    sf::ConvArgs a{};
+    a.x = x;
+    a.w = w;
+    a.tail_in = tail ? tail_in : nullptr;
+    a.y = y;
+    a.tail_out = tail ? tail_out : nullptr;
+    a.B = r.B;
+    a.C = r.C;
+    a.W = r.W;
+    a.act = r.act;
+    a.io = r.io;
+    a.L = r.L;
+    a.T = conv_block(r, false);
+    a.nTB = (int32_t)conv_nblocks(r, false);
+    a.sx_b = r.sx_b;
+    a.sx_l = r.sx_l;
+    if (a.nTB > 65535) return fail(SF_E_UNSUPPORTED, "L too large for one call (%lld tokens)", (long long)r.L);
+    return conv_run(SF_K_CONV_FWD, false, a, (hipStream_t)stream);
+}
+
+sf_status sf_conv_bwd(const sf_conv_shape *shape, const void *x, const float *w, const float *tail_in, const void *dy,
+                      const float *dtail_out, void *dx, float *dw, float *dtail_in, void *ws, size_t ws_bytes,
+                      sf_stream stream) {
+    ConvShape r;
+    TRY(conv_resolve(shape, r));
+    const bool tail = r.W > 1;
+    if (!w || !dw || (r.L > 0 && (!x || !dy || !dx))) return fail(SF_E_NULL, "x, w, dy, dx and dw are required");
+    const size_t need = conv_ws_bytes(r);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(SF_E_WORKSPACE, "workspace of %zu bytes needed (got %zu)", need, ws ? ws_bytes : (size_t)0);
+    TRY(check_align({{x, "x"}, {dy, "dy"}, {dx, "dx"}}));
+    if (((uintptr_t)w | (uintptr_t)dw | (uintptr_t)ws | (uintptr_t)(tail ? tail_in : nullptr) |
+         (uintptr_t)(tail ? dtail_out : nullptr) | (uintptr_t)(tail ? dtail_in : nullptr)) % 4)
+        return fail(SF_E_ALIGN, "w, dw, the workspace and the tails must be 4-byte aligned");
+    const int64_t nt = (int64_t)r.B * (r.W - 1) * r.C, nw = (int64_t)r.C * r.W;
+    TRY(check_alias({conv_xrange(r, x, "x"), frange(w, nw, "w"), frange(tail ? tail_in : nullptr, nt, "tail_in"),
+                     conv_xrange(r, dy, "dy"), frange(tail ? dtail_out : nullptr, nt, "dtail_out")},
+                    {conv_xrange(r, dx, "dx"), frange(dw, nw, "dw"), frange(tail ? dtail_in : nullptr, nt, "dtail_in"),
+                     {(const char *)ws, (const char *)ws + (need ? need : 0), "workspace"}}));
+    sf::ConvArgs a{};
+    a.x = x;
+    a.w = w;
+    a.tail_in = tail ? tail_in : nullptr;
+    a.dy = dy;
+    a.dtail_out = tail ? dtail_out : nullptr;
+    a.dx = dx;
+    a.dw = dw;
+    a.dtail_in = tail ? dtail_in : nullptr;
+    a.ws = (float *)ws;
+    a.B = r.B;
+    a.C = r.C;
+    a.W = r.W;
+    a.act = r.act;
+    a.io = r.io;
+    a.L = r.L;
+    a.T = conv_block(r, true);
+    a.nTB = (int32_t)conv_nblocks(r, true);
+    a.sx_b = r.sx_b;
+    a.sx_l = r.sx_l;
+    return conv_run(SF_K_CONV_BWD, true, a, (hipStream_t)stream);
 }
 
 sf_status sf_prof_enable(int32_t kernel_id, int32_t on) {

@@ -43,4 +43,25 @@ hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t 
 hipError_t launch_kernel_vg(int kind, int io, int D, const SegArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_state_copy(const float *src, float *dst, int64_t n, hipStream_t s);
 
+// Short convolution (sf_conv.hip).  Token block T per workgroup row; nTB
+// blocks per batch; ws holds B * nTB dw partials of C * W floats.
+struct ConvArgs {
+    const void *x;
+    const float *w;
+    const float *tail_in;
+    void *y;
+    float *tail_out;
+    const void *dy;
+    const float *dtail_out;
+    void *dx;
+    float *dw;
+    float *dtail_in;
+    float *ws;
+    int32_t B, C, W, act, io;
+    int32_t nTB;
+    int64_t L, T, sx_b, sx_l;
+};
+int conv_channels_per_thread();
+hipError_t launch_conv(bool bwd, const ConvArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+
 }  // namespace sf

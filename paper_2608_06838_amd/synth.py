@@ -1,4 +1,5 @@
-"""Seeded synthetic inputs for the segmented gated linear recurrence.
+"""Seeded synthetic inputs for the segmented gated linear recurrence and the
+short convolution.
 
 This module only draws random numbers in the shapes and distributions of the
 workloads; it holds none of the recurrence's arithmetic, so both the HIP path
@@ -84,3 +85,39 @@ def make_inputs(w, device="cpu", seed=1000, dS_out_std=0.0, L=None):
     out = dict(q=q.to(io), k=k.to(io), v=v.to(io), g=g.contiguous(), S_in=S_in,
                dO=dO.to(io), dS_out=dS_out, seg_lens=seg_lens)
     return out
+
+
+# Short convolution in front of the recurrence (GDN-style: 4 taps, SiLU) over the
+# q, k and v projections of the 256K-context layer: 3 x 40 x 128 channels, the
+# same 8 segments, tails carried from segment to segment.
+CONV_WORKLOADS = {
+    "conv_ctx256k": dict(B=1, C=3 * 40 * 128, W=4, seg_lens=WORKLOADS["ctx256k_h40"]["seg_lens"], io="bf16",
+                         act="silu"),
+}
+
+
+def conv_workload(name, **override):
+    w = dict(CONV_WORKLOADS[name])
+    w.update(override)
+    w["name"] = name
+    return w
+
+
+def make_conv_inputs(B, L, C, W, io="bf16", device="cpu", seed=2000, tails=True):
+    """Draws, in this order, from one torch.Generator seeded with `seed`:
+    x ~ N(0, 1) [B, L, C]; w ~ N(0, 1/W) [C, W]; tail_in ~ N(0, 1) [B, W-1, C];
+    dy ~ N(0, 1) [B, L, C]; dtail_out ~ N(0, 1) [B, W-1, C].  x, dy and the
+    tail (which holds earlier inputs) are rounded to the I/O dtype; w and the
+    tails are float32.  tails=False gives tail_in = dtail_out = None."""
+    io_t = _IO[io]
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    f32 = dict(dtype=torch.float32, device=device, generator=gen)
+    x = torch.randn(B, L, C, **f32).to(io_t)
+    w = (torch.randn(C, W, **f32) / float(W) ** 0.5).contiguous()
+    tail_in = torch.randn(B, W - 1, C, **f32).to(io_t).float() if W > 1 else None
+    dy = torch.randn(B, L, C, **f32).to(io_t)
+    dtail_out = torch.randn(B, W - 1, C, **f32) if W > 1 else None
+    if not tails:
+        tail_in = dtail_out = None
+    return dict(x=x, w=w, tail_in=tail_in, dy=dy, dtail_out=dtail_out)

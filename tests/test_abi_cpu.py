@@ -131,3 +131,66 @@ def test_chain_validation():
     assert rc == _lib.SF_E_NULL  # dS_init missing
     rc = L.sf_prof_enable(99, 1)
     assert rc == _lib.SF_E_SHAPE
+
+
+# ------------------------------------------------------------ short convolution
+def conv_shape(**kw):
+    s = _lib.SfConvShape()
+    s.B, s.C, s.L, s.W, s.io_dtype, s.act, s.reserved = 2, 64, 1000, 4, _lib.SF_BF16, _lib.SF_ACT_SILU, 0
+    for k, v in kw.items():
+        setattr(s, k, v)
+    return s
+
+
+def conv_fwd(s, x=1, w=2, tail_in=3, y=4, tail_out=5):
+    args = [p(i) if i is not None else None for i in (x, w, tail_in, y, tail_out)]
+    return _lib.lib().sf_conv_fwd(ctypes.byref(s) if s is not None else None, *args, None)
+
+
+def conv_bwd(s, x=1, w=2, tail_in=3, dy=4, dtail_out=5, dx=6, dw=7, dtail_in=8, ws=9, ws_bytes=1 << 30):
+    args = [p(i) if i is not None else None for i in (x, w, tail_in, dy, dtail_out, dx, dw, dtail_in, ws)]
+    return _lib.lib().sf_conv_bwd(ctypes.byref(s), *args, ws_bytes, None)
+
+
+def test_conv_workspace_bytes():
+    L = _lib.lib()
+    # 1000 tokens: blocks of 256, 4 partials per batch of C * W floats
+    assert L.sf_conv_bwd_workspace_bytes(ctypes.byref(conv_shape())) == 2 * 4 * 64 * 4 * 4
+    # 262144 tokens: the block grows to 1024 so that 256 partials per batch remain
+    assert L.sf_conv_bwd_workspace_bytes(ctypes.byref(conv_shape(B=1, L=262144, C=5120))) == 256 * 5120 * 4 * 4
+    assert L.sf_conv_bwd_workspace_bytes(ctypes.byref(conv_shape(L=0))) == 0
+    assert L.sf_conv_bwd_workspace_bytes(ctypes.byref(conv_shape(C=12))) == 0
+    assert L.sf_conv_bwd_workspace_bytes(None) == 0
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=0), _lib.SF_E_SHAPE),
+    (dict(L=-1), _lib.SF_E_SHAPE),
+    (dict(C=12), _lib.SF_E_UNSUPPORTED),
+    (dict(W=5), _lib.SF_E_UNSUPPORTED),
+    (dict(W=0), _lib.SF_E_UNSUPPORTED),
+    (dict(io_dtype=7), _lib.SF_E_DTYPE),
+    (dict(act=3), _lib.SF_E_DTYPE),
+    (dict(reserved=1), _lib.SF_E_SHAPE),
+    (dict(sx_b=1000 * 64, sx_l=32), _lib.SF_E_SHAPE),          # rows overlap
+    (dict(sx_b=1000 * 68, sx_l=68), _lib.SF_E_ALIGN),          # 136-byte rows
+])
+def test_conv_shape_validation(kw, status):
+    assert conv_fwd(conv_shape(**kw)) == status
+    assert _lib.lib().sf_last_error() != b""
+
+
+def test_conv_pointer_validation():
+    s = conv_shape()
+    assert conv_fwd(None) == _lib.SF_E_NULL
+    assert conv_fwd(s, x=None) == _lib.SF_E_NULL
+    assert conv_fwd(s, w=None) == _lib.SF_E_NULL
+    rc = _lib.lib().sf_conv_fwd(ctypes.byref(s), ctypes.c_void_p(FAKE + 8), p(2), p(3), p(4), p(5), None)
+    assert rc == _lib.SF_E_ALIGN
+    assert conv_fwd(s, y=1) == _lib.SF_E_ALIAS          # y over x
+    assert conv_fwd(s, tail_out=2) == _lib.SF_E_ALIAS   # tail_out over w
+    assert conv_bwd(s, dw=None) == _lib.SF_E_NULL
+    assert conv_bwd(s, ws_bytes=16) == _lib.SF_E_WORKSPACE
+    assert conv_bwd(s, ws=None) == _lib.SF_E_WORKSPACE
+    assert conv_bwd(s, dx=4) == _lib.SF_E_ALIAS         # dx over dy
+    assert conv_bwd(s, dtail_in=9) == _lib.SF_E_ALIAS   # dtail_in inside the workspace

@@ -1,0 +1,162 @@
+"""GPU parity of the short convolution (libstateflow's sf_conv_fwd /
+sf_conv_bwd through the C ABI) against the fp64 oracle.
+
+Sizes span several token blocks (256 tokens per workgroup row) with a ragged
+last block, and more than one channel block (2048 channels per workgroup)
+with a ragged last one.  Edge cases: empty and shorter-than-tail segments, no
+tail, strided inputs, segments chained through their tails, run-to-run
+determinism, and the full-size workload checked on sampled channels.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_06838_amd as sf
+from paper_2608_06838_amd import synth
+
+from _helpers import assert_close, to64
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def gpu(d):
+    return {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in d.items()}
+
+
+def run_gpu(inp, act):
+    g = gpu(inp)
+    y, tail_out = sf.conv_fwd(g["x"], g["w"], g["tail_in"], act=act)
+    dx, dw, dtail_in = sf.conv_bwd(g["x"], g["w"], g["tail_in"], g["dy"], g["dtail_out"], act=act)
+    torch.cuda.synchronize()
+    return dict(y=y, tail_out=tail_out, dx=dx, dw=dw, dtail_in=dtail_in)
+
+
+def run_oracle(inp, act):
+    f = {k: (to64(v) if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
+    y, tail_out = oracle.conv_forward(f["x"], f["w"], f["tail_in"], act=act)
+    dx, dw, dtail_in = oracle.conv_backward(f["x"], f["w"], f["tail_in"], f["dy"], f["dtail_out"], act=act)
+    return dict(y=y, tail_out=tail_out, dx=dx, dw=dw, dtail_in=dtail_in)
+
+
+def compare(got, ref, io, W):
+    for name in ("y", "tail_out", "dx", "dw", "dtail_in"):
+        if W == 1 and name in ("tail_out", "dtail_in"):
+            assert got[name] is None
+            continue
+        if ref[name].size == 0:
+            continue
+        assert_close(name, to64(got[name]), ref[name], io)
+
+
+@pytest.mark.parametrize("io", ["bf16", "f32"])
+@pytest.mark.parametrize("W", [1, 2, 3, 4])
+@pytest.mark.parametrize("act", ["none", "silu"])
+def test_conv_parity(io, W, act):
+    B, L, C = 2, 700, 2048 + 64
+    say(f"[conv] io={io} W={W} act={act} B={B} L={L} C={C}")
+    inp = synth.make_conv_inputs(B, L, C, W, io=io, seed=3000 + 10 * W + (act == "silu"))
+    compare(run_gpu(inp, act), run_oracle(inp, act), io, W)
+
+
+@pytest.mark.parametrize("L", [0, 1, 2, 3, 255, 256, 257, 1536])
+def test_conv_lengths(L):
+    W, C = 4, 64
+    say(f"[conv] lengths L={L}")
+    inp = synth.make_conv_inputs(2, L, C, W, io="bf16", seed=3100 + L)
+    got = run_gpu(inp, "silu")
+    ref = run_oracle(inp, "silu")
+    compare(got, ref, "bf16", W)
+    if L == 0:  # the tail passes through; dw is zero
+        assert torch.equal(got["tail_out"].cpu(), inp["tail_in"])
+        assert torch.equal(got["dtail_in"].cpu(), inp["dtail_out"])
+        assert not got["dw"].abs().max().item()
+
+
+def test_conv_no_tails():
+    say("[conv] no tails (start of a sequence)")
+    inp = synth.make_conv_inputs(1, 300, 128, 4, io="bf16", seed=3200, tails=False)
+    compare(run_gpu(inp, "silu"), run_oracle(inp, "silu"), "bf16", 4)
+
+
+def test_conv_strided():
+    """x and dy as views of wider rows (row stride C + 64, batch stride padded)."""
+    B, L, C, W = 2, 333, 256, 3
+    say(f"[conv] strided rows B={B} L={L} C={C}")
+    inp = synth.make_conv_inputs(B, L, C, W, io="bf16", seed=3300)
+    g = gpu(inp)
+    big_x = torch.zeros(B, L + 3, C + 64, dtype=torch.bfloat16, device=DEV)
+    big_dy = torch.zeros_like(big_x)
+    big_x[:, :L, :C] = g["x"]
+    big_dy[:, :L, :C] = g["dy"]
+    x, dy = big_x[:, :L, :C], big_dy[:, :L, :C]
+    y, tail_out = sf.conv_fwd(x, g["w"], g["tail_in"], act="silu")
+    dx, dw, dtail_in = sf.conv_bwd(x, g["w"], g["tail_in"], dy, g["dtail_out"], act="silu")
+    torch.cuda.synchronize()
+    assert y.stride() == x.stride() and dx.stride() == x.stride()
+    compare(dict(y=y, tail_out=tail_out, dx=dx, dw=dw, dtail_in=dtail_in), run_oracle(inp, "silu"), "bf16", W)
+
+
+def test_conv_chained_segments_and_determinism():
+    """Segments chained through their tails (one shorter than the tail) match
+    the oracle over the whole sequence; the backward runs last to first with
+    dtail_in of segment i+1 as dtail_out of segment i.  Two runs are bitwise
+    equal."""
+    B, C, W = 2, 512, 4
+    segs = [300, 2, 700, 64]
+    L = sum(segs)
+    say(f"[conv] chained segments {segs}")
+    inp = synth.make_conv_inputs(B, L, C, W, io="bf16", seed=3400)
+    g = gpu(inp)
+    ref = run_oracle(inp, "silu")
+
+    def chain():
+        ys, tails, t = [], [g["tail_in"]], 0
+        for n in segs:
+            y, to = sf.conv_fwd(g["x"][:, t:t + n], g["w"], tails[-1], act="silu")
+            ys.append(y)
+            tails.append(to)
+            t += n
+        dxs, dw_sum, dt = [], torch.zeros_like(g["w"]), g["dtail_out"]
+        for i in reversed(range(len(segs))):
+            t -= segs[i]
+            dx, dw, dt = sf.conv_bwd(g["x"][:, t:t + segs[i]], g["w"], tails[i], g["dy"][:, t:t + segs[i]], dt,
+                                     act="silu")
+            dxs.insert(0, dx)
+            dw_sum += dw
+        torch.cuda.synchronize()
+        return dict(y=torch.cat(ys, 1), tail_out=tails[-1], dx=torch.cat(dxs, 1), dw=dw_sum, dtail_in=dt)
+
+    a = chain()
+    compare(a, ref, "bf16", W)
+    b = chain()
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+
+
+def test_conv_full_size_sampled():
+    """The measured workload's longest segment (65536 tokens, 15360 channels:
+    the q, k, v projections of 40 heads of 128) on the GPU, checked on sampled
+    channel groups (the convolution is per channel, so the oracle runs on those
+    channels alone)."""
+    w = synth.conv_workload("conv_ctx256k")
+    B, C, W, L = w["B"], w["C"], w["W"], w["seg_lens"][0]
+    say(f"[conv] full size B={B} L={L} C={C} W={W}")
+    inp = synth.make_conv_inputs(B, L, C, W, io=w["io"], seed=3500, device=DEV)
+    got = run_gpu(inp, w["act"])
+    cols = np.concatenate([np.arange(0, 8), np.arange(2040, 2056), np.arange(7680, 7688), np.arange(C - 8, C)])
+    idx = torch.from_numpy(cols).to(DEV)
+
+    def pick(v):
+        return v[..., idx] if v.dim() == 3 else v[idx]
+
+    sub = {k: (pick(v).cpu() if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
+    del inp
+    ref = run_oracle(sub, w["act"])
+    got_sub = {k: pick(v) for k, v in got.items()}
+    compare(got_sub, ref, "bf16", W)
