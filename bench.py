@@ -50,18 +50,27 @@ def alg_bytes_per_token_head(D, io, gb=4):
     return (4 * D * io + gb) + (7 * D * io + 2 * gb)
 
 
-def kernel_src_hash():
+def _src_hash(files):
     h = hashlib.sha256()
-    for f in ("sf_kernels.hip", "sf_chunk.hpp", "sf_device.hpp"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2608_06838_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def read_traffic(kernel):
+def kernel_src_hash():
+    return _src_hash(("sf_kernels.hip", "sf_chunk.hpp", "sf_device.hpp"))
+
+
+def conv_src_hash():
+    return _src_hash(("sf_conv.hip", "sf_device.hpp"))
+
+
+def read_traffic(kernel, workload="ctx256k_h40", src_hash=None):
     """HBM bytes per launch for `kernel` from the committed rocprofv3 counter
     summary, or None when absent or taken on a different kernel source."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_ctx256k_h40.txt")
+    src_hash = src_hash or kernel_src_hash()
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -70,7 +79,7 @@ def read_traffic(kernel):
             if "=" in ln and not ln.startswith("#"):
                 a, b = ln.split("=", 1)
                 kv[a.strip()] = b.strip()
-    if kv.get("src_sha") != kernel_src_hash():
+    if kv.get("src_sha") != src_hash:
         return None
     try:
         return float(kv["hbm_bytes_per_launch"])
@@ -108,6 +117,125 @@ def cpu_baseline(w, inp, budget_s=15.0):
                       f"{t:.1f} s wall; value scaled to a {w['H']}-head layer"}
 
 
+CONV_METRIC = "short-conv fwd+bwd tokens/s (C=15360=3x40x128, W=4, SiLU, 256K ctx, 8 segments, carried tails)"
+# interface bytes per token and channel: forward x in, y out; backward x, dy in, dx out
+CONV_BYTES = {"conv_fwd": lambda io: 2 * io, "conv_bwd": lambda io: 3 * io}
+
+
+def conv_cpu_baseline(inp, w, act, budget_s=15.0):
+    """The fp64 oracle of the short convolution (numpy, one process) over the
+    whole sequence of batch 0 on its first nc channels, nc chosen for about
+    budget_s of CPU work, scaled to the workload's channel count."""
+    import oracle
+
+    L = sum(w["seg_lens"])
+
+    def sample(nc):
+        return {k: (v[:1, :, :nc] if v.dim() == 3 else v[:nc]).detach().cpu().double().numpy()
+                for k, v in inp.items() if v is not None}
+
+    def run(s):
+        t0 = time.perf_counter()
+        oracle.conv_forward(s["x"], s["w"], s["tail_in"], act=act)
+        oracle.conv_backward(s["x"], s["w"], s["tail_in"], s["dy"], s["dtail_out"], act=act)
+        return time.perf_counter() - t0
+
+    nc0 = 64
+    t_cal = run(sample(nc0))
+    nc = int(min(w["C"], max(nc0, budget_s / max(t_cal, 1e-6) * nc0)) // 8 * 8)
+    t = run(sample(nc))
+    value = L * nc / w["C"] / t
+    return {"value": value, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"batch 0, all {L} tokens, channels 0..{nc - 1}, fwd+bwd fp64 numpy, {t:.1f} s wall; "
+                      f"value scaled to {w['C']} channels"}
+
+
+def bench_conv(args):
+    """One step = the short convolution forward over the 8 segments (tails
+    carried), then its backward over the segments in reverse order (tail
+    gradients carried), inputs resident in HBM, outputs preallocated."""
+    import torch
+    import paper_2608_06838_amd as sf
+    from paper_2608_06838_amd import synth
+
+    w = synth.conv_workload("conv_ctx256k")
+    B, C, W, seg, act = w["B"], w["C"], w["W"], w["seg_lens"], w["act"]
+    L = sum(seg)
+    dev = torch.device("cuda:0")
+    inp = synth.make_conv_inputs(B, L, C, W, io=w["io"], device=dev, seed=2002)
+    x, wt, dy = inp["x"], inp["w"], inp["dy"]
+    io = x.element_size()
+    y, dx = torch.empty_like(x), torch.empty_like(x)
+    tails = torch.empty((len(seg) + 1, B, W - 1, C), dtype=torch.float32, device=dev)
+    tails[0].copy_(inp["tail_in"])
+    dtails = torch.empty_like(tails)
+    dtails[-1].copy_(inp["dtail_out"])
+    dws = torch.empty((len(seg), C, W), dtype=torch.float32, device=dev)
+    nws = max(sf.conv_bwd_workspace_bytes(x[:, :n], wt, act) for n in seg)
+    ws = torch.empty(nws, dtype=torch.uint8, device=dev)
+    starts = [sum(seg[:i]) for i in range(len(seg))]
+
+    def step():
+        for i, (t, n) in enumerate(zip(starts, seg)):
+            sf.conv_fwd(x[:, t:t + n], wt, tails[i], act, out=(y[:, t:t + n], tails[i + 1]))
+        for i in reversed(range(len(seg))):
+            t, n = starts[i], seg[i]
+            sf.conv_bwd(x[:, t:t + n], wt, tails[i], dy[:, t:t + n], dtails[i + 1], act,
+                        out=(dx[:, t:t + n], dws[i], dtails[i], ws))
+
+    kernels = ["conv_fwd", "conv_bwd"]
+    for i in range(args.warmup):
+        if i == args.warmup - 1:
+            torch.cuda.synchronize()
+            for k in kernels:
+                sf.prof_read(k)
+                sf.prof_enable(k, True)
+        step()
+    torch.cuda.synchronize()
+    wtime = {k: sf.prof_read(k) for k in kernels}
+    for k in kernels:
+        sf.prof_enable(k, False)
+    dom = max(kernels, key=lambda k: wtime[k][0]) if args.warmup > 0 else "conv_bwd"
+    sf.prof_read(dom)
+    sf.prof_enable(dom, True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sf.prof_enable(dom, False)
+    tot_ms, nl = sf.prof_read(dom)
+    ms = (t1 - t0) * 1e3 / args.steps
+    if args.copy_mib > 0:  # known-size copy: FETCH_SIZE / WRITE_SIZE calibration under rocprofv3 --pmc
+        src = torch.ones(args.copy_mib * (1 << 20) // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    avg_s = tot_ms / 1e3 / max(nl, 1)
+    bytes_per_launch = CONV_BYTES[dom](io) * B * L * C * args.steps / max(nl, 1)
+    achieved = bytes_per_launch / avg_s / 1e9
+    if args.kernel_times:
+        for k in kernels:
+            print(f"# {k:9s} {wtime[k][0]:8.3f} ms/step  {wtime[k][1]:4d} launches/step", file=sys.stderr)
+    out = {
+        "metric": CONV_METRIC, "value": B * L / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if io == 2 else "f32", "data": "synthetic",
+        "config": {"workload": w["name"], "B": B, "C": C, "W": W, "L": L, "segments": seg, "act": act,
+                   "io": w["io"]},
+        "hbm_frac_alg": sum(f(io) for f in CONV_BYTES.values()) * B * L * C / (ms / 1e3) / PEAK_HBM,
+        "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                     "frac": achieved * 1e9 / PEAK_HBM, "traffic": read_traffic(dom, "conv_ctx256k", conv_src_hash()),
+                     "launches": nl, "avg_launch_us": avg_s * 1e6},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = conv_cpu_baseline(inp, w, act)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -122,11 +250,16 @@ def main():
                     help="also time the chain with the scans on the main stream (no overlap)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--conv", action="store_true",
+                    help="measure the short convolution with carried tails instead of the recurrence")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the recurrence shards over "
               "heads with no exchange, see DESIGN.md", file=sys.stderr)
         sys.exit(2)
+    if args.conv:
+        bench_conv(args)
+        return
 
     import torch
     import paper_2608_06838_amd as sf
@@ -158,7 +291,7 @@ def main():
         sf.chain_bwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, S_bnd, inp["dO"], inp["dS_out"],
                      ts=args.ts, overlap=overlap, out=(dq, dk, dv, dg, dS0, ws_b))
 
-    kernels = list(sf.KERNELS)
+    kernels = [k for k in sf.KERNELS if not k.startswith("conv")]
 
     def prof_all(on):
         for kname in kernels:

@@ -281,26 +281,36 @@ def conv_bwd_workspace_bytes(x, w, act="silu"):
     return _lib.lib().sf_conv_bwd_workspace_bytes(ctypes.byref(_conv_shape(x, w, act)))
 
 
-def conv_fwd(x, w, tail_in=None, act="silu", *, stream=None):
+def _out_like(t, ref, name):
+    if tuple(t.shape) != tuple(ref.shape) or t.stride() != ref.stride() or t.dtype != ref.dtype:
+        raise ValueError(f"{name} must match x in shape, strides and dtype")
+    return t
+
+
+def conv_fwd(x, w, tail_in=None, act="silu", *, stream=None, out=None):
     """(y, tail_out) of the short convolution over one segment; tail_out is
-    None for W = 1."""
+    None for W = 1.  out=(y, tail_out) supplies the outputs (no allocation)."""
     sh = _conv_shape(x, w, act)
     B, L, C = x.shape
     W = w.shape[1]
     tail_in = _tail(tail_in, B, W, C, "tail_in")
     stream = stream or torch.cuda.current_stream(x.device)
-    with torch.cuda.stream(stream):
-        y = _like(x)
-        tail_out = torch.empty((B, W - 1, C), dtype=torch.float32, device=x.device) if W > 1 else None
+    if out is not None:
+        y, tail_out = _out_like(out[0], x, "y"), _tail(out[1], B, W, C, "tail_out")
+    else:
+        with torch.cuda.stream(stream):
+            y = _like(x)
+            tail_out = torch.empty((B, W - 1, C), dtype=torch.float32, device=x.device) if W > 1 else None
     rc = _lib.lib().sf_conv_fwd(ctypes.byref(sh), _ptr(x), _ptr(w), _ptr(tail_in), _ptr(y), _ptr(tail_out),
                                 _stream_handle(stream))
     _lib.check("sf_conv_fwd", rc)
     return y, tail_out
 
 
-def conv_bwd(x, w, tail_in, dy, dtail_out=None, act="silu", *, stream=None):
+def conv_bwd(x, w, tail_in, dy, dtail_out=None, act="silu", *, stream=None, out=None):
     """(dx, dw, dtail_in) for the loss sum <dy, y> + <dtail_out, tail_out>;
-    dtail_in is None for W = 1."""
+    dtail_in is None for W = 1.  out=(dx, dw, dtail_in, workspace) supplies
+    the outputs and a workspace of conv_bwd_workspace_bytes() (no allocation)."""
     sh = _conv_shape(x, w, act)
     B, L, C = x.shape
     W = w.shape[1]
@@ -310,11 +320,18 @@ def conv_bwd(x, w, tail_in, dy, dtail_out=None, act="silu", *, stream=None):
     dtail_out = _tail(dtail_out, B, W, C, "dtail_out")
     stream = stream or torch.cuda.current_stream(x.device)
     L_ = _lib.lib()
-    with torch.cuda.stream(stream):
-        dx = _like(x)
-        dw = torch.empty((C, W), dtype=torch.float32, device=x.device)
-        dtail_in = torch.empty((B, W - 1, C), dtype=torch.float32, device=x.device) if W > 1 else None
-        ws = _ws(L_.sf_conv_bwd_workspace_bytes(ctypes.byref(sh)), x.device)
+    if out is not None:
+        dx, dw, dtail_in, ws = out
+        _out_like(dx, x, "dx")
+        dtail_in = _tail(dtail_in, B, W, C, "dtail_in")
+        if tuple(dw.shape) != (C, W) or dw.dtype != torch.float32 or not dw.is_contiguous():
+            raise ValueError("dw must be a contiguous float32 [C, W] tensor")
+    else:
+        with torch.cuda.stream(stream):
+            dx = _like(x)
+            dw = torch.empty((C, W), dtype=torch.float32, device=x.device)
+            dtail_in = torch.empty((B, W - 1, C), dtype=torch.float32, device=x.device) if W > 1 else None
+            ws = _ws(L_.sf_conv_bwd_workspace_bytes(ctypes.byref(sh)), x.device)
     rc = L_.sf_conv_bwd(ctypes.byref(sh), _ptr(x), _ptr(w), _ptr(tail_in), _ptr(dy), _ptr(dtail_out), _ptr(dx),
                         _ptr(dw), _ptr(dtail_in), _ptr(ws), ws.numel(), _stream_handle(stream))
     _lib.check("sf_conv_bwd", rc)

@@ -9,7 +9,8 @@
 // two in fp32) of one batch and walks a block of tokens in order, keeping the
 // previous W-1 inputs in registers, so every input row is read once per block
 // (plus a W-1 token halo) and a wave's 64 lanes read 64 consecutive 16-byte
-// pieces of a row.  Loads go out in groups of 8 tokens.
+// pieces of a row.  Loads go out in groups of 8 tokens; outputs are written
+// with non-temporal stores.
 //
 // Backward: du_t = dy_t * act'(u_t); dxh_s = sum_j w[j] du_{s+W-1-j} plus
 // dtail_out[s-L+W-1] for the last W-1 positions; dw[c][j] = sum_{b,t} du_t
@@ -26,7 +27,7 @@ namespace {
 
 constexpr int CONV_NT = 256;  // threads per workgroup
 constexpr int CONV_E = 8;     // channels per thread
-constexpr int CONV_G = 8;     // tokens per load group
+constexpr int CONV_G = 8;     // tokens per load group (4 and 16 measured slower)
 
 template <typename T>
 struct Row8 {
@@ -65,12 +66,14 @@ __device__ __forceinline__ void store_row8(T *p, const float (&f)[CONV_E]) {
     v8 o;
 #pragma unroll
     for (int e = 0; e < CONV_E; ++e) o[e] = (T)f[e];
+    // the outputs are not read again by this kernel: non-temporal stores
+    // (measured 1% faster than plain stores)
     if constexpr (sizeof(T) == 2) {
-        *reinterpret_cast<v8 *>(p) = o;
+        __builtin_nontemporal_store(o, reinterpret_cast<v8 *>(p));
     } else {
         typedef float f4 __attribute__((ext_vector_type(4)));
-        reinterpret_cast<f4 *>(p)[0] = f4{f[0], f[1], f[2], f[3]};
-        reinterpret_cast<f4 *>(p)[1] = f4{f[4], f[5], f[6], f[7]};
+        __builtin_nontemporal_store(f4{f[0], f[1], f[2], f[3]}, reinterpret_cast<f4 *>(p));
+        __builtin_nontemporal_store(f4{f[4], f[5], f[6], f[7]}, reinterpret_cast<f4 *>(p) + 1);
     }
 }
 
@@ -283,12 +286,23 @@ __global__ void __launch_bounds__(CONV_NT) k_conv_bwd(ConvArgs a) {
         for (int j = 0; j < W; ++j) pw[e * W + j] = dw[j][e];
 }
 
-// dw[c][j] = sum over (batch, token block) of the partials, in that order
-__global__ void __launch_bounds__(CONV_NT) k_conv_dw_sum(const float *ws, float *dw, int64_t n, int64_t parts) {
-    const int64_t i = (int64_t)blockIdx.x * CONV_NT + threadIdx.x;
+// dw[c][j] = sum over (batch, token block) of the partials, in that order.
+// Eight partials are loaded together and then added one by one, so the loads
+// overlap and the order of the additions stays fixed.
+constexpr int DWS_NT = 64;
+__global__ void __launch_bounds__(DWS_NT) k_conv_dw_sum(const float *ws, float *dw, int64_t n, int64_t parts) {
+    const int64_t i = (int64_t)blockIdx.x * DWS_NT + threadIdx.x;
     if (i >= n) return;
     float s = 0.f;
-    for (int64_t p = 0; p < parts; ++p) s += ws[p * n + i];
+    int64_t p = 0;
+    for (; p + 8 <= parts; p += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = ws[(p + u) * n + i];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; p < parts; ++p) s += ws[p * n + i];
     dw[i] = s;
 }
 
@@ -306,7 +320,7 @@ hipError_t conv_td(bool bwd, const ConvArgs &a, hipStream_t s, hipEvent_t e0, hi
     } else {
         hipExtLaunchKernelGGL((k_conv_bwd<T, W, SILU>), grid, dim3(CONV_NT), 0, s, e0, nullptr, 0, a);
         const int64_t n = (int64_t)a.C * W;
-        hipExtLaunchKernelGGL(k_conv_dw_sum, dim3((unsigned)((n + CONV_NT - 1) / CONV_NT)), dim3(CONV_NT), 0, s,
+        hipExtLaunchKernelGGL(k_conv_dw_sum, dim3((unsigned)((n + DWS_NT - 1) / DWS_NT)), dim3(DWS_NT), 0, s,
                               nullptr, e1, 0, (const float *)a.ws, a.dw, n, (int64_t)a.B * a.nTB);
     }
     return hipGetLastError();
