@@ -222,6 +222,26 @@ sf_status sf_conv_bwd(const sf_conv_shape *shape, const void *x, const float *w,
                       void *ws, size_t ws_bytes, sf_stream stream);
 
 /*
+ * Hybrid-aware segment lengths (Sec. 3.2, Hybrid-Aware Sequence Chunking):
+ * host-only, no device work.  For a sequence of T tokens cut into N segments
+ * with boundaries 0 = c_0 < c_1 < ... < c_N = T, the paper prices segment i at
+ *     Cost_i = w_tok * s_i + w_soft * (c_i * s_i + s_i^2 / 2),   s_i = c_{i+1} - c_i,
+ * where w_tok = L_lin * C_lin + C_dense (per-token FLOPs of the linear
+ * recurrence layers and the dense work) and w_soft = L_soft * C_soft (FLOPs
+ * per query-key pair of the softmax layers).  The balanced boundaries
+ * c_i^hybrid make every Cost_i equal; the candidates are
+ *     c_i(alpha) = (1 - alpha) * i * T / N + alpha * c_i^hybrid,
+ * each rounded to the closest multiple of `round_to` (half-way cases round
+ * up).  seg_len[0..N-1] receives c_{i+1} - c_i.
+ *   T > 0 and a multiple of round_to; N >= 1; round_to >= 1; alpha >= 0;
+ *   w_tok >= 0, w_soft >= 0, not both 0.
+ * SF_E_SHAPE if an argument is out of range or rounding leaves a segment
+ * empty; SF_E_NULL if seg_len is NULL.
+ */
+sf_status sf_partition_hybrid(int64_t T, int32_t N, double alpha, double w_tok, double w_soft, int32_t round_to,
+                              int64_t *seg_len);
+
+/*
  * Kernel timing for measurement: while enabled, every launch of kernel
  * `kernel_id` (an sf_kernel_id) carries HIP events that take the begin and
  * end timestamps of its own dispatch.  sf_prof_read() synchronises those

@@ -30,7 +30,7 @@ from ._lib import KERNELS, StateflowError  # noqa: F401
 
 __all__ = ["segment_fwd", "segment_bwd", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
            "bwd_workspace_bytes", "chain_workspace_bytes", "conv_fwd", "conv_bwd", "conv_bwd_workspace_bytes",
-           "prof_enable", "prof_read", "StateflowError", "abi_version"]
+           "partition_hybrid", "prof_enable", "prof_read", "StateflowError", "abi_version"]
 
 _IO = {torch.bfloat16: _lib.SF_BF16, torch.float32: _lib.SF_F32}
 _aux_streams = {}
@@ -336,6 +336,17 @@ def conv_bwd(x, w, tail_in, dy, dtail_out=None, act="silu", *, stream=None, out=
                         _ptr(dw), _ptr(dtail_in), _ptr(ws), ws.numel(), _stream_handle(stream))
     _lib.check("sf_conv_bwd", rc)
     return dx, dw, dtail_in
+
+
+def partition_hybrid(T, N, alpha, w_tok, w_soft, round_to=128):
+    """Segment lengths of the hybrid-aware chunking (host-only, no GPU): N
+    segments of a T-token sequence whose boundaries interpolate, by alpha,
+    between equal lengths and the partition that equalises the per-segment
+    cost w_tok * s + w_soft * (c * s + s^2 / 2)."""
+    out = (ctypes.c_int64 * int(N))()
+    _lib.check("sf_partition_hybrid", _lib.lib().sf_partition_hybrid(int(T), int(N), float(alpha), float(w_tok),
+                                                                      float(w_soft), int(round_to), out))
+    return [int(x) for x in out]
 
 
 def prof_enable(kernel, on=True):

@@ -21,7 +21,7 @@ SF_ACT_NONE, SF_ACT_SILU = 0, 1
 # every symbol include/stateflow.h declares
 EXPORTS = ["sf_abi_version", "sf_status_str", "sf_last_error", "sf_fwd_workspace_bytes",
            "sf_bwd_workspace_bytes", "sf_segment_fwd", "sf_segment_bwd", "sf_chain_workspace_bytes",
-           "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd",
+           "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd", "sf_partition_hybrid",
            "sf_prof_enable", "sf_prof_read"]
 
 
@@ -96,6 +96,8 @@ def lib():
     L.sf_conv_fwd.argtypes = [cp] + [vp] * 5 + [vp]
     L.sf_conv_bwd.restype = ctypes.c_int
     L.sf_conv_bwd.argtypes = [cp] + [vp] * 9 + [sz, vp]
+    L.sf_partition_hybrid.restype = ctypes.c_int
+    L.sf_partition_hybrid.argtypes = [i64, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double, i32, i64p]
     L.sf_prof_enable.restype = ctypes.c_int
     L.sf_prof_enable.argtypes = [i32, i32]
     L.sf_prof_read.restype = ctypes.c_int

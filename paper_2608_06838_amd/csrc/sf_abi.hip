@@ -871,6 +871,40 @@ sf_status sf_conv_bwd(const sf_conv_shape *shape, const void *x, const float *w,
     return conv_run(SF_K_CONV_BWD, true, a, (hipStream_t)stream);
 }
 
+sf_status sf_partition_hybrid(int64_t T, int32_t N, double alpha, double w_tok, double w_soft, int32_t round_to,
+                              int64_t *seg_len) {
+    if (!seg_len) return fail(SF_E_NULL, "seg_len is NULL");
+    if (T <= 0 || N < 1 || round_to < 1 || T % round_to)
+        return fail(SF_E_SHAPE, "need T > 0 a multiple of round_to >= 1 and N >= 1 (T=%lld N=%d round_to=%d)",
+                    (long long)T, N, round_to);
+    if (!(alpha >= 0.0) || !(w_tok >= 0.0) || !(w_soft >= 0.0) || !(w_tok + w_soft > 0.0) || !std::isfinite(alpha) ||
+        !std::isfinite(w_tok) || !std::isfinite(w_soft))
+        return fail(SF_E_SHAPE, "need alpha >= 0, w_tok >= 0, w_soft >= 0, not both weights 0");
+    // accumulated cost A(c) = w_tok c + w_soft c^2 / 2 (Cost_i = A(c_{i+1}) - A(c_i));
+    // the balanced boundary solves A(c) = (i / N) A(T), the positive root of a
+    // quadratic, written in the cancellation-free form 2 r / (w_tok + sqrt(w_tok^2 + 2 w_soft r))
+    const double Td = (double)T, total = w_tok * Td + 0.5 * w_soft * Td * Td;
+    int64_t prev = 0;
+    for (int32_t i = 1; i <= N; ++i) {
+        int64_t c;
+        if (i == N) {
+            c = T;
+        } else {
+            const double r = total * (double)i / (double)N;
+            const double hyb = 2.0 * r / (w_tok + std::sqrt(w_tok * w_tok + 2.0 * w_soft * r));
+            const double equal = Td * (double)i / (double)N;
+            const double x = (1.0 - alpha) * equal + alpha * hyb;
+            c = (int64_t)std::floor(x / round_to + 0.5) * round_to;
+        }
+        if (c <= prev || c > T)
+            return fail(SF_E_SHAPE, "segment %d is empty or out of range after rounding (boundary %lld)", i - 1,
+                        (long long)c);
+        seg_len[i - 1] = c - prev;
+        prev = c;
+    }
+    return SF_OK;
+}
+
 sf_status sf_prof_enable(int32_t kernel_id, int32_t on) {
     if (kernel_id < 0 || kernel_id >= SF_K_COUNT) return fail(SF_E_SHAPE, "unknown kernel id %d", kernel_id);
     std::lock_guard<std::mutex> lk(g_prof_mu);
