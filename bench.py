@@ -236,6 +236,98 @@ def bench_conv(args):
     print(json.dumps(out), flush=True)
 
 
+def make_chain_step(sf, torch, inp, seg, ts, overlap):
+    """fwd+bwd chain over segments `seg` with preallocated outputs and
+    workspaces (the step allocates nothing)."""
+    dev = inp["q"].device
+    B, L, H, D = inp["q"].shape
+    o = torch.empty_like(inp["q"])
+    S_bnd = torch.empty((len(seg) + 1, B, H, D, D), dtype=torch.float32, device=dev)
+    nws = sf.chain_workspace_bytes(inp["q"], inp["g"], seg, ts=ts)
+    ws_f = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    ws_b = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    dq, dk, dv = (torch.empty_like(inp["q"]) for _ in range(3))
+    dg = torch.empty_like(inp["g"])
+    dS0 = torch.empty((B, H, D, D), dtype=torch.float32, device=dev)
+
+    def step():
+        sf.chain_fwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, inp["S_in"], ts=ts, overlap=overlap,
+                     out=(o, S_bnd, ws_f))
+        sf.chain_bwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, S_bnd, inp["dO"], inp["dS_out"],
+                     ts=ts, overlap=overlap, out=(dq, dk, dv, dg, dS0, ws_b))
+    return step
+
+
+def time_steps(torch, step, warmup, steps):
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+# Hybrid cost model of the partition study (the paper gives the form of the
+# per-segment cost, not its coefficients).  A 15B-class period-4 hybrid stack,
+# hidden d = 5120: per 4 layers, 3 linear-recurrence layers and 1 softmax layer,
+# each with q/k/v/o projections (8 d^2 FLOPs per token) and an MLP of width 4d
+# (16 d^2); softmax attention costs 4 d FLOPs per query-key pair (QK^T and AV).
+HYBRID_D = 5120
+HYBRID_W_TOK = 3 * 8 * HYBRID_D ** 2 + 4 * 16 * HYBRID_D ** 2 + 8 * HYBRID_D ** 2
+HYBRID_W_SOFT = 4 * HYBRID_D
+
+
+def study_main(args):
+    """--tune-ts / --partition-study: time the recurrence layer's fwd+bwd chain
+    per candidate and print one JSON line with the table (Sec. 3.2 / 3.4
+    selection by profiling)."""
+    import torch
+    import paper_2608_06838_amd as sf
+    from paper_2608_06838_amd import synth, tune
+
+    w = synth.workload(args.workload)
+    dev = torch.device("cuda:0")
+    inp = synth.make_inputs(w, device=dev, seed=1002)
+    T = inp["q"].shape[1]
+    if args.tune_ts:
+        cands = [(ts, ov) for ts in tune.ts_candidates(w["seg_lens"]) for ov in (True, False)]
+
+        def time_fn(c):
+            return time_steps(torch, make_chain_step(sf, torch, inp, w["seg_lens"], c[0], c[1]), 1, args.steps)
+
+        best, table = tune.search(cands, time_fn)
+        sp = tune.speedups(table, (0, True))
+        rows = [dict(ts=r["candidate"][0] or "auto", overlap=r["candidate"][1], ms=r["ms"], status=r["status"],
+                     speedup_vs_auto_overlap=x) for r, x in zip(table, sp)]
+        out = dict(study="superchunk stride and scan overlap", workload=w["name"], steps=args.steps, table=rows,
+                   best=dict(ts=best[0] or "auto", overlap=best[1]) if best else None)
+    else:
+        cands = tune.partition_candidates(T, HYBRID_W_TOK, HYBRID_W_SOFT)
+
+        def time_fn(c):
+            return time_steps(torch, make_chain_step(sf, torch, inp, c[2], 0, True), 1, args.steps)
+
+        best, table = tune.search(cands, time_fn)
+        sp = tune.speedups(table, next((c for c in cands if c[0] == 8 and c[1] == 0.0), None))
+        rows = []
+        for r, x in zip(table, sp):
+            N, a, lens = r["candidate"]
+            bnd = [0]
+            for n in lens:
+                bnd.append(bnd[-1] + n)
+            costs = [HYBRID_W_TOK * (b1 - b0) + HYBRID_W_SOFT * (b0 * (b1 - b0) + 0.5 * (b1 - b0) ** 2)
+                     for b0, b1 in zip(bnd[:-1], bnd[1:])]
+            rows.append(dict(N=N, alpha=a, seg_lens=lens, recurrence_ms=r["ms"], status=r["status"],
+                             speedup_vs_equal8=x, hybrid_cost_max_over_mean=max(costs) / (sum(costs) / len(costs))))
+        out = dict(study="hybrid-aware partition (recurrence layer timed; hybrid cost modelled)",
+                   workload=w["name"], steps=args.steps,
+                   cost_model=dict(w_tok=HYBRID_W_TOK, w_soft=HYBRID_W_SOFT, note="period-4 hybrid, hidden 5120"),
+                   table=rows, best_for_the_recurrence=dict(N=best[0], alpha=best[1]) if best else None)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -252,6 +344,10 @@ def main():
                     help="after timing, run one plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--conv", action="store_true",
                     help="measure the short convolution with carried tails instead of the recurrence")
+    ap.add_argument("--tune-ts", action="store_true",
+                    help="time the chain for each superchunk stride and overlap setting (one JSON table)")
+    ap.add_argument("--partition-study", action="store_true",
+                    help="time the chain for the hybrid-aware partition candidates (one JSON table)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the recurrence shards over "
@@ -259,6 +355,9 @@ def main():
         sys.exit(2)
     if args.conv:
         bench_conv(args)
+        return
+    if args.tune_ts or args.partition_study:
+        study_main(args)
         return
 
     import torch
