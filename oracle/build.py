@@ -13,10 +13,10 @@ LIB = os.path.join(OUT_DIR, "liboracle.so")
 
 def build(verbose: bool = False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
-    src = os.path.join(HERE, "sf_oracle.c")
+    srcs = [os.path.join(HERE, f) for f in ("sf_oracle.c", "gdn_oracle.c")]
     tmp = LIB + ".tmp"
     cmd = ["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
-           "-Wno-unused-parameter", src, "-o", tmp, "-lm"]
+           "-Wno-unused-parameter", *srcs, "-o", tmp, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
