@@ -242,6 +242,22 @@ sf_status sf_partition_hybrid(int64_t T, int32_t N, double alpha, double w_tok, 
                               int64_t *seg_len);
 
 /*
+ * Gated delta rule (Gated DeltaNet, the scalar-plus-low-rank transition of
+ * Sec. 2.1), forward over one segment:
+ *     S_t = a_t (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T,   o_t = S_t^T q_t,
+ * a_t = exp(g_t), S stored as [Dk][Dv] (the transpose of the paper's S).
+ * q, k, v, o as for sf_segment_fwd (shape->io_dtype must be SF_BF16,
+ * Dk == Dv in {64, 128}, scalar gate); g and beta are float32 [B][L][H] with
+ * the gate strides of `shape`; S_in may be NULL (zero state); S_out receives
+ * the final state.  One workgroup walks each (batch, head) over the whole
+ * segment (no superchunk parallelism yet), so the call suits segments of a
+ * few thousand tokens or many heads.  Same ownership, validation, aliasing
+ * and error rules as the other entry points.
+ */
+sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const void *v, const float *g,
+                     const float *beta, const float *S_in, void *o, float *S_out, sf_stream stream);
+
+/*
  * Kernel timing for measurement: while enabled, every launch of kernel
  * `kernel_id` (an sf_kernel_id) carries HIP events that take the begin and
  * end timestamps of its own dispatch.  sf_prof_read() synchronises those
@@ -257,7 +273,8 @@ typedef enum {
     SF_K_BWD_DKV = 5,  /* dk, dv, dg by a reverse state-gradient walk (PG) */
     SF_K_CONV_FWD = 6, /* short convolution, forward */
     SF_K_CONV_BWD = 7, /* short convolution, backward (dx, dtail_in, dw partials and their sum) */
-    SF_K_COUNT = 8
+    SF_K_GDN_FWD = 8,  /* gated delta rule, forward walk */
+    SF_K_COUNT = 9
 } sf_kernel_id;
 
 sf_status sf_prof_enable(int32_t kernel_id, int32_t on);

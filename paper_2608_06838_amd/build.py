@@ -5,7 +5,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libstateflow.so")
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("sf_kernels.hip", "sf_kernels_vg.hip", "sf_conv.hip", "sf_abi.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("sf_kernels.hip", "sf_kernels_vg.hip", "sf_conv.hip", "sf_gdn.hip", "sf_abi.hip")]
 HEADERS = [os.path.join(HERE, "csrc", f) for f in ("sf_device.hpp", "sf_chunk.hpp", "sf_launch.hpp")] + [
     os.path.join(ROOT, "include", "stateflow.h")]
 

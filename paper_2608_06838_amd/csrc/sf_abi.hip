@@ -871,6 +871,54 @@ sf_status sf_conv_bwd(const sf_conv_shape *shape, const void *x, const float *w,
     return conv_run(SF_K_CONV_BWD, true, a, (hipStream_t)stream);
 }
 
+sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const void *v, const float *g,
+                     const float *beta, const float *S_in, void *o, float *S_out, sf_stream stream) {
+    Shape r;
+    TRY(resolve(shape, r));
+    if (r.io != SF_BF16) return fail(SF_E_UNSUPPORTED, "the gated delta rule needs bf16 I/O");
+    if (r.gate != SF_GATE_SCALAR) return fail(SF_E_UNSUPPORTED, "the gated delta rule takes a scalar gate");
+    if (!S_out || (r.L > 0 && (!q || !k || !v || !g || !beta || !o)))
+        return fail(SF_E_NULL, "q, k, v, g, beta, o and S_out are required");
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_in, "S_in"}, {S_out, "S_out"}}));
+    if (((uintptr_t)g | (uintptr_t)beta) % 4) return fail(SF_E_ALIGN, "g and beta must be 4-byte aligned");
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"), grange(r, g, r.L, "g"),
+                     grange(r, beta, r.L, "beta"), srange(r, S_in, 1, "S_in")},
+                    {xrange(r, o, r.L, "o"), srange(r, S_out, 1, "S_out")}));
+    sf::GdnArgs a{};
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.g = g;
+    a.beta = beta;
+    a.S_in = S_in;
+    a.o = o;
+    a.S_out = S_out;
+    a.B = r.B;
+    a.H = r.H;
+    a.L = r.L;
+    a.sx_b = r.sx_b;
+    a.sx_l = r.sx_l;
+    a.sx_h = r.sx_h;
+    a.sg_b = r.sg_b;
+    a.sg_l = r.sg_l;
+    a.sg_h = r.sg_h;
+    bool on;
+    {
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        on = g_prof_on[SF_K_GDN_FWD];
+    }
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (on && (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess))
+        return hip_fail(hipGetLastError(), "profiling event");
+    hipError_t e = sf::launch_gdn_fwd(a, r.D, (hipStream_t)stream, e0, e1);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    if (on) {
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        g_prof_ev[SF_K_GDN_FWD].push_back({e0, e1});
+    }
+    return SF_OK;
+}
+
 sf_status sf_partition_hybrid(int64_t T, int32_t N, double alpha, double w_tok, double w_soft, int32_t round_to,
                               int64_t *seg_len) {
     if (!seg_len) return fail(SF_E_NULL, "seg_len is NULL");

@@ -62,6 +62,17 @@ struct ConvArgs {
     int64_t L, T, sx_b, sx_l;
 };
 int conv_channels_per_thread();
+
+// Gated delta rule forward (sf_gdn.hip): one workgroup per (batch, head).
+struct GdnArgs {
+    const void *q, *k, *v;
+    const float *g, *beta, *S_in;
+    void *o;
+    float *S_out;
+    int32_t B, H;
+    int64_t L, sx_b, sx_l, sx_h, sg_b, sg_l, sg_h;
+};
+hipError_t launch_gdn_fwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_conv(bool bwd, const ConvArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 
 }  // namespace sf

@@ -121,3 +121,23 @@ def make_conv_inputs(B, L, C, W, io="bf16", device="cpu", seed=2000, tails=True)
     if not tails:
         tail_in = dtail_out = None
     return dict(x=x, w=w, tail_in=tail_in, dy=dy, dtail_out=dtail_out)
+
+
+def make_gdn_inputs(B, L, H, D, device="cpu", seed=4000, s_in_std=0.1, g_mu=3.0):
+    """Gated-delta-rule inputs, drawn in this order from one generator seeded
+    with `seed`: q, k, v ~ N(0, 1) [B, L, H, D] (k then L2-normalised per
+    token, as the delta rule assumes); x_g ~ N(g_mu, 1) and g = log(sigmoid(x_g));
+    x_b ~ N(0, 1) and beta = sigmoid(x_b) [B, L, H]; S_in ~ s_in_std * N(0, 1)
+    [B, H, D, D] (None when s_in_std == 0).  q, k, v are rounded to bf16; g,
+    beta and S_in are float32."""
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    f32 = dict(dtype=torch.float32, device=device, generator=gen)
+    q = torch.randn(B, L, H, D, **f32)
+    k = torch.randn(B, L, H, D, **f32)
+    k = k / k.norm(dim=-1, keepdim=True)
+    v = torch.randn(B, L, H, D, **f32)
+    g = torch.nn.functional.logsigmoid(torch.randn(B, L, H, **f32) + float(g_mu)).contiguous()
+    beta = torch.sigmoid(torch.randn(B, L, H, **f32)).contiguous()
+    S_in = torch.randn(B, H, D, D, **f32) * float(s_in_std) if s_in_std > 0 else None
+    return dict(q=q.to(torch.bfloat16), k=k.to(torch.bfloat16), v=v.to(torch.bfloat16), g=g, beta=beta, S_in=S_in)

@@ -194,3 +194,23 @@ def test_conv_pointer_validation():
     assert conv_bwd(s, ws=None) == _lib.SF_E_WORKSPACE
     assert conv_bwd(s, dx=4) == _lib.SF_E_ALIAS         # dx over dy
     assert conv_bwd(s, dtail_in=9) == _lib.SF_E_ALIAS   # dtail_in inside the workspace
+
+
+# ------------------------------------------------------------ gated delta rule
+def test_gdn_validation():
+    L = _lib.lib()
+
+    def call(s, q=1, k=2, v=3, g=4, beta=5, S_in=None, o=6, S_out=7):
+        args = [p(i) if i is not None else None for i in (q, k, v, g, beta, S_in, o, S_out)]
+        return L.sf_gdn_fwd(ctypes.byref(s) if s is not None else None, *args, None)
+
+    assert call(None) == _lib.SF_E_NULL
+    assert call(shape(io_dtype=_lib.SF_F32, Dk=64, Dv=64)) == _lib.SF_E_UNSUPPORTED
+    assert call(shape(gate=_lib.SF_GATE_VECTOR)) == _lib.SF_E_UNSUPPORTED
+    assert call(shape(L=100)) == _lib.SF_E_SHAPE
+    assert call(shape(), beta=None) == _lib.SF_E_NULL
+    assert call(shape(), S_out=None) == _lib.SF_E_NULL
+    assert call(shape(), o=1) == _lib.SF_E_ALIAS
+    assert call(shape(), S_out=5) == _lib.SF_E_ALIAS   # S_out over beta
+    rc = L.sf_gdn_fwd(ctypes.byref(shape()), ctypes.c_void_p(FAKE + 2), p(2), p(3), p(4), p(5), None, p(6), p(7), None)
+    assert rc == _lib.SF_E_ALIGN
