@@ -328,6 +328,70 @@ def study_main(args):
     print(json.dumps(out), flush=True)
 
 
+GDN_METRIC = "gated-delta-rule fwd tokens/s per layer (H=40,d=128, 256K ctx, 8 segments chained through S)"
+
+
+def bench_gdn(args):
+    """One step = the gated-delta-rule forward over the 8 segments of the
+    256K-context layer, the state carried from segment to segment."""
+    import torch
+    import paper_2608_06838_amd as sf
+    from paper_2608_06838_amd import synth
+
+    w = synth.workload("ctx256k_h40")
+    seg = w["seg_lens"]
+    B, H, D, L = w["B"], w["H"], w["D"], sum(seg)
+    dev = torch.device("cuda:0")
+    inp = synth.make_gdn_inputs(B, L, H, D, device=dev, seed=4002)
+    starts = [sum(seg[:i]) for i in range(len(seg))]
+
+    def step():
+        S = inp["S_in"]
+        for t, n in zip(starts, seg):
+            _, S = sf.gdn_fwd(inp["q"][:, t:t + n], inp["k"][:, t:t + n], inp["v"][:, t:t + n],
+                              inp["g"][:, t:t + n], inp["beta"][:, t:t + n], S)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    sf.prof_read("gdn_fwd")
+    sf.prof_enable("gdn_fwd", True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sf.prof_enable("gdn_fwd", False)
+    tot_ms, nl = sf.prof_read("gdn_fwd")
+    ms = (t1 - t0) * 1e3 / args.steps
+    io = 2
+    per_tok_head = 4 * D * io + 8  # q, k, v in, o out; g and beta
+    avg_s = tot_ms / 1e3 / max(nl, 1)
+    achieved = per_tok_head * B * H * L * args.steps / max(nl, 1) / avg_s / 1e9
+    out = {
+        "metric": GDN_METRIC, "value": B * L / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "gdn_ctx256k_h40", "B": B, "H": H, "Dk": D, "Dv": D, "L": L, "segments": seg,
+                   "parallelism": "one workgroup per (batch, head)"},
+        "roofline": {"kernel": "gdn_fwd", "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM / 1e9,
+                     "unit": "GB/s", "frac": achieved * 1e9 / PEAK_HBM, "traffic": None, "launches": nl,
+                     "avg_launch_us": avg_s * 1e6, "us_per_chunk": avg_s * 1e6 * len(seg) / (L / 64)},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import gdn as ogdn
+        nh = min(H, len(os.sched_getaffinity(0)))
+        L_s = 2048
+        sl = {k: inp[k][:1, :L_s, :nh].detach().cpu().double().numpy() for k in ("q", "k", "v", "g", "beta")}
+        tc = time.perf_counter()
+        ogdn.forward(sl["q"], sl["k"], sl["v"], sl["g"], sl["beta"], None, threads=nh)
+        tc = time.perf_counter() - tc
+        out["cpu_baseline"] = {"value": nh * L_s / H / tc, "unit": "tokens/s", "cores": nh, "kind": "oracle",
+                               "sample": f"batch 0, heads 0..{nh - 1}, first {L_s} tokens, fwd fp64, {tc:.1f} s wall; "
+                                         f"value scaled to a {H}-head layer"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -344,6 +408,7 @@ def main():
                     help="after timing, run one plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--conv", action="store_true",
                     help="measure the short convolution with carried tails instead of the recurrence")
+    ap.add_argument("--gdn", action="store_true", help="measure the gated-delta-rule forward instead")
     ap.add_argument("--tune-ts", action="store_true",
                     help="time the chain for each superchunk stride and overlap setting (one JSON table)")
     ap.add_argument("--partition-study", action="store_true",
@@ -355,6 +420,9 @@ def main():
         sys.exit(2)
     if args.conv:
         bench_conv(args)
+        return
+    if args.gdn:
+        bench_gdn(args)
         return
     if args.tune_ts or args.partition_study:
         study_main(args)
