@@ -349,7 +349,7 @@ def bench_gdn(args):
         S = inp["S_in"]
         for t, n in zip(starts, seg):
             _, S = sf.gdn_fwd(inp["q"][:, t:t + n], inp["k"][:, t:t + n], inp["v"][:, t:t + n],
-                              inp["g"][:, t:t + n], inp["beta"][:, t:t + n], S)
+                              inp["g"][:, t:t + n], inp["beta"][:, t:t + n], S, ts=args.gdn_ts)
 
     for _ in range(args.warmup):
         step()
@@ -373,7 +373,8 @@ def bench_gdn(args):
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "gdn_ctx256k_h40", "B": B, "H": H, "Dk": D, "Dv": D, "L": L, "segments": seg,
-                   "parallelism": "one workgroup per (batch, head)"},
+                   "ts": args.gdn_ts or "auto",
+                   "parallelism": "superchunks: [M|N] prep walk, fp32 state scan, output walk"},
         "roofline": {"kernel": "gdn_fwd", "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM / 1e9,
                      "unit": "GB/s", "frac": achieved * 1e9 / PEAK_HBM, "traffic": None, "launches": nl,
                      "avg_launch_us": avg_s * 1e6, "us_per_chunk": avg_s * 1e6 * len(seg) / (L / 64)},
@@ -409,6 +410,7 @@ def main():
     ap.add_argument("--conv", action="store_true",
                     help="measure the short convolution with carried tails instead of the recurrence")
     ap.add_argument("--gdn", action="store_true", help="measure the gated-delta-rule forward instead")
+    ap.add_argument("--gdn-ts", type=int, default=0, help="gated delta rule superchunk length (0: automatic)")
     ap.add_argument("--tune-ts", action="store_true",
                     help="time the chain for each superchunk stride and overlap setting (one JSON table)")
     ap.add_argument("--partition-study", action="store_true",

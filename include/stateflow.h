@@ -247,15 +247,24 @@ sf_status sf_partition_hybrid(int64_t T, int32_t N, double alpha, double w_tok, 
  *     S_t = a_t (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T,   o_t = S_t^T q_t,
  * a_t = exp(g_t), S stored as [Dk][Dv] (the transpose of the paper's S).
  * q, k, v, o as for sf_segment_fwd (shape->io_dtype must be SF_BF16,
- * Dk == Dv in {64, 128}, scalar gate); g and beta are float32 [B][L][H] with
- * the gate strides of `shape`; S_in may be NULL (zero state); S_out receives
- * the final state.  One workgroup walks each (batch, head) over the whole
- * segment (no superchunk parallelism yet), so the call suits segments of a
- * few thousand tokens or many heads.  Same ownership, validation, aliasing
- * and error rules as the other entry points.
+ * Dk == Dv in {64, 128}, scalar gate, L a multiple of 64); g and beta are
+ * float32 [B][L][H] with the gate strides of `shape`; S_in may be NULL (zero
+ * state); S_out receives the final state.
+ * Superchunks of tuning->ts tokens (0: chosen from the shape and the device's
+ * CU count) run in parallel: since one chunk's update is affine in the state,
+ * each superchunk J reduces to S_{J+1} = M_J S_J + N_J (dense M_J, N_J,
+ * Sec. 2.2's Pre step with a matrix-valued transition), an fp32 scan over J
+ * gives every S_J (ST), and the output walk runs from them (Out).
+ *   ws  device scratch of at least sf_gdn_fwd_workspace_bytes() (0 when the
+ *       segment is one superchunk); contents on entry ignored, on return
+ *       unspecified.
+ * Same ownership, validation, aliasing and error rules as the other entry
+ * points.
  */
+size_t sf_gdn_fwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning);
 sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const void *v, const float *g,
-                     const float *beta, const float *S_in, void *o, float *S_out, sf_stream stream);
+                     const float *beta, const float *S_in, void *o, float *S_out, void *ws, size_t ws_bytes,
+                     const sf_tuning *tuning, sf_stream stream);
 
 /*
  * Kernel timing for measurement: while enabled, every launch of kernel

@@ -30,7 +30,7 @@ from ._lib import KERNELS, StateflowError  # noqa: F401
 
 __all__ = ["segment_fwd", "segment_bwd", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
            "bwd_workspace_bytes", "chain_workspace_bytes", "conv_fwd", "conv_bwd", "conv_bwd_workspace_bytes",
-           "gdn_fwd", "partition_hybrid", "prof_enable", "prof_read", "StateflowError", "abi_version"]
+           "gdn_fwd", "gdn_fwd_workspace_bytes", "partition_hybrid", "prof_enable", "prof_read", "StateflowError", "abi_version"]
 
 _IO = {torch.bfloat16: _lib.SF_BF16, torch.float32: _lib.SF_F32}
 _aux_streams = {}
@@ -112,6 +112,10 @@ def fwd_workspace_bytes(q, g, ts=0):
 
 def bwd_workspace_bytes(q, g, ts=0):
     return _lib.lib().sf_bwd_workspace_bytes(ctypes.byref(_shape(q, g)), ctypes.byref(_tuning(ts)))
+
+
+def gdn_fwd_workspace_bytes(q, g, ts=0):
+    return _lib.lib().sf_gdn_fwd_workspace_bytes(ctypes.byref(_shape(q, g)), ctypes.byref(_tuning(ts)))
 
 
 def chain_workspace_bytes(q, g, seg_lens, ts=0):
@@ -338,10 +342,11 @@ def conv_bwd(x, w, tail_in, dy, dtail_out=None, act="silu", *, stream=None, out=
     return dx, dw, dtail_in
 
 
-def gdn_fwd(q, k, v, g, beta, S_in=None, *, stream=None):
+def gdn_fwd(q, k, v, g, beta, S_in=None, *, ts=0, stream=None):
     """(o, S_out) of the gated delta rule over one segment: q, k, v [B, L, H, D]
     bf16; g (natural-log decay) and beta float32 [B, L, H] with the same
-    strides; S_in [B, H, D, D] float32 or None."""
+    strides; S_in [B, H, D, D] float32 or None.  ts: superchunk length in
+    tokens (a multiple of 64; 0 chooses)."""
     _same_layout(q, k, v)
     sh = _shape(q, g)
     if tuple(beta.shape) != tuple(g.shape) or beta.stride() != g.stride() or beta.dtype != torch.float32:
@@ -349,11 +354,14 @@ def gdn_fwd(q, k, v, g, beta, S_in=None, *, stream=None):
     B, L, H, D = q.shape
     _state(S_in, B, H, D, "S_in")
     stream = stream or torch.cuda.current_stream(q.device)
+    L_ = _lib.lib()
+    tun = _tuning(ts)
     with torch.cuda.stream(stream):
         o = _like(q)
         S_out = torch.empty((B, H, D, D), dtype=torch.float32, device=q.device)
-    rc = _lib.lib().sf_gdn_fwd(ctypes.byref(sh), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S_in), _ptr(o),
-                               _ptr(S_out), _stream_handle(stream))
+        ws = _ws(L_.sf_gdn_fwd_workspace_bytes(ctypes.byref(sh), ctypes.byref(tun)), q.device)
+    rc = L_.sf_gdn_fwd(ctypes.byref(sh), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S_in), _ptr(o),
+                       _ptr(S_out), _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream))
     _lib.check("sf_gdn_fwd", rc)
     return o, S_out
 

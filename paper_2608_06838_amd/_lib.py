@@ -21,7 +21,8 @@ SF_ACT_NONE, SF_ACT_SILU = 0, 1
 # every symbol include/stateflow.h declares
 EXPORTS = ["sf_abi_version", "sf_status_str", "sf_last_error", "sf_fwd_workspace_bytes",
            "sf_bwd_workspace_bytes", "sf_segment_fwd", "sf_segment_bwd", "sf_chain_workspace_bytes",
-           "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd", "sf_gdn_fwd", "sf_partition_hybrid",
+           "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd",
+           "sf_gdn_fwd_workspace_bytes", "sf_gdn_fwd", "sf_partition_hybrid",
            "sf_prof_enable", "sf_prof_read"]
 
 
@@ -96,8 +97,10 @@ def lib():
     L.sf_conv_fwd.argtypes = [cp] + [vp] * 5 + [vp]
     L.sf_conv_bwd.restype = ctypes.c_int
     L.sf_conv_bwd.argtypes = [cp] + [vp] * 9 + [sz, vp]
+    L.sf_gdn_fwd_workspace_bytes.restype = sz
+    L.sf_gdn_fwd_workspace_bytes.argtypes = [sp, tp]
     L.sf_gdn_fwd.restype = ctypes.c_int
-    L.sf_gdn_fwd.argtypes = [sp] + [vp] * 8 + [vp]
+    L.sf_gdn_fwd.argtypes = [sp] + [vp] * 9 + [sz, tp, vp]
     L.sf_partition_hybrid.restype = ctypes.c_int
     L.sf_partition_hybrid.argtypes = [i64, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double, i32, i64p]
     L.sf_prof_enable.restype = ctypes.c_int

@@ -871,19 +871,79 @@ sf_status sf_conv_bwd(const sf_conv_shape *shape, const void *x, const float *w,
     return conv_run(SF_K_CONV_BWD, true, a, (hipStream_t)stream);
 }
 
+namespace {
+
+// Gated delta rule: superchunk length.  One walk workgroup fills a CU (its
+// LDS), so `slots` = CUs; the prep walk ([M | N], twice the columns) costs
+// about kPrep chunk steps of the output walk per chunk and one scan step about
+// kScan.  Choose chunks per superchunk m minimising
+//   rounds(walk) * m + kPrep * rounds(prep) * m + kScan * (superchunks - 1).
+sf_status gdn_pick_ts(const Shape &r, const sf_tuning *t, int &ts) {
+    if (t && t->ts != 0) {
+        if (t->ts < 64 || t->ts % 64) return fail(SF_E_SHAPE, "tuning.ts must be a positive multiple of 64");
+        ts = t->ts;
+        return SF_OK;
+    }
+    const int64_t bh = (int64_t)r.B * r.H, nc = r.L / 64;
+    if (nc <= 1) {
+        ts = 64;
+        return SF_OK;
+    }
+    const double slots = device_cus(), kPrep = 1.3, kScan = 0.15;
+    double best = 1e300;
+    int64_t best_m = nc;
+    for (int64_t m = 1; m <= nc; ++m) {
+        const int64_t ns = (nc + m - 1) / m;
+        if (m > 1 && (nc + m - 2) / (m - 1) == ns) continue;
+        const double walk = std::ceil((double)(bh * ns) / slots) * (double)m;
+        const double prep = ns > 1 ? kPrep * std::ceil((double)(bh * (ns - 1)) / slots) * (double)m : 0.0;
+        const double cost = walk + prep + kScan * (double)(ns - 1);
+        if (cost < best - 1e-9) {
+            best = cost;
+            best_m = m;
+        }
+    }
+    ts = (int)std::min<int64_t>(best_m * 64, 1 << 30);
+    return SF_OK;
+}
+
+size_t gdn_ws_bytes(const Shape &r, int ts) {
+    const int n = n_super_of(r.L, ts);
+    if (n <= 1) return 0;
+    const size_t bh = (size_t)r.B * r.H, SS = (size_t)r.D * r.D * 4;
+    return al(bh * n * SS) + 2 * al(bh * (n - 1) * SS);
+}
+
+}  // namespace
+
+size_t sf_gdn_fwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning) {
+    Shape r;
+    int ts;
+    if (resolve(shape, r) != SF_OK || gdn_pick_ts(r, tuning, ts) != SF_OK) return 0;
+    return gdn_ws_bytes(r, ts);
+}
+
 sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const void *v, const float *g,
-                     const float *beta, const float *S_in, void *o, float *S_out, sf_stream stream) {
+                     const float *beta, const float *S_in, void *o, float *S_out, void *ws, size_t ws_bytes,
+                     const sf_tuning *tuning, sf_stream stream) {
+    g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
     if (r.io != SF_BF16) return fail(SF_E_UNSUPPORTED, "the gated delta rule needs bf16 I/O");
     if (r.gate != SF_GATE_SCALAR) return fail(SF_E_UNSUPPORTED, "the gated delta rule takes a scalar gate");
     if (!S_out || (r.L > 0 && (!q || !k || !v || !g || !beta || !o)))
         return fail(SF_E_NULL, "q, k, v, g, beta, o and S_out are required");
-    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_in, "S_in"}, {S_out, "S_out"}}));
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_in, "S_in"}, {S_out, "S_out"}, {ws, "ws"}}));
     if (((uintptr_t)g | (uintptr_t)beta) % 4) return fail(SF_E_ALIGN, "g and beta must be 4-byte aligned");
+    int ts;
+    TRY(gdn_pick_ts(r, tuning, ts));
+    const size_t need = gdn_ws_bytes(r, ts);
+    if (need > 0 && !ws) return fail(SF_E_NULL, "workspace of %zu bytes required", need);
+    if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
     TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"), grange(r, g, r.L, "g"),
                      grange(r, beta, r.L, "beta"), srange(r, S_in, 1, "S_in")},
-                    {xrange(r, o, r.L, "o"), srange(r, S_out, 1, "S_out")}));
+                    {xrange(r, o, r.L, "o"), srange(r, S_out, 1, "S_out"),
+                     {(const char *)ws, (const char *)ws + (ws ? need : 0), "ws"}}));
     sf::GdnArgs a{};
     a.q = q;
     a.k = k;
@@ -902,6 +962,14 @@ sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const 
     a.sg_b = r.sg_b;
     a.sg_l = r.sg_l;
     a.sg_h = r.sg_h;
+    a.ts = ts;
+    a.n_super = std::max(1, n_super_of(r.L, ts));
+    if (a.n_super > 1) {
+        const size_t bh = (size_t)r.B * r.H, SS = (size_t)r.D * r.D * 4;
+        a.wsS = (float *)ws;
+        a.wsM = (float *)((char *)ws + al(bh * a.n_super * SS));
+        a.wsN = (float *)((char *)a.wsM + al(bh * (a.n_super - 1) * SS));
+    }
     bool on;
     {
         std::lock_guard<std::mutex> lk(g_prof_mu);

@@ -63,13 +63,17 @@ struct ConvArgs {
 };
 int conv_channels_per_thread();
 
-// Gated delta rule forward (sf_gdn.hip): one workgroup per (batch, head).
+// Gated delta rule forward (sf_gdn.hip).  n_super superchunks of ts tokens per
+// (batch, head); with n_super > 1 the workspace holds the boundary states
+// wsS [B*H][n_super][D][D] and the superchunk maps wsM, wsN
+// [B*H][n_super-1][D][D] (all fp32).
 struct GdnArgs {
     const void *q, *k, *v;
     const float *g, *beta, *S_in;
     void *o;
     float *S_out;
-    int32_t B, H;
+    float *wsS, *wsM, *wsN;
+    int32_t B, H, n_super, ts;
     int64_t L, sx_b, sx_l, sx_h, sg_b, sg_l, sg_h;
 };
 hipError_t launch_gdn_fwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);

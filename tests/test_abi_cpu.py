@@ -66,6 +66,12 @@ def p(i):
     return ctypes.c_void_p(FAKE + i * (1 << 32))
 
 
+def _tuning(ts=0):
+    t = _lib.SfTuning()
+    t.ts = ts
+    return t
+
+
 def fwd(s, q=1, k=2, v=3, g=4, S_in=None, o=5, S_out=6, ws=7, ws_bytes=1 << 30, tun=None):
     L = _lib.lib()
     args = [p(x) if x is not None else None for x in (q, k, v, g, S_in, o, S_out, ws)]
@@ -200,9 +206,10 @@ def test_conv_pointer_validation():
 def test_gdn_validation():
     L = _lib.lib()
 
-    def call(s, q=1, k=2, v=3, g=4, beta=5, S_in=None, o=6, S_out=7):
-        args = [p(i) if i is not None else None for i in (q, k, v, g, beta, S_in, o, S_out)]
-        return L.sf_gdn_fwd(ctypes.byref(s) if s is not None else None, *args, None)
+    def call(s, q=1, k=2, v=3, g=4, beta=5, S_in=None, o=6, S_out=7, ws=8, ws_bytes=1 << 30, tun=None):
+        args = [p(i) if i is not None else None for i in (q, k, v, g, beta, S_in, o, S_out, ws)]
+        return L.sf_gdn_fwd(ctypes.byref(s) if s is not None else None, *args, ws_bytes,
+                            ctypes.byref(tun) if tun is not None else None, None)
 
     assert call(None) == _lib.SF_E_NULL
     assert call(shape(io_dtype=_lib.SF_F32, Dk=64, Dv=64)) == _lib.SF_E_UNSUPPORTED
@@ -212,5 +219,18 @@ def test_gdn_validation():
     assert call(shape(), S_out=None) == _lib.SF_E_NULL
     assert call(shape(), o=1) == _lib.SF_E_ALIAS
     assert call(shape(), S_out=5) == _lib.SF_E_ALIAS   # S_out over beta
-    rc = L.sf_gdn_fwd(ctypes.byref(shape()), ctypes.c_void_p(FAKE + 2), p(2), p(3), p(4), p(5), None, p(6), p(7), None)
+    assert call(shape(), ws=6) == _lib.SF_E_ALIAS      # workspace over o
+    rc = L.sf_gdn_fwd(ctypes.byref(shape()), ctypes.c_void_p(FAKE + 2), p(2), p(3), p(4), p(5), None, p(6), p(7),
+                      p(8), 1 << 30, None, None)
     assert rc == _lib.SF_E_ALIGN
+    # superchunks: ts must be a positive multiple of 64; the workspace holds
+    # S_J for every superchunk and (M_J, N_J) for all but the last
+    assert call(shape(), tun=_tuning(ts=100)) == _lib.SF_E_SHAPE
+    s = shape(L=1024)
+    need = L.sf_gdn_fwd_workspace_bytes(ctypes.byref(s), ctypes.byref(_tuning(ts=256)))
+    assert need == 2 * 4 * 128 * 128 * 4 + 2 * (2 * 3 * 128 * 128 * 4)
+    assert L.sf_gdn_fwd_workspace_bytes(ctypes.byref(s), ctypes.byref(_tuning(ts=1024))) == 0
+    assert L.sf_gdn_fwd_workspace_bytes(ctypes.byref(s), ctypes.byref(_tuning(ts=4096))) == 0
+    assert call(s, tun=_tuning(ts=256), ws=None) == _lib.SF_E_NULL
+    assert call(s, tun=_tuning(ts=256), ws_bytes=need - 1) == _lib.SF_E_WORKSPACE
+    assert call(s, tun=_tuning(ts=1024), ws=None, ws_bytes=0, S_out=1) == _lib.SF_E_ALIAS  # passes the workspace checks

@@ -1,7 +1,9 @@
 """GPU parity of the gated-delta-rule forward (sf_gdn_fwd through the C ABI)
 against the fp64 oracle (oracle.gdn): o and S_out, bf16 I/O, both head dims,
-several chunks with a nonzero initial state, an empty segment, no initial
-state, segments chained through S, and a long segment on sampled heads."""
+several chunks with a nonzero initial state, explicit superchunk lengths
+(one superchunk, one chunk each, a ragged last superchunk), an empty segment,
+no initial state, segments chained through S, and a long segment on sampled
+heads."""
 import numpy as np
 import pytest
 import torch
@@ -20,9 +22,9 @@ def say(msg):
     print(msg, flush=True)
 
 
-def run(inp):
+def run(inp, ts=0):
     g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
-    o, S = sf.gdn_fwd(g["q"], g["k"], g["v"], g["g"], g["beta"], g["S_in"])
+    o, S = sf.gdn_fwd(g["q"], g["k"], g["v"], g["g"], g["beta"], g["S_in"], ts=ts)
     torch.cuda.synchronize()
     return o, S
 
@@ -42,6 +44,21 @@ def test_gdn_parity(D):
     say(f"[gdn] D={D} B={B} L={L} H={H}")
     inp = synth.make_gdn_inputs(B, L, H, D, seed=4100 + D)
     o, S = run(inp)
+    ro, rS = ref(inp)
+    assert_close("o", to64(o), ro, "bf16")
+    assert_close("S_out", to64(S), rS, "bf16")
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("ts", [64, 192, 256, 448])
+def test_gdn_superchunks(D, ts):
+    """Prep walk ([M | N] per superchunk), fp32 scan over superchunks and the
+    output walk from the scanned states, for L = 7 chunks: 448 is one
+    superchunk (no prep, no scan), 192 leaves a ragged last superchunk."""
+    B, L, H = 1, 448, 3
+    say(f"[gdn] superchunks D={D} ts={ts}")
+    inp = synth.make_gdn_inputs(B, L, H, D, seed=4500 + D + ts)
+    o, S = run(inp, ts)
     ro, rS = ref(inp)
     assert_close("o", to64(o), ro, "bf16")
     assert_close("S_out", to64(S), rS, "bf16")
