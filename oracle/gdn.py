@@ -19,7 +19,7 @@ def _lib():
     lib = _load()
     if not _ready:
         dp = ctypes.POINTER(ctypes.c_double)
-        lib.gdo_forward.argtypes = [ctypes.c_int] * 4 + [ctypes.c_long] + [dp] * 8 + [ctypes.c_int]
+        lib.gdo_forward.argtypes = [ctypes.c_int] * 4 + [ctypes.c_long] + [dp] * 9 + [ctypes.c_int]
         lib.gdo_forward.restype = ctypes.c_int
         lib.gdo_backward.argtypes = [ctypes.c_int] * 4 + [ctypes.c_long] + [dp] * 14 + [ctypes.c_int]
         lib.gdo_backward.restype = ctypes.c_int
@@ -33,18 +33,21 @@ def _dims(q, v, g, beta):
     return B, L, H, Dk, v.shape[3]
 
 
-def forward(q, k, v, g, beta, S_in=None, threads=0):
-    """Returns (o, S_out) in float64.  q, k: [B, L, H, Dk]; v: [B, L, H, Dv];
-    g (natural-log decay), beta: [B, L, H]; S_in: [B, H, Dk, Dv] or None."""
+def forward(q, k, v, g, beta, S_in=None, threads=0, with_u=False):
+    """Returns (o, S_out) in float64, and u (the corrected values V^new,
+    [B, L, H, Dv]) after them when with_u.  q, k: [B, L, H, Dk];
+    v: [B, L, H, Dv]; g (natural-log decay), beta: [B, L, H];
+    S_in: [B, H, Dk, Dv] or None."""
     q, k, v, g, beta, S_in = (_f64(x) for x in (q, k, v, g, beta, S_in))
     B, L, H, Dk, Dv = _dims(q, v, g, beta)
     o = np.zeros((B, L, H, Dv))
     S_out = np.zeros((B, H, Dk, Dv))
+    u = np.zeros((B, L, H, Dv)) if with_u else None
     rc = _lib().gdo_forward(B, H, Dk, Dv, L, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S_in), _ptr(o),
-                            _ptr(S_out), int(threads))
+                            _ptr(S_out), _ptr(u), int(threads))
     if rc != 0:
         raise RuntimeError(f"gdo_forward failed ({rc})")
-    return o, S_out
+    return (o, S_out, u) if with_u else (o, S_out)
 
 
 def backward(q, k, v, g, beta, S_in, dO, dS_out=None, threads=0):

@@ -14,6 +14,8 @@
  *     u_t = beta_t (v_t - P^T k_t)            (the corrected value, V^new)
  *     S_t = P + k_t u_t^T                     (= a_t (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T)
  *     o_t = S_t^T q_t
+ * u_t is the delta rule's corrected value (the V^new that the paper's ST
+ * step returns beside the state); gdo_forward can return it.
  *
  * Backward of Loss = sum_t <dO_t, o_t> + <dS_out, S_out>, by hand, per token
  * in reverse with G = dLoss/dS_t:
@@ -26,7 +28,7 @@
  * States are replayed from checkpoints every ~sqrt(L) tokens; the recurrence
  * is never inverted.
  *
- * Layouts (double, contiguous): q, k: [B][L][H][Dk]; v, o: [B][L][H][Dv];
+ * Layouts (double, contiguous): q, k: [B][L][H][Dk]; v, o, u_out: [B][L][H][Dv];
  * g, beta: [B][L][H]; states [B][H][Dk][Dv].
  */
 #include <math.h>
@@ -60,7 +62,8 @@ static void gdn_step(const gdims_t *d, double *S, double g, double beta, const d
 }
 
 int gdo_forward(int B, int H, int Dk, int Dv, long L, const double *q, const double *k, const double *v,
-                const double *g, const double *beta, const double *S_in, double *o, double *S_out, int n_threads) {
+                const double *g, const double *beta, const double *S_in, double *o, double *S_out, double *u_out,
+                int n_threads) {
     if (B < 1 || H < 1 || Dk < 1 || Dv < 1 || L < 0 || !S_out) return -2;
     if (L > 0 && (!q || !k || !v || !g || !beta || !o)) return -2;
     gdims_t d = {B, H, Dk, Dv, L};
@@ -84,6 +87,7 @@ int gdo_forward(int B, int H, int Dk, int Dv, long L, const double *q, const dou
         else memset(S, 0, sizeof(double) * SS);
         for (long t = 0; t < L; ++t) {
             gdn_step(&d, S, g[gs(&d, b, t, h)], beta[gs(&d, b, t, h)], k + gx(&d, b, t, h, Dk), v + gx(&d, b, t, h, Dv), u);
+            if (u_out) memcpy(u_out + gx(&d, b, t, h, Dv), u, sizeof(double) * Dv);
             const double *qt = q + gx(&d, b, t, h, Dk);
             double *ot = o + gx(&d, b, t, h, Dv);
             for (int j = 0; j < Dv; ++j) {

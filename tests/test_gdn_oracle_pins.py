@@ -30,30 +30,38 @@ def rand(rng, B=2, L=23, H=2, Dk=6, Dv=5):
 
 def paper_form(q, k, v, g, beta, S_in):
     """S^p_t = S^p_{t-1} F_t + beta_t v_t k_t^T, y_t = S^p_t q_t, with S^p = S^T
-    (Dv x Dk) and F_t = a_t (I - beta_t k_t k_t^T) built as a matrix."""
+    (Dv x Dk) and F_t = a_t (I - beta_t k_t k_t^T) built as a matrix.  Also
+    returns the corrected values: the token's update beyond the decay,
+    S^p_t - a_t S^p_{t-1}, is a rank-one matrix u_t k_t^T, so
+    u_t = (S^p_t - a_t S^p_{t-1}) k_t / |k_t|^2."""
     B, L, H, Dk = q.shape
     Dv = v.shape[3]
     o = np.zeros((B, L, H, Dv))
+    u = np.zeros((B, L, H, Dv))
     S_out = np.zeros((B, H, Dk, Dv))
     for b in range(B):
         for h in range(H):
             Sp = S_in[b, h].T.copy()
             for t in range(L):
                 kt = k[b, t, h]
-                F = np.exp(g[b, t, h]) * (np.eye(Dk) - beta[b, t, h] * np.outer(kt, kt))
+                a = np.exp(g[b, t, h])
+                F = a * (np.eye(Dk) - beta[b, t, h] * np.outer(kt, kt))
+                prev = Sp
                 Sp = Sp @ F + beta[b, t, h] * np.outer(v[b, t, h], kt)
                 o[b, t, h] = Sp @ q[b, t, h]
+                u[b, t, h] = (Sp - a * prev) @ kt / (kt @ kt)
             S_out[b, h] = Sp.T
-    return o, S_out
+    return o, S_out, u
 
 
 def test_matches_paper_matrix_form():
     rng = np.random.default_rng(0)
     q, k, v, g, beta, S_in, _, _ = rand(rng)
-    o, S = gdn.forward(q, k, v, g, beta, S_in)
-    ro, rS = paper_form(q, k, v, g, beta, S_in)
+    o, S, u = gdn.forward(q, k, v, g, beta, S_in, with_u=True)
+    ro, rS, ru = paper_form(q, k, v, g, beta, S_in)
     np.testing.assert_allclose(o, ro, rtol=1e-12, atol=1e-12)
     np.testing.assert_allclose(S, rS, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(u, ru, rtol=1e-10, atol=1e-10)
 
 
 def test_beta_zero_is_pure_decay():
@@ -77,10 +85,12 @@ def test_orthonormal_keys_overwrite_exactly():
     v = rng.standard_normal((1, L, 1, Dv))
     q = rng.standard_normal((1, L, 1, Dk))
     S_in = rng.standard_normal((1, 1, Dk, Dv))
-    _, S = gdn.forward(q, k, v, np.zeros((1, L, 1)), np.ones((1, L, 1)), S_in)
+    _, S, u = gdn.forward(q, k, v, np.zeros((1, L, 1)), np.ones((1, L, 1)), S_in, with_u=True)
     K = k[0, :, 0]
     ref = (np.eye(Dk) - K.T @ K) @ S_in[0, 0] + K.T @ v[0, :, 0]
     np.testing.assert_allclose(S[0, 0], ref, rtol=1e-12, atol=1e-12)
+    # each corrected value replaces the state's old content along k_i: v_i - S_in^T k_i
+    np.testing.assert_allclose(u[0, :, 0], v[0, :, 0] - K @ S_in[0, 0], rtol=1e-12, atol=1e-12)
 
 
 def loss(q, k, v, g, beta, S_in, dO, dS):
