@@ -249,7 +249,10 @@ sf_status sf_partition_hybrid(int64_t T, int32_t N, double alpha, double w_tok, 
  * q, k, v, o as for sf_segment_fwd (shape->io_dtype must be SF_BF16,
  * Dk == Dv in {64, 128}, scalar gate, L a multiple of 64); g and beta are
  * float32 [B][L][H] with the gate strides of `shape`; S_in may be NULL (zero
- * state); S_out receives the final state.
+ * state); S_out receives the final state; v_new, if not NULL, receives the
+ * corrected values u_t = beta_t (v_t - a_t S_{t-1}^T k_t) (the V^new that the
+ * delta rule's ST step returns beside the state, Sec. 2.1), bf16 with the
+ * layout of v.
  * Superchunks of tuning->ts tokens (0: chosen from the shape and the device's
  * CU count) run in parallel: since one chunk's update is affine in the state,
  * each superchunk J reduces to S_{J+1} = M_J S_J + N_J (dense M_J, N_J,
@@ -263,8 +266,8 @@ sf_status sf_partition_hybrid(int64_t T, int32_t N, double alpha, double w_tok, 
  */
 size_t sf_gdn_fwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning);
 sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const void *v, const float *g,
-                     const float *beta, const float *S_in, void *o, float *S_out, void *ws, size_t ws_bytes,
-                     const sf_tuning *tuning, sf_stream stream);
+                     const float *beta, const float *S_in, void *o, float *S_out, void *v_new, void *ws,
+                     size_t ws_bytes, const sf_tuning *tuning, sf_stream stream);
 
 /*
  * Kernel timing for measurement: while enabled, every launch of kernel

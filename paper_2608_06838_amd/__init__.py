@@ -342,11 +342,12 @@ def conv_bwd(x, w, tail_in, dy, dtail_out=None, act="silu", *, stream=None, out=
     return dx, dw, dtail_in
 
 
-def gdn_fwd(q, k, v, g, beta, S_in=None, *, ts=0, stream=None):
+def gdn_fwd(q, k, v, g, beta, S_in=None, *, ts=0, with_v_new=False, stream=None):
     """(o, S_out) of the gated delta rule over one segment: q, k, v [B, L, H, D]
     bf16; g (natural-log decay) and beta float32 [B, L, H] with the same
     strides; S_in [B, H, D, D] float32 or None.  ts: superchunk length in
-    tokens (a multiple of 64; 0 chooses)."""
+    tokens (a multiple of 64; 0 chooses).  with_v_new: also return the
+    corrected values (V^new, laid out like v) as a third result."""
     _same_layout(q, k, v)
     sh = _shape(q, g)
     if tuple(beta.shape) != tuple(g.shape) or beta.stride() != g.stride() or beta.dtype != torch.float32:
@@ -358,12 +359,13 @@ def gdn_fwd(q, k, v, g, beta, S_in=None, *, ts=0, stream=None):
     tun = _tuning(ts)
     with torch.cuda.stream(stream):
         o = _like(q)
+        vn = _like(q) if with_v_new else None
         S_out = torch.empty((B, H, D, D), dtype=torch.float32, device=q.device)
         ws = _ws(L_.sf_gdn_fwd_workspace_bytes(ctypes.byref(sh), ctypes.byref(tun)), q.device)
     rc = L_.sf_gdn_fwd(ctypes.byref(sh), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S_in), _ptr(o),
-                       _ptr(S_out), _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream))
+                       _ptr(S_out), _ptr(vn), _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream))
     _lib.check("sf_gdn_fwd", rc)
-    return o, S_out
+    return (o, S_out, vn) if with_v_new else (o, S_out)
 
 
 def partition_hybrid(T, N, alpha, w_tok, w_soft, round_to=128):

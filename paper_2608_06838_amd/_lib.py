@@ -100,7 +100,7 @@ def lib():
     L.sf_gdn_fwd_workspace_bytes.restype = sz
     L.sf_gdn_fwd_workspace_bytes.argtypes = [sp, tp]
     L.sf_gdn_fwd.restype = ctypes.c_int
-    L.sf_gdn_fwd.argtypes = [sp] + [vp] * 9 + [sz, tp, vp]
+    L.sf_gdn_fwd.argtypes = [sp] + [vp] * 10 + [sz, tp, vp]
     L.sf_partition_hybrid.restype = ctypes.c_int
     L.sf_partition_hybrid.argtypes = [i64, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double, i32, i64p]
     L.sf_prof_enable.restype = ctypes.c_int

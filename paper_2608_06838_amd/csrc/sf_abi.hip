@@ -924,8 +924,8 @@ size_t sf_gdn_fwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning
 }
 
 sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const void *v, const float *g,
-                     const float *beta, const float *S_in, void *o, float *S_out, void *ws, size_t ws_bytes,
-                     const sf_tuning *tuning, sf_stream stream) {
+                     const float *beta, const float *S_in, void *o, float *S_out, void *v_new, void *ws,
+                     size_t ws_bytes, const sf_tuning *tuning, sf_stream stream) {
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
@@ -933,7 +933,8 @@ sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const 
     if (r.gate != SF_GATE_SCALAR) return fail(SF_E_UNSUPPORTED, "the gated delta rule takes a scalar gate");
     if (!S_out || (r.L > 0 && (!q || !k || !v || !g || !beta || !o)))
         return fail(SF_E_NULL, "q, k, v, g, beta, o and S_out are required");
-    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_in, "S_in"}, {S_out, "S_out"}, {ws, "ws"}}));
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_in, "S_in"}, {S_out, "S_out"}, {v_new, "v_new"},
+                     {ws, "ws"}}));
     if (((uintptr_t)g | (uintptr_t)beta) % 4) return fail(SF_E_ALIGN, "g and beta must be 4-byte aligned");
     int ts;
     TRY(gdn_pick_ts(r, tuning, ts));
@@ -942,7 +943,7 @@ sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const 
     if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
     TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"), grange(r, g, r.L, "g"),
                      grange(r, beta, r.L, "beta"), srange(r, S_in, 1, "S_in")},
-                    {xrange(r, o, r.L, "o"), srange(r, S_out, 1, "S_out"),
+                    {xrange(r, o, r.L, "o"), srange(r, S_out, 1, "S_out"), xrange(r, v_new, r.L, "v_new"),
                      {(const char *)ws, (const char *)ws + (ws ? need : 0), "ws"}}));
     sf::GdnArgs a{};
     a.q = q;
@@ -952,6 +953,7 @@ sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const 
     a.beta = beta;
     a.S_in = S_in;
     a.o = o;
+    a.v_new = v_new;
     a.S_out = S_out;
     a.B = r.B;
     a.H = r.H;

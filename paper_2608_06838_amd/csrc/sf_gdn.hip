@@ -69,6 +69,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
     const T *K = (const T *)a.k + xo;
     const T *V = (const T *)a.v + xo;
     T *Y = (T *)a.o + xo;
+    T *VN = a.v_new ? (T *)a.v_new + xo : nullptr;
     const int64_t go = bb * a.sg_b + hh * a.sg_h + tok0 * a.sg_l;
     const float *gp = a.g + go;
     const float *bp = a.beta + go;
@@ -280,6 +281,15 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
             const rsrc_t ro = buf_rsrc(Y + c * cstep, cspan);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) st4_buf<T>(ro, voff, tt * tstep, O[tt]);
+        }
+
+        // V^new (optional): U[16tt + 4q4 + r][c0 + n16]
+        if (!PREP && VN) {
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    VN[(int64_t)(c * C + 16 * tt + 4 * q4 + r) * a.sx_l + c0 + n16] = cvt<T>(U[0][tt][r]);
         }
 
         // S = gamma_C S + K^T (e^{b_C - b} o U)

@@ -70,7 +70,7 @@ int conv_channels_per_thread();
 struct GdnArgs {
     const void *q, *k, *v;
     const float *g, *beta, *S_in;
-    void *o;
+    void *o, *v_new;
     float *S_out;
     float *wsS, *wsM, *wsN;
     int32_t B, H, n_super, ts;

@@ -206,8 +206,8 @@ def test_conv_pointer_validation():
 def test_gdn_validation():
     L = _lib.lib()
 
-    def call(s, q=1, k=2, v=3, g=4, beta=5, S_in=None, o=6, S_out=7, ws=8, ws_bytes=1 << 30, tun=None):
-        args = [p(i) if i is not None else None for i in (q, k, v, g, beta, S_in, o, S_out, ws)]
+    def call(s, q=1, k=2, v=3, g=4, beta=5, S_in=None, o=6, S_out=7, v_new=None, ws=8, ws_bytes=1 << 30, tun=None):
+        args = [p(i) if i is not None else None for i in (q, k, v, g, beta, S_in, o, S_out, v_new, ws)]
         return L.sf_gdn_fwd(ctypes.byref(s) if s is not None else None, *args, ws_bytes,
                             ctypes.byref(tun) if tun is not None else None, None)
 
@@ -220,8 +220,10 @@ def test_gdn_validation():
     assert call(shape(), o=1) == _lib.SF_E_ALIAS
     assert call(shape(), S_out=5) == _lib.SF_E_ALIAS   # S_out over beta
     assert call(shape(), ws=6) == _lib.SF_E_ALIAS      # workspace over o
+    assert call(shape(), v_new=3) == _lib.SF_E_ALIAS   # V^new over v
+    assert call(shape(), v_new=6) == _lib.SF_E_ALIAS   # V^new over o
     rc = L.sf_gdn_fwd(ctypes.byref(shape()), ctypes.c_void_p(FAKE + 2), p(2), p(3), p(4), p(5), None, p(6), p(7),
-                      p(8), 1 << 30, None, None)
+                      None, p(8), 1 << 30, None, None)
     assert rc == _lib.SF_E_ALIGN
     # superchunks: ts must be a positive multiple of 64; the workspace holds
     # S_J for every superchunk and (M_J, N_J) for all but the last

@@ -40,13 +40,20 @@ def ref(inp, heads=None):
 
 @pytest.mark.parametrize("D", [64, 128])
 def test_gdn_parity(D):
+    """o, S_out and the corrected values V^new."""
     B, L, H = 2, 448, 3
     say(f"[gdn] D={D} B={B} L={L} H={H}")
     inp = synth.make_gdn_inputs(B, L, H, D, seed=4100 + D)
-    o, S = run(inp)
-    ro, rS = ref(inp)
+    g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
+    o, S, vn = sf.gdn_fwd(g["q"], g["k"], g["v"], g["g"], g["beta"], g["S_in"], with_v_new=True)
+    torch.cuda.synchronize()
+    o2, S2 = run(inp)
+    assert torch.equal(o, o2) and torch.equal(S, S2)
+    ro, rS, ru = gdn.forward(*(to64(inp[x]) for x in ("q", "k", "v", "g", "beta", "S_in")), threads=cores(),
+                             with_u=True)
     assert_close("o", to64(o), ro, "bf16")
     assert_close("S_out", to64(S), rS, "bf16")
+    assert_close("v_new", to64(vn), ru, "bf16")
 
 
 @pytest.mark.parametrize("D", [64, 128])
