@@ -270,6 +270,29 @@ sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const 
                      size_t ws_bytes, const sf_tuning *tuning, sf_stream stream);
 
 /*
+ * Gated delta rule backward over one segment: given the forward's inputs,
+ * S_in (NULL: zero), dO and dS_out (NULL: zero), the gradients of
+ *     Loss = sum_t <dO_t, o_t> + <dS_out, S_out>
+ * with respect to q, k, v (bf16, layout of q), g and beta (float32, layout of
+ * g) and S_in (dS_in, float32 [B][H][Dk][Dv]; written also when S_in is NULL).
+ * The states are recomputed (superchunk prep, fp32 scan, and a walk that
+ * stores the state entering every chunk); the state gradient runs backwards
+ * over the chunks (dS_start = M_J^T dS_end + E_J per superchunk, the
+ * transpose of the forward's chunk map) and is stored for every chunk; the
+ * parameter gradients of all chunks are then computed in parallel.
+ *   ws  device scratch of at least sf_gdn_bwd_workspace_bytes(): two fp32
+ *       D x D states per 64-token chunk plus the superchunk maps and the
+ *       per-chunk kernel's scratch; contents on entry ignored.
+ * Same shape rules as sf_gdn_fwd; same ownership, validation, aliasing and
+ * error rules as the other entry points.
+ */
+size_t sf_gdn_bwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning);
+sf_status sf_gdn_bwd(const sf_shape *shape, const void *q, const void *k, const void *v, const float *g,
+                     const float *beta, const float *S_in, const void *dO, const float *dS_out, void *dq, void *dk,
+                     void *dv, float *dg, float *dbeta, float *dS_in, void *ws, size_t ws_bytes,
+                     const sf_tuning *tuning, sf_stream stream);
+
+/*
  * Kernel timing for measurement: while enabled, every launch of kernel
  * `kernel_id` (an sf_kernel_id) carries HIP events that take the begin and
  * end timestamps of its own dispatch.  sf_prof_read() synchronises those
@@ -285,8 +308,9 @@ typedef enum {
     SF_K_BWD_DKV = 5,  /* dk, dv, dg by a reverse state-gradient walk (PG) */
     SF_K_CONV_FWD = 6, /* short convolution, forward */
     SF_K_CONV_BWD = 7, /* short convolution, backward (dx, dtail_in, dw partials and their sum) */
-    SF_K_GDN_FWD = 8,  /* gated delta rule, forward walk */
-    SF_K_COUNT = 9
+    SF_K_GDN_FWD = 8,  /* gated delta rule, forward (prep, scan and output walk) */
+    SF_K_GDN_BWD = 9,  /* gated delta rule, backward (every kernel of one call) */
+    SF_K_COUNT = 10
 } sf_kernel_id;
 
 sf_status sf_prof_enable(int32_t kernel_id, int32_t on);

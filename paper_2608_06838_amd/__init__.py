@@ -30,7 +30,7 @@ from ._lib import KERNELS, StateflowError  # noqa: F401
 
 __all__ = ["segment_fwd", "segment_bwd", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
            "bwd_workspace_bytes", "chain_workspace_bytes", "conv_fwd", "conv_bwd", "conv_bwd_workspace_bytes",
-           "gdn_fwd", "gdn_fwd_workspace_bytes", "partition_hybrid", "prof_enable", "prof_read", "StateflowError", "abi_version"]
+           "gdn_fwd", "gdn_fwd_workspace_bytes", "gdn_bwd", "partition_hybrid", "prof_enable", "prof_read", "StateflowError", "abi_version"]
 
 _IO = {torch.bfloat16: _lib.SF_BF16, torch.float32: _lib.SF_F32}
 _aux_streams = {}
@@ -366,6 +366,31 @@ def gdn_fwd(q, k, v, g, beta, S_in=None, *, ts=0, with_v_new=False, stream=None)
                        _ptr(S_out), _ptr(vn), _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream))
     _lib.check("sf_gdn_fwd", rc)
     return (o, S_out, vn) if with_v_new else (o, S_out)
+
+
+def gdn_bwd(q, k, v, g, beta, S_in, dO, dS_out=None, *, ts=0, stream=None):
+    """(dq, dk, dv, dg, dbeta, dS_in) of the gated delta rule over one segment
+    for Loss = sum <dO, o> + <dS_out, S_out>; arguments as for gdn_fwd."""
+    _same_layout(q, k, v, dO)
+    sh = _shape(q, g)
+    if tuple(beta.shape) != tuple(g.shape) or beta.stride() != g.stride() or beta.dtype != torch.float32:
+        raise ValueError("beta must match g in shape, strides and dtype (float32)")
+    B, L, H, D = q.shape
+    _state(S_in, B, H, D, "S_in")
+    _state(dS_out, B, H, D, "dS_out")
+    stream = stream or torch.cuda.current_stream(q.device)
+    L_ = _lib.lib()
+    tun = _tuning(ts)
+    with torch.cuda.stream(stream):
+        dq, dk, dv = _like(q), _like(k), _like(v)
+        dg, dbeta = _like(g), _like(beta)
+        dS_in = torch.empty((B, H, D, D), dtype=torch.float32, device=q.device)
+        ws = _ws(L_.sf_gdn_bwd_workspace_bytes(ctypes.byref(sh), ctypes.byref(tun)), q.device)
+    rc = L_.sf_gdn_bwd(ctypes.byref(sh), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S_in), _ptr(dO),
+                       _ptr(dS_out), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg), _ptr(dbeta), _ptr(dS_in), _ptr(ws),
+                       ws.numel(), ctypes.byref(tun), _stream_handle(stream))
+    _lib.check("sf_gdn_bwd", rc)
+    return dq, dk, dv, dg, dbeta, dS_in
 
 
 def partition_hybrid(T, N, alpha, w_tok, w_soft, round_to=128):

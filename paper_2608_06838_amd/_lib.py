@@ -15,14 +15,16 @@ SF_OK, SF_E_NULL, SF_E_SHAPE, SF_E_DTYPE, SF_E_ALIGN, SF_E_ALIAS, SF_E_WORKSPACE
 SF_F32, SF_BF16 = 0, 1
 SF_GATE_SCALAR, SF_GATE_VECTOR = 0, 1
 KERNELS = {"fwd_prep": 0, "scan": 1, "fwd_out": 2, "bwd_prep": 3, "bwd_dq": 4, "bwd_dkv": 5,
-           "conv_fwd": 6, "conv_bwd": 7, "gdn_fwd": 8}
+           "conv_fwd": 6, "conv_bwd": 7, "gdn_fwd": 8,
+           "gdn_bwd": 9}
 SF_ACT_NONE, SF_ACT_SILU = 0, 1
 
 # every symbol include/stateflow.h declares
 EXPORTS = ["sf_abi_version", "sf_status_str", "sf_last_error", "sf_fwd_workspace_bytes",
            "sf_bwd_workspace_bytes", "sf_segment_fwd", "sf_segment_bwd", "sf_chain_workspace_bytes",
            "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd",
-           "sf_gdn_fwd_workspace_bytes", "sf_gdn_fwd", "sf_partition_hybrid",
+           "sf_gdn_fwd_workspace_bytes", "sf_gdn_fwd", "sf_gdn_bwd_workspace_bytes", "sf_gdn_bwd",
+           "sf_partition_hybrid",
            "sf_prof_enable", "sf_prof_read"]
 
 
@@ -101,6 +103,10 @@ def lib():
     L.sf_gdn_fwd_workspace_bytes.argtypes = [sp, tp]
     L.sf_gdn_fwd.restype = ctypes.c_int
     L.sf_gdn_fwd.argtypes = [sp] + [vp] * 10 + [sz, tp, vp]
+    L.sf_gdn_bwd_workspace_bytes.restype = sz
+    L.sf_gdn_bwd_workspace_bytes.argtypes = [sp, tp]
+    L.sf_gdn_bwd.restype = ctypes.c_int
+    L.sf_gdn_bwd.argtypes = [sp] + [vp] * 15 + [sz, tp, vp]
     L.sf_partition_hybrid.restype = ctypes.c_int
     L.sf_partition_hybrid.argtypes = [i64, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double, i32, i64p]
     L.sf_prof_enable.restype = ctypes.c_int

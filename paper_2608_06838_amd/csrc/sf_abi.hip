@@ -914,6 +914,38 @@ size_t gdn_ws_bytes(const Shape &r, int ts) {
     return al(bh * n * SS) + 2 * al(bh * (n - 1) * SS);
 }
 
+// Backward workspace: the forward's boundary states and maps (M, N for every
+// superchunk), E_J and dS_end(J), the state and the state gradient of every
+// chunk, and the per-chunk gradient kernel's scratch slabs.
+struct GdnBwdWs {
+    size_t S = 0, M = 0, N = 0, E = 0, De = 0, Sc = 0, Dc = 0, X = 0, total = 0;
+    int n_x = 0;
+};
+constexpr int kGdnSlabs = 1024;
+GdnBwdWs gdn_bwd_ws(const Shape &r, int ts) {
+    GdnBwdWs w;
+    const int n = std::max(1, n_super_of(r.L, ts));
+    const size_t bh = (size_t)r.B * r.H, SS = (size_t)r.D * r.D * 4, nc = (size_t)(r.L / 64);
+    size_t off = 0;
+    auto take = [&](size_t &at, size_t bytes) {
+        at = off;
+        off += al(bytes);
+    };
+    if (n > 1) {
+        take(w.S, bh * n * SS);
+        take(w.M, bh * n * SS);
+        take(w.N, bh * n * SS);
+        take(w.E, bh * (n - 1) * SS);
+        take(w.De, bh * n * SS);
+    }
+    take(w.Sc, std::max<size_t>(bh * nc * SS, 1));
+    take(w.Dc, std::max<size_t>(bh * nc * SS, 1));
+    w.n_x = (int)std::max<size_t>(1, std::min<size_t>(bh * nc, kGdnSlabs));
+    take(w.X, (size_t)w.n_x * 6 * 64 * r.D * 4);
+    w.total = off;
+    return w;
+}
+
 }  // namespace
 
 size_t sf_gdn_fwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning) {
@@ -966,6 +998,7 @@ sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const 
     a.sg_h = r.sg_h;
     a.ts = ts;
     a.n_super = std::max(1, n_super_of(r.L, ts));
+    a.n_prep = a.n_super - 1;
     if (a.n_super > 1) {
         const size_t bh = (size_t)r.B * r.H, SS = (size_t)r.D * r.D * 4;
         a.wsS = (float *)ws;
@@ -985,6 +1018,95 @@ sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const 
     if (on) {
         std::lock_guard<std::mutex> lk(g_prof_mu);
         g_prof_ev[SF_K_GDN_FWD].push_back({e0, e1});
+    }
+    return SF_OK;
+}
+
+size_t sf_gdn_bwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning) {
+    Shape r;
+    int ts;
+    if (resolve(shape, r) != SF_OK || gdn_pick_ts(r, tuning, ts) != SF_OK) return 0;
+    return gdn_bwd_ws(r, ts).total;
+}
+
+sf_status sf_gdn_bwd(const sf_shape *shape, const void *q, const void *k, const void *v, const float *g,
+                     const float *beta, const float *S_in, const void *dO, const float *dS_out, void *dq, void *dk,
+                     void *dv, float *dg, float *dbeta, float *dS_in, void *ws, size_t ws_bytes,
+                     const sf_tuning *tuning, sf_stream stream) {
+    g_err.clear();
+    Shape r;
+    TRY(resolve(shape, r));
+    if (r.io != SF_BF16) return fail(SF_E_UNSUPPORTED, "the gated delta rule needs bf16 I/O");
+    if (r.gate != SF_GATE_SCALAR) return fail(SF_E_UNSUPPORTED, "the gated delta rule takes a scalar gate");
+    if (!dS_in || (r.L > 0 && (!q || !k || !v || !g || !beta || !dO || !dq || !dk || !dv || !dg || !dbeta)))
+        return fail(SF_E_NULL, "q, k, v, g, beta, dO, dq, dk, dv, dg, dbeta and dS_in are required");
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {dO, "dO"}, {dq, "dq"}, {dk, "dk"}, {dv, "dv"}, {S_in, "S_in"},
+                     {dS_out, "dS_out"}, {dS_in, "dS_in"}, {ws, "ws"}}));
+    if (((uintptr_t)g | (uintptr_t)beta | (uintptr_t)dg | (uintptr_t)dbeta) % 4)
+        return fail(SF_E_ALIGN, "g, beta, dg and dbeta must be 4-byte aligned");
+    int ts;
+    TRY(gdn_pick_ts(r, tuning, ts));
+    const GdnBwdWs L = gdn_bwd_ws(r, ts);
+    if (!ws) return fail(SF_E_NULL, "workspace of %zu bytes required", L.total);
+    if (ws_bytes < L.total) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, L.total);
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"), grange(r, g, r.L, "g"),
+                     grange(r, beta, r.L, "beta"), srange(r, S_in, 1, "S_in"), xrange(r, dO, r.L, "dO"),
+                     srange(r, dS_out, 1, "dS_out")},
+                    {xrange(r, dq, r.L, "dq"), xrange(r, dk, r.L, "dk"), xrange(r, dv, r.L, "dv"),
+                     grange(r, dg, r.L, "dg"), grange(r, dbeta, r.L, "dbeta"), srange(r, dS_in, 1, "dS_in"),
+                     {(const char *)ws, (const char *)ws + L.total, "ws"}}));
+    sf::GdnArgs a{};
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.g = g;
+    a.beta = beta;
+    a.S_in = S_in;
+    a.dO = dO;
+    a.dS_out = dS_out;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.dg = dg;
+    a.dbeta = dbeta;
+    a.dS_in = dS_in;
+    a.B = r.B;
+    a.H = r.H;
+    a.L = r.L;
+    a.sx_b = r.sx_b;
+    a.sx_l = r.sx_l;
+    a.sx_h = r.sx_h;
+    a.sg_b = r.sg_b;
+    a.sg_l = r.sg_l;
+    a.sg_h = r.sg_h;
+    a.ts = ts;
+    a.n_super = std::max(1, n_super_of(r.L, ts));
+    a.n_prep = a.n_super;
+    char *base = (char *)ws;
+    if (a.n_super > 1) {
+        a.wsS = (float *)(base + L.S);
+        a.wsM = (float *)(base + L.M);
+        a.wsN = (float *)(base + L.N);
+        a.wsE = (float *)(base + L.E);
+        a.wsDe = (float *)(base + L.De);
+    }
+    a.wsSc = (float *)(base + L.Sc);
+    a.wsDc = (float *)(base + L.Dc);
+    a.wsX = (float *)(base + L.X);
+    a.n_x = L.n_x;
+    bool on;
+    {
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        on = g_prof_on[SF_K_GDN_BWD];
+    }
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (on && (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess))
+        return hip_fail(hipGetLastError(), "profiling event");
+    hipError_t e = sf::launch_gdn_bwd(a, r.D, (hipStream_t)stream, e0, e1);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    if (on) {
+        std::lock_guard<std::mutex> lk(g_prof_mu);
+        g_prof_ev[SF_K_GDN_BWD].push_back({e0, e1});
     }
     return SF_OK;
 }

@@ -29,28 +29,81 @@
 // rule's matrix-valued transition): the chunk map S -> gamma_C S + K~^T (Ubar - W S)
 // is affine in S, so a superchunk of chunks maps S_J to S_{J+1} = M_J S_J + N_J
 // with dense M_J, N_J in R^{Dk x Dk}, R^{Dk x Dv}.
-//   k_gdn_walk<PREP>: walks the superchunk's chunks with the state [M | N]
+//   k_gdn_walk<W_PREP>: walks the superchunk's chunks with the state [M | N]
 //     (wave w owns columns [16w, 16w+16) of both; M from the identity with
 //     Ubar = 0, N from zero) and writes M_J, N_J.  No outputs.
 //   k_gdn_scan: S_{J+1} = M_J S_J + N_J in fp32, sequential over J, 16 state
 //     columns per workgroup; writes every S_J and S_out.
-//   k_gdn_walk<!PREP>: the output walk above from S_J over superchunk J.
+//   k_gdn_walk<W_OUT>: the output walk above from S_J over superchunk J;
+//   k_gdn_walk<W_STORE>: the same walk without outputs, writing the state that
+//     enters every chunk (for the backward).
 #include "sf_chunk.hpp"
 
 namespace sf {
 
 namespace {
 
-template <typename T, int D, bool PREP>
+// (I + A) X = R by forward substitution in fp32, one thread per column of
+// R = [diag(beta gamma) K | diag(beta) V] (threads [0, D) the W columns, [D, 2D)
+// the Ubar columns; nrhs = D solves for W only); X = [W | Ubar] goes to sW / sU,
+// whose column of this thread doubles as its working store.  Blocks of 16
+// rows: the earlier blocks' contribution is a 16 x 16 block update from LDS,
+// the diagonal block a 16-row triangular solve in registers (every register
+// index a compile-time constant).
+template <typename T, int D, int LDN, int LDA, int LDU, int SWX>
+__device__ __forceinline__ void gdn_solve(int tid, int nrhs, const T *sK, const T *sV, const float *sA,
+                                          const float *sbeta, const float *sq, float *sW, float *sU) {
+    if (tid >= nrhs) return;
+    const bool wcol = tid < D;
+    const int j = wcol ? tid : tid - D;
+    float *xc = (wcol ? sW : sU) + j;  // column j, row stride LDU
+    for (int tb = 0; tb < C / 16; ++tb) {
+        float xb[16];
+#pragma unroll
+        for (int tl = 0; tl < 16; ++tl) {
+            const int t = 16 * tb + tl;
+            xb[tl] = wcol ? tof<T>(sK[t * LDN + swz_col(t, j, SWX)]) * sbeta[t] * sq[t] : tof<T>(sV[t * LDN + j]) * sbeta[t];
+        }
+        for (int sb = 0; sb < tb; ++sb) {
+            float xs[16];
+#pragma unroll
+            for (int e = 0; e < 16; ++e) xs[e] = xc[(16 * sb + e) * LDU];
+#pragma unroll
+            for (int tl = 0; tl < 16; ++tl) {
+                const float *ar = &sA[(16 * tb + tl) * LDA + 16 * sb];
+#pragma unroll
+                for (int e4 = 0; e4 < 4; ++e4) {
+                    const f32x4 av = *reinterpret_cast<const f32x4 *>(ar + 4 * e4);
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) xb[tl] = fmaf(-av[u], xs[4 * e4 + u], xb[tl]);
+                }
+            }
+        }
+#pragma unroll
+        for (int tl = 1; tl < 16; ++tl) {
+            const float *ar = &sA[(16 * tb + tl) * LDA + 16 * tb];
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                if (e < tl) xb[tl] = fmaf(-ar[e], xb[e], xb[tl]);
+        }
+#pragma unroll
+        for (int tl = 0; tl < 16; ++tl) xc[(16 * tb + tl) * LDU] = xb[tl];
+    }
+}
+
+enum { W_OUT = 0, W_PREP = 1, W_STORE = 2 };
+
+template <typename T, int D, int MODE>
 __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
+    constexpr bool PREP = MODE == W_PREP, OUTP = MODE == W_OUT;  // STORE: states only
     constexpr int NW = D / 16, NT = 64 * NW, NK = D / 16, NS = PREP ? 2 : 1;
     constexpr int LDN = D + pad<T>(), LDT = C + pad<T>(), SWX = swx<T, D>();
     constexpr int LDA = C + 4, LDU = D + 4;  // 16-byte-odd pitches: conflict-free row-varying reads
-    __shared__ __attribute__((aligned(16))) T sQ[PREP ? 8 : C * LDN];    // plain
+    __shared__ __attribute__((aligned(16))) T sQ[OUTP ? C * LDN : 8];    // plain
     __shared__ __attribute__((aligned(16))) T sK[C * LDN];               // plain, swizzled
     __shared__ __attribute__((aligned(16))) T sV[C * LDN];               // plain
-    __shared__ __attribute__((aligned(16))) T sP[PREP ? 8 : C * LDT];    // (Q K^T o Gamma)[t][s] hi
-    __shared__ __attribute__((aligned(16))) T sPl[PREP ? 8 : C * LDT];   // lo
+    __shared__ __attribute__((aligned(16))) T sP[OUTP ? C * LDT : 8];    // (Q K^T o Gamma)[t][s] hi
+    __shared__ __attribute__((aligned(16))) T sPl[OUTP ? C * LDT : 8];   // lo
     __shared__ __attribute__((aligned(16))) float sA[C * LDA];    // beta_t e^{b_t-b_s} k_t.k_s, s < t
     __shared__ __attribute__((aligned(16))) float sW[C * LDU];    // W [t][k], fp32
     __shared__ __attribute__((aligned(16))) float sU[C * LDU];    // Ubar [t][v], fp32
@@ -60,7 +113,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c0 = 16 * w;
     // items: (b, h, J) with J < n_super (walk) or J < n_super - 1 (prep)
-    const int nJ = PREP ? a.n_super - 1 : a.n_super;
+    const int nJ = PREP ? a.n_prep : a.n_super;
     const int item = blockIdx.x, bh = item / nJ, J = item % nJ;
     const int bb = bh / a.H, hh = bh % a.H;
     const int64_t tok0 = (int64_t)J * a.ts;
@@ -107,7 +160,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
     const uint32_t tstep = (uint32_t)(16 * a.sx_l * (int64_t)sizeof(T));
     auto issue = [&](int c) {
         const int64_t nx = c * cstep;
-        if constexpr (!PREP) t1.load_buf(buf_rsrc(Q + nx, cspan), toff, 0);
+        if constexpr (OUTP) t1.load_buf(buf_rsrc(Q + nx, cspan), toff, 0);
         t2.load_buf(buf_rsrc(K + nx, cspan), toff, 0);
         t3.load_buf(buf_rsrc(V + nx, cspan), toff, 0);
         gl = buf_ld<float>(buf_rsrc(gp + (int64_t)c * C * a.sg_l, gspan), goff, 0);
@@ -116,11 +169,18 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
     if (nch > 0) issue(0);
 
     for (int c = 0; c < nch; ++c) {
+        if constexpr (MODE == W_STORE) {
+            float *dst = a.wsSc + ((int64_t)bh * (a.L / C) + tok0 / C + c) * SS;
+#pragma unroll
+            for (int i = 0; i < NK; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = S[0][i][r];
+        }
         const float b2 = wave_scan_dpp(gl * LOG2E);
         const float b63 = lane_value(b2, 63);
         const float betal = bl;
         __syncthreads();  // the previous chunk is done with every LDS tile
-        if constexpr (!PREP) t1.store_swz(sQ, LDN, tid, 0);
+        if constexpr (OUTP) t1.store_swz(sQ, LDN, tid, 0);
         t2.store_swz(sK, LDN, tid, SWX);
         t3.store_swz(sV, LDN, tid, 0);
         if (w == 0) {
@@ -133,7 +193,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         if (c + 1 < nch) issue(c + 1);
 
         // scores on the causal tiles: P^T[s][t] = k_s . q_t and k_s . k_t
-        for (int i = PREP ? 10 + w : w; i < 20; i += NW) {
+        for (int i = OUTP ? w : 10 + w; i < 20; i += NW) {
             const bool kk = i >= 10;
             int tt, st;
             tri_tile(kk ? i - 10 : i, tt, st);
@@ -150,7 +210,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
             const f32x4 bs = *reinterpret_cast<const f32x4 *>(&sb[16 * st + 4 * q4]);
             float v4[4];
             if (!kk) {
-                if constexpr (!PREP) {
+                if constexpr (OUTP) {
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int s = 16 * st + 4 * q4 + r;
@@ -170,7 +230,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
             }
         }
         // P tiles above the diagonal that the output product reads are zero
-        for (int e = tid; e < (PREP ? 0 : 512); e += NT) {
+        for (int e = tid; e < (OUTP ? 512 : 0); e += NT) {
             const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
             const int row = tile ? 32 + rr : rr, col = tile ? 48 + cc : 16 + cc;
             sP[row * LDT + (col ^ asw(row))] = cvt<T>(0.f);
@@ -178,50 +238,8 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         }
         __syncthreads();
 
-        // (I + A) X = R, forward substitution in fp32, one thread per column of
-        // R = [diag(beta gamma) K | diag(beta) V]; X = [W | Ubar] is written to
-        // sW / sU, whose column of this thread doubles as its working store.
-        // Blocks of 16 rows: the earlier blocks' contribution is a 16 x 16
-        // block update from LDS, the diagonal block a 16-row triangular solve in
-        // registers (every register index a compile-time constant).
-        if (tid < 2 * D) {
-            const bool wcol = tid < D;
-            const int j = wcol ? tid : tid - D;
-            float *xc = (wcol ? sW : sU) + j;  // column j, row stride LDU
-            for (int tb = 0; tb < C / 16; ++tb) {
-                float xb[16];
-#pragma unroll
-                for (int tl = 0; tl < 16; ++tl) {
-                    const int t = 16 * tb + tl;
-                    xb[tl] = wcol ? tof<T>(sK[t * LDN + swz_col(t, j, SWX)]) * sbeta[t] * sq[t]
-                                  : tof<T>(sV[t * LDN + j]) * sbeta[t];
-                }
-                for (int sb = 0; sb < tb; ++sb) {
-                    float xs[16];
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) xs[e] = xc[(16 * sb + e) * LDU];
-#pragma unroll
-                    for (int tl = 0; tl < 16; ++tl) {
-                        const float *ar = &sA[(16 * tb + tl) * LDA + 16 * sb];
-#pragma unroll
-                        for (int e4 = 0; e4 < 4; ++e4) {
-                            const f32x4 av = *reinterpret_cast<const f32x4 *>(ar + 4 * e4);
-#pragma unroll
-                            for (int u = 0; u < 4; ++u) xb[tl] = fmaf(-av[u], xs[4 * e4 + u], xb[tl]);
-                        }
-                    }
-                }
-#pragma unroll
-                for (int tl = 1; tl < 16; ++tl) {
-                    const float *ar = &sA[(16 * tb + tl) * LDA + 16 * tb];
-#pragma unroll
-                    for (int e = 0; e < 16; ++e)
-                        if (e < tl) xb[tl] = fmaf(-ar[e], xb[e], xb[tl]);
-                }
-#pragma unroll
-                for (int tl = 0; tl < 16; ++tl) xc[(16 * tb + tl) * LDU] = xb[tl];
-            }
-        }
+        // (I + A) [W | Ubar] = [diag(beta gamma) K | diag(beta) V]
+        gdn_solve<T, D, LDN, LDA, LDU, SWX>(tid, 2 * D, sK, sV, sA, sbeta, sq, sW, sU);
         __syncthreads();
 
         // U[t][v] = Ubar[t][v] - sum_k W[t][k] S[k][v]  (rows t = 16tt + 4q4 + r, column v = c0 + n16);
@@ -257,10 +275,10 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
                     mma(U[m][tt], wh, fl[m]);
                     mma(U[m][tt], wl, fh[m]);
                 }
-                if constexpr (!PREP) mma2<T, true>(O[tt], fh[0], fl[0], ldfrag(sQ, LDN, 16 * tt, 32 * ks, lane));
+                if constexpr (OUTP) mma2<T, true>(O[tt], fh[0], fl[0], ldfrag(sQ, LDN, 16 * tt, 32 * ks, lane));
             }
         }
-        if constexpr (!PREP) {
+        if constexpr (OUTP) {
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) O[tt] *= sq[16 * tt + n16];
 #pragma unroll
@@ -284,7 +302,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         }
 
         // V^new (optional): U[16tt + 4q4 + r][c0 + n16]
-        if (!PREP && VN) {
+        if (OUTP && VN) {
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
@@ -317,7 +335,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         }
     }
     // prep: M_J, N_J; walk: S_out after the last superchunk
-    if (PREP || J == a.n_super - 1) {
+    if (PREP || (OUTP && J == a.n_super - 1)) {
 #pragma unroll
         for (int m = 0; m < NS; ++m) {
             float *dst = PREP ? (m == 0 ? a.wsM : a.wsN) + (int64_t)item * SS : a.S_out + bh * SS;
@@ -343,8 +361,8 @@ __global__ void __launch_bounds__(256) k_gdn_scan(GdnArgs a) {
     const int64_t SS = (int64_t)D * D;
     const int nJ = a.n_super;
     float *wsS = a.wsS + (int64_t)bh * nJ * SS;
-    const float *wsM = a.wsM + (int64_t)bh * (nJ - 1) * SS;
-    const float *wsN = a.wsN + (int64_t)bh * (nJ - 1) * SS;
+    const float *wsM = a.wsM + (int64_t)bh * a.n_prep * SS;
+    const float *wsN = a.wsN + (int64_t)bh * a.n_prep * SS;
     float acc[CPT];
 #pragma unroll
     for (int j = 0; j < CPT; ++j) acc[j] = a.S_in ? a.S_in[bh * SS + (int64_t)k * D + col0 + j] : 0.f;
@@ -387,23 +405,744 @@ __global__ void __launch_bounds__(256) k_gdn_scan(GdnArgs a) {
 }
 
 
+// ------------------------------------------------------------------ backward
+//
+// Per chunk, with S the state entering it, dS' the gradient of the state leaving
+// it and the forward quantities above (b, gamma, Gamma, A, W, Ubar, U, P):
+//   dU  = diag(e^{b_C - b}) K dS' + P^T dO
+//   dS  = gamma_C dS' + Q^T diag(gamma) dO - W^T dU          (the state gradient entering)
+//   dq  = diag(gamma) dO S^T + (dO U^T o Gamma) K
+//   dk  = diag(e^{b_C - b}) U dS'^T + (dO U^T o Gamma)^T Q + diag(beta gamma) G_W + Ah K + Ah^T K
+//   dv  = diag(beta) G_U,   [G_W | G_U] = (I + A)^{-T} [-dU S^T | dU]
+//   dA  = -(G_W W^T + G_U Ubar^T) on s < t,   Ah = dA o beta_t e^{b_t - b_s}
+//   dbeta_t = gamma_t <G_W_t, k_t> + <G_U_t, v_t> + sum_s dA[t][s] e^{b_t - b_s} k_t.k_s
+// and the log-decay gradient collects, per token, every term through b_t
+// (gamma_t, Gamma, A, e^{b_C - b_t}, gamma_C), summed in reverse over the chunk.
+// dS runs backwards over the chunks; it is the chunk map's transpose, so a
+// superchunk maps dS_end to dS_start = M_J^T dS_end + E_J, with M_J the forward
+// prep's and E_J the walk from dS_end = 0.
+//   k_gdn_dwalk<true>:  E_J for J >= 1;
+//   k_gdn_dscan:        dS_end(J) for every J (M_{J+1}^T, fp32, in reverse);
+//   k_gdn_dwalk<false>: from dS_end(J), writes dS' of every chunk and dS_in;
+//   k_gdn_dchunk:       the parameter gradients of every chunk, all chunks in
+//                       parallel, from the stored S and dS' (fp32 arithmetic).
+
+template <typename T, int D, bool PREP>
+__global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
+    constexpr int NW = D / 16, NT = 64 * NW, NK = D / 16;
+    constexpr int LDN = D + pad<T>(), LDT = C + pad<T>(), SWX = swx<T, D>();
+    constexpr int LDA = C + 4, LDU = D + 4;
+    __shared__ __attribute__((aligned(16))) T sQ[C * LDN];   // swizzled
+    __shared__ __attribute__((aligned(16))) T sK[C * LDN];   // swizzled
+    __shared__ __attribute__((aligned(16))) T sO[C * LDN];   // dO, swizzled
+    __shared__ __attribute__((aligned(16))) T sP[C * LDT];   // P^T[s][t] = e^{b_t-b_s} k_s.q_t (s <= t) hi
+    __shared__ __attribute__((aligned(16))) T sPl[C * LDT];  // lo
+    __shared__ __attribute__((aligned(16))) float sA[C * LDA];
+    __shared__ __attribute__((aligned(16))) float sW[C * LDU];
+    __shared__ __attribute__((aligned(16))) float sb[C], sq[C], se[C], sbeta[C];
+
+    const int tid = threadIdx.x, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int c0 = 16 * w;
+    const int nJ = PREP ? a.n_super - 1 : a.n_super;
+    const int item = blockIdx.x, bh = item / nJ, J = (PREP ? 1 : 0) + item % nJ;
+    const int bb = bh / a.H, hh = bh % a.H;
+    const int64_t tok0 = (int64_t)J * a.ts;
+    const int64_t xo = bb * a.sx_b + hh * a.sx_h + tok0 * a.sx_l;
+    const T *Q = (const T *)a.q + xo;
+    const T *K = (const T *)a.k + xo;
+    const T *DO = (const T *)a.dO + xo;
+    const int64_t go = bb * a.sg_b + hh * a.sg_h + tok0 * a.sg_l;
+    const float *gp = a.g + go;
+    const float *bp = a.beta + go;
+    const int64_t SS = (int64_t)D * D;
+    const int nch = (int)((a.L - tok0 < a.ts ? a.L - tok0 : a.ts) / C);
+    const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
+    auto asw = [](int row) { return sizeof(T) == 2 ? 8 * ((row >> 2) & 1) : 0; };
+
+    // dS[16i + 4q4 + r][c0 + n16]: from dS_end(J) (dS_out for one superchunk), or 0 (prep)
+    f32x4 dS[NK];
+    {
+        const float *src = a.n_super == 1 ? (a.dS_out ? a.dS_out + bh * SS : nullptr)
+                                          : a.wsDe + ((int64_t)bh * a.n_super + J) * SS;
+#pragma unroll
+        for (int i = 0; i < NK; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                dS[i][r] = (!PREP && src) ? src[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] : 0.f;
+    }
+
+    using TT = Tile<T, D, NT>;
+    TT t1, t2, t3;
+    float gl, bl;
+    const int64_t cstep = (int64_t)C * a.sx_l;
+    const uint32_t cspan = chunk_span<T, D>(a.sx_l), gspan = (uint32_t)(((C - 1) * a.sg_l + 1) * 4);
+    uint32_t toff[TT::RPT];
+    TT::offsets(toff, a.sx_l, tid);
+    const uint32_t goff = (uint32_t)(lane * a.sg_l * 4);
+    auto issue = [&](int c) {
+        const int64_t nx = c * cstep;
+        t1.load_buf(buf_rsrc(Q + nx, cspan), toff, 0);
+        t2.load_buf(buf_rsrc(K + nx, cspan), toff, 0);
+        t3.load_buf(buf_rsrc(DO + nx, cspan), toff, 0);
+        gl = buf_ld<float>(buf_rsrc(gp + (int64_t)c * C * a.sg_l, gspan), goff, 0);
+        bl = buf_ld<float>(buf_rsrc(bp + (int64_t)c * C * a.sg_l, gspan), goff, 0);
+    };
+    if (nch > 0) issue(nch - 1);
+
+    for (int c = nch - 1; c >= 0; --c) {
+        if constexpr (!PREP) {  // dS' of chunk c: the gradient of the state leaving it
+            float *dst = a.wsDc + ((int64_t)bh * (a.L / C) + tok0 / C + c) * SS;
+#pragma unroll
+            for (int i = 0; i < NK; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = dS[i][r];
+        }
+        const float b2 = wave_scan_dpp(gl * LOG2E);
+        const float b63 = lane_value(b2, 63);
+        const float betal = bl;
+        __syncthreads();  // the previous chunk is done with every LDS tile
+        t1.store_swz(sQ, LDN, tid, SWX);
+        t2.store_swz(sK, LDN, tid, SWX);
+        t3.store_swz(sO, LDN, tid, SWX);
+        if (w == 0) {
+            sb[lane] = b2;
+            sq[lane] = fexp2(b2);
+            se[lane] = fexp2(b63 - b2);
+            sbeta[lane] = betal;
+        }
+        __syncthreads();
+        if (c > 0) issue(c - 1);
+
+        // scores on the causal tiles: k_s . q_t -> P^T, k_s . k_t -> A
+        for (int i = w; i < 20; i += NW) {
+            const bool kk = i >= 10;
+            int tt, st;
+            tri_tile(kk ? i - 10 : i, tt, st);
+            f32x4 p = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks) {
+                const frag_t<T> kf = ldfrag_swz<T, LDN, SWX>(sK, swo, 16 * st, 32 * ks);
+                const frag_t<T> xf = ldfrag_swz<T, LDN, SWX>(kk ? sK : sQ, swo, 16 * tt, 32 * ks);
+                mma(p, kf, xf);
+            }
+            const int t = 16 * tt + n16;
+            const float bt = sb[t];
+            const f32x4 bs = *reinterpret_cast<const f32x4 *>(&sb[16 * st + 4 * q4]);
+            if (!kk) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int s = 16 * st + 4 * q4 + r;
+                    const float v = s <= t ? p[r] * fexp2(bt - bs[r]) : 0.f;
+                    const T h = cvt<T>(v);
+                    sP[s * LDT + (t ^ asw(s))] = h;
+                    sPl[s * LDT + (t ^ asw(s))] = cvt<T>(v - tof<T>(h));
+                }
+            } else {
+                const float be = sbeta[t];
+                float v4[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int s = 16 * st + 4 * q4 + r;
+                    v4[r] = s < t ? be * p[r] * fexp2(bt - bs[r]) : 0.f;
+                }
+                *reinterpret_cast<f32x4 *>(&sA[t * LDA + 16 * st + 4 * q4]) = f32x4{v4[0], v4[1], v4[2], v4[3]};
+            }
+        }
+        // P^T tiles below the diagonal that the dU product reads are zero
+        for (int e = tid; e < 512; e += NT) {
+            const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
+            const int row = tile ? 48 + rr : 16 + rr, col = tile ? 32 + cc : cc;
+            sP[row * LDT + (col ^ asw(row))] = cvt<T>(0.f);
+            sPl[row * LDT + (col ^ asw(row))] = cvt<T>(0.f);
+        }
+        __syncthreads();
+        gdn_solve<T, D, LDN, LDA, LDU, SWX>(tid, D, sK, nullptr, sA, sbeta, sq, sW, nullptr);
+        __syncthreads();
+
+        // dU[t][v] = e^{b_C - b_t} sum_k K[t][k] dS[k][v] + sum_{t' >= t} P^T[t][t'] dO[t'][v]
+        // (rows t = 16tt + 4q4 + r, column v = c0 + n16)
+        f32x4 dU[4];
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) dU[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) {
+            frag_t<T> fh, fl;
+            split_acc_plain<T, true>(dS[2 * ks], dS[2 * ks + 1], fh, fl);
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) {
+                const frag_t<T> kf = ldfrag_swz<T, LDN, SWX>(sK, swo, 16 * tt, 32 * ks);
+                mma(dU[tt], kf, fh);
+                mma(dU[tt], kf, fl);
+            }
+        }
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dU[tt][r] *= se[16 * tt + 4 * q4 + r];
+#pragma unroll
+        for (int ks = 0; ks < C / 32; ++ks) {
+            const frag_t<T> of = ldfragTR<T, LDN, SWX>(sO, tro, 32 * ks, c0);
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) {
+                if (32 * ks + 31 < 16 * tt) continue;
+                const int aw = asw(lane & 15);
+                const int o = (16 * tt + (lane & 15)) * LDT + ((32 * ks + 8 * (lane >> 4)) ^ aw);
+                mma(dU[tt], *reinterpret_cast<const frag_t<T> *>(sP + o), of);
+                mma(dU[tt], *reinterpret_cast<const frag_t<T> *>(sPl + o), of);
+            }
+        }
+
+        // dS = gamma_C dS + Q^T diag(gamma) dO - W^T dU
+        const float gam = fexp2(b63);
+#pragma unroll
+        for (int i = 0; i < NK; ++i) dS[i] *= gam;
+#pragma unroll
+        for (int ks = 0; ks < C / 32; ++ks) {
+            f32x4 g0, g1;  // gamma_t dO[t][c0 + n16], t = 32ks + 16h + 4q4 + r
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int ta = 32 * ks + 4 * q4 + r, tb = ta + 16;
+                g0[r] = sq[ta] * tof<T>(sO[ta * LDN + swz_col(ta, c0 + n16, SWX)]);
+                g1[r] = sq[tb] * tof<T>(sO[tb * LDN + swz_col(tb, c0 + n16, SWX)]);
+            }
+            frag_t<T> gh, glo, uh, ul;
+            split_acc_plain<T, true>(g0, g1, gh, glo);
+            split_acc_plain<T, true>(dU[2 * ks], dU[2 * ks + 1], uh, ul);
+#pragma unroll
+            for (int i = 0; i < NK; ++i) {
+                mma2b<T, true>(dS[i], ldfragTR<T, LDN, SWX>(sQ, tro, 32 * ks, 16 * i), gh, glo);
+                float wn[8];  // -W[t][k], k = 16i + lane % 16, t = 32ks + 8 (lane / 16) + j
+#pragma unroll
+                for (int j = 0; j < 8; ++j) wn[j] = -sW[(32 * ks + 8 * q4 + j) * LDU + 16 * i + n16];
+                frag_t<T> wh, wl;
+                split8<T, true>(wn, wh, wl);
+                mma(dS[i], wh, uh);
+                mma(dS[i], wh, ul);
+                mma(dS[i], wl, uh);
+            }
+        }
+    }
+    float *dst = PREP ? a.wsE + ((int64_t)bh * (a.n_super - 1) + J - 1) * SS : (J == 0 ? a.dS_in + bh * SS : nullptr);
+    if (dst) {
+#pragma unroll
+        for (int i = 0; i < NK; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = dS[i][r];
+    }
+}
+
+// dS_end(n-1) = dS_out (or 0); dS_end(J-1) = M_J^T dS_end(J) + E_J, written to
+// wsDe for every J.  Same shape of work as k_gdn_scan, with M_J read transposed.
+template <int D>
+__global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
+    constexpr int NT = 256, RPT = NT / D, CPT = 16 / RPT, LDM = D + 4, MV = D * D / 4 / NT;
+    __shared__ __attribute__((aligned(16))) float sM[D * LDM];
+    __shared__ __attribute__((aligned(16))) float sS[D * 16];
+    const int tid = threadIdx.x, k = tid % D, cg = tid / D;
+    const int bh = blockIdx.x / (D / 16), col0 = 16 * (blockIdx.x % (D / 16)) + CPT * cg;
+    const int64_t SS = (int64_t)D * D;
+    const int nJ = a.n_super;
+    float *wsDe = a.wsDe + (int64_t)bh * nJ * SS;
+    const float *wsM = a.wsM + (int64_t)bh * a.n_prep * SS;
+    const float *wsE = a.wsE + (int64_t)bh * (nJ - 1) * SS;
+    float acc[CPT];
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) acc[j] = a.dS_out ? a.dS_out[bh * SS + (int64_t)k * D + col0 + j] : 0.f;
+    f32x4 mreg[MV];
+    auto fetch = [&](int J) {
+        const f32x4 *m = reinterpret_cast<const f32x4 *>(wsM + (int64_t)J * SS);
+#pragma unroll
+        for (int i = 0; i < MV; ++i) mreg[i] = m[tid + NT * i];
+    };
+    if (nJ > 1) fetch(nJ - 1);
+    for (int J = nJ - 1;; --J) {
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) {
+            sS[k * 16 + col0 % 16 + j] = acc[j];
+            wsDe[(int64_t)J * SS + (int64_t)k * D + col0 + j] = acc[j];
+        }
+        if (J == 0) break;
+        float nv[CPT];
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) nv[j] = wsE[(int64_t)(J - 1) * SS + (int64_t)k * D + col0 + j];
+#pragma unroll
+        for (int i = 0; i < MV; ++i) {
+            const int e = 4 * (tid + NT * i);
+            *reinterpret_cast<f32x4 *>(&sM[(e / D) * LDM + e % D]) = mreg[i];
+        }
+        __syncthreads();
+        if (J - 1 >= 1) fetch(J - 1);
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) acc[j] = nv[j];
+#pragma unroll 4
+        for (int c = 0; c < D; ++c) {
+            const float m = sM[c * LDM + k];  // M_J^T[k][c]
+#pragma unroll
+            for (int j = 0; j < CPT; ++j) acc[j] = fmaf(m, sS[c * 16 + col0 % 16 + j], acc[j]);
+        }
+        __syncthreads();
+    }
+}
+
+// Parameter gradients of one chunk per item (b, h, chunk), items in a
+// grid-stride loop, fp32 arithmetic throughout.  256 threads; thread
+// (tr, tc) = (tid / 16, tid % 16) owns rows 4tr .. 4tr+3 and columns
+// tc + 16j of every 64 x D and 64 x 64 product.  q, k, v, dO in LDS (bf16),
+// the 64 x 64 matrices in LDS (fp32), the 64 x D intermediates in a per-
+// workgroup scratch slab of wsX (L2 resident), S and dS' read from the stored
+// per-chunk states.
+template <typename T, int D>
+__global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
+    constexpr int LDX = D + 8, LD6 = C + 1, NJ = D / 16;
+    __shared__ __attribute__((aligned(16))) T xq[C * LDX], xk[C * LDX], xv[C * LDX], xo[C * LDX];
+    __shared__ float sKK[C * LD6];  // e^{b_t-b_s} k_t.k_s, s < t (later Ah)
+    __shared__ float sT[C * LD6];   // (I + A)^{-1}
+    __shared__ float sPt[C * LD6];  // e^{b_t-b_s} q_t.k_s, s <= t
+    __shared__ float sdP[C * LD6];  // (dO U^T o Gamma)[t][s], s <= t
+    __shared__ float sb[C], sg[C], se[C], sbe[C];
+    __shared__ float rB[C * 17], rD[C * 17], rC[C * 17], r63[256];
+
+    const int tid = threadIdx.x, tr = tid >> 4, tc = tid & 15;
+    const int64_t SS = (int64_t)D * D, SX = (int64_t)C * D;
+    const int nc = (int)(a.L / C);
+    const int64_t items = (int64_t)a.B * a.H * nc;
+    float *X = a.wsX + (int64_t)blockIdx.x * 6 * SX;
+    float *gW = X, *gUb = X + SX, *gU = X + 2 * SX, *gdU = X + 3 * SX, *gGW = X + 4 * SX, *gGU = X + 5 * SX;
+    auto ld = [](const T *m, int r, int c) { return tof<T>(m[r * LDX + c]); };
+
+    for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
+        const int bh = (int)(it / nc), ch = (int)(it % nc), bb = bh / a.H, hh = bh % a.H;
+        const int64_t xo0 = bb * a.sx_b + hh * a.sx_h + (int64_t)ch * C * a.sx_l;
+        const int64_t go0 = bb * a.sg_b + hh * a.sg_h + (int64_t)ch * C * a.sg_l;
+        const float *S = a.wsSc + ((int64_t)bh * nc + ch) * SS;
+        const float *dS = a.wsDc + ((int64_t)bh * nc + ch) * SS;
+        __syncthreads();  // the previous item is done with LDS and the slab
+        for (int e = tid; e < C * D / 8; e += 256) {
+            const int t = e / (D / 8), c8 = 8 * (e % (D / 8));
+            const int64_t off = xo0 + (int64_t)t * a.sx_l + c8;
+            *reinterpret_cast<frag_t<T> *>(&xq[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.q + off);
+            *reinterpret_cast<frag_t<T> *>(&xk[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.k + off);
+            *reinterpret_cast<frag_t<T> *>(&xv[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.v + off);
+            *reinterpret_cast<frag_t<T> *>(&xo[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.dO + off);
+        }
+        if (tid < 64) {
+            float b = wave_scan_dpp(a.g[go0 + (int64_t)tid * a.sg_l]);
+            const float bC = lane_value(b, 63);
+            sb[tid] = b;
+            sg[tid] = expf(b);
+            se[tid] = expf(bC - b);
+            sbe[tid] = a.beta[go0 + (int64_t)tid * a.sg_l];
+        }
+        __syncthreads();
+
+        float rowb[4] = {0.f, 0.f, 0.f, 0.f}, rowd[4] = {0.f, 0.f, 0.f, 0.f}, colb[4] = {0.f, 0.f, 0.f, 0.f};
+        float tot63 = 0.f;
+        // scores (64 x 64, contraction over the D channels)
+        {
+            float pk[4][4] = {}, pq[4][4] = {};
+            for (int c = 0; c < D; ++c) {
+                float kr[4], qr[4], kc[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    kr[i] = ld(xk, 4 * tr + i, c);
+                    qr[i] = ld(xq, 4 * tr + i, c);
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j) kc[j] = ld(xk, tc + 16 * j, c);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        pk[i][j] = fmaf(kr[i], kc[j], pk[i][j]);
+                        pq[i][j] = fmaf(qr[i], kc[j], pq[i][j]);
+                    }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int t = 4 * tr + i, s = tc + 16 * j;
+                    const float ga = expf(sb[t] - sb[s]);
+                    sKK[t * LD6 + s] = s < t ? ga * pk[i][j] : 0.f;
+                    sPt[t * LD6 + s] = s <= t ? ga * pq[i][j] : 0.f;
+                }
+        }
+        __syncthreads();
+        // T = (I + A)^{-1}, A = diag(beta) KK: column j by forward substitution
+        if (tid < C) {
+            const int j = tid;
+            for (int t = 0; t < C; ++t) {
+                float x = t == j ? 1.f : 0.f;
+                if (t > j) {
+                    float acc = 0.f;
+                    for (int s2 = j; s2 < t; ++s2) acc = fmaf(sKK[t * LD6 + s2], sT[s2 * LD6 + j], acc);
+                    x = -sbe[t] * acc;
+                }
+                sT[t * LD6 + j] = x;
+            }
+        }
+        __syncthreads();
+        // W = T diag(beta gamma) K, Ubar = T diag(beta) V
+        {
+            float w[4][NJ] = {}, u[4][NJ] = {};
+            for (int s2 = 0; s2 < C; ++s2) {
+                float tv[4], kc[NJ], vc[NJ];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) tv[i] = sT[(4 * tr + i) * LD6 + s2];
+                const float fw = sbe[s2] * sg[s2], fv = sbe[s2];
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    kc[j] = fw * ld(xk, s2, tc + 16 * j);
+                    vc[j] = fv * ld(xv, s2, tc + 16 * j);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) {
+                        w[i][j] = fmaf(tv[i], kc[j], w[i][j]);
+                        u[i][j] = fmaf(tv[i], vc[j], u[i][j]);
+                    }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    gW[(4 * tr + i) * D + tc + 16 * j] = w[i][j];
+                    gUb[(4 * tr + i) * D + tc + 16 * j] = u[i][j];
+                }
+        }
+        __syncthreads();
+        // U = Ubar - W S;  dU = diag(e^{b_C - b}) K dS' + P^T dO
+        {
+            float u[4][NJ], du[4][NJ] = {};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) u[i][j] = gUb[(4 * tr + i) * D + tc + 16 * j];
+            for (int c = 0; c < D; ++c) {
+                float wr[4], kr[4], sc[NJ], dc[NJ];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    wr[i] = gW[(4 * tr + i) * D + c];
+                    kr[i] = ld(xk, 4 * tr + i, c);
+                }
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    sc[j] = S[(int64_t)c * D + tc + 16 * j];
+                    dc[j] = dS[(int64_t)c * D + tc + 16 * j];
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) {
+                        u[i][j] = fmaf(-wr[i], sc[j], u[i][j]);
+                        du[i][j] = fmaf(kr[i], dc[j], du[i][j]);
+                    }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) du[i][j] *= se[4 * tr + i];
+            for (int t2 = 0; t2 < C; ++t2) {
+                float pr[4], oc[NJ];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) pr[i] = sPt[t2 * LD6 + 4 * tr + i];
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) oc[j] = ld(xo, t2, tc + 16 * j);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) du[i][j] = fmaf(pr[i], oc[j], du[i][j]);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    gU[(4 * tr + i) * D + tc + 16 * j] = u[i][j];
+                    gdU[(4 * tr + i) * D + tc + 16 * j] = du[i][j];
+                }
+        }
+        __syncthreads();
+        // G_U = T^T dU (dv, dbeta);  dW = -dU S^T (to gGW)
+        {
+            float gu[4][NJ] = {}, dw[4][NJ] = {};
+            for (int t2 = 0; t2 < C; ++t2) {
+                float tr4[4], dc[NJ];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) tr4[i] = sT[t2 * LD6 + 4 * tr + i];
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) dc[j] = gdU[t2 * D + tc + 16 * j];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) gu[i][j] = fmaf(tr4[i], dc[j], gu[i][j]);
+            }
+            for (int c = 0; c < D; ++c) {
+                float dr[4], sc[NJ];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) dr[i] = gdU[(4 * tr + i) * D + c];
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) sc[j] = S[(int64_t)(tc + 16 * j) * D + c];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) dw[i][j] = fmaf(-dr[i], sc[j], dw[i][j]);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int t = 4 * tr + i;
+                T *dv = (T *)a.dv + xo0 + (int64_t)t * a.sx_l;
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    const int c = tc + 16 * j;
+                    gGU[t * D + c] = gu[i][j];
+                    gGW[t * D + c] = dw[i][j];
+                    dv[c] = cvt<T>(sbe[t] * gu[i][j]);
+                    rowd[i] = fmaf(gu[i][j], ld(xv, t, c), rowd[i]);
+                }
+            }
+        }
+        __syncthreads();
+        // G_W = T^T dW; dk starts as diag(beta gamma) G_W
+        float dk[4][NJ];
+        {
+            float gw[4][NJ] = {};
+            for (int t2 = 0; t2 < C; ++t2) {
+                float tr4[4], dc[NJ];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) tr4[i] = sT[t2 * LD6 + 4 * tr + i];
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) dc[j] = gGW[t2 * D + tc + 16 * j];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) gw[i][j] = fmaf(tr4[i], dc[j], gw[i][j]);
+            }
+            __syncthreads();  // every read of dW is done
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int t = 4 * tr + i;
+                float kg = 0.f;
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    const int c = tc + 16 * j;
+                    gGW[t * D + c] = gw[i][j];
+                    dk[i][j] = sbe[t] * sg[t] * gw[i][j];
+                    kg = fmaf(gw[i][j], ld(xk, t, c), kg);
+                }
+                rowd[i] = fmaf(sg[t], kg, rowd[i]);
+                rowb[i] = fmaf(sbe[t] * sg[t], kg, rowb[i]);
+            }
+        }
+        __syncthreads();
+        // dA = -(G_W W^T + G_U Ubar^T) on s < t;  dP = dO U^T on s <= t
+        {
+            float da[4][4] = {}, dp[4][4] = {};
+            for (int c = 0; c < D; ++c) {
+                float gwr[4], gur[4], orr[4], wc[4], uc[4], ucur[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    gwr[i] = gGW[(4 * tr + i) * D + c];
+                    gur[i] = gGU[(4 * tr + i) * D + c];
+                    orr[i] = ld(xo, 4 * tr + i, c);
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int s2 = tc + 16 * j;
+                    wc[j] = gW[s2 * D + c];
+                    uc[j] = gUb[s2 * D + c];
+                    ucur[j] = gU[s2 * D + c];
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        da[i][j] = fmaf(-gwr[i], wc[j], da[i][j]);
+                        da[i][j] = fmaf(-gur[i], uc[j], da[i][j]);
+                        dp[i][j] = fmaf(orr[i], ucur[j], dp[i][j]);
+                    }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int t = 4 * tr + i, s2 = tc + 16 * j;
+                    const float kk = sKK[t * LD6 + s2];  // 0 unless s < t
+                    const float dA = s2 < t ? da[i][j] : 0.f;
+                    rowd[i] = fmaf(dA, kk, rowd[i]);
+                    const float ea = dA * sbe[t] * kk;  // dA o A
+                    rowb[i] += ea;
+                    colb[j] -= ea;
+                    const float pt = sPt[t * LD6 + s2];  // 0 unless s <= t
+                    const float ep = s2 <= t ? dp[i][j] * pt : 0.f;  // dP o P
+                    rowb[i] += ep;
+                    colb[j] -= ep;
+                    const float ga = s2 <= t ? expf(sb[t] - sb[s2]) : 0.f;
+                    sdP[t * LD6 + s2] = s2 <= t ? dp[i][j] * ga : 0.f;
+                    sKK[t * LD6 + s2] = dA * sbe[t] * ga;  // Ah
+                }
+        }
+        __syncthreads();
+        // dq = diag(gamma) dO S^T + dP K;  dk += diag(e^{b_C - b}) U dS'^T + dP^T Q + Ah K + Ah^T K
+        {
+            float dq[4][NJ] = {}, dkt[4][NJ] = {};
+            for (int c = 0; c < D; ++c) {
+                float orr[4], ur[4], sc[NJ], dc[NJ];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    orr[i] = ld(xo, 4 * tr + i, c);
+                    ur[i] = gU[(4 * tr + i) * D + c];
+                }
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    sc[j] = S[(int64_t)(tc + 16 * j) * D + c];
+                    dc[j] = dS[(int64_t)(tc + 16 * j) * D + c];
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) {
+                        dq[i][j] = fmaf(orr[i], sc[j], dq[i][j]);
+                        dkt[i][j] = fmaf(ur[i], dc[j], dkt[i][j]);
+                    }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int t = 4 * tr + i;
+                float qo = 0.f, rk = 0.f;
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    const int c = tc + 16 * j;
+                    dq[i][j] *= sg[t];
+                    qo = fmaf(ld(xq, t, c), dq[i][j], qo);
+                    rk = fmaf(dkt[i][j], ld(xk, t, c), rk);
+                    dk[i][j] = fmaf(se[t], dkt[i][j], dk[i][j]);
+                }
+                rowb[i] += qo - se[t] * rk;
+                tot63 += se[t] * rk;
+            }
+            for (int s2 = 0; s2 < C; ++s2) {
+                float pr[4], pc[4], ar[4], ac[4], kc[NJ], qc[NJ];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    pr[i] = sdP[(4 * tr + i) * LD6 + s2];
+                    pc[i] = sdP[s2 * LD6 + 4 * tr + i];
+                    ar[i] = sKK[(4 * tr + i) * LD6 + s2];
+                    ac[i] = sKK[s2 * LD6 + 4 * tr + i];
+                }
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    kc[j] = ld(xk, s2, tc + 16 * j);
+                    qc[j] = ld(xq, s2, tc + 16 * j);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ; ++j) {
+                        dq[i][j] = fmaf(pr[i], kc[j], dq[i][j]);
+                        dk[i][j] = fmaf(pc[i], qc[j], dk[i][j]);
+                        dk[i][j] = fmaf(ar[i] + ac[i], kc[j], dk[i][j]);
+                    }
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int t = 4 * tr + i;
+                T *dqp = (T *)a.dq + xo0 + (int64_t)t * a.sx_l;
+                T *dkp = (T *)a.dk + xo0 + (int64_t)t * a.sx_l;
+#pragma unroll
+                for (int j = 0; j < NJ; ++j) {
+                    dqp[tc + 16 * j] = cvt<T>(dq[i][j]);
+                    dkp[tc + 16 * j] = cvt<T>(dk[i][j]);
+                }
+            }
+        }
+        // gamma_C <dS', S> for b_C
+        {
+            float sd = 0.f;
+            for (int e = tid; e < D * D; e += 256) sd = fmaf(dS[e], S[e], sd);
+            tot63 = fmaf(sg[C - 1], sd, tot63);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            rB[(4 * tr + i) * 17 + tc] = rowb[i];
+            rD[(4 * tr + i) * 17 + tc] = rowd[i];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) rC[(tc + 16 * j) * 17 + tr] = colb[j];
+        r63[tid] = tot63;
+        __syncthreads();
+        if (tid < C) {
+            float db = 0.f, dbe = 0.f;
+            for (int u = 0; u < 16; ++u) {
+                db += rB[tid * 17 + u] + rC[tid * 17 + u];
+                dbe += rD[tid * 17 + u];
+            }
+            if (tid == C - 1)
+                for (int u = 0; u < 256; ++u) db += r63[u];
+            sb[tid] = db;  // b no longer needed
+            a.dbeta[go0 + (int64_t)tid * a.sg_l] = dbe;
+        }
+        __syncthreads();
+        if (tid == 0) {  // dg_i = sum_{t >= i} db_t
+            float acc = 0.f;
+            for (int t = C - 1; t >= 0; --t) {
+                acc += sb[t];
+                a.dg[go0 + (int64_t)t * a.sg_l] = acc;
+            }
+        }
+    }
+}
+
 template <int D>
 hipError_t gdn_fwd_d(const GdnArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     const unsigned bh = (unsigned)(a.B * a.H);
     if (a.n_super > 1) {
-        hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, true>), dim3(bh * (a.n_super - 1)), dim3(64 * D / 16), 0, s,
+        hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, W_PREP>), dim3(bh * a.n_prep), dim3(64 * D / 16), 0, s,
                               e0, nullptr, 0, a);
         hipExtLaunchKernelGGL((k_gdn_scan<D>), dim3(bh * (D / 16)), dim3(256), 0, s, nullptr, nullptr, 0, a);
     }
-    hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, false>), dim3(bh * a.n_super), dim3(64 * D / 16), 0, s,
+    hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, W_OUT>), dim3(bh * a.n_super), dim3(64 * D / 16), 0, s,
                           a.n_super > 1 ? nullptr : e0, e1, 0, a);
+    return hipGetLastError();
+}
+
+template <int D>
+hipError_t gdn_bwd_d(const GdnArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    const unsigned bh = (unsigned)(a.B * a.H);
+    const int64_t items = (int64_t)bh * (a.L / C);
+    if (a.n_super > 1) {
+        hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, W_PREP>), dim3(bh * a.n_prep), dim3(64 * D / 16), 0, s, e0,
+                              nullptr, 0, a);
+        hipExtLaunchKernelGGL((k_gdn_scan<D>), dim3(bh * (D / 16)), dim3(256), 0, s, nullptr, nullptr, 0, a);
+        hipExtLaunchKernelGGL((k_gdn_dwalk<__bf16, D, true>), dim3(bh * (a.n_super - 1)), dim3(64 * D / 16), 0, s,
+                              nullptr, nullptr, 0, a);
+        hipExtLaunchKernelGGL((k_gdn_dscan<D>), dim3(bh * (D / 16)), dim3(256), 0, s, nullptr, nullptr, 0, a);
+    }
+    hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, W_STORE>), dim3(bh * a.n_super), dim3(64 * D / 16), 0, s,
+                          a.n_super > 1 ? nullptr : e0, nullptr, 0, a);
+    hipExtLaunchKernelGGL((k_gdn_dwalk<__bf16, D, false>), dim3(bh * a.n_super), dim3(64 * D / 16), 0, s, nullptr,
+                          items > 0 ? nullptr : e1, 0, a);
+    if (items > 0)
+        hipExtLaunchKernelGGL((k_gdn_dchunk<__bf16, D>), dim3((unsigned)std::min<int64_t>(items, a.n_x)), dim3(256), 0,
+                              s, nullptr, e1, 0, a);
     return hipGetLastError();
 }
 
 }  // namespace
 
+hipError_t launch_gdn_bwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    if (a.n_super < 1 || !a.wsSc || !a.wsDc || !a.wsX || a.n_x < 1 ||
+        (a.n_super > 1 && (!a.wsS || !a.wsM || !a.wsN || !a.wsE || !a.wsDe || a.n_prep != a.n_super)))
+        return hipErrorInvalidValue;
+    if (D == 128) return gdn_bwd_d<128>(a, s, e0, e1);
+    if (D == 64) return gdn_bwd_d<64>(a, s, e0, e1);
+    return hipErrorInvalidValue;
+}
+
 hipError_t launch_gdn_fwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-    if (a.n_super < 1 || (a.n_super > 1 && (!a.wsS || !a.wsM || !a.wsN))) return hipErrorInvalidValue;
+    if (a.n_super < 1 || (a.n_super > 1 && (!a.wsS || !a.wsM || !a.wsN || a.n_prep < a.n_super - 1)))
+        return hipErrorInvalidValue;
     if (D == 128) return gdn_fwd_d<128>(a, s, e0, e1);
     if (D == 64) return gdn_fwd_d<64>(a, s, e0, e1);
     return hipErrorInvalidValue;

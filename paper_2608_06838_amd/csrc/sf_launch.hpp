@@ -63,20 +63,31 @@ struct ConvArgs {
 };
 int conv_channels_per_thread();
 
-// Gated delta rule forward (sf_gdn.hip).  n_super superchunks of ts tokens per
+// Gated delta rule (sf_gdn.hip).  n_super superchunks of ts tokens per
 // (batch, head); with n_super > 1 the workspace holds the boundary states
 // wsS [B*H][n_super][D][D] and the superchunk maps wsM, wsN
-// [B*H][n_super-1][D][D] (all fp32).
+// [B*H][n_prep][D][D] (all fp32; n_prep = n_super - 1 for the forward,
+// n_super for the backward, which also needs M of the last superchunk).
 struct GdnArgs {
     const void *q, *k, *v;
     const float *g, *beta, *S_in;
     void *o, *v_new;
     float *S_out;
-    float *wsS, *wsM, *wsN;
-    int32_t B, H, n_super, ts;
+    float *wsS, *wsM, *wsN;  // boundary states; superchunk maps (n_prep per head)
+    float *wsSc;             // backward: the state entering every chunk [B*H][L/64][D][D]
+    // backward
+    const void *dO;
+    const float *dS_out;
+    void *dq, *dk, *dv;
+    float *dg, *dbeta, *dS_in;
+    float *wsE, *wsDe;  // superchunk dS offsets E_J [B*H][n_super-1], dS_end(J) [B*H][n_super]
+    float *wsDc;        // dS' of every chunk [B*H][L/64][D][D]
+    float *wsX;         // per-chunk gradient kernel scratch: n_x slabs of 6 x 64 x D floats
+    int32_t B, H, n_super, ts, n_prep, n_x;
     int64_t L, sx_b, sx_l, sx_h, sg_b, sg_l, sg_h;
 };
 hipError_t launch_gdn_fwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+hipError_t launch_gdn_bwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_conv(bool bwd, const ConvArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 
 }  // namespace sf

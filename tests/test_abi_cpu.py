@@ -236,3 +236,34 @@ def test_gdn_validation():
     assert call(s, tun=_tuning(ts=256), ws=None) == _lib.SF_E_NULL
     assert call(s, tun=_tuning(ts=256), ws_bytes=need - 1) == _lib.SF_E_WORKSPACE
     assert call(s, tun=_tuning(ts=1024), ws=None, ws_bytes=0, S_out=1) == _lib.SF_E_ALIAS  # passes the workspace checks
+
+
+def test_gdn_bwd_validation():
+    L = _lib.lib()
+
+    def call(s, q=1, k=2, v=3, g=4, beta=5, S_in=None, dO=6, dS_out=None, dq=7, dk=8, dv=9, dg=10, dbeta=11,
+             dS_in=12, ws=13, ws_bytes=1 << 40, tun=None):
+        args = [p(i) if i is not None else None
+                for i in (q, k, v, g, beta, S_in, dO, dS_out, dq, dk, dv, dg, dbeta, dS_in, ws)]
+        return L.sf_gdn_bwd(ctypes.byref(s) if s is not None else None, *args, ws_bytes,
+                            ctypes.byref(tun) if tun is not None else None, None)
+
+    assert call(None) == _lib.SF_E_NULL
+    assert call(shape(io_dtype=_lib.SF_F32, Dk=64, Dv=64)) == _lib.SF_E_UNSUPPORTED
+    assert call(shape(gate=_lib.SF_GATE_VECTOR)) == _lib.SF_E_UNSUPPORTED
+    assert call(shape(L=100)) == _lib.SF_E_SHAPE
+    assert call(shape(), dO=None) == _lib.SF_E_NULL
+    assert call(shape(), dS_in=None) == _lib.SF_E_NULL
+    assert call(shape(), dbeta=None) == _lib.SF_E_NULL
+    assert call(shape(), dq=1) == _lib.SF_E_ALIAS       # dq over q
+    assert call(shape(), dk=6) == _lib.SF_E_ALIAS       # dk over dO
+    assert call(shape(), ws=7) == _lib.SF_E_ALIAS       # workspace over dq
+    assert call(shape(), ws=None) == _lib.SF_E_NULL
+    assert call(shape(), tun=_tuning(ts=96)) == _lib.SF_E_SHAPE
+    # workspace: states and state gradients of every chunk, the maps of every
+    # superchunk, E_J (all but the first) and dS_end(J), and the chunk kernel's slabs
+    s, n, nc, SS = shape(L=1024), 4, 16, 128 * 128 * 4
+    need = L.sf_gdn_bwd_workspace_bytes(ctypes.byref(s), ctypes.byref(_tuning(ts=256)))
+    slabs = min(2 * nc, 1024) * 6 * 64 * 128 * 4
+    assert need == 2 * SS * (4 * n + (n - 1)) + 2 * (2 * nc * SS) + slabs
+    assert call(s, tun=_tuning(ts=256), ws_bytes=need - 1) == _lib.SF_E_WORKSPACE

@@ -114,3 +114,74 @@ def test_gdn_long_segment_sampled():
     assert_close("o", to64(o[:, :, heads]), ro, "bf16")
     assert_close("S_out", to64(S[:, heads]), rS, "bf16")
     assert np.isfinite(to64(o)).all()
+
+
+# ------------------------------------------------------------------ backward
+def run_bwd(inp, dO, dS_out, ts=0):
+    g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
+    out = sf.gdn_bwd(g["q"], g["k"], g["v"], g["g"], g["beta"], g["S_in"], dO.to(DEV),
+                     None if dS_out is None else dS_out.to(DEV), ts=ts)
+    torch.cuda.synchronize()
+    return out
+
+
+def ref_bwd(inp, dO, dS_out, heads=None):
+    sel = (lambda x: x) if heads is None else (lambda x: x[:, :, heads])
+    S_in, dS = inp["S_in"], dS_out
+    if heads is not None:
+        S_in = None if S_in is None else S_in[:, heads]
+        dS = None if dS is None else dS[:, heads]
+    return gdn.backward(*(to64(sel(inp[x])) for x in ("q", "k", "v", "g", "beta")),
+                        None if S_in is None else to64(S_in), to64(sel(dO)), None if dS is None else to64(dS),
+                        threads=cores())
+
+
+def check_bwd(got, want):
+    for name, x, r in zip(("dq", "dk", "dv", "dg", "dbeta", "dS_in"), got, want):
+        assert_close(name, to64(x), r, "bf16")
+
+
+def grads_inputs(inp, seed):
+    gen = torch.Generator().manual_seed(seed)
+    B, L, H, D = inp["v"].shape
+    dO = torch.randn((B, L, H, D), generator=gen).to(torch.bfloat16)
+    dS = torch.randn((B, H, D, D), generator=gen) * 0.1
+    return dO, dS
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("ts", [0, 192, 448])
+def test_gdn_bwd_parity(D, ts):
+    """Every gradient against the oracle's hand-written backward; ts = 448 is
+    one superchunk, 192 leaves a ragged last one, 0 lets the library choose."""
+    B, L, H = 1, 448, 3
+    say(f"[gdn bwd] D={D} ts={ts}")
+    inp = synth.make_gdn_inputs(B, L, H, D, seed=4600 + D + ts)
+    dO, dS = grads_inputs(inp, 4700 + D + ts)
+    check_bwd(run_bwd(inp, dO, dS, ts), ref_bwd(inp, dO, dS))
+
+
+def test_gdn_bwd_no_state_and_empty():
+    say("[gdn bwd] no S_in, no dS_out; empty segment")
+    inp = synth.make_gdn_inputs(2, 192, 2, 128, seed=4800, s_in_std=0.0)
+    inp["S_in"] = None
+    dO, _ = grads_inputs(inp, 4801)
+    check_bwd(run_bwd(inp, dO, None), ref_bwd(inp, dO, None))
+    e = synth.make_gdn_inputs(1, 0, 2, 128, seed=4802)
+    dO, dS = grads_inputs(e, 4803)
+    out = run_bwd(e, dO, dS)
+    assert torch.equal(out[5].cpu(), dS)
+
+
+def test_gdn_bwd_long_segment_sampled():
+    """8192 tokens (128 chunks, several superchunks) over 8 heads; the oracle
+    runs two of them."""
+    B, L, H, D = 1, 8192, 8, 128
+    say(f"[gdn bwd] long segment L={L} H={H}")
+    inp = synth.make_gdn_inputs(B, L, H, D, seed=4900)
+    dO, dS = grads_inputs(inp, 4901)
+    got = run_bwd(inp, dO, dS)
+    heads = [1, 6]
+    want = ref_bwd(inp, dO, dS, heads)
+    sub = [x[:, :, heads] for x in got[:5]] + [got[5][:, heads]]
+    check_bwd(sub, want)
