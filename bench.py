@@ -328,12 +328,14 @@ def study_main(args):
     print(json.dumps(out), flush=True)
 
 
-GDN_METRIC = "gated-delta-rule fwd tokens/s per layer (H=40,d=128, 256K ctx, 8 segments chained through S)"
+GDN_METRIC = "gated-delta-rule training-step (fwd+bwd) tokens/s per layer (H=40, d=128, 256K ctx, 8 segments chained through S)"
 
 
 def bench_gdn(args):
     """One step = the gated-delta-rule forward over the 8 segments of the
-    256K-context layer, the state carried from segment to segment."""
+    256K-context layer, the state carried from segment to segment, then the
+    backward over the segments in reverse, the state gradient carried back
+    (random bf16 dO, no loss term on the final state)."""
     import torch
     import paper_2608_06838_amd as sf
     from paper_2608_06838_amd import synth
@@ -343,53 +345,75 @@ def bench_gdn(args):
     B, H, D, L = w["B"], w["H"], w["D"], sum(seg)
     dev = torch.device("cuda:0")
     inp = synth.make_gdn_inputs(B, L, H, D, device=dev, seed=4002)
+    gen = torch.Generator(device=dev).manual_seed(4003)
+    dO = torch.randn((B, L, H, D), device=dev, generator=gen).to(torch.bfloat16)
     starts = [sum(seg[:i]) for i in range(len(seg))]
+    sl = lambda x, t, n: x[:, t:t + n]
 
     def step():
-        S = inp["S_in"]
+        S, bounds = inp["S_in"], []
         for t, n in zip(starts, seg):
-            _, S = sf.gdn_fwd(inp["q"][:, t:t + n], inp["k"][:, t:t + n], inp["v"][:, t:t + n],
-                              inp["g"][:, t:t + n], inp["beta"][:, t:t + n], S, ts=args.gdn_ts)
+            bounds.append(S)
+            _, S = sf.gdn_fwd(sl(inp["q"], t, n), sl(inp["k"], t, n), sl(inp["v"], t, n), sl(inp["g"], t, n),
+                              sl(inp["beta"], t, n), S, ts=args.gdn_ts)
+        dS = None
+        for t, n, S0 in reversed(list(zip(starts, seg, bounds))):
+            *_, dS = sf.gdn_bwd(sl(inp["q"], t, n), sl(inp["k"], t, n), sl(inp["v"], t, n), sl(inp["g"], t, n),
+                                sl(inp["beta"], t, n), S0, sl(dO, t, n), dS, ts=args.gdn_ts)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    sf.prof_read("gdn_fwd")
-    sf.prof_enable("gdn_fwd", True)
+    for kn in ("gdn_fwd", "gdn_bwd"):
+        sf.prof_read(kn)
+        sf.prof_enable(kn, True)
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    sf.prof_enable("gdn_fwd", False)
-    tot_ms, nl = sf.prof_read("gdn_fwd")
+    prof = {}
+    for kn in ("gdn_fwd", "gdn_bwd"):
+        sf.prof_enable(kn, False)
+        prof[kn] = sf.prof_read(kn)
     ms = (t1 - t0) * 1e3 / args.steps
     io = 2
-    per_tok_head = 4 * D * io + 8  # q, k, v in, o out; g and beta
-    avg_s = tot_ms / 1e3 / max(nl, 1)
-    achieved = per_tok_head * B * H * L * args.steps / max(nl, 1) / avg_s / 1e9
+    # algorithmic HBM bytes per (token, head): fwd q, k, v in, o out, g, beta;
+    # bwd q, k, v, dO in, dq, dk, dv out, g, beta in, dg, dbeta out
+    per_tok = {"gdn_fwd": 4 * D * io + 8, "gdn_bwd": 7 * D * io + 16}
+    calls = {}
+    for kn, (tot_ms, nl) in prof.items():
+        avg_s = tot_ms / 1e3 / max(nl, 1)
+        ach = per_tok[kn] * B * H * L * args.steps / max(nl, 1) / avg_s / 1e9
+        calls[kn] = {"ms_per_step": tot_ms / args.steps, "launches": nl, "avg_launch_us": avg_s * 1e6,
+                     "achieved_GBps": ach}
+    dom = max(calls, key=lambda kn: calls[kn]["ms_per_step"])
     out = {
         "metric": GDN_METRIC, "value": B * L / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "gdn_ctx256k_h40", "B": B, "H": H, "Dk": D, "Dv": D, "L": L, "segments": seg,
                    "ts": args.gdn_ts or "auto",
-                   "parallelism": "superchunks: [M|N] prep walk, fp32 state scan, output walk"},
-        "roofline": {"kernel": "gdn_fwd", "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM / 1e9,
-                     "unit": "GB/s", "frac": achieved * 1e9 / PEAK_HBM, "traffic": None, "launches": nl,
-                     "avg_launch_us": avg_s * 1e6, "us_per_chunk": avg_s * 1e6 * len(seg) / (L / 64)},
+                   "parallelism": "superchunks: [M|N] prep walk, fp32 state scan, output walk; backward: "
+                                  "state-gradient walk over superchunks, per-chunk gradients over all chunks"},
+        "calls": calls,
+        "roofline": {"kernel": dom, "bound": "hbm", "achieved": calls[dom]["achieved_GBps"], "peak": PEAK_HBM / 1e9,
+                     "unit": "GB/s", "frac": calls[dom]["achieved_GBps"] * 1e9 / PEAK_HBM, "traffic": None,
+                     "launches": calls[dom]["launches"], "avg_launch_us": calls[dom]["avg_launch_us"]},
     }
     if not args.no_cpu_baseline:
         from oracle import gdn as ogdn
         nh = min(H, len(os.sched_getaffinity(0)))
-        L_s = 2048
-        sl = {k: inp[k][:1, :L_s, :nh].detach().cpu().double().numpy() for k in ("q", "k", "v", "g", "beta")}
+        L_s = 1024
+        cs = {k: inp[k][:1, :L_s, :nh].detach().cpu().double().numpy() for k in ("q", "k", "v", "g", "beta")}
+        do = dO[:1, :L_s, :nh].detach().cpu().double().numpy()
         tc = time.perf_counter()
-        ogdn.forward(sl["q"], sl["k"], sl["v"], sl["g"], sl["beta"], None, threads=nh)
+        ogdn.forward(cs["q"], cs["k"], cs["v"], cs["g"], cs["beta"], None, threads=nh)
+        ogdn.backward(cs["q"], cs["k"], cs["v"], cs["g"], cs["beta"], None, do, None, threads=nh)
         tc = time.perf_counter() - tc
         out["cpu_baseline"] = {"value": nh * L_s / H / tc, "unit": "tokens/s", "cores": nh, "kind": "oracle",
-                               "sample": f"batch 0, heads 0..{nh - 1}, first {L_s} tokens, fwd fp64, {tc:.1f} s wall; "
-                                         f"value scaled to a {H}-head layer"}
+                               "sample": f"batch 0, heads 0..{nh - 1}, first {L_s} tokens, fwd + bwd fp64, "
+                                         f"{tc:.1f} s wall; value scaled to a {H}-head layer"}
     print(json.dumps(out), flush=True)
 
 

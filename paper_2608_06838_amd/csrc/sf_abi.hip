@@ -941,7 +941,7 @@ GdnBwdWs gdn_bwd_ws(const Shape &r, int ts) {
     take(w.Sc, std::max<size_t>(bh * nc * SS, 1));
     take(w.Dc, std::max<size_t>(bh * nc * SS, 1));
     w.n_x = (int)std::max<size_t>(1, std::min<size_t>(bh * nc, kGdnSlabs));
-    take(w.X, (size_t)w.n_x * 6 * 64 * r.D * 4);
+    take(w.X, (size_t)w.n_x * 8 * 64 * r.D * 4);
     w.total = off;
     return w;
 }

@@ -686,30 +686,90 @@ __global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
 }
 
 // Parameter gradients of one chunk per item (b, h, chunk), items in a
-// grid-stride loop, fp32 arithmetic throughout.  256 threads; thread
-// (tr, tc) = (tid / 16, tid % 16) owns rows 4tr .. 4tr+3 and columns
-// tc + 16j of every 64 x D and 64 x 64 product.  q, k, v, dO in LDS (bf16),
-// the 64 x 64 matrices in LDS (fp32), the 64 x D intermediates in a per-
-// workgroup scratch slab of wsX (L2 resident), S and dS' read from the stored
-// per-chunk states.
+// grid-stride loop.  Every product runs on MFMA: wave w owns rows
+// [16w, 16w+16) of each 64-row result (64 x D results in halves of 64
+// columns), operands enter as bf16 fragments, computed fp32 operands as hi/lo
+// pairs (three products, the lo x lo term dropped), q, k, v, dO exactly.
+// q, k, v, dO and the 64 x 64 matrices sit in LDS; the 64 x D intermediates
+// in a per-workgroup scratch slab of wsX (eight 64 x D fp32 matrices, L2
+// resident, addressed through one buffer resource); S and dS' come from the
+// stored per-chunk states.  The triangular inverse T = (I + A)^{-1} is a
+// per-column forward substitution in fp32.
 template <typename T, int D>
 __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
-    constexpr int LDX = D + 8, LD6 = C + 1, NJ = D / 16;
-    __shared__ __attribute__((aligned(16))) T xq[C * LDX], xk[C * LDX], xv[C * LDX], xo[C * LDX];
-    __shared__ float sKK[C * LD6];  // e^{b_t-b_s} k_t.k_s, s < t (later Ah)
-    __shared__ float sT[C * LD6];   // (I + A)^{-1}
-    __shared__ float sPt[C * LD6];  // e^{b_t-b_s} q_t.k_s, s <= t
-    __shared__ float sdP[C * LD6];  // (dO U^T o Gamma)[t][s], s <= t
-    __shared__ float sb[C], sg[C], se[C], sbe[C];
-    __shared__ float rB[C * 17], rD[C * 17], rC[C * 17], r63[256];
+    constexpr int LDX = D + 8, LD6 = C + 4, NH = D / 64;
+    __shared__ __attribute__((aligned(16))) T xq[C * LDX], xk[C * LDX], xo[C * LDX], xv[C * LDX];
+    __shared__ __attribute__((aligned(16))) float sKK[C * LD6];  // e^{b_t-b_s} k_t.k_s, s < t (later Ah + Ah^T)
+    __shared__ __attribute__((aligned(16))) float sT[C * LD6];   // (I + A)^{-1}
+    __shared__ __attribute__((aligned(16))) float sPt[C * LD6];  // e^{b_t-b_s} q_t.k_s, s <= t
+    __shared__ __attribute__((aligned(16))) float sdP[C * LD6];  // (dO U^T o Gamma)[t][s], s <= t
+    __shared__ float sb[C], sg[C], se[C], sbe[C], sRb[C], sRd[C], sCol[4 * C], s63[4];
 
-    const int tid = threadIdx.x, tr = tid >> 4, tc = tid & 15;
+    const int tid = threadIdx.x, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), r0 = 16 * w;
     const int64_t SS = (int64_t)D * D, SX = (int64_t)C * D;
     const int nc = (int)(a.L / C);
     const int64_t items = (int64_t)a.B * a.H * nc;
-    float *X = a.wsX + (int64_t)blockIdx.x * 6 * SX;
-    float *gW = X, *gUb = X + SX, *gU = X + 2 * SX, *gdU = X + 3 * SX, *gGW = X + 4 * SX, *gGU = X + 5 * SX;
-    auto ld = [](const T *m, int r, int c) { return tof<T>(m[r * LDX + c]); };
+    const rsrc_t rX = buf_rsrc(a.wsX + (int64_t)blockIdx.x * 8 * SX, (uint32_t)(8 * SX * 4));
+    constexpr uint32_t MB = (uint32_t)(C * D * 4);  // bytes of one slab matrix
+    constexpr uint32_t mW = 0, mUb = MB, mU = 2 * MB, mdU = 3 * MB, mGW = 4 * MB, mGU = 5 * MB, mQ = 6 * MB, mK = 7 * MB;
+    // lane offsets: row-major fragment (row n16, k 8q4..), transposed fragment
+    // (k 8q4 + j, row n16), accumulator element (row 4q4 + r, column n16)
+    const uint32_t v_rm = (uint32_t)((n16 * D + 8 * q4) * 4), v_tr = (uint32_t)((8 * q4 * D + n16) * 4);
+    const uint32_t v_acc = (uint32_t)((4 * q4 * D + n16) * 4);
+
+    auto g_rm = [&](rsrc_t rs, uint32_t base, int rr, int kk, frag_t<T> &h, frag_t<T> &l) {
+        const uint32_t so = base + (uint32_t)((rr * D + kk) * 4);
+        const f32x4 x0 = buf_ld<f32x4>(rs, v_rm, so), x1 = buf_ld<f32x4>(rs, v_rm + 16, so);
+        const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+        split8<T, true>(x, h, l);
+    };
+    auto g_tr = [&](rsrc_t rs, uint32_t base, int rr, int kk, frag_t<T> &h, frag_t<T> &l) {
+        const uint32_t so = base + (uint32_t)((kk * D + rr) * 4);
+        float x[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = buf_ld<float>(rs, v_tr + j * D * 4, so);
+        split8<T, true>(x, h, l);
+    };
+    auto g_acc_ld = [&](rsrc_t rs, uint32_t base, int ct, f32x4 &c) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) c[r] = buf_ld<float>(rs, v_acc + r * D * 4, base + (uint32_t)((r0 * D + 16 * ct) * 4));
+    };
+    auto g_acc_st = [&](rsrc_t rs, uint32_t base, int ct, const f32x4 &c) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) buf_st<float>(rs, v_acc + r * D * 4, base + (uint32_t)((r0 * D + 16 * ct) * 4), c[r]);
+    };
+    auto l_rm = [&](const float *M, int rr, int kk, frag_t<T> &h, frag_t<T> &l) {  // LDS 64 x 64, M[row][k]
+        const float *p = M + (rr + n16) * LD6 + kk + 8 * q4;
+        const f32x4 x0 = *reinterpret_cast<const f32x4 *>(p), x1 = *reinterpret_cast<const f32x4 *>(p + 4);
+        const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+        split8<T, true>(x, h, l);
+    };
+    auto l_tr = [&](const float *M, int rr, int kk, frag_t<T> &h, frag_t<T> &l) {  // LDS 64 x 64, M[k][row]
+        float x[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = M[(kk + 8 * q4 + j) * LD6 + rr + n16];
+        split8<T, true>(x, h, l);
+    };
+    auto x_rm = [&](const T *M, int rr, int kk) {  // exact, M[row][k]
+        return *reinterpret_cast<const frag_t<T> *>(M + (rr + n16) * LDX + kk + 8 * q4);
+    };
+    auto x_tr = [&](const T *M, int rr, int kk) {  // exact, M[k][row]
+        frag_t<T> f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) f[j] = M[(kk + 8 * q4 + j) * LDX + rr + n16];
+        return f;
+    };
+    auto mma3 = [](f32x4 &c, const frag_t<T> &ah, const frag_t<T> &al, const frag_t<T> &bh, const frag_t<T> &bl) {
+        mma(c, ah, bh);
+        mma(c, ah, bl);
+        mma(c, al, bh);
+    };
+    auto zero4 = [](f32x4 (&c)[4]) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) c[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    };
+    // accumulator c[nt][r] <-> row r0 + 4 q4 + r, column 16 (4 hf + nt) + n16
 
     for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
         const int bh = (int)(it / nc), ch = (int)(it % nc), bb = bh / a.H, hh = bh % a.H;
@@ -717,17 +777,18 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
         const int64_t go0 = bb * a.sg_b + hh * a.sg_h + (int64_t)ch * C * a.sg_l;
         const float *S = a.wsSc + ((int64_t)bh * nc + ch) * SS;
         const float *dS = a.wsDc + ((int64_t)bh * nc + ch) * SS;
+        const rsrc_t rS = buf_rsrc(S, (uint32_t)(SS * 4)), rD = buf_rsrc(dS, (uint32_t)(SS * 4));
         __syncthreads();  // the previous item is done with LDS and the slab
         for (int e = tid; e < C * D / 8; e += 256) {
             const int t = e / (D / 8), c8 = 8 * (e % (D / 8));
             const int64_t off = xo0 + (int64_t)t * a.sx_l + c8;
             *reinterpret_cast<frag_t<T> *>(&xq[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.q + off);
             *reinterpret_cast<frag_t<T> *>(&xk[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.k + off);
-            *reinterpret_cast<frag_t<T> *>(&xv[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.v + off);
             *reinterpret_cast<frag_t<T> *>(&xo[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.dO + off);
+            *reinterpret_cast<frag_t<T> *>(&xv[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.v + off);
         }
         if (tid < 64) {
-            float b = wave_scan_dpp(a.g[go0 + (int64_t)tid * a.sg_l]);
+            const float b = wave_scan_dpp(a.g[go0 + (int64_t)tid * a.sg_l]);
             const float bC = lane_value(b, 63);
             sb[tid] = b;
             sg[tid] = expf(b);
@@ -738,34 +799,29 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
 
         float rowb[4] = {0.f, 0.f, 0.f, 0.f}, rowd[4] = {0.f, 0.f, 0.f, 0.f}, colb[4] = {0.f, 0.f, 0.f, 0.f};
         float tot63 = 0.f;
-        // scores (64 x 64, contraction over the D channels)
+        // scores: k_t.k_s and q_t.k_s
         {
-            float pk[4][4] = {}, pq[4][4] = {};
-            for (int c = 0; c < D; ++c) {
-                float kr[4], qr[4], kc[4];
+            f32x4 pk[4], pq[4];
+            zero4(pk);
+            zero4(pq);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    kr[i] = ld(xk, 4 * tr + i, c);
-                    qr[i] = ld(xq, 4 * tr + i, c);
+            for (int kk = 0; kk < D; kk += 32) {
+                const frag_t<T> ak = x_rm(xk, r0, kk), aq = x_rm(xq, r0, kk);
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt) {
+                    const frag_t<T> bk = x_rm(xk, 16 * nt, kk);
+                    mma(pk[nt], ak, bk);
+                    mma(pq[nt], aq, bk);
                 }
-#pragma unroll
-                for (int j = 0; j < 4; ++j) kc[j] = ld(xk, tc + 16 * j, c);
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        pk[i][j] = fmaf(kr[i], kc[j], pk[i][j]);
-                        pq[i][j] = fmaf(qr[i], kc[j], pq[i][j]);
-                    }
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int t = 4 * tr + i, s = tc + 16 * j;
-                    const float ga = expf(sb[t] - sb[s]);
-                    sKK[t * LD6 + s] = s < t ? ga * pk[i][j] : 0.f;
-                    sPt[t * LD6 + s] = s <= t ? ga * pq[i][j] : 0.f;
+                for (int r = 0; r < 4; ++r) {
+                    const int t = r0 + 4 * q4 + r, s2 = 16 * nt + n16;
+                    const float ga = expf(sb[t] - sb[s2]);
+                    sKK[t * LD6 + s2] = s2 < t ? ga * pk[nt][r] : 0.f;
+                    sPt[t * LD6 + s2] = s2 <= t ? ga * pq[nt][r] : 0.f;
                 }
         }
         __syncthreads();
@@ -784,304 +840,354 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
         }
         __syncthreads();
         // W = T diag(beta gamma) K, Ubar = T diag(beta) V
-        {
-            float w[4][NJ] = {}, u[4][NJ] = {};
-            for (int s2 = 0; s2 < C; ++s2) {
-                float tv[4], kc[NJ], vc[NJ];
+#pragma unroll 1
+        for (int hf = 0; hf < NH; ++hf) {
+            f32x4 cw[4], cu[4];
+            zero4(cw);
+            zero4(cu);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) tv[i] = sT[(4 * tr + i) * LD6 + s2];
-                const float fw = sbe[s2] * sg[s2], fv = sbe[s2];
+            for (int kk = 0; kk < C; kk += 32) {
+                frag_t<T> th, tl;
+                l_rm(sT, r0, kk, th, tl);
 #pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    kc[j] = fw * ld(xk, s2, tc + 16 * j);
-                    vc[j] = fv * ld(xv, s2, tc + 16 * j);
-                }
+                for (int nt = 0; nt < 4; ++nt) {
+                    const int col = 16 * (4 * hf + nt) + n16;
+                    float xw[8], xu[8];
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < NJ; ++j) {
-                        w[i][j] = fmaf(tv[i], kc[j], w[i][j]);
-                        u[i][j] = fmaf(tv[i], vc[j], u[i][j]);
+                    for (int j = 0; j < 8; ++j) {
+                        const int s2 = kk + 8 * q4 + j;
+                        xw[j] = sbe[s2] * sg[s2] * tof<T>(xk[s2 * LDX + col]);
+                        xu[j] = sbe[s2] * tof<T>(xv[s2 * LDX + col]);
                     }
+                    frag_t<T> bh, bl;
+                    split8<T, true>(xw, bh, bl);
+                    mma3(cw[nt], th, tl, bh, bl);
+                    split8<T, true>(xu, bh, bl);
+                    mma3(cu[nt], th, tl, bh, bl);
+                }
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    gW[(4 * tr + i) * D + tc + 16 * j] = w[i][j];
-                    gUb[(4 * tr + i) * D + tc + 16 * j] = u[i][j];
-                }
+            for (int nt = 0; nt < 4; ++nt) {
+                g_acc_st(rX, mW, 4 * hf + nt, cw[nt]);
+                g_acc_st(rX, mUb, 4 * hf + nt, cu[nt]);
+            }
         }
         __syncthreads();
         // U = Ubar - W S;  dU = diag(e^{b_C - b}) K dS' + P^T dO
+#pragma unroll 1
+        for (int hf = 0; hf < NH; ++hf) {
+            f32x4 cu[4], cd[4];
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) g_acc_ld(rX, mUb, 4 * hf + nt, cu[nt]);
+            zero4(cd);
+#pragma unroll 1
+            for (int kk = 0; kk < D; kk += 32) {
+                frag_t<T> wh, wl;
+                g_rm(rX, mW, r0, kk, wh, wl);
+                wh = -wh;
+                wl = -wl;
+                const frag_t<T> ak = x_rm(xk, r0, kk);
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt) {
+                    frag_t<T> sh, sl;
+                    g_tr(rS, 0, 16 * (4 * hf + nt), kk, sh, sl);
+                    mma3(cu[nt], wh, wl, sh, sl);
+                    g_tr(rD, 0, 16 * (4 * hf + nt), kk, sh, sl);
+                    mma(cd[nt], ak, sh);
+                    mma(cd[nt], ak, sl);
+                }
+            }
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) cd[nt][r] *= se[r0 + 4 * q4 + r];
+#pragma unroll
+            for (int kk = 0; kk < C; kk += 32) {
+                frag_t<T> ph, pl;
+                l_tr(sPt, r0, kk, ph, pl);  // P^T[t][t'] = P[t'][t]
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt) {
+                    const frag_t<T> bo = x_tr(xo, 16 * (4 * hf + nt), kk);
+                    mma(cd[nt], ph, bo);
+                    mma(cd[nt], pl, bo);
+                }
+            }
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) {
+                g_acc_st(rX, mU, 4 * hf + nt, cu[nt]);
+                g_acc_st(rX, mdU, 4 * hf + nt, cd[nt]);
+            }
+        }
+        __syncthreads();
+        // G_U = T^T dU (dv, dbeta)
+#pragma unroll 1
+        for (int hf = 0; hf < NH; ++hf) {
+            f32x4 cg[4];
+            zero4(cg);
+#pragma unroll
+            for (int kk = 0; kk < C; kk += 32) {
+                frag_t<T> th, tl;
+                l_tr(sT, r0, kk, th, tl);
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt) {
+                    frag_t<T> bh, bl;
+                    g_tr(rX, mdU, 16 * (4 * hf + nt), kk, bh, bl);
+                    mma3(cg[nt], th, tl, bh, bl);
+                }
+            }
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) {
+                g_acc_st(rX, mGU, 4 * hf + nt, cg[nt]);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = r0 + 4 * q4 + r, c = 16 * (4 * hf + nt) + n16;
+                    ((T *)a.dv)[xo0 + (int64_t)t * a.sx_l + c] = cvt<T>(sbe[t] * cg[nt][r]);
+                    rowd[r] = fmaf(cg[nt][r], tof<T>(xv[t * LDX + c]), rowd[r]);
+                }
+            }
+        }
+        // dW = -dU S^T and diag(gamma) dO S^T
+#pragma unroll 1
+        for (int hf = 0; hf < NH; ++hf) {
+            f32x4 cw[4], cq[4];
+            zero4(cw);
+            zero4(cq);
+#pragma unroll 1
+            for (int kk = 0; kk < D; kk += 32) {
+                frag_t<T> uh, ul;
+                g_rm(rX, mdU, r0, kk, uh, ul);
+                uh = -uh;
+                ul = -ul;
+                const frag_t<T> ao = x_rm(xo, r0, kk);
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt) {
+                    frag_t<T> sh, sl;
+                    g_rm(rS, 0, 16 * (4 * hf + nt), kk, sh, sl);  // B[k'][v] = S[k'][v]
+                    mma3(cw[nt], uh, ul, sh, sl);
+                    mma(cq[nt], ao, sh);
+                    mma(cq[nt], ao, sl);
+                }
+            }
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = r0 + 4 * q4 + r, c = 16 * (4 * hf + nt) + n16;
+                    cq[nt][r] *= sg[t];
+                    rowb[r] = fmaf(tof<T>(xq[t * LDX + c]), cq[nt][r], rowb[r]);
+                }
+                g_acc_st(rX, mGW, 4 * hf + nt, cw[nt]);
+                g_acc_st(rX, mQ, 4 * hf + nt, cq[nt]);
+            }
+        }
+        __syncthreads();
+        // G_W = T^T dW, held until every wave has read dW; dk starts as diag(beta gamma) G_W
         {
-            float u[4][NJ], du[4][NJ] = {};
+            f32x4 cg[NH][4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int hf = 0; hf < NH; ++hf) {
+                zero4(cg[hf]);
 #pragma unroll
-                for (int j = 0; j < NJ; ++j) u[i][j] = gUb[(4 * tr + i) * D + tc + 16 * j];
-            for (int c = 0; c < D; ++c) {
-                float wr[4], kr[4], sc[NJ], dc[NJ];
+                for (int kk = 0; kk < C; kk += 32) {
+                    frag_t<T> th, tl;
+                    l_tr(sT, r0, kk, th, tl);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    wr[i] = gW[(4 * tr + i) * D + c];
-                    kr[i] = ld(xk, 4 * tr + i, c);
-                }
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    sc[j] = S[(int64_t)c * D + tc + 16 * j];
-                    dc[j] = dS[(int64_t)c * D + tc + 16 * j];
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < NJ; ++j) {
-                        u[i][j] = fmaf(-wr[i], sc[j], u[i][j]);
-                        du[i][j] = fmaf(kr[i], dc[j], du[i][j]);
+                    for (int nt = 0; nt < 4; ++nt) {
+                        frag_t<T> bh, bl;
+                        g_tr(rX, mGW, 16 * (4 * hf + nt), kk, bh, bl);
+                        mma3(cg[hf][nt], th, tl, bh, bl);
                     }
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) du[i][j] *= se[4 * tr + i];
-            for (int t2 = 0; t2 < C; ++t2) {
-                float pr[4], oc[NJ];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) pr[i] = sPt[t2 * LD6 + 4 * tr + i];
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) oc[j] = ld(xo, t2, tc + 16 * j);
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < NJ; ++j) du[i][j] = fmaf(pr[i], oc[j], du[i][j]);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    gU[(4 * tr + i) * D + tc + 16 * j] = u[i][j];
-                    gdU[(4 * tr + i) * D + tc + 16 * j] = du[i][j];
                 }
-        }
-        __syncthreads();
-        // G_U = T^T dU (dv, dbeta);  dW = -dU S^T (to gGW)
-        {
-            float gu[4][NJ] = {}, dw[4][NJ] = {};
-            for (int t2 = 0; t2 < C; ++t2) {
-                float tr4[4], dc[NJ];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) tr4[i] = sT[t2 * LD6 + 4 * tr + i];
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) dc[j] = gdU[t2 * D + tc + 16 * j];
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < NJ; ++j) gu[i][j] = fmaf(tr4[i], dc[j], gu[i][j]);
-            }
-            for (int c = 0; c < D; ++c) {
-                float dr[4], sc[NJ];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) dr[i] = gdU[(4 * tr + i) * D + c];
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) sc[j] = S[(int64_t)(tc + 16 * j) * D + c];
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < NJ; ++j) dw[i][j] = fmaf(-dr[i], sc[j], dw[i][j]);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int t = 4 * tr + i;
-                T *dv = (T *)a.dv + xo0 + (int64_t)t * a.sx_l;
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    const int c = tc + 16 * j;
-                    gGU[t * D + c] = gu[i][j];
-                    gGW[t * D + c] = dw[i][j];
-                    dv[c] = cvt<T>(sbe[t] * gu[i][j]);
-                    rowd[i] = fmaf(gu[i][j], ld(xv, t, c), rowd[i]);
-                }
-            }
-        }
-        __syncthreads();
-        // G_W = T^T dW; dk starts as diag(beta gamma) G_W
-        float dk[4][NJ];
-        {
-            float gw[4][NJ] = {};
-            for (int t2 = 0; t2 < C; ++t2) {
-                float tr4[4], dc[NJ];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) tr4[i] = sT[t2 * LD6 + 4 * tr + i];
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) dc[j] = gGW[t2 * D + tc + 16 * j];
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < NJ; ++j) gw[i][j] = fmaf(tr4[i], dc[j], gw[i][j]);
             }
             __syncthreads();  // every read of dW is done
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int t = 4 * tr + i;
-                float kg = 0.f;
+            for (int hf = 0; hf < NH; ++hf)
 #pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    const int c = tc + 16 * j;
-                    gGW[t * D + c] = gw[i][j];
-                    dk[i][j] = sbe[t] * sg[t] * gw[i][j];
-                    kg = fmaf(gw[i][j], ld(xk, t, c), kg);
+                for (int nt = 0; nt < 4; ++nt) {
+                    f32x4 kg4;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int t = r0 + 4 * q4 + r, c = 16 * (4 * hf + nt) + n16;
+                        const float kg = cg[hf][nt][r] * tof<T>(xk[t * LDX + c]);
+                        rowd[r] = fmaf(sg[t], kg, rowd[r]);
+                        rowb[r] = fmaf(sbe[t] * sg[t], kg, rowb[r]);
+                        kg4[r] = sbe[t] * sg[t] * cg[hf][nt][r];
+                    }
+                    g_acc_st(rX, mGW, 4 * hf + nt, cg[hf][nt]);
+                    g_acc_st(rX, mK, 4 * hf + nt, kg4);
                 }
-                rowd[i] = fmaf(sg[t], kg, rowd[i]);
-                rowb[i] = fmaf(sbe[t] * sg[t], kg, rowb[i]);
-            }
         }
         __syncthreads();
         // dA = -(G_W W^T + G_U Ubar^T) on s < t;  dP = dO U^T on s <= t
         {
-            float da[4][4] = {}, dp[4][4] = {};
-            for (int c = 0; c < D; ++c) {
-                float gwr[4], gur[4], orr[4], wc[4], uc[4], ucur[4];
+            f32x4 ca[4], cp[4];
+            zero4(ca);
+            zero4(cp);
+#pragma unroll 1
+            for (int kk = 0; kk < D; kk += 32) {
+                frag_t<T> gh, gl, uh, ul;
+                g_rm(rX, mGW, r0, kk, gh, gl);
+                g_rm(rX, mGU, r0, kk, uh, ul);
+                gh = -gh;
+                gl = -gl;
+                uh = -uh;
+                ul = -ul;
+                const frag_t<T> ao = x_rm(xo, r0, kk);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    gwr[i] = gGW[(4 * tr + i) * D + c];
-                    gur[i] = gGU[(4 * tr + i) * D + c];
-                    orr[i] = ld(xo, 4 * tr + i, c);
+                for (int nt = 0; nt < 4; ++nt) {
+                    frag_t<T> bh, bl;
+                    g_rm(rX, mW, 16 * nt, kk, bh, bl);
+                    mma3(ca[nt], gh, gl, bh, bl);
+                    g_rm(rX, mUb, 16 * nt, kk, bh, bl);
+                    mma3(ca[nt], uh, ul, bh, bl);
+                    g_rm(rX, mU, 16 * nt, kk, bh, bl);
+                    mma(cp[nt], ao, bh);
+                    mma(cp[nt], ao, bl);
                 }
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int s2 = tc + 16 * j;
-                    wc[j] = gW[s2 * D + c];
-                    uc[j] = gUb[s2 * D + c];
-                    ucur[j] = gU[s2 * D + c];
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        da[i][j] = fmaf(-gwr[i], wc[j], da[i][j]);
-                        da[i][j] = fmaf(-gur[i], uc[j], da[i][j]);
-                        dp[i][j] = fmaf(orr[i], ucur[j], dp[i][j]);
-                    }
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int t = 4 * tr + i, s2 = tc + 16 * j;
+                for (int r = 0; r < 4; ++r) {
+                    const int t = r0 + 4 * q4 + r, s2 = 16 * nt + n16;
                     const float kk = sKK[t * LD6 + s2];  // 0 unless s < t
-                    const float dA = s2 < t ? da[i][j] : 0.f;
-                    rowd[i] = fmaf(dA, kk, rowd[i]);
+                    const float dA = s2 < t ? ca[nt][r] : 0.f;
+                    rowd[r] = fmaf(dA, kk, rowd[r]);
                     const float ea = dA * sbe[t] * kk;  // dA o A
-                    rowb[i] += ea;
-                    colb[j] -= ea;
                     const float pt = sPt[t * LD6 + s2];  // 0 unless s <= t
-                    const float ep = s2 <= t ? dp[i][j] * pt : 0.f;  // dP o P
-                    rowb[i] += ep;
-                    colb[j] -= ep;
+                    const float ep = s2 <= t ? cp[nt][r] * pt : 0.f;  // dP o P
+                    rowb[r] += ea + ep;
+                    colb[nt] -= ea + ep;
                     const float ga = s2 <= t ? expf(sb[t] - sb[s2]) : 0.f;
-                    sdP[t * LD6 + s2] = s2 <= t ? dp[i][j] * ga : 0.f;
-                    sKK[t * LD6 + s2] = dA * sbe[t] * ga;  // Ah
+                    sdP[t * LD6 + s2] = cp[nt][r] * ga;
+                    ca[nt][r] = dA * sbe[t] * ga;  // Ah
                 }
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) {  // column sums over this wave's rows
+                float v = colb[nt];
+                v += __shfl_xor(v, 16);
+                v += __shfl_xor(v, 32);
+                if (q4 == 0) sCol[w * C + 16 * nt + n16] = v;
+            }
+            __syncthreads();  // every read of the scores in sKK is done
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) sKK[(r0 + 4 * q4 + r) * LD6 + 16 * nt + n16] = ca[nt][r];
         }
         __syncthreads();
-        // dq = diag(gamma) dO S^T + dP K;  dk += diag(e^{b_C - b}) U dS'^T + dP^T Q + Ah K + Ah^T K
-        {
-            float dq[4][NJ] = {}, dkt[4][NJ] = {};
-            for (int c = 0; c < D; ++c) {
-                float orr[4], ur[4], sc[NJ], dc[NJ];
+        // symmetrise: sKK = Ah + Ah^T (Ah strictly lower)
+        for (int e = tid; e < C * C; e += 256) {
+            const int t = e / C, s2 = e % C;
+            if (s2 < t) sKK[s2 * LD6 + t] = sKK[t * LD6 + s2];
+            else if (s2 == t) sKK[t * LD6 + t] = 0.f;
+        }
+        __syncthreads();
+        // dq = diag(gamma) dO S^T + dP K
+#pragma unroll 1
+        for (int hf = 0; hf < NH; ++hf) {
+            f32x4 cq[4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    orr[i] = ld(xo, 4 * tr + i, c);
-                    ur[i] = gU[(4 * tr + i) * D + c];
-                }
+            for (int nt = 0; nt < 4; ++nt) g_acc_ld(rX, mQ, 4 * hf + nt, cq[nt]);
 #pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    sc[j] = S[(int64_t)(tc + 16 * j) * D + c];
-                    dc[j] = dS[(int64_t)(tc + 16 * j) * D + c];
-                }
+            for (int kk = 0; kk < C; kk += 32) {
+                frag_t<T> ph, pl;
+                l_rm(sdP, r0, kk, ph, pl);
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < NJ; ++j) {
-                        dq[i][j] = fmaf(orr[i], sc[j], dq[i][j]);
-                        dkt[i][j] = fmaf(ur[i], dc[j], dkt[i][j]);
-                    }
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int t = 4 * tr + i;
-                float qo = 0.f, rk = 0.f;
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    const int c = tc + 16 * j;
-                    dq[i][j] *= sg[t];
-                    qo = fmaf(ld(xq, t, c), dq[i][j], qo);
-                    rk = fmaf(dkt[i][j], ld(xk, t, c), rk);
-                    dk[i][j] = fmaf(se[t], dkt[i][j], dk[i][j]);
-                }
-                rowb[i] += qo - se[t] * rk;
-                tot63 += se[t] * rk;
-            }
-            for (int s2 = 0; s2 < C; ++s2) {
-                float pr[4], pc[4], ar[4], ac[4], kc[NJ], qc[NJ];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    pr[i] = sdP[(4 * tr + i) * LD6 + s2];
-                    pc[i] = sdP[s2 * LD6 + 4 * tr + i];
-                    ar[i] = sKK[(4 * tr + i) * LD6 + s2];
-                    ac[i] = sKK[s2 * LD6 + 4 * tr + i];
-                }
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    kc[j] = ld(xk, s2, tc + 16 * j);
-                    qc[j] = ld(xq, s2, tc + 16 * j);
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < NJ; ++j) {
-                        dq[i][j] = fmaf(pr[i], kc[j], dq[i][j]);
-                        dk[i][j] = fmaf(pc[i], qc[j], dk[i][j]);
-                        dk[i][j] = fmaf(ar[i] + ac[i], kc[j], dk[i][j]);
-                    }
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int t = 4 * tr + i;
-                T *dqp = (T *)a.dq + xo0 + (int64_t)t * a.sx_l;
-                T *dkp = (T *)a.dk + xo0 + (int64_t)t * a.sx_l;
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    dqp[tc + 16 * j] = cvt<T>(dq[i][j]);
-                    dkp[tc + 16 * j] = cvt<T>(dk[i][j]);
+                for (int nt = 0; nt < 4; ++nt) {
+                    const frag_t<T> bk = x_tr(xk, 16 * (4 * hf + nt), kk);  // B[k'][s] = K[s][k']
+                    mma(cq[nt], ph, bk);
+                    mma(cq[nt], pl, bk);
                 }
             }
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    ((T *)a.dq)[xo0 + (int64_t)(r0 + 4 * q4 + r) * a.sx_l + 16 * (4 * hf + nt) + n16] = cvt<T>(cq[nt][r]);
+        }
+        // dk = diag(beta gamma) G_W + diag(e^{b_C - b}) U dS'^T + dP^T Q + (Ah + Ah^T) K
+#pragma unroll 1
+        for (int hf = 0; hf < NH; ++hf) {
+            f32x4 ck[4];
+            zero4(ck);
+#pragma unroll 1
+            for (int kk = 0; kk < D; kk += 32) {
+                frag_t<T> uh, ul;
+                g_rm(rX, mU, r0, kk, uh, ul);
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt) {
+                    frag_t<T> bh, bl;
+                    g_rm(rD, 0, 16 * (4 * hf + nt), kk, bh, bl);  // B[k'][v] = dS'[k'][v]
+                    mma3(ck[nt], uh, ul, bh, bl);
+                }
+            }
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) {
+                f32x4 gk;
+                g_acc_ld(rX, mK, 4 * hf + nt, gk);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = r0 + 4 * q4 + r, c = 16 * (4 * hf + nt) + n16;
+                    const float rk = ck[nt][r] * tof<T>(xk[t * LDX + c]);
+                    rowb[r] -= se[t] * rk;
+                    tot63 += se[t] * rk;
+                    ck[nt][r] = fmaf(se[t], ck[nt][r], gk[r]);
+                }
+            }
+#pragma unroll
+            for (int kk = 0; kk < C; kk += 32) {
+                frag_t<T> ph, pl, ah, al;
+                l_tr(sdP, r0, kk, ph, pl);  // dP^T[t][t'] = dP[t'][t]
+                l_rm(sKK, r0, kk, ah, al);
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt) {
+                    const frag_t<T> bq = x_tr(xq, 16 * (4 * hf + nt), kk), bk = x_tr(xk, 16 * (4 * hf + nt), kk);
+                    mma(ck[nt], ph, bq);
+                    mma(ck[nt], pl, bq);
+                    mma(ck[nt], ah, bk);
+                    mma(ck[nt], al, bk);
+                }
+            }
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    ((T *)a.dk)[xo0 + (int64_t)(r0 + 4 * q4 + r) * a.sx_l + 16 * (4 * hf + nt) + n16] = cvt<T>(ck[nt][r]);
         }
         // gamma_C <dS', S> for b_C
         {
             float sd = 0.f;
-            for (int e = tid; e < D * D; e += 256) sd = fmaf(dS[e], S[e], sd);
+            for (int e = 4 * tid; e < D * D; e += 4 * 256) {
+                const f32x4 x = buf_ld<f32x4>(rD, (uint32_t)(e * 4), 0), y = buf_ld<f32x4>(rS, (uint32_t)(e * 4), 0);
+                sd = fmaf(x[0], y[0], fmaf(x[1], y[1], fmaf(x[2], y[2], fmaf(x[3], y[3], sd))));
+            }
             tot63 = fmaf(sg[C - 1], sd, tot63);
         }
+        // row sums over the 16 lanes of each row; tot63 over the workgroup
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            rB[(4 * tr + i) * 17 + tc] = rowb[i];
-            rD[(4 * tr + i) * 17 + tc] = rowd[i];
+        for (int r = 0; r < 4; ++r) {
+            float vb = rowb[r], vd = rowd[r];
+#pragma unroll
+            for (int m = 1; m < 16; m <<= 1) {
+                vb += __shfl_xor(vb, m);
+                vd += __shfl_xor(vd, m);
+            }
+            if (n16 == 0) {
+                sRb[r0 + 4 * q4 + r] = vb;
+                sRd[r0 + 4 * q4 + r] = vd;
+            }
         }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) rC[(tc + 16 * j) * 17 + tr] = colb[j];
-        r63[tid] = tot63;
+        for (int m = 1; m < 64; m <<= 1) tot63 += __shfl_xor(tot63, m);
+        if (lane == 0) s63[w] = tot63;
         __syncthreads();
         if (tid < C) {
-            float db = 0.f, dbe = 0.f;
-            for (int u = 0; u < 16; ++u) {
-                db += rB[tid * 17 + u] + rC[tid * 17 + u];
-                dbe += rD[tid * 17 + u];
-            }
-            if (tid == C - 1)
-                for (int u = 0; u < 256; ++u) db += r63[u];
+            float db = sRb[tid];
+            for (int u = 0; u < 4; ++u) db += sCol[u * C + tid];
+            if (tid == C - 1) db += s63[0] + s63[1] + s63[2] + s63[3];
             sb[tid] = db;  // b no longer needed
-            a.dbeta[go0 + (int64_t)tid * a.sg_l] = dbe;
+            a.dbeta[go0 + (int64_t)tid * a.sg_l] = sRd[tid];
         }
         __syncthreads();
         if (tid == 0) {  // dg_i = sum_{t >= i} db_t

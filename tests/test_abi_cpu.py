@@ -264,6 +264,6 @@ def test_gdn_bwd_validation():
     # superchunk, E_J (all but the first) and dS_end(J), and the chunk kernel's slabs
     s, n, nc, SS = shape(L=1024), 4, 16, 128 * 128 * 4
     need = L.sf_gdn_bwd_workspace_bytes(ctypes.byref(s), ctypes.byref(_tuning(ts=256)))
-    slabs = min(2 * nc, 1024) * 6 * 64 * 128 * 4
+    slabs = min(2 * nc, 1024) * 8 * 64 * 128 * 4
     assert need == 2 * SS * (4 * n + (n - 1)) + 2 * (2 * nc * SS) + slabs
     assert call(s, tun=_tuning(ts=256), ws_bytes=need - 1) == _lib.SF_E_WORKSPACE
