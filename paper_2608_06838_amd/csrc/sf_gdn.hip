@@ -686,9 +686,9 @@ __global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
 }
 
 // Parameter gradients of one chunk per item (b, h, chunk), items in a
-// grid-stride loop.  Every product runs on MFMA: wave w owns rows
-// [16w, 16w+16) of each 64-row result (64 x D results in halves of 64
-// columns), operands enter as bf16 fragments, computed fp32 operands as hi/lo
+// grid-stride loop.  Every product runs on MFMA: 8 waves, wave w owns rows
+// [16 (w % 4), +16) and half the column tiles (half w / 4) of each 64-row
+// result, so two waves share each SIMD.  Operands enter as bf16 fragments, computed fp32 operands as hi/lo
 // pairs (three products, the lo x lo term dropped), q, k, v, dO exactly.
 // q, k, v, dO and the 64 x 64 matrices sit in LDS; the 64 x D intermediates
 // in a per-workgroup scratch slab of wsX (eight 64 x D fp32 matrices, L2
@@ -696,17 +696,17 @@ __global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
 // stored per-chunk states.  The triangular inverse T = (I + A)^{-1} is a
 // per-column forward substitution in fp32.
 template <typename T, int D>
-__global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
-    constexpr int LDX = D + 8, LD6 = C + 4, NH = D / 64;
+__global__ void __launch_bounds__(512) k_gdn_dchunk(GdnArgs a) {
+    constexpr int LDX = D + 8, LD6 = C + 4, NT2 = D / 32, NTH = 512;
     __shared__ __attribute__((aligned(16))) T xq[C * LDX], xk[C * LDX], xo[C * LDX], xv[C * LDX];
     __shared__ __attribute__((aligned(16))) float sKK[C * LD6];  // e^{b_t-b_s} k_t.k_s, s < t (later Ah + Ah^T)
     __shared__ __attribute__((aligned(16))) float sT[C * LD6];   // (I + A)^{-1}
     __shared__ __attribute__((aligned(16))) float sPt[C * LD6];  // e^{b_t-b_s} q_t.k_s, s <= t
     __shared__ __attribute__((aligned(16))) float sdP[C * LD6];  // (dO U^T o Gamma)[t][s], s <= t
-    __shared__ float sb[C], sg[C], se[C], sbe[C], sRb[C], sRd[C], sCol[4 * C], s63[4];
+    __shared__ float sb[C], sg[C], se[C], sbe[C], sRb[2 * C], sRd[2 * C], sCol[4 * C], s63[8];
 
     const int tid = threadIdx.x, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), r0 = 16 * w;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), r0 = 16 * (w & 3), hf = w >> 2;
     const int64_t SS = (int64_t)D * D, SX = (int64_t)C * D;
     const int nc = (int)(a.L / C);
     const int64_t items = (int64_t)a.B * a.H * nc;
@@ -765,11 +765,16 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
         mma(c, ah, bl);
         mma(c, al, bh);
     };
-    auto zero4 = [](f32x4 (&c)[4]) {
+    auto zeroN = [](f32x4 (&c)[NT2]) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) c[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < NT2; ++i) c[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     };
-    // accumulator c[nt][r] <-> row r0 + 4 q4 + r, column 16 (4 hf + nt) + n16
+    auto zero2 = [](f32x4 (&c)[2]) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) c[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    };
+    // accumulator c[nt][r] <-> row r0 + 4 q4 + r, column 16 (hf NT2 + nt) + n16 (64 x D results)
+    // or 16 (2 hf + nt) + n16 (64 x 64 results)
 
     for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
         const int bh = (int)(it / nc), ch = (int)(it % nc), bb = bh / a.H, hh = bh % a.H;
@@ -779,7 +784,7 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
         const float *dS = a.wsDc + ((int64_t)bh * nc + ch) * SS;
         const rsrc_t rS = buf_rsrc(S, (uint32_t)(SS * 4)), rD = buf_rsrc(dS, (uint32_t)(SS * 4));
         __syncthreads();  // the previous item is done with LDS and the slab
-        for (int e = tid; e < C * D / 8; e += 256) {
+        for (int e = tid; e < C * D / 8; e += NTH) {
             const int t = e / (D / 8), c8 = 8 * (e % (D / 8));
             const int64_t off = xo0 + (int64_t)t * a.sx_l + c8;
             *reinterpret_cast<frag_t<T> *>(&xq[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.q + off);
@@ -801,24 +806,24 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
         float tot63 = 0.f;
         // scores: k_t.k_s and q_t.k_s
         {
-            f32x4 pk[4], pq[4];
-            zero4(pk);
-            zero4(pq);
+            f32x4 pk[2], pq[2];
+            zero2(pk);
+            zero2(pq);
 #pragma unroll
             for (int kk = 0; kk < D; kk += 32) {
                 const frag_t<T> ak = x_rm(xk, r0, kk), aq = x_rm(xq, r0, kk);
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
-                    const frag_t<T> bk = x_rm(xk, 16 * nt, kk);
+                for (int nt = 0; nt < 2; ++nt) {
+                    const frag_t<T> bk = x_rm(xk, 16 * (2 * hf + nt), kk);
                     mma(pk[nt], ak, bk);
                     mma(pq[nt], aq, bk);
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
+            for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int t = r0 + 4 * q4 + r, s2 = 16 * nt + n16;
+                    const int t = r0 + 4 * q4 + r, s2 = 16 * (2 * hf + nt) + n16;
                     const float ga = expf(sb[t] - sb[s2]);
                     sKK[t * LD6 + s2] = s2 < t ? ga * pk[nt][r] : 0.f;
                     sPt[t * LD6 + s2] = s2 <= t ? ga * pq[nt][r] : 0.f;
@@ -840,18 +845,17 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
         }
         __syncthreads();
         // W = T diag(beta gamma) K, Ubar = T diag(beta) V
-#pragma unroll 1
-        for (int hf = 0; hf < NH; ++hf) {
-            f32x4 cw[4], cu[4];
-            zero4(cw);
-            zero4(cu);
+        {
+            f32x4 cw[NT2], cu[NT2];
+            zeroN(cw);
+            zeroN(cu);
 #pragma unroll
             for (int kk = 0; kk < C; kk += 32) {
                 frag_t<T> th, tl;
                 l_rm(sT, r0, kk, th, tl);
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
-                    const int col = 16 * (4 * hf + nt) + n16;
+                for (int nt = 0; nt < NT2; ++nt) {
+                    const int col = 16 * (NT2 * hf + nt) + n16;
                     float xw[8], xu[8];
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
@@ -867,19 +871,18 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
-                g_acc_st(rX, mW, 4 * hf + nt, cw[nt]);
-                g_acc_st(rX, mUb, 4 * hf + nt, cu[nt]);
+            for (int nt = 0; nt < NT2; ++nt) {
+                g_acc_st(rX, mW, NT2 * hf + nt, cw[nt]);
+                g_acc_st(rX, mUb, NT2 * hf + nt, cu[nt]);
             }
         }
         __syncthreads();
         // U = Ubar - W S;  dU = diag(e^{b_C - b}) K dS' + P^T dO
-#pragma unroll 1
-        for (int hf = 0; hf < NH; ++hf) {
-            f32x4 cu[4], cd[4];
+        {
+            f32x4 cu[NT2], cd[NT2];
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) g_acc_ld(rX, mUb, 4 * hf + nt, cu[nt]);
-            zero4(cd);
+            for (int nt = 0; nt < NT2; ++nt) g_acc_ld(rX, mUb, NT2 * hf + nt, cu[nt]);
+            zeroN(cd);
 #pragma unroll 1
             for (int kk = 0; kk < D; kk += 32) {
                 frag_t<T> wh, wl;
@@ -888,17 +891,17 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
                 wl = -wl;
                 const frag_t<T> ak = x_rm(xk, r0, kk);
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
+                for (int nt = 0; nt < NT2; ++nt) {
                     frag_t<T> sh, sl;
-                    g_tr(rS, 0, 16 * (4 * hf + nt), kk, sh, sl);
+                    g_tr(rS, 0, 16 * (NT2 * hf + nt), kk, sh, sl);
                     mma3(cu[nt], wh, wl, sh, sl);
-                    g_tr(rD, 0, 16 * (4 * hf + nt), kk, sh, sl);
+                    g_tr(rD, 0, 16 * (NT2 * hf + nt), kk, sh, sl);
                     mma(cd[nt], ak, sh);
                     mma(cd[nt], ak, sl);
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
+            for (int nt = 0; nt < NT2; ++nt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) cd[nt][r] *= se[r0 + 4 * q4 + r];
 #pragma unroll
@@ -906,52 +909,50 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
                 frag_t<T> ph, pl;
                 l_tr(sPt, r0, kk, ph, pl);  // P^T[t][t'] = P[t'][t]
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
-                    const frag_t<T> bo = x_tr(xo, 16 * (4 * hf + nt), kk);
+                for (int nt = 0; nt < NT2; ++nt) {
+                    const frag_t<T> bo = x_tr(xo, 16 * (NT2 * hf + nt), kk);
                     mma(cd[nt], ph, bo);
                     mma(cd[nt], pl, bo);
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
-                g_acc_st(rX, mU, 4 * hf + nt, cu[nt]);
-                g_acc_st(rX, mdU, 4 * hf + nt, cd[nt]);
+            for (int nt = 0; nt < NT2; ++nt) {
+                g_acc_st(rX, mU, NT2 * hf + nt, cu[nt]);
+                g_acc_st(rX, mdU, NT2 * hf + nt, cd[nt]);
             }
         }
         __syncthreads();
         // G_U = T^T dU (dv, dbeta)
-#pragma unroll 1
-        for (int hf = 0; hf < NH; ++hf) {
-            f32x4 cg[4];
-            zero4(cg);
+        {
+            f32x4 cg[NT2];
+            zeroN(cg);
 #pragma unroll
             for (int kk = 0; kk < C; kk += 32) {
                 frag_t<T> th, tl;
                 l_tr(sT, r0, kk, th, tl);
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
+                for (int nt = 0; nt < NT2; ++nt) {
                     frag_t<T> bh, bl;
-                    g_tr(rX, mdU, 16 * (4 * hf + nt), kk, bh, bl);
+                    g_tr(rX, mdU, 16 * (NT2 * hf + nt), kk, bh, bl);
                     mma3(cg[nt], th, tl, bh, bl);
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
-                g_acc_st(rX, mGU, 4 * hf + nt, cg[nt]);
+            for (int nt = 0; nt < NT2; ++nt) {
+                g_acc_st(rX, mGU, NT2 * hf + nt, cg[nt]);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int t = r0 + 4 * q4 + r, c = 16 * (4 * hf + nt) + n16;
+                    const int t = r0 + 4 * q4 + r, c = 16 * (NT2 * hf + nt) + n16;
                     ((T *)a.dv)[xo0 + (int64_t)t * a.sx_l + c] = cvt<T>(sbe[t] * cg[nt][r]);
                     rowd[r] = fmaf(cg[nt][r], tof<T>(xv[t * LDX + c]), rowd[r]);
                 }
             }
         }
         // dW = -dU S^T and diag(gamma) dO S^T
-#pragma unroll 1
-        for (int hf = 0; hf < NH; ++hf) {
-            f32x4 cw[4], cq[4];
-            zero4(cw);
-            zero4(cq);
+        {
+            f32x4 cw[NT2], cq[NT2];
+            zeroN(cw);
+            zeroN(cq);
 #pragma unroll 1
             for (int kk = 0; kk < D; kk += 32) {
                 frag_t<T> uh, ul;
@@ -960,69 +961,64 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
                 ul = -ul;
                 const frag_t<T> ao = x_rm(xo, r0, kk);
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
+                for (int nt = 0; nt < NT2; ++nt) {
                     frag_t<T> sh, sl;
-                    g_rm(rS, 0, 16 * (4 * hf + nt), kk, sh, sl);  // B[k'][v] = S[k'][v]
+                    g_rm(rS, 0, 16 * (NT2 * hf + nt), kk, sh, sl);  // B[k'][v] = S[k'][v]
                     mma3(cw[nt], uh, ul, sh, sl);
                     mma(cq[nt], ao, sh);
                     mma(cq[nt], ao, sl);
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
+            for (int nt = 0; nt < NT2; ++nt) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int t = r0 + 4 * q4 + r, c = 16 * (4 * hf + nt) + n16;
+                    const int t = r0 + 4 * q4 + r, c = 16 * (NT2 * hf + nt) + n16;
                     cq[nt][r] *= sg[t];
                     rowb[r] = fmaf(tof<T>(xq[t * LDX + c]), cq[nt][r], rowb[r]);
                 }
-                g_acc_st(rX, mGW, 4 * hf + nt, cw[nt]);
-                g_acc_st(rX, mQ, 4 * hf + nt, cq[nt]);
+                g_acc_st(rX, mGW, NT2 * hf + nt, cw[nt]);
+                g_acc_st(rX, mQ, NT2 * hf + nt, cq[nt]);
             }
         }
         __syncthreads();
         // G_W = T^T dW, held until every wave has read dW; dk starts as diag(beta gamma) G_W
         {
-            f32x4 cg[NH][4];
+            f32x4 cg[NT2];
+            zeroN(cg);
 #pragma unroll
-            for (int hf = 0; hf < NH; ++hf) {
-                zero4(cg[hf]);
+            for (int kk = 0; kk < C; kk += 32) {
+                frag_t<T> th, tl;
+                l_tr(sT, r0, kk, th, tl);
 #pragma unroll
-                for (int kk = 0; kk < C; kk += 32) {
-                    frag_t<T> th, tl;
-                    l_tr(sT, r0, kk, th, tl);
-#pragma unroll
-                    for (int nt = 0; nt < 4; ++nt) {
-                        frag_t<T> bh, bl;
-                        g_tr(rX, mGW, 16 * (4 * hf + nt), kk, bh, bl);
-                        mma3(cg[hf][nt], th, tl, bh, bl);
-                    }
+                for (int nt = 0; nt < NT2; ++nt) {
+                    frag_t<T> bh, bl;
+                    g_tr(rX, mGW, 16 * (NT2 * hf + nt), kk, bh, bl);
+                    mma3(cg[nt], th, tl, bh, bl);
                 }
             }
             __syncthreads();  // every read of dW is done
 #pragma unroll
-            for (int hf = 0; hf < NH; ++hf)
+            for (int nt = 0; nt < NT2; ++nt) {
+                f32x4 kg4;
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
-                    f32x4 kg4;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int t = r0 + 4 * q4 + r, c = 16 * (4 * hf + nt) + n16;
-                        const float kg = cg[hf][nt][r] * tof<T>(xk[t * LDX + c]);
-                        rowd[r] = fmaf(sg[t], kg, rowd[r]);
-                        rowb[r] = fmaf(sbe[t] * sg[t], kg, rowb[r]);
-                        kg4[r] = sbe[t] * sg[t] * cg[hf][nt][r];
-                    }
-                    g_acc_st(rX, mGW, 4 * hf + nt, cg[hf][nt]);
-                    g_acc_st(rX, mK, 4 * hf + nt, kg4);
+                for (int r = 0; r < 4; ++r) {
+                    const int t = r0 + 4 * q4 + r, c = 16 * (NT2 * hf + nt) + n16;
+                    const float kg = cg[nt][r] * tof<T>(xk[t * LDX + c]);
+                    rowd[r] = fmaf(sg[t], kg, rowd[r]);
+                    rowb[r] = fmaf(sbe[t] * sg[t], kg, rowb[r]);
+                    kg4[r] = sbe[t] * sg[t] * cg[nt][r];
                 }
+                g_acc_st(rX, mGW, NT2 * hf + nt, cg[nt]);
+                g_acc_st(rX, mK, NT2 * hf + nt, kg4);
+            }
         }
         __syncthreads();
         // dA = -(G_W W^T + G_U Ubar^T) on s < t;  dP = dO U^T on s <= t
         {
-            f32x4 ca[4], cp[4];
-            zero4(ca);
-            zero4(cp);
+            f32x4 ca[2], cp[2];
+            zero2(ca);
+            zero2(cp);
 #pragma unroll 1
             for (int kk = 0; kk < D; kk += 32) {
                 frag_t<T> gh, gl, uh, ul;
@@ -1034,22 +1030,22 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
                 ul = -ul;
                 const frag_t<T> ao = x_rm(xo, r0, kk);
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
+                for (int nt = 0; nt < 2; ++nt) {
                     frag_t<T> bh, bl;
-                    g_rm(rX, mW, 16 * nt, kk, bh, bl);
+                    g_rm(rX, mW, 16 * (2 * hf + nt), kk, bh, bl);
                     mma3(ca[nt], gh, gl, bh, bl);
-                    g_rm(rX, mUb, 16 * nt, kk, bh, bl);
+                    g_rm(rX, mUb, 16 * (2 * hf + nt), kk, bh, bl);
                     mma3(ca[nt], uh, ul, bh, bl);
-                    g_rm(rX, mU, 16 * nt, kk, bh, bl);
+                    g_rm(rX, mU, 16 * (2 * hf + nt), kk, bh, bl);
                     mma(cp[nt], ao, bh);
                     mma(cp[nt], ao, bl);
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
+            for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int t = r0 + 4 * q4 + r, s2 = 16 * nt + n16;
+                    const int t = r0 + 4 * q4 + r, s2 = 16 * (2 * hf + nt) + n16;
                     const float kk = sKK[t * LD6 + s2];  // 0 unless s < t
                     const float dA = s2 < t ? ca[nt][r] : 0.f;
                     rowd[r] = fmaf(dA, kk, rowd[r]);
@@ -1063,72 +1059,70 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
                     ca[nt][r] = dA * sbe[t] * ga;  // Ah
                 }
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {  // column sums over this wave's rows
+            for (int nt = 0; nt < 2; ++nt) {  // column sums over this wave's rows
                 float v = colb[nt];
                 v += __shfl_xor(v, 16);
                 v += __shfl_xor(v, 32);
-                if (q4 == 0) sCol[w * C + 16 * nt + n16] = v;
+                if (q4 == 0) sCol[(w & 3) * C + 16 * (2 * hf + nt) + n16] = v;
             }
             __syncthreads();  // every read of the scores in sKK is done
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
+            for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) sKK[(r0 + 4 * q4 + r) * LD6 + 16 * nt + n16] = ca[nt][r];
+                for (int r = 0; r < 4; ++r) sKK[(r0 + 4 * q4 + r) * LD6 + 16 * (2 * hf + nt) + n16] = ca[nt][r];
         }
         __syncthreads();
         // symmetrise: sKK = Ah + Ah^T (Ah strictly lower)
-        for (int e = tid; e < C * C; e += 256) {
+        for (int e = tid; e < C * C; e += NTH) {
             const int t = e / C, s2 = e % C;
             if (s2 < t) sKK[s2 * LD6 + t] = sKK[t * LD6 + s2];
             else if (s2 == t) sKK[t * LD6 + t] = 0.f;
         }
         __syncthreads();
         // dq = diag(gamma) dO S^T + dP K
-#pragma unroll 1
-        for (int hf = 0; hf < NH; ++hf) {
-            f32x4 cq[4];
+        {
+            f32x4 cq[NT2];
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) g_acc_ld(rX, mQ, 4 * hf + nt, cq[nt]);
+            for (int nt = 0; nt < NT2; ++nt) g_acc_ld(rX, mQ, NT2 * hf + nt, cq[nt]);
 #pragma unroll
             for (int kk = 0; kk < C; kk += 32) {
                 frag_t<T> ph, pl;
                 l_rm(sdP, r0, kk, ph, pl);
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
-                    const frag_t<T> bk = x_tr(xk, 16 * (4 * hf + nt), kk);  // B[k'][s] = K[s][k']
+                for (int nt = 0; nt < NT2; ++nt) {
+                    const frag_t<T> bk = x_tr(xk, 16 * (NT2 * hf + nt), kk);  // B[k'][s] = K[s][k']
                     mma(cq[nt], ph, bk);
                     mma(cq[nt], pl, bk);
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
+            for (int nt = 0; nt < NT2; ++nt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    ((T *)a.dq)[xo0 + (int64_t)(r0 + 4 * q4 + r) * a.sx_l + 16 * (4 * hf + nt) + n16] = cvt<T>(cq[nt][r]);
+                    ((T *)a.dq)[xo0 + (int64_t)(r0 + 4 * q4 + r) * a.sx_l + 16 * (NT2 * hf + nt) + n16] = cvt<T>(cq[nt][r]);
         }
         // dk = diag(beta gamma) G_W + diag(e^{b_C - b}) U dS'^T + dP^T Q + (Ah + Ah^T) K
-#pragma unroll 1
-        for (int hf = 0; hf < NH; ++hf) {
-            f32x4 ck[4];
-            zero4(ck);
+        {
+            f32x4 ck[NT2];
+            zeroN(ck);
 #pragma unroll 1
             for (int kk = 0; kk < D; kk += 32) {
                 frag_t<T> uh, ul;
                 g_rm(rX, mU, r0, kk, uh, ul);
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
+                for (int nt = 0; nt < NT2; ++nt) {
                     frag_t<T> bh, bl;
-                    g_rm(rD, 0, 16 * (4 * hf + nt), kk, bh, bl);  // B[k'][v] = dS'[k'][v]
+                    g_rm(rD, 0, 16 * (NT2 * hf + nt), kk, bh, bl);  // B[k'][v] = dS'[k'][v]
                     mma3(ck[nt], uh, ul, bh, bl);
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
+            for (int nt = 0; nt < NT2; ++nt) {
                 f32x4 gk;
-                g_acc_ld(rX, mK, 4 * hf + nt, gk);
+                g_acc_ld(rX, mK, NT2 * hf + nt, gk);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int t = r0 + 4 * q4 + r, c = 16 * (4 * hf + nt) + n16;
+                    const int t = r0 + 4 * q4 + r, c = 16 * (NT2 * hf + nt) + n16;
                     const float rk = ck[nt][r] * tof<T>(xk[t * LDX + c]);
                     rowb[r] -= se[t] * rk;
                     tot63 += se[t] * rk;
@@ -1141,8 +1135,8 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
                 l_tr(sdP, r0, kk, ph, pl);  // dP^T[t][t'] = dP[t'][t]
                 l_rm(sKK, r0, kk, ah, al);
 #pragma unroll
-                for (int nt = 0; nt < 4; ++nt) {
-                    const frag_t<T> bq = x_tr(xq, 16 * (4 * hf + nt), kk), bk = x_tr(xk, 16 * (4 * hf + nt), kk);
+                for (int nt = 0; nt < NT2; ++nt) {
+                    const frag_t<T> bq = x_tr(xq, 16 * (NT2 * hf + nt), kk), bk = x_tr(xk, 16 * (NT2 * hf + nt), kk);
                     mma(ck[nt], ph, bq);
                     mma(ck[nt], pl, bq);
                     mma(ck[nt], ah, bk);
@@ -1150,15 +1144,15 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
+            for (int nt = 0; nt < NT2; ++nt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    ((T *)a.dk)[xo0 + (int64_t)(r0 + 4 * q4 + r) * a.sx_l + 16 * (4 * hf + nt) + n16] = cvt<T>(ck[nt][r]);
+                    ((T *)a.dk)[xo0 + (int64_t)(r0 + 4 * q4 + r) * a.sx_l + 16 * (NT2 * hf + nt) + n16] = cvt<T>(ck[nt][r]);
         }
         // gamma_C <dS', S> for b_C
         {
             float sd = 0.f;
-            for (int e = 4 * tid; e < D * D; e += 4 * 256) {
+            for (int e = 4 * tid; e < D * D; e += 4 * NTH) {
                 const f32x4 x = buf_ld<f32x4>(rD, (uint32_t)(e * 4), 0), y = buf_ld<f32x4>(rS, (uint32_t)(e * 4), 0);
                 sd = fmaf(x[0], y[0], fmaf(x[1], y[1], fmaf(x[2], y[2], fmaf(x[3], y[3], sd))));
             }
@@ -1174,8 +1168,8 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
                 vd += __shfl_xor(vd, m);
             }
             if (n16 == 0) {
-                sRb[r0 + 4 * q4 + r] = vb;
-                sRd[r0 + 4 * q4 + r] = vd;
+                sRb[hf * C + r0 + 4 * q4 + r] = vb;
+                sRd[hf * C + r0 + 4 * q4 + r] = vd;
             }
         }
 #pragma unroll
@@ -1183,11 +1177,12 @@ __global__ void __launch_bounds__(256) k_gdn_dchunk(GdnArgs a) {
         if (lane == 0) s63[w] = tot63;
         __syncthreads();
         if (tid < C) {
-            float db = sRb[tid];
+            float db = sRb[tid] + sRb[C + tid];
             for (int u = 0; u < 4; ++u) db += sCol[u * C + tid];
-            if (tid == C - 1) db += s63[0] + s63[1] + s63[2] + s63[3];
+            if (tid == C - 1)
+                for (int u = 0; u < 8; ++u) db += s63[u];
             sb[tid] = db;  // b no longer needed
-            a.dbeta[go0 + (int64_t)tid * a.sg_l] = sRd[tid];
+            a.dbeta[go0 + (int64_t)tid * a.sg_l] = sRd[tid] + sRd[C + tid];
         }
         __syncthreads();
         if (tid == 0) {  // dg_i = sum_{t >= i} db_t
@@ -1230,7 +1225,7 @@ hipError_t gdn_bwd_d(const GdnArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t 
     hipExtLaunchKernelGGL((k_gdn_dwalk<__bf16, D, false>), dim3(bh * a.n_super), dim3(64 * D / 16), 0, s, nullptr,
                           items > 0 ? nullptr : e1, 0, a);
     if (items > 0)
-        hipExtLaunchKernelGGL((k_gdn_dchunk<__bf16, D>), dim3((unsigned)std::min<int64_t>(items, a.n_x)), dim3(256), 0,
+        hipExtLaunchKernelGGL((k_gdn_dchunk<__bf16, D>), dim3((unsigned)std::min<int64_t>(items, a.n_x)), dim3(512), 0,
                               s, nullptr, e1, 0, a);
     return hipGetLastError();
 }
