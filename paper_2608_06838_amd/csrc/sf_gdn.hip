@@ -16,14 +16,15 @@
 // S_t = a_t S_{t-1} + k_t u_t^T is a plain gated linear recurrence in u, and
 // solving the within-chunk dependence of u on the earlier u's.
 //
-// One workgroup walks all chunks of one (batch, head) segment with the state in
-// registers: wave w owns the 16 state columns [16w, 16w+16) (D/16 waves).  Per
-// chunk: the q, k, v tiles are staged in LDS; the QK^T and KK^T scores run on
-// MFMA (10 causal 16x16 tiles each); the triangular system is solved in fp32,
-// one thread per right-hand-side column; U, the output and the state update are
-// MFMA products whose computed operands (S, W, U) go in as bf16 hi/lo pairs,
-// U straight from its accumulators (rows t, columns v), which two lane-row
-// swaps make into operand fragments with the tokens as contraction.
+// One workgroup walks the chunks of one (batch, head) superchunk with the state
+// in registers: wave w owns the 16 state columns [16w, 16w+16) (D/16 waves).
+// Per chunk: the q, k, v tiles are staged in LDS; the KK^T and QK^T scores run
+// on MFMA (10 causal 16x16 tiles each); T = (I + A)^{-1} is formed in fp32 by
+// 16 x 16 blocks (gdn_tinv) and [W | Ubar] = T R on MFMA (gdn_wu); U, the
+// output and the state update are MFMA products whose computed operands
+// (S, W, U) go in as bf16 hi/lo pairs, U straight from its accumulators (rows t,
+// columns v), which two lane-row swaps make into operand fragments with the
+// tokens as contraction.
 //
 // Superchunk parallelism (the Pre / ST / Out split of Sec. 2.2 with the delta
 // rule's matrix-valued transition): the chunk map S -> gamma_C S + K~^T (Ubar - W S)
@@ -43,52 +44,108 @@ namespace sf {
 
 namespace {
 
-// (I + A) X = R by forward substitution in fp32, one thread per column of
-// R = [diag(beta gamma) K | diag(beta) V] (threads [0, D) the W columns, [D, 2D)
-// the Ubar columns; nrhs = D solves for W only); X = [W | Ubar] goes to sW / sU,
-// whose column of this thread doubles as its working store.  Blocks of 16
-// rows: the earlier blocks' contribution is a 16 x 16 block update from LDS,
-// the diagonal block a 16-row triangular solve in registers (every register
-// index a compile-time constant).
-template <typename T, int D, int LDN, int LDA, int LDU, int SWX>
-__device__ __forceinline__ void gdn_solve(int tid, int nrhs, const T *sK, const T *sV, const float *sA,
-                                          const float *sbeta, const float *sq, float *sW, float *sU) {
-    if (tid >= nrhs) return;
-    const bool wcol = tid < D;
-    const int j = wcol ? tid : tid - D;
-    float *xc = (wcol ? sW : sU) + j;  // column j, row stride LDU
-    for (int tb = 0; tb < C / 16; ++tb) {
-        float xb[16];
+// T = (I + A)^{-1} for the strictly lower 64 x 64 A in sA (pitch C + 4), into
+// sT (fp32, pitch C + 4, zero above the diagonal), by 16 x 16 blocks: the four
+// diagonal blocks by forward substitution (64 threads, one column each), then
+// the off-diagonal blocks level by level, T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj
+// (i - j = 1, 2, 3), the inner sums parked in the free upper blocks.  All fp32.
+// NT >= 256 threads; ends with a barrier.
+template <int NT>
+__device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT) {
+    constexpr int LA = C + 4, LT = C + 4;
+    if (tid < 64) {
+        const int o = 16 * (tid >> 4), c = tid & 15;
+        float x[16];
 #pragma unroll
-        for (int tl = 0; tl < 16; ++tl) {
-            const int t = 16 * tb + tl;
-            xb[tl] = wcol ? tof<T>(sK[t * LDN + swz_col(t, j, SWX)]) * sbeta[t] * sq[t] : tof<T>(sV[t * LDN + j]) * sbeta[t];
+        for (int r = 0; r < 16; ++r) {
+            float acc = 0.f;
+#pragma unroll
+            for (int s2 = 0; s2 < r; ++s2) acc = fmaf(sA[(o + r) * LA + o + s2], x[s2], acc);
+            x[r] = r == c ? 1.f : (r > c ? -acc : 0.f);
         }
-        for (int sb = 0; sb < tb; ++sb) {
-            float xs[16];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) xs[e] = xc[(16 * sb + e) * LDU];
+        for (int r = 0; r < 16; ++r) sT[(o + r) * LT + o + c] = x[r];
+    }
+    __syncthreads();
 #pragma unroll
-            for (int tl = 0; tl < 16; ++tl) {
-                const float *ar = &sA[(16 * tb + tl) * LDA + 16 * sb];
+    for (int d = 1; d < 4; ++d) {
+        for (int e = tid; e < (4 - d) * 256; e += NT) {  // Y_ij, kept in block (j, i)
+            const int i = d + (e >> 8), j = i - d, rr = (e >> 4) & 15, cc = e & 15;
+            float y = 0.f;
+            for (int k = j; k < i; ++k)
 #pragma unroll
-                for (int e4 = 0; e4 < 4; ++e4) {
-                    const f32x4 av = *reinterpret_cast<const f32x4 *>(ar + 4 * e4);
+                for (int m = 0; m < 16; ++m)
+                    y = fmaf(sA[(16 * i + rr) * LA + 16 * k + m], sT[(16 * k + m) * LT + 16 * j + cc], y);
+            sT[(16 * j + rr) * LT + 16 * i + cc] = y;
+        }
+        __syncthreads();
+        for (int e = tid; e < (4 - d) * 256; e += NT) {  // T_ij = -T_ii Y_ij
+            const int i = d + (e >> 8), j = i - d, rr = (e >> 4) & 15, cc = e & 15;
+            float t = 0.f;
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) xb[tl] = fmaf(-av[u], xs[4 * e4 + u], xb[tl]);
-                }
+            for (int m = 0; m < 16; ++m)
+                t = fmaf(sT[(16 * i + rr) * LT + 16 * i + m], sT[(16 * j + m) * LT + 16 * i + cc], t);
+            sT[(16 * i + rr) * LT + 16 * j + cc] = -t;
+        }
+        __syncthreads();
+    }
+    for (int e = tid; e < 6 * 256; e += NT) {  // blocks (0,1) (0,2) (0,3) (1,2) (1,3) (2,3)
+        const int b = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
+        const int bi = b < 3 ? 0 : (b < 5 ? 1 : 2), bj = b < 3 ? b + 1 : (b < 5 ? b - 1 : 3);
+        sT[(16 * bi + rr) * LT + 16 * bj + cc] = 0.f;
+    }
+    __syncthreads();
+}
+
+// [W | Ubar] = T [diag(beta gamma) K | diag(beta) V] on MFMA: wave w forms
+// columns [16w, 16w+16) of W (and of Ubar when sU is given); T enters as a hi/lo
+// pair, the scaled K and V columns too (K, V exact in bf16 times an fp32
+// factor).  Results to sW / sU (fp32, pitch LDU).
+template <typename T, int D, int LDN, int LDU, int SWX>
+__device__ __forceinline__ void gdn_wu(int w, int lane, const LaneOff &tro, const float *sT, const T *sK, const T *sV,
+                                       const float *sbeta, const float *sq, float *sW, float *sU) {
+    constexpr int LT = C + 4;
+    const int q4 = lane >> 4, n16 = lane & 15, c0 = 16 * w;
+    f32x4 cw[4], cu[4];
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) cw[tt] = cu[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < C / 32; ++ks) {
+        float fw[8], fu[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int s2 = 32 * ks + 8 * q4 + j;
+            fu[j] = sbeta[s2];
+            fw[j] = sbeta[s2] * sq[s2];
+        }
+        frag_t<T> kh, kl, vh, vl;
+        split_scaled<T, true>(ldfragTR<T, LDN, SWX>(sK, tro, 32 * ks, c0), fw, kh, kl);
+        if (sU) split_scaled<T, true>(ldfragTR<T, LDN, SWX>(sV, tro, 32 * ks, c0), fu, vh, vl);
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) {
+            if (32 * ks > 16 * tt + 15) continue;  // T is lower triangular
+            const float *p = sT + (16 * tt + n16) * LT + 32 * ks + 8 * q4;
+            const f32x4 x0 = *reinterpret_cast<const f32x4 *>(p), x1 = *reinterpret_cast<const f32x4 *>(p + 4);
+            const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+            frag_t<T> th, tl;
+            split8<T, true>(x, th, tl);
+            mma(cw[tt], th, kh);
+            mma(cw[tt], th, kl);
+            mma(cw[tt], tl, kh);
+            if (sU) {
+                mma(cu[tt], th, vh);
+                mma(cu[tt], th, vl);
+                mma(cu[tt], tl, vh);
             }
         }
-#pragma unroll
-        for (int tl = 1; tl < 16; ++tl) {
-            const float *ar = &sA[(16 * tb + tl) * LDA + 16 * tb];
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                if (e < tl) xb[tl] = fmaf(-ar[e], xb[e], xb[tl]);
-        }
-#pragma unroll
-        for (int tl = 0; tl < 16; ++tl) xc[(16 * tb + tl) * LDU] = xb[tl];
     }
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            sW[(16 * tt + 4 * q4 + r) * LDU + c0 + n16] = cw[tt][r];
+            if (sU) sU[(16 * tt + 4 * q4 + r) * LDU + c0 + n16] = cu[tt][r];
+        }
 }
 
 enum { W_OUT = 0, W_PREP = 1, W_STORE = 2 };
@@ -102,8 +159,12 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
     __shared__ __attribute__((aligned(16))) T sQ[OUTP ? C * LDN : 8];    // plain
     __shared__ __attribute__((aligned(16))) T sK[C * LDN];               // plain, swizzled
     __shared__ __attribute__((aligned(16))) T sV[C * LDN];               // plain
-    __shared__ __attribute__((aligned(16))) T sP[OUTP ? C * LDT : 8];    // (Q K^T o Gamma)[t][s] hi
-    __shared__ __attribute__((aligned(16))) T sPl[OUTP ? C * LDT : 8];   // lo
+    // (Q K^T o Gamma)[t][s] hi, then lo; T = (I + A)^{-1} lives here before the P tiles
+    __shared__ __attribute__((aligned(16))) T sPP[OUTP ? 2 * C * LDT : 8];
+    __shared__ __attribute__((aligned(16))) float sTx[OUTP ? 4 : C * (C + 4)];
+    static_assert(!OUTP || 2 * C * LDT * sizeof(T) >= C * (C + 4) * sizeof(float), "T does not fit the P tiles");
+    T *sP = sPP, *sPl = sPP + (OUTP ? C * LDT : 0);
+    float *sT = OUTP ? reinterpret_cast<float *>(sPP) : sTx;
     __shared__ __attribute__((aligned(16))) float sA[C * LDA];    // beta_t e^{b_t-b_s} k_t.k_s, s < t
     __shared__ __attribute__((aligned(16))) float sW[C * LDU];    // W [t][k], fp32
     __shared__ __attribute__((aligned(16))) float sU[C * LDU];    // Ubar [t][v], fp32
@@ -182,7 +243,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         __syncthreads();  // the previous chunk is done with every LDS tile
         if constexpr (OUTP) t1.store_swz(sQ, LDN, tid, 0);
         t2.store_swz(sK, LDN, tid, SWX);
-        t3.store_swz(sV, LDN, tid, 0);
+        t3.store_swz(sV, LDN, tid, SWX);
         if (w == 0) {
             sb[lane] = b2;
             sq[lane] = fexp2(b2);
@@ -192,54 +253,61 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         __syncthreads();
         if (c + 1 < nch) issue(c + 1);
 
-        // scores on the causal tiles: P^T[s][t] = k_s . q_t and k_s . k_t
-        for (int i = OUTP ? w : 10 + w; i < 20; i += NW) {
-            const bool kk = i >= 10;
-            int tt, st;
-            tri_tile(kk ? i - 10 : i, tt, st);
-            f32x4 p = {0.f, 0.f, 0.f, 0.f};
+        // scores on the causal tiles: k_s . k_t (A) first; k_s . q_t (P) after the
+        // solve, whose T occupies the P tiles' LDS
+        auto scores = [&](int i0) {
+            for (int i = i0 + w; i < i0 + 10; i += NW) {
+                const bool kk = i >= 10;
+                int tt, st;
+                tri_tile(kk ? i - 10 : i, tt, st);
+                f32x4 p = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int ks = 0; ks < D / 32; ++ks) {
-                const frag_t<T> kf = ldfrag_swz<T, LDN, SWX>(sK, swo, 16 * st, 32 * ks);
-                const frag_t<T> xf = kk ? ldfrag_swz<T, LDN, SWX>(sK, swo, 16 * tt, 32 * ks)
-                                        : ldfrag(sQ, LDN, 16 * tt, 32 * ks, lane);
-                mma(p, kf, xf);
-            }
-            const int t = 16 * tt + n16;
-            const float bt = sb[t];
-            const f32x4 bs = *reinterpret_cast<const f32x4 *>(&sb[16 * st + 4 * q4]);
-            float v4[4];
-            if (!kk) {
-                if constexpr (OUTP) {
+                for (int ks = 0; ks < D / 32; ++ks) {
+                    const frag_t<T> kf = ldfrag_swz<T, LDN, SWX>(sK, swo, 16 * st, 32 * ks);
+                    const frag_t<T> xf = kk ? ldfrag_swz<T, LDN, SWX>(sK, swo, 16 * tt, 32 * ks)
+                                            : ldfrag(sQ, LDN, 16 * tt, 32 * ks, lane);
+                    mma(p, kf, xf);
+                }
+                const int t = 16 * tt + n16;
+                const float bt = sb[t];
+                const f32x4 bs = *reinterpret_cast<const f32x4 *>(&sb[16 * st + 4 * q4]);
+                float v4[4];
+                if (!kk) {
+                    if constexpr (OUTP) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int s = 16 * st + 4 * q4 + r;
+                            v4[r] = s <= t ? p[r] * fexp2(bt - bs[r]) : 0.f;
+                        }
+                        const int o = t * LDT + ((16 * st + 4 * q4) ^ asw(t));
+                        st4_split<T, true>(&sP[o], &sPl[o], v4);
+                    }
+                } else {
+                    const float be = sbeta[t];
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int s = 16 * st + 4 * q4 + r;
-                        v4[r] = s <= t ? p[r] * fexp2(bt - bs[r]) : 0.f;
+                        v4[r] = s < t ? be * p[r] * fexp2(bt - bs[r]) : 0.f;
                     }
-                    const int o = t * LDT + ((16 * st + 4 * q4) ^ asw(t));
-                    st4_split<T, true>(&sP[o], &sPl[o], v4);
+                    *reinterpret_cast<f32x4 *>(&sA[t * LDA + 16 * st + 4 * q4]) = f32x4{v4[0], v4[1], v4[2], v4[3]};
                 }
-            } else {
-                const float be = sbeta[t];
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int s = 16 * st + 4 * q4 + r;
-                    v4[r] = s < t ? be * p[r] * fexp2(bt - bs[r]) : 0.f;
-                }
-                *reinterpret_cast<f32x4 *>(&sA[t * LDA + 16 * st + 4 * q4]) = f32x4{v4[0], v4[1], v4[2], v4[3]};
+            }
+        };
+        scores(10);
+        __syncthreads();
+        gdn_tinv<NT>(tid, sA, sT);
+        gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sT, sK, sV, sbeta, sq, sW, sU);
+        __syncthreads();
+        if constexpr (OUTP) {
+            scores(0);
+            // P tiles above the diagonal that the output product reads are zero
+            for (int e = tid; e < (OUTP ? 512 : 0); e += NT) {
+                const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
+                const int row = tile ? 32 + rr : rr, col = tile ? 48 + cc : 16 + cc;
+                sP[row * LDT + (col ^ asw(row))] = cvt<T>(0.f);
+                sPl[row * LDT + (col ^ asw(row))] = cvt<T>(0.f);
             }
         }
-        // P tiles above the diagonal that the output product reads are zero
-        for (int e = tid; e < (OUTP ? 512 : 0); e += NT) {
-            const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
-            const int row = tile ? 32 + rr : rr, col = tile ? 48 + cc : 16 + cc;
-            sP[row * LDT + (col ^ asw(row))] = cvt<T>(0.f);
-            sPl[row * LDT + (col ^ asw(row))] = cvt<T>(0.f);
-        }
-        __syncthreads();
-
-        // (I + A) [W | Ubar] = [diag(beta gamma) K | diag(beta) V]
-        gdn_solve<T, D, LDN, LDA, LDU, SWX>(tid, 2 * D, sK, sV, sA, sbeta, sq, sW, sU);
         __syncthreads();
 
         // U[t][v] = Ubar[t][v] - sum_k W[t][k] S[k][v]  (rows t = 16tt + 4q4 + r, column v = c0 + n16);
@@ -435,8 +503,11 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
     __shared__ __attribute__((aligned(16))) T sQ[C * LDN];   // swizzled
     __shared__ __attribute__((aligned(16))) T sK[C * LDN];   // swizzled
     __shared__ __attribute__((aligned(16))) T sO[C * LDN];   // dO, swizzled
-    __shared__ __attribute__((aligned(16))) T sP[C * LDT];   // P^T[s][t] = e^{b_t-b_s} k_s.q_t (s <= t) hi
-    __shared__ __attribute__((aligned(16))) T sPl[C * LDT];  // lo
+    // P^T[s][t] = e^{b_t-b_s} k_s.q_t (s <= t) hi, then lo; T = (I + A)^{-1} lives here first
+    __shared__ __attribute__((aligned(16))) T sPP[2 * C * LDT];
+    static_assert(2 * C * LDT * sizeof(T) >= C * (C + 4) * sizeof(float), "T does not fit the P tiles");
+    T *sP = sPP, *sPl = sPP + C * LDT;
+    float *sT = reinterpret_cast<float *>(sPP);
     __shared__ __attribute__((aligned(16))) float sA[C * LDA];
     __shared__ __attribute__((aligned(16))) float sW[C * LDU];
     __shared__ __attribute__((aligned(16))) float sb[C], sq[C], se[C], sbeta[C];
@@ -514,8 +585,10 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
         __syncthreads();
         if (c > 0) issue(c - 1);
 
-        // scores on the causal tiles: k_s . q_t -> P^T, k_s . k_t -> A
-        for (int i = w; i < 20; i += NW) {
+        // scores on the causal tiles: k_s . k_t -> A first; k_s . q_t -> P^T after the
+        // solve, whose T occupies the P tiles' LDS
+        auto scores = [&](int i0) {
+        for (int i = i0 + w; i < i0 + 10; i += NW) {
             const bool kk = i >= 10;
             int tt, st;
             tri_tile(kk ? i - 10 : i, tt, st);
@@ -549,6 +622,13 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
                 *reinterpret_cast<f32x4 *>(&sA[t * LDA + 16 * st + 4 * q4]) = f32x4{v4[0], v4[1], v4[2], v4[3]};
             }
         }
+        };
+        scores(10);
+        __syncthreads();
+        gdn_tinv<NT>(tid, sA, sT);
+        gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sT, sK, (const T *)nullptr, sbeta, sq, sW, nullptr);
+        __syncthreads();
+        scores(0);
         // P^T tiles below the diagonal that the dU product reads are zero
         for (int e = tid; e < 512; e += NT) {
             const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
@@ -556,8 +636,6 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
             sP[row * LDT + (col ^ asw(row))] = cvt<T>(0.f);
             sPl[row * LDT + (col ^ asw(row))] = cvt<T>(0.f);
         }
-        __syncthreads();
-        gdn_solve<T, D, LDN, LDA, LDU, SWX>(tid, D, sK, nullptr, sA, sbeta, sq, sW, nullptr);
         __syncthreads();
 
         // dU[t][v] = e^{b_C - b_t} sum_k K[t][k] dS[k][v] + sum_{t' >= t} P^T[t][t'] dO[t'][v]
