@@ -44,14 +44,15 @@ namespace sf {
 
 namespace {
 
-// T = (I + A)^{-1} for the strictly lower 64 x 64 A in sA (pitch C + 4), into
+// T = (I + A)^{-1} for the strictly lower 64 x 64 A = diag(rs) M with M in sA
+// (pitch C + 4; rs == nullptr: A = M), into
 // sT (fp32, pitch C + 4, zero above the diagonal), by 16 x 16 blocks: the four
 // diagonal blocks by forward substitution (64 threads, one column each), then
 // the off-diagonal blocks level by level, T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj
 // (i - j = 1, 2, 3), the inner sums parked in the free upper blocks.  All fp32.
 // NT >= 256 threads; ends with a barrier.
 template <int NT>
-__device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT) {
+__device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, const float *rs = nullptr) {
     constexpr int LA = C + 4, LT = C + 4;
     if (tid < 64) {
         const int o = 16 * (tid >> 4), c = tid & 15;
@@ -61,7 +62,7 @@ __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT) {
             float acc = 0.f;
 #pragma unroll
             for (int s2 = 0; s2 < r; ++s2) acc = fmaf(sA[(o + r) * LA + o + s2], x[s2], acc);
-            x[r] = r == c ? 1.f : (r > c ? -acc : 0.f);
+            x[r] = r == c ? 1.f : (r > c ? -(rs ? rs[o + r] : 1.f) * acc : 0.f);
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) sT[(o + r) * LT + o + c] = x[r];
@@ -76,7 +77,7 @@ __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT) {
 #pragma unroll
                 for (int m = 0; m < 16; ++m)
                     y = fmaf(sA[(16 * i + rr) * LA + 16 * k + m], sT[(16 * k + m) * LT + 16 * j + cc], y);
-            sT[(16 * j + rr) * LT + 16 * i + cc] = y;
+            sT[(16 * j + rr) * LT + 16 * i + cc] = rs ? rs[16 * i + rr] * y : y;
         }
         __syncthreads();
         for (int e = tid; e < (4 - d) * 256; e += NT) {  // T_ij = -T_ii Y_ij
@@ -908,20 +909,8 @@ __global__ void __launch_bounds__(512) k_gdn_dchunk(GdnArgs a) {
                 }
         }
         __syncthreads();
-        // T = (I + A)^{-1}, A = diag(beta) KK: column j by forward substitution
-        if (tid < C) {
-            const int j = tid;
-            for (int t = 0; t < C; ++t) {
-                float x = t == j ? 1.f : 0.f;
-                if (t > j) {
-                    float acc = 0.f;
-                    for (int s2 = j; s2 < t; ++s2) acc = fmaf(sKK[t * LD6 + s2], sT[s2 * LD6 + j], acc);
-                    x = -sbe[t] * acc;
-                }
-                sT[t * LD6 + j] = x;
-            }
-        }
-        __syncthreads();
+        // T = (I + A)^{-1}, A = diag(beta) KK
+        gdn_tinv<NTH>(tid, sKK, sT, sbe);
         // W = T diag(beta gamma) K, Ubar = T diag(beta) V
         {
             f32x4 cw[NT2], cu[NT2];
