@@ -185,3 +185,32 @@ def test_gdn_bwd_long_segment_sampled():
     want = ref_bwd(inp, dO, dS, heads)
     sub = [x[:, :, heads] for x in got[:5]] + [got[5][:, heads]]
     check_bwd(sub, want)
+
+
+def test_gdn_bwd_chained_segments():
+    """Forward chained through S, backward chained through dS in reverse: the
+    gradients of the concatenated segments equal the oracle's over the whole
+    sequence."""
+    B, H, D = 1, 2, 128
+    segs = [256, 64, 320]
+    say(f"[gdn bwd] chained {segs}")
+    inp = synth.make_gdn_inputs(B, sum(segs), H, D, seed=5000)
+    dO, dS_out = grads_inputs(inp, 5001)
+    g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
+    dOd, dSd = dO.to(DEV), dS_out.to(DEV)
+    starts = [sum(segs[:i]) for i in range(len(segs))]
+    sl = lambda x, t, n: x[:, t:t + n]
+    S, bounds = g["S_in"], []
+    for t, n in zip(starts, segs):
+        bounds.append(S)
+        _, S = sf.gdn_fwd(sl(g["q"], t, n), sl(g["k"], t, n), sl(g["v"], t, n), sl(g["g"], t, n),
+                          sl(g["beta"], t, n), S)
+    dS, parts = dSd, []
+    for t, n, S0 in reversed(list(zip(starts, segs, bounds))):
+        out = sf.gdn_bwd(sl(g["q"], t, n), sl(g["k"], t, n), sl(g["v"], t, n), sl(g["g"], t, n),
+                         sl(g["beta"], t, n), S0, sl(dOd, t, n), dS)
+        parts.insert(0, out[:5])
+        dS = out[5]
+    torch.cuda.synchronize()
+    got = [torch.cat([p[i] for p in parts], 1) for i in range(5)] + [dS]
+    check_bwd(got, ref_bwd(inp, dO, dS_out))
