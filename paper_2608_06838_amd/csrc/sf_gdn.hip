@@ -44,13 +44,32 @@ namespace sf {
 
 namespace {
 
+// 16x16x16 bf16 MFMA: A lane (q, n) holds row n, k = 4q .. 4q+3; B lane (q, n)
+// holds k = 4q .. 4q+3 of column n; the accumulator holds rows 4q .. 4q+3 of
+// column n, the same slots as a B operand.
+typedef short s4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void mma16(f32x4 &c, s4v a, s4v b) {
+    c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+// hi = bf16(x), lo = bf16(x - hi), as the raw 16-bit patterns
+__device__ __forceinline__ void split4(const f32x4 &x, s4v &hi, s4v &lo) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const __bf16 h = (__bf16)x[j];
+        const __bf16 l = (__bf16)(x[j] - (float)h);
+        hi[j] = __builtin_bit_cast(short, h);
+        lo[j] = __builtin_bit_cast(short, l);
+    }
+}
+
 // T = (I + A)^{-1} for the strictly lower 64 x 64 A = diag(rs) M with M in sA
-// (pitch C + 4; rs == nullptr: A = M), into
-// sT (fp32, pitch C + 4, zero above the diagonal), by 16 x 16 blocks: the four
-// diagonal blocks by forward substitution (64 threads, one column each), then
-// the off-diagonal blocks level by level, T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj
-// (i - j = 1, 2, 3), the inner sums parked in the free upper blocks.  All fp32.
-// NT >= 256 threads; ends with a barrier.
+// (pitch C + 4; rs == nullptr: A = M), into sT (fp32, pitch C + 4, zero above
+// the diagonal), by 16 x 16 blocks: the four diagonal blocks by forward
+// substitution in fp32 (64 threads, one column each); then level by level
+// (i - j = 1, 2, 3) wave j forms T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj on
+// 16x16x16 MFMA with hi/lo operands, the inner sum staying in its
+// accumulator, which is already the B operand of the T_ii product.  NT >= 256
+// threads (four waves); ends with a barrier.
 template <int NT>
 __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, const float *rs = nullptr) {
     constexpr int LA = C + 4, LT = C + 4;
@@ -67,35 +86,44 @@ __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, co
 #pragma unroll
         for (int r = 0; r < 16; ++r) sT[(o + r) * LT + o + c] = x[r];
     }
-    __syncthreads();
-#pragma unroll
-    for (int d = 1; d < 4; ++d) {
-        for (int e = tid; e < (4 - d) * 256; e += NT) {  // Y_ij, kept in block (j, i)
-            const int i = d + (e >> 8), j = i - d, rr = (e >> 4) & 15, cc = e & 15;
-            float y = 0.f;
-            for (int k = j; k < i; ++k)
-#pragma unroll
-                for (int m = 0; m < 16; ++m)
-                    y = fmaf(sA[(16 * i + rr) * LA + 16 * k + m], sT[(16 * k + m) * LT + 16 * j + cc], y);
-            sT[(16 * j + rr) * LT + 16 * i + cc] = rs ? rs[16 * i + rr] * y : y;
-        }
-        __syncthreads();
-        for (int e = tid; e < (4 - d) * 256; e += NT) {  // T_ij = -T_ii Y_ij
-            const int i = d + (e >> 8), j = i - d, rr = (e >> 4) & 15, cc = e & 15;
-            float t = 0.f;
-#pragma unroll
-            for (int m = 0; m < 16; ++m)
-                t = fmaf(sT[(16 * i + rr) * LT + 16 * i + m], sT[(16 * j + m) * LT + 16 * i + cc], t);
-            sT[(16 * i + rr) * LT + 16 * j + cc] = -t;
-        }
-        __syncthreads();
-    }
     for (int e = tid; e < 6 * 256; e += NT) {  // blocks (0,1) (0,2) (0,3) (1,2) (1,3) (2,3)
         const int b = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
         const int bi = b < 3 ? 0 : (b < 5 ? 1 : 2), bj = b < 3 ? b + 1 : (b < 5 ? b - 1 : 3);
         sT[(16 * bi + rr) * LT + 16 * bj + cc] = 0.f;
     }
     __syncthreads();
+    const int w = tid >> 6, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
+#pragma unroll
+    for (int d = 1; d < 4; ++d) {
+        if (w < 4 - d) {  // block (i, j) = (d + w, w)
+            const int i = d + w, j = w;
+            f32x4 y = {0.f, 0.f, 0.f, 0.f};
+            for (int k = j; k < i; ++k) {
+                f32x4 av = *reinterpret_cast<const f32x4 *>(&sA[(16 * i + n16) * LA + 16 * k + 4 * q4]);
+                if (rs) av *= rs[16 * i + n16];
+                f32x4 tb;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) tb[u] = sT[(16 * k + 4 * q4 + u) * LT + 16 * j + n16];
+                s4v ah, al, bh, bl;
+                split4(av, ah, al);
+                split4(tb, bh, bl);
+                mma16(y, ah, bh);
+                mma16(y, ah, bl);
+                mma16(y, al, bh);
+            }
+            const f32x4 tv = *reinterpret_cast<const f32x4 *>(&sT[(16 * i + n16) * LT + 16 * i + 4 * q4]);
+            s4v th, tl, yh, yl;
+            split4(tv, th, tl);
+            split4(y, yh, yl);
+            f32x4 t = {0.f, 0.f, 0.f, 0.f};
+            mma16(t, th, yh);
+            mma16(t, th, yl);
+            mma16(t, tl, yh);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sT[(16 * i + 4 * q4 + r) * LT + 16 * j + n16] = -t[r];
+        }
+        __syncthreads();
+    }
 }
 
 // [W | Ubar] = T [diag(beta gamma) K | diag(beta) V] on MFMA: wave w forms
