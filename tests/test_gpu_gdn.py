@@ -241,3 +241,26 @@ def test_gdn_head_major_layout():
     assert_close("o", to64(o), ro, "bf16")
     assert_close("S_out", to64(S), rS, "bf16")
     check_bwd(grads, ref_bwd(inp, dO, dS_out))
+
+
+def test_gdn_full_size_segment_sampled():
+    """The largest segment of the 256K-context workload at full size
+    (B 1, L 65536, H 40, d 128, the library's own superchunk choice): forward
+    and backward on the GPU, two heads against the oracle."""
+    B, L, H, D = 1, 65536, 40, 128
+    say(f"[gdn] full-size segment L={L} H={H}")
+    inp = synth.make_gdn_inputs(B, L, H, D, device=DEV, seed=5200)
+    gen = torch.Generator(device=DEV).manual_seed(5201)
+    dO = torch.randn((B, L, H, D), device=DEV, generator=gen).to(torch.bfloat16)
+    dS_out = 0.1 * torch.randn((B, H, D, D), device=DEV, generator=gen)
+    o, S = sf.gdn_fwd(inp["q"], inp["k"], inp["v"], inp["g"], inp["beta"], inp["S_in"])
+    grads = sf.gdn_bwd(inp["q"], inp["k"], inp["v"], inp["g"], inp["beta"], inp["S_in"], dO, dS_out)
+    torch.cuda.synchronize()
+    heads = [0, 37]
+    cpu = {k: v[:, :, heads].cpu() for k, v in inp.items() if k != "S_in"}
+    cpu["S_in"] = inp["S_in"][:, heads].cpu()
+    ro, rS = ref(cpu)
+    assert_close("o", to64(o[:, :, heads]), ro, "bf16")
+    assert_close("S_out", to64(S[:, heads]), rS, "bf16")
+    sub = [x[:, :, heads] for x in grads[:5]] + [grads[5][:, heads]]
+    check_bwd(sub, ref_bwd(cpu, dO[:, :, heads].cpu(), dS_out[:, heads].cpu()))
