@@ -293,6 +293,37 @@ sf_status sf_gdn_bwd(const sf_shape *shape, const void *q, const void *k, const 
                      const sf_tuning *tuning, sf_stream stream);
 
 /*
+ * Gated delta rule over n_seg consecutive segments (Sec. 3.1 chaining), one
+ * call each way.  Shapes and per-token tensors as for sf_gdn_fwd with
+ * shape->L = sum of seg_len (each a positive multiple of 64).
+ *   S_bnd  [n_seg + 1][B][H][Dk][Dv] f32: slot 0 is S_init (input, zeros for
+ *          a zero state); the forward writes slot i+1 = the state after
+ *          segment i.  The backward reads slots 0 .. n_seg-1.
+ *   v_new  optional (NULL to skip), as for sf_gdn_fwd.
+ *   dS_final  optional gradient of the state after the last segment.
+ *   dS_init   receives the gradient of S_init.
+ *   ws     at least sf_gdn_chain_workspace_bytes(); contents on entry ignored.
+ * With aux != NULL (and tuning->overlap != 0) the state scans run on aux:
+ * forward, the scan of each segment (which then also writes S_bnd[i+1]) runs
+ * alongside the previous segment's output walk; backward, the state scan
+ * alongside the dS prep and the dS scan alongside the state-storing walk
+ * (Sec. 3.4, "Split and Overlap").  Results do not depend on the overlap.
+ * Both streams must belong to the current device; on return, work is queued on
+ * main that waits for everything queued on aux.
+ */
+size_t sf_gdn_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
+                                    const sf_tuning *tuning);
+sf_status sf_gdn_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
+                           const void *k, const void *v, const float *g, const float *beta, void *o, float *S_bnd,
+                           void *v_new, void *ws, size_t ws_bytes, const sf_tuning *tuning, sf_stream main,
+                           sf_stream aux);
+sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
+                           const void *k, const void *v, const float *g, const float *beta, const float *S_bnd,
+                           const void *dO, const float *dS_final, void *dq, void *dk, void *dv, float *dg,
+                           float *dbeta, float *dS_init, void *ws, size_t ws_bytes, const sf_tuning *tuning,
+                           sf_stream main, sf_stream aux);
+
+/*
  * Kernel timing for measurement: while enabled, every launch of kernel
  * `kernel_id` (an sf_kernel_id) carries HIP events that take the begin and
  * end timestamps of its own dispatch.  sf_prof_read() synchronises those

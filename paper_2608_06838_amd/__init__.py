@@ -30,7 +30,7 @@ from ._lib import KERNELS, StateflowError  # noqa: F401
 
 __all__ = ["segment_fwd", "segment_bwd", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
            "bwd_workspace_bytes", "chain_workspace_bytes", "conv_fwd", "conv_bwd", "conv_bwd_workspace_bytes",
-           "gdn_fwd", "gdn_fwd_workspace_bytes", "gdn_bwd", "partition_hybrid", "prof_enable", "prof_read", "StateflowError", "abi_version"]
+           "gdn_fwd", "gdn_fwd_workspace_bytes", "gdn_bwd", "gdn_chain_fwd", "gdn_chain_bwd", "partition_hybrid", "prof_enable", "prof_read", "StateflowError", "abi_version"]
 
 _IO = {torch.bfloat16: _lib.SF_BF16, torch.float32: _lib.SF_F32}
 _aux_streams = {}
@@ -391,6 +391,73 @@ def gdn_bwd(q, k, v, g, beta, S_in, dO, dS_out=None, *, ts=0, stream=None):
                        ws.numel(), ctypes.byref(tun), _stream_handle(stream))
     _lib.check("sf_gdn_bwd", rc)
     return dq, dk, dv, dg, dbeta, dS_in
+
+
+def gdn_chain_fwd(q, k, v, g, beta, seg_lens, S_init=None, *, ts=0, overlap=True, with_v_new=False, stream=None,
+                  aux_stream=None):
+    """Gated-delta-rule forward over consecutive segments with
+    S_in(i+1) = S_out(i), the state scans overlapped on an aux stream.
+
+    Returns (o, S_bnd) (and V^new after them when with_v_new) with S_bnd[i] the
+    state entering segment i and S_bnd[-1] the final state."""
+    _same_layout(q, k, v)
+    sh = _shape(q, g)
+    if tuple(beta.shape) != tuple(g.shape) or beta.stride() != g.stride() or beta.dtype != torch.float32:
+        raise ValueError("beta must match g in shape, strides and dtype (float32)")
+    B, L, H, D = q.shape
+    n = len(seg_lens)
+    _state(S_init, B, H, D, "S_init")
+    stream = stream or torch.cuda.current_stream(q.device)
+    aux = _aux_for(q.device, aux_stream, overlap)
+    L_ = _lib.lib()
+    tun = _tuning(ts, overlap)
+    sl = (ctypes.c_int64 * n)(*[int(x) for x in seg_lens])
+    with torch.cuda.stream(stream):
+        o = _like(q)
+        vn = _like(q) if with_v_new else None
+        S_bnd = torch.empty((n + 1, B, H, D, D), dtype=torch.float32, device=q.device)
+        ws = _ws(L_.sf_gdn_chain_workspace_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun)), q.device)
+        if S_init is None:
+            S_bnd[0].zero_()
+        else:
+            S_bnd[0].copy_(S_init)
+    rc = L_.sf_gdn_chain_fwd(ctypes.byref(sh), n, sl, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(o),
+                             _ptr(S_bnd), _ptr(vn), _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream),
+                             _stream_handle(aux) if aux is not None else None)
+    _lib.check("sf_gdn_chain_fwd", rc)
+    return (o, S_bnd, vn) if with_v_new else (o, S_bnd)
+
+
+def gdn_chain_bwd(q, k, v, g, beta, seg_lens, S_bnd, dO, dS_final=None, *, ts=0, overlap=True, stream=None,
+                  aux_stream=None):
+    """Gated-delta-rule backward over the segments in reverse with
+    dS_out(i) = dS_in(i+1); S_bnd from gdn_chain_fwd.  Returns
+    (dq, dk, dv, dg, dbeta, dS_init)."""
+    _same_layout(q, k, v, dO)
+    sh = _shape(q, g)
+    if tuple(beta.shape) != tuple(g.shape) or beta.stride() != g.stride() or beta.dtype != torch.float32:
+        raise ValueError("beta must match g in shape, strides and dtype (float32)")
+    B, L, H, D = q.shape
+    n = len(seg_lens)
+    if tuple(S_bnd.shape) != (n + 1, B, H, D, D) or S_bnd.dtype != torch.float32 or not S_bnd.is_contiguous():
+        raise ValueError("S_bnd must be a contiguous float32 [n_seg + 1, B, H, D, D] tensor")
+    _state(dS_final, B, H, D, "dS_final")
+    stream = stream or torch.cuda.current_stream(q.device)
+    aux = _aux_for(q.device, aux_stream, overlap)
+    L_ = _lib.lib()
+    tun = _tuning(ts, overlap)
+    sl = (ctypes.c_int64 * n)(*[int(x) for x in seg_lens])
+    with torch.cuda.stream(stream):
+        dq, dk, dv = _like(q), _like(k), _like(v)
+        dg, dbeta = _like(g), _like(beta)
+        dS_init = torch.empty((B, H, D, D), dtype=torch.float32, device=q.device)
+        ws = _ws(L_.sf_gdn_chain_workspace_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun)), q.device)
+    rc = L_.sf_gdn_chain_bwd(ctypes.byref(sh), n, sl, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S_bnd),
+                             _ptr(dO), _ptr(dS_final), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg), _ptr(dbeta),
+                             _ptr(dS_init), _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream),
+                             _stream_handle(aux) if aux is not None else None)
+    _lib.check("sf_gdn_chain_bwd", rc)
+    return dq, dk, dv, dg, dbeta, dS_init
 
 
 def partition_hybrid(T, N, alpha, w_tok, w_soft, round_to=128):

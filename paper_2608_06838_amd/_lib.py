@@ -24,6 +24,7 @@ EXPORTS = ["sf_abi_version", "sf_status_str", "sf_last_error", "sf_fwd_workspace
            "sf_bwd_workspace_bytes", "sf_segment_fwd", "sf_segment_bwd", "sf_chain_workspace_bytes",
            "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd",
            "sf_gdn_fwd_workspace_bytes", "sf_gdn_fwd", "sf_gdn_bwd_workspace_bytes", "sf_gdn_bwd",
+           "sf_gdn_chain_workspace_bytes", "sf_gdn_chain_fwd", "sf_gdn_chain_bwd",
            "sf_partition_hybrid",
            "sf_prof_enable", "sf_prof_read"]
 
@@ -107,6 +108,12 @@ def lib():
     L.sf_gdn_bwd_workspace_bytes.argtypes = [sp, tp]
     L.sf_gdn_bwd.restype = ctypes.c_int
     L.sf_gdn_bwd.argtypes = [sp] + [vp] * 15 + [sz, tp, vp]
+    L.sf_gdn_chain_workspace_bytes.restype = sz
+    L.sf_gdn_chain_workspace_bytes.argtypes = [sp, i32, i64p, tp]
+    L.sf_gdn_chain_fwd.restype = ctypes.c_int
+    L.sf_gdn_chain_fwd.argtypes = [sp, i32, i64p] + [vp] * 9 + [sz, tp, vp, vp]
+    L.sf_gdn_chain_bwd.restype = ctypes.c_int
+    L.sf_gdn_chain_bwd.argtypes = [sp, i32, i64p] + [vp] * 15 + [sz, tp, vp, vp]
     L.sf_partition_hybrid.restype = ctypes.c_int
     L.sf_partition_hybrid.argtypes = [i64, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double, i32, i64p]
     L.sf_prof_enable.restype = ctypes.c_int

@@ -922,10 +922,10 @@ struct GdnBwdWs {
     int n_x = 0;
 };
 constexpr int kGdnSlabs = 1024;
-GdnBwdWs gdn_bwd_ws(const Shape &r, int ts) {
+// for n superchunks and nc chunks per (batch, head)
+GdnBwdWs gdn_bwd_ws_n(const Shape &r, int n, size_t nc) {
     GdnBwdWs w;
-    const int n = std::max(1, n_super_of(r.L, ts));
-    const size_t bh = (size_t)r.B * r.H, SS = (size_t)r.D * r.D * 4, nc = (size_t)(r.L / 64);
+    const size_t bh = (size_t)r.B * r.H, SS = (size_t)r.D * r.D * 4;
     size_t off = 0;
     auto take = [&](size_t &at, size_t bytes) {
         at = off;
@@ -943,6 +943,78 @@ GdnBwdWs gdn_bwd_ws(const Shape &r, int ts) {
     w.n_x = (int)std::max<size_t>(1, std::min<size_t>(bh * nc, kGdnSlabs));
     take(w.X, (size_t)w.n_x * 8 * 64 * r.D * 4);
     w.total = off;
+    return w;
+}
+GdnBwdWs gdn_bwd_ws(const Shape &r, int ts) { return gdn_bwd_ws_n(r, std::max(1, n_super_of(r.L, ts)), (size_t)(r.L / 64)); }
+
+// Forward workspace: S_J for every superchunk, then M, N for n_prep of them.
+struct GdnFwdWs {
+    size_t S = 0, M = 0, N = 0, total = 0;
+};
+GdnFwdWs gdn_fwd_ws_n(const Shape &r, int n, int n_prep) {
+    GdnFwdWs w;
+    if (n <= 1) return w;
+    const size_t bh = (size_t)r.B * r.H, SS = (size_t)r.D * r.D * 4;
+    w.M = al(bh * n * SS);
+    w.N = w.M + al(bh * n_prep * SS);
+    w.total = w.N + al(bh * n_prep * SS);
+    return w;
+}
+
+// GdnArgs of tokens [tok, tok + L) of the shape's tensors (pointers of the
+// whole-sequence tensors; NULL stays NULL).
+sf::GdnArgs gdn_seg_args(const Shape &r, int64_t tok, int64_t L, int ts, const void *q, const void *k,
+                         const void *v, const float *g, const float *beta) {
+    sf::GdnArgs a{};
+    a.q = offset_x(r, q, tok);
+    a.k = offset_x(r, k, tok);
+    a.v = offset_x(r, v, tok);
+    a.g = offset_g(r, g, tok);
+    a.beta = offset_g(r, beta, tok);
+    a.B = r.B;
+    a.H = r.H;
+    a.L = L;
+    a.sx_b = r.sx_b;
+    a.sx_l = r.sx_l;
+    a.sx_h = r.sx_h;
+    a.sg_b = r.sg_b;
+    a.sg_l = r.sg_l;
+    a.sg_h = r.sg_h;
+    a.ts = ts;
+    a.n_super = std::max(1, n_super_of(L, ts));
+    return a;
+}
+
+// superchunk length and count of every segment, and the largest of each
+struct GdnPlan {
+    std::vector<int> ts, n;
+    int n_max = 1;
+    int64_t nc_max = 0;
+};
+sf_status gdn_plan(const Shape &r, int32_t n_seg, const int64_t *seg_len, const sf_tuning *t, GdnPlan &p) {
+    p.ts.resize(n_seg);
+    p.n.resize(n_seg);
+    for (int i = 0; i < n_seg; ++i) {
+        Shape rs = r;
+        rs.L = seg_len[i];
+        TRY(gdn_pick_ts(rs, t, p.ts[i]));
+        p.n[i] = std::max(1, n_super_of(seg_len[i], p.ts[i]));
+        p.n_max = std::max(p.n_max, p.n[i]);
+        p.nc_max = std::max<int64_t>(p.nc_max, seg_len[i] / 64);
+    }
+    return SF_OK;
+}
+// chain workspace: two forward sets (maps of every superchunk) or one backward
+// set and two boundary-gradient slots, whichever is larger
+struct GdnChainWs {
+    size_t fwd_set = 0, bwd = 0, dslot = 0, total = 0;
+};
+GdnChainWs gdn_chain_ws(const Shape &r, const GdnPlan &p) {
+    GdnChainWs w;
+    w.fwd_set = al(std::max<size_t>(gdn_fwd_ws_n(r, p.n_max, p.n_max).total, 1));
+    w.bwd = al(gdn_bwd_ws_n(r, p.n_max, (size_t)p.nc_max).total);
+    w.dslot = al((size_t)r.B * r.H * r.D * r.D * 4);
+    w.total = std::max(2 * w.fwd_set, w.bwd + 2 * w.dslot);
     return w;
 }
 
@@ -1107,6 +1179,201 @@ sf_status sf_gdn_bwd(const sf_shape *shape, const void *q, const void *k, const 
     if (on) {
         std::lock_guard<std::mutex> lk(g_prof_mu);
         g_prof_ev[SF_K_GDN_BWD].push_back({e0, e1});
+    }
+    return SF_OK;
+}
+
+size_t sf_gdn_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
+                                    const sf_tuning *tuning) {
+    Shape r;
+    GdnPlan p;
+    if (resolve(shape, r) != SF_OK || check_segments(r, n_seg, seg_len) != SF_OK ||
+        gdn_plan(r, n_seg, seg_len, tuning, p) != SF_OK)
+        return 0;
+    return gdn_chain_ws(r, p).total;
+}
+
+sf_status gdn_shape_ok(const Shape &r) {
+    if (r.io != SF_BF16) return fail(SF_E_UNSUPPORTED, "the gated delta rule needs bf16 I/O");
+    if (r.gate != SF_GATE_SCALAR) return fail(SF_E_UNSUPPORTED, "the gated delta rule takes a scalar gate");
+    return SF_OK;
+}
+
+sf_status gdn_launch(int phase, const sf::GdnArgs &a, int D, hipStream_t s) {
+    const hipError_t e = sf::launch_gdn_phase(phase, a, D, s, nullptr, nullptr);
+    return e == hipSuccess ? SF_OK : hip_fail(e, "kernel launch");
+}
+
+sf_status sf_gdn_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
+                           const void *k, const void *v, const float *g, const float *beta, void *o, float *S_bnd,
+                           void *v_new, void *ws, size_t ws_bytes, const sf_tuning *tuning, sf_stream main_s,
+                           sf_stream aux_s) {
+    g_err.clear();
+    Shape r;
+    TRY(resolve(shape, r));
+    TRY(gdn_shape_ok(r));
+    TRY(check_segments(r, n_seg, seg_len));
+    if (!q || !k || !v || !g || !beta || !o || !S_bnd || !ws)
+        return fail(SF_E_NULL, "q, k, v, g, beta, o, S_bnd and ws are required");
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_bnd, "S_bnd"}, {v_new, "v_new"}, {ws, "ws"}}));
+    if (((uintptr_t)g | (uintptr_t)beta) % 4) return fail(SF_E_ALIGN, "g and beta must be 4-byte aligned");
+    GdnPlan p;
+    TRY(gdn_plan(r, n_seg, seg_len, tuning, p));
+    const GdnChainWs W = gdn_chain_ws(r, p);
+    if (ws_bytes < W.total) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, W.total);
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"), grange(r, g, r.L, "g"),
+                     grange(r, beta, r.L, "beta")},
+                    {xrange(r, o, r.L, "o"), srange(r, S_bnd, n_seg + 1, "S_bnd"), xrange(r, v_new, r.L, "v_new"),
+                     {(const char *)ws, (const char *)ws + W.total, "ws"}}));
+    const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
+    const GdnFwdWs F = gdn_fwd_ws_n(r, p.n_max, p.n_max);
+    std::vector<sf::GdnArgs> seg(n_seg);
+    int64_t tok = 0;
+    for (int i = 0; i < n_seg; ++i) {
+        sf::GdnArgs &a = seg[i];
+        a = gdn_seg_args(r, tok, seg_len[i], p.ts[i], q, k, v, g, beta);
+        a.o = (void *)offset_x(r, o, tok);
+        a.v_new = v_new ? (void *)offset_x(r, v_new, tok) : nullptr;
+        a.S_in = S_bnd + i * SSB;
+        a.S_out = S_bnd + (i + 1) * SSB;
+        a.n_prep = a.n_super;  // maps of every superchunk: the scan writes S_out
+        a.scan_out = 1;
+        char *base = (char *)ws + (i % 2) * W.fwd_set;
+        if (a.n_super > 1) {
+            a.wsS = (float *)(base + F.S);
+            a.wsM = (float *)(base + F.M);
+            a.wsN = (float *)(base + F.N);
+        }
+        tok += seg_len[i];
+    }
+    hipStream_t mn = (hipStream_t)main_s;
+    hipStream_t ax = (aux_s && (!tuning || tuning->overlap != 0)) ? (hipStream_t)aux_s : mn;
+    hipEvent_t e0 = nullptr, e1 = nullptr, sd[2] = {nullptr, nullptr};
+    if (ax != mn) TRY(events(e0, e1, sd));
+    // Schedule: Pre(i) on main -> ST(i) on aux, which also produces S_bnd[i+1],
+    // so ST(i+1) follows ST(i) on aux while Out(i) runs on main after ST(i).
+    // A single-superchunk segment's walk produces its S_out on main.  Out(i-1)
+    // waits on main for ST(i-1), queued before Pre(i+1) overwrites workspace set
+    // (i+1) % 2 = (i-1) % 2.
+    int pending = -1;
+    for (int i = 0; i < n_seg; ++i) {
+        sf::GdnArgs &a = seg[i];
+        if (a.n_super > 1) {
+            TRY(gdn_launch(sf::GDN_PREP, a, r.D, mn));
+            TRY(dep(mn, ax, e0));  // prep(i), and any S_bnd[i] written on main
+            TRY(gdn_launch(sf::GDN_SCAN, a, r.D, ax));
+            if (ax != mn) TRY(record(sd[i % 2], ax));
+        }
+        if (pending >= 0) {
+            if (ax != mn) TRY(wait(mn, sd[pending % 2]));
+            TRY(gdn_launch(sf::GDN_OUT, seg[pending], r.D, mn));
+            pending = -1;
+        }
+        if (a.n_super > 1) {
+            pending = i;
+        } else {
+            if (ax != mn && i > 0 && seg[i - 1].n_super > 1) TRY(wait(mn, sd[(i - 1) % 2]));  // S_bnd[i]
+            TRY(gdn_launch(sf::GDN_OUT, a, r.D, mn));
+        }
+    }
+    if (pending >= 0) {
+        if (ax != mn) TRY(wait(mn, sd[pending % 2]));
+        TRY(gdn_launch(sf::GDN_OUT, seg[pending], r.D, mn));
+    }
+    if (ax != mn) TRY(dep(ax, mn, e1));
+    return SF_OK;
+}
+
+sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
+                           const void *k, const void *v, const float *g, const float *beta, const float *S_bnd,
+                           const void *dO, const float *dS_final, void *dq, void *dk, void *dv, float *dg,
+                           float *dbeta, float *dS_init, void *ws, size_t ws_bytes, const sf_tuning *tuning,
+                           sf_stream main_s, sf_stream aux_s) {
+    g_err.clear();
+    Shape r;
+    TRY(resolve(shape, r));
+    TRY(gdn_shape_ok(r));
+    TRY(check_segments(r, n_seg, seg_len));
+    if (!q || !k || !v || !g || !beta || !S_bnd || !dO || !dq || !dk || !dv || !dg || !dbeta || !dS_init || !ws)
+        return fail(SF_E_NULL, "q, k, v, g, beta, S_bnd, dO, dq, dk, dv, dg, dbeta, dS_init and ws are required");
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {dO, "dO"}, {dq, "dq"}, {dk, "dk"}, {dv, "dv"}, {S_bnd, "S_bnd"},
+                     {dS_final, "dS_final"}, {dS_init, "dS_init"}, {ws, "ws"}}));
+    if (((uintptr_t)g | (uintptr_t)beta | (uintptr_t)dg | (uintptr_t)dbeta) % 4)
+        return fail(SF_E_ALIGN, "g, beta, dg and dbeta must be 4-byte aligned");
+    GdnPlan p;
+    TRY(gdn_plan(r, n_seg, seg_len, tuning, p));
+    const GdnChainWs W = gdn_chain_ws(r, p);
+    if (ws_bytes < W.total) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, W.total);
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"), grange(r, g, r.L, "g"),
+                     grange(r, beta, r.L, "beta"), srange(r, S_bnd, n_seg, "S_bnd"), xrange(r, dO, r.L, "dO"),
+                     srange(r, dS_final, 1, "dS_final")},
+                    {xrange(r, dq, r.L, "dq"), xrange(r, dk, r.L, "dk"), xrange(r, dv, r.L, "dv"),
+                     grange(r, dg, r.L, "dg"), grange(r, dbeta, r.L, "dbeta"), srange(r, dS_init, 1, "dS_init"),
+                     {(const char *)ws, (const char *)ws + W.total, "ws"}}));
+    const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
+    const GdnBwdWs Lw = gdn_bwd_ws_n(r, p.n_max, (size_t)p.nc_max);
+    char *base = (char *)ws;
+    float *dslot[2] = {(float *)(base + W.bwd), (float *)(base + W.bwd + W.dslot)};
+    std::vector<sf::GdnArgs> seg(n_seg);
+    int64_t tok = 0;
+    for (int i = 0; i < n_seg; ++i) {
+        sf::GdnArgs &a = seg[i];
+        a = gdn_seg_args(r, tok, seg_len[i], p.ts[i], q, k, v, g, beta);
+        a.S_in = S_bnd + i * SSB;
+        a.dO = offset_x(r, dO, tok);
+        a.dq = (void *)offset_x(r, dq, tok);
+        a.dk = (void *)offset_x(r, dk, tok);
+        a.dv = (void *)offset_x(r, dv, tok);
+        a.dg = (float *)offset_g(r, dg, tok);
+        a.dbeta = (float *)offset_g(r, dbeta, tok);
+        // the state gradient leaving segment i enters it from segment i+1 (slot
+        // (i+1) % 2), and the one entering goes to slot i % 2 (dS_init for i = 0)
+        a.dS_out = i == n_seg - 1 ? dS_final : dslot[(i + 1) % 2];
+        a.dS_in = i == 0 ? dS_init : dslot[i % 2];
+        a.n_prep = a.n_super;
+        if (a.n_super > 1) {
+            a.wsS = (float *)(base + Lw.S);
+            a.wsM = (float *)(base + Lw.M);
+            a.wsN = (float *)(base + Lw.N);
+            a.wsE = (float *)(base + Lw.E);
+            a.wsDe = (float *)(base + Lw.De);
+        }
+        a.wsSc = (float *)(base + Lw.Sc);
+        a.wsDc = (float *)(base + Lw.Dc);
+        a.wsX = (float *)(base + Lw.X);
+        a.n_x = Lw.n_x;
+        tok += seg_len[i];
+    }
+    hipStream_t mn = (hipStream_t)main_s;
+    hipStream_t ax = (aux_s && (!tuning || tuning->overlap != 0)) ? (hipStream_t)aux_s : mn;
+    hipEvent_t e0 = nullptr, e1 = nullptr, sd[2] = {nullptr, nullptr};
+    if (ax != mn) TRY(events(e0, e1, sd));
+    // Segments last to first.  Per segment on main: prep, dS prep, the
+    // state-storing walk (after the scan), the dS walk (after the dS scan), the
+    // per-chunk gradients; on aux: the scan after the prep (overlapping the dS
+    // prep) and the dS scan after the dS prep and the next segment's dS walk
+    // (overlapping the state-storing walk).  One workspace set serves every
+    // segment: the next segment's prep follows this one's gradients on main,
+    // and they follow both scans.
+    for (int i = n_seg - 1; i >= 0; --i) {
+        sf::GdnArgs &a = seg[i];
+        if (a.n_super > 1) {
+            TRY(gdn_launch(sf::GDN_PREP, a, r.D, mn));
+            TRY(dep(mn, ax, e0));
+            TRY(gdn_launch(sf::GDN_SCAN, a, r.D, ax));
+            if (ax != mn) TRY(record(sd[0], ax));
+            TRY(gdn_launch(sf::GDN_DPREP, a, r.D, mn));
+            TRY(dep(mn, ax, e1));  // dS prep, and dS_out written by the later segment's dS walk
+            TRY(gdn_launch(sf::GDN_DSCAN, a, r.D, ax));
+            if (ax != mn) {
+                TRY(record(sd[1], ax));
+                TRY(wait(mn, sd[0]));
+            }
+        }
+        TRY(gdn_launch(sf::GDN_STORE, a, r.D, mn));
+        if (a.n_super > 1 && ax != mn) TRY(wait(mn, sd[1]));
+        TRY(gdn_launch(sf::GDN_DWALK, a, r.D, mn));
+        TRY(gdn_launch(sf::GDN_DCHUNK, a, r.D, mn));
     }
     return SF_OK;
 }

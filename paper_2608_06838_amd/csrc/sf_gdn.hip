@@ -432,7 +432,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         }
     }
     // prep: M_J, N_J; walk: S_out after the last superchunk
-    if (PREP || (OUTP && J == a.n_super - 1)) {
+    if (PREP || (OUTP && J == a.n_super - 1 && !(a.scan_out && a.n_super > 1))) {
 #pragma unroll
         for (int m = 0; m < NS; ++m) {
             float *dst = PREP ? (m == 0 ? a.wsM : a.wsN) + (int64_t)item * SS : a.S_out + bh * SS;
@@ -445,7 +445,8 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
 }
 
 // S_{J+1} = M_J S_J + N_J for J = 0 .. n_super - 2 in fp32, S_0 = S_in (or 0);
-// writes S_J (J < n_super) to wsS.  Workgroup (b, h, 16-column block); thread
+// writes S_J (J < n_super) to wsS; with scan_out (maps of every superchunk)
+// one more step gives S_out.  Workgroup (b, h, 16-column block); thread
 // row k = tid % D owns CPT consecutive columns of the block.  M_J is staged
 // in LDS (row pitch D + 4 floats) with the next one prefetched in registers.
 template <int D>
@@ -469,14 +470,20 @@ __global__ void __launch_bounds__(256) k_gdn_scan(GdnArgs a) {
 #pragma unroll
         for (int i = 0; i < MV; ++i) mreg[i] = m[tid + NT * i];
     };
-    if (nJ > 1) fetch(0);
-    for (int J = 0;; ++J) {
+    const int last = a.scan_out ? nJ : nJ - 1;  // steps taken
+    // S_J and S_out go out through buffer stores (32-bit lane offsets)
+    constexpr int NV = CPT / 4;
+    const rsrc_t rS = buf_rsrc(wsS, (uint32_t)(nJ * SS * 4));
+    const uint32_t vo = (uint32_t)(((int64_t)k * D + col0) * 4);
+    if (last > 0) fetch(0);
+    for (int J = 0; J < nJ; ++J) {
 #pragma unroll
-        for (int j = 0; j < CPT; ++j) {
-            sS[k * 16 + col0 % 16 + j] = acc[j];
-            wsS[(int64_t)J * SS + (int64_t)k * D + col0 + j] = acc[j];
+        for (int u = 0; u < NV; ++u) {
+            const f32x4 x = {acc[4 * u], acc[4 * u + 1], acc[4 * u + 2], acc[4 * u + 3]};
+            *reinterpret_cast<f32x4 *>(&sS[k * 16 + col0 % 16 + 4 * u]) = x;
+            buf_st(rS, vo + 16 * u, (uint32_t)(J * SS * 4), x);
         }
-        if (J == nJ - 1) break;
+        if (J == last) break;
         float nv[CPT];
 #pragma unroll
         for (int j = 0; j < CPT; ++j) nv[j] = wsN[(int64_t)J * SS + (int64_t)k * D + col0 + j];
@@ -486,7 +493,7 @@ __global__ void __launch_bounds__(256) k_gdn_scan(GdnArgs a) {
             *reinterpret_cast<f32x4 *>(&sM[(e / D) * LDM + e % D]) = mreg[i];
         }
         __syncthreads();
-        if (J + 2 < nJ) fetch(J + 1);
+        if (J + 1 < last) fetch(J + 1);
 #pragma unroll
         for (int j = 0; j < CPT; ++j) acc[j] = nv[j];
 #pragma unroll 4
@@ -498,6 +505,12 @@ __global__ void __launch_bounds__(256) k_gdn_scan(GdnArgs a) {
                 for (int j = 0; j < CPT; ++j) acc[j] = fmaf(m4[u], sS[(c + u) * 16 + col0 % 16 + j], acc[j]);
         }
         __syncthreads();  // every read of sM and sS is done
+    }
+    if (a.scan_out) {  // the state after the last superchunk
+        const rsrc_t rO = buf_rsrc(a.S_out + bh * SS, (uint32_t)(SS * 4));
+#pragma unroll
+        for (int u = 0; u < NV; ++u)
+            buf_st(rO, vo + 16 * u, 0u, f32x4{acc[4 * u], acc[4 * u + 1], acc[4 * u + 2], acc[4 * u + 3]});
     }
 }
 
@@ -1291,57 +1304,97 @@ __global__ void __launch_bounds__(512) k_gdn_dchunk(GdnArgs a) {
 }
 
 template <int D>
-hipError_t gdn_fwd_d(const GdnArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+hipError_t gdn_phase_d(int phase, const GdnArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     const unsigned bh = (unsigned)(a.B * a.H);
-    if (a.n_super > 1) {
-        hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, W_PREP>), dim3(bh * a.n_prep), dim3(64 * D / 16), 0, s,
-                              e0, nullptr, 0, a);
-        hipExtLaunchKernelGGL((k_gdn_scan<D>), dim3(bh * (D / 16)), dim3(256), 0, s, nullptr, nullptr, 0, a);
+    const dim3 wblk(64 * D / 16);
+    switch (phase) {
+    case GDN_PREP:
+        hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, W_PREP>), dim3(bh * a.n_prep), wblk, 0, s, e0, e1, 0, a);
+        break;
+    case GDN_SCAN: hipExtLaunchKernelGGL((k_gdn_scan<D>), dim3(bh * (D / 16)), dim3(256), 0, s, e0, e1, 0, a); break;
+    case GDN_OUT:
+        hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, W_OUT>), dim3(bh * a.n_super), wblk, 0, s, e0, e1, 0, a);
+        break;
+    case GDN_STORE:
+        hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, W_STORE>), dim3(bh * a.n_super), wblk, 0, s, e0, e1, 0, a);
+        break;
+    case GDN_DPREP:
+        hipExtLaunchKernelGGL((k_gdn_dwalk<__bf16, D, true>), dim3(bh * (a.n_super - 1)), wblk, 0, s, e0, e1, 0, a);
+        break;
+    case GDN_DSCAN: hipExtLaunchKernelGGL((k_gdn_dscan<D>), dim3(bh * (D / 16)), dim3(256), 0, s, e0, e1, 0, a); break;
+    case GDN_DWALK:
+        hipExtLaunchKernelGGL((k_gdn_dwalk<__bf16, D, false>), dim3(bh * a.n_super), wblk, 0, s, e0, e1, 0, a);
+        break;
+    case GDN_DCHUNK: {
+        const int64_t items = (int64_t)bh * (a.L / C);
+        if (items > 0)
+            hipExtLaunchKernelGGL((k_gdn_dchunk<__bf16, D>), dim3((unsigned)std::min<int64_t>(items, a.n_x)),
+                                  dim3(512), 0, s, e0, e1, 0, a);
+        break;
     }
-    hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, W_OUT>), dim3(bh * a.n_super), dim3(64 * D / 16), 0, s,
-                          a.n_super > 1 ? nullptr : e0, e1, 0, a);
-    return hipGetLastError();
-}
-
-template <int D>
-hipError_t gdn_bwd_d(const GdnArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-    const unsigned bh = (unsigned)(a.B * a.H);
-    const int64_t items = (int64_t)bh * (a.L / C);
-    if (a.n_super > 1) {
-        hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, W_PREP>), dim3(bh * a.n_prep), dim3(64 * D / 16), 0, s, e0,
-                              nullptr, 0, a);
-        hipExtLaunchKernelGGL((k_gdn_scan<D>), dim3(bh * (D / 16)), dim3(256), 0, s, nullptr, nullptr, 0, a);
-        hipExtLaunchKernelGGL((k_gdn_dwalk<__bf16, D, true>), dim3(bh * (a.n_super - 1)), dim3(64 * D / 16), 0, s,
-                              nullptr, nullptr, 0, a);
-        hipExtLaunchKernelGGL((k_gdn_dscan<D>), dim3(bh * (D / 16)), dim3(256), 0, s, nullptr, nullptr, 0, a);
+    default: return hipErrorInvalidValue;
     }
-    hipExtLaunchKernelGGL((k_gdn_walk<__bf16, D, W_STORE>), dim3(bh * a.n_super), dim3(64 * D / 16), 0, s,
-                          a.n_super > 1 ? nullptr : e0, nullptr, 0, a);
-    hipExtLaunchKernelGGL((k_gdn_dwalk<__bf16, D, false>), dim3(bh * a.n_super), dim3(64 * D / 16), 0, s, nullptr,
-                          items > 0 ? nullptr : e1, 0, a);
-    if (items > 0)
-        hipExtLaunchKernelGGL((k_gdn_dchunk<__bf16, D>), dim3((unsigned)std::min<int64_t>(items, a.n_x)), dim3(512), 0,
-                              s, nullptr, e1, 0, a);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_gdn_bwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-    if (a.n_super < 1 || !a.wsSc || !a.wsDc || !a.wsX || a.n_x < 1 ||
-        (a.n_super > 1 && (!a.wsS || !a.wsM || !a.wsN || !a.wsE || !a.wsDe || a.n_prep != a.n_super)))
-        return hipErrorInvalidValue;
-    if (D == 128) return gdn_bwd_d<128>(a, s, e0, e1);
-    if (D == 64) return gdn_bwd_d<64>(a, s, e0, e1);
+// Argument checks shared by every phase: the superchunk buffers a phase reads
+// or writes must be there.
+hipError_t launch_gdn_phase(int phase, const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    if (a.n_super < 1) return hipErrorInvalidValue;
+    const bool multi = a.n_super > 1;
+    switch (phase) {
+    case GDN_PREP:
+    case GDN_SCAN:
+        if (!multi || !a.wsS || !a.wsM || !a.wsN || a.n_prep < a.n_super - 1) return hipErrorInvalidValue;
+        if (a.scan_out && (a.n_prep != a.n_super || !a.S_out)) return hipErrorInvalidValue;
+        break;
+    case GDN_DPREP:
+    case GDN_DSCAN:
+        if (!multi || !a.wsM || !a.wsE || !a.wsDe || a.n_prep != a.n_super) return hipErrorInvalidValue;
+        break;
+    case GDN_OUT:
+        if (multi && !a.wsS) return hipErrorInvalidValue;
+        break;
+    case GDN_STORE:
+        if (!a.wsSc || (multi && !a.wsS)) return hipErrorInvalidValue;
+        break;
+    case GDN_DWALK:
+        if (!a.wsDc || (multi && !a.wsDe)) return hipErrorInvalidValue;
+        break;
+    case GDN_DCHUNK:
+        if (!a.wsSc || !a.wsDc || !a.wsX || a.n_x < 1) return hipErrorInvalidValue;
+        break;
+    default: return hipErrorInvalidValue;
+    }
+    if (D == 128) return gdn_phase_d<128>(phase, a, s, e0, e1);
+    if (D == 64) return gdn_phase_d<64>(phase, a, s, e0, e1);
     return hipErrorInvalidValue;
 }
 
+hipError_t launch_gdn_bwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+    if (a.n_super > 1 && a.n_prep != a.n_super) return hipErrorInvalidValue;
+    hipError_t e = hipSuccess;
+    const bool multi = a.n_super > 1;
+    const int seq[] = {GDN_PREP, GDN_SCAN, GDN_DPREP, GDN_DSCAN, GDN_STORE, GDN_DWALK, GDN_DCHUNK};
+    bool first = true;
+    for (int ph : seq) {
+        if (!multi && (ph == GDN_PREP || ph == GDN_SCAN || ph == GDN_DPREP || ph == GDN_DSCAN)) continue;
+        const bool last = ph == GDN_DCHUNK;
+        if ((e = launch_gdn_phase(ph, a, D, s, first ? e0 : nullptr, last ? e1 : nullptr)) != hipSuccess) return e;
+        first = false;
+    }
+    return e;
+}
+
 hipError_t launch_gdn_fwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-    if (a.n_super < 1 || (a.n_super > 1 && (!a.wsS || !a.wsM || !a.wsN || a.n_prep < a.n_super - 1)))
-        return hipErrorInvalidValue;
-    if (D == 128) return gdn_fwd_d<128>(a, s, e0, e1);
-    if (D == 64) return gdn_fwd_d<64>(a, s, e0, e1);
-    return hipErrorInvalidValue;
+    hipError_t e = hipSuccess;
+    if (a.n_super > 1) {
+        if ((e = launch_gdn_phase(GDN_PREP, a, D, s, e0, nullptr)) != hipSuccess) return e;
+        if ((e = launch_gdn_phase(GDN_SCAN, a, D, s, nullptr, nullptr)) != hipSuccess) return e;
+    }
+    return launch_gdn_phase(GDN_OUT, a, D, s, a.n_super > 1 ? nullptr : e0, e1);
 }
 
 }  // namespace sf

@@ -84,8 +84,14 @@ struct GdnArgs {
     float *wsDc;        // dS' of every chunk [B*H][L/64][D][D]
     float *wsX;         // per-chunk gradient kernel scratch: n_x slabs of 8 x 64 x D floats
     int32_t B, H, n_super, ts, n_prep, n_x;
+    int32_t scan_out;  // forward chains: maps of every superchunk, the scan writes S_out
     int64_t L, sx_b, sx_l, sx_h, sg_b, sg_l, sg_h;
 };
+// One kernel of the delta-rule pipeline: forward prep ([M|N] maps of the
+// superchunks), scan (S_J), output walk; backward state-storing walk, dS prep
+// (E_J), dS scan (dS_end(J)), dS walk, per-chunk gradients.
+enum GdnPhase { GDN_PREP, GDN_SCAN, GDN_OUT, GDN_STORE, GDN_DPREP, GDN_DSCAN, GDN_DWALK, GDN_DCHUNK };
+hipError_t launch_gdn_phase(int phase, const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_gdn_fwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_gdn_bwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_conv(bool bwd, const ConvArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1);

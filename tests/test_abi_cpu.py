@@ -267,3 +267,31 @@ def test_gdn_bwd_validation():
     slabs = min(2 * nc, 1024) * 8 * 64 * 128 * 4
     assert need == 2 * SS * (4 * n + (n - 1)) + 2 * (2 * nc * SS) + slabs
     assert call(s, tun=_tuning(ts=256), ws_bytes=need - 1) == _lib.SF_E_WORKSPACE
+
+
+def test_gdn_chain_validation():
+    L = _lib.lib()
+    segs = (ctypes.c_int64 * 3)(256, 512, 256)
+
+    def fwd(s, n=3, sl=segs, q=1, k=2, v=3, g=4, beta=5, o=6, S_bnd=7, v_new=None, ws=8, ws_bytes=1 << 40):
+        args = [p(i) if i is not None else None for i in (q, k, v, g, beta, o, S_bnd, v_new, ws)]
+        return L.sf_gdn_chain_fwd(ctypes.byref(s), n, sl, *args, ws_bytes, None, None, None)
+
+    def bwd(s, n=3, sl=segs, dq=9, dS_init=14, ws=15):
+        args = [p(i) if i is not None else None for i in (1, 2, 3, 4, 5, 7, 6, None, dq, 10, 11, 12, 13, dS_init, ws)]
+        return L.sf_gdn_chain_bwd(ctypes.byref(s), n, sl, *args, 1 << 40, None, None, None)
+
+    s = shape(L=1024)
+    assert fwd(s, n=0) == _lib.SF_E_SHAPE
+    assert fwd(shape(L=1000)) == _lib.SF_E_SHAPE
+    assert fwd(s, sl=(ctypes.c_int64 * 3)(256, 500, 268)) == _lib.SF_E_SHAPE   # not multiples of 64
+    assert fwd(s, sl=(ctypes.c_int64 * 3)(256, 512, 128)) == _lib.SF_E_SHAPE   # sum != L
+    assert fwd(s, beta=None) == _lib.SF_E_NULL
+    assert fwd(s, o=1) == _lib.SF_E_ALIAS
+    assert fwd(s, ws_bytes=16) == _lib.SF_E_WORKSPACE
+    assert fwd(shape(L=1024, gate=_lib.SF_GATE_VECTOR)) == _lib.SF_E_UNSUPPORTED
+    assert bwd(s, dq=2) == _lib.SF_E_ALIAS
+    assert bwd(s, dS_init=None) == _lib.SF_E_NULL
+    need = L.sf_gdn_chain_workspace_bytes(ctypes.byref(s), 3, segs, None)
+    assert need > 0
+    assert L.sf_gdn_chain_workspace_bytes(ctypes.byref(s), 3, (ctypes.c_int64 * 3)(256, 512, 128), None) == 0

@@ -1,0 +1,76 @@
+"""The gfx950 assembly of every kernel source (built here with hipcc) has no
+store whose address registers overlap its data registers.
+
+A store such as `global_store_dwordx4 v[4:5], v[2:5]` writes part of its own
+address as data.  One loop shape of the delta-rule state scan was compiled
+into exactly that; the sources avoid it (buffer stores with 32-bit offsets
+there), and this test keeps it from coming back.  CPU only; skipped without
+hipcc.
+"""
+import concurrent.futures
+import os
+import re
+import shutil
+import subprocess
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2608_06838_amd", "csrc")
+HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+SOURCES = ["sf_kernels.hip", "sf_kernels_vg.hip", "sf_conv.hip", "sf_gdn.hip"]
+R = r"(v\[\d+:\d+\]|v\d+)"
+PATTERNS = ((re.compile(r"\s+(?:global|flat)_store_\w+\s+" + R + r",\s*" + R), 1, 2),
+            (re.compile(r"\s+buffer_store_\w+\s+" + R + r",\s*" + R), 2, 1),
+            (re.compile(r"\s+ds_write\w*\s+" + R + r",\s*" + R), 1, 2))
+
+
+def regs(s):
+    m = re.match(r"v\[(\d+):(\d+)\]", s)
+    if m:
+        return set(range(int(m.group(1)), int(m.group(2)) + 1))
+    m = re.match(r"v(\d+)$", s)
+    return {int(m.group(1))} if m else set()
+
+
+def overlapping_stores(asm_text):
+    bad, n, fn = [], 0, None
+    for line in asm_text.splitlines():
+        if re.match(r"^_Z\w+:", line):
+            fn = line.strip()[:-1]
+        for pat, ai, di in PATTERNS:
+            m = pat.match(line)
+            if m:
+                n += 1
+                if regs(m.group(ai)) & regs(m.group(di)):
+                    bad.append((fn, line.strip()))
+    return n, bad
+
+
+def test_overlap_detector():
+    n, bad = overlapping_stores("\tglobal_store_dwordx4 v[4:5], v[2:5], off\n\tglobal_store_dwordx4 v[6:7], v[2:5], off\n"
+                                "\tbuffer_store_dwordx4 v[2:5], v3, s[0:3], 0 offen\n\tds_write_b128 v1, v[2:5]\n")
+    assert n == 4 and len(bad) == 2
+
+
+@pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not available")
+def test_no_store_overlaps_its_address():
+    tmp = tempfile.mkdtemp()
+
+    def build(src):
+        out = os.path.join(tmp, src + ".s")
+        subprocess.run([HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "--cuda-device-only", "-S",
+                        "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"),
+                        "-I", CSRC, os.path.join(CSRC, src), "-o", out], check=True, capture_output=True)
+        with open(out) as f:
+            return src, overlapping_stores(f.read())
+
+    try:
+        with concurrent.futures.ThreadPoolExecutor(max_workers=4) as ex:
+            results = list(ex.map(build, SOURCES))
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+    for src, (n, bad) in results:
+        assert n > 100, f"{src}: too few stores parsed ({n})"
+        assert not bad, f"{src}: {bad[:3]}"

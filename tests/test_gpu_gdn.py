@@ -264,3 +264,39 @@ def test_gdn_full_size_segment_sampled():
     assert_close("S_out", to64(S[:, heads]), rS, "bf16")
     sub = [x[:, :, heads] for x in grads[:5]] + [grads[5][:, heads]]
     check_bwd(sub, ref_bwd(cpu, dO[:, :, heads].cpu(), dS_out[:, heads].cpu()))
+
+
+@pytest.mark.parametrize("ts", [0, 128])
+def test_gdn_chain_entry_points(ts):
+    """sf_gdn_chain_fwd / sf_gdn_chain_bwd over nonuniform segments (one of
+    them a single superchunk when ts = 128): forward, V^new and every gradient
+    against the oracle over the whole sequence; the scans overlapped on an aux
+    stream give bitwise the same results as serialised on one stream."""
+    B, H, D = 1, 3, 128
+    segs = [256, 64, 384, 192]
+    say(f"[gdn chain] segs={segs} ts={ts}")
+    inp = synth.make_gdn_inputs(B, sum(segs), H, D, seed=5300 + ts)
+    dO, dS_final = grads_inputs(inp, 5301 + ts)
+    g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
+    args = (g["q"], g["k"], g["v"], g["g"], g["beta"], segs)
+    res = {}
+    for ov in (True, False):
+        o, S_bnd, vn = sf.gdn_chain_fwd(*args, g["S_in"], ts=ts, overlap=ov, with_v_new=True)
+        grads = sf.gdn_chain_bwd(*args, S_bnd, dO.to(DEV), dS_final.to(DEV), ts=ts, overlap=ov)
+        torch.cuda.synchronize()
+        res[ov] = (o, S_bnd, vn) + tuple(grads)
+    for x, y in zip(res[True], res[False]):
+        assert torch.equal(x, y)
+    o, S_bnd, vn = res[True][:3]
+    ro, rS, ru = gdn.forward(*(to64(inp[x]) for x in ("q", "k", "v", "g", "beta", "S_in")), threads=cores(),
+                             with_u=True)
+    assert_close("o", to64(o), ro, "bf16")
+    assert_close("v_new", to64(vn), ru, "bf16")
+    assert_close("S_out", to64(S_bnd[-1]), rS, "bf16")
+    t = 0
+    for i, n in enumerate(segs[:-1]):  # interior boundary states
+        t += n
+        _, Si = gdn.forward(*(to64(inp[x][:, :t]) for x in ("q", "k", "v", "g", "beta")), to64(inp["S_in"]),
+                            threads=cores())
+        assert_close(f"S_bnd{i + 1}", to64(S_bnd[i + 1]), Si, "bf16")
+    check_bwd(res[True][3:], ref_bwd(inp, dO, dS_final))
