@@ -335,7 +335,8 @@ def bench_gdn(args):
     """One step = the gated-delta-rule forward over the 8 segments of the
     256K-context layer, the state carried from segment to segment, then the
     backward over the segments in reverse, the state gradient carried back
-    (random bf16 dO, no loss term on the final state)."""
+    (random bf16 dO, no loss term on the final state), through the chain entry
+    points (state scans overlapped on a second stream unless --gdn-serial)."""
     import torch
     import paper_2608_06838_amd as sf
     from paper_2608_06838_amd import synth
@@ -347,59 +348,56 @@ def bench_gdn(args):
     inp = synth.make_gdn_inputs(B, L, H, D, device=dev, seed=4002)
     gen = torch.Generator(device=dev).manual_seed(4003)
     dO = torch.randn((B, L, H, D), device=dev, generator=gen).to(torch.bfloat16)
-    starts = [sum(seg[:i]) for i in range(len(seg))]
-    sl = lambda x, t, n: x[:, t:t + n]
+    x = (inp["q"], inp["k"], inp["v"], inp["g"], inp["beta"], seg)
+    ov = not args.gdn_serial
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
 
-    def step():
-        S, bounds = inp["S_in"], []
-        for t, n in zip(starts, seg):
-            bounds.append(S)
-            _, S = sf.gdn_fwd(sl(inp["q"], t, n), sl(inp["k"], t, n), sl(inp["v"], t, n), sl(inp["g"], t, n),
-                              sl(inp["beta"], t, n), S, ts=args.gdn_ts)
-        dS = None
-        for t, n, S0 in reversed(list(zip(starts, seg, bounds))):
-            *_, dS = sf.gdn_bwd(sl(inp["q"], t, n), sl(inp["k"], t, n), sl(inp["v"], t, n), sl(inp["g"], t, n),
-                                sl(inp["beta"], t, n), S0, sl(dO, t, n), dS, ts=args.gdn_ts)
+    def step(t=None):
+        if t is not None:
+            ev[0].record()
+        _, S_bnd = sf.gdn_chain_fwd(*x, inp["S_in"], ts=args.gdn_ts, overlap=ov)
+        if t is not None:
+            ev[1].record()
+        sf.gdn_chain_bwd(*x, S_bnd, dO, None, ts=args.gdn_ts, overlap=ov)
+        if t is not None:
+            ev[2].record()
+            torch.cuda.synchronize()
+            t[0] += ev[0].elapsed_time(ev[1])
+            t[1] += ev[1].elapsed_time(ev[2])
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    for kn in ("gdn_fwd", "gdn_bwd"):
-        sf.prof_read(kn)
-        sf.prof_enable(kn, True)
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    prof = {}
-    for kn in ("gdn_fwd", "gdn_bwd"):
-        sf.prof_enable(kn, False)
-        prof[kn] = sf.prof_read(kn)
+    tt = [0.0, 0.0]
+    for _ in range(args.steps):  # per-call split, from events on the main stream
+        step(tt)
     ms = (t1 - t0) * 1e3 / args.steps
     io = 2
     # algorithmic HBM bytes per (token, head): fwd q, k, v in, o out, g, beta;
     # bwd q, k, v, dO in, dq, dk, dv out, g, beta in, dg, dbeta out
     per_tok = {"gdn_fwd": 4 * D * io + 8, "gdn_bwd": 7 * D * io + 16}
     calls = {}
-    for kn, (tot_ms, nl) in prof.items():
-        avg_s = tot_ms / 1e3 / max(nl, 1)
-        ach = per_tok[kn] * B * H * L * args.steps / max(nl, 1) / avg_s / 1e9
-        calls[kn] = {"ms_per_step": tot_ms / args.steps, "launches": nl, "avg_launch_us": avg_s * 1e6,
-                     "achieved_GBps": ach}
+    for kn, tot in zip(("gdn_fwd", "gdn_bwd"), tt):
+        avg_s = tot / 1e3 / args.steps
+        calls[kn] = {"ms_per_step": tot / args.steps, "achieved_GBps": per_tok[kn] * B * H * L / avg_s / 1e9}
     dom = max(calls, key=lambda kn: calls[kn]["ms_per_step"])
     out = {
         "metric": GDN_METRIC, "value": B * L / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "gdn_ctx256k_h40", "B": B, "H": H, "Dk": D, "Dv": D, "L": L, "segments": seg,
-                   "ts": args.gdn_ts or "auto",
+                   "ts": args.gdn_ts or "auto", "overlap": ov,
                    "parallelism": "superchunks: [M|N] prep walk, fp32 state scan, output walk; backward: "
                                   "state-gradient walk over superchunks, per-chunk gradients over all chunks"},
         "calls": calls,
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": calls[dom]["achieved_GBps"], "peak": PEAK_HBM / 1e9,
                      "unit": "GB/s", "frac": calls[dom]["achieved_GBps"] * 1e9 / PEAK_HBM, "traffic": None,
-                     "launches": calls[dom]["launches"], "avg_launch_us": calls[dom]["avg_launch_us"]},
+                     "avg_call_ms": calls[dom]["ms_per_step"]},
     }
     if not args.no_cpu_baseline:
         from oracle import gdn as ogdn
@@ -435,6 +433,7 @@ def main():
                     help="measure the short convolution with carried tails instead of the recurrence")
     ap.add_argument("--gdn", action="store_true", help="measure the gated-delta-rule forward instead")
     ap.add_argument("--gdn-ts", type=int, default=0, help="gated delta rule superchunk length (0: automatic)")
+    ap.add_argument("--gdn-serial", action="store_true", help="gated delta rule: state scans on the main stream")
     ap.add_argument("--tune-ts", action="store_true",
                     help="time the chain for each superchunk stride and overlap setting (one JSON table)")
     ap.add_argument("--partition-study", action="store_true",
