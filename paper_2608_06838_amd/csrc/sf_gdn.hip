@@ -8,7 +8,7 @@
 // Chunkwise form (per chunk of C tokens, S the state entering it, b_t the
 // chunk-local inclusive cumulative log-decay, gamma_t = e^{b_t}):
 //   A[t][s]  = beta_t e^{b_t - b_s} (k_t . k_s)      for s < t   (strictly lower)
-//   (I + A) [W | Ubar] = [diag(beta gamma) K | diag(beta) V]     (forward substitution)
+//   (I + A) [W | Ubar] = [diag(beta gamma) K | diag(beta) V]     (T = (I + A)^{-1} by blocks, then T R)
 //   U        = Ubar - W S                                          (the corrected values, V^new)
 //   O        = diag(gamma) Q S + (Q K^T o Gamma) U,  Gamma[t][s] = e^{b_t - b_s} (s <= t)
 //   S_next   = gamma_C S + (K o e^{b_C - b})^T U
@@ -808,13 +808,13 @@ __global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
 // Parameter gradients of one chunk per item (b, h, chunk), items in a
 // grid-stride loop.  Every product runs on MFMA: 8 waves, wave w owns rows
 // [16 (w % 4), +16) and half the column tiles (half w / 4) of each 64-row
-// result, so two waves share each SIMD.  Operands enter as bf16 fragments, computed fp32 operands as hi/lo
-// pairs (three products, the lo x lo term dropped), q, k, v, dO exactly.
-// q, k, v, dO and the 64 x 64 matrices sit in LDS; the 64 x D intermediates
-// in a per-workgroup scratch slab of wsX (eight 64 x D fp32 matrices, L2
-// resident, addressed through one buffer resource); S and dS' come from the
-// stored per-chunk states.  The triangular inverse T = (I + A)^{-1} is a
-// per-column forward substitution in fp32.
+// result, so two waves share each SIMD.  Operands enter as bf16 fragments,
+// computed fp32 operands as hi/lo pairs (three products, the lo x lo term
+// dropped), q, k, v, dO exactly.  q, k, v, dO and the 64 x 64 matrices sit in
+// LDS; the 64 x D intermediates in a per-workgroup scratch slab of wsX (eight
+// 64 x D fp32 matrices, addressed through one buffer resource); S and dS' come
+// from the stored per-chunk states.  T = (I + A)^{-1} comes from gdn_tinv
+// with beta applied per row.
 template <typename T, int D>
 __global__ void __launch_bounds__(512) k_gdn_dchunk(GdnArgs a) {
     constexpr int LDX = D + 8, LD6 = C + 4, NT2 = D / 32, NTH = 512;
