@@ -266,17 +266,17 @@ def test_gdn_full_size_segment_sampled():
     check_bwd(sub, ref_bwd(cpu, dO[:, :, heads].cpu(), dS_out[:, heads].cpu()))
 
 
-@pytest.mark.parametrize("ts", [0, 128])
-def test_gdn_chain_entry_points(ts):
+@pytest.mark.parametrize("D,ts", [(128, 0), (128, 128), (64, 0)])
+def test_gdn_chain_entry_points(D, ts):
     """sf_gdn_chain_fwd / sf_gdn_chain_bwd over nonuniform segments (one of
     them a single superchunk when ts = 128): forward, V^new and every gradient
     against the oracle over the whole sequence; the scans overlapped on an aux
     stream give bitwise the same results as serialised on one stream."""
-    B, H, D = 1, 3, 128
+    B, H = 1, 3
     segs = [256, 64, 384, 192]
-    say(f"[gdn chain] segs={segs} ts={ts}")
-    inp = synth.make_gdn_inputs(B, sum(segs), H, D, seed=5300 + ts)
-    dO, dS_final = grads_inputs(inp, 5301 + ts)
+    say(f"[gdn chain] D={D} segs={segs} ts={ts}")
+    inp = synth.make_gdn_inputs(B, sum(segs), H, D, seed=5300 + ts + D)
+    dO, dS_final = grads_inputs(inp, 5301 + ts + D)
     g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
     args = (g["q"], g["k"], g["v"], g["g"], g["beta"], segs)
     res = {}
