@@ -871,6 +871,8 @@ sf_status sf_conv_bwd(const sf_conv_shape *shape, const void *x, const float *w,
     return conv_run(SF_K_CONV_BWD, true, a, (hipStream_t)stream);
 }
 
+}  // extern "C"
+
 namespace {
 
 // Gated delta rule: superchunk length.  One walk workgroup fills a CU (its
@@ -1019,6 +1021,8 @@ GdnChainWs gdn_chain_ws(const Shape &r, const GdnPlan &p) {
 }
 
 }  // namespace
+
+extern "C" {
 
 size_t sf_gdn_fwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning) {
     Shape r;
