@@ -859,6 +859,15 @@ __global__ void __launch_bounds__(512) k_gdn_dchunk(GdnArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) buf_st<float>(rs, v_acc + r * D * 4, base + (uint32_t)((r0 * D + 16 * ct) * 4), c[r]);
     };
+    // the same at an explicit row base (row tile rt: rows 16 rt + 4 q4 + r)
+    auto g_acc_ld_rt = [&](rsrc_t rs, uint32_t base, int rt, int ct, f32x4 &c) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) c[r] = buf_ld<float>(rs, v_acc + r * D * 4, base + (uint32_t)((16 * rt * D + 16 * ct) * 4));
+    };
+    auto g_acc_st_rt = [&](rsrc_t rs, uint32_t base, int rt, int ct, const f32x4 &c) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) buf_st<float>(rs, v_acc + r * D * 4, base + (uint32_t)((16 * rt * D + 16 * ct) * 4), c[r]);
+    };
     auto l_rm = [&](const float *M, int rr, int kk, frag_t<T> &h, frag_t<T> &l) {  // LDS 64 x 64, M[row][k]
         const float *p = M + (rr + n16) * LD6 + kk + 8 * q4;
         const f32x4 x0 = *reinterpret_cast<const f32x4 *>(p), x1 = *reinterpret_cast<const f32x4 *>(p + 4);
@@ -985,49 +994,73 @@ __global__ void __launch_bounds__(512) k_gdn_dchunk(GdnArgs a) {
             }
         }
         __syncthreads();
-        // U = Ubar - W S;  dU = diag(e^{b_C - b}) K dS' + P^T dO
+        // U = Ubar - W S;  dU = diag(e^{b_C - b}) K dS' + P^T dO.  Here wave w
+        // owns row tiles 2 (w % 2) + i (i < 2) and column tiles CT (w / 2) + j
+        // (j < CT), so no two waves load the same S or dS' fragment.
         {
-            f32x4 cu[NT2], cd[NT2];
+            constexpr int CT = NT2 / 2 > 0 ? NT2 / 2 : 1;
+            static_assert(2 * CT * 8 == 4 * (D / 16), "eight waves cover the 4 x D/16 tiles once");
+            const int rp = w & 1, cg = w >> 1;
+            f32x4 cu[2][CT], cd[2][CT];
 #pragma unroll
-            for (int nt = 0; nt < NT2; ++nt) g_acc_ld(rX, mUb, NT2 * hf + nt, cu[nt]);
-            zeroN(cd);
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < CT; ++j) {
+                    g_acc_ld_rt(rX, mUb, 2 * rp + i, CT * cg + j, cu[i][j]);
+                    cd[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+                }
 #pragma unroll 1
             for (int kk = 0; kk < D; kk += 32) {
-                frag_t<T> wh, wl;
-                g_rm(rX, mW, r0, kk, wh, wl);
-                wh = -wh;
-                wl = -wl;
-                const frag_t<T> ak = x_rm(xk, r0, kk);
+                frag_t<T> wh[2], wl[2], ak[2];
 #pragma unroll
-                for (int nt = 0; nt < NT2; ++nt) {
+                for (int i = 0; i < 2; ++i) {
+                    g_rm(rX, mW, 16 * (2 * rp + i), kk, wh[i], wl[i]);
+                    wh[i] = -wh[i];
+                    wl[i] = -wl[i];
+                    ak[i] = x_rm(xk, 16 * (2 * rp + i), kk);
+                }
+#pragma unroll
+                for (int j = 0; j < CT; ++j) {
                     frag_t<T> sh, sl;
-                    g_tr(rS, 0, 16 * (NT2 * hf + nt), kk, sh, sl);
-                    mma3(cu[nt], wh, wl, sh, sl);
-                    g_tr(rD, 0, 16 * (NT2 * hf + nt), kk, sh, sl);
-                    mma(cd[nt], ak, sh);
-                    mma(cd[nt], ak, sl);
+                    g_tr(rS, 0, 16 * (CT * cg + j), kk, sh, sl);
+#pragma unroll
+                    for (int i = 0; i < 2; ++i) mma3(cu[i][j], wh[i], wl[i], sh, sl);
+                    g_tr(rD, 0, 16 * (CT * cg + j), kk, sh, sl);
+#pragma unroll
+                    for (int i = 0; i < 2; ++i) {
+                        mma(cd[i][j], ak[i], sh);
+                        mma(cd[i][j], ak[i], sl);
+                    }
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < NT2; ++nt)
+            for (int i = 0; i < 2; ++i)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) cd[nt][r] *= se[r0 + 4 * q4 + r];
+                for (int j = 0; j < CT; ++j)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) cd[i][j][r] *= se[16 * (2 * rp + i) + 4 * q4 + r];
 #pragma unroll
             for (int kk = 0; kk < C; kk += 32) {
-                frag_t<T> ph, pl;
-                l_tr(sPt, r0, kk, ph, pl);  // P^T[t][t'] = P[t'][t]
+                frag_t<T> ph[2], pl[2];
 #pragma unroll
-                for (int nt = 0; nt < NT2; ++nt) {
-                    const frag_t<T> bo = x_tr(xo, 16 * (NT2 * hf + nt), kk);
-                    mma(cd[nt], ph, bo);
-                    mma(cd[nt], pl, bo);
+                for (int i = 0; i < 2; ++i) l_tr(sPt, 16 * (2 * rp + i), kk, ph[i], pl[i]);  // P^T[t][t'] = P[t'][t]
+#pragma unroll
+                for (int j = 0; j < CT; ++j) {
+                    const frag_t<T> bo = x_tr(xo, 16 * (CT * cg + j), kk);
+#pragma unroll
+                    for (int i = 0; i < 2; ++i) {
+                        mma(cd[i][j], ph[i], bo);
+                        mma(cd[i][j], pl[i], bo);
+                    }
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < NT2; ++nt) {
-                g_acc_st(rX, mU, NT2 * hf + nt, cu[nt]);
-                g_acc_st(rX, mdU, NT2 * hf + nt, cd[nt]);
-            }
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < CT; ++j) {
+                    g_acc_st_rt(rX, mU, 2 * rp + i, CT * cg + j, cu[i][j]);
+                    g_acc_st_rt(rX, mdU, 2 * rp + i, CT * cg + j, cd[i][j]);
+                }
         }
         __syncthreads();
         // G_U = T^T dU (dv, dbeta)
