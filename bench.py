@@ -5,6 +5,8 @@ One step = chain_fwd + chain_bwd over the whole sequence of the workload
 backward's replay, scans, dq walk and dk/dv/dg walk), inputs resident in HBM.
 Default workload: B=1, H=40, d=128, L=262144 in 8 nonuniform segments
 (the 256K-context layer of a hidden-5120 model), bf16 I/O, fp32 state.
+--workload selects the other shapes (tiny_fp32, mid_bf16, vector_gate,
+scan_stress); --conv and --gdn the short convolution and the gated delta rule.
 
 Prints one JSON line ("Measurement").
 """
@@ -18,9 +20,11 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-PEAK_BF16 = 2.5e15   # dense bf16 MFMA, FLOP/s
-PEAK_HBM = 8.0e12    # HBM3E, B/s
+PEAK_BF16 = 2.5e15    # dense bf16 MFMA, FLOP/s
+PEAK_F32_MFMA = 157.3e12  # dense fp32 matrix, FLOP/s
+PEAK_HBM = 8.0e12     # HBM3E, B/s
 METRIC = "fwd+bwd tokens/s per layer (H=40,d=128, 256K ctx); % bf16 MFMA peak"
+MALL_FLUSH_MIB = 512  # written between timed steps of workloads whose inputs are small enough to stay cached
 
 # interface bytes per token-head that each kernel must move (io = element bytes, D = head dim):
 #   fwd_prep: k, v, g            fwd_out: q, k, v, g in; o out
@@ -35,6 +39,7 @@ KERNEL_BYTES = {
     "bwd_dq": lambda D, io, gb: 5 * D * io + 2 * gb,
     "bwd_dkv": lambda D, io, gb: 6 * D * io + 3 * gb if gb == 4 else 9 * D * io + 4 * gb,
 }
+RECURRENCE_KERNELS = ["fwd_prep", "scan", "fwd_out", "bwd_prep", "bwd_dq", "bwd_dkv"]
 
 
 def alg_flops_per_token_head(D, C=64):
@@ -62,14 +67,21 @@ def kernel_src_hash():
     return _src_hash(("sf_kernels.hip", "sf_chunk.hpp", "sf_device.hpp"))
 
 
+def vg_src_hash():
+    return _src_hash(("sf_kernels_vg.hip", "sf_chunk.hpp", "sf_device.hpp"))
+
+
 def conv_src_hash():
     return _src_hash(("sf_conv.hip", "sf_device.hpp"))
 
 
-def read_traffic(kernel, workload="ctx256k_h40", src_hash=None):
+def gdn_src_hash():
+    return _src_hash(("sf_gdn.hip", "sf_device.hpp"))
+
+
+def read_traffic(kernel, workload, src_hash):
     """HBM bytes per launch for `kernel` from the committed rocprofv3 counter
     summary, or None when absent or taken on a different kernel source."""
-    src_hash = src_hash or kernel_src_hash()
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
     if not os.path.exists(path):
         return None
@@ -90,11 +102,11 @@ def read_traffic(kernel, workload="ctx256k_h40", src_hash=None):
 def cpu_baseline(w, inp, budget_s=15.0):
     """Time the fp64 oracle (fwd + bwd) on the host cores on a bounded sample of
     the same workload: the first n_h heads of batch 0 over the first L_s tokens."""
-    import numpy as np
     import oracle
 
     cores = len(os.sched_getaffinity(0))
     nh = min(w["H"], cores)
+    L = sum(w["seg_lens"])
 
     def sample(L_s):
         sl = {k: inp[k][:1, :L_s, :nh] for k in ("q", "k", "v", "g", "dO")}
@@ -102,19 +114,66 @@ def cpu_baseline(w, inp, budget_s=15.0):
 
     def run(s):
         t0 = time.perf_counter()
-        _, _, _ = oracle.forward(s["q"], s["k"], s["v"], s["g"], None, threads=nh)
+        oracle.forward(s["q"], s["k"], s["v"], s["g"], None, threads=nh)
         oracle.backward(s["q"], s["k"], s["v"], s["g"], None, s["dO"], None, threads=nh)
         return time.perf_counter() - t0
 
-    L0 = 1024
+    L0 = min(L, 1024)
     t_cal = run(sample(L0))
-    L_s = int(min(w["L"], max(L0, (budget_s / max(t_cal, 1e-6)) * L0)) // 64 * 64)
+    L_s = int(min(L, max(L0, (budget_s / max(t_cal, 1e-6)) * L0)) // 64 * 64)
     s = sample(L_s)
     t = run(s)
     value = nh * L_s / w["H"] / t  # layer tokens/s: a layer token is H token-heads
     return {"value": value, "unit": "tokens/s", "cores": nh, "kind": "oracle",
             "sample": f"batch 0, heads 0..{nh - 1}, first {L_s} tokens, fwd+bwd fp64, "
                       f"{t:.1f} s wall; value scaled to a {w['H']}-head layer"}
+
+
+class Flusher:
+    """Writes a buffer larger than the 256 MB Infinity Cache (MALL) between
+    timed steps, so that a small workload's inputs are read from HBM."""
+
+    def __init__(self, torch, dev, mib):
+        self.buf = torch.empty(mib * (1 << 20) // 4, dtype=torch.float32, device=dev) if mib > 0 else None
+
+    def __call__(self):
+        if self.buf is not None:
+            self.buf.fill_(1.0)
+
+
+def timed_steps(torch, step, steps, flush):
+    """ms per step over `steps` calls of step().  Without a flush: host clock
+    across all steps, bracketed by device synchronisations.  With one: each
+    step is bracketed by synchronisations and the flush runs outside them."""
+    if flush.buf is None:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / steps
+    tot = 0.0
+    for _ in range(steps):
+        flush()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        step()
+        torch.cuda.synchronize()
+        tot += time.perf_counter() - t0
+    return tot * 1e3 / steps
+
+
+def copy_calibration(torch, dev, mib):
+    """One plain device copy of known size (FETCH_SIZE / WRITE_SIZE
+    calibration under rocprofv3 --pmc)."""
+    if mib <= 0:
+        return
+    src = torch.ones(mib * (1 << 20) // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 CONV_METRIC = "short-conv fwd+bwd tokens/s (C=15360=3x40x128, W=4, SiLU, 256K ctx, 8 segments, carried tails)"
@@ -174,52 +233,44 @@ def bench_conv(args):
     nws = max(sf.conv_bwd_workspace_bytes(x[:, :n], wt, act) for n in seg)
     ws = torch.empty(nws, dtype=torch.uint8, device=dev)
     starts = [sum(seg[:i]) for i in range(len(seg))]
+    kernels = ["conv_fwd", "conv_bwd"]
+    timer = sf.KernelTimer(capacity=64 * max(1, args.steps))
 
-    def step():
+    def step(tm=None):
         for i, (t, n) in enumerate(zip(starts, seg)):
-            sf.conv_fwd(x[:, t:t + n], wt, tails[i], act, out=(y[:, t:t + n], tails[i + 1]))
+            sf.conv_fwd(x[:, t:t + n], wt, tails[i], act, out=(y[:, t:t + n], tails[i + 1]), timing=tm)
         for i in reversed(range(len(seg))):
             t, n = starts[i], seg[i]
             sf.conv_bwd(x[:, t:t + n], wt, tails[i], dy[:, t:t + n], dtails[i + 1], act,
-                        out=(dx[:, t:t + n], dws[i], dtails[i], ws))
+                        out=(dx[:, t:t + n], dws[i], dtails[i], ws), timing=tm)
 
-    kernels = ["conv_fwd", "conv_bwd"]
     for i in range(args.warmup):
         if i == args.warmup - 1:
             torch.cuda.synchronize()
-            for k in kernels:
-                sf.prof_read(k)
-                sf.prof_enable(k, True)
-        step()
+            timer.select(kernels)
+            step(timer)
+        else:
+            step()
     torch.cuda.synchronize()
-    wtime = {k: sf.prof_read(k) for k in kernels}
-    for k in kernels:
-        sf.prof_enable(k, False)
-    dom = max(kernels, key=lambda k: wtime[k][0]) if args.warmup > 0 else "conv_bwd"
-    sf.prof_read(dom)
-    sf.prof_enable(dom, True)
+    wtime = timer.read()
+    dom = max(kernels, key=lambda k: wtime.get(k, (0.0, 0))[0]) if wtime else "conv_bwd"
+    timer.select([dom])
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step()
+        step(timer)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    sf.prof_enable(dom, False)
-    tot_ms, nl = sf.prof_read(dom)
+    tot_ms, nl = timer.read()[dom]
     ms = (t1 - t0) * 1e3 / args.steps
-    if args.copy_mib > 0:  # known-size copy: FETCH_SIZE / WRITE_SIZE calibration under rocprofv3 --pmc
-        src = torch.ones(args.copy_mib * (1 << 20) // 4, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+    copy_calibration(torch, dev, args.copy_mib)
     avg_s = tot_ms / 1e3 / max(nl, 1)
     bytes_per_launch = CONV_BYTES[dom](io) * B * L * C * args.steps / max(nl, 1)
     achieved = bytes_per_launch / avg_s / 1e9
     if args.kernel_times:
         for k in kernels:
-            print(f"# {k:9s} {wtime[k][0]:8.3f} ms/step  {wtime[k][1]:4d} launches/step", file=sys.stderr)
+            t, n = wtime.get(k, (0.0, 0))
+            print(f"# {k:9s} {t:8.3f} ms/step  {n:4d} launches/step", file=sys.stderr)
     out = {
         "metric": CONV_METRIC, "value": B * L / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
@@ -234,11 +285,13 @@ def bench_conv(args):
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = conv_cpu_baseline(inp, w, act)
     print(json.dumps(out), flush=True)
+    timer.close()
 
 
 def make_chain_step(sf, torch, inp, seg, ts, overlap):
     """fwd+bwd chain over segments `seg` with preallocated outputs and
-    workspaces (the step allocates nothing)."""
+    workspaces (the step allocates nothing).  step(timer) times the launches
+    of the kernels the timer selects."""
     dev = inp["q"].device
     B, L, H, D = inp["q"].shape
     o = torch.empty_like(inp["q"])
@@ -250,11 +303,11 @@ def make_chain_step(sf, torch, inp, seg, ts, overlap):
     dg = torch.empty_like(inp["g"])
     dS0 = torch.empty((B, H, D, D), dtype=torch.float32, device=dev)
 
-    def step():
+    def step(tm=None, overlap=overlap):
         sf.chain_fwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, inp["S_in"], ts=ts, overlap=overlap,
-                     out=(o, S_bnd, ws_f))
+                     out=(o, S_bnd, ws_f), timing=tm)
         sf.chain_bwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, S_bnd, inp["dO"], inp["dS_out"],
-                     ts=ts, overlap=overlap, out=(dq, dk, dv, dg, dS0, ws_b))
+                     ts=ts, overlap=overlap, out=(dq, dk, dv, dg, dS0, ws_b), timing=tm)
     return step
 
 
@@ -329,6 +382,18 @@ def study_main(args):
 
 
 GDN_METRIC = "gated-delta-rule training-step (fwd+bwd) tokens/s per layer (H=40, d=128, 256K ctx, 8 segments chained through S)"
+GDN_KERNELS = ["gdn_prep", "gdn_scan", "gdn_out", "gdn_store", "gdn_dprep", "gdn_dscan", "gdn_dwalk", "gdn_dchunk"]
+
+
+def gdn_dchunk_flops(D, C=64):
+    """Algorithmic flops per 64-token chunk and head of the delta rule's
+    per-chunk parameter gradients, given the state S entering the chunk and
+    dS' leaving it (gated delta rule, for the term list):
+    dense D-contractions 10 C D^2 (U = Ubar - W S, K dS', dO S^T, dU S^T,
+    U dS'^T), strictly lower C x C products 6 C^2 D / 2 each counted as
+    C^2 D (scores, the two dP-type products, dq, dk and their mirror), the
+    triangular inverse C^3 / 3 and the two T-products 4 C^2 D."""
+    return 10 * C * D * D + 6 * C * C * D + C ** 3 // 3 + 4 * C * C * D
 
 
 def bench_gdn(args):
@@ -350,42 +415,48 @@ def bench_gdn(args):
     dO = torch.randn((B, L, H, D), device=dev, generator=gen).to(torch.bfloat16)
     x = (inp["q"], inp["k"], inp["v"], inp["g"], inp["beta"], seg)
     ov = not args.gdn_serial
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    timer = sf.KernelTimer(capacity=256 * max(1, args.steps))
 
-    def step(t=None):
-        if t is not None:
-            ev[0].record()
-        _, S_bnd = sf.gdn_chain_fwd(*x, inp["S_in"], ts=args.gdn_ts, overlap=ov)
-        if t is not None:
-            ev[1].record()
-        sf.gdn_chain_bwd(*x, S_bnd, dO, None, ts=args.gdn_ts, overlap=ov)
-        if t is not None:
-            ev[2].record()
+    def step(tm=None):
+        _, S_bnd = sf.gdn_chain_fwd(*x, inp["S_in"], ts=args.gdn_ts, overlap=ov, timing=tm)
+        sf.gdn_chain_bwd(*x, S_bnd, dO, None, ts=args.gdn_ts, overlap=ov, timing=tm)
+
+    for i in range(args.warmup):
+        if i == args.warmup - 1:
             torch.cuda.synchronize()
-            t[0] += ev[0].elapsed_time(ev[1])
-            t[1] += ev[1].elapsed_time(ev[2])
-
-    for _ in range(args.warmup):
-        step()
+            timer.select(GDN_KERNELS)
+            step(timer)
+        else:
+            step()
+    torch.cuda.synchronize()
+    wtime = timer.read()
+    dom = max(GDN_KERNELS, key=lambda k: wtime.get(k, (0.0, 0))[0]) if wtime else "gdn_dchunk"
+    timer.select([dom])
+    torch.cuda.reset_peak_memory_stats()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step()
+        step(timer)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    tt = [0.0, 0.0]
-    for _ in range(args.steps):  # per-call split, from events on the main stream
-        step(tt)
+    peak = torch.cuda.max_memory_allocated()
+    tot_ms, nl = timer.read()[dom]
     ms = (t1 - t0) * 1e3 / args.steps
-    io = 2
-    # algorithmic HBM bytes per (token, head): fwd q, k, v in, o out, g, beta;
-    # bwd q, k, v, dO in, dq, dk, dv out, g, beta in, dg, dbeta out
-    per_tok = {"gdn_fwd": 4 * D * io + 8, "gdn_bwd": 7 * D * io + 16}
-    calls = {}
-    for kn, tot in zip(("gdn_fwd", "gdn_bwd"), tt):
-        avg_s = tot / 1e3 / args.steps
-        calls[kn] = {"ms_per_step": tot / args.steps, "achieved_GBps": per_tok[kn] * B * H * L / avg_s / 1e9}
-    dom = max(calls, key=lambda kn: calls[kn]["ms_per_step"])
+    copy_calibration(torch, dev, args.copy_mib)
+    avg_s = tot_ms / 1e3 / max(nl, 1)
+    if dom == "gdn_dchunk":
+        flops = gdn_dchunk_flops(D) * B * H * (L // 64) * args.steps / max(nl, 1)
+        roof = {"kernel": dom, "bound": "mfma", "achieved": flops / avg_s / 1e12, "peak": PEAK_BF16 / 1e12,
+                "unit": "TFLOP/s", "frac": flops / avg_s / PEAK_BF16}
+    else:
+        roof = {"kernel": dom, "bound": "mfma", "achieved": None, "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
+                "frac": None}
+    roof.update(traffic=read_traffic(dom, "gdn_ctx256k_h40", gdn_src_hash()), launches=nl,
+                avg_launch_us=avg_s * 1e6)
+    if args.kernel_times:
+        for k in GDN_KERNELS:
+            t, n = wtime.get(k, (0.0, 0))
+            print(f"# {k:10s} {t:8.3f} ms/step  {n:4d} launches/step", file=sys.stderr)
     out = {
         "metric": GDN_METRIC, "value": B * L / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
@@ -394,10 +465,9 @@ def bench_gdn(args):
                    "ts": args.gdn_ts or "auto", "overlap": ov,
                    "parallelism": "superchunks: [M|N] prep walk, fp32 state scan, output walk; backward: "
                                   "state-gradient walk over superchunks, per-chunk gradients over all chunks"},
-        "calls": calls,
-        "roofline": {"kernel": dom, "bound": "hbm", "achieved": calls[dom]["achieved_GBps"], "peak": PEAK_HBM / 1e9,
-                     "unit": "GB/s", "frac": calls[dom]["achieved_GBps"] * 1e9 / PEAK_HBM, "traffic": None,
-                     "avg_call_ms": calls[dom]["ms_per_step"]},
+        "kernels_ms_per_step": {k: wtime.get(k, (0.0, 0))[0] for k in GDN_KERNELS},
+        "peak_mem_bytes": peak,
+        "roofline": roof,
     }
     if not args.no_cpu_baseline:
         from oracle import gdn as ogdn
@@ -413,25 +483,126 @@ def bench_gdn(args):
                                "sample": f"batch 0, heads 0..{nh - 1}, first {L_s} tokens, fwd + bwd fp64, "
                                          f"{tc:.1f} s wall; value scaled to a {H}-head layer"}
     print(json.dumps(out), flush=True)
+    timer.close()
+
+
+def bench_recurrence(args):
+    import torch
+    import paper_2608_06838_amd as sf
+    from paper_2608_06838_amd import synth, tuned
+
+    w = synth.workload(args.workload)
+    w["L"] = sum(w["seg_lens"])
+    dev = torch.device("cuda:0")
+    inp = synth.make_inputs(w, device=dev, seed=1002)
+    B, L, H, D = inp["q"].shape
+    io = inp["q"].element_size()
+    gb = 4 * (D if inp["g"].dim() == 4 else 1)
+    seg = w["seg_lens"]
+    pick = tuned.choice(w["name"])  # the profiled per-shape setting (ts, overlap)
+    ts = args.ts if args.ts is not None else pick["ts"]
+    overlap = (not args.no_overlap) if (args.no_overlap or args.overlap) else pick["overlap"]
+    # inputs below ~2 GiB could sit partly in the 256 MB MALL between steps
+    in_bytes = sum(inp[k].numel() * inp[k].element_size() for k in ("q", "k", "v", "g", "dO"))
+    flush = Flusher(torch, dev, MALL_FLUSH_MIB if in_bytes < (2 << 30) else 0)
+    step = make_chain_step(sf, torch, inp, seg, ts, overlap)
+    timer = sf.KernelTimer(capacity=max(512, 8 * len(seg) * (args.steps + 1)))
+
+    # The last warmup step carries HIP events on every kernel launch: per-kernel
+    # times for the report and the choice of the dominant kernel.  The timed
+    # steps then carry events on the dominant kernel's launches only.
+    for i in range(args.warmup):
+        flush()
+        if i == args.warmup - 1:
+            torch.cuda.synchronize()
+            timer.select(RECURRENCE_KERNELS)
+            step(timer)
+        else:
+            step()
+    torch.cuda.synchronize()
+    kstep = timer.read()
+    dom = max(KERNEL_BYTES, key=lambda k: kstep.get(k, (0.0, 0))[0]) if kstep else "bwd_dkv"
+    timer.select([dom])
+    torch.cuda.reset_peak_memory_stats()
+    ms = timed_steps(torch, lambda: step(timer), args.steps, flush)
+    peak = torch.cuda.max_memory_allocated()
+    tot_ms, nlaunch = timer.read()[dom]
+    if not kstep:  # no warmup: per-kernel times from one more step
+        timer.select(RECURRENCE_KERNELS)
+        step(timer)
+        kstep = timer.read()
+
+    # Split-and-overlap figures (Sec. 3.4): the same step with the scans
+    # serialised on the main stream, the scans' own time there, and with them
+    # overlapped on the aux stream.
+    ov = {"default_overlap": overlap}
+    if not args.no_overlap_study:
+        timer.select(["scan"])
+        t_serial = timed_steps(torch, lambda: step(timer, overlap=False), args.steps, flush)
+        t_scan = timer.read().get("scan", (0.0, 0))[0] / args.steps
+        t_over = timed_steps(torch, lambda: step(None, overlap=True), args.steps, flush)
+        t_intra = t_serial - t_scan
+        ov.update(t_e2e_ms=ms, t_overlapped_ms=t_over, t_serial_ms=t_serial, t_scan_serial_ms=t_scan,
+                  t_intra_only_ms=t_intra, e2e_over_intra_only=ms / t_intra if t_intra > 0 else None,
+                  hidden_frac_of_scan=(t_serial - t_over) / t_scan if t_scan > 0 else None)
+    copy_calibration(torch, dev, args.copy_mib)
+
+    value = B * L / (ms / 1e3)
+    avg_s = tot_ms / 1e3 / max(nlaunch, 1)
+    bytes_per_launch = KERNEL_BYTES[dom](D, io, gb) * B * H * L * args.steps / max(nlaunch, 1)
+    achieved = bytes_per_launch / avg_s / 1e9
+    vec = gb > 4
+    traffic = read_traffic(dom, w["name"], vg_src_hash() if vec else kernel_src_hash())
+    flops = alg_flops_per_token_head(D) * B * H * L
+    peak_mfma = PEAK_BF16 if io == 2 else PEAK_F32_MFMA
+    if args.kernel_times:
+        for k in RECURRENCE_KERNELS:
+            msk, n = kstep.get(k, (0.0, 0))
+            print(f"# {k:9s} {msk:8.3f} ms/step  {n:4d} launches/step", file=sys.stderr)
+    out = {
+        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if io == 2 else "f32", "data": "synthetic",
+        "config": {"workload": w["name"], "B": B, "H": H, "Dk": D, "Dv": D, "L": L, "segments": seg,
+                   "gate": "per-key-channel" if vec else "scalar",
+                   "chunk": 64, "io": "bf16" if io == 2 else "f32", "state": "f32",
+                   "overlap": overlap, "ts": ts or "auto", "mall_flush_mib": MALL_FLUSH_MIB if flush.buf is not None
+                   else 0},
+        "mfma_frac_of_peak": flops / (ms / 1e3) / peak_mfma,
+        "mfma_peak": "bf16 2.5 PFLOP/s" if io == 2 else "fp32 matrix 157.3 TFLOP/s",
+        "hbm_frac_alg": alg_bytes_per_token_head(D, io, gb) * B * H * L / (ms / 1e3) / PEAK_HBM,
+        "kernels_ms_per_step": {k: kstep.get(k, (0.0, 0))[0] for k in RECURRENCE_KERNELS},
+        "peak_mem_bytes": peak,
+        "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM / 1e9,
+                     "unit": "GB/s", "frac": achieved * 1e9 / PEAK_HBM, "traffic": traffic,
+                     "launches": nlaunch, "avg_launch_us": avg_s * 1e6},
+        "overlap": ov,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, inp)
+    print(json.dumps(out), flush=True)
+    timer.close()
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="ctx256k_h40")
-    ap.add_argument("--ts", type=int, default=0)
-    ap.add_argument("--no-overlap", action="store_true")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="ctx256k_h40",
+                    help="ctx256k_h40 (default), mid_bf16, tiny_fp32, vector_gate or scan_stress")
+    ap.add_argument("--ts", type=int, default=None, help="superchunk length (0: automatic; default: the tuned one)")
+    ap.add_argument("--no-overlap", action="store_true", help="scans serialised on the main stream")
+    ap.add_argument("--overlap", action="store_true", help="scans overlapped on the aux stream")
+    ap.add_argument("--no-overlap-study", action="store_true",
+                    help="skip the serial / overlapped comparison after the timed steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-times", action="store_true", help="print per-kernel times to stderr")
-    ap.add_argument("--overlap-study", action="store_true",
-                    help="also time the chain with the scans on the main stream (no overlap)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--conv", action="store_true",
                     help="measure the short convolution with carried tails instead of the recurrence")
-    ap.add_argument("--gdn", action="store_true", help="measure the gated-delta-rule forward instead")
+    ap.add_argument("--gdn", action="store_true", help="measure the gated-delta-rule training step instead")
     ap.add_argument("--gdn-ts", type=int, default=0, help="gated delta rule superchunk length (0: automatic)")
     ap.add_argument("--gdn-serial", action="store_true", help="gated delta rule: state scans on the main stream")
     ap.add_argument("--tune-ts", action="store_true",
@@ -445,144 +616,12 @@ def main():
         sys.exit(2)
     if args.conv:
         bench_conv(args)
-        return
-    if args.gdn:
+    elif args.gdn:
         bench_gdn(args)
-        return
-    if args.tune_ts or args.partition_study:
+    elif args.tune_ts or args.partition_study:
         study_main(args)
-        return
-
-    import torch
-    import paper_2608_06838_amd as sf
-    from paper_2608_06838_amd import synth
-
-    w = synth.workload(args.workload)
-    w["L"] = sum(w["seg_lens"])
-    dev = torch.device("cuda:0")
-    inp = synth.make_inputs(w, device=dev, seed=1002)
-    B, L, H, D = inp["q"].shape
-    io = inp["q"].element_size()
-    gb = 4 * (D if inp["g"].dim() == 4 else 1)
-    seg = w["seg_lens"]
-    overlap = not args.no_overlap
-
-    # preallocated outputs and workspaces: the timed region does no allocation
-    o = torch.empty_like(inp["q"])
-    S_bnd = torch.empty((len(seg) + 1, B, H, D, D), dtype=torch.float32, device=dev)
-    nws = sf.chain_workspace_bytes(inp["q"], inp["g"], seg, ts=args.ts)
-    ws_f = torch.empty(nws, dtype=torch.uint8, device=dev)
-    ws_b = torch.empty(nws, dtype=torch.uint8, device=dev)
-    dq, dk, dv = (torch.empty_like(inp["q"]) for _ in range(3))
-    dg = torch.empty_like(inp["g"])
-    dS0 = torch.empty((B, H, D, D), dtype=torch.float32, device=dev)
-
-    def step():
-        sf.chain_fwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, inp["S_in"], ts=args.ts, overlap=overlap,
-                     out=(o, S_bnd, ws_f))
-        sf.chain_bwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, S_bnd, inp["dO"], inp["dS_out"],
-                     ts=args.ts, overlap=overlap, out=(dq, dk, dv, dg, dS0, ws_b))
-
-    kernels = [k for k in sf.KERNELS if not k.startswith("conv")]
-
-    def prof_all(on):
-        for kname in kernels:
-            sf.prof_read(kname)  # drop anything recorded before
-            sf.prof_enable(kname, on)
-
-    # The last warmup step carries HIP events around every kernel: per-kernel times for the report
-    # and the choice of the dominant kernel.  The timed steps then carry events
-    # for the dominant kernel only (events on all ~40 launches of a step cost
-    # 0.8% of it; on one kernel, 0.2%).
-    for i in range(args.warmup):
-        if i == args.warmup - 1:  # the last warmup step, caches and clocks settled
-            torch.cuda.synchronize()
-            prof_all(True)
-        step()
-    torch.cuda.synchronize()
-    wtime = {kname: sf.prof_read(kname) for kname in kernels}
-    prof_all(False)
-    if args.warmup > 0:
-        dom = max((k for k in KERNEL_BYTES), key=lambda k: wtime[k][0])
-        timed = [dom]
     else:
-        dom, timed = None, kernels
-    for kname in timed:
-        sf.prof_enable(kname, True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ktime = {}
-    for kname in timed:
-        sf.prof_enable(kname, False)
-        ktime[kname] = sf.prof_read(kname)
-    ms = (t1 - t0) * 1e3 / args.steps
-    if dom is None:
-        dom = max((k for k in KERNEL_BYTES), key=lambda k: ktime[k][0])
-    # per-kernel ms per step for the report: the last warmup step (timed steps without warmup)
-    kstep = ({k: (wtime[k][0], wtime[k][1]) for k in kernels} if args.warmup > 0
-             else {k: (ktime[k][0] / args.steps, ktime[k][1] // args.steps) for k in kernels})
-    if args.copy_mib > 0:  # known-size copy: FETCH_SIZE / WRITE_SIZE calibration under rocprofv3 --pmc
-        n = args.copy_mib * (1 << 20) // 4
-        src = torch.ones(n, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-    tokens = B * L
-    value = tokens / (ms / 1e3)
-
-    # dominant kernel and its roofline (HIP events over the timed steps)
-    tot_ms, nlaunch = ktime[dom]
-    avg_s = tot_ms / 1e3 / max(nlaunch, 1)
-    bytes_per_launch = KERNEL_BYTES[dom](D, io, gb) * B * H * L * args.steps / max(nlaunch, 1)
-    achieved = bytes_per_launch / avg_s / 1e9
-    traffic = read_traffic(dom) if w["name"] == "ctx256k_h40" else None
-    flops = alg_flops_per_token_head(D) * B * H * L
-    if args.kernel_times:
-        for k in kernels:
-            msk, n = kstep[k]
-            print(f"# {k:9s} {msk:8.3f} ms/step  {n:4d} launches/step", file=sys.stderr)
-    out = {
-        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16" if io == 2 else "f32", "data": "synthetic",
-        "config": {"workload": w["name"], "B": B, "H": H, "Dk": D, "Dv": D, "L": L, "segments": seg,
-                   "gate": "per-key-channel" if gb > 4 else "scalar",
-                   "chunk": 64, "io": "bf16" if io == 2 else "f32", "state": "f32",
-                   "overlap": overlap, "ts": args.ts or "auto"},
-        "mfma_frac_of_bf16_peak": flops / (ms / 1e3) / PEAK_BF16,
-        "hbm_frac_alg": alg_bytes_per_token_head(D, io, gb) * B * H * L / (ms / 1e3) / PEAK_HBM,
-        "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM / 1e9,
-                     "unit": "GB/s", "frac": achieved * 1e9 / PEAK_HBM, "traffic": traffic,
-                     "launches": nlaunch, "avg_launch_us": avg_s * 1e6},
-    }
-    # scan overlap (the fp32 superchunk scans run on a second stream): the chain's
-    # time against the summed times of its other kernels, which is the chain time
-    # with the scans taking no time at all
-    # (per-kernel times from the last warmup step, which carries events on every kernel)
-    t_other = sum(kstep[k][0] for k in kernels if k != "scan")
-    out["overlap"] = {"t_e2e_ms": ms, "t_without_scan_ms": t_other, "t_scan_ms": kstep["scan"][0],
-                      "e2e_over_without_scan": ms / t_other if t_other > 0 else None}
-    if args.overlap_study:
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            sf.chain_fwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, inp["S_in"], ts=args.ts, overlap=False,
-                         out=(o, S_bnd, ws_f))
-            sf.chain_bwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, S_bnd, inp["dO"], inp["dS_out"],
-                         ts=args.ts, overlap=False, out=(dq, dk, dv, dg, dS0, ws_b))
-        torch.cuda.synchronize()
-        t_serial = (time.perf_counter() - t0) * 1e3 / args.steps
-        out["overlap"]["t_serial_ms"] = t_serial
-        out["overlap"]["hidden_frac_of_scan"] = ((t_serial - ms) / out["overlap"]["t_scan_ms"]
-                                                 if out["overlap"]["t_scan_ms"] > 0 else None)
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, inp)
-    print(json.dumps(out), flush=True)
+        bench_recurrence(args)
 
 
 if __name__ == "__main__":

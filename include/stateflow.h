@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define SF_ABI_VERSION 1
+#define SF_ABI_VERSION 2
 
 typedef enum {
     SF_OK = 0,
@@ -90,6 +90,50 @@ typedef struct sf_shape {
                                  selects the packed layout */
 } sf_shape;
 
+/*
+ * Kernel timing for measurement, owned by the caller (no library state).
+ * When sf_tuning.timing points at one of these, every launch of a kernel kind
+ * k (an sf_kernel_id) with bit k of `mask` set takes the next free pair
+ * (start[count], stop[count]) -- HIP events the caller created with timing
+ * enabled -- as the begin and end timestamps of its own dispatch (no marker
+ * packets are added to the stream), writes k to kind[count] and increments
+ * count.  A launch that finds count == capacity increments `dropped` and is
+ * not timed.  The library never creates, synchronises, reads or destroys the
+ * events; the caller reads them after synchronising (hipEventElapsedTime).
+ * One record must not be shared by calls running concurrently on several
+ * host threads.
+ */
+typedef struct sf_timing {
+    uint32_t mask;     /* bit k: time the launches of sf_kernel_id k */
+    int32_t capacity;  /* pairs in start / stop / kind */
+    int32_t count;     /* pairs used so far (the library increments it) */
+    int32_t dropped;   /* timed launches that found no free pair */
+    void **start;      /* hipEvent_t[capacity] */
+    void **stop;       /* hipEvent_t[capacity] */
+    int32_t *kind;     /* int32_t[capacity]: the kernel id of each used pair */
+} sf_timing;
+
+/* Kernel kinds: what one timed launch covers (sf_timing.mask bits). */
+typedef enum {
+    SF_K_FWD_PREP = 0,   /* per-superchunk state contribution (Pre) */
+    SF_K_SCAN = 1,       /* fp32 state scan (ST / STB) */
+    SF_K_FWD_OUT = 2,    /* intra-chunk attention + inter-chunk output (Out) */
+    SF_K_BWD_PREP = 3,   /* per-superchunk state and state-gradient contributions */
+    SF_K_BWD_DQ = 4,     /* dq by a forward state walk (OG) */
+    SF_K_BWD_DKV = 5,    /* dk, dv, dg by a reverse state-gradient walk (PG) */
+    SF_K_CONV_FWD = 6,   /* short convolution, forward */
+    SF_K_CONV_BWD = 7,   /* short convolution, backward (dx, dtail_in, dw partials and their sum) */
+    SF_K_GDN_PREP = 8,   /* gated delta rule: superchunk maps (M_J, N_J) */
+    SF_K_GDN_SCAN = 9,   /* gated delta rule: fp32 affine state scan */
+    SF_K_GDN_OUT = 10,   /* gated delta rule: output walk */
+    SF_K_GDN_STORE = 11, /* gated delta rule backward: walk storing the state entering every chunk */
+    SF_K_GDN_DPREP = 12, /* gated delta rule backward: superchunk state-gradient offsets E_J */
+    SF_K_GDN_DSCAN = 13, /* gated delta rule backward: transposed scan */
+    SF_K_GDN_DWALK = 14, /* gated delta rule backward: state-gradient walk */
+    SF_K_GDN_DCHUNK = 15, /* gated delta rule backward: per-chunk parameter gradients */
+    SF_K_COUNT = 16
+} sf_kernel_id;
+
 /* Tuning knobs; a NULL pointer selects the defaults for every field. */
 typedef struct sf_tuning {
     int32_t ts;       /* state-materialisation stride in tokens (superchunk):
@@ -99,7 +143,8 @@ typedef struct sf_tuning {
                          state scans on the aux stream overlapped with the
                          neighbouring segment's dense kernels (Sec. 3.4
                          "Split and Overlap"); 0 serialises on main. */
-    int32_t reserved[6];
+    int32_t reserved[4];
+    sf_timing *timing; /* NULL: no timing (see sf_timing) */
 } sf_tuning;
 
 /* ABI version (SF_ABI_VERSION). */
@@ -199,8 +244,9 @@ sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
  * over batch and tokens, in a fixed order: bitwise reproducible).  dw needs
  * a workspace of sf_conv_bwd_workspace_bytes().  Supported: 1 <= W <= 4
  * (W = 1 has no tail; the tail pointers are then ignored), C a multiple of 8,
- * L >= 0, 16-byte aligned pointers and strides.  Same ownership, error and
- * aliasing rules as the recurrence entry points.
+ * L >= 0, 16-byte aligned pointers and strides.  tuning may be NULL; of its
+ * fields only `timing` applies here.  Same ownership, error and aliasing rules
+ * as the recurrence entry points.
  */
 typedef enum { SF_ACT_NONE = 0, SF_ACT_SILU = 1 } sf_act;
 
@@ -216,10 +262,10 @@ typedef struct sf_conv_shape {
 
 size_t sf_conv_bwd_workspace_bytes(const sf_conv_shape *shape);
 sf_status sf_conv_fwd(const sf_conv_shape *shape, const void *x, const float *w, const float *tail_in,
-                      void *y, float *tail_out, sf_stream stream);
+                      void *y, float *tail_out, const sf_tuning *tuning, sf_stream stream);
 sf_status sf_conv_bwd(const sf_conv_shape *shape, const void *x, const float *w, const float *tail_in,
                       const void *dy, const float *dtail_out, void *dx, float *dw, float *dtail_in,
-                      void *ws, size_t ws_bytes, sf_stream stream);
+                      void *ws, size_t ws_bytes, const sf_tuning *tuning, sf_stream stream);
 
 /*
  * Hybrid-aware segment lengths (Sec. 3.2, Hybrid-Aware Sequence Chunking):
@@ -323,29 +369,6 @@ sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *
                            float *dbeta, float *dS_init, void *ws, size_t ws_bytes, const sf_tuning *tuning,
                            sf_stream main, sf_stream aux);
 
-/*
- * Kernel timing for measurement: while enabled, every launch of kernel
- * `kernel_id` (an sf_kernel_id) carries HIP events that take the begin and
- * end timestamps of its own dispatch.  sf_prof_read() synchronises those
- * events and returns the summed milliseconds and launch count since the last
- * reset.
- */
-typedef enum {
-    SF_K_FWD_PREP = 0, /* per-superchunk state contribution (Pre) */
-    SF_K_SCAN = 1,     /* fp32 state scan (ST / STB) */
-    SF_K_FWD_OUT = 2,  /* intra-chunk attention + inter-chunk output (Out) */
-    SF_K_BWD_PREP = 3, /* per-superchunk state and state-gradient contributions */
-    SF_K_BWD_DQ = 4,   /* dq by a forward state walk (OG) */
-    SF_K_BWD_DKV = 5,  /* dk, dv, dg by a reverse state-gradient walk (PG) */
-    SF_K_CONV_FWD = 6, /* short convolution, forward */
-    SF_K_CONV_BWD = 7, /* short convolution, backward (dx, dtail_in, dw partials and their sum) */
-    SF_K_GDN_FWD = 8,  /* gated delta rule, forward (prep, scan and output walk) */
-    SF_K_GDN_BWD = 9,  /* gated delta rule, backward (every kernel of one call) */
-    SF_K_COUNT = 10
-} sf_kernel_id;
-
-sf_status sf_prof_enable(int32_t kernel_id, int32_t on);
-sf_status sf_prof_read(int32_t kernel_id, double *total_ms, int64_t *launches);
 
 #ifdef __cplusplus
 }

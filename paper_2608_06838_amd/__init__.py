@@ -27,10 +27,12 @@ import torch
 
 from . import _lib
 from ._lib import KERNELS, StateflowError  # noqa: F401
+from . import tuned
+from .timing import KernelTimer  # noqa: F401
 
 __all__ = ["segment_fwd", "segment_bwd", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
            "bwd_workspace_bytes", "chain_workspace_bytes", "conv_fwd", "conv_bwd", "conv_bwd_workspace_bytes",
-           "gdn_fwd", "gdn_fwd_workspace_bytes", "gdn_bwd", "gdn_chain_fwd", "gdn_chain_bwd", "partition_hybrid", "prof_enable", "prof_read", "StateflowError", "abi_version"]
+           "gdn_fwd", "gdn_fwd_workspace_bytes", "gdn_bwd", "gdn_chain_fwd", "gdn_chain_bwd", "partition_hybrid", "KernelTimer", "StateflowError", "abi_version"]
 
 _IO = {torch.bfloat16: _lib.SF_BF16, torch.float32: _lib.SF_F32}
 _aux_streams = {}
@@ -48,10 +50,13 @@ def _stream_handle(s):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _tuning(ts=0, overlap=True):
+def _tuning(ts=0, overlap=True, timing=None):
+    """timing: a timing.KernelTimer whose record the call's launches use."""
     t = _lib.SfTuning()
     t.ts = int(ts)
     t.overlap = 1 if overlap else 0
+    if timing is not None:
+        t.timing = ctypes.pointer(timing.rec)
     return t
 
 
@@ -124,7 +129,7 @@ def chain_workspace_bytes(q, g, seg_lens, ts=0):
                                                ctypes.byref(_tuning(ts)))
 
 
-def segment_fwd(q, k, v, g, S_in=None, *, ts=0, stream=None):
+def segment_fwd(q, k, v, g, S_in=None, *, ts=0, stream=None, timing=None):
     """(o, S_out) = Fwd(q, k, v, g; S_in) for one segment."""
     _same_layout(q, k, v)
     sh = _shape(q, g)
@@ -132,7 +137,7 @@ def segment_fwd(q, k, v, g, S_in=None, *, ts=0, stream=None):
     _state(S_in, B, H, D, "S_in")
     stream = stream or torch.cuda.current_stream(q.device)
     L_ = _lib.lib()
-    tun = _tuning(ts)
+    tun = _tuning(ts, timing=timing)
     with torch.cuda.stream(stream):
         o = _like(q)
         S_out = torch.empty((B, H, D, D), dtype=torch.float32, device=q.device)
@@ -144,7 +149,7 @@ def segment_fwd(q, k, v, g, S_in=None, *, ts=0, stream=None):
     return o, S_out
 
 
-def segment_bwd(q, k, v, g, S_in, dO, dS_out=None, *, ts=0, stream=None):
+def segment_bwd(q, k, v, g, S_in, dO, dS_out=None, *, ts=0, stream=None, timing=None):
     """(dq, dk, dv, dg, dS_in) = Bwd(q, k, v, g, S_in; dO, dS_out) for one segment."""
     _same_layout(q, k, v, dO)
     sh = _shape(q, g)
@@ -153,7 +158,7 @@ def segment_bwd(q, k, v, g, S_in, dO, dS_out=None, *, ts=0, stream=None):
     _state(dS_out, B, H, D, "dS_out")
     stream = stream or torch.cuda.current_stream(q.device)
     L_ = _lib.lib()
-    tun = _tuning(ts)
+    tun = _tuning(ts, timing=timing)
     with torch.cuda.stream(stream):
         dq, dk, dv = _like(q), _like(q), _like(q)
         dg = _like(g)
@@ -178,8 +183,18 @@ def _aux_for(device, aux_stream, overlap):
     return _aux_streams[key]
 
 
-def chain_fwd(q, k, v, g, seg_lens, S_init=None, *, ts=0, overlap=True, stream=None, aux_stream=None,
-              out=None):
+def _pick(q, g, seg_lens, ts, overlap):
+    """ts / overlap left as None take the profiled per-shape setting."""
+    if ts is not None and overlap is not None:
+        return int(ts), bool(overlap)
+    B, L, H, D = q.shape
+    t = tuned.lookup(B, H, D, "bf16" if q.dtype == torch.bfloat16 else "f32",
+                     "vector" if g.dim() == 4 else "scalar", seg_lens)
+    return (t["ts"] if ts is None else int(ts)), (t["overlap"] if overlap is None else bool(overlap))
+
+
+def chain_fwd(q, k, v, g, seg_lens, S_init=None, *, ts=None, overlap=None, stream=None, aux_stream=None,
+              out=None, timing=None):
     """Forward over consecutive segments with S_in(i+1) = S_out(i).
 
     Returns (o, S_bnd) with S_bnd[i] the state entering segment i
@@ -191,10 +206,11 @@ def chain_fwd(q, k, v, g, seg_lens, S_init=None, *, ts=0, overlap=True, stream=N
     B, L, H, D = q.shape
     n = len(seg_lens)
     _state(S_init, B, H, D, "S_init")
+    ts, overlap = _pick(q, g, seg_lens, ts, overlap)
     stream = stream or torch.cuda.current_stream(q.device)
     aux = _aux_for(q.device, aux_stream, overlap)
     L_ = _lib.lib()
-    tun = _tuning(ts, overlap)
+    tun = _tuning(ts, overlap, timing)
     sl = (ctypes.c_int64 * n)(*[int(x) for x in seg_lens])
     with torch.cuda.stream(stream):
         if out is None:
@@ -214,8 +230,8 @@ def chain_fwd(q, k, v, g, seg_lens, S_init=None, *, ts=0, overlap=True, stream=N
     return o, S_bnd
 
 
-def chain_bwd(q, k, v, g, seg_lens, S_bnd, dO, dS_final=None, *, ts=0, overlap=True, stream=None,
-              aux_stream=None, out=None):
+def chain_bwd(q, k, v, g, seg_lens, S_bnd, dO, dS_final=None, *, ts=None, overlap=None, stream=None,
+              aux_stream=None, out=None, timing=None):
     """Backward over the segments in reverse with dS_out(i) = dS_in(i+1).
 
     Returns (dq, dk, dv, dg, dS_init).  `out` may supply preallocated
@@ -229,10 +245,11 @@ def chain_bwd(q, k, v, g, seg_lens, S_bnd, dO, dS_final=None, *, ts=0, overlap=T
             or S_bnd.dtype != torch.float32 or not S_bnd.is_contiguous()):
         raise ValueError("S_bnd must be a contiguous float32 [n_seg(+1), B, H, D, D] tensor")
     _state(dS_final, B, H, D, "dS_final")
+    ts, overlap = _pick(q, g, seg_lens, ts, overlap)
     stream = stream or torch.cuda.current_stream(q.device)
     aux = _aux_for(q.device, aux_stream, overlap)
     L_ = _lib.lib()
-    tun = _tuning(ts, overlap)
+    tun = _tuning(ts, overlap, timing)
     sl = (ctypes.c_int64 * n)(*[int(x) for x in seg_lens])
     with torch.cuda.stream(stream):
         if out is None:
@@ -291,7 +308,7 @@ def _out_like(t, ref, name):
     return t
 
 
-def conv_fwd(x, w, tail_in=None, act="silu", *, stream=None, out=None):
+def conv_fwd(x, w, tail_in=None, act="silu", *, stream=None, out=None, timing=None):
     """(y, tail_out) of the short convolution over one segment; tail_out is
     None for W = 1.  out=(y, tail_out) supplies the outputs (no allocation)."""
     sh = _conv_shape(x, w, act)
@@ -306,12 +323,12 @@ def conv_fwd(x, w, tail_in=None, act="silu", *, stream=None, out=None):
             y = _like(x)
             tail_out = torch.empty((B, W - 1, C), dtype=torch.float32, device=x.device) if W > 1 else None
     rc = _lib.lib().sf_conv_fwd(ctypes.byref(sh), _ptr(x), _ptr(w), _ptr(tail_in), _ptr(y), _ptr(tail_out),
-                                _stream_handle(stream))
+                                ctypes.byref(_tuning(timing=timing)), _stream_handle(stream))
     _lib.check("sf_conv_fwd", rc)
     return y, tail_out
 
 
-def conv_bwd(x, w, tail_in, dy, dtail_out=None, act="silu", *, stream=None, out=None):
+def conv_bwd(x, w, tail_in, dy, dtail_out=None, act="silu", *, stream=None, out=None, timing=None):
     """(dx, dw, dtail_in) for the loss sum <dy, y> + <dtail_out, tail_out>;
     dtail_in is None for W = 1.  out=(dx, dw, dtail_in, workspace) supplies
     the outputs and a workspace of conv_bwd_workspace_bytes() (no allocation)."""
@@ -337,12 +354,13 @@ def conv_bwd(x, w, tail_in, dy, dtail_out=None, act="silu", *, stream=None, out=
             dtail_in = torch.empty((B, W - 1, C), dtype=torch.float32, device=x.device) if W > 1 else None
             ws = _ws(L_.sf_conv_bwd_workspace_bytes(ctypes.byref(sh)), x.device)
     rc = L_.sf_conv_bwd(ctypes.byref(sh), _ptr(x), _ptr(w), _ptr(tail_in), _ptr(dy), _ptr(dtail_out), _ptr(dx),
-                        _ptr(dw), _ptr(dtail_in), _ptr(ws), ws.numel(), _stream_handle(stream))
+                        _ptr(dw), _ptr(dtail_in), _ptr(ws), ws.numel(), ctypes.byref(_tuning(timing=timing)),
+                        _stream_handle(stream))
     _lib.check("sf_conv_bwd", rc)
     return dx, dw, dtail_in
 
 
-def gdn_fwd(q, k, v, g, beta, S_in=None, *, ts=0, with_v_new=False, stream=None):
+def gdn_fwd(q, k, v, g, beta, S_in=None, *, ts=0, with_v_new=False, stream=None, timing=None):
     """(o, S_out) of the gated delta rule over one segment: q, k, v [B, L, H, D]
     bf16; g (natural-log decay) and beta float32 [B, L, H] with the same
     strides; S_in [B, H, D, D] float32 or None.  ts: superchunk length in
@@ -356,7 +374,7 @@ def gdn_fwd(q, k, v, g, beta, S_in=None, *, ts=0, with_v_new=False, stream=None)
     _state(S_in, B, H, D, "S_in")
     stream = stream or torch.cuda.current_stream(q.device)
     L_ = _lib.lib()
-    tun = _tuning(ts)
+    tun = _tuning(ts, timing=timing)
     with torch.cuda.stream(stream):
         o = _like(q)
         vn = _like(q) if with_v_new else None
@@ -368,7 +386,7 @@ def gdn_fwd(q, k, v, g, beta, S_in=None, *, ts=0, with_v_new=False, stream=None)
     return (o, S_out, vn) if with_v_new else (o, S_out)
 
 
-def gdn_bwd(q, k, v, g, beta, S_in, dO, dS_out=None, *, ts=0, stream=None):
+def gdn_bwd(q, k, v, g, beta, S_in, dO, dS_out=None, *, ts=0, stream=None, timing=None):
     """(dq, dk, dv, dg, dbeta, dS_in) of the gated delta rule over one segment
     for Loss = sum <dO, o> + <dS_out, S_out>; arguments as for gdn_fwd."""
     _same_layout(q, k, v, dO)
@@ -380,7 +398,7 @@ def gdn_bwd(q, k, v, g, beta, S_in, dO, dS_out=None, *, ts=0, stream=None):
     _state(dS_out, B, H, D, "dS_out")
     stream = stream or torch.cuda.current_stream(q.device)
     L_ = _lib.lib()
-    tun = _tuning(ts)
+    tun = _tuning(ts, timing=timing)
     with torch.cuda.stream(stream):
         dq, dk, dv = _like(q), _like(k), _like(v)
         dg, dbeta = _like(g), _like(beta)
@@ -394,7 +412,7 @@ def gdn_bwd(q, k, v, g, beta, S_in, dO, dS_out=None, *, ts=0, stream=None):
 
 
 def gdn_chain_fwd(q, k, v, g, beta, seg_lens, S_init=None, *, ts=0, overlap=True, with_v_new=False, stream=None,
-                  aux_stream=None):
+                  aux_stream=None, timing=None):
     """Gated-delta-rule forward over consecutive segments with
     S_in(i+1) = S_out(i), the state scans overlapped on an aux stream.
 
@@ -410,7 +428,7 @@ def gdn_chain_fwd(q, k, v, g, beta, seg_lens, S_init=None, *, ts=0, overlap=True
     stream = stream or torch.cuda.current_stream(q.device)
     aux = _aux_for(q.device, aux_stream, overlap)
     L_ = _lib.lib()
-    tun = _tuning(ts, overlap)
+    tun = _tuning(ts, overlap, timing)
     sl = (ctypes.c_int64 * n)(*[int(x) for x in seg_lens])
     with torch.cuda.stream(stream):
         o = _like(q)
@@ -429,7 +447,7 @@ def gdn_chain_fwd(q, k, v, g, beta, seg_lens, S_init=None, *, ts=0, overlap=True
 
 
 def gdn_chain_bwd(q, k, v, g, beta, seg_lens, S_bnd, dO, dS_final=None, *, ts=0, overlap=True, stream=None,
-                  aux_stream=None):
+                  aux_stream=None, timing=None):
     """Gated-delta-rule backward over the segments in reverse with
     dS_out(i) = dS_in(i+1); S_bnd from gdn_chain_fwd.  Returns
     (dq, dk, dv, dg, dbeta, dS_init)."""
@@ -445,7 +463,7 @@ def gdn_chain_bwd(q, k, v, g, beta, seg_lens, S_bnd, dO, dS_final=None, *, ts=0,
     stream = stream or torch.cuda.current_stream(q.device)
     aux = _aux_for(q.device, aux_stream, overlap)
     L_ = _lib.lib()
-    tun = _tuning(ts, overlap)
+    tun = _tuning(ts, overlap, timing)
     sl = (ctypes.c_int64 * n)(*[int(x) for x in seg_lens])
     with torch.cuda.stream(stream):
         dq, dk, dv = _like(q), _like(k), _like(v)
@@ -469,14 +487,3 @@ def partition_hybrid(T, N, alpha, w_tok, w_soft, round_to=128):
     _lib.check("sf_partition_hybrid", _lib.lib().sf_partition_hybrid(int(T), int(N), float(alpha), float(w_tok),
                                                                       float(w_soft), int(round_to), out))
     return [int(x) for x in out]
-
-
-def prof_enable(kernel, on=True):
-    _lib.check("sf_prof_enable", _lib.lib().sf_prof_enable(KERNELS[kernel], 1 if on else 0))
-
-
-def prof_read(kernel):
-    ms = ctypes.c_double()
-    n = ctypes.c_int64()
-    _lib.check("sf_prof_read", _lib.lib().sf_prof_read(KERNELS[kernel], ctypes.byref(ms), ctypes.byref(n)))
-    return ms.value, n.value

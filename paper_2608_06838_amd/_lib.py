@@ -14,9 +14,10 @@ SF_OK, SF_E_NULL, SF_E_SHAPE, SF_E_DTYPE, SF_E_ALIGN, SF_E_ALIAS, SF_E_WORKSPACE
     SF_E_UNSUPPORTED, SF_E_HIP = range(9)
 SF_F32, SF_BF16 = 0, 1
 SF_GATE_SCALAR, SF_GATE_VECTOR = 0, 1
+# sf_kernel_id: the kernel kinds a timing record can select
 KERNELS = {"fwd_prep": 0, "scan": 1, "fwd_out": 2, "bwd_prep": 3, "bwd_dq": 4, "bwd_dkv": 5,
-           "conv_fwd": 6, "conv_bwd": 7, "gdn_fwd": 8,
-           "gdn_bwd": 9}
+           "conv_fwd": 6, "conv_bwd": 7, "gdn_prep": 8, "gdn_scan": 9, "gdn_out": 10, "gdn_store": 11,
+           "gdn_dprep": 12, "gdn_dscan": 13, "gdn_dwalk": 14, "gdn_dchunk": 15}
 SF_ACT_NONE, SF_ACT_SILU = 0, 1
 
 # every symbol include/stateflow.h declares
@@ -25,8 +26,7 @@ EXPORTS = ["sf_abi_version", "sf_status_str", "sf_last_error", "sf_fwd_workspace
            "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd",
            "sf_gdn_fwd_workspace_bytes", "sf_gdn_fwd", "sf_gdn_bwd_workspace_bytes", "sf_gdn_bwd",
            "sf_gdn_chain_workspace_bytes", "sf_gdn_chain_fwd", "sf_gdn_chain_bwd",
-           "sf_partition_hybrid",
-           "sf_prof_enable", "sf_prof_read"]
+           "sf_partition_hybrid"]
 
 
 class SfShape(ctypes.Structure):
@@ -43,9 +43,15 @@ class SfConvShape(ctypes.Structure):
                 ("sx_b", ctypes.c_int64), ("sx_l", ctypes.c_int64)]
 
 
+class SfTiming(ctypes.Structure):
+    _fields_ = [("mask", ctypes.c_uint32), ("capacity", ctypes.c_int32), ("count", ctypes.c_int32),
+                ("dropped", ctypes.c_int32), ("start", ctypes.POINTER(ctypes.c_void_p)),
+                ("stop", ctypes.POINTER(ctypes.c_void_p)), ("kind", ctypes.POINTER(ctypes.c_int32))]
+
+
 class SfTuning(ctypes.Structure):
     _fields_ = [("ts", ctypes.c_int32), ("overlap", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 6)]
+                ("reserved", ctypes.c_int32 * 4), ("timing", ctypes.POINTER(SfTiming))]
 
 
 class StateflowError(RuntimeError):
@@ -97,9 +103,9 @@ def lib():
     L.sf_conv_bwd_workspace_bytes.restype = sz
     L.sf_conv_bwd_workspace_bytes.argtypes = [cp]
     L.sf_conv_fwd.restype = ctypes.c_int
-    L.sf_conv_fwd.argtypes = [cp] + [vp] * 5 + [vp]
+    L.sf_conv_fwd.argtypes = [cp] + [vp] * 5 + [tp, vp]
     L.sf_conv_bwd.restype = ctypes.c_int
-    L.sf_conv_bwd.argtypes = [cp] + [vp] * 9 + [sz, vp]
+    L.sf_conv_bwd.argtypes = [cp] + [vp] * 9 + [sz, tp, vp]
     L.sf_gdn_fwd_workspace_bytes.restype = sz
     L.sf_gdn_fwd_workspace_bytes.argtypes = [sp, tp]
     L.sf_gdn_fwd.restype = ctypes.c_int
@@ -116,10 +122,6 @@ def lib():
     L.sf_gdn_chain_bwd.argtypes = [sp, i32, i64p] + [vp] * 15 + [sz, tp, vp, vp]
     L.sf_partition_hybrid.restype = ctypes.c_int
     L.sf_partition_hybrid.argtypes = [i64, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double, i32, i64p]
-    L.sf_prof_enable.restype = ctypes.c_int
-    L.sf_prof_enable.argtypes = [i32, i32]
-    L.sf_prof_read.restype = ctypes.c_int
-    L.sf_prof_read.argtypes = [i32, ctypes.POINTER(ctypes.c_double), i64p]
     _lib = L
     return L
 

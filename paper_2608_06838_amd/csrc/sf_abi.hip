@@ -18,7 +18,6 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
-#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -150,6 +149,10 @@ Range srange(const Shape &r, const float *p, int64_t nstates, const char *name) 
     const char *b = (const char *)p;
     return {b, b + (p ? nstates * r.B * r.H * (int64_t)r.D * r.D * 4 : 0), name};
 }
+Range wsrange(const void *ws, size_t bytes) {
+    const char *b = (const char *)ws;
+    return {b, b + (ws ? bytes : 0), "ws"};
+}
 bool overlap(const Range &a, const Range &b) {
     return a.lo && b.lo && a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi;
 }
@@ -260,30 +263,42 @@ WsLayout ws_layout(const Shape &r, int64_t L, int ts, bool bwd) {
     return w;
 }
 
-// ------------------------------------------------------------- profiling
-std::mutex g_prof_mu;
-bool g_prof_on[SF_K_COUNT] = {};
-std::vector<std::pair<hipEvent_t, hipEvent_t>> g_prof_ev[SF_K_COUNT];
+// ------------------------------------------------------------- kernel timing
+// The caller's timing record (sf_timing, carried by sf_tuning): a launch of a
+// kernel kind whose bit is set takes the next pair of the caller's events as
+// the begin and end timestamps of its own dispatch packets.  The library keeps
+// nothing: the pairs, the count and the kinds live in the caller's record.
+sf_status check_timing(const sf_tuning *t) {
+    const sf_timing *tm = t ? t->timing : nullptr;
+    if (!tm) return SF_OK;
+    if (tm->capacity < 0 || tm->count < 0 || tm->count > tm->capacity)
+        return fail(SF_E_SHAPE, "timing: need 0 <= count <= capacity (count=%d capacity=%d)", tm->count,
+                    tm->capacity);
+    if (tm->capacity > 0 && (!tm->start || !tm->stop || !tm->kind))
+        return fail(SF_E_NULL, "timing: start, stop and kind arrays are required");
+    return SF_OK;
+}
+sf_timing *timing_of(const sf_tuning *t) { return t ? t->timing : nullptr; }
 
-sf_status launch(int kind, const Shape &r, const sf::SegArgs &a, hipStream_t s) {
-    bool on;
-    {
-        std::lock_guard<std::mutex> lk(g_prof_mu);
-        on = g_prof_on[kind];
+void take_pair(sf_timing *tm, int kind, hipEvent_t &e0, hipEvent_t &e1) {
+    e0 = e1 = nullptr;
+    if (!tm || kind < 0 || kind >= 32 || !((tm->mask >> kind) & 1u)) return;
+    if (tm->count >= tm->capacity) {
+        ++tm->dropped;
+        return;
     }
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (on) {
-        if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess)
-            return hip_fail(hipGetLastError(), "profiling event");
-    }
+    e0 = (hipEvent_t)tm->start[tm->count];
+    e1 = (hipEvent_t)tm->stop[tm->count];
+    tm->kind[tm->count] = kind;
+    ++tm->count;
+}
+
+sf_status launch(int kind, const Shape &r, const sf::SegArgs &a, hipStream_t s, sf_timing *tm) {
+    hipEvent_t e0, e1;
+    take_pair(tm, kind, e0, e1);
     // the events take the dispatch timestamps of the launch itself
     hipError_t e = sf::launch_kernel(kind, r.io, r.D, a, s, e0, e1);
-    if (e != hipSuccess) return hip_fail(e, "kernel launch");
-    if (on) {
-        std::lock_guard<std::mutex> lk(g_prof_mu);
-        g_prof_ev[kind].push_back({e0, e1});
-    }
-    return SF_OK;
+    return e == hipSuccess ? SF_OK : hip_fail(e, "kernel launch");
 }
 
 // ------------------------------------------------------ short convolution
@@ -348,34 +363,23 @@ Range frange(const void *p, int64_t n, const char *name) {
     return {b, b + (p ? n * 4 : 0), name};
 }
 
-sf_status conv_run(int kind, bool bwd, const sf::ConvArgs &a, hipStream_t s) {
-    bool on;
-    {
-        std::lock_guard<std::mutex> lk(g_prof_mu);
-        on = g_prof_on[kind];
-    }
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (on) {
-        if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess)
-            return hip_fail(hipGetLastError(), "profiling event");
-    }
+sf_status conv_run(int kind, bool bwd, const sf::ConvArgs &a, hipStream_t s, sf_timing *tm) {
+    hipEvent_t e0, e1;
+    take_pair(tm, kind, e0, e1);
     hipError_t e = sf::launch_conv(bwd, a, s, e0, e1);
-    if (e != hipSuccess) return hip_fail(e, "kernel launch");
-    if (on) {
-        std::lock_guard<std::mutex> lk(g_prof_mu);
-        g_prof_ev[kind].push_back({e0, e1});
-    }
-    return SF_OK;
+    return e == hipSuccess ? SF_OK : hip_fail(e, "kernel launch");
 }
 
 // ----------------------------------------------------------- segment plans
 struct Seg {
     sf::SegArgs a;
     int n;  // superchunks
+    sf_timing *tm;
 };
 
-Seg make_seg(const Shape &r, int64_t L, int ts, char *ws, bool bwd) {
+Seg make_seg(const Shape &r, int64_t L, int ts, char *ws, bool bwd, sf_timing *tm) {
     Seg s{};
+    s.tm = tm;
     sf::SegArgs &a = s.a;
     a.sx_b = r.sx_b;
     a.sx_l = r.sx_l;
@@ -408,10 +412,10 @@ const float *offset_g(const Shape &r, const float *p, int64_t tok) { return p ? 
 
 // forward phases of one segment
 sf_status fwd_prep(const Shape &r, const Seg &s, hipStream_t st) {
-    return s.n > 1 ? launch(SF_K_FWD_PREP, r, s.a, st) : SF_OK;
+    return s.n > 1 ? launch(SF_K_FWD_PREP, r, s.a, st, s.tm) : SF_OK;
 }
 sf_status fwd_scan(const Shape &r, const Seg &s, hipStream_t st) {
-    if (s.n > 1) return launch(SF_K_SCAN, r, s.a, st);
+    if (s.n > 1) return launch(SF_K_SCAN, r, s.a, st, s.tm);
     return SF_OK;
 }
 sf_status fwd_out(const Shape &r, const Seg &s, hipStream_t st) {
@@ -421,23 +425,23 @@ sf_status fwd_out(const Shape &r, const Seg &s, hipStream_t st) {
     }
     sf::SegArgs a = s.a;
     if (s.n > 1) a.S_out = nullptr;  // the scan wrote S_out
-    return launch(SF_K_FWD_OUT, r, a, st);
+    return launch(SF_K_FWD_OUT, r, a, st, s.tm);
 }
 // backward phases
 sf_status bwd_prep(const Shape &r, const Seg &s, hipStream_t st) {
-    return s.n > 1 ? launch(SF_K_BWD_PREP, r, s.a, st) : SF_OK;
+    return s.n > 1 ? launch(SF_K_BWD_PREP, r, s.a, st, s.tm) : SF_OK;
 }
 sf_status bwd_scan(const Shape &r, const Seg &s, hipStream_t st) {
-    return s.n > 1 ? launch(SF_K_SCAN, r, s.a, st) : SF_OK;
+    return s.n > 1 ? launch(SF_K_SCAN, r, s.a, st, s.tm) : SF_OK;
 }
 sf_status bwd_grad(const Shape &r, const Seg &s, hipStream_t st) {
     if (s.n == 0) {
         hipError_t e = sf::launch_state_copy(s.a.dS_out, s.a.dS_in, (int64_t)r.B * r.H * r.D * r.D, st);
         return e == hipSuccess ? SF_OK : hip_fail(e, "state copy");
     }
-    sf_status rc = launch(SF_K_BWD_DQ, r, s.a, st);
+    sf_status rc = launch(SF_K_BWD_DQ, r, s.a, st, s.tm);
     if (rc != SF_OK) return rc;
-    return launch(SF_K_BWD_DKV, r, s.a, st);
+    return launch(SF_K_BWD_DKV, r, s.a, st, s.tm);
 }
 
 // ------------------------------------------------------------ stream events
@@ -560,18 +564,19 @@ sf_status sf_segment_fwd(const sf_shape *shape, const void *q, const void *k, co
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
+    TRY(check_timing(tuning));
     if (!S_out || (r.L > 0 && (!q || !k || !v || !g || !o)))
         return fail(SF_E_NULL, "q, k, v, g, o and S_out are required");
     TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_in, "S_in"}, {S_out, "S_out"}, {ws, "ws"}}));
-    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
-                     grange(r, g, r.L, "g"), srange(r, S_in, 1, "S_in")},
-                    {xrange(r, o, r.L, "o"), srange(r, S_out, 1, "S_out")}));
     int ts;
     TRY(pick_ts(r, r.L, tuning, ts));
     const size_t need = ws_layout(r, r.L, ts, false).total;
     if (need > 0 && !ws) return fail(SF_E_NULL, "workspace of %zu bytes required", need);
     if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
-    Seg s = make_seg(r, r.L, ts, (char *)ws, false);
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
+                     grange(r, g, r.L, "g"), srange(r, S_in, 1, "S_in")},
+                    {xrange(r, o, r.L, "o"), srange(r, S_out, 1, "S_out"), wsrange(ws, need)}));
+    Seg s = make_seg(r, r.L, ts, (char *)ws, false, timing_of(tuning));
     s.a.q = q;
     s.a.k = k;
     s.a.v = v;
@@ -593,21 +598,22 @@ sf_status sf_segment_bwd(const sf_shape *shape, const void *q, const void *k, co
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
+    TRY(check_timing(tuning));
     if (!dS_in || (r.L > 0 && (!q || !k || !v || !g || !dO || !dq || !dk || !dv || !dg)))
         return fail(SF_E_NULL, "q, k, v, g, dO, dq, dk, dv, dg and dS_in are required");
     TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {dO, "dO"}, {dq, "dq"}, {dk, "dk"}, {dv, "dv"},
                      {S_in, "S_in"}, {dS_out, "dS_out"}, {dS_in, "dS_in"}, {ws, "ws"}}));
-    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
-                     grange(r, g, r.L, "g"), srange(r, S_in, 1, "S_in"), xrange(r, dO, r.L, "dO"),
-                     srange(r, dS_out, 1, "dS_out")},
-                    {xrange(r, dq, r.L, "dq"), xrange(r, dk, r.L, "dk"), xrange(r, dv, r.L, "dv"),
-                     grange(r, dg, r.L, "dg"), srange(r, dS_in, 1, "dS_in")}));
     int ts;
     TRY(pick_ts(r, r.L, tuning, ts));
     const size_t need = ws_layout(r, r.L, ts, true).total;
     if (need > 0 && !ws) return fail(SF_E_NULL, "workspace of %zu bytes required", need);
     if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
-    Seg s = make_seg(r, r.L, ts, (char *)ws, true);
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
+                     grange(r, g, r.L, "g"), srange(r, S_in, 1, "S_in"), xrange(r, dO, r.L, "dO"),
+                     srange(r, dS_out, 1, "dS_out")},
+                    {xrange(r, dq, r.L, "dq"), xrange(r, dk, r.L, "dk"), xrange(r, dv, r.L, "dv"),
+                     grange(r, dg, r.L, "dg"), srange(r, dS_in, 1, "dS_in"), wsrange(ws, need)}));
+    Seg s = make_seg(r, r.L, ts, (char *)ws, true, timing_of(tuning));
     s.a.q = q;
     s.a.k = k;
     s.a.v = v;
@@ -640,16 +646,17 @@ sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
+    TRY(check_timing(tuning));
     TRY(check_segments(r, n_seg, seg_len));
     if (!q || !k || !v || !g || !o || !S_bnd || !ws)
         return fail(SF_E_NULL, "q, k, v, g, o, S_bnd and ws are required");
     TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_bnd, "S_bnd"}, {ws, "ws"}}));
-    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
-                     grange(r, g, r.L, "g")},
-                    {xrange(r, o, r.L, "o"), srange(r, S_bnd, n_seg + 1, "S_bnd")}));
     const size_t need = chain_ws(r, n_seg, seg_len, tuning);
     if (need == 0) return fail(SF_E_SHAPE, "cannot size the chain workspace");
     if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
+                     grange(r, g, r.L, "g")},
+                    {xrange(r, o, r.L, "o"), srange(r, S_bnd, n_seg + 1, "S_bnd"), wsrange(ws, need)}));
     const size_t slot = (need - 2 * al((size_t)r.B * r.H * r.D * r.D * 4)) / 2;
     const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
     hipStream_t mn = (hipStream_t)main_s;
@@ -664,7 +671,7 @@ sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
         int ts;
         TRY(pick_ts(r, seg_len[i], tuning, ts));
         Seg &s = segs[i];
-        s = make_seg(r, seg_len[i], ts, (char *)ws + (i % 2) * slot, false);
+        s = make_seg(r, seg_len[i], ts, (char *)ws + (i % 2) * slot, false, timing_of(tuning));
         s.a.q = offset_x(r, q, tok);
         s.a.k = offset_x(r, k, tok);
         s.a.v = offset_x(r, v, tok);
@@ -714,19 +721,20 @@ sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
+    TRY(check_timing(tuning));
     TRY(check_segments(r, n_seg, seg_len));
     if (!q || !k || !v || !g || !S_bnd || !dO || !dq || !dk || !dv || !dg || !dS_init || !ws)
         return fail(SF_E_NULL, "q, k, v, g, S_bnd, dO, dq, dk, dv, dg, dS_init and ws are required");
     TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {dO, "dO"}, {dq, "dq"}, {dk, "dk"}, {dv, "dv"},
                      {S_bnd, "S_bnd"}, {dS_final, "dS_final"}, {dS_init, "dS_init"}, {ws, "ws"}}));
+    const size_t need = chain_ws(r, n_seg, seg_len, tuning);
+    if (need == 0) return fail(SF_E_SHAPE, "cannot size the chain workspace");
+    if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
     TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
                      grange(r, g, r.L, "g"), srange(r, S_bnd, n_seg, "S_bnd"), xrange(r, dO, r.L, "dO"),
                      srange(r, dS_final, 1, "dS_final")},
                     {xrange(r, dq, r.L, "dq"), xrange(r, dk, r.L, "dk"), xrange(r, dv, r.L, "dv"),
-                     grange(r, dg, r.L, "dg"), srange(r, dS_init, 1, "dS_init")}));
-    const size_t need = chain_ws(r, n_seg, seg_len, tuning);
-    if (need == 0) return fail(SF_E_SHAPE, "cannot size the chain workspace");
-    if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
+                     grange(r, dg, r.L, "dg"), srange(r, dS_init, 1, "dS_init"), wsrange(ws, need)}));
     const size_t gb = al((size_t)r.B * r.H * r.D * r.D * 4);
     const size_t slot = (need - 2 * gb) / 2;
     float *gbnd[2] = {(float *)((char *)ws + 2 * slot), (float *)((char *)ws + 2 * slot + gb)};
@@ -743,7 +751,7 @@ sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
         int ts;
         TRY(pick_ts(r, seg_len[i], tuning, ts));
         Seg &s = segs[i];
-        s = make_seg(r, seg_len[i], ts, (char *)ws + (i % 2) * slot, true);
+        s = make_seg(r, seg_len[i], ts, (char *)ws + (i % 2) * slot, true, timing_of(tuning));
         s.a.q = offset_x(r, q, tok);
         s.a.k = offset_x(r, k, tok);
         s.a.v = offset_x(r, v, tok);
@@ -796,9 +804,11 @@ size_t sf_conv_bwd_workspace_bytes(const sf_conv_shape *shape) {
 }
 
 sf_status sf_conv_fwd(const sf_conv_shape *shape, const void *x, const float *w, const float *tail_in, void *y,
-                      float *tail_out, sf_stream stream) {
+                      float *tail_out, const sf_tuning *tuning, sf_stream stream) {
+    g_err.clear();
     ConvShape r;
     TRY(conv_resolve(shape, r));
+    TRY(check_timing(tuning));
     const bool tail = r.W > 1;
     if (!w || (r.L > 0 && (!x || !y))) return fail(SF_E_NULL, "x, w and y are required");
     TRY(check_align({{x, "x"}, {y, "y"}}));
@@ -826,14 +836,16 @@ sf_status sf_conv_fwd(const sf_conv_shape *shape, const void *x, const float *w,
     a.sx_b = r.sx_b;
     a.sx_l = r.sx_l;
     if (a.nTB > 65535) return fail(SF_E_UNSUPPORTED, "L too large for one call (%lld tokens)", (long long)r.L);
-    return conv_run(SF_K_CONV_FWD, false, a, (hipStream_t)stream);
+    return conv_run(SF_K_CONV_FWD, false, a, (hipStream_t)stream, timing_of(tuning));
 }
 
 sf_status sf_conv_bwd(const sf_conv_shape *shape, const void *x, const float *w, const float *tail_in, const void *dy,
                       const float *dtail_out, void *dx, float *dw, float *dtail_in, void *ws, size_t ws_bytes,
-                      sf_stream stream) {
+                      const sf_tuning *tuning, sf_stream stream) {
+    g_err.clear();
     ConvShape r;
     TRY(conv_resolve(shape, r));
+    TRY(check_timing(tuning));
     const bool tail = r.W > 1;
     if (!w || !dw || (r.L > 0 && (!x || !dy || !dx))) return fail(SF_E_NULL, "x, w, dy, dx and dw are required");
     const size_t need = conv_ws_bytes(r);
@@ -868,7 +880,7 @@ sf_status sf_conv_bwd(const sf_conv_shape *shape, const void *x, const float *w,
     a.nTB = (int32_t)conv_nblocks(r, true);
     a.sx_b = r.sx_b;
     a.sx_l = r.sx_l;
-    return conv_run(SF_K_CONV_BWD, true, a, (hipStream_t)stream);
+    return conv_run(SF_K_CONV_BWD, true, a, (hipStream_t)stream, timing_of(tuning));
 }
 
 }  // extern "C"
@@ -1020,6 +1032,42 @@ GdnChainWs gdn_chain_ws(const Shape &r, const GdnPlan &p) {
     return w;
 }
 
+sf_status gdn_shape_ok(const Shape &r) {
+    if (r.io != SF_BF16) return fail(SF_E_UNSUPPORTED, "the gated delta rule needs bf16 I/O");
+    if (r.gate != SF_GATE_SCALAR) return fail(SF_E_UNSUPPORTED, "the gated delta rule takes a scalar gate");
+    return SF_OK;
+}
+
+// one kernel of the delta-rule pipeline; its timing kind is SF_K_GDN_PREP + phase
+sf_status gdn_launch(int phase, const sf::GdnArgs &a, int D, hipStream_t s, sf_timing *tm) {
+    if (phase == sf::GDN_DCHUNK && a.L < 64) return SF_OK;  // no chunk: nothing to launch
+    hipEvent_t e0, e1;
+    take_pair(tm, SF_K_GDN_PREP + phase, e0, e1);
+    const hipError_t e = sf::launch_gdn_phase(phase, a, D, s, e0, e1);
+    return e == hipSuccess ? SF_OK : hip_fail(e, "kernel launch");
+}
+
+
+// the phases of one delta-rule segment call, in order, on one stream
+sf_status gdn_run_fwd(const sf::GdnArgs &a, int D, hipStream_t s, sf_timing *tm) {
+    if (a.n_super > 1) {
+        TRY(gdn_launch(sf::GDN_PREP, a, D, s, tm));
+        TRY(gdn_launch(sf::GDN_SCAN, a, D, s, tm));
+    }
+    return gdn_launch(sf::GDN_OUT, a, D, s, tm);
+}
+sf_status gdn_run_bwd(const sf::GdnArgs &a, int D, hipStream_t s, sf_timing *tm) {
+    if (a.n_super > 1) {
+        TRY(gdn_launch(sf::GDN_PREP, a, D, s, tm));
+        TRY(gdn_launch(sf::GDN_SCAN, a, D, s, tm));
+        TRY(gdn_launch(sf::GDN_DPREP, a, D, s, tm));
+        TRY(gdn_launch(sf::GDN_DSCAN, a, D, s, tm));
+    }
+    TRY(gdn_launch(sf::GDN_STORE, a, D, s, tm));
+    TRY(gdn_launch(sf::GDN_DWALK, a, D, s, tm));
+    return gdn_launch(sf::GDN_DCHUNK, a, D, s, tm);
+}
+
 }  // namespace
 
 extern "C" {
@@ -1037,6 +1085,7 @@ sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const 
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
+    TRY(check_timing(tuning));
     if (r.io != SF_BF16) return fail(SF_E_UNSUPPORTED, "the gated delta rule needs bf16 I/O");
     if (r.gate != SF_GATE_SCALAR) return fail(SF_E_UNSUPPORTED, "the gated delta rule takes a scalar gate");
     if (!S_out || (r.L > 0 && (!q || !k || !v || !g || !beta || !o)))
@@ -1081,21 +1130,7 @@ sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const 
         a.wsM = (float *)((char *)ws + al(bh * a.n_super * SS));
         a.wsN = (float *)((char *)a.wsM + al(bh * (a.n_super - 1) * SS));
     }
-    bool on;
-    {
-        std::lock_guard<std::mutex> lk(g_prof_mu);
-        on = g_prof_on[SF_K_GDN_FWD];
-    }
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (on && (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess))
-        return hip_fail(hipGetLastError(), "profiling event");
-    hipError_t e = sf::launch_gdn_fwd(a, r.D, (hipStream_t)stream, e0, e1);
-    if (e != hipSuccess) return hip_fail(e, "kernel launch");
-    if (on) {
-        std::lock_guard<std::mutex> lk(g_prof_mu);
-        g_prof_ev[SF_K_GDN_FWD].push_back({e0, e1});
-    }
-    return SF_OK;
+    return gdn_run_fwd(a, r.D, (hipStream_t)stream, timing_of(tuning));
 }
 
 size_t sf_gdn_bwd_workspace_bytes(const sf_shape *shape, const sf_tuning *tuning) {
@@ -1112,6 +1147,7 @@ sf_status sf_gdn_bwd(const sf_shape *shape, const void *q, const void *k, const 
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
+    TRY(check_timing(tuning));
     if (r.io != SF_BF16) return fail(SF_E_UNSUPPORTED, "the gated delta rule needs bf16 I/O");
     if (r.gate != SF_GATE_SCALAR) return fail(SF_E_UNSUPPORTED, "the gated delta rule takes a scalar gate");
     if (!dS_in || (r.L > 0 && (!q || !k || !v || !g || !beta || !dO || !dq || !dk || !dv || !dg || !dbeta)))
@@ -1170,21 +1206,7 @@ sf_status sf_gdn_bwd(const sf_shape *shape, const void *q, const void *k, const 
     a.wsDc = (float *)(base + L.Dc);
     a.wsX = (float *)(base + L.X);
     a.n_x = L.n_x;
-    bool on;
-    {
-        std::lock_guard<std::mutex> lk(g_prof_mu);
-        on = g_prof_on[SF_K_GDN_BWD];
-    }
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (on && (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess))
-        return hip_fail(hipGetLastError(), "profiling event");
-    hipError_t e = sf::launch_gdn_bwd(a, r.D, (hipStream_t)stream, e0, e1);
-    if (e != hipSuccess) return hip_fail(e, "kernel launch");
-    if (on) {
-        std::lock_guard<std::mutex> lk(g_prof_mu);
-        g_prof_ev[SF_K_GDN_BWD].push_back({e0, e1});
-    }
-    return SF_OK;
+    return gdn_run_bwd(a, r.D, (hipStream_t)stream, timing_of(tuning));
 }
 
 size_t sf_gdn_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
@@ -1197,17 +1219,6 @@ size_t sf_gdn_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const 
     return gdn_chain_ws(r, p).total;
 }
 
-sf_status gdn_shape_ok(const Shape &r) {
-    if (r.io != SF_BF16) return fail(SF_E_UNSUPPORTED, "the gated delta rule needs bf16 I/O");
-    if (r.gate != SF_GATE_SCALAR) return fail(SF_E_UNSUPPORTED, "the gated delta rule takes a scalar gate");
-    return SF_OK;
-}
-
-sf_status gdn_launch(int phase, const sf::GdnArgs &a, int D, hipStream_t s) {
-    const hipError_t e = sf::launch_gdn_phase(phase, a, D, s, nullptr, nullptr);
-    return e == hipSuccess ? SF_OK : hip_fail(e, "kernel launch");
-}
-
 sf_status sf_gdn_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
                            const void *k, const void *v, const float *g, const float *beta, void *o, float *S_bnd,
                            void *v_new, void *ws, size_t ws_bytes, const sf_tuning *tuning, sf_stream main_s,
@@ -1215,6 +1226,7 @@ sf_status sf_gdn_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
+    TRY(check_timing(tuning));
     TRY(gdn_shape_ok(r));
     TRY(check_segments(r, n_seg, seg_len));
     if (!q || !k || !v || !g || !beta || !o || !S_bnd || !ws)
@@ -1263,26 +1275,26 @@ sf_status sf_gdn_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *
     for (int i = 0; i < n_seg; ++i) {
         sf::GdnArgs &a = seg[i];
         if (a.n_super > 1) {
-            TRY(gdn_launch(sf::GDN_PREP, a, r.D, mn));
+            TRY(gdn_launch(sf::GDN_PREP, a, r.D, mn, timing_of(tuning)));
             TRY(dep(mn, ax, e0));  // prep(i), and any S_bnd[i] written on main
-            TRY(gdn_launch(sf::GDN_SCAN, a, r.D, ax));
+            TRY(gdn_launch(sf::GDN_SCAN, a, r.D, ax, timing_of(tuning)));
             if (ax != mn) TRY(record(sd[i % 2], ax));
         }
         if (pending >= 0) {
             if (ax != mn) TRY(wait(mn, sd[pending % 2]));
-            TRY(gdn_launch(sf::GDN_OUT, seg[pending], r.D, mn));
+            TRY(gdn_launch(sf::GDN_OUT, seg[pending], r.D, mn, timing_of(tuning)));
             pending = -1;
         }
         if (a.n_super > 1) {
             pending = i;
         } else {
             if (ax != mn && i > 0 && seg[i - 1].n_super > 1) TRY(wait(mn, sd[(i - 1) % 2]));  // S_bnd[i]
-            TRY(gdn_launch(sf::GDN_OUT, a, r.D, mn));
+            TRY(gdn_launch(sf::GDN_OUT, a, r.D, mn, timing_of(tuning)));
         }
     }
     if (pending >= 0) {
         if (ax != mn) TRY(wait(mn, sd[pending % 2]));
-        TRY(gdn_launch(sf::GDN_OUT, seg[pending], r.D, mn));
+        TRY(gdn_launch(sf::GDN_OUT, seg[pending], r.D, mn, timing_of(tuning)));
     }
     if (ax != mn) TRY(dep(ax, mn, e1));
     return SF_OK;
@@ -1296,6 +1308,7 @@ sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
+    TRY(check_timing(tuning));
     TRY(gdn_shape_ok(r));
     TRY(check_segments(r, n_seg, seg_len));
     if (!q || !k || !v || !g || !beta || !S_bnd || !dO || !dq || !dk || !dv || !dg || !dbeta || !dS_init || !ws)
@@ -1362,22 +1375,22 @@ sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *
     for (int i = n_seg - 1; i >= 0; --i) {
         sf::GdnArgs &a = seg[i];
         if (a.n_super > 1) {
-            TRY(gdn_launch(sf::GDN_PREP, a, r.D, mn));
+            TRY(gdn_launch(sf::GDN_PREP, a, r.D, mn, timing_of(tuning)));
             TRY(dep(mn, ax, e0));
-            TRY(gdn_launch(sf::GDN_SCAN, a, r.D, ax));
+            TRY(gdn_launch(sf::GDN_SCAN, a, r.D, ax, timing_of(tuning)));
             if (ax != mn) TRY(record(sd[0], ax));
-            TRY(gdn_launch(sf::GDN_DPREP, a, r.D, mn));
+            TRY(gdn_launch(sf::GDN_DPREP, a, r.D, mn, timing_of(tuning)));
             TRY(dep(mn, ax, e1));  // dS prep, and dS_out written by the later segment's dS walk
-            TRY(gdn_launch(sf::GDN_DSCAN, a, r.D, ax));
+            TRY(gdn_launch(sf::GDN_DSCAN, a, r.D, ax, timing_of(tuning)));
             if (ax != mn) {
                 TRY(record(sd[1], ax));
                 TRY(wait(mn, sd[0]));
             }
         }
-        TRY(gdn_launch(sf::GDN_STORE, a, r.D, mn));
+        TRY(gdn_launch(sf::GDN_STORE, a, r.D, mn, timing_of(tuning)));
         if (a.n_super > 1 && ax != mn) TRY(wait(mn, sd[1]));
-        TRY(gdn_launch(sf::GDN_DWALK, a, r.D, mn));
-        TRY(gdn_launch(sf::GDN_DCHUNK, a, r.D, mn));
+        TRY(gdn_launch(sf::GDN_DWALK, a, r.D, mn, timing_of(tuning)));
+        TRY(gdn_launch(sf::GDN_DCHUNK, a, r.D, mn, timing_of(tuning)));
     }
     return SF_OK;
 }
@@ -1414,37 +1427,6 @@ sf_status sf_partition_hybrid(int64_t T, int32_t N, double alpha, double w_tok, 
         prev = c;
     }
     return SF_OK;
-}
-
-sf_status sf_prof_enable(int32_t kernel_id, int32_t on) {
-    if (kernel_id < 0 || kernel_id >= SF_K_COUNT) return fail(SF_E_SHAPE, "unknown kernel id %d", kernel_id);
-    std::lock_guard<std::mutex> lk(g_prof_mu);
-    g_prof_on[kernel_id] = on != 0;
-    return SF_OK;
-}
-
-sf_status sf_prof_read(int32_t kernel_id, double *total_ms, int64_t *launches) {
-    if (kernel_id < 0 || kernel_id >= SF_K_COUNT) return fail(SF_E_SHAPE, "unknown kernel id %d", kernel_id);
-    if (!total_ms || !launches) return fail(SF_E_NULL, "total_ms and launches are required");
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> evs;
-    {
-        std::lock_guard<std::mutex> lk(g_prof_mu);
-        evs.swap(g_prof_ev[kernel_id]);
-    }
-    double tot = 0.0;
-    sf_status rc = SF_OK;
-    for (auto &p : evs) {
-        float ms = 0.f;
-        hipError_t e = hipEventSynchronize(p.second);
-        if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.first, p.second);
-        if (e != hipSuccess && rc == SF_OK) rc = hip_fail(e, "profiling event");
-        tot += ms;
-        (void)hipEventDestroy(p.first);
-        (void)hipEventDestroy(p.second);
-    }
-    *total_ms = tot;
-    *launches = (int64_t)evs.size();
-    return rc;
 }
 
 }  // extern "C"

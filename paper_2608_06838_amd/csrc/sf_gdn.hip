@@ -1406,28 +1406,4 @@ hipError_t launch_gdn_phase(int phase, const GdnArgs &a, int D, hipStream_t s, h
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_gdn_bwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-    if (a.n_super > 1 && a.n_prep != a.n_super) return hipErrorInvalidValue;
-    hipError_t e = hipSuccess;
-    const bool multi = a.n_super > 1;
-    const int seq[] = {GDN_PREP, GDN_SCAN, GDN_DPREP, GDN_DSCAN, GDN_STORE, GDN_DWALK, GDN_DCHUNK};
-    bool first = true;
-    for (int ph : seq) {
-        if (!multi && (ph == GDN_PREP || ph == GDN_SCAN || ph == GDN_DPREP || ph == GDN_DSCAN)) continue;
-        const bool last = ph == GDN_DCHUNK;
-        if ((e = launch_gdn_phase(ph, a, D, s, first ? e0 : nullptr, last ? e1 : nullptr)) != hipSuccess) return e;
-        first = false;
-    }
-    return e;
-}
-
-hipError_t launch_gdn_fwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-    hipError_t e = hipSuccess;
-    if (a.n_super > 1) {
-        if ((e = launch_gdn_phase(GDN_PREP, a, D, s, e0, nullptr)) != hipSuccess) return e;
-        if ((e = launch_gdn_phase(GDN_SCAN, a, D, s, nullptr, nullptr)) != hipSuccess) return e;
-    }
-    return launch_gdn_phase(GDN_OUT, a, D, s, a.n_super > 1 ? nullptr : e0, e1);
-}
-
 }  // namespace sf

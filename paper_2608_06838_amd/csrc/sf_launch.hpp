@@ -92,8 +92,6 @@ struct GdnArgs {
 // (E_J), dS scan (dS_end(J)), dS walk, per-chunk gradients.
 enum GdnPhase { GDN_PREP, GDN_SCAN, GDN_OUT, GDN_STORE, GDN_DPREP, GDN_DSCAN, GDN_DWALK, GDN_DCHUNK };
 hipError_t launch_gdn_phase(int phase, const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
-hipError_t launch_gdn_fwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
-hipError_t launch_gdn_bwd(const GdnArgs &a, int D, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_conv(bool bwd, const ConvArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 
 }  // namespace sf

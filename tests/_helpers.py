@@ -1,5 +1,24 @@
 """Shared helpers for the parity tests: error metrics and oracle runs on
-selected (batch, head) pairs."""
+selected (batch, head) pairs.
+
+Parity bar (X the tested tensor, R the fp64 oracle, RMS = RMS(R)):
+  fp32 I/O:  max_i |X_i - R_i| / max(|R_i|, RMS) <= 1e-4 ("mixed"), and the
+             normwise error ||X - R|| / ||R|| <= 1e-5.
+  bf16 I/O:  the bound on max_i |X_i - R_i| / RMS is 2e-2.  A tensor stored
+             in bf16 cannot beat its own rounding: the rounding floor
+             floor = max_i |rne_bf16(R_i) - R_i| / RMS is computed and printed,
+             and where it exceeds 1e-2 the bound becomes floor + 2e-3.  That
+             is sound: a kernel whose value before the final rounding is off
+             by e_i lands either on rne(R_i) (error r_i) or on its neighbour,
+             which needs e_i >= h_i - r_i (h_i the half ulp) and gives an error
+             2 h_i - r_i <= r_i + 2 e_i; so the bound asks max e_i <= 1e-3 RMS.
+             The same argument is asserted element by element ("excess" =
+             max_i (|X_i - R_i| - r_i) / RMS <= 2e-3).  Regression bars: mixed
+             <= 8e-3 (one bf16 ulp; correct rounding gives 2^-8 = 3.9e-3) and
+             normwise <= 4e-3.  Tensors stored in fp32 (states, state
+             gradients, dg, dbeta) have no output rounding: max / RMS <= 2e-2
+             as stated for bf16 I/O, and mixed <= 2e-3.
+"""
 import os
 
 import numpy as np
@@ -7,10 +26,9 @@ import torch
 
 import oracle
 
-# Tolerances:
-#  fp32 I/O: elementwise relative error floored by the tensor RMS <= 1e-4.
-#  bf16 I/O: the same mixed metric <= 2e-2, and the normwise error <= 1e-2.
-TOL = {"f32": dict(mixed=1e-4, l2=1e-5), "bf16": dict(mixed=2e-2, l2=1e-2)}
+TOL = {"f32": dict(mixed=1e-4, l2=1e-5, max_over_rms=1e-4),
+       "bf16": dict(mixed=8e-3, l2=4e-3, max_over_rms=2e-2, excess=2e-3, floor_limit=1e-2,
+                    margin=2e-3, mixed_f32_out=2e-3)}
 
 
 def cores():
@@ -19,6 +37,14 @@ def cores():
 
 def to64(t):
     return t.detach().to("cpu").double().numpy()
+
+
+def rne_bf16(R):
+    """Round float64 values to bfloat16 (8 significant bits) to nearest, ties
+    to even: np.round rounds half to even."""
+    R = np.asarray(R, dtype=np.float64)
+    m, e = np.frexp(R)  # R = m 2^e, 0.5 <= |m| < 1
+    return np.ldexp(np.round(m * 256.0) / 256.0, e)
 
 
 def err(X, R, floor=0.0):
@@ -30,17 +56,42 @@ def err(X, R, floor=0.0):
     return dict(mixed=float(np.max(d / np.maximum(np.abs(R), rms))) if d.size else 0.0,
                 max_over_rms=float(d.max() / rms) if d.size else 0.0,
                 l2=float(np.linalg.norm(d) / max(np.linalg.norm(R), floor * np.sqrt(R.size), 1e-30))
-                if d.size else 0.0)
+                if d.size else 0.0, rms=rms)
 
 
 def assert_close(name, X, R, io, floor=0.0):
-    """floor: an extra lower bound on the error scale (used for dg, see dg_floor)."""
+    """X: the tested tensor (torch: its dtype says whether it is stored in
+    bf16; numpy: taken as stored in fp32).  io: the I/O mode of the call
+    ("f32" or "bf16").  floor: an extra lower bound on the error scale (only
+    the vector-gate tests of near-zero dg pass one, see dg_floor)."""
+    stored_bf16 = isinstance(X, torch.Tensor) and X.dtype == torch.bfloat16
+    X = to64(X) if isinstance(X, torch.Tensor) else np.asarray(X, dtype=np.float64)
+    R = np.asarray(R, dtype=np.float64)
+    assert X.shape == R.shape, f"{name}: shape {X.shape} != {R.shape}"
+    assert np.all(np.isfinite(X)), f"{name}: non-finite values"
     e = err(X, R, floor)
     tol = TOL[io]
-    print(f"  {name:7s} mixed={e['mixed']:.3e} max/rms={e['max_over_rms']:.3e} l2={e['l2']:.3e}",
+    if io == "f32":
+        print(f"  {name:7s} mixed={e['mixed']:.3e} max/rms={e['max_over_rms']:.3e} l2={e['l2']:.3e}", flush=True)
+        assert e["mixed"] <= tol["mixed"] and e["l2"] <= tol["l2"], f"{name}: {e} exceeds {tol}"
+        return e
+    if stored_bf16:
+        r = np.abs(rne_bf16(R) - R)
+        fl = float(r.max() / e["rms"]) if r.size else 0.0
+        excess = float(np.max(np.abs(X - R) - r) / e["rms"]) if r.size else 0.0
+        bound = tol["max_over_rms"] if fl <= tol["floor_limit"] else fl + tol["margin"]
+        e.update(floor=fl, excess=excess, bound=bound)
+        print(f"  {name:7s} mixed={e['mixed']:.3e} max/rms={e['max_over_rms']:.3e} (floor {fl:.3e}, "
+              f"bound {bound:.3e}) excess={excess:.3e} l2={e['l2']:.3e}", flush=True)
+        assert e["max_over_rms"] <= bound, f"{name}: max/rms {e['max_over_rms']:.3e} > {bound:.3e}"
+        assert excess <= tol["excess"], f"{name}: excess over rounding {excess:.3e} > {tol['excess']}"
+        assert e["mixed"] <= tol["mixed"], f"{name}: mixed {e['mixed']:.3e} > {tol['mixed']}"
+        assert e["l2"] <= tol["l2"], f"{name}: l2 {e['l2']:.3e} > {tol['l2']}"
+        return e
+    print(f"  {name:7s} mixed={e['mixed']:.3e} max/rms={e['max_over_rms']:.3e} l2={e['l2']:.3e} (fp32 out)",
           flush=True)
-    assert np.all(np.isfinite(np.asarray(X, dtype=np.float64))), f"{name}: non-finite values"
-    assert e["mixed"] <= tol["mixed"] and e["l2"] <= tol["l2"], f"{name}: {e} exceeds {tol}"
+    assert e["max_over_rms"] <= tol["max_over_rms"], f"{name}: max/rms {e['max_over_rms']:.3e} > 2e-2"
+    assert e["mixed"] <= tol["mixed_f32_out"], f"{name}: mixed {e['mixed']:.3e} > {tol['mixed_f32_out']}"
     return e
 
 
@@ -73,17 +124,40 @@ def oracle_run(inp, pairs=None, snap_pos=None):
     return dict(o=o, S_out=S_out, snaps=snaps, dq=dq, dk=dk, dv=dv, dg=dg, dS_in=dS_in, pairs=pairs)
 
 
+def token_terms(ref, q, k):
+    """The per-token terms q_t.dq_t and k_t.dk_t (per channel for the vector
+    gate) of the reference, whose telescoping sum is the decay gradient:
+    dg_t = sum_{t' >= t} (q.dq - k.dk)_{t'} plus the carry of later
+    superchunks."""
+    if ref["dg"].ndim == q.ndim:  # per-key-channel gate
+        return q * ref["dq"], k * ref["dk"]
+    return np.sum(q * ref["dq"], axis=-1), np.sum(k * ref["dk"], axis=-1)
+
+
 def dg_floor(ref, q, k):
-    """Scale of the per-token terms q_t.dq_t and k_t.dk_t (per channel for the
-    vector gate) whose telescoping sum
-    gives the decay gradient (dg_t = sum_{t'>=t} (q.dq - k.dk)_{t'} plus the
-    carry from later superchunks).  The kernels evaluate dg through that sum,
-    so its absolute error is relative to this scale; when the gate is so
-    strong that dg itself is many orders smaller (a_t ~ 0), this floor keeps
-    the metric meaningful."""
-    if ref["dg"].ndim == q.ndim:  # per-key-channel gate: dg per channel
-        qd, kd = q * ref["dq"], k * ref["dk"]
-    else:
-        qd = np.sum(q * ref["dq"], axis=-1)
-        kd = np.sum(k * ref["dk"], axis=-1)
+    """RMS of the per-token terms (see token_terms)."""
+    qd, kd = token_terms(ref, q, k)
     return float(np.sqrt(np.mean(qd * qd + kd * kd)))
+
+
+def assert_dg_apriori(name, X, ref, q, k, ts, ulps=64.0):
+    """Elementwise a-priori bound for a decay gradient that is many orders
+    below its per-token terms (near-memoryless gates, a_t ~ e^-30, where the
+    exact dg_t is ~1e-13 while q.dq and k.dk are O(1) and cancel).  The
+    kernels form dg_t as the suffix sum, within the ts-token superchunk, of
+    (q.dq - k.dk) computed in fp32, so |dg_t - exact| is at most a few fp32
+    ulps of sum_{t' >= t in the superchunk} (|q.dq| + |k.dk|)_{t'}; the test
+    asserts `ulps` of them (plus the fp32 rounding of that sum itself)."""
+    X = to64(X) if isinstance(X, torch.Tensor) else np.asarray(X, dtype=np.float64)
+    qd, kd = token_terms(ref, q, k)
+    m = np.abs(qd) + np.abs(kd)  # [1, L, P] or [1, L, P, D]
+    L = m.shape[1]
+    suf = np.zeros_like(m)
+    for s0 in range(0, L, ts):
+        blk = m[:, s0:s0 + ts]
+        suf[:, s0:s0 + ts] = np.flip(np.cumsum(np.flip(blk, axis=1), axis=1), axis=1)
+    bound = ulps * 2.0 ** -24 * suf + 1e-30
+    ratio = float(np.max(np.abs(X - ref["dg"]) / bound))
+    print(f"  {name:7s} |dg - ref| / ({ulps:g} fp32 ulps of the superchunk's suffix term sum): max {ratio:.3e}; "
+          f"max|ref| {float(np.max(np.abs(ref['dg']))):.3e}", flush=True)
+    assert ratio <= 1.0, f"{name}: dg exceeds its a-priori fp32 bound ({ratio:.3e})"

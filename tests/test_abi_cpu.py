@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
     assert set(declared) == set(_lib.EXPORTS), (declared, _lib.EXPORTS)
     for name in declared:
         assert hasattr(L, name), name
-    assert L.sf_abi_version() == 1
+    assert L.sf_abi_version() == 2
     assert L.sf_status_str(_lib.SF_E_ALIAS) == b"SF_E_ALIAS"
 
 
@@ -121,6 +121,38 @@ def test_pointer_validation():
     assert fwd(s, tun=t) == _lib.SF_E_SHAPE
 
 
+def test_workspace_alias():
+    """The workspace is an output: it may overlap no input and no other output
+    (segment and chain calls, both directions)."""
+    L = _lib.lib()
+    t = _tuning(ts=128)  # several superchunks: the calls need a workspace
+    s = shape()
+    assert fwd(s, ws=5, tun=t) == _lib.SF_E_ALIAS   # over o
+    assert fwd(s, ws=1, tun=t) == _lib.SF_E_ALIAS   # over q
+    assert fwd(s, ws=6, tun=t) == _lib.SF_E_ALIAS   # over S_out
+
+    def bwd(ws, dq=8):
+        args = [p(i) for i in (1, 2, 3, 4)] + [None, p(6), None] + [p(i) for i in (dq, 9, 10, 11, 12, ws)]
+        return L.sf_segment_bwd(ctypes.byref(s), *args, 1 << 30, ctypes.byref(t), None)
+
+    assert bwd(ws=8) == _lib.SF_E_ALIAS      # over dq
+    assert bwd(ws=6) == _lib.SF_E_ALIAS      # over dO
+    assert bwd(ws=12) == _lib.SF_E_ALIAS     # over dS_in
+    segs = (ctypes.c_int64 * 2)(512, 512)
+    rc = L.sf_chain_fwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), p(5), 1 << 30, None,
+                        None, None)
+    assert rc == _lib.SF_E_ALIAS             # workspace over o
+    rc = L.sf_chain_fwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), p(6), 1 << 30, None,
+                        None, None)
+    assert rc == _lib.SF_E_ALIAS             # workspace over S_bnd
+    rc = L.sf_chain_bwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, p(8), p(9),
+                        p(10), p(11), p(12), p(8), 1 << 30, None, None, None)
+    assert rc == _lib.SF_E_ALIAS             # workspace over dq
+    rc = L.sf_chain_bwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, p(8), p(9),
+                        p(10), p(11), p(12), p(5), 1 << 30, None, None, None)
+    assert rc == _lib.SF_E_ALIAS             # workspace over S_bnd (an input of the backward)
+
+
 def test_chain_validation():
     L = _lib.lib()
     s = shape(L=1024)
@@ -135,8 +167,21 @@ def test_chain_validation():
     rc = L.sf_chain_bwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, p(8), p(9),
                         p(10), p(11), None, p(13), 1 << 30, None, None, None)
     assert rc == _lib.SF_E_NULL  # dS_init missing
-    rc = L.sf_prof_enable(99, 1)
-    assert rc == _lib.SF_E_SHAPE
+
+
+def test_timing_validation():
+    """A caller's timing record is checked before any launch."""
+    tm = _lib.SfTiming()
+    t = _tuning()
+    t.timing = ctypes.pointer(tm)
+    s = shape()
+    tm.capacity, tm.count = 4, 5
+    assert fwd(s, tun=t) == _lib.SF_E_SHAPE      # count beyond capacity
+    tm.capacity, tm.count = -1, 0
+    assert fwd(s, tun=t) == _lib.SF_E_SHAPE
+    tm.capacity, tm.count = 4, 0
+    assert fwd(s, tun=t) == _lib.SF_E_NULL       # no event arrays
+    assert conv_fwd(conv_shape(), tun=t) == _lib.SF_E_NULL
 
 
 # ------------------------------------------------------------ short convolution
@@ -148,14 +193,15 @@ def conv_shape(**kw):
     return s
 
 
-def conv_fwd(s, x=1, w=2, tail_in=3, y=4, tail_out=5):
+def conv_fwd(s, x=1, w=2, tail_in=3, y=4, tail_out=5, tun=None):
     args = [p(i) if i is not None else None for i in (x, w, tail_in, y, tail_out)]
-    return _lib.lib().sf_conv_fwd(ctypes.byref(s) if s is not None else None, *args, None)
+    return _lib.lib().sf_conv_fwd(ctypes.byref(s) if s is not None else None, *args,
+                                  ctypes.byref(tun) if tun is not None else None, None)
 
 
 def conv_bwd(s, x=1, w=2, tail_in=3, dy=4, dtail_out=5, dx=6, dw=7, dtail_in=8, ws=9, ws_bytes=1 << 30):
     args = [p(i) if i is not None else None for i in (x, w, tail_in, dy, dtail_out, dx, dw, dtail_in, ws)]
-    return _lib.lib().sf_conv_bwd(ctypes.byref(s), *args, ws_bytes, None)
+    return _lib.lib().sf_conv_bwd(ctypes.byref(s), *args, ws_bytes, None, None)
 
 
 def test_conv_workspace_bytes():
@@ -191,7 +237,7 @@ def test_conv_pointer_validation():
     assert conv_fwd(None) == _lib.SF_E_NULL
     assert conv_fwd(s, x=None) == _lib.SF_E_NULL
     assert conv_fwd(s, w=None) == _lib.SF_E_NULL
-    rc = _lib.lib().sf_conv_fwd(ctypes.byref(s), ctypes.c_void_p(FAKE + 8), p(2), p(3), p(4), p(5), None)
+    rc = _lib.lib().sf_conv_fwd(ctypes.byref(s), ctypes.c_void_p(FAKE + 8), p(2), p(3), p(4), p(5), None, None)
     assert rc == _lib.SF_E_ALIGN
     assert conv_fwd(s, y=1) == _lib.SF_E_ALIAS          # y over x
     assert conv_fwd(s, tail_out=2) == _lib.SF_E_ALIAS   # tail_out over w

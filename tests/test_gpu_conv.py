@@ -51,7 +51,7 @@ def compare(got, ref, io, W):
             continue
         if ref[name].size == 0:
             continue
-        assert_close(name, to64(got[name]), ref[name], io)
+        assert_close(name, got[name], ref[name], io)
 
 
 @pytest.mark.parametrize("io", ["bf16", "f32"])

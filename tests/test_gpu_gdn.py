@@ -51,9 +51,9 @@ def test_gdn_parity(D):
     assert torch.equal(o, o2) and torch.equal(S, S2)
     ro, rS, ru = gdn.forward(*(to64(inp[x]) for x in ("q", "k", "v", "g", "beta", "S_in")), threads=cores(),
                              with_u=True)
-    assert_close("o", to64(o), ro, "bf16")
-    assert_close("S_out", to64(S), rS, "bf16")
-    assert_close("v_new", to64(vn), ru, "bf16")
+    assert_close("o", o, ro, "bf16")
+    assert_close("S_out", S, rS, "bf16")
+    assert_close("v_new", vn, ru, "bf16")
 
 
 @pytest.mark.parametrize("D", [64, 128])
@@ -67,8 +67,8 @@ def test_gdn_superchunks(D, ts):
     inp = synth.make_gdn_inputs(B, L, H, D, seed=4500 + D + ts)
     o, S = run(inp, ts)
     ro, rS = ref(inp)
-    assert_close("o", to64(o), ro, "bf16")
-    assert_close("S_out", to64(S), rS, "bf16")
+    assert_close("o", o, ro, "bf16")
+    assert_close("S_out", S, rS, "bf16")
 
 
 def test_gdn_no_state_and_empty():
@@ -76,8 +76,8 @@ def test_gdn_no_state_and_empty():
     inp = synth.make_gdn_inputs(1, 192, 2, 128, seed=4200, s_in_std=0.0)
     o, S = run(inp)
     ro, rS = ref(inp)
-    assert_close("o", to64(o), ro, "bf16")
-    assert_close("S_out", to64(S), rS, "bf16")
+    assert_close("o", o, ro, "bf16")
+    assert_close("S_out", S, rS, "bf16")
     e = synth.make_gdn_inputs(1, 0, 2, 128, seed=4201)
     _, S0 = run(e)
     assert torch.equal(S0.cpu(), e["S_in"])
@@ -99,8 +99,8 @@ def test_gdn_chained_segments():
         t += n
     torch.cuda.synchronize()
     ro, rS = ref(inp)
-    assert_close("o", to64(torch.cat(outs, 1)), ro, "bf16")
-    assert_close("S_out", to64(S), rS, "bf16")
+    assert_close("o", torch.cat(outs, 1), ro, "bf16")
+    assert_close("S_out", S, rS, "bf16")
 
 
 def test_gdn_long_segment_sampled():
@@ -111,8 +111,8 @@ def test_gdn_long_segment_sampled():
     o, S = run(inp)
     heads = [0, 5]
     ro, rS = ref(inp, heads)
-    assert_close("o", to64(o[:, :, heads]), ro, "bf16")
-    assert_close("S_out", to64(S[:, heads]), rS, "bf16")
+    assert_close("o", o[:, :, heads], ro, "bf16")
+    assert_close("S_out", S[:, heads], rS, "bf16")
     assert np.isfinite(to64(o)).all()
 
 
@@ -138,7 +138,7 @@ def ref_bwd(inp, dO, dS_out, heads=None):
 
 def check_bwd(got, want):
     for name, x, r in zip(("dq", "dk", "dv", "dg", "dbeta", "dS_in"), got, want):
-        assert_close(name, to64(x), r, "bf16")
+        assert_close(name, x, r, "bf16")
 
 
 def grads_inputs(inp, seed):
@@ -238,8 +238,8 @@ def test_gdn_head_major_layout():
     torch.cuda.synchronize()
     assert o.stride() == q.stride() and grads[3].stride() == g.stride()
     ro, rS = ref(inp)
-    assert_close("o", to64(o), ro, "bf16")
-    assert_close("S_out", to64(S), rS, "bf16")
+    assert_close("o", o, ro, "bf16")
+    assert_close("S_out", S, rS, "bf16")
     check_bwd(grads, ref_bwd(inp, dO, dS_out))
 
 
@@ -260,8 +260,8 @@ def test_gdn_full_size_segment_sampled():
     cpu = {k: v[:, :, heads].cpu() for k, v in inp.items() if k != "S_in"}
     cpu["S_in"] = inp["S_in"][:, heads].cpu()
     ro, rS = ref(cpu)
-    assert_close("o", to64(o[:, :, heads]), ro, "bf16")
-    assert_close("S_out", to64(S[:, heads]), rS, "bf16")
+    assert_close("o", o[:, :, heads], ro, "bf16")
+    assert_close("S_out", S[:, heads], rS, "bf16")
     sub = [x[:, :, heads] for x in grads[:5]] + [grads[5][:, heads]]
     check_bwd(sub, ref_bwd(cpu, dO[:, :, heads].cpu(), dS_out[:, heads].cpu()))
 
@@ -290,13 +290,13 @@ def test_gdn_chain_entry_points(D, ts):
     o, S_bnd, vn = res[True][:3]
     ro, rS, ru = gdn.forward(*(to64(inp[x]) for x in ("q", "k", "v", "g", "beta", "S_in")), threads=cores(),
                              with_u=True)
-    assert_close("o", to64(o), ro, "bf16")
-    assert_close("v_new", to64(vn), ru, "bf16")
-    assert_close("S_out", to64(S_bnd[-1]), rS, "bf16")
+    assert_close("o", o, ro, "bf16")
+    assert_close("v_new", vn, ru, "bf16")
+    assert_close("S_out", S_bnd[-1], rS, "bf16")
     t = 0
     for i, n in enumerate(segs[:-1]):  # interior boundary states
         t += n
         _, Si = gdn.forward(*(to64(inp[x][:, :t]) for x in ("q", "k", "v", "g", "beta")), to64(inp["S_in"]),
                             threads=cores())
-        assert_close(f"S_bnd{i + 1}", to64(S_bnd[i + 1]), Si, "bf16")
+        assert_close(f"S_bnd{i + 1}", S_bnd[i + 1], Si, "bf16")
     check_bwd(res[True][3:], ref_bwd(inp, dO, dS_final))

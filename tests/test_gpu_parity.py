@@ -10,7 +10,7 @@ import torch
 
 import paper_2608_06838_amd as sf
 from paper_2608_06838_amd import synth
-from tests._helpers import assert_close, dg_floor, oracle_run, select, select_state, to64
+from tests._helpers import assert_close, assert_dg_apriori, oracle_run, select, select_state, to64
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -27,13 +27,19 @@ def on_gpu(inp):
     return out
 
 
-def check_all(io, got, ref, inp, names=("o", "S_out", "dq", "dk", "dv", "dg", "dS_in")):
+def check_all(io, got, ref, inp, names=("o", "S_out", "dq", "dk", "dv", "dg", "dS_in"), dg_apriori_ts=None):
+    """Every output against the oracle.  dg_apriori_ts: for near-memoryless
+    gates, whose exact dg is ~1e-13, dg is held to its elementwise fp32 bound
+    over superchunks of that many tokens instead of the relative bar."""
     pairs = ref["pairs"]
-    fl = dg_floor(ref, to64(select(inp["q"], pairs)), to64(select(inp["k"], pairs)))
     for n in names:
         X = got[n]
         X = select_state(X, pairs) if n in ("S_out", "dS_in") else select(X, pairs)
-        assert_close(n, to64(X), ref[n], io, floor=fl if n == "dg" else 0.0)
+        if n == "dg" and dg_apriori_ts:
+            assert_dg_apriori(n, X, ref, to64(select(inp["q"], pairs)), to64(select(inp["k"], pairs)),
+                              dg_apriori_ts)
+        else:
+            assert_close(n, X, ref[n], io)
 
 
 def seg_case(w, L, ts, seed, dS_std=0.1, s_in_std=None):
@@ -73,7 +79,17 @@ def test_fp32_strong_decay_and_memoryless():
     """Very negative gates (a_t -> 0): each token sees only itself."""
     w = synth.workload("tiny_fp32", g_mu=-30.0)
     inp, got = seg_case(w, 256, 128, seed=3)
-    check_all("f32", got, oracle_run(inp), inp)
+    check_all("f32", got, oracle_run(inp), inp, dg_apriori_ts=128)
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_strong_decay_dg(io):
+    """a_t ~ e^-3 (x ~ N(-3, 1)): a short memory, yet dg is of the order of its
+    per-token terms, so it is held to the plain relative bar."""
+    w = synth.workload("tiny_fp32", g_mu=-3.0) if io == "f32" else synth.workload("mid_bf16", B=1, H=2, D=128,
+                                                                                    g_mu=-3.0)
+    inp, got = seg_case(w, 512, 128, seed=13)
+    check_all(io, got, oracle_run(inp), inp)
 
 
 def test_empty_segment():
@@ -105,7 +121,7 @@ def check_chain(io, inp, got, seg_lens, pairs=None):
     for i in range(1, len(pos) - 1):  # interior boundary states
         X = got["S_bnd"][i]
         X = select_state(X, ref["pairs"])
-        assert_close(f"S_bnd{i}", to64(X), ref["snaps"][i], io)
+        assert_close(f"S_bnd{i}", X, ref["snaps"][i], io)
 
 
 @pytest.mark.parametrize("ts", [0, 64, 128])
@@ -147,17 +163,19 @@ def test_scan_stress_sampled():
 
 def test_ctx256k_sampled():
     """B=1, H=40, d=128, L=262144 in 8 nonuniform segments (the 256K-context
-    workload).  Full-size run; the oracle checks one head end to end; the run
-    is repeated and must be bitwise identical."""
+    workload) with a nonzero gradient of the final state.  Full-size run; the
+    oracle checks the first, a middle and the last head end to end, interior
+    boundary states included; the run is repeated and every output must be
+    bitwise identical."""
     w = synth.workload("ctx256k_h40")
     say("[chain] ctx256k_h40 full size")
-    inp = synth.make_inputs(w, device=DEV, seed=1002, dS_out_std=0.0)
+    inp = synth.make_inputs(w, device=DEV, seed=1002, dS_out_std=0.1)
     got = run_chain(inp, w["seg_lens"])
     again = run_chain(inp, w["seg_lens"])
-    for key in ("o", "dq", "dg", "dS_in"):
+    for key in ("o", "S_bnd", "dq", "dk", "dv", "dg", "dS_in"):
         assert torch.equal(got[key], again[key]), key
-    say("[chain] ctx256k_h40 oracle on head 17")
-    check_chain("bf16", inp, got, w["seg_lens"], pairs=[(0, 17)])
+    say("[chain] ctx256k_h40 oracle on heads 0, 17, 39")
+    check_chain("bf16", inp, got, w["seg_lens"], pairs=[(0, 0), (0, 17), (0, 39)])
 
 
 # ------------------------------------------------------------------ vector gate
@@ -178,7 +196,7 @@ def test_vector_gate_decay_regimes(g_mu):
     token by token; the rest take the tiled path."""
     w = synth.workload("vector_gate", B=1, H=2, D=128, g_mu=g_mu)
     inp, got = seg_case(w, 512, 128, seed=41, s_in_std=0.1)
-    check_all("bf16", got, oracle_run(inp), inp)
+    check_all("bf16", got, oracle_run(inp), inp, dg_apriori_ts=128 if g_mu < -10 else None)
 
 
 @pytest.mark.parametrize("ts", [0, 64])
