@@ -1,4 +1,5 @@
-"""fp64 oracle of the hybrid-aware segment lengths.
+"""Oracle of the hybrid-aware segment lengths, in exact rational arithmetic
+where it decides an integer.
 
 TEST INFRASTRUCTURE ONLY (tests/ may use it; the product path never does).
 
@@ -9,19 +10,28 @@ asks for the boundaries that make every Cost_i equal, interpolates them with
 the equal-length boundaries i T / N by alpha, and rounds each boundary to the
 closest multiple of round_to (half-way cases up, this package's reading).
 
-The balanced boundaries are found here one at a time by bisection: c_i is the
-point where the summed cost of the segments before it reaches i / N of the
-total.  Pinned by tests/test_partition.py (equal per-segment costs at
-alpha = 1, the equal-length cases, a closed form for w_tok = 0).
+The summed cost of the segments before a cut at c telescopes to
+A(c) = w_tok c + w_soft c^2 / 2, so the balanced boundary c_i^hyb is where A
+reaches i / N of A(T).  Bisection gives c_i^hyb in floating point (used for
+the cost pins and as a first guess); the rounded boundary is then decided
+exactly: with every input taken at its exact value (fractions.Fraction),
+c_i(alpha) >= y holds iff
+    alpha = 0:  i T / N >= y
+    alpha > 0:  x <= 0 or A(x) <= (i / N) A(T),  x = (y - (1 - alpha) i T / N) / alpha
+(A increases on x >= 0 and c_i^hyb >= 0), and the rounded boundary is the
+multiple m * round_to with (m - 1/2) round_to <= c_i(alpha) < (m + 1/2) round_to.
+Pinned by tests/test_partition.py (equal per-segment costs at alpha = 1, the
+equal-length cases, the closed form for w_tok = 0, exact ties).
 """
 import math
+from fractions import Fraction
 
 
 def prefix_cost(c, w_tok, w_soft):
     """Summed cost of the segments covering tokens [0, c): sum_i Cost_i for a
     cut at c, which telescopes to w_tok c + w_soft c^2 / 2 whatever the cuts
     inside [0, c) are."""
-    return w_tok * c + 0.5 * w_soft * c * c
+    return w_tok * c + w_soft * c * c / 2
 
 
 def balanced_boundaries(T, N, w_tok, w_soft, iters=200):
@@ -43,15 +53,39 @@ def balanced_boundaries(T, N, w_tok, w_soft, iters=200):
 
 
 def candidate_boundaries(T, N, alpha, w_tok, w_soft):
-    """Unrounded c_i(alpha) = (1 - alpha) i T / N + alpha c_i^hybrid."""
+    """Unrounded c_i(alpha) = (1 - alpha) i T / N + alpha c_i^hybrid (floats)."""
     hyb = balanced_boundaries(T, N, w_tok, w_soft)
     return [(1.0 - alpha) * (T * i / N) + alpha * hyb[i] for i in range(N + 1)]
+
+
+def boundary_at_least(T, N, i, alpha, w_tok, w_soft, y):
+    """Exactly: is c_i(alpha) >= y?  (inputs at their exact values)"""
+    a, p, s, y = Fraction(alpha), Fraction(w_tok), Fraction(w_soft), Fraction(y)
+    equal = Fraction(i * T, N)
+    if a == 0:
+        return equal >= y
+    x = (y - (1 - a) * equal) / a
+    if x <= 0:
+        return True
+    return prefix_cost(x, p, s) <= Fraction(i, N) * prefix_cost(Fraction(T), p, s)
+
+
+def rounded_boundary(T, N, i, alpha, w_tok, w_soft, round_to, guess):
+    """The multiple of round_to closest to c_i(alpha), half-way cases up,
+    starting the exact search from the floating-point guess."""
+    m = int(math.floor(guess / round_to + 0.5))
+    half = Fraction(round_to, 2)
+    while not boundary_at_least(T, N, i, alpha, w_tok, w_soft, m * round_to - half):
+        m -= 1
+    while boundary_at_least(T, N, i, alpha, w_tok, w_soft, m * round_to + half):
+        m += 1
+    return m * round_to
 
 
 def partition_hybrid(T, N, alpha, w_tok, w_soft, round_to=128):
     """Segment lengths, or None when rounding leaves a segment empty."""
     c = candidate_boundaries(T, N, alpha, w_tok, w_soft)
-    r = [0] + [int(math.floor(x / round_to + 0.5)) * round_to for x in c[1:-1]] + [T]
+    r = [0] + [rounded_boundary(T, N, i, alpha, w_tok, w_soft, round_to, c[i]) for i in range(1, N)] + [T]
     lens = [r[i + 1] - r[i] for i in range(N)]
     return lens if all(x > 0 for x in lens) else None
 

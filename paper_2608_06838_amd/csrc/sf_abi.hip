@@ -520,6 +520,134 @@ size_t chain_ws(const Shape &r, int32_t n_seg, const int64_t *seg_len, const sf_
     return 2 * al(slot) + 2 * gbnd;
 }
 
+// ------------------------------------------------- exact partition rounding
+// The boundary c_i(alpha) = (1 - alpha) i T / N + alpha c_i^hyb, with
+// A(c_i^hyb) = (i / N) A(T) and A(c) = w_tok c + w_soft c^2 / 2, is compared
+// with a half-way point y = (2m + 1) R / 2 exactly, the fp64 inputs taken at
+// their exact values.  With K = (2m + 1) R N, J = 2 i T, U = K - J and
+// Z = U + alpha J (so y = K / 2N and c_i(alpha) >= y iff c_i^hyb >= Z / 2N alpha),
+// multiplying A(Z / 2N alpha) <= (i / N) A(T) by 8 N^2 alpha^2 gives
+//     c_i(alpha) >= y  iff  alpha = 0 and U <= 0,  or  Z <= 0,  or  F <= 0,
+//     F = 4 N U (alpha w_tok) + U^2 w_soft + 2 U J (alpha w_soft) + 4 i T^2 (i - N) (alpha^2 w_soft).
+// Every term is an integer times a product of doubles, i.e. an integer times a
+// power of two; their sum is formed exactly in a fixed-size big integer.
+constexpr int64_t kPartMaxT = int64_t(1) << 40;
+constexpr int32_t kPartMaxN = 1 << 20;
+
+struct BigInt {  // sign and magnitude, little-endian 64-bit limbs
+    static constexpr int W = 112;  // 7168 bits: every term below, shifted by any exponent gap of three doubles
+    bool neg = false;
+    uint64_t w[W] = {};
+    bool zero() const {
+        for (uint64_t x : w)
+            if (x) return false;
+        return true;
+    }
+};
+void big_mul_small(BigInt &a, uint64_t m) {
+    unsigned __int128 carry = 0;
+    for (int i = 0; i < BigInt::W; ++i) {
+        const unsigned __int128 t = (unsigned __int128)a.w[i] * m + carry;
+        a.w[i] = (uint64_t)t;
+        carry = t >> 64;
+    }
+}
+void big_shl(BigInt &a, int k) {
+    const int q = k / 64, r = k % 64;
+    for (int i = BigInt::W - 1; i >= 0; --i) {
+        uint64_t v = i - q >= 0 ? a.w[i - q] << r : 0;
+        if (r && i - q - 1 >= 0) v |= a.w[i - q - 1] >> (64 - r);
+        a.w[i] = v;
+    }
+}
+int big_cmp_mag(const BigInt &a, const BigInt &b) {
+    for (int i = BigInt::W - 1; i >= 0; --i)
+        if (a.w[i] != b.w[i]) return a.w[i] < b.w[i] ? -1 : 1;
+    return 0;
+}
+void big_add(BigInt &acc, const BigInt &t) {  // acc += t (signed)
+    if (acc.neg == t.neg) {
+        unsigned __int128 carry = 0;
+        for (int i = 0; i < BigInt::W; ++i) {
+            const unsigned __int128 s = (unsigned __int128)acc.w[i] + t.w[i] + carry;
+            acc.w[i] = (uint64_t)s;
+            carry = s >> 64;
+        }
+        return;
+    }
+    const bool acc_bigger = big_cmp_mag(acc, t) >= 0;
+    const BigInt &hi = acc_bigger ? acc : t, &lo = acc_bigger ? t : acc;
+    BigInt d;
+    d.neg = hi.neg;
+    uint64_t borrow = 0;
+    for (int i = 0; i < BigInt::W; ++i) {
+        const uint64_t a = hi.w[i], b = lo.w[i];
+        d.w[i] = a - b - borrow;
+        borrow = (a < b || (a == b && borrow)) ? 1 : 0;
+    }
+    acc = d;
+}
+// x = mant * 2^ex with mant a non-negative integer below 2^53 (x finite, >= 0)
+void split_double(double x, uint64_t &mant, int &ex) {
+    int e = 0;
+    const double f = std::frexp(x, &e);  // x = f 2^e, 0.5 <= f < 1 (or 0)
+    mant = (uint64_t)std::ldexp(f, 53);
+    ex = e - 53;
+}
+struct Term {
+    __int128 coef;   // integer factor
+    int nd;          // number of doubles multiplied in
+    uint64_t m[3];   // their mantissas
+    int ex;          // sum of their exponents
+};
+// sign (-1, 0, 1) of sum_k coef_k * prod mantissas * 2^ex_k, exactly
+int exact_sign(const Term *t, int n) {
+    int emin = 0;
+    bool any = false;
+    for (int k = 0; k < n; ++k) {
+        bool nz = t[k].coef != 0;
+        for (int j = 0; j < t[k].nd; ++j) nz = nz && t[k].m[j] != 0;
+        if (nz && (!any || t[k].ex < emin)) emin = t[k].ex;
+        any = any || nz;
+    }
+    if (!any) return 0;
+    BigInt acc;
+    for (int k = 0; k < n; ++k) {
+        bool nz = t[k].coef != 0;
+        for (int j = 0; j < t[k].nd; ++j) nz = nz && t[k].m[j] != 0;
+        if (!nz) continue;
+        BigInt b;
+        const unsigned __int128 mag = t[k].coef < 0 ? (unsigned __int128)(-t[k].coef) : (unsigned __int128)t[k].coef;
+        b.w[0] = (uint64_t)mag;
+        b.w[1] = (uint64_t)(mag >> 64);
+        b.neg = t[k].coef < 0;
+        for (int j = 0; j < t[k].nd; ++j) big_mul_small(b, t[k].m[j]);
+        big_shl(b, t[k].ex - emin);
+        big_add(acc, b);
+    }
+    if (acc.zero()) return 0;
+    return acc.neg ? -1 : 1;
+}
+// exactly: is c_i(alpha) >= (odd * R) / 2 ?
+bool part_at_least(int64_t T, int32_t N, int32_t i, double alpha, double w_tok, double w_soft, int32_t R,
+                   int64_t odd) {
+    const __int128 K = (__int128)odd * R * N, J = (__int128)2 * i * T, U = K - J;
+    if (alpha == 0.0) return U <= 0;
+    uint64_t ma, mp, ms;
+    int ea, ep, es;
+    split_double(alpha, ma, ea);
+    split_double(w_tok, mp, ep);
+    split_double(w_soft, ms, es);
+    const Term z[2] = {{U, 0, {0, 0, 0}, 0}, {J, 1, {ma, 0, 0}, ea}};  // Z = U + alpha J
+    if (exact_sign(z, 2) <= 0) return true;
+    const __int128 T2 = (__int128)T * T;
+    const Term f[4] = {{4 * (__int128)N * U, 2, {ma, mp, 0}, ea + ep},
+                       {U * U, 1, {ms, 0, 0}, es},
+                       {2 * U * J, 2, {ma, ms, 0}, ea + es},
+                       {4 * (__int128)i * T2 * (i - N), 3, {ma, ma, ms}, 2 * ea + es}};
+    return exact_sign(f, 4) <= 0;
+}
+
 }  // namespace
 
 // ===================================================================== ABI
@@ -1397,16 +1525,19 @@ sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *
 
 sf_status sf_partition_hybrid(int64_t T, int32_t N, double alpha, double w_tok, double w_soft, int32_t round_to,
                               int64_t *seg_len) {
+    g_err.clear();
     if (!seg_len) return fail(SF_E_NULL, "seg_len is NULL");
-    if (T <= 0 || N < 1 || round_to < 1 || T % round_to)
-        return fail(SF_E_SHAPE, "need T > 0 a multiple of round_to >= 1 and N >= 1 (T=%lld N=%d round_to=%d)",
+    if (T <= 0 || T > kPartMaxT || N < 1 || N > kPartMaxN || round_to < 1 || T % round_to)
+        return fail(SF_E_SHAPE,
+                    "need 0 < T <= 2^40 a multiple of round_to >= 1 and 1 <= N <= 2^20 (T=%lld N=%d round_to=%d)",
                     (long long)T, N, round_to);
     if (!(alpha >= 0.0) || !(w_tok >= 0.0) || !(w_soft >= 0.0) || !(w_tok + w_soft > 0.0) || !std::isfinite(alpha) ||
         !std::isfinite(w_tok) || !std::isfinite(w_soft))
         return fail(SF_E_SHAPE, "need alpha >= 0, w_tok >= 0, w_soft >= 0, not both weights 0");
     // accumulated cost A(c) = w_tok c + w_soft c^2 / 2 (Cost_i = A(c_{i+1}) - A(c_i));
     // the balanced boundary solves A(c) = (i / N) A(T), the positive root of a
-    // quadratic, written in the cancellation-free form 2 r / (w_tok + sqrt(w_tok^2 + 2 w_soft r))
+    // quadratic, written in the cancellation-free form 2 r / (w_tok + sqrt(w_tok^2 + 2 w_soft r)).
+    // That fp64 value is a first guess; the rounding is then decided exactly.
     const double Td = (double)T, total = w_tok * Td + 0.5 * w_soft * Td * Td;
     int64_t prev = 0;
     for (int32_t i = 1; i <= N; ++i) {
@@ -1418,7 +1549,13 @@ sf_status sf_partition_hybrid(int64_t T, int32_t N, double alpha, double w_tok, 
             const double hyb = 2.0 * r / (w_tok + std::sqrt(w_tok * w_tok + 2.0 * w_soft * r));
             const double equal = Td * (double)i / (double)N;
             const double x = (1.0 - alpha) * equal + alpha * hyb;
-            c = (int64_t)std::floor(x / round_to + 0.5) * round_to;
+            // closest multiple of round_to, half-way cases up: the m with
+            // (m - 1/2) R <= c_i < (m + 1/2) R, found exactly from the guess
+            int64_t m = (int64_t)std::floor(x / round_to + 0.5);
+            m = std::max<int64_t>(0, std::min<int64_t>(m, T / round_to));
+            while (m > 0 && !part_at_least(T, N, i, alpha, w_tok, w_soft, round_to, 2 * m - 1)) --m;
+            while (m < T / round_to && part_at_least(T, N, i, alpha, w_tok, w_soft, round_to, 2 * m + 1)) ++m;
+            c = m * round_to;
         }
         if (c <= prev || c > T)
             return fail(SF_E_SHAPE, "segment %d is empty or out of range after rounding (boundary %lld)", i - 1,

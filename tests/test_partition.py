@@ -52,13 +52,12 @@ def test_rounding():
 
 
 def test_library_matches_oracle():
-    """sf_partition_hybrid (closed-form root) against the oracle (bisection).
-    A boundary within 1e-6 tokens of a rounding midpoint can round either way
-    in fp64 (the two sides reach it by different arithmetic); such draws are
-    skipped: about a quarter of these seeds, mostly equal-length splits whose
-    boundaries fall exactly half-way between multiples of round_to."""
+    """sf_partition_hybrid (closed-form root, exact rounding decision) against
+    the oracle (bisection, exact rational rounding decision), integer for
+    integer on every draw: equal-length splits whose boundaries fall exactly
+    half-way between multiples of round_to included."""
     rng = random.Random(42)
-    checked = 0
+    ties = 0
     for _ in range(400):
         round_to = rng.choice([64, 128, 256, 2048])
         T = round_to * rng.randint(16, 4096)
@@ -67,16 +66,51 @@ def test_library_matches_oracle():
         w_tok = rng.choice([0.0, 1.0, 7.5])
         w_soft = rng.choice([0.0, 1.0 / T, 30.0 / T, 1e-3]) if w_tok > 0 else rng.choice([1.0 / T, 1e-3])
         c = op.candidate_boundaries(T, N, alpha, w_tok, w_soft)
-        if any(abs((x / round_to) % 1.0 - 0.5) < 1e-6 / round_to for x in c[1:-1]):
-            continue
+        ties += any(abs((x / round_to) % 1.0 - 0.5) < 1e-6 / round_to for x in c[1:-1])
         ref = op.partition_hybrid(T, N, alpha, w_tok, w_soft, round_to)
         if ref is None:
             with pytest.raises(sf.StateflowError):
                 sf.partition_hybrid(T, N, alpha, w_tok, w_soft, round_to)
         else:
             assert sf.partition_hybrid(T, N, alpha, w_tok, w_soft, round_to) == ref, (T, N, alpha, w_tok, w_soft)
-        checked += 1
-    assert checked > 250
+    assert ties > 50  # the half-way cases are well represented
+
+
+@pytest.mark.parametrize("T,N,alpha,w_tok,w_soft,want", [
+    # alpha = 0: boundary i T / N = 192 = 1.5 * 128, half-way: rounds up
+    (384, 2, 0.0, 1.0, 1.0, [256, 128]),
+    # no softmax layers: every alpha gives i T / N; 0.25 * 1.5 ... = 192 again
+    (384, 2, 0.5, 1.0, 0.0, [256, 128]),
+    (384, 2, 1.25, 1.0, 0.0, [256, 128]),
+    # softmax only, alpha = 1: c_1 = T sqrt(1/4) = 320 = 2.5 * 128 exactly; c_2 = T sqrt(1/2),
+    # c_3 = T sqrt(3/4) are irrational (453.5..., 554.2...)
+    (640, 4, 1.0, 0.0, 1e-3, [384, 128, 128, 0]),
+    (1280, 4, 1.0, 0.0, 1.0, [640, 256, 256, 128]),
+])
+def test_half_way_rounds_up(T, N, alpha, w_tok, w_soft, want):
+    """Exact ties, decided by the oracle's rational arithmetic: the half-up
+    reading of "the closest multiple of 128"."""
+    ref = op.partition_hybrid(T, N, alpha, w_tok, w_soft, 128)
+    if 0 in want:
+        assert ref is None
+        with pytest.raises(sf.StateflowError):
+            sf.partition_hybrid(T, N, alpha, w_tok, w_soft, 128)
+        return
+    assert ref == want
+    assert sf.partition_hybrid(T, N, alpha, w_tok, w_soft, 128) == want
+
+
+def test_exact_decision_pins():
+    """The oracle's exact comparison against hand-computed boundaries."""
+    # equal lengths: c_1 = 1 * 1000 / 3 = 333.33...
+    assert op.boundary_at_least(1000, 3, 1, 0.0, 1.0, 0.0, 333)
+    assert not op.boundary_at_least(1000, 3, 1, 0.0, 1.0, 0.0, 334)
+    # softmax only, alpha = 1: c_1 = 400 sqrt(1/4) = 200 exactly
+    assert op.boundary_at_least(400, 4, 1, 1.0, 0.0, 2.0, 200)
+    assert not op.boundary_at_least(400, 4, 1, 1.0, 0.0, 2.0, 200 + 1e-9)
+    # alpha = 1/2 between 100 (equal) and 200 (balanced): 150
+    assert op.boundary_at_least(400, 4, 1, 0.5, 0.0, 2.0, 150)
+    assert not op.boundary_at_least(400, 4, 1, 0.5, 0.0, 2.0, 150.000001)
 
 
 def test_library_validation():
