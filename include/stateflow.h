@@ -174,6 +174,26 @@ sf_status sf_segment_fwd(const sf_shape *shape, const void *q, const void *k, co
                          size_t ws_bytes, const sf_tuning *tuning, sf_stream stream);
 
 /*
+ * Allocation-free variant of sf_segment_fwd, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same operation, arguments, validation
+ * and results as sf_segment_fwd with the same tuning (bitwise), but no
+ * workspace argument: the superchunk states go to a scratch array that the
+ * library holds in static device memory, SF_NOALLOC_SCRATCH_BYTES per GPU,
+ * resident from the library's first use on that GPU until the process ends.
+ * A shape whose workspace (sf_fwd_workspace_bytes) exceeds that size is
+ * rejected with SF_E_WORKSPACE before any launch (a larger tuning.ts needs
+ * less).  The call allocates nothing; the scratch's previous contents are
+ * never read.  Every call on one GPU shares its scratch: calls that may run
+ * concurrently on one GPU (other streams or host threads) race and must be
+ * serialised by the caller.
+ */
+#define SF_NOALLOC_SCRATCH_BYTES (64u << 20)
+sf_status sf_segment_fwd_noalloc(const sf_shape *shape, const void *q, const void *k, const void *v,
+                                 const float *g, const float *S_in, void *o, float *S_out,
+                                 const sf_tuning *tuning, sf_stream stream);
+
+/*
  * One segment backward (Sec. 3.1, Bwd): given the forward inputs, S_in, the
  * output gradient dO and the boundary gradient dS_out (NULL = zero), writes
  * dq, dk, dv, dg and dS_in.  Nothing from the forward is reused: the states

@@ -30,7 +30,7 @@ from ._lib import KERNELS, StateflowError  # noqa: F401
 from . import tuned
 from .timing import KernelTimer  # noqa: F401
 
-__all__ = ["segment_fwd", "segment_bwd", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
+__all__ = ["segment_fwd", "segment_fwd_noalloc", "segment_bwd", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
            "bwd_workspace_bytes", "chain_workspace_bytes", "conv_fwd", "conv_bwd", "conv_bwd_workspace_bytes",
            "gdn_fwd", "gdn_fwd_workspace_bytes", "gdn_bwd", "gdn_chain_fwd", "gdn_chain_bwd", "partition_hybrid", "KernelTimer", "StateflowError", "abi_version"]
 
@@ -146,6 +146,23 @@ def segment_fwd(q, k, v, g, S_in=None, *, ts=0, stream=None, timing=None):
     rc = L_.sf_segment_fwd(ctypes.byref(sh), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(S_in), _ptr(o),
                            _ptr(S_out), _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream))
     _lib.check("sf_segment_fwd", rc)
+    return o, S_out
+
+
+def segment_fwd_noalloc(q, k, v, g, S_in, o, S_out, *, ts=0, stream=None, timing=None):
+    """segment_fwd into caller-supplied o and S_out through the library's
+    allocation-free entry point (no workspace; nothing is allocated here
+    either).  o: like q; S_out: float32 [B, H, D, D] contiguous."""
+    _same_layout(q, k, v, o)
+    sh = _shape(q, g)
+    B, L, H, D = q.shape
+    _state(S_in, B, H, D, "S_in")
+    _state(S_out, B, H, D, "S_out")
+    stream = stream or torch.cuda.current_stream(q.device)
+    rc = _lib.lib().sf_segment_fwd_noalloc(ctypes.byref(sh), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(S_in),
+                                           _ptr(o), _ptr(S_out), ctypes.byref(_tuning(ts, timing=timing)),
+                                           _stream_handle(stream))
+    _lib.check("sf_segment_fwd_noalloc", rc)
     return o, S_out
 
 

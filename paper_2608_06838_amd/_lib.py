@@ -19,10 +19,11 @@ KERNELS = {"fwd_prep": 0, "scan": 1, "fwd_out": 2, "bwd_prep": 3, "bwd_dq": 4, "
            "conv_fwd": 6, "conv_bwd": 7, "gdn_prep": 8, "gdn_scan": 9, "gdn_out": 10, "gdn_store": 11,
            "gdn_dprep": 12, "gdn_dscan": 13, "gdn_dwalk": 14, "gdn_dchunk": 15}
 SF_ACT_NONE, SF_ACT_SILU = 0, 1
+NOALLOC_SCRATCH_BYTES = 64 << 20  # SF_NOALLOC_SCRATCH_BYTES
 
 # every symbol include/stateflow.h declares
 EXPORTS = ["sf_abi_version", "sf_status_str", "sf_last_error", "sf_fwd_workspace_bytes",
-           "sf_bwd_workspace_bytes", "sf_segment_fwd", "sf_segment_bwd", "sf_chain_workspace_bytes",
+           "sf_bwd_workspace_bytes", "sf_segment_fwd", "sf_segment_fwd_noalloc", "sf_segment_bwd", "sf_chain_workspace_bytes",
            "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd",
            "sf_gdn_fwd_workspace_bytes", "sf_gdn_fwd", "sf_gdn_bwd_workspace_bytes", "sf_gdn_bwd",
            "sf_gdn_chain_workspace_bytes", "sf_gdn_chain_fwd", "sf_gdn_chain_bwd",
@@ -91,6 +92,8 @@ def lib():
         f.argtypes = [sp, tp]
     L.sf_segment_fwd.restype = ctypes.c_int
     L.sf_segment_fwd.argtypes = [sp] + [vp] * 8 + [sz, tp, vp]
+    L.sf_segment_fwd_noalloc.restype = ctypes.c_int
+    L.sf_segment_fwd_noalloc.argtypes = [sp] + [vp] * 7 + [tp, vp]
     L.sf_segment_bwd.restype = ctypes.c_int
     L.sf_segment_bwd.argtypes = [sp] + [vp] * 13 + [sz, tp, vp]
     L.sf_chain_workspace_bytes.restype = sz

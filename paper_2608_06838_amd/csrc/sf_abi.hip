@@ -18,12 +18,20 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
 
 #include "sf_launch.hpp"
 #include "stateflow.h"
+
+// Scratch of sf_segment_fwd_noalloc: the superchunk states and decays of one
+// segment forward, for callers that cannot allocate.  One copy per GPU, held
+// for the life of the process; host code reaches it only through the address
+// hipGetSymbolAddress returns for the current device (the name itself is a
+// host-side stand-in).  Calls that overlap on one GPU share it and race.
+static __device__ __align__(256) unsigned char scratch[SF_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -41,6 +49,26 @@ sf_status fail(sf_status s, const char *fmt, ...) {
 
 sf_status hip_fail(hipError_t e, const char *what) {
     return fail(SF_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Device address of `scratch` on the current device, resolved once per device
+// with that device current.
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void *g_scratch_addr[kMaxDevices];
+hipError_t g_scratch_rc[kMaxDevices];
+
+sf_status scratch_of_device(char *&out) {
+    int dev = -1;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(SF_E_UNSUPPORTED, "device index %d out of range", dev);
+    std::call_once(g_scratch_once[dev], [dev] {
+        g_scratch_rc[dev] = hipGetSymbolAddress(&g_scratch_addr[dev], HIP_SYMBOL(scratch));
+    });
+    if (g_scratch_rc[dev] != hipSuccess) return hip_fail(g_scratch_rc[dev], "hipGetSymbolAddress(scratch)");
+    out = (char *)g_scratch_addr[dev];
+    return SF_OK;
 }
 
 // ------------------------------------------------------------- validation
@@ -520,6 +548,38 @@ size_t chain_ws(const Shape &r, int32_t n_seg, const int64_t *seg_len, const sf_
     return 2 * al(slot) + 2 * gbnd;
 }
 
+// argument checks shared by the two segment-forward entry points; resolves the
+// shape, the superchunk length and the workspace the phases need
+sf_status segment_fwd_check(const sf_shape *shape, const void *q, const void *k, const void *v, const float *g,
+                            const float *S_in, void *o, float *S_out, const sf_tuning *tuning, Shape &r, int &ts,
+                            size_t &need) {
+    TRY(resolve(shape, r));
+    TRY(check_timing(tuning));
+    if (!S_out || (r.L > 0 && (!q || !k || !v || !g || !o)))
+        return fail(SF_E_NULL, "q, k, v, g, o and S_out are required");
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_in, "S_in"}, {S_out, "S_out"}}));
+    TRY(pick_ts(r, r.L, tuning, ts));
+    need = ws_layout(r, r.L, ts, false).total;
+    return SF_OK;
+}
+
+sf_status segment_fwd_run(const Shape &r, int ts, const void *q, const void *k, const void *v, const float *g,
+                          const float *S_in, void *o, float *S_out, char *ws, const sf_tuning *tuning,
+                          hipStream_t st) {
+    Seg s = make_seg(r, r.L, ts, ws, false, timing_of(tuning));
+    s.a.q = q;
+    s.a.k = k;
+    s.a.v = v;
+    s.a.g = g;
+    s.a.o = o;
+    s.a.S_in = S_in;
+    s.a.S_out = S_out;
+    TRY(fwd_prep(r, s, st));
+    TRY(fwd_scan(r, s, st));
+    TRY(fwd_out(r, s, st));
+    return SF_OK;
+}
+
 // ------------------------------------------------- exact partition rounding
 // The boundary c_i(alpha) = (1 - alpha) i T / N + alpha c_i^hyb, with
 // A(c_i^hyb) = (i / N) A(T) and A(c) = w_tok c + w_soft c^2 / 2, is compared
@@ -691,32 +751,37 @@ sf_status sf_segment_fwd(const sf_shape *shape, const void *q, const void *k, co
                          size_t ws_bytes, const sf_tuning *tuning, sf_stream stream) {
     g_err.clear();
     Shape r;
-    TRY(resolve(shape, r));
-    TRY(check_timing(tuning));
-    if (!S_out || (r.L > 0 && (!q || !k || !v || !g || !o)))
-        return fail(SF_E_NULL, "q, k, v, g, o and S_out are required");
-    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_in, "S_in"}, {S_out, "S_out"}, {ws, "ws"}}));
     int ts;
-    TRY(pick_ts(r, r.L, tuning, ts));
-    const size_t need = ws_layout(r, r.L, ts, false).total;
+    size_t need;
+    TRY(segment_fwd_check(shape, q, k, v, g, S_in, o, S_out, tuning, r, ts, need));
+    TRY(check_align({{ws, "ws"}}));
     if (need > 0 && !ws) return fail(SF_E_NULL, "workspace of %zu bytes required", need);
     if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
     TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
                      grange(r, g, r.L, "g"), srange(r, S_in, 1, "S_in")},
                     {xrange(r, o, r.L, "o"), srange(r, S_out, 1, "S_out"), wsrange(ws, need)}));
-    Seg s = make_seg(r, r.L, ts, (char *)ws, false, timing_of(tuning));
-    s.a.q = q;
-    s.a.k = k;
-    s.a.v = v;
-    s.a.g = g;
-    s.a.o = o;
-    s.a.S_in = S_in;
-    s.a.S_out = S_out;
-    hipStream_t st = (hipStream_t)stream;
-    TRY(fwd_prep(r, s, st));
-    TRY(fwd_scan(r, s, st));
-    TRY(fwd_out(r, s, st));
-    return SF_OK;
+    return segment_fwd_run(r, ts, q, k, v, g, S_in, o, S_out, (char *)ws, tuning, (hipStream_t)stream);
+}
+
+sf_status sf_segment_fwd_noalloc(const sf_shape *shape, const void *q, const void *k, const void *v,
+                                 const float *g, const float *S_in, void *o, float *S_out,
+                                 const sf_tuning *tuning, sf_stream stream) {
+    g_err.clear();
+    Shape r;
+    int ts;
+    size_t need;
+    TRY(segment_fwd_check(shape, q, k, v, g, S_in, o, S_out, tuning, r, ts, need));
+    if (need > SF_NOALLOC_SCRATCH_BYTES)
+        return fail(SF_E_WORKSPACE,
+                    "this shape needs %zu bytes of scratch; the allocation-free call holds %zu "
+                    "(use sf_segment_fwd with a workspace, or a larger tuning.ts)",
+                    need, (size_t)SF_NOALLOC_SCRATCH_BYTES);
+    TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
+                     grange(r, g, r.L, "g"), srange(r, S_in, 1, "S_in")},
+                    {xrange(r, o, r.L, "o"), srange(r, S_out, 1, "S_out")}));
+    char *ws = nullptr;
+    if (need > 0) TRY(scratch_of_device(ws));
+    return segment_fwd_run(r, ts, q, k, v, g, S_in, o, S_out, ws, tuning, (hipStream_t)stream);
 }
 
 sf_status sf_segment_bwd(const sf_shape *shape, const void *q, const void *k, const void *v,
