@@ -8,20 +8,23 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 OUT_DIR = os.path.join(HERE, "_build")
-LIB = os.path.join(OUT_DIR, "liboracle.so")
+# SF_ORACLE_LIB selects another build of the same sources (the sanitizer test
+# loads an AddressSanitizer / UndefinedBehaviorSanitizer build through it)
+DEFAULT_LIB = os.path.join(OUT_DIR, "liboracle.so")
+LIB = os.environ.get("SF_ORACLE_LIB") or DEFAULT_LIB
 
 
 def build(verbose: bool = False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
     srcs = [os.path.join(HERE, f) for f in ("sf_oracle.c", "gdn_oracle.c")]
-    tmp = LIB + ".tmp"
+    tmp = DEFAULT_LIB + ".tmp"
     cmd = ["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
            "-Wno-unused-parameter", *srcs, "-o", tmp, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, DEFAULT_LIB)
+    return DEFAULT_LIB
 
 
 if __name__ == "__main__":

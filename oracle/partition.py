@@ -13,17 +13,17 @@ closest multiple of round_to (half-way cases up, this package's reading).
 The summed cost of the segments before a cut at c telescopes to
 A(c) = w_tok c + w_soft c^2 / 2, so the balanced boundary c_i^hyb is where A
 reaches i / N of A(T).  Bisection gives c_i^hyb in floating point (used for
-the cost pins and as a first guess); the rounded boundary is then decided
-exactly: with every input taken at its exact value (fractions.Fraction),
+the cost pins); the rounded boundary is decided exactly: with every input
+taken at its exact value (fractions.Fraction),
 c_i(alpha) >= y holds iff
     alpha = 0:  i T / N >= y
     alpha > 0:  x <= 0 or A(x) <= (i / N) A(T),  x = (y - (1 - alpha) i T / N) / alpha
 (A increases on x >= 0 and c_i^hyb >= 0), and the rounded boundary is the
-multiple m * round_to with (m - 1/2) round_to <= c_i(alpha) < (m + 1/2) round_to.
+multiple m * round_to with (m - 1/2) round_to <= c_i(alpha) < (m + 1/2) round_to,
+m at most T / round_to (a boundary past T leaves a segment empty).
 Pinned by tests/test_partition.py (equal per-segment costs at alpha = 1, the
 equal-length cases, the closed form for w_tok = 0, exact ties).
 """
-import math
 from fractions import Fraction
 
 
@@ -70,22 +70,24 @@ def boundary_at_least(T, N, i, alpha, w_tok, w_soft, y):
     return prefix_cost(x, p, s) <= Fraction(i, N) * prefix_cost(Fraction(T), p, s)
 
 
-def rounded_boundary(T, N, i, alpha, w_tok, w_soft, round_to, guess):
-    """The multiple of round_to closest to c_i(alpha), half-way cases up,
-    starting the exact search from the floating-point guess."""
-    m = int(math.floor(guess / round_to + 0.5))
+def rounded_boundary(T, N, i, alpha, w_tok, w_soft, round_to):
+    """The multiple of round_to closest to c_i(alpha), half-way cases up: the
+    largest m in [0, T / round_to] with c_i(alpha) >= (m - 1/2) round_to, by
+    bisection over m on the exact comparison (m = 0 always qualifies)."""
     half = Fraction(round_to, 2)
-    while not boundary_at_least(T, N, i, alpha, w_tok, w_soft, m * round_to - half):
-        m -= 1
-    while boundary_at_least(T, N, i, alpha, w_tok, w_soft, m * round_to + half):
-        m += 1
-    return m * round_to
+    lo, hi = 0, T // round_to
+    while lo < hi:
+        mid = (lo + hi + 1) // 2
+        if boundary_at_least(T, N, i, alpha, w_tok, w_soft, mid * round_to - half):
+            lo = mid
+        else:
+            hi = mid - 1
+    return lo * round_to
 
 
 def partition_hybrid(T, N, alpha, w_tok, w_soft, round_to=128):
     """Segment lengths, or None when rounding leaves a segment empty."""
-    c = candidate_boundaries(T, N, alpha, w_tok, w_soft)
-    r = [0] + [rounded_boundary(T, N, i, alpha, w_tok, w_soft, round_to, c[i]) for i in range(1, N)] + [T]
+    r = [0] + [rounded_boundary(T, N, i, alpha, w_tok, w_soft, round_to) for i in range(1, N)] + [T]
     lens = [r[i + 1] - r[i] for i in range(N)]
     return lens if all(x > 0 for x in lens) else None
 

@@ -157,30 +157,30 @@ sf_status resolve(const sf_shape *sh, Shape &r) {
     return SF_OK;
 }
 
-// byte extent of a tensor
+// byte extent of a tensor, as integer addresses ([lo, hi); lo = 0 for an
+// absent tensor): no pointer arithmetic on absent (NULL) pointers and no
+// ordering of pointers into different objects
 struct Range {
-    const char *lo, *hi;
+    uintptr_t lo, hi;
     const char *name;
 };
+Range span(const void *p, int64_t bytes, const char *name) {
+    const uintptr_t b = (uintptr_t)p;
+    return {b, b && bytes > 0 ? b + (uintptr_t)bytes : b, name};
+}
 Range xrange(const Shape &r, const void *p, int64_t L, const char *name) {
-    const char *b = (const char *)p;
-    int64_t last = (r.B - 1) * r.sx_b + (L - 1) * r.sx_l + (r.H - 1) * r.sx_h + r.D;
-    return {b, b + (L > 0 ? last * (int64_t)r.esz : 0), name};
+    const int64_t last = (r.B - 1) * r.sx_b + (L - 1) * r.sx_l + (r.H - 1) * r.sx_h + r.D;
+    return span(p, L > 0 ? last * (int64_t)r.esz : 0, name);
 }
 Range grange(const Shape &r, const float *p, int64_t L, const char *name) {
-    const char *b = (const char *)p;
     const int64_t gin = r.gate == SF_GATE_VECTOR ? r.D : 1;
-    int64_t last = (r.B - 1) * r.sg_b + (L - 1) * r.sg_l + (r.H - 1) * r.sg_h + gin;
-    return {b, b + (L > 0 ? last * 4 : 0), name};
+    const int64_t last = (r.B - 1) * r.sg_b + (L - 1) * r.sg_l + (r.H - 1) * r.sg_h + gin;
+    return span(p, L > 0 ? last * 4 : 0, name);
 }
 Range srange(const Shape &r, const float *p, int64_t nstates, const char *name) {
-    const char *b = (const char *)p;
-    return {b, b + (p ? nstates * r.B * r.H * (int64_t)r.D * r.D * 4 : 0), name};
+    return span(p, nstates * r.B * r.H * (int64_t)r.D * r.D * 4, name);
 }
-Range wsrange(const void *ws, size_t bytes) {
-    const char *b = (const char *)ws;
-    return {b, b + (ws ? bytes : 0), "ws"};
-}
+Range wsrange(const void *ws, size_t bytes) { return span(ws, (int64_t)bytes, "ws"); }
 bool overlap(const Range &a, const Range &b) {
     return a.lo && b.lo && a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi;
 }
@@ -232,27 +232,33 @@ sf_status pick_ts(const Shape &r, int64_t L, const sf_tuning *t, int &ts) {
         ts = t->ts;
         return SF_OK;
     }
-    // Superchunks of one head run one after another inside a workgroup, and the
-    // workgroups of a launch run in rounds of `slots` (two per CU).  Choose the
-    // superchunk length (a multiple of 64) that minimises
-    //   rounds * chunks_per_superchunk + kState * superchunks,
-    // the walk time in chunk steps plus the cost of materialising, scanning and
-    // re-reading one more boundary state per superchunk (about 0.006 chunk
-    // steps per state at d = 128).
+    // Superchunks of one head run one after another inside a workgroup.  The
+    // superchunk length (a multiple of 64) minimises a cost in chunk steps,
+    // fitted to measured fwd+bwd steps of five workloads (2 to 128 heads,
+    // 512- to 65536-token segments):
+    //   walks: m chunks per workgroup; up to one workgroup per CU they run in
+    //     m steps; beyond that the CUs hold two each, in rounds of 2 * CUs,
+    //     a round taking kPair * m (a second workgroup adds 1 / kPair - 1/2 of
+    //     a CU's throughput); with superchunks the two prep kernels add kPrep;
+    //   + kState per superchunk state of all heads (materialised, scanned and
+    //     re-read: about 0.01 steps each at d = 128)
+    //   + kScan per superchunk of one head (the scans' sequential steps).
     const int64_t bh = (int64_t)r.B * r.H;
     const int64_t nc = (L + 63) / 64;
     if (nc <= 1) {
         ts = (int)std::max<int64_t>(64, std::min<int64_t>(L, 1 << 30));
         return SF_OK;
     }
-    const double slots = 2.0 * device_cus(), kState = 0.006 * (double)r.D * r.D / (128.0 * 128.0);
+    const double cus = (double)device_cus(), kState = 0.01 * (double)r.D * r.D / (128.0 * 128.0);
+    constexpr double kScan = 0.1, kPair = 1.6, kPrep = 1.5;
     double best = 1e300;
     int64_t best_m = nc;
     for (int64_t m = 1; m <= nc; ++m) {  // chunks per superchunk
         const int64_t ns = (nc + m - 1) / m;
         if (m > 1 && (nc + m - 2) / (m - 1) == ns) continue;  // same split as a shorter m
-        const double rounds = std::ceil((double)(bh * ns) / slots);
-        const double cost = rounds * (double)m + kState * (double)(bh * ns);
+        const double wg = (double)(bh * ns);
+        double cost = wg <= cus ? (double)m : std::ceil(wg / (2.0 * cus)) * (double)m * kPair;
+        if (ns > 1) cost = cost * kPrep + kState * wg + kScan * (double)ns;
         if (cost < best - 1e-9) {
             best = cost;
             best_m = m;
@@ -382,14 +388,10 @@ size_t conv_ws_bytes(const ConvShape &r) {
 }
 
 Range conv_xrange(const ConvShape &r, const void *p, const char *name) {
-    const char *b = (const char *)p;
     const int64_t last = (r.B - 1) * r.sx_b + (r.L - 1) * r.sx_l + r.C;
-    return {b, b + (r.L > 0 ? last * (int64_t)r.esz : 0), name};
+    return span(p, r.L > 0 ? last * (int64_t)r.esz : 0, name);
 }
-Range frange(const void *p, int64_t n, const char *name) {
-    const char *b = (const char *)p;
-    return {b, b + (p ? n * 4 : 0), name};
-}
+Range frange(const void *p, int64_t n, const char *name) { return span(p, n * 4, name); }
 
 sf_status conv_run(int kind, bool bwd, const sf::ConvArgs &a, hipStream_t s, sf_timing *tm) {
     hipEvent_t e0, e1;
@@ -1052,7 +1054,7 @@ sf_status sf_conv_bwd(const sf_conv_shape *shape, const void *x, const float *w,
     TRY(check_alias({conv_xrange(r, x, "x"), frange(w, nw, "w"), frange(tail ? tail_in : nullptr, nt, "tail_in"),
                      conv_xrange(r, dy, "dy"), frange(tail ? dtail_out : nullptr, nt, "dtail_out")},
                     {conv_xrange(r, dx, "dx"), frange(dw, nw, "dw"), frange(tail ? dtail_in : nullptr, nt, "dtail_in"),
-                     {(const char *)ws, (const char *)ws + (need ? need : 0), "workspace"}}));
+                     wsrange(ws, need)}));
     sf::ConvArgs a{};
     a.x = x;
     a.w = w;
@@ -1294,7 +1296,7 @@ sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const 
     TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"), grange(r, g, r.L, "g"),
                      grange(r, beta, r.L, "beta"), srange(r, S_in, 1, "S_in")},
                     {xrange(r, o, r.L, "o"), srange(r, S_out, 1, "S_out"), xrange(r, v_new, r.L, "v_new"),
-                     {(const char *)ws, (const char *)ws + (ws ? need : 0), "ws"}}));
+                     wsrange(ws, need)}));
     sf::GdnArgs a{};
     a.q = q;
     a.k = k;
@@ -1359,7 +1361,7 @@ sf_status sf_gdn_bwd(const sf_shape *shape, const void *q, const void *k, const 
                      srange(r, dS_out, 1, "dS_out")},
                     {xrange(r, dq, r.L, "dq"), xrange(r, dk, r.L, "dk"), xrange(r, dv, r.L, "dv"),
                      grange(r, dg, r.L, "dg"), grange(r, dbeta, r.L, "dbeta"), srange(r, dS_in, 1, "dS_in"),
-                     {(const char *)ws, (const char *)ws + L.total, "ws"}}));
+                     wsrange(ws, L.total)}));
     sf::GdnArgs a{};
     a.q = q;
     a.k = k;
@@ -1433,7 +1435,7 @@ sf_status sf_gdn_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *
     TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"), grange(r, g, r.L, "g"),
                      grange(r, beta, r.L, "beta")},
                     {xrange(r, o, r.L, "o"), srange(r, S_bnd, n_seg + 1, "S_bnd"), xrange(r, v_new, r.L, "v_new"),
-                     {(const char *)ws, (const char *)ws + W.total, "ws"}}));
+                     wsrange(ws, W.total)}));
     const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
     const GdnFwdWs F = gdn_fwd_ws_n(r, p.n_max, p.n_max);
     std::vector<sf::GdnArgs> seg(n_seg);
@@ -1519,7 +1521,7 @@ sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *
                      srange(r, dS_final, 1, "dS_final")},
                     {xrange(r, dq, r.L, "dq"), xrange(r, dk, r.L, "dk"), xrange(r, dv, r.L, "dv"),
                      grange(r, dg, r.L, "dg"), grange(r, dbeta, r.L, "dbeta"), srange(r, dS_init, 1, "dS_init"),
-                     {(const char *)ws, (const char *)ws + W.total, "ws"}}));
+                     wsrange(ws, W.total)}));
     const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
     const GdnBwdWs Lw = gdn_bwd_ws_n(r, p.n_max, (size_t)p.nc_max);
     char *base = (char *)ws;
@@ -1614,12 +1616,28 @@ sf_status sf_partition_hybrid(int64_t T, int32_t N, double alpha, double w_tok, 
             const double hyb = 2.0 * r / (w_tok + std::sqrt(w_tok * w_tok + 2.0 * w_soft * r));
             const double equal = Td * (double)i / (double)N;
             const double x = (1.0 - alpha) * equal + alpha * hyb;
-            // closest multiple of round_to, half-way cases up: the m with
-            // (m - 1/2) R <= c_i < (m + 1/2) R, found exactly from the guess
-            int64_t m = (int64_t)std::floor(x / round_to + 0.5);
-            m = std::max<int64_t>(0, std::min<int64_t>(m, T / round_to));
-            while (m > 0 && !part_at_least(T, N, i, alpha, w_tok, w_soft, round_to, 2 * m - 1)) --m;
-            while (m < T / round_to && part_at_least(T, N, i, alpha, w_tok, w_soft, round_to, 2 * m + 1)) ++m;
+            // closest multiple of round_to, half-way cases up: the largest m
+            // in [0, T / R] with c_i >= (m - 1/2) R, decided exactly; the fp64
+            // value is tried first, else a binary search (it may be inf or NaN
+            // for extreme weights)
+            const int64_t top = T / round_to;
+            auto ok = [&](int64_t m) {
+                return m == 0 || part_at_least(T, N, i, alpha, w_tok, w_soft, round_to, 2 * m - 1);
+            };
+            int64_t m = -1;
+            if (std::isfinite(x) && x > -(double)round_to && x < (double)T + round_to) {
+                const int64_t g = std::max<int64_t>(0, std::min<int64_t>((int64_t)std::floor(x / round_to + 0.5), top));
+                if (ok(g) && (g == top || !ok(g + 1))) m = g;
+            }
+            if (m < 0) {
+                int64_t lo = 0, hi = top;  // ok(lo) holds
+                while (lo < hi) {
+                    const int64_t mid = lo + (hi - lo + 1) / 2;
+                    if (ok(mid)) lo = mid;
+                    else hi = mid - 1;
+                }
+                m = lo;
+            }
             c = m * round_to;
         }
         if (c <= prev || c > T)

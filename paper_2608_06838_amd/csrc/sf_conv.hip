@@ -63,7 +63,7 @@ struct Row8 {
 template <typename T>
 __device__ __forceinline__ void store_row8(T *p, const float (&f)[CONV_E]) {
     typedef T v8 __attribute__((ext_vector_type(8)));
-    v8 o;
+    v8 o = {};
 #pragma unroll
     for (int e = 0; e < CONV_E; ++e) o[e] = (T)f[e];
     // the outputs are not read again by this kernel: non-temporal stores

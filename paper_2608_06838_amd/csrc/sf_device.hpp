@@ -461,7 +461,7 @@ __device__ __forceinline__ frag_t<T> ldfragTR(const T *M, const LaneOff &o, int 
         const s8 v = __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7);
         return __builtin_bit_cast(frag_t<T>, v);
     } else {
-        frag_t<T> f;
+        frag_t<T> f = {};
 #pragma unroll
         for (int j = 0; j < 8; ++j) f[j] = M[e + j * LD];
         return f;

@@ -884,7 +884,7 @@ __global__ void __launch_bounds__(512) k_gdn_dchunk(GdnArgs a) {
         return *reinterpret_cast<const frag_t<T> *>(M + (rr + n16) * LDX + kk + 8 * q4);
     };
     auto x_tr = [&](const T *M, int rr, int kk) {  // exact, M[k][row]
-        frag_t<T> f;
+        frag_t<T> f = {};
 #pragma unroll
         for (int j = 0; j < 8; ++j) f[j] = M[(kk + 8 * q4 + j) * LDX + rr + n16];
         return f;

@@ -113,7 +113,7 @@ __device__ __forceinline__ void store_scaled(const Tile<T, D, NT> &t, const floa
             float x[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) x[e] = tof<T>(t.r[j][4 * u + e]) * f[j][4 * u + e];
-            h4 vh, vl;
+            h4 vh = {}, vl = {};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 vh[e] = cvt<T>(x[e]);
@@ -226,7 +226,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
                 const frag_t<T> xh = ldfragTR<T, LDN, SWX>(sX, tro, 32 * ks, 16 * i);
-                frag_t<T> xl;
+                frag_t<T> xl = {};
                 if constexpr (SP) xl = ldfragTR<T, LDN, SWX>(sXl, tro, 32 * ks, 16 * i);
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) {
@@ -351,7 +351,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_walk_vg(SegArgs a) {
                 for (int ks = 0; ks < D / 32; ++ks) {
                     const frag_t<T> kh = ldfrag_swz<T, LDN, SWX>(sK, swo, 16 * st, 32 * ks);
                     const frag_t<T> qh = ldfrag_unperm<T>(sQ, LDN, 16 * tt, 32 * ks, lane);
-                    frag_t<T> kl, ql;
+                    frag_t<T> kl = {}, ql = {};
                     if constexpr (SP) {
                         kl = ldfrag_swz<T, LDN, SWX>(sKl, swo, 16 * st, 32 * ks);
                         ql = ldfrag_unperm<T>(sQl, LDN, 16 * tt, 32 * ks, lane);
@@ -387,7 +387,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_walk_vg(SegArgs a) {
                     split_acc<T>(S[ct][2 * ks], S[ct][2 * ks + 1], fh, fl);
 #pragma unroll
                     for (int tt = 0; tt < 4; ++tt) {
-                        frag_t<T> qh = ldfrag(sQ, LDN, 16 * tt, 32 * ks, lane), ql;
+                        frag_t<T> qh = ldfrag(sQ, LDN, 16 * tt, 32 * ks, lane), ql = {};
                         if constexpr (SP) ql = ldfrag(sQl, LDN, 16 * tt, 32 * ks, lane);
                         mma3<T>(O[tt], fh, fl, qh, ql);
                     }
@@ -413,7 +413,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_walk_vg(SegArgs a) {
 #pragma unroll
                 for (int i = 0; i < NK; ++i) {
                     const frag_t<T> kh = ldfragTR<T, LDN, SWX>(sK, tro, 32 * ks, 16 * i);
-                    frag_t<T> kl;
+                    frag_t<T> kl = {};
                     if constexpr (SP) kl = ldfragTR<T, LDN, SWX>(sKl, tro, 32 * ks, 16 * i);
 #pragma unroll
                     for (int ct = 0; ct < NCT; ++ct) mma2<T>(S[ct][i], kh, kl, vf[ct][ks]);
@@ -621,7 +621,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dq_vg(SegArgs a) {
 #pragma unroll
                     for (int tt = 0; tt < 4; ++tt) {
                         if (32 * ks > 16 * tt + 15) continue;
-                        frag_t<T> ph = ldfrag(sP, LDT, 16 * tt, 32 * ks, lane), pl;
+                        frag_t<T> ph = ldfrag(sP, LDT, 16 * tt, 32 * ks, lane), pl = {};
                         if constexpr (SP) pl = ldfrag(sPl, LDT, 16 * tt, 32 * ks, lane);
                         mma3<T>(O[tt], kh[ct][ks], kl[ct][ks], ph, pl);
                     }
@@ -815,7 +815,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dv_vg(SegArgs a) {
                 for (int ks = 0; ks < D / 32; ++ks) {
                     const frag_t<T> qh = ldfrag_swz<T, LDN, SWX>(sQ, swo, 16 * tt, 32 * ks);
                     const frag_t<T> kh = ldfrag_unperm<T>(sK, LDN, 16 * st, 32 * ks, lane);
-                    frag_t<T> ql, kl;
+                    frag_t<T> ql = {}, kl = {};
                     if constexpr (SP) {
                         ql = ldfrag_swz<T, LDN, SWX>(sQl, swo, 16 * tt, 32 * ks);
                         kl = ldfrag_unperm<T>(sKl, LDN, 16 * st, 32 * ks, lane);
@@ -859,7 +859,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dv_vg(SegArgs a) {
                     split8<T>(x, gh, gl);
 #pragma unroll
                     for (int st = 0; st < 4; ++st) {
-                        frag_t<T> khf = ldfrag(sK, LDN, 16 * st, 32 * ks, lane), klf;
+                        frag_t<T> khf = ldfrag(sK, LDN, 16 * st, 32 * ks, lane), klf = {};
                         if constexpr (SP) klf = ldfrag(sKl, LDN, 16 * st, 32 * ks, lane);
                         mma3<T>(DV[st], gh, gl, khf, klf);
                     }
@@ -890,7 +890,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dv_vg(SegArgs a) {
 #pragma unroll
                 for (int i = 0; i < NK; ++i) {
                     const frag_t<T> qh = ldfragTR<T, LDN, SWX>(sQ, tro, 32 * ks, 16 * i);
-                    frag_t<T> ql;
+                    frag_t<T> ql = {};
                     if constexpr (SP) ql = ldfragTR<T, LDN, SWX>(sQl, tro, 32 * ks, 16 * i);
 #pragma unroll
                     for (int ct = 0; ct < NCT; ++ct) mma2<T>(G[ct][i], qh, ql, of[ct][ks]);
@@ -1117,7 +1117,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dk_vg(SegArgs a) {
                 for (int st = 0; st < 4; ++st)
 #pragma unroll
                     for (int ks = st / 2; ks < C / 32; ++ks) {
-                        frag_t<T> ph = ldfrag(sPT, LDT, 16 * st, 32 * ks, lane), pl;
+                        frag_t<T> ph = ldfrag(sPT, LDT, 16 * st, 32 * ks, lane), pl = {};
                         if constexpr (SP) pl = ldfrag(sPTl, LDT, 16 * st, 32 * ks, lane);
                         mma3<T>(X2[st], qh[ct][ks], ql[ct][ks], ph, pl);
                     }

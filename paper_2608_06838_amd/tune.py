@@ -26,7 +26,7 @@ PARTITION_NS = (2, 4, 6, 8, 16, 32)
 PARTITION_ALPHAS = (0.0, 0.1, 0.2, 0.3, 0.4, 0.5, 0.6, 0.7, 0.8, 0.9, 1.0, 1.25)
 
 
-def ts_candidates(seg_lens, extra=(512, 1024, 2048, 4096, 8192)):
+def ts_candidates(seg_lens, extra=(128, 256, 512, 1024, 2048, 4096, 8192)):
     """0 (the library's automatic choice) and fixed strides that fit the
     longest segment, each a multiple of 64."""
     longest = max(seg_lens)

@@ -7,15 +7,28 @@ tuner's measurements (bench.py --tune-ts), one row per shape:
   key   (B, H, D, io, gate, segment lengths)
   value dict(ts=superchunk stride or 0 for the library's automatic choice,
              overlap=whether the state scans run on the aux stream)
-Shapes without a row get ts = 0 and the paper's overlapped schedule.
+Shapes without a row get ts = 0 (the library's cost model, fitted to these
+same measurements) and the scans serialised on the main stream: on every
+measured shape the serial schedule was as fast as the overlapped one or
+faster (the dense kernels keep every CU busy, so an overlapped scan only
+slows the kernel it shares a CU with).  overlap=True still selects the
+paper's split-and-overlap schedule.
 """
 
-DEFAULT = dict(ts=0, overlap=True)
+DEFAULT = dict(ts=0, overlap=False)
 
 _SEG_256K = (65536, 40960, 32768, 28672, 26624, 24576, 22528, 20480)
 
-# Filled from the measured study tables (DESIGN.md, tuner section).
-TABLE = {}
+# Profiled on MI355X (bench.py --tune-ts, fwd+bwd chain steps, best of the
+# ts x overlap grid; DESIGN.md, tuner section).  ts = 0 where the library's
+# per-segment choice beat every fixed stride.
+TABLE = {
+    (1, 2, 64, "f32", "scalar", (1024,)): dict(ts=0, overlap=False),
+    (1, 16, 128, "bf16", "scalar", (4096,) * 8): dict(ts=256, overlap=False),
+    (1, 40, 128, "bf16", "scalar", _SEG_256K): dict(ts=0, overlap=False),
+    (2, 16, 128, "bf16", "vector", (4096,) * 16): dict(ts=512, overlap=False),
+    (4, 32, 128, "bf16", "scalar", (512,) * 32): dict(ts=512, overlap=False),
+}
 
 
 def key(B, H, D, io, gate, seg_lens):

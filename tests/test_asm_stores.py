@@ -2,10 +2,11 @@
 store whose address registers overlap its data registers.
 
 A store such as `global_store_dwordx4 v[4:5], v[2:5]` writes part of its own
-address as data.  One loop shape of the delta-rule state scan was compiled
-into exactly that; the sources avoid it (buffer stores with 32-bit offsets
-there), and this test keeps it from coming back.  CPU only; skipped without
-hipcc.
+address as data.  One loop shape of the delta-rule state scan once produced
+exactly that store; the likeliest cause is a stored value the compiler saw as
+undefined (read before written), which frees it to reuse any register.  The
+build therefore also compiles every source with clang's uninitialized-value
+warnings and fails on any.  CPU only; skipped without hipcc.
 """
 import concurrent.futures
 import os
@@ -60,17 +61,23 @@ def test_no_store_overlaps_its_address():
 
     def build(src):
         out = os.path.join(tmp, src + ".s")
-        subprocess.run([HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "--cuda-device-only", "-S",
-                        "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"),
-                        "-I", CSRC, os.path.join(CSRC, src), "-o", out], check=True, capture_output=True)
+        res = subprocess.run([HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "--cuda-device-only", "-S",
+                              "-Wuninitialized", "-Wconditional-uninitialized", "-Wsometimes-uninitialized",
+                              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-I",
+                              os.path.join(ROOT, "include"), "-I", CSRC, os.path.join(CSRC, src), "-o", out],
+                             check=True, capture_output=True, text=True)
+        warn = [ln for ln in res.stderr.splitlines() if "uninitialized" in ln]
         with open(out) as f:
-            return src, overlapping_stores(f.read())
+            return src, overlapping_stores(f.read()), warn
 
     try:
         with concurrent.futures.ThreadPoolExecutor(max_workers=4) as ex:
             results = list(ex.map(build, SOURCES))
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
-    for src, (n, bad) in results:
+    for src, (n, bad), warn in results:
         assert n > 100, f"{src}: too few stores parsed ({n})"
         assert not bad, f"{src}: {bad[:3]}"
+        # a value read before it is written is undefined: the compiler may then
+        # store whatever register it likes (an address included)
+        assert not warn, f"{src}: {warn[:3]}"

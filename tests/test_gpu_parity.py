@@ -221,3 +221,33 @@ def test_vector_gate_workload_sampled():
     inp = synth.make_inputs(w, device=DEV, seed=1003, dS_out_std=0.0)
     got = run_chain(inp, w["seg_lens"])
     check_chain("bf16", inp, got, w["seg_lens"], pairs=[(0, 5), (1, 12)])
+
+
+def test_tuned_setting_is_applied(monkeypatch):
+    """chain_fwd / chain_bwd with ts and overlap left unset take the profiled
+    per-shape setting (paper_2608_06838_amd.tuned): bitwise the outputs of
+    passing that setting explicitly, different from the automatic stride's
+    rounding, and within the parity bar of the oracle."""
+    from paper_2608_06838_amd import tuned
+    w = synth.workload("mid_bf16", B=1, H=4, D=128)
+    seg_lens = [512, 256, 448]
+    key = tuned.key(1, 4, 128, "bf16", "scalar", seg_lens)
+    monkeypatch.setitem(tuned.TABLE, key, dict(ts=128, overlap=False))
+    inp = synth.make_inputs(w, device="cpu", seed=17, dS_out_std=0.1, L=sum(seg_lens))
+    g = on_gpu(inp)
+    say("[chain] tuned setting lookup")
+
+    def chain(**kw):
+        o, S_bnd = sf.chain_fwd(g["q"], g["k"], g["v"], g["g"], seg_lens, g["S_in"], **kw)
+        grads = sf.chain_bwd(g["q"], g["k"], g["v"], g["g"], seg_lens, S_bnd, g["dO"], g["dS_out"], **kw)
+        torch.cuda.synchronize()
+        return (o, S_bnd) + tuple(grads)
+
+    looked_up, explicit, other = chain(), chain(ts=128, overlap=False), chain(ts=0, overlap=False)
+    for x, y in zip(looked_up, explicit):
+        assert torch.equal(x, y)
+    # a different stride sums in another order: some output differs in its last bits
+    assert any(not torch.equal(x, y) for x, y in zip(looked_up, other))
+    got = dict(zip(("o", "S_bnd", "dq", "dk", "dv", "dg", "dS_in"), looked_up))
+    got["S_out"] = got["S_bnd"][-1]
+    check_chain("bf16", inp, got, seg_lens)

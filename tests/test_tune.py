@@ -8,7 +8,7 @@ from paper_2608_06838_amd import tune
 def test_ts_candidates():
     c = tune.ts_candidates([65536, 20480])
     assert c[0] == 0 and all(t % 64 == 0 and 0 < t <= 65536 for t in c[1:])
-    assert tune.ts_candidates([640]) == [0, 512]
+    assert tune.ts_candidates([640]) == [0, 128, 256, 512]
 
 
 def test_partition_candidates():
