@@ -388,12 +388,14 @@ GDN_KERNELS = ["gdn_prep", "gdn_scan", "gdn_out", "gdn_store", "gdn_dprep", "gdn
 def gdn_dchunk_flops(D, C=64):
     """Algorithmic flops per 64-token chunk and head of the delta rule's
     per-chunk parameter gradients, given the state S entering the chunk and
-    dS' leaving it (gated delta rule, for the term list):
-    dense D-contractions 10 C D^2 (U = Ubar - W S, K dS', dO S^T, dU S^T,
-    U dS'^T), strictly lower C x C products 6 C^2 D / 2 each counted as
-    C^2 D (scores, the two dP-type products, dq, dk and their mirror), the
-    triangular inverse C^3 / 3 and the two T-products 4 C^2 D."""
-    return 10 * C * D * D + 6 * C * C * D + C ** 3 // 3 + 4 * C * C * D
+    the gradient dS' of the state leaving it (2 m n k per product, triangular
+    factors at their triangular size, gated delta rule):
+      five C x D x D products (K S, K dS', G_U S^T, dO S^T, U dS'^T): 10 C D^2;
+      lower-triangular-with-diagonal C x C products (Q K^T, T R, P^T dO, T^T dU,
+      dO U^T, (dP o Gamma) K, (dP o Gamma)^T Q): 7 C (C + 1) D;
+      strictly lower ones (K K^T, G_U U^T, Ah K, Ah^T K): 4 C (C - 1) D;
+      the triangular inverse: C^3 / 3."""
+    return 10 * C * D * D + 7 * C * (C + 1) * D + 4 * C * (C - 1) * D + C ** 3 // 3
 
 
 def bench_gdn(args):
@@ -484,6 +486,101 @@ def bench_gdn(args):
                                          f"{tc:.1f} s wall; value scaled to a {H}-head layer"}
     print(json.dumps(out), flush=True)
     timer.close()
+
+
+TABLE4_HEADS = (20, 10, 8)           # heads per GPU of the paper's 3B / 15B / 32B GDN models
+TABLE4_LENS = (8192, 16384, 32768, 65536)
+TABLE4_SPLITS = (None, 0.3, 0.5, 0.7, 0.9)  # split fraction f of the call (None: one segment)
+
+
+def _split(L, f):
+    if f is None:
+        return [L]
+    a = int(round(f * L / 64)) * 64
+    return [a, L - a] if 0 < a < L else [L]
+
+
+def table4_main(args):
+    """Table-4(a)-style study (Sec. 3.4 "State Transition Grid Optimization"
+    and "Split and Overlap", Table 4(a)): for each operator call of L tokens
+    at the per-GPU head counts of the paper's models, time the forward and the
+    backward separately for every superchunk length and split fraction f (the
+    call run as two chained segments f L and (1 - f) L with the state scans
+    overlapped, the paper's split schedule), and report the default and the
+    fastest setting per pass."""
+    import torch
+    import paper_2608_06838_amd as sf
+    from paper_2608_06838_amd import synth, tune
+
+    dev = torch.device("cuda:0")
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ops = [args.table4] if args.table4 in ("gla", "gdn") else ["gla", "gdn"]
+    rows = []
+    for op in ops:
+        for H in TABLE4_HEADS:
+            for L in TABLE4_LENS:
+                if op == "gla":
+                    w = synth.workload("ctx256k_h40", H=H, seg_lens=[L])
+                    inp = synth.make_inputs(w, device=dev, seed=1100 + H)
+                    tss = [0, 256, 512, 1024, 2048, 4096]
+                else:
+                    inp = synth.make_gdn_inputs(1, L, H, 128, device=dev, seed=4100 + H)
+                    gen = torch.Generator(device=dev).manual_seed(4200 + H)
+                    inp["dO"] = torch.randn((1, L, H, 128), device=dev, generator=gen).to(torch.bfloat16)
+                    tss = [0, 1024, 2048, 4096, 8192]
+                res = []
+                for f in TABLE4_SPLITS:
+                    seg = _split(L, f)
+                    if f is not None and len(seg) == 1:
+                        continue
+                    for ts in tss:
+                        if ts and ts > max(seg):
+                            continue
+                        ov = f is not None
+
+                        def call():
+                            if op == "gla":
+                                o, S_bnd = sf.chain_fwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, inp["S_in"],
+                                                        ts=ts, overlap=ov)
+                                ev[1].record()
+                                sf.chain_bwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, S_bnd, inp["dO"], None,
+                                             ts=ts, overlap=ov)
+                            else:
+                                x = (inp["q"], inp["k"], inp["v"], inp["g"], inp["beta"], seg)
+                                o, S_bnd = sf.gdn_chain_fwd(*x, inp["S_in"], ts=ts, overlap=ov)
+                                ev[1].record()
+                                sf.gdn_chain_bwd(*x, S_bnd, inp["dO"], None, ts=ts, overlap=ov)
+
+                        try:
+                            call()
+                            torch.cuda.synchronize()
+                            tf = tb = 0.0
+                            for _ in range(args.steps):
+                                ev[0].record()
+                                call()
+                                ev[2].record()
+                                torch.cuda.synchronize()
+                                tf += ev[0].elapsed_time(ev[1])
+                                tb += ev[1].elapsed_time(ev[2])
+                            res.append(dict(ts=ts or "auto", f=f, fwd_ms=tf / args.steps, bwd_ms=tb / args.steps))
+                        except Exception as e:  # a candidate that does not run is reported
+                            res.append(dict(ts=ts or "auto", f=f, error=str(e)[:200]))
+                ok = [r for r in res if "error" not in r]
+                base = next(r for r in ok if r["ts"] == "auto" and r["f"] is None)
+                bf = min(ok, key=lambda r: r["fwd_ms"])
+                bb = min(ok, key=lambda r: r["bwd_ms"])
+                rows.append(dict(op=op, heads=H, L=L, default=dict(fwd_ms=base["fwd_ms"], bwd_ms=base["bwd_ms"]),
+                                 best_fwd=dict(ts=bf["ts"], f=bf["f"], ms=bf["fwd_ms"],
+                                               speedup=base["fwd_ms"] / bf["fwd_ms"]),
+                                 best_bwd=dict(ts=bb["ts"], f=bb["f"], ms=bb["bwd_ms"],
+                                               speedup=base["bwd_ms"] / bb["bwd_ms"]),
+                                 total_speedup=(base["fwd_ms"] + base["bwd_ms"]) / (bf["fwd_ms"] + bb["bwd_ms"]),
+                                 candidates=res))
+                print(json.dumps({k: v for k, v in rows[-1].items() if k != "candidates"}), file=sys.stderr, flush=True)
+                del inp
+                torch.cuda.empty_cache()
+    print(json.dumps(dict(study="Table 4(a)-style: superchunk length x split fraction, fwd and bwd per call",
+                          steps=args.steps, rows=rows)), flush=True)
 
 
 def bench_recurrence(args):
@@ -609,6 +706,8 @@ def main():
                     help="time the chain for each superchunk stride and overlap setting (one JSON table)")
     ap.add_argument("--partition-study", action="store_true",
                     help="time the chain for the hybrid-aware partition candidates (one JSON table)")
+    ap.add_argument("--table4", default=None, choices=("gla", "gdn", "both"),
+                    help="per-call study over heads 20/10/8 and 8K-64K tokens: superchunk length x split fraction")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the recurrence shards over "
@@ -620,6 +719,8 @@ def main():
         bench_gdn(args)
     elif args.tune_ts or args.partition_study:
         study_main(args)
+    elif args.table4:
+        table4_main(args)
     else:
         bench_recurrence(args)
 

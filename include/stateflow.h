@@ -347,8 +347,8 @@ sf_status sf_gdn_fwd(const sf_shape *shape, const void *q, const void *k, const 
  * transpose of the forward's chunk map) and is stored for every chunk; the
  * parameter gradients of all chunks are then computed in parallel.
  *   ws  device scratch of at least sf_gdn_bwd_workspace_bytes(): two fp32
- *       D x D states per 64-token chunk plus the superchunk maps and the
- *       per-chunk kernel's scratch; contents on entry ignored.
+ *       D x D states per 64-token chunk plus the superchunk maps; contents
+ *       on entry ignored.
  * Same shape rules as sf_gdn_fwd; same ownership, validation, aliasing and
  * error rules as the other entry points.
  */

@@ -1124,13 +1124,12 @@ size_t gdn_ws_bytes(const Shape &r, int ts) {
 }
 
 // Backward workspace: the forward's boundary states and maps (M, N for every
-// superchunk), E_J and dS_end(J), the state and the state gradient of every
-// chunk, and the per-chunk gradient kernel's scratch slabs.
+// superchunk), E_J and dS_end(J), and the state and the state gradient of
+// every chunk.  n_x: workgroups of the per-chunk gradient kernel (one per CU).
 struct GdnBwdWs {
-    size_t S = 0, M = 0, N = 0, E = 0, De = 0, Sc = 0, Dc = 0, X = 0, total = 0;
+    size_t S = 0, M = 0, N = 0, E = 0, De = 0, Sc = 0, Dc = 0, total = 0;
     int n_x = 0;
 };
-constexpr int kGdnSlabs = 1024;
 // for n superchunks and nc chunks per (batch, head)
 GdnBwdWs gdn_bwd_ws_n(const Shape &r, int n, size_t nc) {
     GdnBwdWs w;
@@ -1149,8 +1148,7 @@ GdnBwdWs gdn_bwd_ws_n(const Shape &r, int n, size_t nc) {
     }
     take(w.Sc, std::max<size_t>(bh * nc * SS, 1));
     take(w.Dc, std::max<size_t>(bh * nc * SS, 1));
-    w.n_x = (int)std::max<size_t>(1, std::min<size_t>(bh * nc, kGdnSlabs));
-    take(w.X, (size_t)w.n_x * 8 * 64 * r.D * 4);
+    w.n_x = (int)std::max<size_t>(1, std::min<size_t>(bh * nc, (size_t)device_cus()));
     w.total = off;
     return w;
 }
@@ -1399,7 +1397,6 @@ sf_status sf_gdn_bwd(const sf_shape *shape, const void *q, const void *k, const 
     }
     a.wsSc = (float *)(base + L.Sc);
     a.wsDc = (float *)(base + L.Dc);
-    a.wsX = (float *)(base + L.X);
     a.n_x = L.n_x;
     return gdn_run_bwd(a, r.D, (hipStream_t)stream, timing_of(tuning));
 }
@@ -1552,7 +1549,6 @@ sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *
         }
         a.wsSc = (float *)(base + Lw.Sc);
         a.wsDc = (float *)(base + Lw.Dc);
-        a.wsX = (float *)(base + Lw.X);
         a.n_x = Lw.n_x;
         tok += seg_len[i];
     }

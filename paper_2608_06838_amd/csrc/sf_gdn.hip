@@ -806,121 +806,150 @@ __global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
 }
 
 // Parameter gradients of one chunk per item (b, h, chunk), items in a
-// grid-stride loop.  Every product runs on MFMA: 8 waves, wave w owns rows
-// [16 (w % 4), +16) and half the column tiles (half w / 4) of each 64-row
-// result, so two waves share each SIMD.  Operands enter as bf16 fragments,
-// computed fp32 operands as hi/lo pairs (three products, the lo x lo term
-// dropped), q, k, v, dO exactly.  q, k, v, dO and the 64 x 64 matrices sit in
-// LDS; the 64 x D intermediates in a per-workgroup scratch slab of wsX (eight
-// 64 x D fp32 matrices, addressed through one buffer resource); S and dS' come
-// from the stored per-chunk states.  T = (I + A)^{-1} comes from gdn_tinv
-// with beta applied per row.
+// grid-stride loop, one workgroup of 16 waves per CU.  S is the state entering
+// the chunk and dS' the gradient of the state leaving it (both stored per chunk
+// by the walks).  The value channels go in blocks of VB = 32 columns: each
+// block of S and dS' is read from memory once and staged in LDS, and every
+// contraction over the value channels accumulates in registers across the
+// blocks.  Two identities keep W = T diag(beta gamma) K and Ubar out of the
+// kernel (and out of memory):
+//   U_J = Ubar_J - W S_J = T diag(beta) (V_J - diag(gamma) K S_J),
+//   G_W = T^T (-dU S^T) = -G_U S^T,   dA = -(G_W W^T + G_U Ubar^T) = -G_U U^T.
+// Per block J, waves 0-7 (group A) and 8-15 (group B):
+//   A: Y = K S_J, R = diag(beta) (V_J - diag(gamma) Y), U_J = T R;
+//   B: dU_J = diag(e) K dS'_J + P^T dO_J, G_U,J = T^T dU_J (dv_J = beta G_U,J);
+//   A: G_W -= G_U,J S_J^T, dK_S += U_J dS'_J^T;
+//   B: dQ_S += dO_J S_J^T, dA -= G_U,J U_J^T, dP += dO_J U_J^T.
+// After the blocks (Gamma[t][s] = e^{b_t - b_s}, Ah = dA o beta_t Gamma):
+//   dq = diag(gamma) dQ_S + (dP o Gamma) K                                (B)
+//   dk = diag(e) dK_S + (dP o Gamma)^T Q + diag(beta gamma) G_W + (Ah + Ah^T) K   (A)
+// and dbeta and the log-decay gradient from row and column sums in a fixed
+// order (no atomics).  q, k, v, dO enter the products exactly (bf16); the
+// computed fp32 operands (S, dS', T, P, R, U, dU, G_U, dP o Gamma, Ah) as
+// hi/lo bf16 pairs (three products, lo x lo dropped).
 template <typename T, int D>
-__global__ void __launch_bounds__(512) k_gdn_dchunk(GdnArgs a) {
-    constexpr int LDX = D + 8, LD6 = C + 4, NT2 = D / 32, NTH = 512;
-    __shared__ __attribute__((aligned(16))) T xq[C * LDX], xk[C * LDX], xo[C * LDX], xv[C * LDX];
-    __shared__ __attribute__((aligned(16))) float sKK[C * LD6];  // e^{b_t-b_s} k_t.k_s, s < t (later Ah + Ah^T)
-    __shared__ __attribute__((aligned(16))) float sT[C * LD6];   // (I + A)^{-1}
-    __shared__ __attribute__((aligned(16))) float sPt[C * LD6];  // e^{b_t-b_s} q_t.k_s, s <= t
-    __shared__ __attribute__((aligned(16))) float sdP[C * LD6];  // (dO U^T o Gamma)[t][s], s <= t
-    __shared__ float sb[C], sg[C], se[C], sbe[C], sRb[2 * C], sRd[2 * C], sCol[4 * C], s63[8];
+__global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
+    constexpr int NTH = 1024, VB = 32, NBLK = D / VB, NTW = D / 32;
+    constexpr int LDX = D + 8, LD6 = C + 4, LDB = VB + 4, LDV = VB + 8, LDOT = C + 8, LDU = VB + 4, LDR = VB + 1;
+    constexpr int NBLKF = 2 * D * LDB > 2 * C * LD6 ? 2 * D * LDB : 2 * C * LD6;
+    static_assert(2 * C * LDR <= C * LD6, "R and dU fit in the scores' buffer");
+    __shared__ __attribute__((aligned(16))) T xq[C * LDX], xk[C * LDX];
+    __shared__ __attribute__((aligned(16))) float sT[C * LD6];  // T = (I + A)^{-1}
+    __shared__ __attribute__((aligned(16))) float sP[C * LD6];  // P[t][s] = e^{b_t - b_s} q_t.k_s, s <= t
+    __shared__ __attribute__((aligned(16))) float sX[C * LD6];  // KK o Gamma (s < t) for the inverse; then R, dU
+    __shared__ __attribute__((aligned(16))) float sBlk[NBLKF];  // S_J, dS'_J; after the blocks dP o Gamma, Ah + Ah^T
+    __shared__ __attribute__((aligned(16))) T sV[C * LDV], sO[C * LDV], sOt[VB * LDOT];
+    __shared__ __attribute__((aligned(16))) float sU[C * LDU], sGU[C * LDU];
+    __shared__ float sb[C], sg[C], se[C], sbe[C];
+    __shared__ float sRow[6][2][C];  // row-sum partials, two waves per row tile
+    __shared__ float sCol[4][C];     // column-sum partials, one per row tile
+    __shared__ float sWav[16];
 
-    const int tid = threadIdx.x, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), r0 = 16 * (w & 3), hf = w >> 2;
-    const int64_t SS = (int64_t)D * D, SX = (int64_t)C * D;
+    float *const sSb = sBlk, *const sDb = sBlk + D * LDB;      // [k'][v] of the block
+    float *const sE1 = sBlk, *const sE2 = sBlk + C * LD6;      // dP o Gamma, Ah + Ah^T
+    float *const sR = sX, *const sdU = sX + C * LDR;           // [t][v] of the block
+
+    const int tid = threadIdx.x;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    int lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
+    const bool grpB = w >= 8;
+    const int wg = w & 7, mt = wg & 3, half = wg >> 2;  // row tile; which half of the column tiles
+    const int64_t SS = (int64_t)D * D;
     const int nc = (int)(a.L / C);
     const int64_t items = (int64_t)a.B * a.H * nc;
-    const rsrc_t rX = buf_rsrc(a.wsX + (int64_t)blockIdx.x * 8 * SX, (uint32_t)(8 * SX * 4));
-    constexpr uint32_t MB = (uint32_t)(C * D * 4);  // bytes of one slab matrix
-    constexpr uint32_t mW = 0, mUb = MB, mU = 2 * MB, mdU = 3 * MB, mGW = 4 * MB, mGU = 5 * MB, mQ = 6 * MB, mK = 7 * MB;
-    // lane offsets: row-major fragment (row n16, k 8q4..), transposed fragment
-    // (k 8q4 + j, row n16), accumulator element (row 4q4 + r, column n16)
-    const uint32_t v_rm = (uint32_t)((n16 * D + 8 * q4) * 4), v_tr = (uint32_t)((8 * q4 * D + n16) * 4);
-    const uint32_t v_acc = (uint32_t)((4 * q4 * D + n16) * 4);
 
-    auto g_rm = [&](rsrc_t rs, uint32_t base, int rr, int kk, frag_t<T> &h, frag_t<T> &l) {
-        const uint32_t so = base + (uint32_t)((rr * D + kk) * 4);
-        const f32x4 x0 = buf_ld<f32x4>(rs, v_rm, so), x1 = buf_ld<f32x4>(rs, v_rm + 16, so);
-        const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-        split8<T, true>(x, h, l);
+    // fragments: rows row0 + n16, contraction k0 + 8 q4 + j (j < 8)
+    auto x_rm = [&](const T *M, int ld, int row0, int k0) {  // exact, M[row][k]
+        return *reinterpret_cast<const frag_t<T> *>(M + (row0 + n16) * ld + k0 + 8 * q4);
     };
-    auto g_tr = [&](rsrc_t rs, uint32_t base, int rr, int kk, frag_t<T> &h, frag_t<T> &l) {
-        const uint32_t so = base + (uint32_t)((kk * D + rr) * 4);
-        float x[8];
+    auto x_tr = [&](const T *M, int ld, int row0, int k0) {  // exact, M[k][row]
+        frag_t<T> f = {};
 #pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] = buf_ld<float>(rs, v_tr + j * D * 4, so);
-        split8<T, true>(x, h, l);
+        for (int j = 0; j < 8; ++j) f[j] = M[(k0 + 8 * q4 + j) * ld + row0 + n16];
+        return f;
     };
-    auto g_acc_ld = [&](rsrc_t rs, uint32_t base, int ct, f32x4 &c) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) c[r] = buf_ld<float>(rs, v_acc + r * D * 4, base + (uint32_t)((r0 * D + 16 * ct) * 4));
-    };
-    auto g_acc_st = [&](rsrc_t rs, uint32_t base, int ct, const f32x4 &c) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) buf_st<float>(rs, v_acc + r * D * 4, base + (uint32_t)((r0 * D + 16 * ct) * 4), c[r]);
-    };
-    // the same at an explicit row base (row tile rt: rows 16 rt + 4 q4 + r)
-    auto g_acc_ld_rt = [&](rsrc_t rs, uint32_t base, int rt, int ct, f32x4 &c) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) c[r] = buf_ld<float>(rs, v_acc + r * D * 4, base + (uint32_t)((16 * rt * D + 16 * ct) * 4));
-    };
-    auto g_acc_st_rt = [&](rsrc_t rs, uint32_t base, int rt, int ct, const f32x4 &c) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) buf_st<float>(rs, v_acc + r * D * 4, base + (uint32_t)((16 * rt * D + 16 * ct) * 4), c[r]);
-    };
-    auto l_rm = [&](const float *M, int rr, int kk, frag_t<T> &h, frag_t<T> &l) {  // LDS 64 x 64, M[row][k]
-        const float *p = M + (rr + n16) * LD6 + kk + 8 * q4;
+    auto f_rm = [&](const float *M, int ld, int row0, int k0, frag_t<T> &h, frag_t<T> &l) {  // M[row][k], split
+        const float *p = M + (row0 + n16) * ld + k0 + 8 * q4;
         const f32x4 x0 = *reinterpret_cast<const f32x4 *>(p), x1 = *reinterpret_cast<const f32x4 *>(p + 4);
         const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
         split8<T, true>(x, h, l);
     };
-    auto l_tr = [&](const float *M, int rr, int kk, frag_t<T> &h, frag_t<T> &l) {  // LDS 64 x 64, M[k][row]
+    auto f_tr = [&](const float *M, int ld, int row0, int k0, frag_t<T> &h, frag_t<T> &l) {  // M[k][row], split
         float x[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] = M[(kk + 8 * q4 + j) * LD6 + rr + n16];
+        for (int j = 0; j < 8; ++j) x[j] = M[(k0 + 8 * q4 + j) * ld + row0 + n16];
         split8<T, true>(x, h, l);
-    };
-    auto x_rm = [&](const T *M, int rr, int kk) {  // exact, M[row][k]
-        return *reinterpret_cast<const frag_t<T> *>(M + (rr + n16) * LDX + kk + 8 * q4);
-    };
-    auto x_tr = [&](const T *M, int rr, int kk) {  // exact, M[k][row]
-        frag_t<T> f = {};
-#pragma unroll
-        for (int j = 0; j < 8; ++j) f[j] = M[(kk + 8 * q4 + j) * LDX + rr + n16];
-        return f;
     };
     auto mma3 = [](f32x4 &c, const frag_t<T> &ah, const frag_t<T> &al, const frag_t<T> &bh, const frag_t<T> &bl) {
         mma(c, ah, bh);
         mma(c, ah, bl);
         mma(c, al, bh);
     };
-    auto zeroN = [](f32x4 (&c)[NT2]) {
+    auto rowsum16 = [](float v) {  // sum over the 16 lanes of a row group
 #pragma unroll
-        for (int i = 0; i < NT2; ++i) c[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int m = 1; m < 16; m <<= 1) v += __shfl_xor(v, m);
+        return v;
     };
-    auto zero2 = [](f32x4 (&c)[2]) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) c[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    };
-    // accumulator c[nt][r] <-> row r0 + 4 q4 + r, column 16 (hf NT2 + nt) + n16 (64 x D results)
-    // or 16 (2 hf + nt) + n16 (64 x 64 results)
+    const f32x4 z4 = {0.f, 0.f, 0.f, 0.f};
 
     for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
+        // the lane index, opaque per item: the many per-lane LDS addresses are
+        // recomputed where they are used instead of being hoisted out of the
+        // item loop (where they would not fit the 128 registers of 16 waves)
+        asm volatile("" : "+v"(lane));
+        q4 = lane >> 4;
+        n16 = lane & 15;
         const int bh = (int)(it / nc), ch = (int)(it % nc), bb = bh / a.H, hh = bh % a.H;
         const int64_t xo0 = bb * a.sx_b + hh * a.sx_h + (int64_t)ch * C * a.sx_l;
         const int64_t go0 = bb * a.sg_b + hh * a.sg_h + (int64_t)ch * C * a.sg_l;
-        const float *S = a.wsSc + ((int64_t)bh * nc + ch) * SS;
-        const float *dS = a.wsDc + ((int64_t)bh * nc + ch) * SS;
-        const rsrc_t rS = buf_rsrc(S, (uint32_t)(SS * 4)), rD = buf_rsrc(dS, (uint32_t)(SS * 4));
-        __syncthreads();  // the previous item is done with LDS and the slab
+        const float *Sg = a.wsSc + ((int64_t)bh * nc + ch) * SS;
+        const float *dSg = a.wsDc + ((int64_t)bh * nc + ch) * SS;
+        const T *Vg = (const T *)a.v + xo0, *Og = (const T *)a.dO + xo0;
+
+        // block staging: S_J and dS'_J as D x VB floats (one 16-byte unit of
+        // each per thread), V_J and dO_J as C x VB bf16 (threads 0-255 and 256-511)
+        constexpr int NSU = D * VB / 4;
+        int tidv = tid;
+        asm volatile("" : "+v"(tidv));
+        const int su_r = tidv / (VB / 4), su_c = 4 * (tidv % (VB / 4));
+        const int vu = tidv & 255, vu_t = vu / (VB / 8), vu_c = 8 * (vu % (VB / 8));
+        f32x4 pS = z4, pD = z4;
+        frag_t<T> pX = {};
+        auto fetch = [&](int jb) {
+            const int v0 = jb * VB;
+            if (tid < NSU) {
+                pS = *reinterpret_cast<const f32x4 *>(Sg + (int64_t)su_r * D + v0 + su_c);
+                pD = *reinterpret_cast<const f32x4 *>(dSg + (int64_t)su_r * D + v0 + su_c);
+            }
+            if (tid < 512) {
+                const T *src = (tid < 256 ? Vg : Og) + (int64_t)vu_t * a.sx_l + v0 + vu_c;
+                pX = *reinterpret_cast<const frag_t<T> *>(src);
+            }
+        };
+        float sd = 0.f;  // <dS', S> over this thread's units
+        auto stage = [&]() {
+            if (tid < NSU) {
+                *reinterpret_cast<f32x4 *>(&sSb[su_r * LDB + su_c]) = pS;
+                *reinterpret_cast<f32x4 *>(&sDb[su_r * LDB + su_c]) = pD;
+                sd = fmaf(pS[0], pD[0], fmaf(pS[1], pD[1], fmaf(pS[2], pD[2], fmaf(pS[3], pD[3], sd))));
+            }
+            if (tid < 256) {
+                *reinterpret_cast<frag_t<T> *>(&sV[vu_t * LDV + vu_c]) = pX;
+            } else if (tid < 512) {
+                *reinterpret_cast<frag_t<T> *>(&sO[vu_t * LDV + vu_c]) = pX;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) sOt[(vu_c + j) * LDOT + vu_t] = pX[j];
+            }
+        };
+
+        __syncthreads();  // the previous item is done with LDS
         for (int e = tid; e < C * D / 8; e += NTH) {
             const int t = e / (D / 8), c8 = 8 * (e % (D / 8));
             const int64_t off = xo0 + (int64_t)t * a.sx_l + c8;
             *reinterpret_cast<frag_t<T> *>(&xq[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.q + off);
             *reinterpret_cast<frag_t<T> *>(&xk[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.k + off);
-            *reinterpret_cast<frag_t<T> *>(&xo[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.dO + off);
-            *reinterpret_cast<frag_t<T> *>(&xv[t * LDX + c8]) = *reinterpret_cast<const frag_t<T> *>((const T *)a.v + off);
         }
+        fetch(0);
         if (tid < 64) {
             const float b = wave_scan_dpp(a.g[go0 + (int64_t)tid * a.sg_l]);
             const float bC = lane_value(b, 63);
@@ -931,407 +960,301 @@ __global__ void __launch_bounds__(512) k_gdn_dchunk(GdnArgs a) {
         }
         __syncthreads();
 
-        float rowb[4] = {0.f, 0.f, 0.f, 0.f}, rowd[4] = {0.f, 0.f, 0.f, 0.f}, colb[4] = {0.f, 0.f, 0.f, 0.f};
-        float tot63 = 0.f;
-        // scores: k_t.k_s and q_t.k_s
+        // scores: wave w forms tile (w % 4, w / 4) of K K^T and of Q K^T
         {
-            f32x4 pk[2], pq[2];
-            zero2(pk);
-            zero2(pq);
-#pragma unroll
-            for (int kk = 0; kk < D; kk += 32) {
-                const frag_t<T> ak = x_rm(xk, r0, kk), aq = x_rm(xq, r0, kk);
-#pragma unroll
-                for (int nt = 0; nt < 2; ++nt) {
-                    const frag_t<T> bk = x_rm(xk, 16 * (2 * hf + nt), kk);
-                    mma(pk[nt], ak, bk);
-                    mma(pq[nt], aq, bk);
-                }
-            }
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = r0 + 4 * q4 + r, s2 = 16 * (2 * hf + nt) + n16;
-                    const float ga = expf(sb[t] - sb[s2]);
-                    sKK[t * LD6 + s2] = s2 < t ? ga * pk[nt][r] : 0.f;
-                    sPt[t * LD6 + s2] = s2 <= t ? ga * pq[nt][r] : 0.f;
-                }
-        }
-        __syncthreads();
-        // T = (I + A)^{-1}, A = diag(beta) KK
-        gdn_tinv<NTH>(tid, sKK, sT, sbe);
-        // W = T diag(beta gamma) K, Ubar = T diag(beta) V
-        {
-            f32x4 cw[NT2], cu[NT2];
-            zeroN(cw);
-            zeroN(cu);
-#pragma unroll
-            for (int kk = 0; kk < C; kk += 32) {
-                frag_t<T> th, tl;
-                l_rm(sT, r0, kk, th, tl);
-#pragma unroll
-                for (int nt = 0; nt < NT2; ++nt) {
-                    const int col = 16 * (NT2 * hf + nt) + n16;
-                    float xw[8], xu[8];
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const int s2 = kk + 8 * q4 + j;
-                        xw[j] = sbe[s2] * sg[s2] * tof<T>(xk[s2 * LDX + col]);
-                        xu[j] = sbe[s2] * tof<T>(xv[s2 * LDX + col]);
-                    }
-                    frag_t<T> bh, bl;
-                    split8<T, true>(xw, bh, bl);
-                    mma3(cw[nt], th, tl, bh, bl);
-                    split8<T, true>(xu, bh, bl);
-                    mma3(cu[nt], th, tl, bh, bl);
-                }
-            }
-#pragma unroll
-            for (int nt = 0; nt < NT2; ++nt) {
-                g_acc_st(rX, mW, NT2 * hf + nt, cw[nt]);
-                g_acc_st(rX, mUb, NT2 * hf + nt, cu[nt]);
-            }
-        }
-        __syncthreads();
-        // U = Ubar - W S;  dU = diag(e^{b_C - b}) K dS' + P^T dO.  Here wave w
-        // owns row tiles 2 (w % 2) + i (i < 2) and column tiles CT (w / 2) + j
-        // (j < CT), so no two waves load the same S or dS' fragment.
-        {
-            constexpr int CT = NT2 / 2 > 0 ? NT2 / 2 : 1;
-            static_assert(2 * CT * 8 == 4 * (D / 16), "eight waves cover the 4 x D/16 tiles once");
-            const int rp = w & 1, cg = w >> 1;
-            f32x4 cu[2][CT], cd[2][CT];
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < CT; ++j) {
-                    g_acc_ld_rt(rX, mUb, 2 * rp + i, CT * cg + j, cu[i][j]);
-                    cd[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-                }
+            const int st = w >> 2;
+            f32x4 pk = z4, pq = z4;
 #pragma unroll 1
             for (int kk = 0; kk < D; kk += 32) {
-                frag_t<T> wh[2], wl[2], ak[2];
-#pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    g_rm(rX, mW, 16 * (2 * rp + i), kk, wh[i], wl[i]);
-                    wh[i] = -wh[i];
-                    wl[i] = -wl[i];
-                    ak[i] = x_rm(xk, 16 * (2 * rp + i), kk);
-                }
-#pragma unroll
-                for (int j = 0; j < CT; ++j) {
-                    frag_t<T> sh, sl;
-                    g_tr(rS, 0, 16 * (CT * cg + j), kk, sh, sl);
-#pragma unroll
-                    for (int i = 0; i < 2; ++i) mma3(cu[i][j], wh[i], wl[i], sh, sl);
-                    g_tr(rD, 0, 16 * (CT * cg + j), kk, sh, sl);
-#pragma unroll
-                    for (int i = 0; i < 2; ++i) {
-                        mma(cd[i][j], ak[i], sh);
-                        mma(cd[i][j], ak[i], sl);
-                    }
-                }
+                const frag_t<T> bk = x_rm(xk, LDX, 16 * st, kk);
+                mma(pk, x_rm(xk, LDX, 16 * mt, kk), bk);
+                mma(pq, x_rm(xq, LDX, 16 * mt, kk), bk);
             }
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < CT; ++j)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) cd[i][j][r] *= se[16 * (2 * rp + i) + 4 * q4 + r];
-#pragma unroll
-            for (int kk = 0; kk < C; kk += 32) {
-                frag_t<T> ph[2], pl[2];
-#pragma unroll
-                for (int i = 0; i < 2; ++i) l_tr(sPt, 16 * (2 * rp + i), kk, ph[i], pl[i]);  // P^T[t][t'] = P[t'][t]
-#pragma unroll
-                for (int j = 0; j < CT; ++j) {
-                    const frag_t<T> bo = x_tr(xo, 16 * (CT * cg + j), kk);
-#pragma unroll
-                    for (int i = 0; i < 2; ++i) {
-                        mma(cd[i][j], ph[i], bo);
-                        mma(cd[i][j], pl[i], bo);
-                    }
-                }
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * mt + 4 * q4 + r, s2 = 16 * st + n16;
+                const float ga = expf(sb[t] - sb[s2]);
+                sX[t * LD6 + s2] = s2 < t ? ga * pk[r] : 0.f;
+                sP[t * LD6 + s2] = s2 <= t ? ga * pq[r] : 0.f;
             }
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < CT; ++j) {
-                    g_acc_st_rt(rX, mU, 2 * rp + i, CT * cg + j, cu[i][j]);
-                    g_acc_st_rt(rX, mdU, 2 * rp + i, CT * cg + j, cd[i][j]);
-                }
         }
         __syncthreads();
-        // G_U = T^T dU (dv, dbeta)
-        {
-            f32x4 cg[NT2];
-            zeroN(cg);
+        gdn_tinv<NTH>(tid, sX, sT, sbe);  // T = (I + diag(beta) KK o Gamma)^{-1}; ends with a barrier
+
+        // one accumulator array, overlaid by role (both roles run the same code,
+        // so separate arrays would all stay live on every wave):
+        //   A: G_W = acc[0, NTW), dK_S = acc[NTW, 2 NTW)
+        //   B: dQ_S = acc[0, NTW), dA = acc[NTW, NTW + 2), dP = acc[NTW + 2, NTW + 4)
+        constexpr int NACC = 2 * NTW > NTW + 4 ? 2 * NTW : NTW + 4;
+        f32x4 acc[NACC];
 #pragma unroll
-            for (int kk = 0; kk < C; kk += 32) {
-                frag_t<T> th, tl;
-                l_tr(sT, r0, kk, th, tl);
-#pragma unroll
-                for (int nt = 0; nt < NT2; ++nt) {
-                    frag_t<T> bh, bl;
-                    g_tr(rX, mdU, 16 * (NT2 * hf + nt), kk, bh, bl);
-                    mma3(cg[nt], th, tl, bh, bl);
-                }
-            }
-#pragma unroll
-            for (int nt = 0; nt < NT2; ++nt) {
-                g_acc_st(rX, mGU, NT2 * hf + nt, cg[nt]);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = r0 + 4 * q4 + r, c = 16 * (NT2 * hf + nt) + n16;
-                    ((T *)a.dv)[xo0 + (int64_t)t * a.sx_l + c] = cvt<T>(sbe[t] * cg[nt][r]);
-                    rowd[r] = fmaf(cg[nt][r], tof<T>(xv[t * LDX + c]), rowd[r]);
-                }
-            }
-        }
-        // dW = -dU S^T and diag(gamma) dO S^T
-        {
-            f32x4 cw[NT2], cq[NT2];
-            zeroN(cw);
-            zeroN(cq);
+        for (int j = 0; j < NACC; ++j) acc[j] = z4;
+        f32x4 *const accA = acc, *const accB = acc + NTW, *const dA2 = acc + NTW, *const dP2 = acc + NTW + 2;
+        float rGUv[4] = {0.f, 0.f, 0.f, 0.f};  // B: sum_v G_U v over the blocks
+
+        for (int jb = 0; jb < NBLK; ++jb) {
+            const int v0 = jb * VB, nb = half;  // the wave's 16 columns of the block
+            asm volatile("" : "+v"(lane));      // (as at the top of the item loop)
+            q4 = lane >> 4;
+            n16 = lane & 15;
+            if (jb > 0) __syncthreads();     // every read of the previous block is done
+            stage();
+            if (jb + 1 < NBLK) fetch(jb + 1);
+            __syncthreads();
+            if (!grpB) {  // Y = K S_J;  R = beta (V_J - gamma Y)
+                f32x4 y = z4;
 #pragma unroll 1
-            for (int kk = 0; kk < D; kk += 32) {
-                frag_t<T> uh, ul;
-                g_rm(rX, mdU, r0, kk, uh, ul);
-                uh = -uh;
-                ul = -ul;
-                const frag_t<T> ao = x_rm(xo, r0, kk);
-#pragma unroll
-                for (int nt = 0; nt < NT2; ++nt) {
-                    frag_t<T> sh, sl;
-                    g_rm(rS, 0, 16 * (NT2 * hf + nt), kk, sh, sl);  // B[k'][v] = S[k'][v]
-                    mma3(cw[nt], uh, ul, sh, sl);
-                    mma(cq[nt], ao, sh);
-                    mma(cq[nt], ao, sl);
-                }
-            }
-#pragma unroll
-            for (int nt = 0; nt < NT2; ++nt) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = r0 + 4 * q4 + r, c = 16 * (NT2 * hf + nt) + n16;
-                    cq[nt][r] *= sg[t];
-                    rowb[r] = fmaf(tof<T>(xq[t * LDX + c]), cq[nt][r], rowb[r]);
-                }
-                g_acc_st(rX, mGW, NT2 * hf + nt, cw[nt]);
-                g_acc_st(rX, mQ, NT2 * hf + nt, cq[nt]);
-            }
-        }
-        __syncthreads();
-        // G_W = T^T dW, held until every wave has read dW; dk starts as diag(beta gamma) G_W
-        {
-            f32x4 cg[NT2];
-            zeroN(cg);
-#pragma unroll
-            for (int kk = 0; kk < C; kk += 32) {
-                frag_t<T> th, tl;
-                l_tr(sT, r0, kk, th, tl);
-#pragma unroll
-                for (int nt = 0; nt < NT2; ++nt) {
+                for (int kk = 0; kk < D; kk += 32) {
                     frag_t<T> bh, bl;
-                    g_tr(rX, mGW, 16 * (NT2 * hf + nt), kk, bh, bl);
-                    mma3(cg[nt], th, tl, bh, bl);
+                    f_tr(sSb, LDB, 16 * nb, kk, bh, bl);  // B[v][k'] = S_J[k'][v]
+                    const frag_t<T> ak = x_rm(xk, LDX, 16 * mt, kk);
+                    mma(y, ak, bh);
+                    mma(y, ak, bl);
                 }
-            }
-            __syncthreads();  // every read of dW is done
-#pragma unroll
-            for (int nt = 0; nt < NT2; ++nt) {
-                f32x4 kg4;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int t = r0 + 4 * q4 + r, c = 16 * (NT2 * hf + nt) + n16;
-                    const float kg = cg[nt][r] * tof<T>(xk[t * LDX + c]);
-                    rowd[r] = fmaf(sg[t], kg, rowd[r]);
-                    rowb[r] = fmaf(sbe[t] * sg[t], kg, rowb[r]);
-                    kg4[r] = sbe[t] * sg[t] * cg[nt][r];
+                    const int t = 16 * mt + 4 * q4 + r, v = 16 * nb + n16;
+                    sR[t * LDR + v] = sbe[t] * (tof<T>(sV[t * LDV + v]) - sg[t] * y[r]);
                 }
-                g_acc_st(rX, mGW, NT2 * hf + nt, cg[nt]);
-                g_acc_st(rX, mK, NT2 * hf + nt, kg4);
-            }
-        }
-        __syncthreads();
-        // dA = -(G_W W^T + G_U Ubar^T) on s < t;  dP = dO U^T on s <= t
-        {
-            f32x4 ca[2], cp[2];
-            zero2(ca);
-            zero2(cp);
+            } else {  // dU_J = e o K dS'_J + P^T dO_J
+                f32x4 u = z4;
 #pragma unroll 1
-            for (int kk = 0; kk < D; kk += 32) {
+                for (int kk = 0; kk < D; kk += 32) {
+                    frag_t<T> bh, bl;
+                    f_tr(sDb, LDB, 16 * nb, kk, bh, bl);  // B[v][k'] = dS'_J[k'][v]
+                    const frag_t<T> ak = x_rm(xk, LDX, 16 * mt, kk);
+                    mma(u, ak, bh);
+                    mma(u, ak, bl);
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) u[r] *= se[16 * mt + 4 * q4 + r];
+#pragma unroll 1
+                for (int kk = 0; kk < C; kk += 32) {
+                    frag_t<T> ph, pl;
+                    f_tr(sP, LD6, 16 * mt, kk, ph, pl);                 // A[t][s] = P[s][t]
+                    const frag_t<T> bo = x_rm(sOt, LDOT, 16 * nb, kk);  // B[v][s] = dO_J[s][v]
+                    mma(u, ph, bo);
+                    mma(u, pl, bo);
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) sdU[(16 * mt + 4 * q4 + r) * LDR + 16 * nb + n16] = u[r];
+            }
+            __syncthreads();
+            if (!grpB) {  // U_J = T R
+                f32x4 u = z4;
+#pragma unroll 1
+                for (int kk = 0; kk < C; kk += 32) {
+                    frag_t<T> th, tl, rh, rl;
+                    f_rm(sT, LD6, 16 * mt, kk, th, tl);
+                    f_tr(sR, LDR, 16 * nb, kk, rh, rl);  // B[v][s] = R[s][v]
+                    mma3(u, th, tl, rh, rl);
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) sU[(16 * mt + 4 * q4 + r) * LDU + 16 * nb + n16] = u[r];
+            } else {  // G_U,J = T^T dU_J;  dv_J = beta G_U,J
+                f32x4 gu = z4;
+#pragma unroll 1
+                for (int kk = 0; kk < C; kk += 32) {
+                    frag_t<T> th, tl, dh, dl;
+                    f_tr(sT, LD6, 16 * mt, kk, th, tl);   // A[t][s] = T[s][t]
+                    f_tr(sdU, LDR, 16 * nb, kk, dh, dl);  // B[v][s] = dU[s][v]
+                    mma3(gu, th, tl, dh, dl);
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = 16 * mt + 4 * q4 + r, v = 16 * nb + n16;
+                    sGU[t * LDU + v] = gu[r];
+                    ((T *)a.dv)[xo0 + (int64_t)t * a.sx_l + v0 + v] = cvt<T>(sbe[t] * gu[r]);
+                    rGUv[r] = fmaf(gu[r], tof<T>(sV[t * LDV + v]), rGUv[r]);
+                }
+            }
+            __syncthreads();
+            if (!grpB) {  // G_W -= G_U,J S_J^T;  dK_S += U_J dS'_J^T  (contraction over the block's 32 v)
                 frag_t<T> gh, gl, uh, ul;
-                g_rm(rX, mGW, r0, kk, gh, gl);
-                g_rm(rX, mGU, r0, kk, uh, ul);
+                f_rm(sGU, LDU, 16 * mt, 0, gh, gl);
+                f_rm(sU, LDU, 16 * mt, 0, uh, ul);
                 gh = -gh;
                 gl = -gl;
-                uh = -uh;
-                ul = -ul;
-                const frag_t<T> ao = x_rm(xo, r0, kk);
 #pragma unroll
-                for (int nt = 0; nt < 2; ++nt) {
+                for (int j = 0; j < NTW; ++j) {
+                    const int nt = NTW * half + j;
                     frag_t<T> bh, bl;
-                    g_rm(rX, mW, 16 * (2 * hf + nt), kk, bh, bl);
-                    mma3(ca[nt], gh, gl, bh, bl);
-                    g_rm(rX, mUb, 16 * (2 * hf + nt), kk, bh, bl);
-                    mma3(ca[nt], uh, ul, bh, bl);
-                    g_rm(rX, mU, 16 * (2 * hf + nt), kk, bh, bl);
-                    mma(cp[nt], ao, bh);
-                    mma(cp[nt], ao, bl);
+                    f_rm(sSb, LDB, 16 * nt, 0, bh, bl);  // B[k'][v] = S_J[k'][v]
+                    mma3(accA[j], gh, gl, bh, bl);
+                    f_rm(sDb, LDB, 16 * nt, 0, bh, bl);
+                    mma3(accB[j], uh, ul, bh, bl);
+                    sched_fence();  // one tile's operands live at a time
+                }
+            } else {  // dQ_S += dO_J S_J^T;  dA -= G_U,J U_J^T;  dP += dO_J U_J^T
+                const frag_t<T> ao = x_rm(sO, LDV, 16 * mt, 0);
+#pragma unroll
+                for (int j = 0; j < NTW; ++j) {
+                    frag_t<T> bh, bl;
+                    f_rm(sSb, LDB, 16 * (NTW * half + j), 0, bh, bl);
+                    mma(accA[j], ao, bh);
+                    mma(accA[j], ao, bl);
+                    sched_fence();
+                }
+                frag_t<T> gh, gl;
+                f_rm(sGU, LDU, 16 * mt, 0, gh, gl);
+                gh = -gh;
+                gl = -gl;
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    frag_t<T> uh, ul;
+                    f_rm(sU, LDU, 16 * (2 * half + j), 0, uh, ul);  // B[s][v] = U_J[s][v]
+                    mma3(dA2[j], gh, gl, uh, ul);
+                    mma(dP2[j], ao, uh);
+                    mma(dP2[j], ao, ul);
+                    sched_fence();
                 }
             }
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = r0 + 4 * q4 + r, s2 = 16 * (2 * hf + nt) + n16;
-                    const float kk = sKK[t * LD6 + s2];  // 0 unless s < t
-                    const float dA = s2 < t ? ca[nt][r] : 0.f;
-                    rowd[r] = fmaf(dA, kk, rowd[r]);
-                    const float ea = dA * sbe[t] * kk;  // dA o A
-                    const float pt = sPt[t * LD6 + s2];  // 0 unless s <= t
-                    const float ep = s2 <= t ? cp[nt][r] * pt : 0.f;  // dP o P
-                    rowb[r] += ea + ep;
-                    colb[nt] -= ea + ep;
-                    const float ga = s2 <= t ? expf(sb[t] - sb[s2]) : 0.f;
-                    sdP[t * LD6 + s2] = cp[nt][r] * ga;
-                    ca[nt][r] = dA * sbe[t] * ga;  // Ah
-                }
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt) {  // column sums over this wave's rows
-                float v = colb[nt];
-                v += __shfl_xor(v, 16);
-                v += __shfl_xor(v, 32);
-                if (q4 == 0) sCol[(w & 3) * C + 16 * (2 * hf + nt) + n16] = v;
-            }
-            __syncthreads();  // every read of the scores in sKK is done
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) sKK[(r0 + 4 * q4 + r) * LD6 + 16 * (2 * hf + nt) + n16] = ca[nt][r];
         }
-        __syncthreads();
-        // symmetrise: sKK = Ah + Ah^T (Ah strictly lower)
-        for (int e = tid; e < C * C; e += NTH) {
-            const int t = e / C, s2 = e % C;
-            if (s2 < t) sKK[s2 * LD6 + t] = sKK[t * LD6 + s2];
-            else if (s2 == t) sKK[t * LD6 + t] = 0.f;
-        }
-        __syncthreads();
-        // dq = diag(gamma) dO S^T + dP K
-        {
-            f32x4 cq[NT2];
+        __syncthreads();  // the blocks are done: sBlk, sX are free
+        asm volatile("" : "+v"(lane));
+        q4 = lane >> 4;
+        n16 = lane & 15;
+
+        // B: dA and dP terms.  KK of the wave's two C x C tiles again (exact
+        // bf16 operands), dbeta and decay-gradient sums, dP o Gamma and
+        // Ah + Ah^T (Ah strictly lower, mirrored) to LDS.
+        float rowX[4] = {0.f, 0.f, 0.f, 0.f}, rowY[4] = {0.f, 0.f, 0.f, 0.f};
+        if (grpB) {
 #pragma unroll
-            for (int nt = 0; nt < NT2; ++nt) g_acc_ld(rX, mQ, NT2 * hf + nt, cq[nt]);
-#pragma unroll
-            for (int kk = 0; kk < C; kk += 32) {
-                frag_t<T> ph, pl;
-                l_rm(sdP, r0, kk, ph, pl);
-#pragma unroll
-                for (int nt = 0; nt < NT2; ++nt) {
-                    const frag_t<T> bk = x_tr(xk, 16 * (NT2 * hf + nt), kk);  // B[k'][s] = K[s][k']
-                    mma(cq[nt], ph, bk);
-                    mma(cq[nt], pl, bk);
-                }
-            }
-#pragma unroll
-            for (int nt = 0; nt < NT2; ++nt)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    ((T *)a.dq)[xo0 + (int64_t)(r0 + 4 * q4 + r) * a.sx_l + 16 * (NT2 * hf + nt) + n16] = cvt<T>(cq[nt][r]);
-        }
-        // dk = diag(beta gamma) G_W + diag(e^{b_C - b}) U dS'^T + dP^T Q + (Ah + Ah^T) K
-        {
-            f32x4 ck[NT2];
-            zeroN(ck);
+            for (int j = 0; j < 2; ++j) {
+                const int ns = 2 * half + j;
+                f32x4 kk4 = z4;
 #pragma unroll 1
-            for (int kk = 0; kk < D; kk += 32) {
-                frag_t<T> uh, ul;
-                g_rm(rX, mU, r0, kk, uh, ul);
-#pragma unroll
-                for (int nt = 0; nt < NT2; ++nt) {
-                    frag_t<T> bh, bl;
-                    g_rm(rD, 0, 16 * (NT2 * hf + nt), kk, bh, bl);  // B[k'][v] = dS'[k'][v]
-                    mma3(ck[nt], uh, ul, bh, bl);
-                }
-            }
-#pragma unroll
-            for (int nt = 0; nt < NT2; ++nt) {
-                f32x4 gk;
-                g_acc_ld(rX, mK, NT2 * hf + nt, gk);
+                for (int kk = 0; kk < D; kk += 32) mma(kk4, x_rm(xk, LDX, 16 * mt, kk), x_rm(xk, LDX, 16 * ns, kk));
+                float col = 0.f;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int t = r0 + 4 * q4 + r, c = 16 * (NT2 * hf + nt) + n16;
-                    const float rk = ck[nt][r] * tof<T>(xk[t * LDX + c]);
-                    rowb[r] -= se[t] * rk;
-                    tot63 += se[t] * rk;
-                    ck[nt][r] = fmaf(se[t], ck[nt][r], gk[r]);
+                    const int t = 16 * mt + 4 * q4 + r, s2 = 16 * ns + n16;
+                    const float ge = expf(sb[t] - sb[s2]);
+                    const float dAv = s2 < t ? dA2[j][r] : 0.f;
+                    const float kkm = s2 < t ? ge * kk4[r] : 0.f;
+                    const float dPv = s2 <= t ? dP2[j][r] : 0.f;
+                    rowX[r] = fmaf(dAv, kkm, rowX[r]);                           // sum_s dA KK o Gamma (dbeta)
+                    const float ex = dAv * sbe[t] * kkm + dPv * sP[t * LD6 + s2];  // dA o A + dP o P
+                    rowY[r] += ex;
+                    col -= ex;
+                    sE1[t * LD6 + s2] = s2 <= t ? dPv * ge : 0.f;
+                    const float ah = dAv * sbe[t] * ge;
+                    if (s2 < t) {
+                        sE2[t * LD6 + s2] = ah;
+                        sE2[s2 * LD6 + t] = ah;
+                    } else if (s2 == t) {
+                        sE2[t * LD6 + t] = 0.f;
+                    }
+                }
+                col += __shfl_xor(col, 16);
+                col += __shfl_xor(col, 32);
+                if (q4 == 0) sCol[mt][16 * ns + n16] = col;
+            }
+        }
+        __syncthreads();
+        float rowZ[4] = {0.f, 0.f, 0.f, 0.f};  // A: sum G_W k;  B: gamma sum q dQ_S
+        float rowW[4] = {0.f, 0.f, 0.f, 0.f};  // A: sum dK_S k
+        if (!grpB) {  // dk
+            f32x4 dk[NTW];
+#pragma unroll
+            for (int j = 0; j < NTW; ++j) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = 16 * mt + 4 * q4 + r, c = 16 * (NTW * half + j) + n16;
+                    const float kv = tof<T>(xk[t * LDX + c]);
+                    rowZ[r] = fmaf(accA[j][r], kv, rowZ[r]);
+                    rowW[r] = fmaf(accB[j][r], kv, rowW[r]);
+                    dk[j][r] = se[t] * accB[j][r] + sbe[t] * sg[t] * accA[j][r];
                 }
             }
-#pragma unroll
+#pragma unroll 1
             for (int kk = 0; kk < C; kk += 32) {
-                frag_t<T> ph, pl, ah, al;
-                l_tr(sdP, r0, kk, ph, pl);  // dP^T[t][t'] = dP[t'][t]
-                l_rm(sKK, r0, kk, ah, al);
+                frag_t<T> eh, el, ah, al;
+                f_tr(sE1, LD6, 16 * mt, kk, eh, el);  // A[t][s] = (dP o Gamma)[s][t]
+                f_rm(sE2, LD6, 16 * mt, kk, ah, al);  // A[t][s] = (Ah + Ah^T)[t][s]
 #pragma unroll
-                for (int nt = 0; nt < NT2; ++nt) {
-                    const frag_t<T> bq = x_tr(xq, 16 * (NT2 * hf + nt), kk), bk = x_tr(xk, 16 * (NT2 * hf + nt), kk);
-                    mma(ck[nt], ph, bq);
-                    mma(ck[nt], pl, bq);
-                    mma(ck[nt], ah, bk);
-                    mma(ck[nt], al, bk);
+                for (int j = 0; j < NTW; ++j) {
+                    const int c0 = 16 * (NTW * half + j);
+                    const frag_t<T> bq = x_tr(xq, LDX, c0, kk), bk = x_tr(xk, LDX, c0, kk);  // B[c][s] = X[s][c]
+                    mma(dk[j], eh, bq);
+                    mma(dk[j], el, bq);
+                    mma(dk[j], ah, bk);
+                    mma(dk[j], al, bk);
+                    sched_fence();
                 }
             }
 #pragma unroll
-            for (int nt = 0; nt < NT2; ++nt)
+            for (int j = 0; j < NTW; ++j)
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    ((T *)a.dk)[xo0 + (int64_t)(r0 + 4 * q4 + r) * a.sx_l + 16 * (NT2 * hf + nt) + n16] = cvt<T>(ck[nt][r]);
-        }
-        // gamma_C <dS', S> for b_C
-        {
-            float sd = 0.f;
-            for (int e = 4 * tid; e < D * D; e += 4 * NTH) {
-                const f32x4 x = buf_ld<f32x4>(rD, (uint32_t)(e * 4), 0), y = buf_ld<f32x4>(rS, (uint32_t)(e * 4), 0);
-                sd = fmaf(x[0], y[0], fmaf(x[1], y[1], fmaf(x[2], y[2], fmaf(x[3], y[3], sd))));
+                    ((T *)a.dk)[xo0 + (int64_t)(16 * mt + 4 * q4 + r) * a.sx_l + 16 * (NTW * half + j) + n16] =
+                        cvt<T>(dk[j][r]);
+        } else {  // dq
+            f32x4 dq[NTW];
+#pragma unroll
+            for (int j = 0; j < NTW; ++j) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int t = 16 * mt + 4 * q4 + r, c = 16 * (NTW * half + j) + n16;
+                    dq[j][r] = sg[t] * accA[j][r];
+                    rowZ[r] = fmaf(tof<T>(xq[t * LDX + c]), dq[j][r], rowZ[r]);
+                }
             }
-            tot63 = fmaf(sg[C - 1], sd, tot63);
+#pragma unroll 1
+            for (int kk = 0; kk < C; kk += 32) {
+                frag_t<T> eh, el;
+                f_rm(sE1, LD6, 16 * mt, kk, eh, el);  // A[t][s] = (dP o Gamma)[t][s]
+#pragma unroll
+                for (int j = 0; j < NTW; ++j) {
+                    const frag_t<T> bk = x_tr(xk, LDX, 16 * (NTW * half + j), kk);
+                    mma(dq[j], eh, bk);
+                    mma(dq[j], el, bk);
+                    sched_fence();
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < NTW; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    ((T *)a.dq)[xo0 + (int64_t)(16 * mt + 4 * q4 + r) * a.sx_l + 16 * (NTW * half + j) + n16] =
+                        cvt<T>(dq[j][r]);
         }
-        // row sums over the 16 lanes of each row; tot63 over the workgroup
+        // row sums over the 16 lanes of each row, two waves (halves) per row tile
+        //   sRow[0]: A sum G_W k        [1]: A sum dK_S k       [2]: B gamma sum q dQ_S
+        //   sRow[3]: B sum_v G_U v      [4]: B sum dA KK o Gamma [5]: B rows of dA o A + dP o P
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            float vb = rowb[r], vd = rowd[r];
-#pragma unroll
-            for (int m = 1; m < 16; m <<= 1) {
-                vb += __shfl_xor(vb, m);
-                vd += __shfl_xor(vd, m);
-            }
+            const int t = 16 * mt + 4 * q4 + r;
+            const float z = rowsum16(rowZ[r]), wv = rowsum16(rowW[r]);
+            const float x = rowsum16(rowX[r]), y = rowsum16(rowY[r]), u = rowsum16(rGUv[r]);
             if (n16 == 0) {
-                sRb[hf * C + r0 + 4 * q4 + r] = vb;
-                sRd[hf * C + r0 + 4 * q4 + r] = vd;
+                if (!grpB) {
+                    sRow[0][half][t] = z;
+                    sRow[1][half][t] = wv;
+                } else {
+                    sRow[2][half][t] = z;
+                    sRow[3][half][t] = u;
+                    sRow[4][half][t] = x;
+                    sRow[5][half][t] = y;
+                }
             }
         }
-#pragma unroll
-        for (int m = 1; m < 64; m <<= 1) tot63 += __shfl_xor(tot63, m);
-        if (lane == 0) s63[w] = tot63;
+        sd = wave_sum(sd);
+        if (lane == 0) sWav[w] = sd;
         __syncthreads();
-        if (tid < C) {
-            float db = sRb[tid] + sRb[C + tid];
-            for (int u = 0; u < 4; ++u) db += sCol[u * C + tid];
-            if (tid == C - 1)
-                for (int u = 0; u < 8; ++u) db += s63[u];
-            sb[tid] = db;  // b no longer needed
-            a.dbeta[go0 + (int64_t)tid * a.sg_l] = sRd[tid] + sRd[C + tid];
-        }
-        __syncthreads();
-        if (tid == 0) {  // dg_i = sum_{t >= i} db_t
-            float acc = 0.f;
-            for (int t = C - 1; t >= 0; --t) {
-                acc += sb[t];
-                a.dg[go0 + (int64_t)t * a.sg_l] = acc;
-            }
+        if (tid < 64) {  // per token, then dg_t = sum_{t' >= t} db_t' (one wave)
+            const int t = tid;
+            auto R = [&](int k) { return sRow[k][0][t] + sRow[k][1][t]; };
+            const float gwk = R(0), rt = se[t] * R(1);
+            a.dbeta[go0 + (int64_t)t * a.sg_l] = sg[t] * gwk + R(3) + R(4);
+            // sCol holds the column sums negated (rows minus columns of dA o A + dP o P)
+            float db = R(2) + R(5) + (sCol[0][t] + sCol[1][t] + sCol[2][t] + sCol[3][t]) + sbe[t] * sg[t] * gwk - rt;
+            float tot = 0.f;
+            for (int u = 0; u < 16; ++u) tot += sWav[u];
+            const float rsum = wave_sum(rt);
+            if (t == C - 1) db += rsum + sg[C - 1] * tot;
+            a.dg[go0 + (int64_t)t * a.sg_l] = wave_incl_suffix(db, lane);
         }
     }
 }
@@ -1362,7 +1285,7 @@ hipError_t gdn_phase_d(int phase, const GdnArgs &a, hipStream_t s, hipEvent_t e0
         const int64_t items = (int64_t)bh * (a.L / C);
         if (items > 0)
             hipExtLaunchKernelGGL((k_gdn_dchunk<__bf16, D>), dim3((unsigned)std::min<int64_t>(items, a.n_x)),
-                                  dim3(512), 0, s, e0, e1, 0, a);
+                                  dim3(1024), 0, s, e0, e1, 0, a);
         break;
     }
     default: return hipErrorInvalidValue;
@@ -1397,7 +1320,7 @@ hipError_t launch_gdn_phase(int phase, const GdnArgs &a, int D, hipStream_t s, h
         if (!a.wsDc || (multi && !a.wsDe)) return hipErrorInvalidValue;
         break;
     case GDN_DCHUNK:
-        if (!a.wsSc || !a.wsDc || !a.wsX || a.n_x < 1) return hipErrorInvalidValue;
+        if (!a.wsSc || !a.wsDc || a.n_x < 1) return hipErrorInvalidValue;
         break;
     default: return hipErrorInvalidValue;
     }

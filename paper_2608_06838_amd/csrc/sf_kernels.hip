@@ -190,22 +190,38 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
     const int LS = VG ? D : 1;  // wsLg entries per superchunk
     const float *lg = a.wsLg + bh * n * LS + (VG ? row : 0);
 
+    // The chain over J is sequential; its loads are not.  Superchunks go in
+    // batches of SB, double-buffered: the loads of the next batch are in flight
+    // while the current one is applied (slot indices stay compile-time).
+    constexpr int SB = 8;
     f32x4 S = a.S_in ? *reinterpret_cast<const f32x4 *>(a.S_in + bh * SS + e) : f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int J = 0; J < n; J += 4) {
-        f32x4 dd[4];
-        float f[4];
+    {
+        f32x4 dd[2][SB];
+        float f[2][SB];
+        auto fetch = [&](int slot, int J0) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (J + u < n) {
-                dd[u] = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)(J + u) * SS);
-                f[u] = fexp2(lg[(J + u) * LS]);
-            }
+            for (int u = 0; u < SB; ++u)
+                if (J0 + u < n) {
+                    dd[slot][u] = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)(J0 + u) * SS);
+                    f[slot][u] = fexp2(lg[(J0 + u) * LS]);
+                }
+        };
+        // slot J of wsS: D_J in, S_J out (this thread reads each element before it writes it)
+        auto apply = [&](int slot, int J0) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (J + u < n) {
-                *reinterpret_cast<f32x4 *>(Sb + (int64_t)(J + u) * SS) = S;
-                S = f[u] * S + dd[u];
-            }
+            for (int u = 0; u < SB; ++u)
+                if (J0 + u < n) {
+                    *reinterpret_cast<f32x4 *>(Sb + (int64_t)(J0 + u) * SS) = S;
+                    S = f[slot][u] * S + dd[slot][u];
+                }
+        };
+        fetch(0, 0);
+        for (int J0 = 0; J0 < n; J0 += 2 * SB) {
+            if (J0 + SB < n) fetch(1, J0 + SB);
+            apply(0, J0);
+            if (J0 + 2 * SB < n) fetch(0, J0 + 2 * SB);
+            if (J0 + SB < n) apply(1, J0 + SB);
+        }
     }
     if constexpr (!BWD) {
         if (a.S_out) *reinterpret_cast<f32x4 *>(a.S_out + bh * SS + e) = S;
@@ -215,20 +231,21 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
         f32x4 G = a.dS_out ? *reinterpret_cast<const f32x4 *>(a.dS_out + bh * SS + e)
                            : f32x4{0.f, 0.f, 0.f, 0.f};
         f32x4 Sn = S;  // S_{J+1} for J = n-1 is S_out
-        // four superchunks per step: their loads go out together, ahead of the
-        // dependent chain
-        for (int J0 = n - 1; J0 >= 0; J0 -= 4) {
-            f32x4 E[4], Sj[4];
-            float f[4];
+        f32x4 E[2][SB], Sj[2][SB];
+        float f[2][SB];
+        // batch starting at J0 going down: superchunks J0, J0-1, ..., J0-SB+1
+        auto fetch = [&](int slot, int J0) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < SB; ++u)
                 if (J0 - u >= 0) {
-                    E[u] = *reinterpret_cast<const f32x4 *>(Eb + (int64_t)(J0 - u) * SS);
-                    Sj[u] = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)(J0 - u) * SS);
-                    f[u] = fexp2(lg[(J0 - u) * LS]);
+                    E[slot][u] = *reinterpret_cast<const f32x4 *>(Eb + (int64_t)(J0 - u) * SS);
+                    Sj[slot][u] = *reinterpret_cast<const f32x4 *>(Sb + (int64_t)(J0 - u) * SS);
+                    f[slot][u] = fexp2(lg[(J0 - u) * LS]);
                 }
+        };
+        auto apply = [&](int slot, int J0) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < SB; ++u)
                 if (J0 - u >= 0) {
                     const int J = J0 - u;
                     float p = G[0] * Sn[0] + G[1] * Sn[1] + G[2] * Sn[2] + G[3] * Sn[3];
@@ -241,9 +258,16 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
                         if ((lane & (D / 4 - 1)) == 0) a.wsDot[(bh * n + J) * ndot + row] = p;
                     }
                     *reinterpret_cast<f32x4 *>(Eb + (int64_t)J * SS) = G;
-                    G = f[u] * G + E[u];
-                    Sn = Sj[u];
+                    G = f[slot][u] * G + E[slot][u];
+                    Sn = Sj[slot][u];
                 }
+        };
+        fetch(0, n - 1);
+        for (int J0 = n - 1; J0 >= 0; J0 -= 2 * SB) {
+            if (J0 - SB >= 0) fetch(1, J0 - SB);
+            apply(0, J0);
+            if (J0 - 2 * SB >= 0) fetch(0, J0 - 2 * SB);
+            if (J0 - SB >= 0) apply(1, J0 - SB);
         }
         if (a.dS_in) *reinterpret_cast<f32x4 *>(a.dS_in + bh * SS + e) = G;
     }

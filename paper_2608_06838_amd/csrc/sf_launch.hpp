@@ -82,8 +82,7 @@ struct GdnArgs {
     float *dg, *dbeta, *dS_in;
     float *wsE, *wsDe;  // superchunk dS offsets E_J [B*H][n_super-1], dS_end(J) [B*H][n_super]
     float *wsDc;        // dS' of every chunk [B*H][L/64][D][D]
-    float *wsX;         // per-chunk gradient kernel scratch: n_x slabs of 8 x 64 x D floats
-    int32_t B, H, n_super, ts, n_prep, n_x;
+    int32_t B, H, n_super, ts, n_prep, n_x;  // n_x: workgroups of the per-chunk gradient kernel
     int32_t scan_out;  // forward chains: maps of every superchunk, the scan writes S_out
     int64_t L, sx_b, sx_l, sx_h, sg_b, sg_l, sg_h;
 };

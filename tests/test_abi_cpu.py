@@ -307,11 +307,10 @@ def test_gdn_bwd_validation():
     assert call(shape(), ws=None) == _lib.SF_E_NULL
     assert call(shape(), tun=_tuning(ts=96)) == _lib.SF_E_SHAPE
     # workspace: states and state gradients of every chunk, the maps of every
-    # superchunk, E_J (all but the first) and dS_end(J), and the chunk kernel's slabs
+    # superchunk, E_J (all but the first) and dS_end(J)
     s, n, nc, SS = shape(L=1024), 4, 16, 128 * 128 * 4
     need = L.sf_gdn_bwd_workspace_bytes(ctypes.byref(s), ctypes.byref(_tuning(ts=256)))
-    slabs = min(2 * nc, 1024) * 8 * 64 * 128 * 4
-    assert need == 2 * SS * (4 * n + (n - 1)) + 2 * (2 * nc * SS) + slabs
+    assert need == 2 * SS * (4 * n + (n - 1)) + 2 * (2 * nc * SS)
     assert call(s, tun=_tuning(ts=256), ws_bytes=need - 1) == _lib.SF_E_WORKSPACE
 
 

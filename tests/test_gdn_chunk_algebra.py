@@ -197,3 +197,67 @@ def test_superchunk_affine_maps():
     np.testing.assert_allclose(M.T @ dSend + E, back(dSend, S0), rtol=1e-12, atol=1e-12)
     # the state gradient does not depend on the forward state (the map is affine)
     np.testing.assert_allclose(back(dSend, np.zeros_like(S0)), back(dSend, S0), rtol=1e-12, atol=1e-12)
+
+
+def chunk_bwd_vblocks(q, k, v, g, beta, S, dO, dSn, vb=2):
+    """The per-chunk gradients as the per-chunk kernel forms them: the value
+    channels in blocks of vb columns, each block of S and dS' read once.
+    Two identities remove the W and Ubar products of chunk_bwd:
+      G_W = T^T (-dU S^T) = -G_U S^T,
+      dA  = -(G_W W^T + G_U Ubar^T) = -G_U (Ubar - W S)^T = -G_U U^T.
+    Per block b (columns J of v): U_J = Ubar_J - W S_J, dU_J = e o K dS'_J +
+    P^T dO_J, G_U,J = T^T dU_J (so dv_J = beta o G_U,J); the v-contractions
+    G_W, dO S^T, U dS'^T, dA and dP = dO U^T accumulate over the blocks."""
+    c = chunk_parts(q, k, v, g, beta)
+    b, gam, A, T, W, P, se = (c[x] for x in ("b", "gam", "A", "T", "W", "P", "se"))
+    n, Dk = k.shape
+    Dv = v.shape[1]
+    Ge = np.exp(b[:, None] - b[None, :])
+    KK = np.tril(Ge * (k @ k.T), -1)
+    GW, dqS, dkS = np.zeros((n, Dk)), np.zeros((n, Dk)), np.zeros((n, Dk))
+    dA, dP = np.zeros((n, n)), np.zeros((n, n))
+    dv = np.zeros((n, Dv))
+    rowU = np.zeros(n)  # sum_v G_U v (for dbeta)
+    for j0 in range(0, Dv, vb):
+        J = slice(j0, j0 + vb)
+        UbJ = T @ (beta[:, None] * v[:, J])
+        UJ = UbJ - W @ S[:, J]
+        dUJ = se[:, None] * (k @ dSn[:, J]) + P.T @ dO[:, J]
+        GUJ = T.T @ dUJ
+        dv[:, J] = beta[:, None] * GUJ
+        rowU += np.sum(GUJ * v[:, J], 1)
+        GW -= GUJ @ S[:, J].T
+        dqS += dO[:, J] @ S[:, J].T
+        dkS += UJ @ dSn[:, J].T
+        dA -= GUJ @ UJ.T
+        dP += dO[:, J] @ UJ.T
+    dA = np.tril(dA, -1)
+    dP = np.tril(dP)
+    Ah = dA * beta[:, None] * Ge
+    dq = gam[:, None] * dqS + (dP * Ge) @ k
+    dk = se[:, None] * dkS + (dP * Ge).T @ q + (beta * gam)[:, None] * GW + (Ah + Ah.T) @ k
+    dbeta = gam * np.sum(GW * k, 1) + rowU + np.sum(dA * KK, 1)
+    db = gam * np.sum(q * dqS, 1)
+    E = dP * P
+    db += E.sum(1) - E.sum(0)
+    db += beta * gam * np.sum(GW * k, 1)
+    EA = dA * A
+    db += EA.sum(1) - EA.sum(0)
+    r = se * np.sum(dkS * k, 1)
+    db -= r
+    db[-1] += r.sum() + gam[-1] * np.sum(dSn * S)
+    dg = np.cumsum(db[::-1])[::-1]
+    return dq, dk, dv, dg, dbeta
+
+
+@pytest.mark.parametrize("vb", [1, 2, 6])
+def test_chunk_backward_vblocks(vb):
+    """The blocked form equals the direct per-chunk backward (fp64)."""
+    rng = np.random.default_rng(13 + vb)
+    q, k, v, g, beta, S = rand(rng, C)
+    dO = rng.standard_normal(v.shape)
+    dSn = rng.standard_normal(S.shape)
+    ref = chunk_bwd(q, k, v, g, beta, S, dO, dSn)
+    got = chunk_bwd_vblocks(q, k, v, g, beta, S, dO, dSn, vb=vb)
+    for name, x, y in zip(("dq", "dk", "dv", "dg", "dbeta"), got, ref):
+        np.testing.assert_allclose(x, y, rtol=1e-10, atol=1e-10, err_msg=name)
