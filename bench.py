@@ -288,10 +288,11 @@ def bench_conv(args):
     timer.close()
 
 
-def make_chain_step(sf, torch, inp, seg, ts, overlap):
+def make_chain_step(sf, torch, inp, seg, ts, overlap, keep=True):
     """fwd+bwd chain over segments `seg` with preallocated outputs and
     workspaces (the step allocates nothing).  step(timer) times the launches
-    of the kernels the timer selects."""
+    of the kernels the timer selects.  keep: the forward keeps its superchunk
+    states and the backward reads them (else the backward replays them)."""
     dev = inp["q"].device
     B, L, H, D = inp["q"].shape
     o = torch.empty_like(inp["q"])
@@ -302,12 +303,15 @@ def make_chain_step(sf, torch, inp, seg, ts, overlap):
     dq, dk, dv = (torch.empty_like(inp["q"]) for _ in range(3))
     dg = torch.empty_like(inp["g"])
     dS0 = torch.empty((B, H, D, D), dtype=torch.float32, device=dev)
+    nck = sf.chain_ckpt_bytes(inp["q"], inp["g"], seg, ts=ts, overlap=overlap)
+    ck = torch.empty(max(nck, 1), dtype=torch.uint8, device=dev)
 
-    def step(tm=None, overlap=overlap):
+    def step(tm=None, overlap=overlap, keep=keep):
         sf.chain_fwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, inp["S_in"], ts=ts, overlap=overlap,
-                     out=(o, S_bnd, ws_f), timing=tm)
+                     out=(o, S_bnd, ws_f, ck), timing=tm, keep_states=keep)
         sf.chain_bwd(inp["q"], inp["k"], inp["v"], inp["g"], seg, S_bnd, inp["dO"], inp["dS_out"],
-                     ts=ts, overlap=overlap, out=(dq, dk, dv, dg, dS0, ws_b), timing=tm)
+                     ts=ts, overlap=overlap, out=(dq, dk, dv, dg, dS0, ws_b), timing=tm, ckpt=ck if keep else None)
+    step.ckpt_bytes = nck
     return step
 
 
@@ -602,7 +606,8 @@ def bench_recurrence(args):
     # inputs below ~2 GiB could sit partly in the 256 MB MALL between steps
     in_bytes = sum(inp[k].numel() * inp[k].element_size() for k in ("q", "k", "v", "g", "dO"))
     flush = Flusher(torch, dev, MALL_FLUSH_MIB if in_bytes < (2 << 30) else 0)
-    step = make_chain_step(sf, torch, inp, seg, ts, overlap)
+    keep = not args.recompute
+    step = make_chain_step(sf, torch, inp, seg, ts, overlap, keep=keep)
     timer = sf.KernelTimer(capacity=max(512, 8 * len(seg) * (args.steps + 1)))
 
     # The last warmup step carries HIP events on every kernel launch: per-kernel
@@ -642,6 +647,12 @@ def bench_recurrence(args):
         ov.update(t_e2e_ms=ms, t_overlapped_ms=t_over, t_serial_ms=t_serial, t_scan_serial_ms=t_scan,
                   t_intra_only_ms=t_intra, e2e_over_intra_only=ms / t_intra if t_intra > 0 else None,
                   hidden_frac_of_scan=(t_serial - t_over) / t_scan if t_scan > 0 else None)
+    # The superchunk states: kept by the forward for the backward (default), or
+    # replayed by the backward (the same step with every state recomputed).
+    kept = {"kept": keep, "bytes": step.ckpt_bytes}
+    if not args.no_overlap_study:
+        kept["t_recompute_ms" if keep else "t_kept_ms"] = timed_steps(torch, lambda: step(None, keep=not keep),
+                                                                      args.steps, flush)
     copy_calibration(torch, dev, args.copy_mib)
 
     value = B * L / (ms / 1e3)
@@ -674,6 +685,7 @@ def bench_recurrence(args):
                      "unit": "GB/s", "frac": achieved * 1e9 / PEAK_HBM, "traffic": traffic,
                      "launches": nlaunch, "avg_launch_us": avg_s * 1e6},
         "overlap": ov,
+        "superchunk_states": kept,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, inp)
@@ -693,6 +705,8 @@ def main():
     ap.add_argument("--overlap", action="store_true", help="scans overlapped on the aux stream")
     ap.add_argument("--no-overlap-study", action="store_true",
                     help="skip the serial / overlapped comparison after the timed steps")
+    ap.add_argument("--recompute", action="store_true",
+                    help="the backward replays the superchunk states instead of reading the forward's")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-times", action="store_true", help="print per-kernel times to stderr")
     ap.add_argument("--copy-mib", type=int, default=0,

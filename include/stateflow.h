@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define SF_ABI_VERSION 2
+#define SF_ABI_VERSION 3
 
 typedef enum {
     SF_OK = 0,
@@ -210,6 +210,18 @@ size_t sf_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const int6
                                 const sf_tuning *tuning);
 
 /*
+ * Bytes of the kept superchunk states of a chain (optional `ckpt` buffer of
+ * sf_chain_fwd / sf_chain_bwd): per segment of more than one superchunk, the
+ * state entering each superchunk (the ST output of Sec. 2.2, fp32 Dk x Dv per
+ * (b, h, superchunk)), each superchunk's log-decay and the state leaving the
+ * segment.  The superchunk lengths are those the same shape, segments and
+ * tuning select.  0 when no segment has more than one superchunk, and on
+ * invalid arguments (then sf_last_error() is set).
+ */
+size_t sf_chain_ckpt_bytes(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
+                           const sf_tuning *tuning);
+
+/*
  * Segment driver, forward (Sec. 3.1 chaining: S_0^in = S_init,
  * S_{i+1}^in = S_i^out).  shape->L is the whole sequence; seg_len[0..n_seg-1]
  * (host array, each > 0 and a multiple of 64) sums to it.  The token tensors
@@ -217,6 +229,12 @@ size_t sf_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const int6
  *   S_bnd  [n_seg+1][B][H][Dk][Dv] f32: slot 0 is the input S_init (read);
  *          slots 1..n_seg receive S_out of each segment (slot n_seg = the
  *          final state).
+ *   ckpt   NULL, or a device buffer of at least sf_chain_ckpt_bytes() bytes
+ *          (16-byte aligned, caller-owned) that receives the superchunk
+ *          states the forward computes anyway, so that sf_chain_bwd can read
+ *          them instead of replaying the preparation and the forward scan.
+ *          Its contents are only meaningful to sf_chain_bwd with the same
+ *          shape, segments and tuning.
  * With aux != NULL and overlap enabled, each segment's state scan runs on aux
  * concurrently with the next segment's preparation and the previous
  * segment's output kernels (Sec. 3.4, fwd split-and-overlap schedule); both
@@ -225,8 +243,8 @@ size_t sf_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const int6
  */
 sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
                        const void *q, const void *k, const void *v, const float *g, void *o,
-                       float *S_bnd, void *ws, size_t ws_bytes, const sf_tuning *tuning,
-                       sf_stream main, sf_stream aux);
+                       float *S_bnd, void *ckpt, size_t ckpt_bytes, void *ws, size_t ws_bytes,
+                       const sf_tuning *tuning, sf_stream main, sf_stream aux);
 
 /*
  * Segment driver, backward (Sec. 3.1 reverse chaining dS_i^out = dS_{i+1}^in),
@@ -234,12 +252,17 @@ sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
  * (slot i = S_in of segment i; slot n_seg is not read).  dS_final is the
  * gradient of the final state (NULL = zero); dS_init receives the gradient
  * of S_init.  Overlap as in sf_chain_fwd (Sec. 3.4, bwd schedule).
+ * ckpt: NULL (every superchunk state is recomputed: the preparation replays
+ * D_J and the scan runs forward again), or the buffer that sf_chain_fwd
+ * filled for the same shape, segments and tuning (read only; at least
+ * sf_chain_ckpt_bytes() bytes).  The results are the same either way.
  */
 sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
                        const void *q, const void *k, const void *v, const float *g,
-                       const float *S_bnd, const void *dO, const float *dS_final, void *dq,
-                       void *dk, void *dv, float *dg, float *dS_init, void *ws, size_t ws_bytes,
-                       const sf_tuning *tuning, sf_stream main, sf_stream aux);
+                       const float *S_bnd, const void *ckpt, size_t ckpt_bytes, const void *dO,
+                       const float *dS_final, void *dq, void *dk, void *dv, float *dg,
+                       float *dS_init, void *ws, size_t ws_bytes, const sf_tuning *tuning,
+                       sf_stream main, sf_stream aux);
 
 /*
  * Short convolution with a boundary tail: the auxiliary boundary state that

@@ -30,7 +30,7 @@ from ._lib import KERNELS, StateflowError  # noqa: F401
 from . import tuned
 from .timing import KernelTimer  # noqa: F401
 
-__all__ = ["segment_fwd", "segment_fwd_noalloc", "segment_bwd", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
+__all__ = ["segment_fwd", "segment_fwd_noalloc", "segment_bwd", "chain_ckpt_bytes", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
            "bwd_workspace_bytes", "chain_workspace_bytes", "conv_fwd", "conv_bwd", "conv_bwd_workspace_bytes",
            "gdn_fwd", "gdn_fwd_workspace_bytes", "gdn_bwd", "gdn_chain_fwd", "gdn_chain_bwd", "partition_hybrid", "KernelTimer", "StateflowError", "abi_version"]
 
@@ -210,13 +210,30 @@ def _pick(q, g, seg_lens, ts, overlap):
     return (t["ts"] if ts is None else int(ts)), (t["overlap"] if overlap is None else bool(overlap))
 
 
+def chain_ckpt_bytes(q, g, seg_lens, ts=None, overlap=None):
+    """Bytes of the superchunk states chain_fwd(keep_states=True) keeps."""
+    sh = _shape(q, g)
+    n = len(seg_lens)
+    ts, overlap = _pick(q, g, seg_lens, ts, overlap)
+    tun = _tuning(ts, overlap)
+    sl = (ctypes.c_int64 * n)(*[int(x) for x in seg_lens])
+    L_ = _lib.lib()
+    nb = L_.sf_chain_ckpt_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun))
+    if nb == 0 and L_.sf_last_error():
+        raise StateflowError("sf_chain_ckpt_bytes: " + L_.sf_last_error().decode())
+    return nb
+
+
 def chain_fwd(q, k, v, g, seg_lens, S_init=None, *, ts=None, overlap=None, stream=None, aux_stream=None,
-              out=None, timing=None):
+              out=None, timing=None, keep_states=False):
     """Forward over consecutive segments with S_in(i+1) = S_out(i).
 
     Returns (o, S_bnd) with S_bnd[i] the state entering segment i
     (S_bnd[0] = S_init or zero, S_bnd[-1] the final state).  `out` may supply
-    preallocated (o, S_bnd, workspace) buffers.
+    preallocated (o, S_bnd, workspace) buffers.  keep_states=True also returns
+    the superchunk states (a uint8 device tensor of chain_ckpt_bytes bytes, or
+    a caller's buffer given as out[3]) for chain_bwd(ckpt=...), which then
+    skips replaying them; the results are the same.
     """
     _same_layout(q, k, v)
     sh = _shape(q, g)
@@ -229,30 +246,37 @@ def chain_fwd(q, k, v, g, seg_lens, S_init=None, *, ts=None, overlap=None, strea
     L_ = _lib.lib()
     tun = _tuning(ts, overlap, timing)
     sl = (ctypes.c_int64 * n)(*[int(x) for x in seg_lens])
+    ck = None
     with torch.cuda.stream(stream):
         if out is None:
             o = _like(q)
             S_bnd = torch.empty((n + 1, B, H, D, D), dtype=torch.float32, device=q.device)
             ws = _ws(L_.sf_chain_workspace_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun)), q.device)
         else:
-            o, S_bnd, ws = out
+            o, S_bnd, ws = out[:3]
+            ck = out[3] if len(out) > 3 else None
+        if keep_states and ck is None:
+            ck = _ws(L_.sf_chain_ckpt_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun)), q.device)
         if S_init is None:
             S_bnd[0].zero_()
         else:
             S_bnd[0].copy_(S_init)
+    if not keep_states:
+        ck = None
     rc = L_.sf_chain_fwd(ctypes.byref(sh), n, sl, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(o), _ptr(S_bnd),
-                         _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream),
-                         _stream_handle(aux) if aux is not None else None)
+                         _ptr(ck), ck.numel() if ck is not None else 0, _ptr(ws), ws.numel(),
+                         ctypes.byref(tun), _stream_handle(stream), _stream_handle(aux) if aux is not None else None)
     _lib.check("sf_chain_fwd", rc)
-    return o, S_bnd
+    return (o, S_bnd, ck) if keep_states else (o, S_bnd)
 
 
 def chain_bwd(q, k, v, g, seg_lens, S_bnd, dO, dS_final=None, *, ts=None, overlap=None, stream=None,
-              aux_stream=None, out=None, timing=None):
+              aux_stream=None, out=None, timing=None, ckpt=None):
     """Backward over the segments in reverse with dS_out(i) = dS_in(i+1).
 
     Returns (dq, dk, dv, dg, dS_init).  `out` may supply preallocated
-    (dq, dk, dv, dg, dS_init, workspace) buffers.
+    (dq, dk, dv, dg, dS_init, workspace) buffers.  ckpt: the superchunk states
+    of chain_fwd(keep_states=True) for the same inputs, segments and settings.
     """
     _same_layout(q, k, v, dO)
     sh = _shape(q, g)
@@ -276,7 +300,10 @@ def chain_bwd(q, k, v, g, seg_lens, S_bnd, dO, dS_final=None, *, ts=None, overla
             ws = _ws(L_.sf_chain_workspace_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun)), q.device)
         else:
             dq, dk, dv, dg, dS_init, ws = out
-    rc = L_.sf_chain_bwd(ctypes.byref(sh), n, sl, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(S_bnd), _ptr(dO),
+    if ckpt is not None and (ckpt.device != q.device or not ckpt.is_contiguous()):
+        raise ValueError("ckpt must be a contiguous buffer on the inputs' device")
+    rc = L_.sf_chain_bwd(ctypes.byref(sh), n, sl, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(S_bnd), _ptr(ckpt),
+                         ckpt.numel() * ckpt.element_size() if ckpt is not None else 0, _ptr(dO),
                          _ptr(dS_final), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg), _ptr(dS_init), _ptr(ws),
                          ws.numel(), ctypes.byref(tun), _stream_handle(stream),
                          _stream_handle(aux) if aux is not None else None)

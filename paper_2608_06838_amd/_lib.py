@@ -24,7 +24,7 @@ NOALLOC_SCRATCH_BYTES = 64 << 20  # SF_NOALLOC_SCRATCH_BYTES
 # every symbol include/stateflow.h declares
 EXPORTS = ["sf_abi_version", "sf_status_str", "sf_last_error", "sf_fwd_workspace_bytes",
            "sf_bwd_workspace_bytes", "sf_segment_fwd", "sf_segment_fwd_noalloc", "sf_segment_bwd", "sf_chain_workspace_bytes",
-           "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd",
+           "sf_chain_ckpt_bytes", "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd",
            "sf_gdn_fwd_workspace_bytes", "sf_gdn_fwd", "sf_gdn_bwd_workspace_bytes", "sf_gdn_bwd",
            "sf_gdn_chain_workspace_bytes", "sf_gdn_chain_fwd", "sf_gdn_chain_bwd",
            "sf_partition_hybrid"]
@@ -99,9 +99,13 @@ def lib():
     L.sf_chain_workspace_bytes.restype = sz
     L.sf_chain_workspace_bytes.argtypes = [sp, i32, i64p, tp]
     L.sf_chain_fwd.restype = ctypes.c_int
-    L.sf_chain_fwd.argtypes = [sp, i32, i64p] + [vp] * 7 + [sz, tp, vp, vp]
+    L.sf_chain_ckpt_bytes.restype = sz
+    L.sf_chain_ckpt_bytes.argtypes = [sp, i32, i64p, tp]
+    # (..., o, S_bnd, ckpt, ckpt_bytes, ws, ws_bytes, tuning, main, aux)
+    L.sf_chain_fwd.argtypes = [sp, i32, i64p] + [vp] * 7 + [sz, vp, sz, tp, vp, vp]
     L.sf_chain_bwd.restype = ctypes.c_int
-    L.sf_chain_bwd.argtypes = [sp, i32, i64p] + [vp] * 13 + [sz, tp, vp, vp]
+    # (..., g, S_bnd, ckpt, ckpt_bytes, dO, dS_final, dq, dk, dv, dg, dS_init, ws, ws_bytes, ...)
+    L.sf_chain_bwd.argtypes = [sp, i32, i64p] + [vp] * 6 + [sz] + [vp] * 8 + [sz, tp, vp, vp]
     cp = ctypes.POINTER(SfConvShape)
     L.sf_conv_bwd_workspace_bytes.restype = sz
     L.sf_conv_bwd_workspace_bytes.argtypes = [cp]

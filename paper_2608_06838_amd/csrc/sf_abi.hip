@@ -538,6 +538,40 @@ sf_status check_segments(const Shape &r, int32_t n_seg, const int64_t *seg_len) 
     return SF_OK;
 }
 
+// Kept superchunk states of one segment with more than one superchunk: the
+// kernels' wsS (S_J after the forward scan), wsLg and wsSn regions.
+struct CkptLayout {
+    size_t S = 0, Lg = 0, Sn = 0, total = 0;
+};
+CkptLayout ckpt_layout(const Shape &r, int64_t L, int ts) {
+    CkptLayout c;
+    const int n = n_super_of(L, ts);
+    if (n <= 1) return c;
+    const size_t bh = (size_t)r.B * r.H, SS = (size_t)r.D * r.D;
+    c.Lg = al(bh * n * SS * 4);
+    c.Sn = c.Lg + al(bh * n * (r.gate == SF_GATE_VECTOR ? r.D : 1) * 4);
+    c.total = c.Sn + al(bh * SS * 4);
+    return c;
+}
+sf_status chain_ckpt(const Shape &r, int32_t n_seg, const int64_t *seg_len, const sf_tuning *t, size_t &bytes) {
+    bytes = 0;
+    for (int i = 0; i < n_seg; ++i) {
+        int ts;
+        TRY(pick_ts(r, seg_len[i], t, ts));
+        bytes += ckpt_layout(r, seg_len[i], ts).total;
+    }
+    return SF_OK;
+}
+// point a segment's superchunk-state regions into the kept-state buffer
+void use_ckpt(const Shape &r, Seg &s, char *base, bool bwd) {
+    const CkptLayout c = ckpt_layout(r, s.a.L, s.a.ts);
+    if (c.total == 0) return;
+    s.a.wsS = (float *)(base + c.S);
+    s.a.wsLg = (float *)(base + c.Lg);
+    s.a.wsSn = (float *)(base + c.Sn);
+    s.a.ckpt = bwd ? 1 : 0;
+}
+
 size_t chain_ws(const Shape &r, int32_t n_seg, const int64_t *seg_len, const sf_tuning *t) {
     size_t slot = 0;
     for (int i = 0; i < n_seg; ++i) {
@@ -835,9 +869,21 @@ size_t sf_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const int6
     return chain_ws(r, n_seg, seg_len, tuning);
 }
 
+size_t sf_chain_ckpt_bytes(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
+                           const sf_tuning *tuning) {
+    g_err.clear();
+    Shape r;
+    size_t bytes = 0;
+    if (resolve(shape, r) != SF_OK || check_segments(r, n_seg, seg_len) != SF_OK ||
+        chain_ckpt(r, n_seg, seg_len, tuning, bytes) != SF_OK)
+        return 0;
+    return bytes;
+}
+
 sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
-                       const void *k, const void *v, const float *g, void *o, float *S_bnd, void *ws,
-                       size_t ws_bytes, const sf_tuning *tuning, sf_stream main_s, sf_stream aux_s) {
+                       const void *k, const void *v, const float *g, void *o, float *S_bnd, void *ckpt,
+                       size_t ckpt_bytes, void *ws, size_t ws_bytes, const sf_tuning *tuning, sf_stream main_s,
+                       sf_stream aux_s) {
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
@@ -845,13 +891,17 @@ sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
     TRY(check_segments(r, n_seg, seg_len));
     if (!q || !k || !v || !g || !o || !S_bnd || !ws)
         return fail(SF_E_NULL, "q, k, v, g, o, S_bnd and ws are required");
-    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_bnd, "S_bnd"}, {ws, "ws"}}));
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_bnd, "S_bnd"}, {ckpt, "ckpt"}, {ws, "ws"}}));
     const size_t need = chain_ws(r, n_seg, seg_len, tuning);
     if (need == 0) return fail(SF_E_SHAPE, "cannot size the chain workspace");
     if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
+    size_t kneed = 0;
+    TRY(chain_ckpt(r, n_seg, seg_len, tuning, kneed));
+    if (ckpt && ckpt_bytes < kneed) return fail(SF_E_WORKSPACE, "ckpt %zu < required %zu", ckpt_bytes, kneed);
     TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
                      grange(r, g, r.L, "g")},
-                    {xrange(r, o, r.L, "o"), srange(r, S_bnd, n_seg + 1, "S_bnd"), wsrange(ws, need)}));
+                    {xrange(r, o, r.L, "o"), srange(r, S_bnd, n_seg + 1, "S_bnd"),
+                     span(ckpt, (int64_t)kneed, "ckpt"), wsrange(ws, need)}));
     const size_t slot = (need - 2 * al((size_t)r.B * r.H * r.D * r.D * 4)) / 2;
     const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
     hipStream_t mn = (hipStream_t)main_s;
@@ -862,11 +912,16 @@ sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
 
     std::vector<Seg> segs(n_seg);
     int64_t tok = 0;
+    size_t kofs = 0;
     for (int i = 0; i < n_seg; ++i) {
         int ts;
         TRY(pick_ts(r, seg_len[i], tuning, ts));
         Seg &s = segs[i];
         s = make_seg(r, seg_len[i], ts, (char *)ws + (i % 2) * slot, false, timing_of(tuning));
+        if (ckpt) {
+            use_ckpt(r, s, (char *)ckpt + kofs, false);
+            kofs += ckpt_layout(r, seg_len[i], ts).total;
+        }
         s.a.q = offset_x(r, q, tok);
         s.a.k = offset_x(r, k, tok);
         s.a.v = offset_x(r, v, tok);
@@ -909,10 +964,10 @@ sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
 }
 
 sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
-                       const void *k, const void *v, const float *g, const float *S_bnd, const void *dO,
-                       const float *dS_final, void *dq, void *dk, void *dv, float *dg, float *dS_init,
-                       void *ws, size_t ws_bytes, const sf_tuning *tuning, sf_stream main_s,
-                       sf_stream aux_s) {
+                       const void *k, const void *v, const float *g, const float *S_bnd, const void *ckpt,
+                       size_t ckpt_bytes, const void *dO, const float *dS_final, void *dq, void *dk, void *dv,
+                       float *dg, float *dS_init, void *ws, size_t ws_bytes, const sf_tuning *tuning,
+                       sf_stream main_s, sf_stream aux_s) {
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
@@ -921,13 +976,17 @@ sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
     if (!q || !k || !v || !g || !S_bnd || !dO || !dq || !dk || !dv || !dg || !dS_init || !ws)
         return fail(SF_E_NULL, "q, k, v, g, S_bnd, dO, dq, dk, dv, dg, dS_init and ws are required");
     TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {dO, "dO"}, {dq, "dq"}, {dk, "dk"}, {dv, "dv"},
-                     {S_bnd, "S_bnd"}, {dS_final, "dS_final"}, {dS_init, "dS_init"}, {ws, "ws"}}));
+                     {S_bnd, "S_bnd"}, {ckpt, "ckpt"}, {dS_final, "dS_final"}, {dS_init, "dS_init"},
+                     {ws, "ws"}}));
     const size_t need = chain_ws(r, n_seg, seg_len, tuning);
     if (need == 0) return fail(SF_E_SHAPE, "cannot size the chain workspace");
     if (ws_bytes < need) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, need);
+    size_t kneed = 0;
+    TRY(chain_ckpt(r, n_seg, seg_len, tuning, kneed));
+    if (ckpt && ckpt_bytes < kneed) return fail(SF_E_WORKSPACE, "ckpt %zu < required %zu", ckpt_bytes, kneed);
     TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"),
-                     grange(r, g, r.L, "g"), srange(r, S_bnd, n_seg, "S_bnd"), xrange(r, dO, r.L, "dO"),
-                     srange(r, dS_final, 1, "dS_final")},
+                     grange(r, g, r.L, "g"), srange(r, S_bnd, n_seg, "S_bnd"), span(ckpt, (int64_t)kneed, "ckpt"),
+                     xrange(r, dO, r.L, "dO"), srange(r, dS_final, 1, "dS_final")},
                     {xrange(r, dq, r.L, "dq"), xrange(r, dk, r.L, "dk"), xrange(r, dv, r.L, "dv"),
                      grange(r, dg, r.L, "dg"), srange(r, dS_init, 1, "dS_init"), wsrange(ws, need)}));
     const size_t gb = al((size_t)r.B * r.H * r.D * r.D * 4);
@@ -942,11 +1001,16 @@ sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
 
     std::vector<Seg> segs(n_seg);
     int64_t tok = 0;
+    size_t kofs = 0;
     for (int i = 0; i < n_seg; ++i) {
         int ts;
         TRY(pick_ts(r, seg_len[i], tuning, ts));
         Seg &s = segs[i];
         s = make_seg(r, seg_len[i], ts, (char *)ws + (i % 2) * slot, true, timing_of(tuning));
+        if (ckpt) {
+            use_ckpt(r, s, (char *)ckpt + kofs, true);
+            kofs += ckpt_layout(r, seg_len[i], ts).total;
+        }
         s.a.q = offset_x(r, q, tok);
         s.a.k = offset_x(r, k, tok);
         s.a.v = offset_x(r, v, tok);

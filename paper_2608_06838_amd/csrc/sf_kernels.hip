@@ -48,8 +48,13 @@ constexpr int SCAN_NT = 256;
 // transposing loads as the exact shared operand; the per-token decay goes on
 // the wave's own value (dO) columns, split hi/lo:
 //   D[k][col] = gam D[k][col] + sum_s K[s][k] (exp2(b63 - b_s) V[s][col])
-template <typename T, int D, int NCT, bool BWD>
+// EONLY (backward from kept superchunk states): E_J alone, with the forward
+// form's layout: q in the key role, dO in the value role and the weights
+// exp2(off + b_t) in place of the decay, no per-chunk decay of the sum.  Per
+// element its products are the BWD form's E products in the same order.
+template <typename T, int D, int NCT, bool BWD, bool EONLY = false>
 __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_prep(SegArgs a) {
+    static_assert(!(BWD && EONLY), "EONLY is a form of the forward layout");
     constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
     constexpr int LDN = D + pad<T>(), SWX = swx<T, D>();
     constexpr bool SPD = kSplitDecay<T>;
@@ -64,8 +69,8 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     const Decode d = decode(a);
     const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
-    const T *K = (const T *)a.k + xo;
-    const T *V = (const T *)a.v + xo;
+    const T *K = (const T *)(EONLY ? a.q : a.k) + xo;
+    const T *V = (const T *)(EONLY ? a.dO : a.v) + xo;
     const T *Q = (const T *)a.q + xo;
     const T *dO = (const T *)a.dO + xo;
     const float *gp = a.g + d.b * a.sg_b + d.h * a.sg_h + d.tok0 * a.sg_l;
@@ -101,7 +106,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         const float b63 = lane_value(b2, 63);
         __syncthreads();
         if (w == 0) {
-            se[lane] = fexp2(b63 - b2);
+            se[lane] = EONLY ? fexp2(off + b2) : fexp2(b63 - b2);
             if constexpr (BWD) sqs[lane] = fexp2(off + b2);
         }
         tk.store_swz(sK, LDN, tid, SWX);
@@ -112,11 +117,13 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         }
         if (c + 1 < d.nch) issue(c + 1);
         __syncthreads();
-        const float gam = fexp2(b63);
+        if constexpr (!EONLY) {
+            const float gam = fexp2(b63);
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct)
+            for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-            for (int i = 0; i < NK; ++i) Ds[ct][i] *= gam;
+                for (int i = 0; i < NK; ++i) Ds[ct][i] *= gam;
+        }
 #pragma unroll
         for (int ks = 0; ks < C / 32; ++ks) {
             const int s0 = 32 * ks + 8 * q4;
@@ -152,6 +159,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         off += b63;
     }
     const int64_t so = ((int64_t)d.bh * a.n_super + d.J) * D * D;
+    float *dstD = EONLY ? a.wsE : a.wsS;
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct) {
         const int c0 = 16 * (NCT * w + ct);
@@ -160,11 +168,11 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int64_t e = so + (int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16;
-                a.wsS[e] = Ds[ct][i][r];
+                dstD[e] = Ds[ct][i][r];
                 if constexpr (BWD) a.wsE[e] = Es[ct][i][r];
             }
     }
-    if (tid == 0) a.wsLg[(int64_t)d.bh * a.n_super + d.J] = off;
+    if (!EONLY && tid == 0) a.wsLg[(int64_t)d.bh * a.n_super + d.J] = off;
 }
 
 // ---------------------------------------------------------------------------
@@ -176,6 +184,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 // [(bh, J)][part*4 + wave], vector gate (VG) per key row at [(bh, J)][row].
 // VG: the superchunk decay is per key row (wsLg[(bh, J)][row]); a thread's 4
 // elements lie in one row.
+// Kept states: the forward also writes the final state to wsSn; a backward
+// with a.ckpt set finds S_J already in wsS and the final state in wsSn, and
+// runs the backward half only.
 template <bool BWD, bool VG>
 __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -195,7 +206,9 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
     // while the current one is applied (slot indices stay compile-time).
     constexpr int SB = 8;
     f32x4 S = a.S_in ? *reinterpret_cast<const f32x4 *>(a.S_in + bh * SS + e) : f32x4{0.f, 0.f, 0.f, 0.f};
-    {
+    if (BWD && a.ckpt) {
+        S = *reinterpret_cast<const f32x4 *>(a.wsSn + bh * SS + e);
+    } else {
         f32x4 dd[2][SB];
         float f[2][SB];
         auto fetch = [&](int slot, int J0) {
@@ -225,6 +238,7 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
     }
     if constexpr (!BWD) {
         if (a.S_out) *reinterpret_cast<f32x4 *>(a.S_out + bh * SS + e) = S;
+        if (a.wsSn) *reinterpret_cast<f32x4 *>(a.wsSn + bh * SS + e) = S;
     } else {
         const int ndot = VG ? D : D * D / 256;
         float *Eb = a.wsE + bh * n * SS + e;
@@ -906,7 +920,10 @@ static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s, hipEvent_
     switch (kind) {
     case SF_K_FWD_PREP: hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, false>), grid, dim3(NTP), 0, s, e0, e1, 0, a); break;
     case SF_K_FWD_OUT: hipExtLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, false>), grid, dim3(NTW), 0, s, e0, e1, 0, a); break;
-    case SF_K_BWD_PREP: hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREPB, true>), grid, dim3(NTB), 0, s, e0, e1, 0, a); break;
+    case SF_K_BWD_PREP:
+        if (a.ckpt) hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, false, true>), grid, dim3(NTP), 0, s, e0, e1, 0, a);
+        else hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREPB, true>), grid, dim3(NTB), 0, s, e0, e1, 0, a);
+        break;
     case SF_K_BWD_DQ: hipExtLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, true>), grid, dim3(NTW), 0, s, e0, e1, 0, a); break;
     case SF_K_BWD_DKV:
         hipExtLaunchKernelGGL((k_bwd_dkv<T, D>), grid, dim3(128 * D / 16), 0, s, e0, e1, 0, a);

@@ -1238,9 +1238,13 @@ static hipError_t launch_vg_td(int kind, const SegArgs &a, hipStream_t s, hipEve
     switch (kind) {
     case SF_K_FWD_PREP: hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, false>), grid, dim3(NT), 0, s, e0, e1, 0, a); break;
     case SF_K_FWD_OUT: hipExtLaunchKernelGGL((k_walk_vg<T, D, NC1>), grid, dim3(NT1), 0, s, e0, e1, 0, a); break;
-    case SF_K_BWD_PREP:
-        hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, false>), grid, dim3(NT), 0, s, e0, nullptr, 0, a);
-        hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, true>), grid, dim3(NT), 0, s, nullptr, e1, 0, a);
+    case SF_K_BWD_PREP:  // the replay of D_J is skipped when the forward kept the states
+        if (a.ckpt) {
+            hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, true>), grid, dim3(NT), 0, s, e0, e1, 0, a);
+        } else {
+            hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, false>), grid, dim3(NT), 0, s, e0, nullptr, 0, a);
+            hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, true>), grid, dim3(NT), 0, s, nullptr, e1, 0, a);
+        }
         break;
     case SF_K_BWD_DQ: hipExtLaunchKernelGGL((k_dq_vg<T, D, NCT>), grid, dim3(NT), 0, s, e0, e1, 0, a); break;
     case SF_K_BWD_DKV:

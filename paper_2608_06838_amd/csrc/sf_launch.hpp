@@ -32,6 +32,10 @@ struct SegArgs {
     float *wsLg;   // [B][H][n_super] (vector gate: [..][D]): log2 of the superchunk decay
     float *wsDot;  // [B][H][n_super][D*D/256]: partials of <G_{J+1}, S_{J+1}>;
                    // vector gate: [B][H][n_super][D], the per-key-row sums
+    float *wsSn;   // [B][H][D][D] or NULL: the state leaving the segment, kept
+                   // beside the superchunk states when the forward keeps them
+    int32_t ckpt;  // backward: 1 when wsS, wsLg and wsSn already hold the
+                   // forward's superchunk states, decays and final state
 };
 
 // kind is an sf_kernel_id; io an sf_dtype.  The scan runs its backward form

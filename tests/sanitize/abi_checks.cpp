@@ -56,15 +56,26 @@ int main() {
                           P(13), 1 << 30, &t, nullptr) == SF_E_NULL);
     // chains
     const int64_t segs[2] = {512, 448};
-    EXPECT(sf_chain_fwd(&s, 2, segs, P(1), P(2), P(3), F(4), P(5), F(6), P(7), 1 << 30, nullptr, nullptr, nullptr) ==
+    EXPECT(sf_chain_fwd(&s, 2, segs, P(1), P(2), P(3), F(4), P(5), F(6), nullptr, 0, P(7), 1 << 30, nullptr, nullptr, nullptr) ==
            SF_E_SHAPE);
     const int64_t segs2[2] = {512, 512};
-    EXPECT(sf_chain_fwd(&s, 2, segs2, P(1), P(2), P(3), F(4), P(5), F(6), P(5), 1 << 30, nullptr, nullptr, nullptr) ==
+    EXPECT(sf_chain_fwd(&s, 2, segs2, P(1), P(2), P(3), F(4), P(5), F(6), nullptr, 0, P(5), 1 << 30, nullptr, nullptr, nullptr) ==
            SF_E_ALIAS);
-    EXPECT(sf_chain_bwd(&s, 2, segs2, P(1), P(2), P(3), F(4), F(5), P(6), nullptr, P(8), P(9), P(10), F(11), nullptr,
+    EXPECT(sf_chain_bwd(&s, 2, segs2, P(1), P(2), P(3), F(4), F(5), nullptr, 0, P(6), nullptr, P(8), P(9), P(10), F(11), nullptr,
                         P(13), 1 << 30, nullptr, nullptr, nullptr) == SF_E_NULL);
     EXPECT(sf_chain_workspace_bytes(&s, 2, segs2, nullptr) > 0);
     EXPECT(sf_chain_workspace_bytes(&s, 2, segs, nullptr) == 0);
+    // kept superchunk states
+    sf_tuning t128;
+    std::memset(&t128, 0, sizeof t128);
+    t128.ts = 128;
+    const size_t kneed = sf_chain_ckpt_bytes(&s, 2, segs2, &t128);
+    EXPECT(kneed > 0);
+    EXPECT(sf_chain_ckpt_bytes(&s, 2, segs, &t128) == 0 && std::strlen(sf_last_error()) > 0);
+    EXPECT(sf_chain_fwd(&s, 2, segs2, P(1), P(2), P(3), F(4), P(5), F(6), P(8), kneed - 1, P(7), 1 << 30, &t128,
+                        nullptr, nullptr) == SF_E_WORKSPACE);
+    EXPECT(sf_chain_bwd(&s, 2, segs2, P(1), P(2), P(3), F(4), F(5), P(8), kneed, P(6), nullptr, P(8), P(9), P(10),
+                        F(11), F(12), P(13), 1 << 30, &t128, nullptr, nullptr) == SF_E_ALIAS);
     // timing record
     sf_timing tm;
     std::memset(&tm, 0, sizeof tm);

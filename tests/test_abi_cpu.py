@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
     assert set(declared) == set(_lib.EXPORTS), (declared, _lib.EXPORTS)
     for name in declared:
         assert hasattr(L, name), name
-    assert L.sf_abi_version() == 2
+    assert L.sf_abi_version() == 3
     assert L.sf_status_str(_lib.SF_E_ALIAS) == b"SF_E_ALIAS"
 
 
@@ -139,32 +139,80 @@ def test_workspace_alias():
     assert bwd(ws=6) == _lib.SF_E_ALIAS      # over dO
     assert bwd(ws=12) == _lib.SF_E_ALIAS     # over dS_in
     segs = (ctypes.c_int64 * 2)(512, 512)
-    rc = L.sf_chain_fwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), p(5), 1 << 30, None,
+    rc = L.sf_chain_fwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, 0, p(5), 1 << 30, None,
                         None, None)
     assert rc == _lib.SF_E_ALIAS             # workspace over o
-    rc = L.sf_chain_fwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), p(6), 1 << 30, None,
+    rc = L.sf_chain_fwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, 0, p(6), 1 << 30, None,
                         None, None)
     assert rc == _lib.SF_E_ALIAS             # workspace over S_bnd
-    rc = L.sf_chain_bwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, p(8), p(9),
+    rc = L.sf_chain_bwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), None, 0, p(6), None, p(8), p(9),
                         p(10), p(11), p(12), p(8), 1 << 30, None, None, None)
     assert rc == _lib.SF_E_ALIAS             # workspace over dq
-    rc = L.sf_chain_bwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, p(8), p(9),
+    rc = L.sf_chain_bwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), None, 0, p(6), None, p(8), p(9),
                         p(10), p(11), p(12), p(5), 1 << 30, None, None, None)
     assert rc == _lib.SF_E_ALIAS             # workspace over S_bnd (an input of the backward)
+
+
+def test_chain_ckpt():
+    """Kept superchunk states: sizing, and the buffer is an output of the
+    forward and an input of the backward (alias and size checks)."""
+    L = _lib.lib()
+    t = _tuning(ts=128)
+    s = shape(L=1024)
+    segs = (ctypes.c_int64 * 3)(512, 384, 128)  # 4, 3 and 1 superchunks
+    SS, bh = 128 * 128 * 4, 2
+
+    def al(x):
+        return (x + 255) // 256 * 256
+
+    def seg(n):
+        return al(bh * n * SS) + al(bh * n * 4) + al(bh * SS) if n > 1 else 0
+
+    need = L.sf_chain_ckpt_bytes(ctypes.byref(s), 3, segs, ctypes.byref(t))
+    assert need == seg(4) + seg(3) + seg(1)
+    one = (ctypes.c_int64 * 1)(1024)
+    t1 = _tuning(ts=1024)
+    assert L.sf_chain_ckpt_bytes(ctypes.byref(s), 1, one, ctypes.byref(t1)) == 0
+    vs = shape(L=1024, gate=_lib.SF_GATE_VECTOR)
+    assert L.sf_chain_ckpt_bytes(ctypes.byref(vs), 3, segs, ctypes.byref(t)) == \
+        sum(al(bh * n * SS) + al(bh * n * 128 * 4) + al(bh * SS) for n in (4, 3))
+    bad = (ctypes.c_int64 * 3)(512, 384, 64)
+    assert L.sf_chain_ckpt_bytes(ctypes.byref(s), 3, bad, ctypes.byref(t)) == 0
+    assert L.sf_last_error()
+    tp = ctypes.byref(t)
+
+    def fwd(ck, nb=1 << 30, ws=7):
+        return L.sf_chain_fwd(ctypes.byref(s), 3, segs, p(1), p(2), p(3), p(4), p(5), p(6), ck, nb, p(ws), 1 << 30,
+                              tp, None, None)
+
+    assert fwd(p(5)) == _lib.SF_E_ALIAS             # over o
+    assert fwd(p(6)) == _lib.SF_E_ALIAS             # over S_bnd
+    assert fwd(p(7)) == _lib.SF_E_ALIAS             # over the workspace
+    assert fwd(p(1)) == _lib.SF_E_ALIAS             # over q
+    assert fwd(p(8), nb=need - 1) == _lib.SF_E_WORKSPACE
+    assert fwd(ctypes.c_void_p(p(8).value + 4)) == _lib.SF_E_ALIGN
+
+    def bwd(ck, nb=1 << 30, dq=8):
+        return L.sf_chain_bwd(ctypes.byref(s), 3, segs, p(1), p(2), p(3), p(4), p(5), ck, nb, p(6), None,
+                              p(dq), p(9), p(10), p(11), p(12), p(13), 1 << 30, tp, None, None)
+
+    assert bwd(p(8)) == _lib.SF_E_ALIAS             # over dq
+    assert bwd(p(13)) == _lib.SF_E_ALIAS            # over the workspace
+    assert bwd(p(14), nb=need - 256) == _lib.SF_E_WORKSPACE
 
 
 def test_chain_validation():
     L = _lib.lib()
     s = shape(L=1024)
     segs = (ctypes.c_int64 * 2)(512, 448)   # sums to 960
-    rc = L.sf_chain_fwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), p(7), 1 << 30, None,
+    rc = L.sf_chain_fwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, 0, p(7), 1 << 30, None,
                         None, None)
     assert rc == _lib.SF_E_SHAPE
     segs = (ctypes.c_int64 * 2)(512, 512)
-    rc = L.sf_chain_fwd(ctypes.byref(s), 0, segs, p(1), p(2), p(3), p(4), p(5), p(6), p(7), 1 << 30, None,
+    rc = L.sf_chain_fwd(ctypes.byref(s), 0, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, 0, p(7), 1 << 30, None,
                         None, None)
     assert rc == _lib.SF_E_SHAPE
-    rc = L.sf_chain_bwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, p(8), p(9),
+    rc = L.sf_chain_bwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), None, 0, p(6), None, p(8), p(9),
                         p(10), p(11), None, p(13), 1 << 30, None, None, None)
     assert rc == _lib.SF_E_NULL  # dS_init missing
 

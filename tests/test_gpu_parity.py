@@ -106,10 +106,16 @@ def test_empty_segment():
     assert torch.equal(dS_in, inp["dS_out"])
 
 
-def run_chain(g, seg_lens, ts=0, overlap=True):
-    o, S_bnd = sf.chain_fwd(g["q"], g["k"], g["v"], g["g"], seg_lens, g["S_in"], ts=ts, overlap=overlap)
+def run_chain(g, seg_lens, ts=0, overlap=True, keep=False):
+    """keep: the backward reads the superchunk states the forward kept."""
+    ck = None
+    if keep:
+        o, S_bnd, ck = sf.chain_fwd(g["q"], g["k"], g["v"], g["g"], seg_lens, g["S_in"], ts=ts, overlap=overlap,
+                                    keep_states=True)
+    else:
+        o, S_bnd = sf.chain_fwd(g["q"], g["k"], g["v"], g["g"], seg_lens, g["S_in"], ts=ts, overlap=overlap)
     dq, dk, dv, dg, dS0 = sf.chain_bwd(g["q"], g["k"], g["v"], g["g"], seg_lens, S_bnd, g["dO"], g["dS_out"],
-                                       ts=ts, overlap=overlap)
+                                       ts=ts, overlap=overlap, ckpt=ck)
     torch.cuda.synchronize()
     return dict(o=o, S_bnd=S_bnd, S_out=S_bnd[-1], dq=dq, dk=dk, dv=dv, dg=dg, dS_in=dS0)
 
@@ -139,6 +145,28 @@ def test_chain_nonuniform_small(ts):
     check_chain("bf16", inp, a, seg_lens)
 
 
+KEPT_CASES = [("mid_bf16", 128, "bf16", 0), ("mid_bf16", 128, "bf16", 64), ("mid_bf16", 64, "bf16", 128),
+              ("tiny_fp32", 64, "f32", 128), ("vector_gate", 128, "bf16", 128), ("vector_gate", 64, "f32", 64)]
+
+
+@pytest.mark.parametrize("name,D,io,ts", KEPT_CASES)
+def test_kept_states(name, D, io, ts):
+    """Backward from the superchunk states the forward kept: bitwise the
+    outputs of the backward that replays them (segments of one and of several
+    superchunks, overlap on and off), and within the bar of the oracle."""
+    w = synth.workload(name, B=1, H=3, D=D, io=io)
+    seg_lens = [192, 64, 320, 128]
+    inp = synth.make_inputs(w, device="cpu", seed=53 + D + ts, dS_out_std=0.1, L=sum(seg_lens))
+    g = on_gpu(inp)
+    say(f"[chain] kept states {name} D={D} {io} ts={ts}")
+    for overlap in (False, True):
+        a = run_chain(g, seg_lens, ts=ts, overlap=overlap)
+        b = run_chain(g, seg_lens, ts=ts, overlap=overlap, keep=True)
+        for key in a:
+            assert torch.equal(a[key], b[key]), (key, overlap)
+    check_chain(io, inp, b, seg_lens)
+
+
 def test_mid_layer_chain():
     """B=1, H=16, d=128, L=32768 in 8 segments of 4096, bf16 I/O, S_in ~ 0.1 N(0,1)."""
     w = synth.workload("mid_bf16")
@@ -155,7 +183,7 @@ def test_scan_stress_sampled():
     say("[chain] scan_stress full size")
     inp = synth.make_inputs(w, device=DEV, seed=1004, dS_out_std=0.1)
     got = run_chain(inp, w["seg_lens"])
-    again = run_chain(inp, w["seg_lens"], overlap=False)
+    again = run_chain(inp, w["seg_lens"], overlap=False, keep=True)
     for key in got:
         assert torch.equal(got[key], again[key]), key
     check_chain("bf16", inp, got, w["seg_lens"], pairs=[(0, 0), (1, 7), (2, 31), (3, 16), (0, 20), (3, 3)])
@@ -165,13 +193,14 @@ def test_ctx256k_sampled():
     """B=1, H=40, d=128, L=262144 in 8 nonuniform segments (the 256K-context
     workload) with a nonzero gradient of the final state.  Full-size run; the
     oracle checks the first, a middle and the last head end to end, interior
-    boundary states included; the run is repeated and every output must be
-    bitwise identical."""
+    boundary states included; the run is repeated with the backward reading the
+    forward's kept superchunk states, and every output must be bitwise
+    identical."""
     w = synth.workload("ctx256k_h40")
     say("[chain] ctx256k_h40 full size")
     inp = synth.make_inputs(w, device=DEV, seed=1002, dS_out_std=0.1)
     got = run_chain(inp, w["seg_lens"])
-    again = run_chain(inp, w["seg_lens"])
+    again = run_chain(inp, w["seg_lens"], keep=True)
     for key in ("o", "S_bnd", "dq", "dk", "dv", "dg", "dS_in"):
         assert torch.equal(got[key], again[key]), key
     say("[chain] ctx256k_h40 oracle on heads 0, 17, 39")
