@@ -423,9 +423,12 @@ def bench_gdn(args):
     ov = not args.gdn_serial
     timer = sf.KernelTimer(capacity=256 * max(1, args.steps))
 
-    def step(tm=None):
-        _, S_bnd = sf.gdn_chain_fwd(*x, inp["S_in"], ts=args.gdn_ts, overlap=ov, timing=tm)
-        sf.gdn_chain_bwd(*x, S_bnd, dO, None, ts=args.gdn_ts, overlap=ov, timing=tm)
+    keep = not args.recompute
+
+    def step(tm=None, keep=keep):
+        out = sf.gdn_chain_fwd(*x, inp["S_in"], ts=args.gdn_ts, overlap=ov, timing=tm, keep_states=keep)
+        sf.gdn_chain_bwd(*x, out[1], dO, None, ts=args.gdn_ts, overlap=ov, timing=tm,
+                         ckpt=out[2] if keep else None)
 
     for i in range(args.warmup):
         if i == args.warmup - 1:
@@ -448,6 +451,15 @@ def bench_gdn(args):
     peak = torch.cuda.max_memory_allocated()
     tot_ms, nl = timer.read()[dom]
     ms = (t1 - t0) * 1e3 / args.steps
+    # the same step with the backward replaying the superchunk states and maps
+    # (or reading the kept ones, under --recompute)
+    kept = {"kept": keep, "bytes": sf.gdn_chain_ckpt_bytes(inp["q"], inp["g"], seg, ts=args.gdn_ts, overlap=ov)}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(keep=not keep)
+    torch.cuda.synchronize()
+    kept["t_recompute_ms" if keep else "t_kept_ms"] = (time.perf_counter() - t0) * 1e3 / args.steps
     copy_calibration(torch, dev, args.copy_mib)
     avg_s = tot_ms / 1e3 / max(nl, 1)
     if dom == "gdn_dchunk":
@@ -474,6 +486,7 @@ def bench_gdn(args):
         "kernels_ms_per_step": {k: wtime.get(k, (0.0, 0))[0] for k in GDN_KERNELS},
         "peak_mem_bytes": peak,
         "roofline": roof,
+        "superchunk_states": kept,
     }
     if not args.no_cpu_baseline:
         from oracle import gdn as ogdn

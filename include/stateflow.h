@@ -392,6 +392,13 @@ sf_status sf_gdn_bwd(const sf_shape *shape, const void *q, const void *k, const 
  *   dS_final  optional gradient of the state after the last segment.
  *   dS_init   receives the gradient of S_init.
  *   ws     at least sf_gdn_chain_workspace_bytes(); contents on entry ignored.
+ *   ckpt   NULL, or a caller buffer (16-byte aligned) of at least
+ *          sf_gdn_chain_ckpt_bytes(): the forward writes there, per segment of
+ *          more than one superchunk, the state entering every superchunk and
+ *          every superchunk's map M_J (fp32 Dk x Dk); the backward, given the
+ *          buffer the forward filled for the same shape, segments and tuning,
+ *          reads them instead of running the prep walk and the state scan
+ *          again.  The results are the same either way.
  * With aux != NULL (and tuning->overlap != 0) the state scans run on aux:
  * forward, the scan of each segment (which then also writes S_bnd[i+1]) runs
  * alongside the previous segment's output walk; backward, the state scan
@@ -402,15 +409,19 @@ sf_status sf_gdn_bwd(const sf_shape *shape, const void *q, const void *k, const 
  */
 size_t sf_gdn_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
                                     const sf_tuning *tuning);
+/* Bytes of the kept states and maps (0 when no segment has more than one
+ * superchunk, and on invalid arguments, with sf_last_error() set). */
+size_t sf_gdn_chain_ckpt_bytes(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
+                               const sf_tuning *tuning);
 sf_status sf_gdn_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
                            const void *k, const void *v, const float *g, const float *beta, void *o, float *S_bnd,
-                           void *v_new, void *ws, size_t ws_bytes, const sf_tuning *tuning, sf_stream main,
-                           sf_stream aux);
+                           void *ckpt, size_t ckpt_bytes, void *v_new, void *ws, size_t ws_bytes,
+                           const sf_tuning *tuning, sf_stream main, sf_stream aux);
 sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
                            const void *k, const void *v, const float *g, const float *beta, const float *S_bnd,
-                           const void *dO, const float *dS_final, void *dq, void *dk, void *dv, float *dg,
-                           float *dbeta, float *dS_init, void *ws, size_t ws_bytes, const sf_tuning *tuning,
-                           sf_stream main, sf_stream aux);
+                           const void *ckpt, size_t ckpt_bytes, const void *dO, const float *dS_final, void *dq,
+                           void *dk, void *dv, float *dg, float *dbeta, float *dS_init, void *ws, size_t ws_bytes,
+                           const sf_tuning *tuning, sf_stream main, sf_stream aux);
 
 
 #ifdef __cplusplus

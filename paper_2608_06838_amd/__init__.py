@@ -32,7 +32,7 @@ from .timing import KernelTimer  # noqa: F401
 
 __all__ = ["segment_fwd", "segment_fwd_noalloc", "segment_bwd", "chain_ckpt_bytes", "chain_fwd", "chain_bwd", "fwd_workspace_bytes",
            "bwd_workspace_bytes", "chain_workspace_bytes", "conv_fwd", "conv_bwd", "conv_bwd_workspace_bytes",
-           "gdn_fwd", "gdn_fwd_workspace_bytes", "gdn_bwd", "gdn_chain_fwd", "gdn_chain_bwd", "partition_hybrid", "KernelTimer", "StateflowError", "abi_version"]
+           "gdn_fwd", "gdn_fwd_workspace_bytes", "gdn_bwd", "gdn_chain_ckpt_bytes", "gdn_chain_fwd", "gdn_chain_bwd", "partition_hybrid", "KernelTimer", "StateflowError", "abi_version"]
 
 _IO = {torch.bfloat16: _lib.SF_BF16, torch.float32: _lib.SF_F32}
 _aux_streams = {}
@@ -455,13 +455,28 @@ def gdn_bwd(q, k, v, g, beta, S_in, dO, dS_out=None, *, ts=0, stream=None, timin
     return dq, dk, dv, dg, dbeta, dS_in
 
 
+def gdn_chain_ckpt_bytes(q, g, seg_lens, ts=0, overlap=True):
+    """Bytes of the superchunk states and maps gdn_chain_fwd(keep_states=True) keeps."""
+    sh = _shape(q, g)
+    n = len(seg_lens)
+    tun = _tuning(ts, overlap)
+    sl = (ctypes.c_int64 * n)(*[int(x) for x in seg_lens])
+    L_ = _lib.lib()
+    nb = L_.sf_gdn_chain_ckpt_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun))
+    if nb == 0 and L_.sf_last_error():
+        raise StateflowError("sf_gdn_chain_ckpt_bytes: " + L_.sf_last_error().decode())
+    return nb
+
+
 def gdn_chain_fwd(q, k, v, g, beta, seg_lens, S_init=None, *, ts=0, overlap=True, with_v_new=False, stream=None,
-                  aux_stream=None, timing=None):
+                  aux_stream=None, timing=None, keep_states=False):
     """Gated-delta-rule forward over consecutive segments with
     S_in(i+1) = S_out(i), the state scans overlapped on an aux stream.
 
     Returns (o, S_bnd) (and V^new after them when with_v_new) with S_bnd[i] the
-    state entering segment i and S_bnd[-1] the final state."""
+    state entering segment i and S_bnd[-1] the final state.  keep_states=True
+    appends the kept superchunk states and maps (a uint8 device tensor) for
+    gdn_chain_bwd(ckpt=...), which then skips replaying them."""
     _same_layout(q, k, v)
     sh = _shape(q, g)
     if tuple(beta.shape) != tuple(g.shape) or beta.stride() != g.stride() or beta.dtype != torch.float32:
@@ -479,21 +494,26 @@ def gdn_chain_fwd(q, k, v, g, beta, seg_lens, S_init=None, *, ts=0, overlap=True
         vn = _like(q) if with_v_new else None
         S_bnd = torch.empty((n + 1, B, H, D, D), dtype=torch.float32, device=q.device)
         ws = _ws(L_.sf_gdn_chain_workspace_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun)), q.device)
+        ck = _ws(L_.sf_gdn_chain_ckpt_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun)), q.device) \
+            if keep_states else None
         if S_init is None:
             S_bnd[0].zero_()
         else:
             S_bnd[0].copy_(S_init)
     rc = L_.sf_gdn_chain_fwd(ctypes.byref(sh), n, sl, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(o),
-                             _ptr(S_bnd), _ptr(vn), _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream),
+                             _ptr(S_bnd), _ptr(ck), ck.numel() if ck is not None else 0, _ptr(vn), _ptr(ws),
+                             ws.numel(), ctypes.byref(tun), _stream_handle(stream),
                              _stream_handle(aux) if aux is not None else None)
     _lib.check("sf_gdn_chain_fwd", rc)
-    return (o, S_bnd, vn) if with_v_new else (o, S_bnd)
+    out = (o, S_bnd, vn) if with_v_new else (o, S_bnd)
+    return out + (ck,) if keep_states else out
 
 
 def gdn_chain_bwd(q, k, v, g, beta, seg_lens, S_bnd, dO, dS_final=None, *, ts=0, overlap=True, stream=None,
-                  aux_stream=None, timing=None):
+                  aux_stream=None, timing=None, ckpt=None):
     """Gated-delta-rule backward over the segments in reverse with
-    dS_out(i) = dS_in(i+1); S_bnd from gdn_chain_fwd.  Returns
+    dS_out(i) = dS_in(i+1); S_bnd from gdn_chain_fwd, ckpt its kept states
+    (same inputs, segments and settings) or None.  Returns
     (dq, dk, dv, dg, dbeta, dS_init)."""
     _same_layout(q, k, v, dO)
     sh = _shape(q, g)
@@ -514,7 +534,10 @@ def gdn_chain_bwd(q, k, v, g, beta, seg_lens, S_bnd, dO, dS_final=None, *, ts=0,
         dg, dbeta = _like(g), _like(beta)
         dS_init = torch.empty((B, H, D, D), dtype=torch.float32, device=q.device)
         ws = _ws(L_.sf_gdn_chain_workspace_bytes(ctypes.byref(sh), n, sl, ctypes.byref(tun)), q.device)
+    if ckpt is not None and (ckpt.device != q.device or not ckpt.is_contiguous()):
+        raise ValueError("ckpt must be a contiguous buffer on the inputs' device")
     rc = L_.sf_gdn_chain_bwd(ctypes.byref(sh), n, sl, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(S_bnd),
+                             _ptr(ckpt), ckpt.numel() * ckpt.element_size() if ckpt is not None else 0,
                              _ptr(dO), _ptr(dS_final), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg), _ptr(dbeta),
                              _ptr(dS_init), _ptr(ws), ws.numel(), ctypes.byref(tun), _stream_handle(stream),
                              _stream_handle(aux) if aux is not None else None)

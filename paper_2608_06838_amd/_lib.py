@@ -26,7 +26,7 @@ EXPORTS = ["sf_abi_version", "sf_status_str", "sf_last_error", "sf_fwd_workspace
            "sf_bwd_workspace_bytes", "sf_segment_fwd", "sf_segment_fwd_noalloc", "sf_segment_bwd", "sf_chain_workspace_bytes",
            "sf_chain_ckpt_bytes", "sf_chain_fwd", "sf_chain_bwd", "sf_conv_bwd_workspace_bytes", "sf_conv_fwd", "sf_conv_bwd",
            "sf_gdn_fwd_workspace_bytes", "sf_gdn_fwd", "sf_gdn_bwd_workspace_bytes", "sf_gdn_bwd",
-           "sf_gdn_chain_workspace_bytes", "sf_gdn_chain_fwd", "sf_gdn_chain_bwd",
+           "sf_gdn_chain_workspace_bytes", "sf_gdn_chain_ckpt_bytes", "sf_gdn_chain_fwd", "sf_gdn_chain_bwd",
            "sf_partition_hybrid"]
 
 
@@ -124,9 +124,13 @@ def lib():
     L.sf_gdn_chain_workspace_bytes.restype = sz
     L.sf_gdn_chain_workspace_bytes.argtypes = [sp, i32, i64p, tp]
     L.sf_gdn_chain_fwd.restype = ctypes.c_int
-    L.sf_gdn_chain_fwd.argtypes = [sp, i32, i64p] + [vp] * 9 + [sz, tp, vp, vp]
+    L.sf_gdn_chain_ckpt_bytes.restype = sz
+    L.sf_gdn_chain_ckpt_bytes.argtypes = [sp, i32, i64p, tp]
+    # (..., beta, o, S_bnd, ckpt, ckpt_bytes, v_new, ws, ws_bytes, tuning, main, aux)
+    L.sf_gdn_chain_fwd.argtypes = [sp, i32, i64p] + [vp] * 8 + [sz] + [vp] * 2 + [sz, tp, vp, vp]
     L.sf_gdn_chain_bwd.restype = ctypes.c_int
-    L.sf_gdn_chain_bwd.argtypes = [sp, i32, i64p] + [vp] * 15 + [sz, tp, vp, vp]
+    # (..., beta, S_bnd, ckpt, ckpt_bytes, dO, dS_final, dq, dk, dv, dg, dbeta, dS_init, ws, ws_bytes, ...)
+    L.sf_gdn_chain_bwd.argtypes = [sp, i32, i64p] + [vp] * 7 + [sz] + [vp] * 9 + [sz, tp, vp, vp]
     L.sf_partition_hybrid.restype = ctypes.c_int
     L.sf_partition_hybrid.argtypes = [i64, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double, i32, i64p]
     _lib = L

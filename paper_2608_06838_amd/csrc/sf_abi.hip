@@ -1289,6 +1289,16 @@ GdnChainWs gdn_chain_ws(const Shape &r, const GdnPlan &p) {
     return w;
 }
 
+// kept states of a chain: per segment of n > 1 superchunks, S_J then M_J
+size_t gdn_ckpt_seg(const Shape &r, int n) {
+    return n > 1 ? 2 * al((size_t)r.B * r.H * n * (size_t)r.D * r.D * 4) : 0;
+}
+size_t gdn_ckpt_total(const Shape &r, const GdnPlan &p) {
+    size_t t = 0;
+    for (int n : p.n) t += gdn_ckpt_seg(r, n);
+    return t;
+}
+
 sf_status gdn_shape_ok(const Shape &r) {
     if (r.io != SF_BF16) return fail(SF_E_UNSUPPORTED, "the gated delta rule needs bf16 I/O");
     if (r.gate != SF_GATE_SCALAR) return fail(SF_E_UNSUPPORTED, "the gated delta rule takes a scalar gate");
@@ -1475,10 +1485,21 @@ size_t sf_gdn_chain_workspace_bytes(const sf_shape *shape, int32_t n_seg, const 
     return gdn_chain_ws(r, p).total;
 }
 
+size_t sf_gdn_chain_ckpt_bytes(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len,
+                               const sf_tuning *tuning) {
+    g_err.clear();
+    Shape r;
+    GdnPlan p;
+    if (resolve(shape, r) != SF_OK || check_segments(r, n_seg, seg_len) != SF_OK ||
+        gdn_plan(r, n_seg, seg_len, tuning, p) != SF_OK)
+        return 0;
+    return gdn_ckpt_total(r, p);
+}
+
 sf_status sf_gdn_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
                            const void *k, const void *v, const float *g, const float *beta, void *o, float *S_bnd,
-                           void *v_new, void *ws, size_t ws_bytes, const sf_tuning *tuning, sf_stream main_s,
-                           sf_stream aux_s) {
+                           void *ckpt, size_t ckpt_bytes, void *v_new, void *ws, size_t ws_bytes,
+                           const sf_tuning *tuning, sf_stream main_s, sf_stream aux_s) {
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
@@ -1487,20 +1508,24 @@ sf_status sf_gdn_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *
     TRY(check_segments(r, n_seg, seg_len));
     if (!q || !k || !v || !g || !beta || !o || !S_bnd || !ws)
         return fail(SF_E_NULL, "q, k, v, g, beta, o, S_bnd and ws are required");
-    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_bnd, "S_bnd"}, {v_new, "v_new"}, {ws, "ws"}}));
+    TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {o, "o"}, {S_bnd, "S_bnd"}, {ckpt, "ckpt"}, {v_new, "v_new"},
+                     {ws, "ws"}}));
     if (((uintptr_t)g | (uintptr_t)beta) % 4) return fail(SF_E_ALIGN, "g and beta must be 4-byte aligned");
     GdnPlan p;
     TRY(gdn_plan(r, n_seg, seg_len, tuning, p));
     const GdnChainWs W = gdn_chain_ws(r, p);
     if (ws_bytes < W.total) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, W.total);
+    const size_t kneed = gdn_ckpt_total(r, p);
+    if (ckpt && ckpt_bytes < kneed) return fail(SF_E_WORKSPACE, "ckpt %zu < required %zu", ckpt_bytes, kneed);
     TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"), grange(r, g, r.L, "g"),
                      grange(r, beta, r.L, "beta")},
                     {xrange(r, o, r.L, "o"), srange(r, S_bnd, n_seg + 1, "S_bnd"), xrange(r, v_new, r.L, "v_new"),
-                     wsrange(ws, W.total)}));
+                     span(ckpt, (int64_t)kneed, "ckpt"), wsrange(ws, W.total)}));
     const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
     const GdnFwdWs F = gdn_fwd_ws_n(r, p.n_max, p.n_max);
     std::vector<sf::GdnArgs> seg(n_seg);
     int64_t tok = 0;
+    size_t kofs = 0;
     for (int i = 0; i < n_seg; ++i) {
         sf::GdnArgs &a = seg[i];
         a = gdn_seg_args(r, tok, seg_len[i], p.ts[i], q, k, v, g, beta);
@@ -1515,6 +1540,12 @@ sf_status sf_gdn_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *
             a.wsS = (float *)(base + F.S);
             a.wsM = (float *)(base + F.M);
             a.wsN = (float *)(base + F.N);
+            if (ckpt) {  // S_J and M_J go to the kept-state buffer
+                char *kb = (char *)ckpt + kofs;
+                a.wsS = (float *)kb;
+                a.wsM = (float *)(kb + gdn_ckpt_seg(r, a.n_super) / 2);
+                kofs += gdn_ckpt_seg(r, a.n_super);
+            }
         }
         tok += seg_len[i];
     }
@@ -1558,9 +1589,9 @@ sf_status sf_gdn_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *
 
 sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_len, const void *q,
                            const void *k, const void *v, const float *g, const float *beta, const float *S_bnd,
-                           const void *dO, const float *dS_final, void *dq, void *dk, void *dv, float *dg,
-                           float *dbeta, float *dS_init, void *ws, size_t ws_bytes, const sf_tuning *tuning,
-                           sf_stream main_s, sf_stream aux_s) {
+                           const void *ckpt, size_t ckpt_bytes, const void *dO, const float *dS_final, void *dq,
+                           void *dk, void *dv, float *dg, float *dbeta, float *dS_init, void *ws, size_t ws_bytes,
+                           const sf_tuning *tuning, sf_stream main_s, sf_stream aux_s) {
     g_err.clear();
     Shape r;
     TRY(resolve(shape, r));
@@ -1570,16 +1601,18 @@ sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *
     if (!q || !k || !v || !g || !beta || !S_bnd || !dO || !dq || !dk || !dv || !dg || !dbeta || !dS_init || !ws)
         return fail(SF_E_NULL, "q, k, v, g, beta, S_bnd, dO, dq, dk, dv, dg, dbeta, dS_init and ws are required");
     TRY(check_align({{q, "q"}, {k, "k"}, {v, "v"}, {dO, "dO"}, {dq, "dq"}, {dk, "dk"}, {dv, "dv"}, {S_bnd, "S_bnd"},
-                     {dS_final, "dS_final"}, {dS_init, "dS_init"}, {ws, "ws"}}));
+                     {ckpt, "ckpt"}, {dS_final, "dS_final"}, {dS_init, "dS_init"}, {ws, "ws"}}));
     if (((uintptr_t)g | (uintptr_t)beta | (uintptr_t)dg | (uintptr_t)dbeta) % 4)
         return fail(SF_E_ALIGN, "g, beta, dg and dbeta must be 4-byte aligned");
     GdnPlan p;
     TRY(gdn_plan(r, n_seg, seg_len, tuning, p));
     const GdnChainWs W = gdn_chain_ws(r, p);
     if (ws_bytes < W.total) return fail(SF_E_WORKSPACE, "workspace %zu < required %zu", ws_bytes, W.total);
+    const size_t kneed = gdn_ckpt_total(r, p);
+    if (ckpt && ckpt_bytes < kneed) return fail(SF_E_WORKSPACE, "ckpt %zu < required %zu", ckpt_bytes, kneed);
     TRY(check_alias({xrange(r, q, r.L, "q"), xrange(r, k, r.L, "k"), xrange(r, v, r.L, "v"), grange(r, g, r.L, "g"),
-                     grange(r, beta, r.L, "beta"), srange(r, S_bnd, n_seg, "S_bnd"), xrange(r, dO, r.L, "dO"),
-                     srange(r, dS_final, 1, "dS_final")},
+                     grange(r, beta, r.L, "beta"), srange(r, S_bnd, n_seg, "S_bnd"), span(ckpt, (int64_t)kneed, "ckpt"),
+                     xrange(r, dO, r.L, "dO"), srange(r, dS_final, 1, "dS_final")},
                     {xrange(r, dq, r.L, "dq"), xrange(r, dk, r.L, "dk"), xrange(r, dv, r.L, "dv"),
                      grange(r, dg, r.L, "dg"), grange(r, dbeta, r.L, "dbeta"), srange(r, dS_init, 1, "dS_init"),
                      wsrange(ws, W.total)}));
@@ -1588,7 +1621,9 @@ sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *
     char *base = (char *)ws;
     float *dslot[2] = {(float *)(base + W.bwd), (float *)(base + W.bwd + W.dslot)};
     std::vector<sf::GdnArgs> seg(n_seg);
+    std::vector<char> kept(n_seg, 0);
     int64_t tok = 0;
+    size_t kofs = 0;
     for (int i = 0; i < n_seg; ++i) {
         sf::GdnArgs &a = seg[i];
         a = gdn_seg_args(r, tok, seg_len[i], p.ts[i], q, k, v, g, beta);
@@ -1610,6 +1645,13 @@ sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *
             a.wsN = (float *)(base + Lw.N);
             a.wsE = (float *)(base + Lw.E);
             a.wsDe = (float *)(base + Lw.De);
+            if (ckpt) {  // the forward's S_J and M_J (read only)
+                char *kb = (char *)ckpt + kofs;
+                a.wsS = (float *)kb;
+                a.wsM = (float *)(kb + gdn_ckpt_seg(r, a.n_super) / 2);
+                kofs += gdn_ckpt_seg(r, a.n_super);
+                kept[i] = 1;
+            }
         }
         a.wsSc = (float *)(base + Lw.Sc);
         a.wsDc = (float *)(base + Lw.Dc);
@@ -1630,16 +1672,18 @@ sf_status sf_gdn_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *
     for (int i = n_seg - 1; i >= 0; --i) {
         sf::GdnArgs &a = seg[i];
         if (a.n_super > 1) {
-            TRY(gdn_launch(sf::GDN_PREP, a, r.D, mn, timing_of(tuning)));
-            TRY(dep(mn, ax, e0));
-            TRY(gdn_launch(sf::GDN_SCAN, a, r.D, ax, timing_of(tuning)));
-            if (ax != mn) TRY(record(sd[0], ax));
+            if (!kept[i]) {  // replay the forward's maps and states
+                TRY(gdn_launch(sf::GDN_PREP, a, r.D, mn, timing_of(tuning)));
+                TRY(dep(mn, ax, e0));
+                TRY(gdn_launch(sf::GDN_SCAN, a, r.D, ax, timing_of(tuning)));
+                if (ax != mn) TRY(record(sd[0], ax));
+            }
             TRY(gdn_launch(sf::GDN_DPREP, a, r.D, mn, timing_of(tuning)));
             TRY(dep(mn, ax, e1));  // dS prep, and dS_out written by the later segment's dS walk
             TRY(gdn_launch(sf::GDN_DSCAN, a, r.D, ax, timing_of(tuning)));
             if (ax != mn) {
                 TRY(record(sd[1], ax));
-                TRY(wait(mn, sd[0]));
+                if (!kept[i]) TRY(wait(mn, sd[0]));
             }
         }
         TRY(gdn_launch(sf::GDN_STORE, a, r.D, mn, timing_of(tuning)));

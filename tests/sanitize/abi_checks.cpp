@@ -107,8 +107,14 @@ int main() {
                       nullptr) == SF_E_ALIAS);
     EXPECT(sf_gdn_bwd(&s, P(1), P(2), P(3), F(4), F(5), nullptr, P(6), nullptr, P(7), P(8), P(9), F(10), F(11), F(12),
                       P(7), 1ull << 40, nullptr, nullptr) == SF_E_ALIAS);
-    EXPECT(sf_gdn_chain_fwd(&s, 2, segs2, P(1), P(2), P(3), F(4), F(5), P(1), F(7), nullptr, P(8), 1ull << 40, nullptr,
-                            nullptr, nullptr) == SF_E_ALIAS);
+    EXPECT(sf_gdn_chain_fwd(&s, 2, segs2, P(1), P(2), P(3), F(4), F(5), P(1), F(7), nullptr, 0, nullptr, P(8),
+                            1ull << 40, nullptr, nullptr, nullptr) == SF_E_ALIAS);
+    const size_t gk = sf_gdn_chain_ckpt_bytes(&s, 2, segs2, &t128);
+    EXPECT(gk > 0);
+    EXPECT(sf_gdn_chain_fwd(&s, 2, segs2, P(1), P(2), P(3), F(4), F(5), P(6), F(7), P(9), gk - 1, nullptr, P(8),
+                            1ull << 40, &t128, nullptr, nullptr) == SF_E_WORKSPACE);
+    EXPECT(sf_gdn_chain_bwd(&s, 2, segs2, P(1), P(2), P(3), F(4), F(5), F(7), P(9), gk, P(6), nullptr, P(9), P(10),
+                            P(11), F(12), F(13), F(14), P(8), 1ull << 40, &t128, nullptr, nullptr) == SF_E_ALIAS);
     // partition: exact half-way cases round up, irrational boundaries, errors
     int64_t len[8];
     EXPECT(sf_partition_hybrid(384, 2, 0.0, 1.0, 1.0, 128, len) == SF_OK && len[0] == 256 && len[1] == 128);

@@ -366,13 +366,18 @@ def test_gdn_chain_validation():
     L = _lib.lib()
     segs = (ctypes.c_int64 * 3)(256, 512, 256)
 
-    def fwd(s, n=3, sl=segs, q=1, k=2, v=3, g=4, beta=5, o=6, S_bnd=7, v_new=None, ws=8, ws_bytes=1 << 40):
-        args = [p(i) if i is not None else None for i in (q, k, v, g, beta, o, S_bnd, v_new, ws)]
-        return L.sf_gdn_chain_fwd(ctypes.byref(s), n, sl, *args, ws_bytes, None, None, None)
+    def fwd(s, n=3, sl=segs, q=1, k=2, v=3, g=4, beta=5, o=6, S_bnd=7, v_new=None, ws=8, ws_bytes=1 << 40,
+            ck=None, ck_bytes=1 << 40, tun=None):
+        a1 = [p(i) if i is not None else None for i in (q, k, v, g, beta, o, S_bnd)]
+        a2 = [p(i) if i is not None else None for i in (v_new, ws)]
+        return L.sf_gdn_chain_fwd(ctypes.byref(s), n, sl, *a1, p(ck) if ck else None, ck_bytes, *a2, ws_bytes,
+                                  tun, None, None)
 
-    def bwd(s, n=3, sl=segs, dq=9, dS_init=14, ws=15):
-        args = [p(i) if i is not None else None for i in (1, 2, 3, 4, 5, 7, 6, None, dq, 10, 11, 12, 13, dS_init, ws)]
-        return L.sf_gdn_chain_bwd(ctypes.byref(s), n, sl, *args, 1 << 40, None, None, None)
+    def bwd(s, n=3, sl=segs, dq=9, dS_init=14, ws=15, ck=None, ck_bytes=1 << 40, tun=None):
+        a1 = [p(i) for i in (1, 2, 3, 4, 5, 7)]
+        a2 = [p(i) if i is not None else None for i in (6, None, dq, 10, 11, 12, 13, dS_init, ws)]
+        return L.sf_gdn_chain_bwd(ctypes.byref(s), n, sl, *a1, p(ck) if ck else None, ck_bytes, *a2, 1 << 40,
+                                  tun, None, None)
 
     s = shape(L=1024)
     assert fwd(s, n=0) == _lib.SF_E_SHAPE
@@ -388,3 +393,17 @@ def test_gdn_chain_validation():
     need = L.sf_gdn_chain_workspace_bytes(ctypes.byref(s), 3, segs, None)
     assert need > 0
     assert L.sf_gdn_chain_workspace_bytes(ctypes.byref(s), 3, (ctypes.c_int64 * 3)(256, 512, 128), None) == 0
+    # kept states: S_J and M_J of each segment of more than one superchunk
+    t = _tuning(ts=128)
+    SS, bh = 128 * 128 * 4, 2
+    kneed = L.sf_gdn_chain_ckpt_bytes(ctypes.byref(s), 3, segs, ctypes.byref(t))
+    assert kneed == sum(2 * ((bh * n * SS + 255) // 256 * 256) for n in (2, 4, 2))
+    # one superchunk per segment: nothing to keep
+    assert L.sf_gdn_chain_ckpt_bytes(ctypes.byref(s), 3, segs, ctypes.byref(_tuning(ts=512))) == 0
+    assert L.sf_gdn_chain_ckpt_bytes(ctypes.byref(s), 3, (ctypes.c_int64 * 3)(256, 512, 128), ctypes.byref(t)) == 0
+    tp = ctypes.byref(t)
+    assert fwd(s, ck=6, tun=tp) == _lib.SF_E_ALIAS        # over o
+    assert fwd(s, ck=8, tun=tp) == _lib.SF_E_ALIAS        # over the workspace
+    assert fwd(s, ck=16, ck_bytes=kneed - 1, tun=tp) == _lib.SF_E_WORKSPACE
+    assert bwd(s, ck=9, tun=tp) == _lib.SF_E_ALIAS        # over dq
+    assert bwd(s, ck=16, ck_bytes=kneed - 256, tun=tp) == _lib.SF_E_WORKSPACE

@@ -271,7 +271,9 @@ def test_gdn_chain_entry_points(D, ts):
     """sf_gdn_chain_fwd / sf_gdn_chain_bwd over nonuniform segments (one of
     them a single superchunk when ts = 128): forward, V^new and every gradient
     against the oracle over the whole sequence; the scans overlapped on an aux
-    stream give bitwise the same results as serialised on one stream."""
+    stream give bitwise the same results as serialised on one stream, and the
+    backward that reads the forward's kept superchunk states and maps gives
+    bitwise the results of the one that replays them."""
     B, H = 1, 3
     segs = [256, 64, 384, 192]
     say(f"[gdn chain] D={D} segs={segs} ts={ts}")
@@ -281,12 +283,17 @@ def test_gdn_chain_entry_points(D, ts):
     args = (g["q"], g["k"], g["v"], g["g"], g["beta"], segs)
     res = {}
     for ov in (True, False):
-        o, S_bnd, vn = sf.gdn_chain_fwd(*args, g["S_in"], ts=ts, overlap=ov, with_v_new=True)
-        grads = sf.gdn_chain_bwd(*args, S_bnd, dO.to(DEV), dS_final.to(DEV), ts=ts, overlap=ov)
-        torch.cuda.synchronize()
-        res[ov] = (o, S_bnd, vn) + tuple(grads)
-    for x, y in zip(res[True], res[False]):
-        assert torch.equal(x, y)
+        for keep in (False, True):
+            out = sf.gdn_chain_fwd(*args, g["S_in"], ts=ts, overlap=ov, with_v_new=True, keep_states=keep)
+            o, S_bnd, vn = out[:3]
+            grads = sf.gdn_chain_bwd(*args, S_bnd, dO.to(DEV), dS_final.to(DEV), ts=ts, overlap=ov,
+                                     ckpt=out[3] if keep else None)
+            torch.cuda.synchronize()
+            res[ov, keep] = (o, S_bnd, vn) + tuple(grads)
+    for key in res:
+        for x, y in zip(res[True, False], res[key]):
+            assert torch.equal(x, y), key
+    res[True] = res[True, False]
     o, S_bnd, vn = res[True][:3]
     ro, rS, ru = gdn.forward(*(to64(inp[x]) for x in ("q", "k", "v", "g", "beta", "S_in")), threads=cores(),
                              with_u=True)
