@@ -288,7 +288,7 @@ def bench_conv(args):
     timer.close()
 
 
-def make_chain_step(sf, torch, inp, seg, ts, overlap, keep=True):
+def make_chain_step(sf, torch, inp, seg, ts, overlap, keep=False):
     """fwd+bwd chain over segments `seg` with preallocated outputs and
     workspaces (the step allocates nothing).  step(timer) times the launches
     of the kernels the timer selects.  keep: the forward keeps its superchunk
@@ -423,7 +423,7 @@ def bench_gdn(args):
     ov = not args.gdn_serial
     timer = sf.KernelTimer(capacity=256 * max(1, args.steps))
 
-    keep = not args.recompute
+    keep = args.keep_states
 
     def step(tm=None, keep=keep):
         out = sf.gdn_chain_fwd(*x, inp["S_in"], ts=args.gdn_ts, overlap=ov, timing=tm, keep_states=keep)
@@ -451,8 +451,8 @@ def bench_gdn(args):
     peak = torch.cuda.max_memory_allocated()
     tot_ms, nl = timer.read()[dom]
     ms = (t1 - t0) * 1e3 / args.steps
-    # the same step with the backward replaying the superchunk states and maps
-    # (or reading the kept ones, under --recompute)
+    # the same step with the backward reading the superchunk states and maps the
+    # forward kept (or replaying them, under --keep-states)
     kept = {"kept": keep, "bytes": sf.gdn_chain_ckpt_bytes(inp["q"], inp["g"], seg, ts=args.gdn_ts, overlap=ov)}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -619,7 +619,7 @@ def bench_recurrence(args):
     # inputs below ~2 GiB could sit partly in the 256 MB MALL between steps
     in_bytes = sum(inp[k].numel() * inp[k].element_size() for k in ("q", "k", "v", "g", "dO"))
     flush = Flusher(torch, dev, MALL_FLUSH_MIB if in_bytes < (2 << 30) else 0)
-    keep = not args.recompute
+    keep = args.keep_states
     step = make_chain_step(sf, torch, inp, seg, ts, overlap, keep=keep)
     timer = sf.KernelTimer(capacity=max(512, 8 * len(seg) * (args.steps + 1)))
 
@@ -660,8 +660,9 @@ def bench_recurrence(args):
         ov.update(t_e2e_ms=ms, t_overlapped_ms=t_over, t_serial_ms=t_serial, t_scan_serial_ms=t_scan,
                   t_intra_only_ms=t_intra, e2e_over_intra_only=ms / t_intra if t_intra > 0 else None,
                   hidden_frac_of_scan=(t_serial - t_over) / t_scan if t_scan > 0 else None)
-    # The superchunk states: kept by the forward for the backward (default), or
-    # replayed by the backward (the same step with every state recomputed).
+    # The superchunk states: replayed by the backward (the default: the paper's
+    # full recomputation, every row of the path in the timed step), or kept by
+    # the forward for the backward (the same step without the replay).
     kept = {"kept": keep, "bytes": step.ckpt_bytes}
     if not args.no_overlap_study:
         kept["t_recompute_ms" if keep else "t_kept_ms"] = timed_steps(torch, lambda: step(None, keep=not keep),
@@ -718,8 +719,9 @@ def main():
     ap.add_argument("--overlap", action="store_true", help="scans overlapped on the aux stream")
     ap.add_argument("--no-overlap-study", action="store_true",
                     help="skip the serial / overlapped comparison after the timed steps")
-    ap.add_argument("--recompute", action="store_true",
-                    help="the backward replays the superchunk states instead of reading the forward's")
+    ap.add_argument("--keep-states", action="store_true",
+                    help="time the step whose backward reads the superchunk states the forward kept, instead of "
+                         "replaying them (the paper's full recomputation, the default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-times", action="store_true", help="print per-kernel times to stderr")
     ap.add_argument("--copy-mib", type=int, default=0,

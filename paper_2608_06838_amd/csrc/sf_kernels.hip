@@ -12,14 +12,15 @@
 //
 // Kernels (one workgroup of D/16 waves per (batch, head, superchunk); wave w
 // owns the 16 state columns [16w, 16w+16)):
-//   k_prep<.., BWD=false>  Pre: superchunk state contribution D_J and its decay
-//   k_scan<false>          ST:  S_{J+1} = Gamma_J S_J + D_J (fp32), S_out
-//   k_walk<.., DQ=false>   Out: walk the chunks from S_J, write o
-//   k_prep<.., BWD=true>   replay D_J and the state-gradient contribution E_J
-//   k_scan<true>           ST + STB: S_J forward, G_{J+1} backward, dS_in,
-//                          <G_{J+1}, S_{J+1}> partials for dg
-//   k_walk<.., DQ=true>    dq by a forward walk; also q.dq per token
-//   k_bwd_dkv              dk, dv, dg by a reverse walk of the state gradient
+//   k_prep<.., EONLY=false> Pre: superchunk state contribution D_J and its decay
+//                           (in the backward too, as the replay of the forward's)
+//   k_scan<false>           ST:  S_{J+1} = Gamma_J S_J + D_J (fp32), S_out
+//   k_walk<.., DQ=false>    Out: walk the chunks from S_J, write o
+//   k_prep<.., EONLY=true>  the state-gradient contribution E_J
+//   k_scan<true>            ST + STB: S_J forward, G_{J+1} backward, dS_in,
+//                           <G_{J+1}, S_{J+1}> partials for dg
+//   k_walk<.., DQ=true>     dq by a forward walk; also q.dq per token
+//   k_bwd_dkv               dk, dv, dg by a reverse walk of the state gradient
 // A segment that fits in one superchunk skips prep and scan: the walkers start
 // from S_in / dS_out directly and produce S_out / dS_in themselves.
 #include "sf_chunk.hpp"
@@ -34,66 +35,48 @@ constexpr int SCAN_NT = 256;
 #ifndef SF_NCT_PREP
 #define SF_NCT_PREP 2
 #endif
-#ifndef SF_NCT_PREPB
-#define SF_NCT_PREPB 1
-#endif
 #ifndef SF_NCT_WALK
 #define SF_NCT_WALK 2
 #endif
 
 // ---------------------------------------------------------------------------
-// Pre: per superchunk, D_J = sum_c (decay after c) (K~_c)^T V_c, and for the
-// backward E_J = sum_t exp(B_t) q_t dO_t^T (B superchunk-local, inclusive).
-// Wave w owns NCT state column tiles.  The key (query) tile is read through
-// transposing loads as the exact shared operand; the per-token decay goes on
-// the wave's own value (dO) columns, split hi/lo:
+// Pre: per superchunk, D_J = sum_c (decay after c) (K~_c)^T V_c (forward, and
+// its replay in the backward), or E_J = sum_t exp(B_t) q_t dO_t^T (backward,
+// B superchunk-local, inclusive).  Wave w owns NCT state column tiles.  The key
+// (query) tile is read through transposing loads as the exact shared operand;
+// the per-token factor goes on the wave's own value (dO) columns, split hi/lo:
 //   D[k][col] = gam D[k][col] + sum_s K[s][k] (exp2(b63 - b_s) V[s][col])
-// EONLY (backward from kept superchunk states): E_J alone, with the forward
-// form's layout: q in the key role, dO in the value role and the weights
-// exp2(off + b_t) in place of the decay, no per-chunk decay of the sum.  Per
-// element its products are the BWD form's E products in the same order.
-template <typename T, int D, int NCT, bool BWD, bool EONLY = false>
+//   E[k][col] =                 sum_t Q[t][k] (exp2(off + b_t) dO[t][col])
+// with off the log2 decay of the superchunk's earlier chunks (E: EONLY).
+template <typename T, int D, int NCT, bool EONLY>
 __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_prep(SegArgs a) {
-    static_assert(!(BWD && EONLY), "EONLY is a form of the forward layout");
     constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
     constexpr int LDN = D + pad<T>(), SWX = swx<T, D>();
     constexpr bool SPD = kSplitDecay<T>;
-    __shared__ __attribute__((aligned(16))) T sK[C * LDN];
-    __shared__ __attribute__((aligned(16))) T sV[C * LDN];
-    __shared__ __attribute__((aligned(16))) T sQ[BWD ? C * LDN : 8];
-    __shared__ __attribute__((aligned(16))) T sO[BWD ? C * LDN : 8];
-    __shared__ __attribute__((aligned(16))) float se[C];   // exp2(b63 - b_s)
-    __shared__ __attribute__((aligned(16))) float sqs[BWD ? C : 4];  // exp2(off + b_t)
+    __shared__ __attribute__((aligned(16))) T sK[C * LDN];  // k (q for E)
+    __shared__ __attribute__((aligned(16))) T sV[C * LDN];  // v (dO for E)
+    __shared__ __attribute__((aligned(16))) float se[C];    // the per-token factor
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
     const Decode d = decode(a);
-    const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
+    const LaneOff tro = tr_off<T, LDN, SWX>(lane);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *K = (const T *)(EONLY ? a.q : a.k) + xo;
     const T *V = (const T *)(EONLY ? a.dO : a.v) + xo;
-    const T *Q = (const T *)a.q + xo;
-    const T *dO = (const T *)a.dO + xo;
     const float *gp = a.g + d.b * a.sg_b + d.h * a.sg_h + d.tok0 * a.sg_l;
 
-    f32x4 Ds[NCT][NK], Es[BWD ? NCT : 1][NK];
+    f32x4 Ds[NCT][NK];
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-        for (int i = 0; i < NK; ++i) {
-            Ds[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-            if constexpr (BWD) Es[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
+        for (int i = 0; i < NK; ++i) Ds[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    Tile<T, D, NT> tk, tv, tq, to;
+    Tile<T, D, NT> tk, tv;
     float gl;
     auto issue = [&](int c) {
         const int64_t nx = (int64_t)c * C * a.sx_l;
         tk.load(K + nx, a.sx_l, tid);
         tv.load(V + nx, a.sx_l, tid);
-        if constexpr (BWD) {
-            tq.load(Q + nx, a.sx_l, tid);
-            to.load(dO + nx, a.sx_l, tid);
-        }
         gl = gp[(c * C + lane) * a.sg_l];
     };
     issue(0);
@@ -101,20 +84,13 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 
     const unsigned par = pair_parity(a.n_cu);
     for (int c = 0; c < d.nch; ++c) {
-        if constexpr (!BWD) pair_turn(par);  // the backward form runs one workgroup per CU
+        pair_turn(par);
         const float b2 = wave_scan_dpp(gl * LOG2E);
         const float b63 = lane_value(b2, 63);
         __syncthreads();
-        if (w == 0) {
-            se[lane] = EONLY ? fexp2(off + b2) : fexp2(b63 - b2);
-            if constexpr (BWD) sqs[lane] = fexp2(off + b2);
-        }
+        if (w == 0) se[lane] = EONLY ? fexp2(off + b2) : fexp2(b63 - b2);
         tk.store_swz(sK, LDN, tid, SWX);
         tv.store_swz(sV, LDN, tid, SWX);
-        if constexpr (BWD) {
-            tq.store_swz(sQ, LDN, tid, SWX);
-            to.store_swz(sO, LDN, tid, SWX);
-        }
         if (c + 1 < d.nch) issue(c + 1);
         __syncthreads();
         if constexpr (!EONLY) {
@@ -130,47 +106,28 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             const f32x4 e0 = *reinterpret_cast<const f32x4 *>(&se[s0]);
             const f32x4 e1 = *reinterpret_cast<const f32x4 *>(&se[s0 + 4]);
             const float ev[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
-            frag_t<T> vh[NCT], vl[NCT], oh[BWD ? NCT : 1], ol[BWD ? NCT : 1];
-            float qv[8];
-            if constexpr (BWD) {
-                const f32x4 u0 = *reinterpret_cast<const f32x4 *>(&sqs[s0]);
-                const f32x4 u1 = *reinterpret_cast<const f32x4 *>(&sqs[s0 + 4]);
-                qv[0] = u0[0]; qv[1] = u0[1]; qv[2] = u0[2]; qv[3] = u0[3];
-                qv[4] = u1[0]; qv[5] = u1[1]; qv[6] = u1[2]; qv[7] = u1[3];
-            }
+            frag_t<T> vh[NCT], vl[NCT];
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) {
-                const int c0 = 16 * (NCT * w + ct);
-                split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sV, tro, 32 * ks, c0), ev, vh[ct], vl[ct]);
-                if constexpr (BWD) split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sO, tro, 32 * ks, c0), qv, oh[ct], ol[ct]);
-            }
+            for (int ct = 0; ct < NCT; ++ct)
+                split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sV, tro, 32 * ks, 16 * (NCT * w + ct)), ev, vh[ct], vl[ct]);
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
                 const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sK, tro, 32 * ks, 16 * i);
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) mma2b<T, SPD>(Ds[ct][i], kf, vh[ct], vl[ct]);
-                if constexpr (BWD) {
-                    const frag_t<T> qf = ldfragTR<T, LDN, SWX>(sQ, tro, 32 * ks, 16 * i);
-#pragma unroll
-                    for (int ct = 0; ct < NCT; ++ct) mma2b<T, SPD>(Es[ct][i], qf, oh[ct], ol[ct]);
-                }
             }
         }
         off += b63;
     }
     const int64_t so = ((int64_t)d.bh * a.n_super + d.J) * D * D;
-    float *dstD = EONLY ? a.wsE : a.wsS;
+    float *dst = EONLY ? a.wsE : a.wsS;
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct) {
         const int c0 = 16 * (NCT * w + ct);
 #pragma unroll
         for (int i = 0; i < NK; ++i)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t e = so + (int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16;
-                dstD[e] = Ds[ct][i][r];
-                if constexpr (BWD) a.wsE[e] = Es[ct][i][r];
-            }
+            for (int r = 0; r < 4; ++r) dst[so + (int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = Ds[ct][i][r];
     }
     if (!EONLY && tid == 0) a.wsLg[(int64_t)d.bh * a.n_super + d.J] = off;
 }
@@ -915,14 +872,15 @@ __global__ void __launch_bounds__(SCAN_NT) k_state_copy(const float *src, float 
 template <typename T, int D>
 static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     const dim3 grid((unsigned)((int64_t)a.B * a.H * a.n_super));
-    constexpr int NTP = 64 * D / (16 * SF_NCT_PREP), NTB = 64 * D / (16 * SF_NCT_PREPB);
+    constexpr int NTP = 64 * D / (16 * SF_NCT_PREP);
     constexpr int NTW = 64 * D / (16 * SF_NCT_WALK);
     switch (kind) {
     case SF_K_FWD_PREP: hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, false>), grid, dim3(NTP), 0, s, e0, e1, 0, a); break;
     case SF_K_FWD_OUT: hipExtLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, false>), grid, dim3(NTW), 0, s, e0, e1, 0, a); break;
-    case SF_K_BWD_PREP:
-        if (a.ckpt) hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, false, true>), grid, dim3(NTP), 0, s, e0, e1, 0, a);
-        else hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREPB, true>), grid, dim3(NTB), 0, s, e0, e1, 0, a);
+    case SF_K_BWD_PREP:  // the replay of D_J (the forward's prep), skipped for kept states, then E_J
+        if (!a.ckpt) hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, false>), grid, dim3(NTP), 0, s, e0, nullptr, 0, a);
+        hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, true>), grid, dim3(NTP), 0, s, a.ckpt ? e0 : nullptr,
+                              e1, 0, a);
         break;
     case SF_K_BWD_DQ: hipExtLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, true>), grid, dim3(NTW), 0, s, e0, e1, 0, a); break;
     case SF_K_BWD_DKV:
