@@ -34,7 +34,8 @@
  *    SF_F32 (fp32 arithmetic throughout, fp32 matrix cores) or SF_BF16
  *    (bf16 MFMA operands, fp32 accumulation and fp32 state).
  *  - Supported (v1): Dk == Dv in {64, 128}; chunk == 64 (0 selects 64);
- *    L % 64 == 0; SF_F32 needs Dk <= 64; pointers 16-byte aligned, strides a
+ *    L % 64 == 0; SF_F32 with the per-channel gate needs Dk <= 64 (the scalar
+ *    gate takes both head dims); pointers 16-byte aligned, strides a
  *    multiple of 16 bytes; 64 consecutive tokens of a tensor span < 2 GiB
  *    (63 * sx_l + Dk elements).  Anything else is rejected before any launch.
  *  - Errors.  Validation failures return a status synchronously and launch

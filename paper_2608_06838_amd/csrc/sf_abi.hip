@@ -115,8 +115,8 @@ sf_status resolve(const sf_shape *sh, Shape &r) {
     if (sh->chunk != 0 && sh->chunk != 64)
         return fail(SF_E_UNSUPPORTED, "chunk must be 64 (got %d)", sh->chunk);
     if (sh->L % 64 != 0) return fail(SF_E_SHAPE, "L must be a multiple of 64 (got %lld)", (long long)sh->L);
-    if (sh->io_dtype == SF_F32 && sh->Dk > 64)
-        return fail(SF_E_UNSUPPORTED, "fp32 I/O supports Dk <= 64 (got %d)", sh->Dk);
+    if (sh->io_dtype == SF_F32 && sh->Dk > 64 && sh->gate == SF_GATE_VECTOR)
+        return fail(SF_E_UNSUPPORTED, "fp32 I/O with the per-channel gate supports Dk <= 64 (got %d)", sh->Dk);
     r.B = sh->B;
     r.H = sh->H;
     r.D = sh->Dk;

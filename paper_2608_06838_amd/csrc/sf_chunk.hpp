@@ -34,10 +34,11 @@ struct Decode {
     int J, bh, b, h, nch;
     int64_t tok0;
 };
-__device__ __forceinline__ Decode decode(const SegArgs &a) {
+// item = (batch * H + head) * n_super + superchunk
+__device__ __forceinline__ Decode decode(const SegArgs &a, int item) {
     Decode d;
-    d.J = blockIdx.x % a.n_super;
-    d.bh = blockIdx.x / a.n_super;
+    d.J = item % a.n_super;
+    d.bh = item / a.n_super;
     d.b = d.bh / a.H;
     d.h = d.bh % a.H;
     d.tok0 = (int64_t)d.J * a.ts;
@@ -45,5 +46,6 @@ __device__ __forceinline__ Decode decode(const SegArgs &a) {
     d.nch = (int)((rem < a.ts ? rem : a.ts) / C);
     return d;
 }
+__device__ __forceinline__ Decode decode(const SegArgs &a) { return decode(a, (int)blockIdx.x); }
 
 }  // namespace sf

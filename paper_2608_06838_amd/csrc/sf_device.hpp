@@ -426,9 +426,10 @@ constexpr int swx() { return (D * (int)sizeof(T) >= 256 ? 128 : 64) / (int)sizeo
 __device__ __forceinline__ int swz_col(int row, int col, int swx) { return col ^ (((row >> 3) & 1) * swx); }
 
 // Per-lane element offsets into a swizzled natural tile.  Every row a lane
-// touches in a fragment read has the same bit 3, so the swizzle reduces to
-// +swx for channel blocks below swx and -swx above it: two offsets per lane,
-// and each fragment address is one of them plus a compile-time constant.
+// touches in a fragment read has the same bit 3, and every channel of a
+// fragment the same swx bit, so the swizzle reduces to +swx for channel blocks
+// with that bit clear and -swx where it is set: two offsets per lane, and each
+// fragment address is one of them plus a compile-time constant.
 struct LaneOff {
     int lo, hi;
 };
@@ -452,7 +453,7 @@ __device__ __forceinline__ LaneOff swz_off(int lane) {
 // (k0 a multiple of 32, c0 of 16; o = tr_off(lane)).
 template <typename T, int LD, int SWX>
 __device__ __forceinline__ frag_t<T> ldfragTR(const T *M, const LaneOff &o, int k0, int c0) {
-    const int e = (c0 < SWX ? o.lo : o.hi) + k0 * LD + c0;
+    const int e = ((c0 & SWX) ? o.hi : o.lo) + k0 * LD + c0;
     if constexpr (sizeof(T) == 2) {
         typedef short s4 __attribute__((ext_vector_type(4)));
         typedef short s8 __attribute__((ext_vector_type(8)));
@@ -471,7 +472,7 @@ __device__ __forceinline__ frag_t<T> ldfragTR(const T *M, const LaneOff &o, int 
 // row0 a multiple of 16, k0 of 32; o = swz_off(lane)).
 template <typename T, int LD, int SWX>
 __device__ __forceinline__ frag_t<T> ldfrag_swz(const T *M, const LaneOff &o, int row0, int k0) {
-    return *reinterpret_cast<const frag_t<T> *>(M + (k0 < SWX ? o.lo : o.hi) + row0 * LD + k0);
+    return *reinterpret_cast<const frag_t<T> *>(M + ((k0 & SWX) ? o.hi : o.lo) + row0 * LD + k0);
 }
 // Fragment in plain channel order (channels k0 + 8q .. +7) from a tile stored
 // in nat_pos order: the 8 channels sit in two 4-channel runs 8 apart.

@@ -861,6 +861,245 @@ __global__ void __launch_bounds__(128 * D / 16) k_bwd_dkv(SegArgs a) {
     }
 }
 
+// PG with the two roles in workgroups of their own (D/16 waves each), the form
+// used where the one-workgroup walk above does not fit the LDS (fp32 I/O at
+// d = 128: four fp32 tiles and two score tiles need 175 KB).  The v-role
+// workgroup keeps G[k][v] and writes dv; the k-role workgroup keeps G^T[v][k]
+// and writes dk and dg.  Each stages three tiles (q and dO, plus k or v) and
+// its one score tile (A^T or dA^T).  The two workgroups of an item lie 8 apart
+// in dispatch order, which puts them on the same XCD (L2) for their second
+// read of q and dO.  The k role reads k at its dk elements straight from
+// memory for the k.dk dots.  Products and their order are those of k_bwd_dkv.
+template <typename T, int D>
+__global__ void __launch_bounds__(64 * D / 16) k_bwd_dkv_wg(SegArgs a) {
+    constexpr int NW = D / 16, NT = 64 * NW, NK = D / 16;
+    constexpr int LDN = D + pad<T>(), LDT = C + pad<T>(), SWX = swx<T, D>();
+    constexpr bool SP = kSplitScores<T>, SPS = kSplitState<T>, SPD = kSplitDecay<T>;
+    __shared__ __attribute__((aligned(16))) T sQ[C * LDN];   // plain, swizzled
+    __shared__ __attribute__((aligned(16))) T sO[C * LDN];   // dO, plain, swizzled
+    __shared__ __attribute__((aligned(16))) T sX[C * LDN];   // k (v role) or v (k role), plain
+    __shared__ __attribute__((aligned(16))) T sAT[C * LDT];  // A^T (v role) or dA^T (k role), hi
+    __shared__ __attribute__((aligned(16))) T sATl[SP ? C * LDT : 8];
+    __shared__ __attribute__((aligned(16))) float sb[C];   // b_t (log2, chunk-local)
+    __shared__ __attribute__((aligned(16))) float se[C];   // exp2(b63 - b_s)
+    __shared__ __attribute__((aligned(16))) float sq[C];   // exp2(b_t)
+    __shared__ float sred[NW * C];
+
+    const int tid = threadIdx.x, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int blk = (int)blockIdx.x;
+    const bool kside = (blk >> 3) & 1;
+    const int item = (blk >> 4) * 8 + (blk & 7);
+    if (item >= a.B * a.H * a.n_super) return;  // the last group of 8 items is ragged
+    const int c0 = 16 * w;
+    const Decode d = decode(a, item);
+    auto asw = [](int row) { return sizeof(T) == 2 ? 8 * ((row >> 2) & 1) : 0; };
+    auto ldfrag_a = [&](const T *M, int row0, int k0) {
+        return *reinterpret_cast<const frag_t<T> *>(M + (row0 + n16) * LDT + ((k0 + 8 * q4) ^ asw(n16)));
+    };
+    const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
+    const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
+    const T *Q = (const T *)a.q + xo;
+    const T *K = (const T *)a.k + xo;
+    const T *V = (const T *)a.v + xo;
+    const T *dO = (const T *)a.dO + xo;
+    T *Out = (T *)(kside ? a.dk : a.dv) + xo;
+    const int64_t go = d.b * a.sg_b + d.h * a.sg_h + d.tok0 * a.sg_l;
+    const float *gp = a.g + go;
+    float *dgp = a.dg + go;
+    const int64_t SS = (int64_t)D * D;
+    const int ndot = D * D / 256;
+    // role operands: the own-column transposed tile of the intra-chunk product
+    // and of the G update, the shared operand of the G update, and the t side
+    // of the score product (A = Q K^T, dA = dO V^T); sX is the other side of
+    // the scores and the B side of the decayed-state product
+    const T *Own = kside ? sQ : sO;
+    const T *Oth = kside ? sO : sQ;
+    const T *Xt = kside ? sO : sQ;
+
+    const float *gsrc = a.n_super == 1 ? (a.dS_out ? a.dS_out + d.bh * SS : nullptr)
+                                       : a.wsE + ((int64_t)d.bh * a.n_super + d.J) * SS;
+    f32x4 G[NK];  // v role: G[k][v] rows 16i.. of v-tile w; k role: G^T[v][k] rows of k-tile w
+#pragma unroll
+    for (int i = 0; i < NK; ++i) {
+        if (!gsrc) {
+            G[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        } else if (!kside) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) G[i][r] = gsrc[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16];
+        } else {
+            G[i] = *reinterpret_cast<const f32x4 *>(gsrc + (int64_t)(c0 + n16) * D + 16 * i + 4 * q4);
+        }
+    }
+    float carry = 0.f;  // k role, wave 0: decay gradient carried in from later tokens
+    if (kside && w == 0) {
+        const float *dot = a.wsDot + ((int64_t)d.bh * a.n_super + d.J) * ndot;
+        carry = wave_sum(lane < ndot ? dot[lane] : 0.f);
+    }
+    // score tile entries read by the products but above the diagonal stay zero
+    for (int e = tid; e < 512; e += NT) {
+        const int tile = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
+        const int idx = (tile ? (48 + rr) * LDT : (16 + rr) * LDT) + ((tile ? 32 + cc : cc) ^ asw(rr));
+        sAT[idx] = cvt<T>(0.f);
+        if constexpr (SP) sATl[idx] = cvt<T>(0.f);
+    }
+
+    using HT = Tile<T, D, NT>;
+    typedef T vec4T __attribute__((ext_vector_type(4)));
+    HT t1, t2, t3;
+    float gl, rn = 0.f;
+    vec4T kn[4];  // k role: k at this lane's dk elements (tokens 16 st + n16, channels c0 + 4 q4 ..)
+    const int64_t cstep = (int64_t)C * a.sx_l;
+    const uint32_t cspan = chunk_span<T, D>(a.sx_l), gspan = (uint32_t)(((C - 1) * a.sg_l + 1) * 4);
+    uint32_t toff[HT::RPT];
+    HT::offsets(toff, a.sx_l, tid);
+    const uint32_t goff = (uint32_t)(lane * a.sg_l * 4);
+    const uint32_t tstep = (uint32_t)(16 * a.sx_l * (int64_t)sizeof(T));
+    const uint32_t voff = (uint32_t)((n16 * a.sx_l + c0 + 4 * q4) * (int64_t)sizeof(T));
+    const T *LX = kside ? V : K;
+    auto issue_qo = [&](int c) {
+        t1.load_buf(buf_rsrc(Q + c * cstep, cspan), toff, 0);
+        t2.load_buf(buf_rsrc(dO + c * cstep, cspan), toff, 0);
+    };
+    auto issue_x = [&](int c) { t3.load_buf(buf_rsrc(LX + c * cstep, cspan), toff, 0); };
+    auto issue_k = [&](int c) {
+        const rsrc_t rk = buf_rsrc(K + c * cstep, cspan);
+#pragma unroll
+        for (int st = 0; st < 4; ++st) kn[st] = buf_ld<vec4T>(rk, voff, st * tstep);
+    };
+    auto issue_g = [&](int c) {
+        const int64_t ng = (int64_t)c * C * a.sg_l;
+        gl = buf_ld<float>(buf_rsrc(gp + ng, gspan), goff, 0);
+        if (kside) rn = buf_ld<float>(buf_rsrc(dgp + ng, gspan), goff, 0);  // q.dq left in dg by the dq walk
+    };
+    issue_g(d.nch - 1);
+    issue_qo(d.nch - 1);
+    issue_x(d.nch - 1);
+    if (kside) issue_k(d.nch - 1);
+    float rprev = 0.f;  // k role, wave 0: q.dq of the chunk whose dg is still pending
+
+    auto finish_dg = [&](int cp) {
+        float kd = 0.f;
+#pragma unroll
+        for (int jj = 0; jj < NW; ++jj) kd += sred[jj * C + lane];
+        const float suf = wave_incl_suffix(rprev - kd, lane);
+        dgp[((int64_t)cp * C + lane) * a.sg_l] = carry + suf;
+        carry += lane_value(suf, 0);
+    };
+
+    for (int c = d.nch - 1; c >= 0; --c) {
+        const float b2 = wave_scan_dpp(gl * LOG2E);
+        const float b63 = lane_value(b2, 63);
+        const float rc = rn;
+        __syncthreads();
+        t1.store_swz(sQ, LDN, tid, SWX);
+        t2.store_swz(sO, LDN, tid, SWX);
+        t3.store_swz(sX, LDN, tid, 0);
+        if (kside && w == 0) {
+            if (c < d.nch - 1) finish_dg(c + 1);
+            rprev = rc;
+        }
+        if (w == NW - 1) {  // the decay tables, from another wave than the dg finish
+            sb[lane] = b2;
+            se[lane] = fexp2(b63 - b2);
+            sq[lane] = fexp2(b2);
+        }
+        if (c > 0) issue_g(c - 1);
+        __syncthreads();
+        if (c > 0) issue_qo(c - 1);
+
+        // A^T (v role) or dA^T (k role) on the causal tiles: P[t][s] = sum X[t][ch] Y[s][ch]
+        for (int i = w; i < 10; i += NW) {
+            int tt, st;
+            tri_tile(i, tt, st);
+            f32x4 p = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks)
+                mma(p, ldfrag_swz<T, LDN, SWX>(Xt, swo, 16 * tt, 32 * ks), ldfrag(sX, LDN, 16 * st, 32 * ks, lane));
+            const int s = 16 * st + n16;
+            const float bs = sb[s];
+            const f32x4 bt = *reinterpret_cast<const f32x4 *>(&sb[16 * tt + 4 * q4]);
+            float v4[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * tt + 4 * q4 + r;
+                v4[r] = s <= t ? p[r] * fexp2(bt[r] - bs) : 0.f;
+            }
+            const int o = s * LDT + ((16 * tt + 4 * q4) ^ asw(s));
+            st4_split<T, SP>(&sAT[o], &sATl[SP ? o : 0], v4);
+        }
+        __syncthreads();
+        if (c > 0) issue_x(c - 1);
+
+        // decayed state part: out^T[col][s] += G^T X^T over the wave's 16 columns
+        f32x4 DX[4];
+#pragma unroll
+        for (int st = 0; st < 4; ++st) DX[st] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) {
+            frag_t<T> xfr[4];
+#pragma unroll
+            for (int st = 0; st < 4; ++st) xfr[st] = ldfrag(sX, LDN, 16 * st, 32 * ks, lane);
+            frag_t<T> gh, glo;
+            split_acc_plain<T, SPS>(G[2 * ks], G[2 * ks + 1], gh, glo);
+#pragma unroll
+            for (int st = 0; st < 4; ++st) mma2<T, SPS>(DX[st], gh, glo, xfr[st]);
+        }
+        const frag_t<T> of0 = ldfragTR<T, LDN, SWX>(Own, tro, 0, c0), of1 = ldfragTR<T, LDN, SWX>(Own, tro, 32, c0);
+#pragma unroll
+        for (int st = 0; st < 4; ++st) DX[st] *= se[16 * st + n16];
+        // intra-chunk part: dv^T += dO^T A^T (v role), dk^T += Q^T dA^T (k role),
+        // over the (st, ks) pairs whose score block is not above the diagonal
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+#pragma unroll
+            for (int ks = st / 2; ks < C / 32; ++ks) {
+                const frag_t<T> &ofk = ks ? of1 : of0;
+                mma(DX[st], ofk, ldfrag_a(sAT, 16 * st, 32 * ks));
+                if constexpr (SP) mma(DX[st], ofk, ldfrag_a(sATl, 16 * st, 32 * ks));
+            }
+        const rsrc_t ro = buf_rsrc(Out + c * cstep, cspan);
+#pragma unroll
+        for (int st = 0; st < 4; ++st) st4_buf<T>(ro, voff, st * tstep, DX[st]);
+        if (kside) {  // k.dk partials of this wave's 16 channels, then the next chunk's k
+#pragma unroll
+            for (int st = 0; st < 4; ++st) {
+                float kd = 0.f;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) kd += DX[st][r] * tof<T>(kn[st][r]);
+                kd = sum_rows(kd);
+                if (q4 == 0) sred[w * C + 16 * st + n16] = kd;
+            }
+            if (c > 0) issue_k(c - 1);
+        }
+
+        // G <- exp2(b63) G + Q^T (exp2(b) o dO) (v role), G^T <- exp2(b63) G^T + dO^T (exp2(b) o Q) (k role)
+        const float gam = fexp2(b63);
+#pragma unroll
+        for (int i = 0; i < NK; ++i) G[i] *= gam;
+#pragma unroll
+        for (int ks = 0; ks < C / 32; ++ks) {
+            const int t0 = 32 * ks + 8 * q4;
+            const f32x4 e0 = *reinterpret_cast<const f32x4 *>(&sq[t0]);
+            const f32x4 e1 = *reinterpret_cast<const f32x4 *>(&sq[t0 + 4]);
+            const float ev[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
+            frag_t<T> oh, ol;
+            split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(Own, tro, 32 * ks, c0), ev, oh, ol);
+#pragma unroll
+            for (int i = 0; i < NK; ++i) mma2b<T, SPD>(G[i], ldfragTR<T, LDN, SWX>(Oth, tro, 32 * ks, 16 * i), oh, ol);
+        }
+    }
+    __syncthreads();
+    if (kside && w == 0 && d.nch > 0) finish_dg(0);
+    if (a.n_super == 1 && a.dS_in && !kside) {
+        float *dst = a.dS_in + d.bh * SS;
+#pragma unroll
+        for (int i = 0; i < NK; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = G[i][r];
+    }
+}
+
 // Boundary state of an empty segment: dst = src, or zero when src is NULL.
 __global__ void __launch_bounds__(SCAN_NT) k_state_copy(const float *src, float *dst, int64_t n) {
     const int64_t i = (int64_t)blockIdx.x * SCAN_NT + threadIdx.x;
@@ -884,7 +1123,13 @@ static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s, hipEvent_
         break;
     case SF_K_BWD_DQ: hipExtLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, true>), grid, dim3(NTW), 0, s, e0, e1, 0, a); break;
     case SF_K_BWD_DKV:
-        hipExtLaunchKernelGGL((k_bwd_dkv<T, D>), grid, dim3(128 * D / 16), 0, s, e0, e1, 0, a);
+        if constexpr (sizeof(T) == 4 && D == 128) {  // two workgroups per item, 8 apart in dispatch order
+            const int64_t items = (int64_t)a.B * a.H * a.n_super;
+            hipExtLaunchKernelGGL((k_bwd_dkv_wg<T, D>), dim3((unsigned)((items + 7) / 8 * 16)), dim3(64 * D / 16), 0, s,
+                                  e0, e1, 0, a);
+        } else {
+            hipExtLaunchKernelGGL((k_bwd_dkv<T, D>), grid, dim3(128 * D / 16), 0, s, e0, e1, 0, a);
+        }
         break;
     default: return hipErrorInvalidValue;
     }
@@ -907,6 +1152,7 @@ hipError_t launch_kernel(int kind, int io, int D, const SegArgs &a, hipStream_t 
     if (io == SF_BF16 && D == 128) return launch_td<__bf16, 128>(kind, a, s, e0, e1);
     if (io == SF_BF16 && D == 64) return launch_td<__bf16, 64>(kind, a, s, e0, e1);
     if (io == SF_F32 && D == 64) return launch_td<float, 64>(kind, a, s, e0, e1);
+    if (io == SF_F32 && D == 128) return launch_td<float, 128>(kind, a, s, e0, e1);
     return hipErrorInvalidValue;
 }
 

@@ -87,7 +87,7 @@ def fwd(s, q=1, k=2, v=3, g=4, S_in=None, o=5, S_out=6, ws=7, ws_bytes=1 << 30, 
     (dict(chunk=32), _lib.SF_E_UNSUPPORTED),
     (dict(io_dtype=7), _lib.SF_E_DTYPE),
     (dict(gate=5), _lib.SF_E_DTYPE),
-    (dict(io_dtype=_lib.SF_F32, Dk=128, Dv=128), _lib.SF_E_UNSUPPORTED),
+    (dict(io_dtype=_lib.SF_F32, Dk=128, Dv=128, gate=_lib.SF_GATE_VECTOR), _lib.SF_E_UNSUPPORTED),
     (dict(reserved=1), _lib.SF_E_SHAPE),
     (dict(sx_b=1024 * 2 * 128, sx_l=100, sx_h=128), _lib.SF_E_SHAPE),   # rows overlap
     (dict(sx_b=1024 * 2 * 136, sx_l=2 * 136, sx_h=132), _lib.SF_E_ALIGN),  # 264-byte head stride
@@ -97,6 +97,16 @@ def fwd(s, q=1, k=2, v=3, g=4, S_in=None, o=5, S_out=6, ws=7, ws_bytes=1 << 30, 
 def test_shape_validation(kw, status):
     assert fwd(shape(**kw)) == status
     assert _lib.lib().sf_last_error() != b""
+
+
+def test_fp32_d128_scalar_gate_accepted():
+    """fp32 I/O at d = 128 takes the scalar gate: validation passes up to the
+    workspace check (no launch: a too-small workspace is reported)."""
+    t = _lib.SfTuning()
+    t.ts = 128
+    s = shape(io_dtype=_lib.SF_F32, Dk=128, Dv=128)
+    assert fwd(s, ws_bytes=16, tun=t) == _lib.SF_E_WORKSPACE
+    assert _lib.lib().sf_fwd_workspace_bytes(ctypes.byref(s), ctypes.byref(t)) > 0
 
 
 def test_pointer_validation():

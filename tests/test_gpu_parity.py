@@ -75,6 +75,33 @@ def test_bf16_segment_paths(D, ts):
     check_all("bf16", got, oracle_run(inp), inp)
 
 
+@pytest.mark.parametrize("ts", [1024, 128, 192])
+def test_fp32_d128_segment(ts):
+    """fp32 I/O at d = 128 (scalar gate; its dk/dv walk runs as two workgroups
+    per superchunk): B=1, H=2, L=1024 as one superchunk, eight, and a ragged
+    192-token split, with S_in and dS_out; fp32 bar."""
+    w = synth.workload("tiny_fp32", D=128)
+    inp, got = seg_case(w, 1024, ts, seed=1200 + ts, dS_std=0.1, s_in_std=0.1)
+    check_all("f32", got, oracle_run(inp), inp)
+
+
+@pytest.mark.parametrize("ts", [0, 64])
+def test_fp32_d128_chain(ts):
+    """fp32 I/O at d = 128 over four nonuniform segments: overlap on and off and
+    kept superchunk states give bitwise the same outputs; fp32 bar."""
+    w = synth.workload("tiny_fp32", B=1, H=3, D=128)
+    seg_lens = [192, 64, 320, 128]
+    inp = synth.make_inputs(w, device="cpu", seed=1210 + ts, dS_out_std=0.1, L=sum(seg_lens))
+    g = on_gpu(inp)
+    say(f"[chain] fp32 d=128 ts={ts}")
+    a = run_chain(g, seg_lens, ts=ts, overlap=True)
+    for kw in (dict(overlap=False), dict(overlap=True, keep=True)):
+        b = run_chain(g, seg_lens, ts=ts, **kw)
+        for key in a:
+            assert torch.equal(a[key], b[key]), (key, kw)
+    check_chain("f32", inp, a, seg_lens)
+
+
 def test_fp32_strong_decay_and_memoryless():
     """Very negative gates (a_t -> 0): each token sees only itself."""
     w = synth.workload("tiny_fp32", g_mu=-30.0)
