@@ -279,6 +279,34 @@ def test_vector_gate_workload_sampled():
     check_chain("bf16", inp, got, w["seg_lens"], pairs=[(0, 5), (1, 12)])
 
 
+@pytest.mark.parametrize("gate", ["scalar", "vector"])
+def test_head_major_layout(gate):
+    """q, k, v, dO stored head-major ([B, H, L, D] in memory) and g as [B, H, L]
+    (vector gate: [B, H, L, D]), passed as [B, L, H, ...] views: the strides go
+    through the ABI, the outputs come back in the same layout, every value is
+    bitwise that of the packed layout, and the oracle bar holds (chained
+    nonuniform segments, several superchunks)."""
+    name = "vector_gate" if gate == "vector" else "mid_bf16"
+    w = synth.workload(name, B=2, H=3, D=128)
+    seg_lens = [192, 64, 320]
+    inp = synth.make_inputs(w, device="cpu", seed=61, dS_out_std=0.1, L=sum(seg_lens))
+    say(f"[chain] head-major layout, {gate} gate")
+
+    def hm(x):  # the same values in head-major memory
+        p = (0, 2, 1, 3) if x.dim() == 4 else (0, 2, 1)
+        return x.permute(*p).contiguous().permute(*p).to(DEV)
+
+    g = on_gpu(inp)
+    h = dict(g, **{n: hm(inp[n]) for n in ("q", "k", "v", "g", "dO")})
+    assert h["q"].stride(2) == sum(seg_lens) * 128 and h["q"].stride(1) == 128
+    a = run_chain(g, seg_lens, ts=128)
+    b = run_chain(h, seg_lens, ts=128)
+    assert b["o"].stride() == h["q"].stride() and b["dg"].stride() == h["g"].stride()
+    for key in a:
+        assert torch.equal(a[key].contiguous(), b[key].contiguous()), key
+    check_chain("bf16", inp, b, seg_lens)
+
+
 def test_tuned_setting_is_applied(monkeypatch):
     """chain_fwd / chain_bwd with ts and overlap left unset take the profiled
     per-shape setting (paper_2608_06838_amd.tuned): bitwise the outputs of
