@@ -441,6 +441,14 @@ __device__ __forceinline__ LaneOff tr_off(int lane) {
     const int base = sizeof(T) == 2 ? (8 * q + (a >> 2)) * LD + 4 * (a & 3) : 8 * q * LD + a;
     return {base + S, base - S};
 }
+// for ldfragTR with channel runs 8 apart (bf16): rows k0 + 8q + (a / 4) (+4),
+// channels c0 + 8 (a % 4), so fragment row n is channel c0 + 8 (n / 4) + n % 4
+template <typename T, int LD, int SWX>
+__device__ __forceinline__ LaneOff tr_off8(int lane) {
+    const int q = lane >> 4, a = lane & 15, S = (q & 1) * SWX;
+    const int base = (8 * q + (a >> 2)) * LD + 8 * (a & 3);  // (16-bit tiles only)
+    return {base + S, base - S};
+}
 // for ldfrag_swz: rows row0 + n, channels k0 + 8q .. +7
 template <typename T, int LD, int SWX>
 __device__ __forceinline__ LaneOff swz_off(int lane) {

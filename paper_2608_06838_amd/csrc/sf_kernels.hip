@@ -38,6 +38,9 @@ constexpr int SCAN_NT = 256;
 #ifndef SF_NCT_WALK
 #define SF_NCT_WALK 2
 #endif
+#ifndef SF_NCT_DKV
+#define SF_NCT_DKV 2
+#endif
 
 // ---------------------------------------------------------------------------
 // Pre: per superchunk, D_J = sum_c (decay after c) (K~_c)^T V_c (forward, and
@@ -284,6 +287,13 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
     const Decode d = decode(a);
     const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
+    // bf16: the state's rows are read into the update's A operands in the order
+    // that puts channels 8q..8q+7 of each 32-channel block in lane row q of the
+    // accumulator pair (2m, 2m+1), the plain order of the Q.S operand: row r of
+    // tile i holds channel srow(i, r), and the pair splits with no lane swaps
+    constexpr bool RP = sizeof(T) == 2;
+    const LaneOff tro8 = RP ? tr_off8<T, LDN, SWX>(lane) : tro;  // (tr_off8 serves 16-bit tiles only)
+    auto srow = [&](int i, int r) { return RP ? 32 * (i >> 1) + 8 * q4 + 4 * (i & 1) + r : 16 * i + 4 * q4 + r; };
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *X1 = (const T *)(DQ ? a.dO : a.q) + xo;
     const T *X2 = (const T *)(DQ ? a.v : a.k) + xo;
@@ -303,14 +313,14 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
         for (int i = 0; i < NK; ++i) {
-            const int col = 16 * (NCT * w + ct) + n16, row = 16 * i + 4 * q4;
+            const int col = 16 * (NCT * w + ct) + n16;
             if (!src) {
                 S[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
             } else if constexpr (!DQ) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) S[ct][i][r] = src[(int64_t)(row + r) * D + col];
+                for (int r = 0; r < 4; ++r) S[ct][i][r] = src[(int64_t)srow(i, r) * D + col];
             } else {
-                S[ct][i] = *reinterpret_cast<const f32x4 *>(src + (int64_t)col * D + row);
+                S[ct][i] = *reinterpret_cast<const f32x4 *>(src + (int64_t)col * D + srow(i, 0));
             }
         }
     typedef T vec4T __attribute__((ext_vector_type(4)));
@@ -442,7 +452,10 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         for (int ks = 0; ks < D / 32; ++ks) {
             frag_t<T> fh[NCT], fl[NCT];
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) split_acc_plain<T, SPS>(S[ct][2 * ks], S[ct][2 * ks + 1], fh[ct], fl[ct]);
+            for (int ct = 0; ct < NCT; ++ct) {
+                if constexpr (RP) split_acc<T, SPS>(S[ct][2 * ks], S[ct][2 * ks + 1], fh[ct], fl[ct]);
+                else split_acc_plain<T, SPS>(S[ct][2 * ks], S[ct][2 * ks + 1], fh[ct], fl[ct]);
+            }
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
                 const frag_t<T> xf = ldfrag(sX1, LDN, 16 * tt, 32 * ks, lane);
@@ -517,7 +530,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
                 split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sX3, tro, 32 * ks, 16 * (NCT * w + ct)), ev, vh[ct], vl[ct]);
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
-                const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sX2, tro, 32 * ks, 16 * i);
+                const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sX2, tro8, 32 * ks, RP ? 32 * (i >> 1) + 4 * (i & 1) : 16 * i);
 #pragma unroll
                 for (int ct = 0; ct < NCT; ++ct) mma2b<T, SPD>(S[ct][i], kf, vh[ct], vl[ct]);
             }
@@ -547,7 +560,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
                     for (int i = 0; i < NK; ++i)
 #pragma unroll
                         for (int r = 0; r < 4; ++r)
-                            dst[(int64_t)(16 * i + 4 * q4 + r) * D + 16 * (NCT * w + ct) + n16] = S[ct][i][r];
+                            dst[(int64_t)srow(i, r) * D + 16 * (NCT * w + ct) + n16] = S[ct][i][r];
             }
         } else {
             // <dS_out, S_out> for dg (the state here is S_out^T)
@@ -559,7 +572,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 #pragma unroll
                     for (int i = 0; i < NK; ++i) {
                         const f32x4 x = *reinterpret_cast<const f32x4 *>(
-                            ds + (int64_t)(16 * (NCT * w + ct) + n16) * D + 16 * i + 4 * q4);
+                            ds + (int64_t)(16 * (NCT * w + ct) + n16) * D + srow(i, 0));
                         p += x[0] * S[ct][i][0] + x[1] * S[ct][i][1] + x[2] * S[ct][i][2] + x[3] * S[ct][i][3];
                     }
             }
@@ -591,9 +604,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 // reordered by split_acc_plain), Q and dO plain and swizzled for the
 // transposing loads of the G updates, where the per-token decay goes on the
 // wave's own columns.
-template <typename T, int D>
-__global__ void __launch_bounds__(128 * D / 16) k_bwd_dkv(SegArgs a) {
-    constexpr int NJ = D / 16, NW = 2 * NJ, NT = 64 * NW, NH = NT / 2, NK = D / 16;
+template <typename T, int D, int NCT>
+__global__ void __launch_bounds__(128 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
+    constexpr int NJ = D / (16 * NCT), NW = 2 * NJ, NT = 64 * NW, NH = NT / 2, NK = D / 16;
     constexpr int LDN = D + pad<T>(), LDT = C + pad<T>(), SWX = swx<T, D>();
     constexpr bool SP = kSplitScores<T>, SPS = kSplitState<T>, SPD = kSplitDecay<T>;
     __shared__ __attribute__((aligned(16))) T sQ[C * LDN];   // plain, swizzled
@@ -614,7 +627,7 @@ __global__ void __launch_bounds__(128 * D / 16) k_bwd_dkv(SegArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bool kside = w >= NJ;
-    const int j = kside ? w - NJ : w, c0 = 16 * j, htid = kside ? tid - NH : tid;
+    const int j = kside ? w - NJ : w, c0 = 16 * NCT * j, htid = kside ? tid - NH : tid;
     const Decode d = decode(a);
     // score tiles XOR their 16-byte blocks by bit 2 of the row (bf16): the 8-byte
     // accumulator-row writes then spread over twice the banks
@@ -623,6 +636,14 @@ __global__ void __launch_bounds__(128 * D / 16) k_bwd_dkv(SegArgs a) {
         return *reinterpret_cast<const frag_t<T> *>(M + (row0 + n16) * LDT + ((k0 + 8 * q4) ^ asw(n16)));
     };
     const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
+    // bf16: the rows of G (v-side; of G^T on the k-side) are read into the
+    // update's A operands in the order that puts channels 8q..8q+7 of each
+    // 32-channel block in lane row q of the accumulator pair (2m, 2m+1), the
+    // plain order of the decayed-state product's operand: row r of tile i holds
+    // channel grow(i, r), and the pair splits with no lane swaps
+    constexpr bool RP = sizeof(T) == 2;
+    const LaneOff tro8 = RP ? tr_off8<T, LDN, SWX>(lane) : tro;  // (tr_off8 serves 16-bit tiles only)
+    auto grow = [&](int i, int r) { return RP ? 32 * (i >> 1) + 8 * q4 + 4 * (i & 1) + r : 16 * i + 4 * q4 + r; };
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *Q = (const T *)a.q + xo;
     const T *K = (const T *)a.k + xo;
@@ -645,18 +666,22 @@ __global__ void __launch_bounds__(128 * D / 16) k_bwd_dkv(SegArgs a) {
 
     const float *gsrc = a.n_super == 1 ? (a.dS_out ? a.dS_out + d.bh * SS : nullptr)
                                        : a.wsE + ((int64_t)d.bh * a.n_super + d.J) * SS;
-    f32x4 G[NK];  // v-side: G[k][v] rows 16i.. of v-tile j; k-side: G^T[v][k] rows of k-tile j
+    // v-side: G[k][v] rows 16i.. of the wave's v-tiles; k-side: G^T[v][k] rows of its k-tiles
+    f32x4 G[NCT][NK];
 #pragma unroll
-    for (int i = 0; i < NK; ++i) {
-        if (!gsrc) {
-            G[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        } else if (!kside) {
+    for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) G[i][r] = gsrc[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16];
-        } else {
-            G[i] = *reinterpret_cast<const f32x4 *>(gsrc + (int64_t)(c0 + n16) * D + 16 * i + 4 * q4);
+        for (int i = 0; i < NK; ++i) {
+            const int col = c0 + 16 * ct + n16;
+            if (!gsrc) {
+                G[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+            } else if (!kside) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) G[ct][i][r] = gsrc[(int64_t)grow(i, r) * D + col];
+            } else {
+                G[ct][i] = *reinterpret_cast<const f32x4 *>(gsrc + (int64_t)col * D + grow(i, 0));
+            }
         }
-    }
     float carry = 0.f;  // wave 0: decay gradient carried in from later tokens
     if (w == 0) {
         const float *dot = a.wsDot + ((int64_t)d.bh * a.n_super + d.J) * ndot;
@@ -765,25 +790,42 @@ __global__ void __launch_bounds__(128 * D / 16) k_bwd_dkv(SegArgs a) {
         // priority (the step measured 0.8% faster, the walk 7%)
         if (kside) __builtin_amdgcn_s_setprio(2);
 
-        // decayed state part: out^T[col][s] += G^T X^T over the wave's 16 columns
-        f32x4 DX[4];
+        // decayed state part: out^T[col][s] += G^T X^T over the wave's 16 NCT columns
+        f32x4 DX[NCT][4];
 #pragma unroll
-        for (int st = 0; st < 4; ++st) DX[st] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int st = 0; st < 4; ++st) DX[ct][st] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < D / 32; ++ks) {
             frag_t<T> xfr[4];
 #pragma unroll
             for (int st = 0; st < 4; ++st) xfr[st] = ldfrag(Xs, LDN, 16 * st, 32 * ks, lane);
             sched_fence();  // keep the fragment reads ahead of the split below
-            frag_t<T> gh, glo;
-            split_acc_plain<T, SPS>(G[2 * ks], G[2 * ks + 1], gh, glo);
+            frag_t<T> gh[NCT], glo[NCT];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) {
+                if constexpr (RP) split_acc<T, SPS>(G[ct][2 * ks], G[ct][2 * ks + 1], gh[ct], glo[ct]);
+                else split_acc_plain<T, SPS>(G[ct][2 * ks], G[ct][2 * ks + 1], gh[ct], glo[ct]);
+            }
             sched_fence();
 #pragma unroll
-            for (int st = 0; st < 4; ++st) mma2<T, SPS>(DX[st], gh, glo, xfr[st]);
-        }
-        const frag_t<T> of0 = ldfragTR<T, LDN, SWX>(Own, tro, 0, c0), of1 = ldfragTR<T, LDN, SWX>(Own, tro, 32, c0);
+            for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-        for (int st = 0; st < 4; ++st) DX[st] *= se[16 * st + n16];
+                for (int st = 0; st < 4; ++st) mma2<T, SPS>(DX[ct][st], gh[ct], glo[ct], xfr[st]);
+        }
+        frag_t<T> of0[NCT], of1[NCT];
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) {
+            of0[ct] = ldfragTR<T, LDN, SWX>(Own, tro, 0, c0 + 16 * ct);
+            of1[ct] = ldfragTR<T, LDN, SWX>(Own, tro, 32, c0 + 16 * ct);
+        }
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+            const float es = se[16 * st + n16];
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) DX[ct][st] *= es;
+        }
         // intra-chunk part: dv^T += dO^T A^T (v side), dk^T += Q^T dA^T (k side), score
         // tiles zero above the diagonal, over the (st, ks) pairs (0,0) (0,1) (1,0)
         // (1,1) (2,1) (3,1), each pair's fragments read two pairs ahead of its products
@@ -795,9 +837,12 @@ __global__ void __launch_bounds__(128 * D / 16) k_bwd_dkv(SegArgs a) {
             if constexpr (SP) f.l = ldfrag_a(Atl, 16 * st, 32 * ks);
         };
         auto mma_pair = [&](int st, int ks, const AF &f) {
-            const frag_t<T> &ofk = ks ? of1 : of0;
-            mma(DX[st], ofk, f.h);
-            if constexpr (SP) mma(DX[st], ofk, f.l);
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct) {
+                const frag_t<T> &ofk = ks ? of1[ct] : of0[ct];
+                mma(DX[ct][st], ofk, f.h);
+                if constexpr (SP) mma(DX[ct][st], ofk, f.l);
+            }
         };
         {
             AF f0, f1;
@@ -822,12 +867,19 @@ __global__ void __launch_bounds__(128 * D / 16) k_bwd_dkv(SegArgs a) {
         const rsrc_t ro = buf_rsrc(Out + c * cstep, cspan);
         const uint32_t voff = (uint32_t)((n16 * a.sx_l + c0 + 4 * q4) * (int64_t)sizeof(T));
 #pragma unroll
-        for (int st = 0; st < 4; ++st) st4_buf<T>(ro, voff, st * tstep, DX[st]);
-        if (kside) {  // k.dk partials of this wave's 16 channels
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+                st4_buf<T>(ro, voff, st * tstep + 16 * ct * (uint32_t)sizeof(T), DX[ct][st]);
+        if (kside) {  // k.dk partials of this wave's 16 NCT channels
 #pragma unroll
             for (int st = 0; st < 4; ++st) {
-                const f32x4 kv = ld4f(&sK[(16 * st + n16) * LDN + c0 + 4 * q4]);
-                float kd = DX[st][0] * kv[0] + DX[st][1] * kv[1] + DX[st][2] * kv[2] + DX[st][3] * kv[3];
+                float kd = 0.f;
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) {
+                    const f32x4 kv = ld4f(&sK[(16 * st + n16) * LDN + c0 + 16 * ct + 4 * q4]);
+                    kd += DX[ct][st][0] * kv[0] + DX[ct][st][1] * kv[1] + DX[ct][st][2] * kv[2] + DX[ct][st][3] * kv[3];
+                }
                 kd = sum_rows(kd);
                 if (q4 == 0) sred[j * C + 16 * st + n16] = kd;
             }
@@ -837,17 +889,25 @@ __global__ void __launch_bounds__(128 * D / 16) k_bwd_dkv(SegArgs a) {
         // G <- exp2(b63) G + Q^T (exp2(b) o dO) (v side), G^T <- exp2(b63) G^T + dO^T (exp2(b) o Q) (k side)
         const float gam = fexp2(b63);
 #pragma unroll
-        for (int i = 0; i < NK; ++i) G[i] *= gam;
+        for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+            for (int i = 0; i < NK; ++i) G[ct][i] *= gam;
 #pragma unroll
         for (int ks = 0; ks < C / 32; ++ks) {
             const int t0 = 32 * ks + 8 * q4;
             const f32x4 e0 = *reinterpret_cast<const f32x4 *>(&sq[t0]);
             const f32x4 e1 = *reinterpret_cast<const f32x4 *>(&sq[t0 + 4]);
             const float ev[8] = {e0[0], e0[1], e0[2], e0[3], e1[0], e1[1], e1[2], e1[3]};
-            frag_t<T> oh, ol;
-            split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(Own, tro, 32 * ks, c0), ev, oh, ol);
+            frag_t<T> oh[NCT], ol[NCT];
 #pragma unroll
-            for (int i = 0; i < NK; ++i) mma2b<T, SPD>(G[i], ldfragTR<T, LDN, SWX>(Oth, tro, 32 * ks, 16 * i), oh, ol);
+            for (int ct = 0; ct < NCT; ++ct)
+                split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(Own, tro, 32 * ks, c0 + 16 * ct), ev, oh[ct], ol[ct]);
+#pragma unroll
+            for (int i = 0; i < NK; ++i) {
+                const frag_t<T> b = ldfragTR<T, LDN, SWX>(Oth, tro8, 32 * ks, RP ? 32 * (i >> 1) + 4 * (i & 1) : 16 * i);
+#pragma unroll
+                for (int ct = 0; ct < NCT; ++ct) mma2b<T, SPD>(G[ct][i], b, oh[ct], ol[ct]);
+            }
         }
     }
     __syncthreads();
@@ -855,9 +915,11 @@ __global__ void __launch_bounds__(128 * D / 16) k_bwd_dkv(SegArgs a) {
     if (a.n_super == 1 && a.dS_in && !kside) {
         float *dst = a.dS_in + d.bh * SS;
 #pragma unroll
-        for (int i = 0; i < NK; ++i)
+        for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = G[i][r];
+            for (int i = 0; i < NK; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) dst[(int64_t)grow(i, r) * D + c0 + 16 * ct + n16] = G[ct][i][r];
     }
 }
 
@@ -1128,7 +1190,8 @@ static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s, hipEvent_
             hipExtLaunchKernelGGL((k_bwd_dkv_wg<T, D>), dim3((unsigned)((items + 7) / 8 * 16)), dim3(64 * D / 16), 0, s,
                                   e0, e1, 0, a);
         } else {
-            hipExtLaunchKernelGGL((k_bwd_dkv<T, D>), grid, dim3(128 * D / 16), 0, s, e0, e1, 0, a);
+            constexpr int NCT = sizeof(T) == 2 && D == 128 ? SF_NCT_DKV : 1;
+            hipExtLaunchKernelGGL((k_bwd_dkv<T, D, NCT>), grid, dim3(128 * D / (16 * NCT)), 0, s, e0, e1, 0, a);
         }
         break;
     default: return hipErrorInvalidValue;
