@@ -801,14 +801,12 @@ __global__ void __launch_bounds__(128 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
             frag_t<T> xfr[4];
 #pragma unroll
             for (int st = 0; st < 4; ++st) xfr[st] = ldfrag(Xs, LDN, 16 * st, 32 * ks, lane);
-            sched_fence();  // keep the fragment reads ahead of the split below
             frag_t<T> gh[NCT], glo[NCT];
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
                 if constexpr (RP) split_acc<T, SPS>(G[ct][2 * ks], G[ct][2 * ks + 1], gh[ct], glo[ct]);
                 else split_acc_plain<T, SPS>(G[ct][2 * ks], G[ct][2 * ks + 1], gh[ct], glo[ct]);
             }
-            sched_fence();
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
