@@ -17,6 +17,7 @@
 //   k_scan<false>           ST:  S_{J+1} = Gamma_J S_J + D_J (fp32), S_out
 //   k_walk<.., DQ=false>    Out: walk the chunks from S_J, write o
 //   k_prep<.., EONLY=true>  the state-gradient contribution E_J
+//   k_prep_bwd              the backward's replay of D_J and its E_J in one launch
 //   k_scan<true>            ST + STB: S_J forward, G_{J+1} backward, dS_in,
 //                           <G_{J+1}, S_{J+1}> partials for dg
 //   k_walk<.., DQ=true>     dq by a forward walk; also q.dq per token
@@ -51,17 +52,16 @@ constexpr int SCAN_NT = 256;
 //   D[k][col] = gam D[k][col] + sum_s K[s][k] (exp2(b63 - b_s) V[s][col])
 //   E[k][col] =                 sum_t Q[t][k] (exp2(off + b_t) dO[t][col])
 // with off the log2 decay of the superchunk's earlier chunks (E: EONLY).
+// One superchunk (item) of either summary; the LDS tiles come from the kernel:
+// sK (q for E) and sV (dO for E), C x (D + pad), and se, the per-token factor.
 template <typename T, int D, int NCT, bool EONLY>
-__global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_prep(SegArgs a) {
+__device__ __forceinline__ void prep_item(const SegArgs &a, int item, T *sK, T *sV, float *se) {
     constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
     constexpr int LDN = D + pad<T>(), SWX = swx<T, D>();
     constexpr bool SPD = kSplitDecay<T>;
-    __shared__ __attribute__((aligned(16))) T sK[C * LDN];  // k (q for E)
-    __shared__ __attribute__((aligned(16))) T sV[C * LDN];  // v (dO for E)
-    __shared__ __attribute__((aligned(16))) float se[C];    // the per-token factor
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
-    const Decode d = decode(a);
+    const Decode d = decode(a, item);
     const LaneOff tro = tr_off<T, LDN, SWX>(lane);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *K = (const T *)(EONLY ? a.q : a.k) + xo;
@@ -133,6 +133,29 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             for (int r = 0; r < 4; ++r) dst[so + (int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = Ds[ct][i][r];
     }
     if (!EONLY && tid == 0) a.wsLg[(int64_t)d.bh * a.n_super + d.J] = off;
+}
+
+template <typename T, int D, int NCT, bool EONLY>
+__global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_prep(SegArgs a) {
+    constexpr int LDN = D + pad<T>();
+    __shared__ __attribute__((aligned(16))) T sK[C * LDN];
+    __shared__ __attribute__((aligned(16))) T sV[C * LDN];
+    __shared__ __attribute__((aligned(16))) float se[C];
+    prep_item<T, D, NCT, EONLY>(a, (int)blockIdx.x, sK, sV, se);
+}
+
+// The backward's two summaries in one launch: workgroups [0, n) replay D_J,
+// [n, 2n) form E_J (n = B H n_super).  Neither waits for the other, and the
+// last dispatch round of one overlaps the other's work.
+template <typename T, int D, int NCT>
+__global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_prep_bwd(SegArgs a) {
+    constexpr int LDN = D + pad<T>();
+    __shared__ __attribute__((aligned(16))) T sK[C * LDN];
+    __shared__ __attribute__((aligned(16))) T sV[C * LDN];
+    __shared__ __attribute__((aligned(16))) float se[C];
+    const int n = (int)(gridDim.x / 2), item = (int)blockIdx.x;
+    if (item < n) prep_item<T, D, NCT, false>(a, item, sK, sV, se);
+    else prep_item<T, D, NCT, true>(a, item - n, sK, sV, se);
 }
 
 // ---------------------------------------------------------------------------
@@ -1177,9 +1200,10 @@ static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s, hipEvent_
     case SF_K_FWD_PREP: hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, false>), grid, dim3(NTP), 0, s, e0, e1, 0, a); break;
     case SF_K_FWD_OUT: hipExtLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, false>), grid, dim3(NTW), 0, s, e0, e1, 0, a); break;
     case SF_K_BWD_PREP:  // the replay of D_J (the forward's prep), skipped for kept states, then E_J
-        if (!a.ckpt) hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, false>), grid, dim3(NTP), 0, s, e0, nullptr, 0, a);
-        hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, true>), grid, dim3(NTP), 0, s, a.ckpt ? e0 : nullptr,
-                              e1, 0, a);
+        if (!a.ckpt)
+            hipExtLaunchKernelGGL((k_prep_bwd<T, D, SF_NCT_PREP>), dim3(2 * grid.x), dim3(NTP), 0, s, e0, e1, 0, a);
+        else
+            hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, true>), grid, dim3(NTP), 0, s, e0, e1, 0, a);
         break;
     case SF_K_BWD_DQ: hipExtLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, true>), grid, dim3(NTW), 0, s, e0, e1, 0, a); break;
     case SF_K_BWD_DKV:
