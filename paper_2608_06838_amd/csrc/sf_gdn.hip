@@ -219,9 +219,18 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
     const int64_t SS = (int64_t)D * D;
     const int nch = (int)((a.L - tok0 < a.ts ? a.L - tok0 : a.ts) / C);
     const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
+    const LaneOff tro8 = tr_off8<T, LDN, SWX>(lane);
     auto asw = [](int row) { return sizeof(T) == 2 ? 8 * ((row >> 2) & 1) : 0; };
+    // Accumulator pairs (2m, 2m+1) of the state (rows: key channels) and of U
+    // (rows: tokens) hold, in lane row q4, indices 32m + 8 q4 .. +7 (slot r of
+    // tile i: prow(i, r)), so each pair splits into an operand fragment in plain
+    // order with no lane swaps.  The products that build them read their A rows
+    // in that order: fragment row n of tile i is prow(i, n / 4, n % 4).
+    auto prow = [&](int i, int r) { return 32 * (i >> 1) + 8 * q4 + 4 * (i & 1) + r; };
+    auto arow = [](int i, int n) { return 32 * (i >> 1) + 8 * (n >> 2) + 4 * (i & 1) + (n & 3); };
+    auto roff = [](int i) { return 32 * (i >> 1) + 4 * (i & 1); };  // ldfragTR column for tro8
 
-    // S[m][16i + 4q4 + r][c0 + n16]: the walk's state starts from S_J (S_in for
+    // S[m][prow(i, r)][c0 + n16]: the walk's state starts from S_J (S_in for
     // one superchunk); the prep's M (m = 0) from I and its N (m = 1) from 0
     const float *src = a.n_super == 1 ? a.S_in + (a.S_in ? bh * SS : 0) : a.wsS + (int64_t)item * SS;
     f32x4 S[NS][NK];
@@ -229,7 +238,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
     for (int i = 0; i < NK; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int row = 16 * i + 4 * q4 + r;
+            const int row = prow(i, r);
             if constexpr (PREP) {
                 S[0][i][r] = row == c0 + n16 ? 1.f : 0.f;
                 S[1][i][r] = 0.f;
@@ -264,7 +273,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
 #pragma unroll
             for (int i = 0; i < NK; ++i)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = S[0][i][r];
+                for (int r = 0; r < 4; ++r) dst[(int64_t)prow(i, r) * D + c0 + n16] = S[0][i][r];
         }
         const float b2 = wave_scan_dpp(gl * LOG2E);
         const float b63 = lane_value(b2, 63);
@@ -339,7 +348,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         }
         __syncthreads();
 
-        // U[t][v] = Ubar[t][v] - sum_k W[t][k] S[k][v]  (rows t = 16tt + 4q4 + r, column v = c0 + n16);
+        // U[t][v] = Ubar[t][v] - sum_k W[t][k] S[k][v]  (rows t = prow(tt, r), column v = c0 + n16);
         // the prep's M columns take Ubar = 0
         f32x4 U[NS][4];
 #pragma unroll
@@ -348,7 +357,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
             for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    U[m][tt][r] = PREP && m == 0 ? 0.f : sU[(16 * tt + 4 * q4 + r) * LDU + c0 + n16];
+                    U[m][tt][r] = PREP && m == 0 ? 0.f : sU[prow(tt, r) * LDU + c0 + n16];
         // O^T[v][t] = gamma_t sum_k S[k][v] Q[t][k] + sum_s U[s][v] P[t][s]
         f32x4 O[4];
 #pragma unroll
@@ -357,11 +366,11 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         for (int ks = 0; ks < D / 32; ++ks) {
             frag_t<T> fh[NS], fl[NS];
 #pragma unroll
-            for (int m = 0; m < NS; ++m) split_acc_plain<T, true>(S[m][2 * ks], S[m][2 * ks + 1], fh[m], fl[m]);
+            for (int m = 0; m < NS; ++m) split_acc<T, true>(S[m][2 * ks], S[m][2 * ks + 1], fh[m], fl[m]);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
-                // -W[t][32ks + 8q4 .. +7], split hi/lo (fp32 in LDS)
-                const float *wp = &sW[(16 * tt + n16) * LDU + 32 * ks + 8 * q4];
+                // -W[t][32ks + 8q4 .. +7], t = arow(tt, n16), split hi/lo (fp32 in LDS)
+                const float *wp = &sW[arow(tt, n16) * LDU + 32 * ks + 8 * q4];
                 const f32x4 w0 = *reinterpret_cast<const f32x4 *>(wp), w1 = *reinterpret_cast<const f32x4 *>(wp + 4);
                 const float wn[8] = {-w0[0], -w0[1], -w0[2], -w0[3], -w1[0], -w1[1], -w1[2], -w1[3]};
                 frag_t<T> wh, wl;
@@ -381,7 +390,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
 #pragma unroll
             for (int ks = 0; ks < C / 32; ++ks) {
                 frag_t<T> uh, ul;
-                split_acc_plain<T, true>(U[0][2 * ks], U[0][2 * ks + 1], uh, ul);
+                split_acc<T, true>(U[0][2 * ks], U[0][2 * ks + 1], uh, ul);
 #pragma unroll
                 for (int tt = 0; tt < 4; ++tt) {
                     if (32 * ks > 16 * tt + 15) continue;
@@ -398,13 +407,13 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
             for (int tt = 0; tt < 4; ++tt) st4_buf<T>(ro, voff, tt * tstep, O[tt]);
         }
 
-        // V^new (optional): U[16tt + 4q4 + r][c0 + n16]
+        // V^new (optional): U[prow(tt, r)][c0 + n16]
         if (OUTP && VN) {
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    VN[(int64_t)(c * C + 16 * tt + 4 * q4 + r) * a.sx_l + c0 + n16] = cvt<T>(U[0][tt][r]);
+                    VN[(int64_t)(c * C + prow(tt, r)) * a.sx_l + c0 + n16] = cvt<T>(U[0][tt][r]);
         }
 
         // S = gamma_C S + K^T (e^{b_C - b} o U)
@@ -416,16 +425,16 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) U[m][tt][r] *= se[16 * tt + 4 * q4 + r];
+                for (int r = 0; r < 4; ++r) U[m][tt][r] *= se[prow(tt, r)];
         }
 #pragma unroll
         for (int ks = 0; ks < C / 32; ++ks) {
             frag_t<T> uh[NS], ul[NS];
 #pragma unroll
-            for (int m = 0; m < NS; ++m) split_acc_plain<T, true>(U[m][2 * ks], U[m][2 * ks + 1], uh[m], ul[m]);
+            for (int m = 0; m < NS; ++m) split_acc<T, true>(U[m][2 * ks], U[m][2 * ks + 1], uh[m], ul[m]);
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
-                const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sK, tro, 32 * ks, 16 * i);
+                const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sK, tro8, 32 * ks, roff(i));
 #pragma unroll
                 for (int m = 0; m < NS; ++m) mma2b<T, true>(S[m][i], kf, uh[m], ul[m]);
             }
@@ -439,7 +448,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
 #pragma unroll
             for (int i = 0; i < NK; ++i)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = S[m][i][r];
+                for (int r = 0; r < 4; ++r) dst[(int64_t)prow(i, r) * D + c0 + n16] = S[m][i][r];
         }
     }
 }
@@ -571,9 +580,18 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
     const int64_t SS = (int64_t)D * D;
     const int nch = (int)((a.L - tok0 < a.ts ? a.L - tok0 : a.ts) / C);
     const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
+    const LaneOff tro8 = tr_off8<T, LDN, SWX>(lane);
     auto asw = [](int row) { return sizeof(T) == 2 ? 8 * ((row >> 2) & 1) : 0; };
+    // Accumulator pairs (2m, 2m+1) of dS (rows: key channels) and of dU (rows:
+    // tokens) hold, in lane row q4, indices 32m + 8 q4 .. +7 (slot r of tile i:
+    // prow(i, r)), so each pair splits into an operand fragment in plain order
+    // with no lane swaps; the products that build them read their A rows in that
+    // order (fragment row n of tile i: arow(i, n)).
+    auto prow = [&](int i, int r) { return 32 * (i >> 1) + 8 * q4 + 4 * (i & 1) + r; };
+    auto arow = [](int i, int n) { return 32 * (i >> 1) + 8 * (n >> 2) + 4 * (i & 1) + (n & 3); };
+    auto roff = [](int i) { return 32 * (i >> 1) + 4 * (i & 1); };  // ldfragTR column for tro8
 
-    // dS[16i + 4q4 + r][c0 + n16]: from dS_end(J) (dS_out for one superchunk), or 0 (prep)
+    // dS[prow(i, r)][c0 + n16]: from dS_end(J) (dS_out for one superchunk), or 0 (prep)
     f32x4 dS[NK];
     {
         const float *src = a.n_super == 1 ? (a.dS_out ? a.dS_out + bh * SS : nullptr)
@@ -582,7 +600,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
         for (int i = 0; i < NK; ++i)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                dS[i][r] = (!PREP && src) ? src[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] : 0.f;
+                dS[i][r] = (!PREP && src) ? src[(int64_t)prow(i, r) * D + c0 + n16] : 0.f;
     }
 
     using TT = Tile<T, D, NT>;
@@ -609,7 +627,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
 #pragma unroll
             for (int i = 0; i < NK; ++i)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = dS[i][r];
+                for (int r = 0; r < 4; ++r) dst[(int64_t)prow(i, r) * D + c0 + n16] = dS[i][r];
         }
         const float b2 = wave_scan_dpp(gl * LOG2E);
         const float b63 = lane_value(b2, 63);
@@ -681,17 +699,19 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
         __syncthreads();
 
         // dU[t][v] = e^{b_C - b_t} sum_k K[t][k] dS[k][v] + sum_{t' >= t} P^T[t][t'] dO[t'][v]
-        // (rows t = 16tt + 4q4 + r, column v = c0 + n16)
+        // (rows t = prow(tt, r), column v = c0 + n16)
         f32x4 dU[4];
 #pragma unroll
         for (int tt = 0; tt < 4; ++tt) dU[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < D / 32; ++ks) {
             frag_t<T> fh, fl;
-            split_acc_plain<T, true>(dS[2 * ks], dS[2 * ks + 1], fh, fl);
+            split_acc<T, true>(dS[2 * ks], dS[2 * ks + 1], fh, fl);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
-                const frag_t<T> kf = ldfrag_swz<T, LDN, SWX>(sK, swo, 16 * tt, 32 * ks);
+                const int t = arow(tt, n16);  // K[t][32ks + 8q4 ..] (swizzled rows)
+                const frag_t<T> kf =
+                    *reinterpret_cast<const frag_t<T> *>(&sK[t * LDN + swz_col(t, 32 * ks + 8 * q4, SWX)]);
                 mma(dU[tt], kf, fh);
                 mma(dU[tt], kf, fl);
             }
@@ -699,15 +719,15 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
 #pragma unroll
         for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) dU[tt][r] *= se[16 * tt + 4 * q4 + r];
+            for (int r = 0; r < 4; ++r) dU[tt][r] *= se[prow(tt, r)];
 #pragma unroll
         for (int ks = 0; ks < C / 32; ++ks) {
             const frag_t<T> of = ldfragTR<T, LDN, SWX>(sO, tro, 32 * ks, c0);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
                 if (32 * ks + 31 < 16 * tt) continue;
-                const int aw = asw(lane & 15);
-                const int o = (16 * tt + (lane & 15)) * LDT + ((32 * ks + 8 * (lane >> 4)) ^ aw);
+                const int row = arow(tt, n16);
+                const int o = row * LDT + ((32 * ks + 8 * (lane >> 4)) ^ asw(row));
                 mma(dU[tt], *reinterpret_cast<const frag_t<T> *>(sP + o), of);
                 mma(dU[tt], *reinterpret_cast<const frag_t<T> *>(sPl + o), of);
             }
@@ -719,22 +739,22 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
         for (int i = 0; i < NK; ++i) dS[i] *= gam;
 #pragma unroll
         for (int ks = 0; ks < C / 32; ++ks) {
-            f32x4 g0, g1;  // gamma_t dO[t][c0 + n16], t = 32ks + 16h + 4q4 + r
+            f32x4 g0, g1;  // gamma_t dO[t][c0 + n16], t = 32ks + 8q4 + 4h + r
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int ta = 32 * ks + 4 * q4 + r, tb = ta + 16;
+                const int ta = 32 * ks + 8 * q4 + r, tb = ta + 4;
                 g0[r] = sq[ta] * tof<T>(sO[ta * LDN + swz_col(ta, c0 + n16, SWX)]);
                 g1[r] = sq[tb] * tof<T>(sO[tb * LDN + swz_col(tb, c0 + n16, SWX)]);
             }
             frag_t<T> gh, glo, uh, ul;
-            split_acc_plain<T, true>(g0, g1, gh, glo);
-            split_acc_plain<T, true>(dU[2 * ks], dU[2 * ks + 1], uh, ul);
+            split_acc<T, true>(g0, g1, gh, glo);
+            split_acc<T, true>(dU[2 * ks], dU[2 * ks + 1], uh, ul);
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
-                mma2b<T, true>(dS[i], ldfragTR<T, LDN, SWX>(sQ, tro, 32 * ks, 16 * i), gh, glo);
-                float wn[8];  // -W[t][k], k = 16i + lane % 16, t = 32ks + 8 (lane / 16) + j
+                mma2b<T, true>(dS[i], ldfragTR<T, LDN, SWX>(sQ, tro8, 32 * ks, roff(i)), gh, glo);
+                float wn[8];  // -W[t][k], k = arow(i, lane % 16), t = 32ks + 8 (lane / 16) + j
 #pragma unroll
-                for (int j = 0; j < 8; ++j) wn[j] = -sW[(32 * ks + 8 * q4 + j) * LDU + 16 * i + n16];
+                for (int j = 0; j < 8; ++j) wn[j] = -sW[(32 * ks + 8 * q4 + j) * LDU + arow(i, n16)];
                 frag_t<T> wh, wl;
                 split8<T, true>(wn, wh, wl);
                 mma(dS[i], wh, uh);
@@ -748,7 +768,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
 #pragma unroll
         for (int i = 0; i < NK; ++i)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) dst[(int64_t)(16 * i + 4 * q4 + r) * D + c0 + n16] = dS[i][r];
+            for (int r = 0; r < 4; ++r) dst[(int64_t)prow(i, r) * D + c0 + n16] = dS[i][r];
     }
 }
 
