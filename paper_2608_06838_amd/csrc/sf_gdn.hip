@@ -64,16 +64,25 @@ __device__ __forceinline__ void split4(const f32x4 &x, s4v &hi, s4v &lo) {
 
 // T = (I + A)^{-1} for the strictly lower 64 x 64 A = diag(rs) M with M in sA
 // (pitch C + 4; rs == nullptr: A = M), into sT (fp32, pitch C + 4, zero above
-// the diagonal), by 16 x 16 blocks: the four diagonal blocks by forward
-// substitution in fp32 (64 threads, one column each); then level by level
+// the diagonal), by 16 x 16 blocks.  A diagonal block N = A_ii is nilpotent
+// (N^16 = 0), so its inverse is the finite series sum_k (-N)^k, which factors as
+//   (I + N)^{-1} = (I + N^8)(I + N^4)(I + N^2)(I - N):
+// wave i forms N^2, N^4, N^8 by squaring and applies the three factors to
+// I - N, eight 16x16x16 MFMA products with hi/lo operands.  A product's
+// accumulator is the B-operand layout, and the transpose of a product lands in
+// the A-operand layout (P^T = N^T N^T has the accumulator slots of P's rows),
+// so each power is formed in both layouts and nothing moves between lanes.
+// (SERIES = false: forward substitution in fp32 instead, 64 threads, one
+// column each; the per-chunk gradient kernel keeps that form, which measured
+// faster there.)  Then level by level
 // (i - j = 1, 2, 3) wave j forms T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj on
 // 16x16x16 MFMA with hi/lo operands, the inner sum staying in its
 // accumulator, which is already the B operand of the T_ii product.  NT >= 256
 // threads (four waves); ends with a barrier.
-template <int NT>
+template <int NT, bool SERIES>
 __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, const float *rs = nullptr) {
     constexpr int LA = C + 4, LT = C + 4;
-    if (tid < 64) {
+    if (!SERIES && tid < 64) {  // one column of a diagonal block per thread, by substitution
         const int o = 16 * (tid >> 4), c = tid & 15;
         float x[16];
 #pragma unroll
@@ -85,6 +94,43 @@ __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, co
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) sT[(o + r) * LT + o + c] = x[r];
+    }
+    if (SERIES && tid < 256) {  // wave i: T_ii
+        const int o = 16 * (tid >> 6), q = (tid >> 4) & 3, n = tid & 15;
+        // N in the A layout (row n, columns 4q..4q+3) and the B layout (rows 4q..4q+3, column n)
+        f32x4 na = {0.f, 0.f, 0.f, 0.f}, nb = na;
+        {
+            const f32x4 x = *reinterpret_cast<const f32x4 *>(&sA[(o + n) * LA + o + 4 * q]);
+            const float sn = rs ? rs[o + n] : 1.f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int row = 4 * q + j;
+                na[j] = row < n ? sn * x[j] : 0.f;
+                nb[j] = n < row ? (rs ? rs[o + row] : 1.f) * sA[(o + row) * LA + o + n] : 0.f;
+            }
+        }
+        // c + a b with a in the A layout, b in the B layout; c and the result in the B layout
+        auto mm = [](f32x4 c, const f32x4 &a, const f32x4 &b) {
+            s4v ah, al, bh, bl;
+            split4(a, ah, al);
+            split4(b, bh, bl);
+            mma16(c, ah, bh);
+            mma16(c, ah, bl);
+            mma16(c, al, bh);
+            return c;
+        };
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        const f32x4 n2b = mm(z, na, nb), n2a = mm(z, nb, na);    // N^2 (B layout), N^2 (A layout)
+        const f32x4 n4b = mm(z, n2a, n2b), n4a = mm(z, n2b, n2a);
+        const f32x4 n8a = mm(z, n4b, n4a);
+        f32x4 x = z;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = (4 * q + j == n ? 1.f : 0.f) - nb[j];  // I - N
+        x = mm(x, n2a, x);
+        x = mm(x, n4a, x);
+        x = mm(x, n8a, x);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sT[(o + 4 * q + j) * LT + o + n] = x[j];
     }
     for (int e = tid; e < 6 * 256; e += NT) {  // blocks (0,1) (0,2) (0,3) (1,2) (1,3) (2,3)
         const int b = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
@@ -333,7 +379,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         };
         scores(10);
         __syncthreads();
-        gdn_tinv<NT>(tid, sA, sT);
+        gdn_tinv<NT, true>(tid, sA, sT);
         gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sT, sK, sV, sbeta, sq, sW, sU);
         __syncthreads();
         if constexpr (OUTP) {
@@ -685,7 +731,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
         };
         scores(10);
         __syncthreads();
-        gdn_tinv<NT>(tid, sA, sT);
+        gdn_tinv<NT, true>(tid, sA, sT);
         gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sT, sK, (const T *)nullptr, sbeta, sq, sW, nullptr);
         __syncthreads();
         scores(0);
@@ -999,7 +1045,7 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
             }
         }
         __syncthreads();
-        gdn_tinv<NTH>(tid, sX, sT, sbe);  // T = (I + diag(beta) KK o Gamma)^{-1}; ends with a barrier
+        gdn_tinv<NTH, false>(tid, sX, sT, sbe);  // T = (I + diag(beta) KK o Gamma)^{-1}; ends with a barrier
 
         // one accumulator array, overlaid by role (both roles run the same code,
         // so separate arrays would all stay live on every wave):
