@@ -175,10 +175,13 @@ __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, co
 // [W | Ubar] = T [diag(beta gamma) K | diag(beta) V] on MFMA: wave w forms
 // columns [16w, 16w+16) of W (and of Ubar when sU is given); T enters as a hi/lo
 // pair, the scaled K and V columns too (K, V exact in bf16 times an fp32
-// factor).  Results to sW / sU (fp32, pitch LDU).
+// factor).  Results: -W as a bf16 hi/lo pair (sWh, sWl: natural [t][k] tiles,
+// pitch LDN, channel blocks of rows with bit 3 set XOR-swizzled by SWX, the
+// layout of the staged q/k tiles), split once here for every wave that reads
+// it; Ubar to sU (fp32, pitch LDU).
 template <typename T, int D, int LDN, int LDU, int SWX>
 __device__ __forceinline__ void gdn_wu(int w, int lane, const LaneOff &tro, const float *sT, const T *sK, const T *sV,
-                                       const float *sbeta, const float *sq, float *sW, float *sU) {
+                                       const float *sbeta, const float *sq, T *sWh, T *sWl, float *sU) {
     constexpr int LT = C + 4;
     const int q4 = lane >> 4, n16 = lane & 15, c0 = 16 * w;
     f32x4 cw[4], cu[4];
@@ -218,8 +221,12 @@ __device__ __forceinline__ void gdn_wu(int w, int lane, const LaneOff &tro, cons
     for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            sW[(16 * tt + 4 * q4 + r) * LDU + c0 + n16] = cw[tt][r];
-            if (sU) sU[(16 * tt + 4 * q4 + r) * LDU + c0 + n16] = cu[tt][r];
+            const int t = 16 * tt + 4 * q4 + r, pw = t * LDN + swz_col(t, c0 + n16, SWX);
+            const float x = -cw[tt][r];
+            const T h = cvt<T>(x);
+            sWh[pw] = h;
+            sWl[pw] = cvt<T>(x - tof<T>(h));
+            if (sU) sU[t * LDU + c0 + n16] = cu[tt][r];
         }
 }
 
@@ -240,8 +247,12 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
     static_assert(!OUTP || 2 * C * LDT * sizeof(T) >= C * (C + 4) * sizeof(float), "T does not fit the P tiles");
     T *sP = sPP, *sPl = sPP + (OUTP ? C * LDT : 0);
     float *sT = OUTP ? reinterpret_cast<float *>(sPP) : sTx;
-    __shared__ __attribute__((aligned(16))) float sA[C * LDA];    // beta_t e^{b_t-b_s} k_t.k_s, s < t
-    __shared__ __attribute__((aligned(16))) float sW[C * LDU];    // W [t][k], fp32
+    // A = beta_t e^{b_t-b_s} k_t.k_s (s < t, fp32) until the inverse is formed; then -W
+    // as a hi/lo pair of bf16 tiles in the same bytes
+    constexpr int AWB = C * LDA * 4 > 2 * C * LDN * (int)sizeof(T) ? C * LDA * 4 : 2 * C * LDN * (int)sizeof(T);
+    __shared__ __attribute__((aligned(16))) char sAW[AWB];
+    float *const sA = reinterpret_cast<float *>(sAW);
+    T *const sWh = reinterpret_cast<T *>(sAW), *const sWl = sWh + C * LDN;
     __shared__ __attribute__((aligned(16))) float sU[C * LDU];    // Ubar [t][v], fp32
     __shared__ __attribute__((aligned(16))) float sb[C], sq[C], se[C], sbeta[C];
 
@@ -380,7 +391,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         scores(10);
         __syncthreads();
         gdn_tinv<NT, true>(tid, sA, sT);
-        gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sT, sK, sV, sbeta, sq, sW, sU);
+        gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sT, sK, sV, sbeta, sq, sWh, sWl, sU);
         __syncthreads();
         if constexpr (OUTP) {
             scores(0);
@@ -415,12 +426,10 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
             for (int m = 0; m < NS; ++m) split_acc<T, true>(S[m][2 * ks], S[m][2 * ks + 1], fh[m], fl[m]);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
-                // -W[t][32ks + 8q4 .. +7], t = arow(tt, n16), split hi/lo (fp32 in LDS)
-                const float *wp = &sW[arow(tt, n16) * LDU + 32 * ks + 8 * q4];
-                const f32x4 w0 = *reinterpret_cast<const f32x4 *>(wp), w1 = *reinterpret_cast<const f32x4 *>(wp + 4);
-                const float wn[8] = {-w0[0], -w0[1], -w0[2], -w0[3], -w1[0], -w1[1], -w1[2], -w1[3]};
-                frag_t<T> wh, wl;
-                split8<T, true>(wn, wh, wl);
+                // -W[t][32ks + 8q4 .. +7], t = arow(tt, n16), as its hi/lo pair
+                const int t = arow(tt, n16), pw = t * LDN + swz_col(t, 32 * ks + 8 * q4, SWX);
+                const frag_t<T> wh = *reinterpret_cast<const frag_t<T> *>(&sWh[pw]);
+                const frag_t<T> wl = *reinterpret_cast<const frag_t<T> *>(&sWl[pw]);
 #pragma unroll
                 for (int m = 0; m < NS; ++m) {
                     mma(U[m][tt], wh, fh[m]);
@@ -605,8 +614,11 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
     static_assert(2 * C * LDT * sizeof(T) >= C * (C + 4) * sizeof(float), "T does not fit the P tiles");
     T *sP = sPP, *sPl = sPP + C * LDT;
     float *sT = reinterpret_cast<float *>(sPP);
-    __shared__ __attribute__((aligned(16))) float sA[C * LDA];
-    __shared__ __attribute__((aligned(16))) float sW[C * LDU];
+    // A until the inverse is formed, then -W as a hi/lo pair of bf16 tiles (see the walk)
+    constexpr int AWB = C * LDA * 4 > 2 * C * LDN * (int)sizeof(T) ? C * LDA * 4 : 2 * C * LDN * (int)sizeof(T);
+    __shared__ __attribute__((aligned(16))) char sAW[AWB];
+    float *const sA = reinterpret_cast<float *>(sAW);
+    T *const sWh = reinterpret_cast<T *>(sAW), *const sWl = sWh + C * LDN;
     __shared__ __attribute__((aligned(16))) float sb[C], sq[C], se[C], sbeta[C];
 
     const int tid = threadIdx.x, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
@@ -732,7 +744,7 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
         scores(10);
         __syncthreads();
         gdn_tinv<NT, true>(tid, sA, sT);
-        gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sT, sK, (const T *)nullptr, sbeta, sq, sW, nullptr);
+        gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sT, sK, (const T *)nullptr, sbeta, sq, sWh, sWl, nullptr);
         __syncthreads();
         scores(0);
         // P^T tiles below the diagonal that the dU product reads are zero
@@ -798,11 +810,9 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
                 mma2b<T, true>(dS[i], ldfragTR<T, LDN, SWX>(sQ, tro8, 32 * ks, roff(i)), gh, glo);
-                float wn[8];  // -W[t][k], k = arow(i, lane % 16), t = 32ks + 8 (lane / 16) + j
-#pragma unroll
-                for (int j = 0; j < 8; ++j) wn[j] = -sW[(32 * ks + 8 * q4 + j) * LDU + arow(i, n16)];
-                frag_t<T> wh, wl;
-                split8<T, true>(wn, wh, wl);
+                // -W[t][k] hi/lo, k = arow(i, lane % 16), t = 32ks + 8 (lane / 16) + j
+                const frag_t<T> wh = ldfragTR<T, LDN, SWX>(sWh, tro8, 32 * ks, roff(i));
+                const frag_t<T> wl = ldfragTR<T, LDN, SWX>(sWl, tro8, 32 * ks, roff(i));
                 mma(dS[i], wh, uh);
                 mma(dS[i], wh, ul);
                 mma(dS[i], wl, uh);
