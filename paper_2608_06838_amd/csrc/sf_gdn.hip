@@ -64,25 +64,17 @@ __device__ __forceinline__ void split4(const f32x4 &x, s4v &hi, s4v &lo) {
 
 // T = (I + A)^{-1} for the strictly lower 64 x 64 A = diag(rs) M with M in sA
 // (pitch C + 4; rs == nullptr: A = M), into sT (fp32, pitch C + 4, zero above
-// the diagonal), by 16 x 16 blocks.  A diagonal block N = A_ii is nilpotent
-// (N^16 = 0), so its inverse is the finite series sum_k (-N)^k, which factors as
-//   (I + N)^{-1} = (I + N^8)(I + N^4)(I + N^2)(I - N):
-// wave i forms N^2, N^4, N^8 by squaring and applies the three factors to
-// I - N, eight 16x16x16 MFMA products with hi/lo operands.  A product's
-// accumulator is the B-operand layout, and the transpose of a product lands in
-// the A-operand layout (P^T = N^T N^T has the accumulator slots of P's rows),
-// so each power is formed in both layouts and nothing moves between lanes.
-// (SERIES = false: forward substitution in fp32 instead, 64 threads, one
-// column each; the per-chunk gradient kernel keeps that form, which measured
-// faster there.)  Then level by level
+// the diagonal), by 16 x 16 blocks: the four diagonal blocks by forward
+// substitution in fp32 (64 threads, one column each); then level by level
 // (i - j = 1, 2, 3) wave j forms T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj on
 // 16x16x16 MFMA with hi/lo operands, the inner sum staying in its
 // accumulator, which is already the B operand of the T_ii product.  NT >= 256
-// threads (four waves); ends with a barrier.
-template <int NT, bool SERIES>
+// threads (four waves); ends with a barrier.  (The per-chunk gradient kernel's
+// form; the walks use gdn_tinv_hl below.)
+template <int NT>
 __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, const float *rs = nullptr) {
     constexpr int LA = C + 4, LT = C + 4;
-    if (!SERIES && tid < 64) {  // one column of a diagonal block per thread, by substitution
+    if (tid < 64) {
         const int o = 16 * (tid >> 4), c = tid & 15;
         float x[16];
 #pragma unroll
@@ -94,43 +86,6 @@ __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, co
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) sT[(o + r) * LT + o + c] = x[r];
-    }
-    if (SERIES && tid < 256) {  // wave i: T_ii
-        const int o = 16 * (tid >> 6), q = (tid >> 4) & 3, n = tid & 15;
-        // N in the A layout (row n, columns 4q..4q+3) and the B layout (rows 4q..4q+3, column n)
-        f32x4 na = {0.f, 0.f, 0.f, 0.f}, nb = na;
-        {
-            const f32x4 x = *reinterpret_cast<const f32x4 *>(&sA[(o + n) * LA + o + 4 * q]);
-            const float sn = rs ? rs[o + n] : 1.f;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int row = 4 * q + j;
-                na[j] = row < n ? sn * x[j] : 0.f;
-                nb[j] = n < row ? (rs ? rs[o + row] : 1.f) * sA[(o + row) * LA + o + n] : 0.f;
-            }
-        }
-        // c + a b with a in the A layout, b in the B layout; c and the result in the B layout
-        auto mm = [](f32x4 c, const f32x4 &a, const f32x4 &b) {
-            s4v ah, al, bh, bl;
-            split4(a, ah, al);
-            split4(b, bh, bl);
-            mma16(c, ah, bh);
-            mma16(c, ah, bl);
-            mma16(c, al, bh);
-            return c;
-        };
-        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-        const f32x4 n2b = mm(z, na, nb), n2a = mm(z, nb, na);    // N^2 (B layout), N^2 (A layout)
-        const f32x4 n4b = mm(z, n2a, n2b), n4a = mm(z, n2b, n2a);
-        const f32x4 n8a = mm(z, n4b, n4a);
-        f32x4 x = z;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) x[j] = (4 * q + j == n ? 1.f : 0.f) - nb[j];  // I - N
-        x = mm(x, n2a, x);
-        x = mm(x, n4a, x);
-        x = mm(x, n8a, x);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sT[(o + 4 * q + j) * LT + o + n] = x[j];
     }
     for (int e = tid; e < 6 * 256; e += NT) {  // blocks (0,1) (0,2) (0,3) (1,2) (1,3) (2,3)
         const int b = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
@@ -172,17 +127,117 @@ __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, co
     }
 }
 
+// The walks' T = (I + A)^{-1} (A = M in sA, pitch C + 4), stored as the bf16
+// hi/lo pair that every consumer splits it into (sTh, sTl: raw 16-bit
+// patterns, pitch C + 16, zero above the diagonal).  A diagonal block N = A_ii
+// is nilpotent (N^16 = 0), so its inverse is the finite series sum_k (-N)^k,
+// which factors as
+//   (I + N)^{-1} = (I + N^8)(I + N^4)(I + N^2)(I - N):
+// wave i forms N^2, N^4, N^8 by squaring and applies the three factors to
+// I - N, eight 16x16x16 MFMA products with hi/lo operands.  A product's
+// accumulator is the B-operand layout, and the transpose of a product lands in
+// the A-operand layout (P^T = N^T N^T has the accumulator slots of P's rows),
+// so each power is formed in both layouts and nothing moves between lanes.
+// The off-diagonal blocks then go level by level as in gdn_tinv, reading the
+// stored pairs.  NT >= 256 threads; ends with a barrier.
+template <int NT>
+__device__ __forceinline__ void gdn_tinv_hl(int tid, const float *sA, short *sTh, short *sTl) {
+    constexpr int LA = C + 4, LTB = C + 16;
+    const int w = tid >> 6, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
+    // c + a b with a in the A layout, b in the B layout; c and the result in the B layout
+    auto mm = [](f32x4 c, const f32x4 &a, const f32x4 &b) {
+        s4v ah, al, bh, bl;
+        split4(a, ah, al);
+        split4(b, bh, bl);
+        mma16(c, ah, bh);
+        mma16(c, ah, bl);
+        mma16(c, al, bh);
+        return c;
+    };
+    // rows row0 .. row0+3 of column col (the B layout), as hi/lo
+    auto put = [&](int row0, int col, const f32x4 &x) {
+        s4v h, l;
+        split4(x, h, l);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            sTh[(row0 + r) * LTB + col] = h[r];
+            sTl[(row0 + r) * LTB + col] = l[r];
+        }
+    };
+    if (tid < 256) {  // wave w: T_ww
+        const int o = 16 * w;
+        // N in the A layout (row n16, columns 4q4..4q4+3) and the B layout (rows 4q4.., column n16)
+        f32x4 na = {0.f, 0.f, 0.f, 0.f}, nb = na;
+        const f32x4 x = *reinterpret_cast<const f32x4 *>(&sA[(o + n16) * LA + o + 4 * q4]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int row = 4 * q4 + j;
+            na[j] = row < n16 ? x[j] : 0.f;
+            nb[j] = n16 < row ? sA[(o + row) * LA + o + n16] : 0.f;
+        }
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        const f32x4 n2b = mm(z, na, nb), n2a = mm(z, nb, na);  // N^2 (B layout), N^2 (A layout)
+        const f32x4 n4b = mm(z, n2a, n2b), n4a = mm(z, n2b, n2a);
+        const f32x4 n8a = mm(z, n4b, n4a);
+        f32x4 t = z;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) t[j] = (4 * q4 + j == n16 ? 1.f : 0.f) - nb[j];  // I - N
+        t = mm(t, n2a, t);
+        t = mm(t, n4a, t);
+        t = mm(t, n8a, t);
+        put(o + 4 * q4, o + n16, t);
+    }
+    for (int e = tid; e < 6 * 256; e += NT) {  // blocks (0,1) (0,2) (0,3) (1,2) (1,3) (2,3)
+        const int b = e >> 8, rr = (e >> 4) & 15, cc = e & 15;
+        const int bi = b < 3 ? 0 : (b < 5 ? 1 : 2), bj = b < 3 ? b + 1 : (b < 5 ? b - 1 : 3);
+        sTh[(16 * bi + rr) * LTB + 16 * bj + cc] = 0;
+        sTl[(16 * bi + rr) * LTB + 16 * bj + cc] = 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int d = 1; d < 4; ++d) {
+        if (w < 4 - d) {  // block (i, j) = (d + w, w)
+            const int i = d + w, j = w;
+            f32x4 y = {0.f, 0.f, 0.f, 0.f};
+            for (int k = j; k < i; ++k) {
+                const f32x4 av = *reinterpret_cast<const f32x4 *>(&sA[(16 * i + n16) * LA + 16 * k + 4 * q4]);
+                s4v ah, al, bh = {0, 0, 0, 0}, bl = bh;
+                split4(av, ah, al);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    bh[u] = sTh[(16 * k + 4 * q4 + u) * LTB + 16 * j + n16];
+                    bl[u] = sTl[(16 * k + 4 * q4 + u) * LTB + 16 * j + n16];
+                }
+                mma16(y, ah, bh);
+                mma16(y, ah, bl);
+                mma16(y, al, bh);
+            }
+            const s4v th = *reinterpret_cast<const s4v *>(&sTh[(16 * i + n16) * LTB + 16 * i + 4 * q4]);
+            const s4v tl = *reinterpret_cast<const s4v *>(&sTl[(16 * i + n16) * LTB + 16 * i + 4 * q4]);
+            s4v yh, yl;
+            split4(y, yh, yl);
+            f32x4 t = {0.f, 0.f, 0.f, 0.f};
+            mma16(t, th, yh);
+            mma16(t, th, yl);
+            mma16(t, tl, yh);
+            put(16 * i + 4 * q4, 16 * j + n16, -t);
+        }
+        __syncthreads();
+    }
+}
+
 // [W | Ubar] = T [diag(beta gamma) K | diag(beta) V] on MFMA: wave w forms
-// columns [16w, 16w+16) of W (and of Ubar when sU is given); T enters as a hi/lo
-// pair, the scaled K and V columns too (K, V exact in bf16 times an fp32
+// columns [16w, 16w+16) of W (and of Ubar when sU is given); T enters as its
+// stored hi/lo pair (gdn_tinv_hl), the scaled K and V columns as hi/lo pairs too (K, V exact in bf16 times an fp32
 // factor).  Results: -W as a bf16 hi/lo pair (sWh, sWl: natural [t][k] tiles,
 // pitch LDN, channel blocks of rows with bit 3 set XOR-swizzled by SWX, the
 // layout of the staged q/k tiles), split once here for every wave that reads
 // it; Ubar to sU (fp32, pitch LDU).
 template <typename T, int D, int LDN, int LDU, int SWX>
-__device__ __forceinline__ void gdn_wu(int w, int lane, const LaneOff &tro, const float *sT, const T *sK, const T *sV,
+__device__ __forceinline__ void gdn_wu(int w, int lane, const LaneOff &tro, const short *sTh, const short *sTl,
+                                       const T *sK, const T *sV,
                                        const float *sbeta, const float *sq, T *sWh, T *sWl, float *sU) {
-    constexpr int LT = C + 4;
+    constexpr int LTB = C + 16;
     const int q4 = lane >> 4, n16 = lane & 15, c0 = 16 * w;
     f32x4 cw[4], cu[4];
 #pragma unroll
@@ -202,11 +257,9 @@ __device__ __forceinline__ void gdn_wu(int w, int lane, const LaneOff &tro, cons
 #pragma unroll
         for (int tt = 0; tt < 4; ++tt) {
             if (32 * ks > 16 * tt + 15) continue;  // T is lower triangular
-            const float *p = sT + (16 * tt + n16) * LT + 32 * ks + 8 * q4;
-            const f32x4 x0 = *reinterpret_cast<const f32x4 *>(p), x1 = *reinterpret_cast<const f32x4 *>(p + 4);
-            const float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-            frag_t<T> th, tl;
-            split8<T, true>(x, th, tl);
+            const int pt = (16 * tt + n16) * LTB + 32 * ks + 8 * q4;
+            const frag_t<T> th = *reinterpret_cast<const frag_t<T> *>(sTh + pt);
+            const frag_t<T> tl = *reinterpret_cast<const frag_t<T> *>(sTl + pt);
             mma(cw[tt], th, kh);
             mma(cw[tt], th, kl);
             mma(cw[tt], tl, kh);
@@ -243,10 +296,10 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
     __shared__ __attribute__((aligned(16))) T sV[C * LDN];               // plain
     // (Q K^T o Gamma)[t][s] hi, then lo; T = (I + A)^{-1} lives here before the P tiles
     __shared__ __attribute__((aligned(16))) T sPP[OUTP ? 2 * C * LDT : 8];
-    __shared__ __attribute__((aligned(16))) float sTx[OUTP ? 4 : C * (C + 4)];
-    static_assert(!OUTP || 2 * C * LDT * sizeof(T) >= C * (C + 4) * sizeof(float), "T does not fit the P tiles");
+    __shared__ __attribute__((aligned(16))) T sTx[OUTP ? 8 : 2 * C * LDT];
+    static_assert(LDT == C + 16, "T's hi/lo pair has the P tiles' pitch");
     T *sP = sPP, *sPl = sPP + (OUTP ? C * LDT : 0);
-    float *sT = OUTP ? reinterpret_cast<float *>(sPP) : sTx;
+    short *const sTh = reinterpret_cast<short *>(OUTP ? sPP : sTx), *const sTl = sTh + C * LDT;
     // A = beta_t e^{b_t-b_s} k_t.k_s (s < t, fp32) until the inverse is formed; then -W
     // as a hi/lo pair of bf16 tiles in the same bytes
     constexpr int AWB = C * LDA * 4 > 2 * C * LDN * (int)sizeof(T) ? C * LDA * 4 : 2 * C * LDN * (int)sizeof(T);
@@ -390,8 +443,8 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
         };
         scores(10);
         __syncthreads();
-        gdn_tinv<NT, true>(tid, sA, sT);
-        gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sT, sK, sV, sbeta, sq, sWh, sWl, sU);
+        gdn_tinv_hl<NT>(tid, sA, sTh, sTl);
+        gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sTh, sTl, sK, sV, sbeta, sq, sWh, sWl, sU);
         __syncthreads();
         if constexpr (OUTP) {
             scores(0);
@@ -611,9 +664,9 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
     __shared__ __attribute__((aligned(16))) T sO[C * LDN];   // dO, swizzled
     // P^T[s][t] = e^{b_t-b_s} k_s.q_t (s <= t) hi, then lo; T = (I + A)^{-1} lives here first
     __shared__ __attribute__((aligned(16))) T sPP[2 * C * LDT];
-    static_assert(2 * C * LDT * sizeof(T) >= C * (C + 4) * sizeof(float), "T does not fit the P tiles");
+    static_assert(LDT == C + 16, "T's hi/lo pair has the P tiles' pitch");
     T *sP = sPP, *sPl = sPP + C * LDT;
-    float *sT = reinterpret_cast<float *>(sPP);
+    short *const sTh = reinterpret_cast<short *>(sPP), *const sTl = sTh + C * LDT;
     // A until the inverse is formed, then -W as a hi/lo pair of bf16 tiles (see the walk)
     constexpr int AWB = C * LDA * 4 > 2 * C * LDN * (int)sizeof(T) ? C * LDA * 4 : 2 * C * LDN * (int)sizeof(T);
     __shared__ __attribute__((aligned(16))) char sAW[AWB];
@@ -743,8 +796,8 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
         };
         scores(10);
         __syncthreads();
-        gdn_tinv<NT, true>(tid, sA, sT);
-        gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sT, sK, (const T *)nullptr, sbeta, sq, sWh, sWl, nullptr);
+        gdn_tinv_hl<NT>(tid, sA, sTh, sTl);
+        gdn_wu<T, D, LDN, LDU, SWX>(w, lane, tro, sTh, sTl, sK, (const T *)nullptr, sbeta, sq, sWh, sWl, nullptr);
         __syncthreads();
         scores(0);
         // P^T tiles below the diagonal that the dU product reads are zero
@@ -1055,7 +1108,7 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
             }
         }
         __syncthreads();
-        gdn_tinv<NTH, false>(tid, sX, sT, sbe);  // T = (I + diag(beta) KK o Gamma)^{-1}; ends with a barrier
+        gdn_tinv<NTH>(tid, sX, sT, sbe);  // T = (I + diag(beta) KK o Gamma)^{-1}; ends with a barrier
 
         // one accumulator array, overlaid by role (both roles run the same code,
         // so separate arrays would all stay live on every wave):
