@@ -974,7 +974,13 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
     __shared__ float sCol[4][C];     // column-sum partials, one per row tile
     __shared__ float sWav[16];
 
-    float *const sSb = sBlk, *const sDb = sBlk + D * LDB;      // [k'][v] of the block
+    // S_J and dS'_J of the block as hi/lo bf16 pairs, split once when staged:
+    // [k'][v] tiles of VB = 32 channels (64-byte rows), the 16-byte channel blocks
+    // of row r XOR-swizzled by (r / 4) % 4
+    static_assert(VB == 32 && 4 * D * VB * (int)sizeof(T) <= NBLKF * 4, "block tiles fit sBlk");
+    T *const sSh = reinterpret_cast<T *>(sBlk), *const sSl = sSh + D * VB;
+    T *const sDh = sSl + D * VB, *const sDl = sDh + D * VB;
+    auto bpos = [](int r, int ch) { return r * VB + ((((ch >> 3) ^ (r >> 2)) & 3) << 3) + (ch & 7); };
     float *const sE1 = sBlk, *const sE2 = sBlk + C * LD6;      // dP o Gamma, Ah + Ah^T
     float *const sR = sX, *const sdU = sX + C * LDR;           // [t][v] of the block
 
@@ -1008,6 +1014,21 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) x[j] = M[(k0 + 8 * q4 + j) * ld + row0 + n16];
         split8<T, true>(x, h, l);
+    };
+    // from a block tile [k'][v] (bpos layout): rows row0 + n16 over channels
+    // 8 q4 .. +7 (b_rm), or rows = channels c0 + n16 over k0 + 8 q4 + j through
+    // two transposing reads (b_tr; the lane map of ldfragTR)
+    auto b_rm = [&](const T *M, int row0) {
+        return *reinterpret_cast<const frag_t<T> *>(M + bpos(row0 + n16, 8 * q4));
+    };
+    auto b_tr = [&](const T *M, int k0, int c0) {
+        typedef short s4 __attribute__((ext_vector_type(4)));
+        typedef short s8 __attribute__((ext_vector_type(8)));
+        const int ch = c0 + 4 * (lane & 3), r0 = k0 + 8 * q4 + ((lane & 15) >> 2);
+        const s4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)(M + bpos(r0, ch)));
+        const s4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)(M + bpos(r0 + 4, ch)));
+        const s8 v = __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7);
+        return __builtin_bit_cast(frag_t<T>, v);
     };
     auto mma3 = [](f32x4 &c, const frag_t<T> &ah, const frag_t<T> &al, const frag_t<T> &bh, const frag_t<T> &bl) {
         mma(c, ah, bh);
@@ -1058,8 +1079,20 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
         float sd = 0.f;  // <dS', S> over this thread's units
         auto stage = [&]() {
             if (tid < NSU) {
-                *reinterpret_cast<f32x4 *>(&sSb[su_r * LDB + su_c]) = pS;
-                *reinterpret_cast<f32x4 *>(&sDb[su_r * LDB + su_c]) = pD;
+                typedef T t4 __attribute__((ext_vector_type(4)));
+                t4 sh = {}, sl = {}, dh = {}, dl = {};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    sh[j] = cvt<T>(pS[j]);
+                    sl[j] = cvt<T>(pS[j] - tof<T>(sh[j]));
+                    dh[j] = cvt<T>(pD[j]);
+                    dl[j] = cvt<T>(pD[j] - tof<T>(dh[j]));
+                }
+                const int pb = bpos(su_r, su_c);
+                *reinterpret_cast<t4 *>(&sSh[pb]) = sh;
+                *reinterpret_cast<t4 *>(&sSl[pb]) = sl;
+                *reinterpret_cast<t4 *>(&sDh[pb]) = dh;
+                *reinterpret_cast<t4 *>(&sDl[pb]) = dl;
                 sd = fmaf(pS[0], pD[0], fmaf(pS[1], pD[1], fmaf(pS[2], pD[2], fmaf(pS[3], pD[3], sd))));
             }
             if (tid < 256) {
@@ -1134,8 +1167,7 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
                 f32x4 y = z4;
 #pragma unroll 1
                 for (int kk = 0; kk < D; kk += 32) {
-                    frag_t<T> bh, bl;
-                    f_tr(sSb, LDB, 16 * nb, kk, bh, bl);  // B[v][k'] = S_J[k'][v]
+                    const frag_t<T> bh = b_tr(sSh, kk, 16 * nb), bl = b_tr(sSl, kk, 16 * nb);  // B[v][k'] = S_J[k'][v]
                     const frag_t<T> ak = x_rm(xk, LDX, 16 * mt, kk);
                     mma(y, ak, bh);
                     mma(y, ak, bl);
@@ -1149,8 +1181,7 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
                 f32x4 u = z4;
 #pragma unroll 1
                 for (int kk = 0; kk < D; kk += 32) {
-                    frag_t<T> bh, bl;
-                    f_tr(sDb, LDB, 16 * nb, kk, bh, bl);  // B[v][k'] = dS'_J[k'][v]
+                    const frag_t<T> bh = b_tr(sDh, kk, 16 * nb), bl = b_tr(sDl, kk, 16 * nb);  // B[v][k'] = dS'_J[k'][v]
                     const frag_t<T> ak = x_rm(xk, LDX, 16 * mt, kk);
                     mma(u, ak, bh);
                     mma(u, ak, bl);
@@ -1207,21 +1238,16 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
 #pragma unroll
                 for (int j = 0; j < NTW; ++j) {
                     const int nt = NTW * half + j;
-                    frag_t<T> bh, bl;
-                    f_rm(sSb, LDB, 16 * nt, 0, bh, bl);  // B[k'][v] = S_J[k'][v]
-                    mma3(accA[j], gh, gl, bh, bl);
-                    f_rm(sDb, LDB, 16 * nt, 0, bh, bl);
-                    mma3(accB[j], uh, ul, bh, bl);
+                    mma3(accA[j], gh, gl, b_rm(sSh, 16 * nt), b_rm(sSl, 16 * nt));  // B[k'][v] = S_J[k'][v]
+                    mma3(accB[j], uh, ul, b_rm(sDh, 16 * nt), b_rm(sDl, 16 * nt));
                     sched_fence();  // one tile's operands live at a time
                 }
             } else {  // dQ_S += dO_J S_J^T;  dA -= G_U,J U_J^T;  dP += dO_J U_J^T
                 const frag_t<T> ao = x_rm(sO, LDV, 16 * mt, 0);
 #pragma unroll
                 for (int j = 0; j < NTW; ++j) {
-                    frag_t<T> bh, bl;
-                    f_rm(sSb, LDB, 16 * (NTW * half + j), 0, bh, bl);
-                    mma(accA[j], ao, bh);
-                    mma(accA[j], ao, bl);
+                    mma(accA[j], ao, b_rm(sSh, 16 * (NTW * half + j)));
+                    mma(accA[j], ao, b_rm(sSl, 16 * (NTW * half + j)));
                     sched_fence();
                 }
                 frag_t<T> gh, gl;
