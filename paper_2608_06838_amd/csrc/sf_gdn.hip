@@ -981,6 +981,11 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
     T *const sSh = reinterpret_cast<T *>(sBlk), *const sSl = sSh + D * VB;
     T *const sDh = sSl + D * VB, *const sDl = sDh + D * VB;
     auto bpos = [](int r, int ch) { return r * VB + ((((ch >> 3) ^ (r >> 2)) & 3) << 3) + (ch & 7); };
+    // T, once formed, as a hi/lo pair of C x C bf16 tiles in its own bytes (128-byte
+    // rows, the 16-byte blocks of row r XOR-swizzled by r % 8)
+    static_assert(2 * C * C * (int)sizeof(T) <= C * LD6 * 4, "T's pair fits its fp32 bytes");
+    T *const sTh = reinterpret_cast<T *>(sT), *const sTl = sTh + C * C;
+    auto tpos = [](int r, int c) { return r * C + ((((c >> 3) ^ r) & 7) << 3) + (c & 7); };
     float *const sE1 = sBlk, *const sE2 = sBlk + C * LD6;      // dP o Gamma, Ah + Ah^T
     float *const sR = sX, *const sdU = sX + C * LDR;           // [t][v] of the block
 
@@ -1027,6 +1032,19 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
         const int ch = c0 + 4 * (lane & 3), r0 = k0 + 8 * q4 + ((lane & 15) >> 2);
         const s4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)(M + bpos(r0, ch)));
         const s4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)(M + bpos(r0 + 4, ch)));
+        const s8 v = __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7);
+        return __builtin_bit_cast(frag_t<T>, v);
+    };
+    // the same two forms from T's tiles (tpos layout)
+    auto t_rm = [&](const T *M, int row0, int k0) {
+        return *reinterpret_cast<const frag_t<T> *>(M + tpos(row0 + n16, k0 + 8 * q4));
+    };
+    auto t_tr = [&](const T *M, int k0, int c0) {
+        typedef short s4 __attribute__((ext_vector_type(4)));
+        typedef short s8 __attribute__((ext_vector_type(8)));
+        const int ch = c0 + 4 * (lane & 3), r0 = k0 + 8 * q4 + ((lane & 15) >> 2);
+        const s4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)(M + tpos(r0, ch)));
+        const s4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)(M + tpos(r0 + 4, ch)));
         const s8 v = __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7);
         return __builtin_bit_cast(frag_t<T>, v);
     };
@@ -1142,6 +1160,21 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
         }
         __syncthreads();
         gdn_tinv<NTH>(tid, sX, sT, sbe);  // T = (I + diag(beta) KK o Gamma)^{-1}; ends with a barrier
+        {  // T -> its hi/lo pair, split once for every wave that reads it
+            static_assert(4 * NTH == C * C, "four elements of T per thread");
+            typedef T t4 __attribute__((ext_vector_type(4)));
+            const int r = (4 * tid) / C, c = (4 * tid) % C;
+            const f32x4 x = *reinterpret_cast<const f32x4 *>(&sT[r * LD6 + c]);
+            t4 h = {}, l = {};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                h[j] = cvt<T>(x[j]);
+                l[j] = cvt<T>(x[j] - tof<T>(h[j]));
+            }
+            __syncthreads();  // every fp32 read of T is done
+            *reinterpret_cast<t4 *>(&sTh[tpos(r, c)]) = h;
+            *reinterpret_cast<t4 *>(&sTl[tpos(r, c)]) = l;
+        }
 
         // one accumulator array, overlaid by role (both roles run the same code,
         // so separate arrays would all stay live on every wave):
@@ -1205,7 +1238,8 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
 #pragma unroll 1
                 for (int kk = 0; kk < C; kk += 32) {
                     frag_t<T> th, tl, rh, rl;
-                    f_rm(sT, LD6, 16 * mt, kk, th, tl);
+                    th = t_rm(sTh, 16 * mt, kk);
+                    tl = t_rm(sTl, 16 * mt, kk);
                     f_tr(sR, LDR, 16 * nb, kk, rh, rl);  // B[v][s] = R[s][v]
                     mma3(u, th, tl, rh, rl);
                 }
@@ -1216,7 +1250,8 @@ __global__ void __launch_bounds__(1024) k_gdn_dchunk(GdnArgs a) {
 #pragma unroll 1
                 for (int kk = 0; kk < C; kk += 32) {
                     frag_t<T> th, tl, dh, dl;
-                    f_tr(sT, LD6, 16 * mt, kk, th, tl);   // A[t][s] = T[s][t]
+                    th = t_tr(sTh, kk, 16 * mt);  // A[t][s] = T[s][t]
+                    tl = t_tr(sTl, kk, 16 * mt);
                     f_tr(sdU, LDR, 16 * nb, kk, dh, dl);  // B[v][s] = dU[s][v]
                     mma3(gu, th, tl, dh, dl);
                 }
