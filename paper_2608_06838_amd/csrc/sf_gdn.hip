@@ -563,24 +563,32 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_walk(GdnArgs a) {
 
 // S_{J+1} = M_J S_J + N_J for J = 0 .. n_super - 2 in fp32, S_0 = S_in (or 0);
 // writes S_J (J < n_super) to wsS; with scan_out (maps of every superchunk)
-// one more step gives S_out.  Workgroup (b, h, 16-column block); thread
-// row k = tid % D owns CPT consecutive columns of the block.  M_J is staged
-// in LDS (row pitch D + 4 floats) with the next one prefetched in registers.
+// one more step gives S_out.  Workgroup (b, h, 16-column block), four waves;
+// wave w owns the row tiles RTW w .. RTW w + RTW - 1 of the block, and the
+// product runs on the fp32 MFMA (16x16x4, fp32 products and sums): in step m
+// of the contraction lane (q4, n16) supplies M[row n16][KQ q4 + m] and
+// S[KQ q4 + m][col n16], the same order on both sides, so a lane's M operands
+// are KQ consecutive floats of its row.  M_J is staged in LDS (row pitch
+// D + 4 floats) with the next one prefetched in registers; S_J sits in LDS
+// (pitch 17) for the B operands.
 template <int D>
 __global__ void __launch_bounds__(256) k_gdn_scan(GdnArgs a) {
-    constexpr int NT = 256, RPT = NT / D, CPT = 16 / RPT, LDM = D + 4, MV = D * D / 4 / NT;
+    constexpr int NT = 256, LDM = D + 4, MV = D * D / 4 / NT, RTW = D / 64, KQ = D / 4, LS = 17;
     __shared__ __attribute__((aligned(16))) float sM[D * LDM];
-    __shared__ __attribute__((aligned(16))) float sS[D * 16];
-    const int tid = threadIdx.x, k = tid % D, cg = tid / D;
-    const int bh = blockIdx.x / (D / 16), col0 = 16 * (blockIdx.x % (D / 16)) + CPT * cg;
+    __shared__ float sS[D * LS];
+    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
+    const int bh = blockIdx.x / (D / 16), col0 = 16 * (blockIdx.x % (D / 16));
     const int64_t SS = (int64_t)D * D;
     const int nJ = a.n_super;
     float *wsS = a.wsS + (int64_t)bh * nJ * SS;
     const float *wsM = a.wsM + (int64_t)bh * a.n_prep * SS;
     const float *wsN = a.wsN + (int64_t)bh * a.n_prep * SS;
-    float acc[CPT];
+    auto row = [&](int i, int r) { return 16 * (RTW * w + i) + 4 * q4 + r; };
+    f32x4 acc[RTW];  // S[row(i, r)][col0 + n16]
 #pragma unroll
-    for (int j = 0; j < CPT; ++j) acc[j] = a.S_in ? a.S_in[bh * SS + (int64_t)k * D + col0 + j] : 0.f;
+    for (int i = 0; i < RTW; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[i][r] = a.S_in ? a.S_in[bh * SS + (int64_t)row(i, r) * D + col0 + n16] : 0.f;
     f32x4 mreg[MV];
     auto fetch = [&](int J) {
         const f32x4 *m = reinterpret_cast<const f32x4 *>(wsM + (int64_t)J * SS);
@@ -589,21 +597,22 @@ __global__ void __launch_bounds__(256) k_gdn_scan(GdnArgs a) {
     };
     const int last = a.scan_out ? nJ : nJ - 1;  // steps taken
     // S_J and S_out go out through buffer stores (32-bit lane offsets)
-    constexpr int NV = CPT / 4;
     const rsrc_t rS = buf_rsrc(wsS, (uint32_t)(nJ * SS * 4));
-    const uint32_t vo = (uint32_t)(((int64_t)k * D + col0) * 4);
     if (last > 0) fetch(0);
     for (int J = 0; J < nJ; ++J) {
 #pragma unroll
-        for (int u = 0; u < NV; ++u) {
-            const f32x4 x = {acc[4 * u], acc[4 * u + 1], acc[4 * u + 2], acc[4 * u + 3]};
-            *reinterpret_cast<f32x4 *>(&sS[k * 16 + col0 % 16 + 4 * u]) = x;
-            buf_st(rS, vo + 16 * u, (uint32_t)(J * SS * 4), x);
-        }
-        if (J == last) break;
-        float nv[CPT];
+        for (int i = 0; i < RTW; ++i)
 #pragma unroll
-        for (int j = 0; j < CPT; ++j) nv[j] = wsN[(int64_t)J * SS + (int64_t)k * D + col0 + j];
+            for (int r = 0; r < 4; ++r) {
+                sS[row(i, r) * LS + n16] = acc[i][r];
+                buf_st(rS, (uint32_t)((row(i, r) * D + col0 + n16) * 4), (uint32_t)(J * SS * 4), acc[i][r]);
+            }
+        if (J == last) break;
+        float nv[RTW][4];
+#pragma unroll
+        for (int i = 0; i < RTW; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) nv[i][r] = wsN[(int64_t)J * SS + (int64_t)row(i, r) * D + col0 + n16];
 #pragma unroll
         for (int i = 0; i < MV; ++i) {
             const int e = 4 * (tid + NT * i);
@@ -612,22 +621,27 @@ __global__ void __launch_bounds__(256) k_gdn_scan(GdnArgs a) {
         __syncthreads();
         if (J + 1 < last) fetch(J + 1);
 #pragma unroll
-        for (int j = 0; j < CPT; ++j) acc[j] = nv[j];
-#pragma unroll 4
-        for (int c = 0; c < D; c += 4) {
-            const f32x4 m4 = *reinterpret_cast<const f32x4 *>(&sM[k * LDM + c]);
+        for (int i = 0; i < RTW; ++i) acc[i] = f32x4{nv[i][0], nv[i][1], nv[i][2], nv[i][3]};
+#pragma unroll 2
+        for (int m = 0; m < KQ; m += 4) {
+            float bv[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < 4; ++u) bv[u] = sS[(KQ * q4 + m + u) * LS + n16];
 #pragma unroll
-                for (int j = 0; j < CPT; ++j) acc[j] = fmaf(m4[u], sS[(c + u) * 16 + col0 % 16 + j], acc[j]);
+            for (int i = 0; i < RTW; ++i) {
+                const f32x4 av = *reinterpret_cast<const f32x4 *>(&sM[(16 * (RTW * w + i) + n16) * LDM + KQ * q4 + m]);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], acc[i], 0, 0, 0);
+            }
         }
         __syncthreads();  // every read of sM and sS is done
     }
     if (a.scan_out) {  // the state after the last superchunk
         const rsrc_t rO = buf_rsrc(a.S_out + bh * SS, (uint32_t)(SS * 4));
 #pragma unroll
-        for (int u = 0; u < NV; ++u)
-            buf_st(rO, vo + 16 * u, 0u, f32x4{acc[4 * u], acc[4 * u + 1], acc[4 * u + 2], acc[4 * u + 3]});
+        for (int i = 0; i < RTW; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) buf_st(rO, (uint32_t)((row(i, r) * D + col0 + n16) * 4), 0u, acc[i][r]);
     }
 }
 
@@ -882,22 +896,27 @@ __global__ void __launch_bounds__(64 * D / 16) k_gdn_dwalk(GdnArgs a) {
 }
 
 // dS_end(n-1) = dS_out (or 0); dS_end(J-1) = M_J^T dS_end(J) + E_J, written to
-// wsDe for every J.  Same shape of work as k_gdn_scan, with M_J read transposed.
+// wsDe for every J.  Same shape of work as k_gdn_scan, with M_J read
+// transposed: in step m lane (q4, n16) supplies M[4 m + q4][row n16] (the
+// pitch D + 16 spreads the four q4 rows over the banks) and dS[4 m + q4][col].
 template <int D>
 __global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
-    constexpr int NT = 256, RPT = NT / D, CPT = 16 / RPT, LDM = D + 4, MV = D * D / 4 / NT;
+    constexpr int NT = 256, LDM = D + 16, MV = D * D / 4 / NT, RTW = D / 64, LS = 17;
     __shared__ __attribute__((aligned(16))) float sM[D * LDM];
-    __shared__ __attribute__((aligned(16))) float sS[D * 16];
-    const int tid = threadIdx.x, k = tid % D, cg = tid / D;
-    const int bh = blockIdx.x / (D / 16), col0 = 16 * (blockIdx.x % (D / 16)) + CPT * cg;
+    __shared__ float sS[D * LS];
+    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
+    const int bh = blockIdx.x / (D / 16), col0 = 16 * (blockIdx.x % (D / 16));
     const int64_t SS = (int64_t)D * D;
     const int nJ = a.n_super;
     float *wsDe = a.wsDe + (int64_t)bh * nJ * SS;
     const float *wsM = a.wsM + (int64_t)bh * a.n_prep * SS;
     const float *wsE = a.wsE + (int64_t)bh * (nJ - 1) * SS;
-    float acc[CPT];
+    auto row = [&](int i, int r) { return 16 * (RTW * w + i) + 4 * q4 + r; };
+    f32x4 acc[RTW];  // dS[row(i, r)][col0 + n16]
 #pragma unroll
-    for (int j = 0; j < CPT; ++j) acc[j] = a.dS_out ? a.dS_out[bh * SS + (int64_t)k * D + col0 + j] : 0.f;
+    for (int i = 0; i < RTW; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[i][r] = a.dS_out ? a.dS_out[bh * SS + (int64_t)row(i, r) * D + col0 + n16] : 0.f;
     f32x4 mreg[MV];
     auto fetch = [&](int J) {
         const f32x4 *m = reinterpret_cast<const f32x4 *>(wsM + (int64_t)J * SS);
@@ -907,14 +926,18 @@ __global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
     if (nJ > 1) fetch(nJ - 1);
     for (int J = nJ - 1;; --J) {
 #pragma unroll
-        for (int j = 0; j < CPT; ++j) {
-            sS[k * 16 + col0 % 16 + j] = acc[j];
-            wsDe[(int64_t)J * SS + (int64_t)k * D + col0 + j] = acc[j];
-        }
-        if (J == 0) break;
-        float nv[CPT];
+        for (int i = 0; i < RTW; ++i)
 #pragma unroll
-        for (int j = 0; j < CPT; ++j) nv[j] = wsE[(int64_t)(J - 1) * SS + (int64_t)k * D + col0 + j];
+            for (int r = 0; r < 4; ++r) {
+                sS[row(i, r) * LS + n16] = acc[i][r];
+                wsDe[(int64_t)J * SS + (int64_t)row(i, r) * D + col0 + n16] = acc[i][r];
+            }
+        if (J == 0) break;
+        float nv[RTW][4];
+#pragma unroll
+        for (int i = 0; i < RTW; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) nv[i][r] = wsE[(int64_t)(J - 1) * SS + (int64_t)row(i, r) * D + col0 + n16];
 #pragma unroll
         for (int i = 0; i < MV; ++i) {
             const int e = 4 * (tid + NT * i);
@@ -923,12 +946,14 @@ __global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
         __syncthreads();
         if (J - 1 >= 1) fetch(J - 1);
 #pragma unroll
-        for (int j = 0; j < CPT; ++j) acc[j] = nv[j];
+        for (int i = 0; i < RTW; ++i) acc[i] = f32x4{nv[i][0], nv[i][1], nv[i][2], nv[i][3]};
 #pragma unroll 4
-        for (int c = 0; c < D; ++c) {
-            const float m = sM[c * LDM + k];  // M_J^T[k][c]
+        for (int m = 0; m < D / 4; ++m) {
+            const float bv = sS[(4 * m + q4) * LS + n16];
 #pragma unroll
-            for (int j = 0; j < CPT; ++j) acc[j] = fmaf(m, sS[c * 16 + col0 % 16 + j], acc[j]);
+            for (int i = 0; i < RTW; ++i)
+                acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(sM[(4 * m + q4) * LDM + 16 * (RTW * w + i) + n16], bv, acc[i],
+                                                              0, 0, 0);
         }
         __syncthreads();
     }
