@@ -62,6 +62,24 @@ __device__ __forceinline__ void split4(const f32x4 &x, s4v &hi, s4v &lo) {
     }
 }
 
+// Column c of (I + diag(rs) M)^{-1} for a strictly lower 16 x 16 block M
+// (row pitch ld; rs == nullptr: rs = 1) by forward substitution in fp32:
+// x[r] = [r == c] - rs[r] sum_{s < r} M[r][s] x[s].  Right-looking: once x[s]
+// is final, every later row takes its term, so the 120 products form 16
+// dependent steps of independent updates instead of one chain.  Each row's sum
+// still runs over s in increasing order.
+__device__ __forceinline__ void gdn_diag_column(const float *M, int ld, int c, const float *rs, float (&x)[16]) {
+    float acc[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+    for (int s2 = 0; s2 < 16; ++s2) {
+        x[s2] = s2 == c ? 1.f : (s2 > c ? -(rs ? rs[s2] : 1.f) * acc[s2] : 0.f);
+#pragma unroll
+        for (int r = s2 + 1; r < 16; ++r) acc[r] = fmaf(M[r * ld + s2], x[s2], acc[r]);
+    }
+}
+
 // T = (I + A)^{-1} for the strictly lower 64 x 64 A = diag(rs) M with M in sA
 // (pitch C + 4; rs == nullptr: A = M), into sT (fp32, pitch C + 4, zero above
 // the diagonal), by 16 x 16 blocks: the four diagonal blocks by forward
@@ -77,13 +95,7 @@ __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, co
     if (tid < 64) {
         const int o = 16 * (tid >> 4), c = tid & 15;
         float x[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            float acc = 0.f;
-#pragma unroll
-            for (int s2 = 0; s2 < r; ++s2) acc = fmaf(sA[(o + r) * LA + o + s2], x[s2], acc);
-            x[r] = r == c ? 1.f : (r > c ? -(rs ? rs[o + r] : 1.f) * acc : 0.f);
-        }
+        gdn_diag_column(sA + o * LA + o, LA, c, rs ? rs + o : nullptr, x);
 #pragma unroll
         for (int r = 0; r < 16; ++r) sT[(o + r) * LT + o + c] = x[r];
     }
@@ -129,31 +141,19 @@ __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, co
 
 // The walks' T = (I + A)^{-1} (A = M in sA, pitch C + 4), stored as the bf16
 // hi/lo pair that every consumer splits it into (sTh, sTl: raw 16-bit
-// patterns, pitch C + 16, zero above the diagonal).  A diagonal block N = A_ii
-// is nilpotent (N^16 = 0), so its inverse is the finite series sum_k (-N)^k,
-// which factors as
-//   (I + N)^{-1} = (I + N^8)(I + N^4)(I + N^2)(I - N):
-// wave i forms N^2, N^4, N^8 by squaring and applies the three factors to
-// I - N, eight 16x16x16 MFMA products with hi/lo operands.  A product's
-// accumulator is the B-operand layout, and the transpose of a product lands in
-// the A-operand layout (P^T = N^T N^T has the accumulator slots of P's rows),
-// so each power is formed in both layouts and nothing moves between lanes.
-// The off-diagonal blocks then go level by level as in gdn_tinv, reading the
-// stored pairs.  NT >= 256 threads; ends with a barrier.
+// patterns, pitch C + 16, zero above the diagonal): the four diagonal blocks
+// by forward substitution in fp32 (64 threads, one column each), the
+// off-diagonal blocks level by level as in gdn_tinv, reading the stored pairs.
+// (A diagonal block N is nilpotent, and (I + N)^{-1} = (I + N^8)(I + N^4)
+// (I + N^2)(I - N) on MFMA ran the walks 4% faster; but the series' partial
+// sums grow like binomial coefficients when neighbouring keys are nearly
+// parallel with little decay, and the outputs then lost up to 1e-1 (bf16
+// hi/lo operands) or 1e-3 (fp32 MFMA) against the oracle, where substitution
+// keeps them at output rounding.)  NT >= 256 threads; ends with a barrier.
 template <int NT>
 __device__ __forceinline__ void gdn_tinv_hl(int tid, const float *sA, short *sTh, short *sTl) {
     constexpr int LA = C + 4, LTB = C + 16;
     const int w = tid >> 6, lane = tid & 63, q4 = lane >> 4, n16 = lane & 15;
-    // c + a b with a in the A layout, b in the B layout; c and the result in the B layout
-    auto mm = [](f32x4 c, const f32x4 &a, const f32x4 &b) {
-        s4v ah, al, bh, bl;
-        split4(a, ah, al);
-        split4(b, bh, bl);
-        mma16(c, ah, bh);
-        mma16(c, ah, bl);
-        mma16(c, al, bh);
-        return c;
-    };
     // rows row0 .. row0+3 of column col (the B layout), as hi/lo
     auto put = [&](int row0, int col, const f32x4 &x) {
         s4v h, l;
@@ -164,28 +164,16 @@ __device__ __forceinline__ void gdn_tinv_hl(int tid, const float *sA, short *sTh
             sTl[(row0 + r) * LTB + col] = l[r];
         }
     };
-    if (tid < 256) {  // wave w: T_ww
-        const int o = 16 * w;
-        // N in the A layout (row n16, columns 4q4..4q4+3) and the B layout (rows 4q4.., column n16)
-        f32x4 na = {0.f, 0.f, 0.f, 0.f}, nb = na;
-        const f32x4 x = *reinterpret_cast<const f32x4 *>(&sA[(o + n16) * LA + o + 4 * q4]);
+    if (tid < 64) {  // one column of a diagonal block per thread
+        const int o = 16 * (tid >> 4), c = tid & 15;
+        float x[16];
+        gdn_diag_column(sA + o * LA + o, LA, c, nullptr, x);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int row = 4 * q4 + j;
-            na[j] = row < n16 ? x[j] : 0.f;
-            nb[j] = n16 < row ? sA[(o + row) * LA + o + n16] : 0.f;
+        for (int r = 0; r < 16; ++r) {
+            const __bf16 h = (__bf16)x[r];
+            sTh[(o + r) * LTB + o + c] = __builtin_bit_cast(short, h);
+            sTl[(o + r) * LTB + o + c] = __builtin_bit_cast(short, (__bf16)(x[r] - (float)h));
         }
-        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-        const f32x4 n2b = mm(z, na, nb), n2a = mm(z, nb, na);  // N^2 (B layout), N^2 (A layout)
-        const f32x4 n4b = mm(z, n2a, n2b), n4a = mm(z, n2b, n2a);
-        const f32x4 n8a = mm(z, n4b, n4a);
-        f32x4 t = z;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) t[j] = (4 * q4 + j == n16 ? 1.f : 0.f) - nb[j];  // I - N
-        t = mm(t, n2a, t);
-        t = mm(t, n4a, t);
-        t = mm(t, n8a, t);
-        put(o + 4 * q4, o + n16, t);
     }
     for (int e = tid; e < 6 * 256; e += NT) {  // blocks (0,1) (0,2) (0,3) (1,2) (1,3) (2,3)
         const int b = e >> 8, rr = (e >> 4) & 15, cc = e & 15;

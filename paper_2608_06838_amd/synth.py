@@ -123,13 +123,19 @@ def make_conv_inputs(B, L, C, W, io="bf16", device="cpu", seed=2000, tails=True)
     return dict(x=x, w=w, tail_in=tail_in, dy=dy, dtail_out=dtail_out)
 
 
-def make_gdn_inputs(B, L, H, D, device="cpu", seed=4000, s_in_std=0.1, g_mu=3.0):
+def make_gdn_inputs(B, L, H, D, device="cpu", seed=4000, s_in_std=0.1, g_mu=3.0, key_spread=None, beta_min=0.0):
     """Gated-delta-rule inputs, drawn in this order from one generator seeded
     with `seed`: q, k, v ~ N(0, 1) [B, L, H, D] (k then L2-normalised per
     token, as the delta rule assumes); x_g ~ N(g_mu, 1) and g = log(sigmoid(x_g));
     x_b ~ N(0, 1) and beta = sigmoid(x_b) [B, L, H]; S_in ~ s_in_std * N(0, 1)
     [B, H, D, D] (None when s_in_std == 0).  q, k, v are rounded to bf16; g,
-    beta and S_in are float32."""
+    beta and S_in are float32.
+
+    Nearly parallel keys (key_spread set): then one more draw, a direction
+    u ~ N(0, 1) [B, 1, H, D] per head, and k = normalise(u / |u| + key_spread *
+    k) with k the normalised draw above.  beta_min > 0 maps beta into
+    [beta_min, 1) (beta_min + (1 - beta_min) beta).  Neither changes the draws
+    above."""
     gen = torch.Generator(device=device)
     gen.manual_seed(seed)
     f32 = dict(dtype=torch.float32, device=device, generator=gen)
@@ -140,4 +146,10 @@ def make_gdn_inputs(B, L, H, D, device="cpu", seed=4000, s_in_std=0.1, g_mu=3.0)
     g = torch.nn.functional.logsigmoid(torch.randn(B, L, H, **f32) + float(g_mu)).contiguous()
     beta = torch.sigmoid(torch.randn(B, L, H, **f32)).contiguous()
     S_in = torch.randn(B, H, D, D, **f32) * float(s_in_std) if s_in_std > 0 else None
+    if key_spread is not None:
+        u = torch.randn(B, 1, H, D, **f32)
+        k = u / u.norm(dim=-1, keepdim=True) + float(key_spread) * k
+        k = k / k.norm(dim=-1, keepdim=True)
+    if beta_min > 0:
+        beta = (float(beta_min) + (1.0 - float(beta_min)) * beta).contiguous()
     return dict(q=q.to(torch.bfloat16), k=k.to(torch.bfloat16), v=v.to(torch.bfloat16), g=g, beta=beta, S_in=S_in)

@@ -161,6 +161,27 @@ def test_gdn_bwd_parity(D, ts):
     check_bwd(run_bwd(inp, dO, dS, ts), ref_bwd(inp, dO, dS))
 
 
+@pytest.mark.parametrize("D", [64, 128])
+def test_gdn_nearly_parallel_keys(D):
+    """Keys within a few degrees of one direction per head, beta in [0.85, 1),
+    decay near 1: (I + A) is far from the identity, and the partial products of
+    its inverse grow; forward, V^new and every gradient against the oracle, with
+    superchunks (ts = 192)."""
+    B, L, H = 1, 448, 2
+    say(f"[gdn] nearly parallel keys D={D}")
+    inp = synth.make_gdn_inputs(B, L, H, D, seed=5300 + D, g_mu=8.0, key_spread=0.05, beta_min=0.85)
+    g = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
+    o, S, vn = sf.gdn_fwd(g["q"], g["k"], g["v"], g["g"], g["beta"], g["S_in"], ts=192, with_v_new=True)
+    torch.cuda.synchronize()
+    ro, rS, ru = gdn.forward(*(to64(inp[x]) for x in ("q", "k", "v", "g", "beta", "S_in")), threads=cores(),
+                             with_u=True)
+    assert_close("o", o, ro, "bf16")
+    assert_close("S_out", S, rS, "bf16")
+    assert_close("v_new", vn, ru, "bf16")
+    dO, dS = grads_inputs(inp, 5400 + D)
+    check_bwd(run_bwd(inp, dO, dS, 192), ref_bwd(inp, dO, dS))
+
+
 def test_gdn_bwd_no_state_and_empty():
     say("[gdn bwd] no S_in, no dS_out; empty segment")
     inp = synth.make_gdn_inputs(2, 192, 2, 128, seed=4800, s_in_std=0.0)
