@@ -616,17 +616,19 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 //   G   <- exp(b_63) G + Q^T (exp(b) o dO)          (and its transpose)
 //   dg_t = sum_{t' >= t in superchunk} (q.dq - k.dk)_{t'} + <G_{J+1}, S_{J+1}>
 // (the last term is the decay gradient carried in from later superchunks).
-// The workgroup has two halves of D/16 waves.  Wave j of the v-side half keeps
-// G[k][v] for v-tile j (an A-operand fragment for dv) and computes dv; wave j
-// of the k-side half keeps G^T[v][k] for k-tile j and computes dk and k.dk.
-// Each half updates only its own orientation, so per wave the products, the
-// hi/lo splits and the registers are half of a both-orientations walk, and the
-// four waves per SIMD (d = 128) hide each other's latency.  The v-side half
-// stages q and dO, the k-side half k and v.  LDS holds natural tiles only: K
-// and V plain and unswizzled (they meet the accumulator-built G fragments,
-// reordered by split_acc_plain), Q and dO plain and swizzled for the
-// transposing loads of the G updates, where the per-token decay goes on the
-// wave's own columns.
+// The workgroup has two halves of D/(16 NCT) waves.  Wave j of the v-side half
+// keeps G[k][v] for its NCT v-tiles (A-operand fragments for dv) and computes
+// dv; wave j of the k-side half keeps G^T[v][k] for its NCT k-tiles and
+// computes dk and k.dk.  Each half updates only its own orientation, so per
+// wave the products, the hi/lo splits and the registers are half of a
+// both-orientations walk.  bf16 at d = 128 runs NCT = 2 (8 waves, two per SIMD,
+// every K/V/Q/dO fragment read from LDS feeding four MFMAs); the other forms
+// NCT = 1.  The v-side half stages q and dO, the k-side half k and v.  LDS
+// holds natural tiles only: K and V plain and unswizzled (they meet the G
+// fragments split from accumulator pairs: bf16 builds G's rows in the split's
+// plain order, see the update; fp32 reorders them with split_acc_plain), Q and
+// dO plain and swizzled for the transposing loads of the G updates, where the
+// per-token decay goes on the wave's own columns.
 template <typename T, int D, int NCT>
 __global__ void __launch_bounds__(128 * D / (16 * NCT)) k_bwd_dkv(SegArgs a) {
     constexpr int NJ = D / (16 * NCT), NW = 2 * NJ, NT = 64 * NW, NH = NT / 2, NK = D / 16;
