@@ -317,6 +317,15 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     constexpr bool RP = sizeof(T) == 2;
     const LaneOff tro8 = RP ? tr_off8<T, LDN, SWX>(lane) : tro;  // (tr_off8 serves 16-bit tiles only)
     auto srow = [&](int i, int r) { return RP ? 32 * (i >> 1) + 8 * q4 + 4 * (i & 1) + r : 16 * i + 4 * q4 + r; };
+    // bf16 with two column tiles per wave: the state's columns (the value
+    // channels of the update's own operand, read through tro8) in the order
+    // that gives lane row q4 channels 32w + 8 q4 .. +7 across the two tiles of
+    // the output accumulators, so its q values and its output row segments are
+    // single 16-byte accesses: column n of tile ct is channel scol(ct, n)
+    constexpr bool CP = RP && NCT == 2;
+    auto scol = [&](int ct, int n) { return CP ? 32 * w + 8 * (n >> 2) + 4 * ct + (n & 3) : 16 * (NCT * w + ct) + n; };
+    const int ccol0 = CP ? 32 * w : 16 * NCT * w, ccstep = CP ? 4 : 16;  // ldfragTR column of tile ct
+    const LaneOff troc = CP ? tro8 : tro;
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *X1 = (const T *)(DQ ? a.dO : a.q) + xo;
     const T *X2 = (const T *)(DQ ? a.v : a.k) + xo;
@@ -336,7 +345,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
         for (int i = 0; i < NK; ++i) {
-            const int col = 16 * (NCT * w + ct) + n16;
+            const int col = scol(ct, n16);
             if (!src) {
                 S[ct][i] = f32x4{0.f, 0.f, 0.f, 0.f};
             } else if constexpr (!DQ) {
@@ -358,7 +367,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     uint32_t toff[Tile<T, D, NT>::RPT];
     Tile<T, D, NT>::offsets(toff, a.sx_l, tid);
     const uint32_t goff = (uint32_t)(lane * a.sg_l * 4);
-    const uint32_t aoff = (uint32_t)((n16 * a.sx_l + 16 * NCT * w + 4 * q4) * (int64_t)sizeof(T));
+    const uint32_t aoff = (uint32_t)((n16 * a.sx_l + (CP ? 32 * w + 8 * q4 : 16 * NCT * w + 4 * q4)) * (int64_t)sizeof(T));
     const uint32_t tstep = (uint32_t)(16 * a.sx_l * (int64_t)sizeof(T));
     // the next chunk's tiles go out in three batches (X1 and g at staging, X2 at
     // the start of the scores, X3 at the start of the output products), so the
@@ -372,21 +381,39 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     auto issue3 = [&](int c) { t3.load_buf(buf_rsrc(X3 + c * cstep, cspan), toff, 0); };
     auto issue_q = [&](int c) {  // DQ: q at this lane's dq elements, read after chunk c-1's dot
         const rsrc_t rq = buf_rsrc(Qd + c * cstep, cspan);
+        if constexpr (CP) {  // channels 32w + 8q4 .. +7: tile 0's four, then tile 1's
+            typedef T vec8T __attribute__((ext_vector_type(8)));
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct)
+            for (int tt = 0; tt < 4; ++tt) {
+                const vec8T x = buf_ld<vec8T>(rq, aoff, tt * tstep);
+                qn[tt] = __builtin_shufflevector(x, x, 0, 1, 2, 3);
+                qn[4 + tt] = __builtin_shufflevector(x, x, 4, 5, 6, 7);
+            }
+        } else {
 #pragma unroll
-            for (int tt = 0; tt < 4; ++tt)
-                qn[4 * ct + tt] = buf_ld<vec4T>(rq, aoff + 16 * ct * (uint32_t)sizeof(T), tt * tstep);
+            for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                for (int tt = 0; tt < 4; ++tt)
+                    qn[4 * ct + tt] = buf_ld<vec4T>(rq, aoff + 16 * ct * (uint32_t)sizeof(T), tt * tstep);
+        }
     };
     vec4T yo[NCT][4];  // this lane's outputs of the chunk, accumulator layout
     // a chunk's outputs go registers -> LDS tile (once every wave is done with the
     // score tiles) -> whole-row 16-byte global stores early in the next chunk
     auto put_y = [&]() {
-#pragma unroll
-        for (int ct = 0; ct < NCT; ++ct)
+        if constexpr (CP) {  // one 16-byte row segment per token tile
+            typedef T vec8T __attribute__((ext_vector_type(8)));
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
-                *reinterpret_cast<vec4T *>(&sY[(16 * tt + n16) * LDY + 16 * (NCT * w + ct) + 4 * q4]) = yo[ct][tt];
+                *reinterpret_cast<vec8T *>(&sY[(16 * tt + n16) * LDY + 32 * w + 8 * q4]) =
+                    __builtin_shufflevector(yo[0][tt], yo[1][tt], 0, 1, 2, 3, 4, 5, 6, 7);
+        } else {
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+                for (int tt = 0; tt < 4; ++tt)
+                    *reinterpret_cast<vec4T *>(&sY[(16 * tt + n16) * LDY + 16 * (NCT * w + ct) + 4 * q4]) = yo[ct][tt];
+        }
     };
     auto store_y = [&](int cp) {
         typedef typename Tile<T, D, NT>::vecE vecE;
@@ -496,7 +523,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         for (int ks = 0; ks < C / 32; ++ks) {
             frag_t<T> vf[NCT];
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) vf[ct] = ldfragTR<T, LDN, SWX>(sX3, tro, 32 * ks, 16 * (NCT * w + ct));
+            for (int ct = 0; ct < NCT; ++ct) vf[ct] = ldfragTR<T, LDN, SWX>(sX3, troc, 32 * ks, ccol0 + ccstep * ct);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
                 if (32 * ks > 16 * tt + 15) continue;
@@ -550,7 +577,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             frag_t<T> vh[NCT], vl[NCT];
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct)
-                split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sX3, tro, 32 * ks, 16 * (NCT * w + ct)), ev, vh[ct], vl[ct]);
+                split_scaled<T, SPD>(ldfragTR<T, LDN, SWX>(sX3, troc, 32 * ks, ccol0 + ccstep * ct), ev, vh[ct], vl[ct]);
 #pragma unroll
             for (int i = 0; i < NK; ++i) {
                 const frag_t<T> kf = ldfragTR<T, LDN, SWX>(sX2, tro8, 32 * ks, RP ? 32 * (i >> 1) + 4 * (i & 1) : 16 * i);
@@ -583,7 +610,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
                     for (int i = 0; i < NK; ++i)
 #pragma unroll
                         for (int r = 0; r < 4; ++r)
-                            dst[(int64_t)srow(i, r) * D + 16 * (NCT * w + ct) + n16] = S[ct][i][r];
+                            dst[(int64_t)srow(i, r) * D + scol(ct, n16)] = S[ct][i][r];
             }
         } else {
             // <dS_out, S_out> for dg (the state here is S_out^T)
@@ -595,7 +622,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
 #pragma unroll
                     for (int i = 0; i < NK; ++i) {
                         const f32x4 x = *reinterpret_cast<const f32x4 *>(
-                            ds + (int64_t)(16 * (NCT * w + ct) + n16) * D + srow(i, 0));
+                            ds + (int64_t)scol(ct, n16) * D + srow(i, 0));
                         p += x[0] * S[ct][i][0] + x[1] * S[ct][i][1] + x[2] * S[ct][i][2] + x[3] * S[ct][i][3];
                     }
             }
