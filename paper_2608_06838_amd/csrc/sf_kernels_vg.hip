@@ -39,7 +39,8 @@ constexpr float kMinChunkLog2 = -100.f;  // fast path iff every channel keeps >=
 template <typename T, int D, int NT>
 struct GTile {
     using TT = Tile<T, D, NT>;
-    static constexpr int E = TT::E, RPT = TT::RPT, CB = TT::CB, NG = NT / CB, NV = E / 4;
+    static constexpr int E = TT::E, RPT = TT::RPT, CB = TT::CB, NV = E / 4;
+    static constexpr int SCR = NT / 64 * D;  // floats of gate_cumsum scratch
     f32x4 r[RPT][NV];
     __device__ __forceinline__ void load(const float *g, int64_t ls, int tid) {
         const float *p = g + (int64_t)(tid / CB) * RPT * ls + (tid % CB) * E;
@@ -53,14 +54,22 @@ struct GTile {
 
 // Per-channel inclusive cumulative log2-decay over the chunk for this thread's
 // tile elements (b[j][c]) and the chunk totals of its channels (tot[c]).
-// scratch holds NG x D floats; there is one barrier inside, and the caller
-// must pass a barrier before scratch is written again.
+// A thread sums its own rows in registers; the row groups of a wave (threads
+// CB lanes apart) are combined by lane swaps (DPP rotate within a 16-lane row,
+// then the 16- and 32-lane swaps of gfx950), the waves through scratch
+// (NT/64 x D floats).  Every thread adds the wave totals in the same order, so
+// tot[c] is the same value in every thread, and it is also the value of the
+// last row's b.  There is one barrier inside; the
+// caller must pass a barrier before scratch is written again.
 template <typename T, int D, int NT>
 __device__ __forceinline__ void gate_cumsum(const GTile<T, D, NT> &gt, float (&b)[GTile<T, D, NT>::RPT][GTile<T, D, NT>::E],
                                             float (&tot)[GTile<T, D, NT>::E], float *scratch, int tid) {
     using G = GTile<T, D, NT>;
-    constexpr int E = G::E, RPT = G::RPT;
-    const int grp = tid / G::CB, ch0 = (tid % G::CB) * E;
+    constexpr int E = G::E, RPT = G::RPT, CB = G::CB, NW = NT / 64;
+    static_assert(CB == 8 || CB == 16 || CB == 32, "row groups of a wave");
+    const int lane = tid & 63, ch0 = (tid % CB) * E;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    float pre[E], wt[E];
 #pragma unroll
     for (int c = 0; c < E; ++c) {
         float acc = 0.f;
@@ -69,30 +78,68 @@ __device__ __forceinline__ void gate_cumsum(const GTile<T, D, NT> &gt, float (&b
             acc += gt.at(j, c) * LOG2E;
             b[j][c] = acc;
         }
+        // exclusive prefix over the wave's lower row groups (p) and the wave total (x)
+        float x = acc, p = 0.f;
+        if constexpr (CB == 8) {  // the other group of the 16-lane row: lanes l ^ 8
+            const float z = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x128, 0xf, 0xf, false));
+            if (lane & 8) p = z;
+            x += z;
+        }
+        if constexpr (CB <= 16) {  // rows 2r, 2r+1 of the wave: [0] the even row's, [1] the odd row's
+            const unsigned u = __builtin_bit_cast(unsigned, x);
+            const auto s = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+            const float lo = __builtin_bit_cast(float, (unsigned)s[0]), hi = __builtin_bit_cast(float, (unsigned)s[1]);
+            if (lane & 16) p += lo;
+            x = lo + hi;
+        }
+        {  // lanes 0-31 and 32-63: [0] the lower half's, [1] the upper half's
+            const unsigned u = __builtin_bit_cast(unsigned, x);
+            const auto s = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+            const float lo = __builtin_bit_cast(float, (unsigned)s[0]), hi = __builtin_bit_cast(float, (unsigned)s[1]);
+            if (lane & 32) p += lo;
+            x = lo + hi;
+        }
+        pre[c] = p;
+        wt[c] = x;
     }
+    if (lane < CB) {
 #pragma unroll
-    for (int v = 0; v < G::NV; ++v)
-        *reinterpret_cast<f32x4 *>(&scratch[grp * D + ch0 + 4 * v]) =
-            f32x4{b[RPT - 1][4 * v], b[RPT - 1][4 * v + 1], b[RPT - 1][4 * v + 2], b[RPT - 1][4 * v + 3]};
+        for (int v = 0; v < G::NV; ++v)
+            *reinterpret_cast<f32x4 *>(&scratch[w * D + ch0 + 4 * v]) = f32x4{wt[4 * v], wt[4 * v + 1], wt[4 * v + 2], wt[4 * v + 3]};
+    }
     __syncthreads();
-    float pre[E];
+    float pw[E];
 #pragma unroll
-    for (int c = 0; c < E; ++c) pre[c] = tot[c] = 0.f;
-    for (int g2 = 0; g2 < G::NG; ++g2) {
+    for (int c = 0; c < E; ++c) pw[c] = 0.f;
+    for (int v2 = 0; v2 < w; ++v2) {  // waves before this one
 #pragma unroll
         for (int v = 0; v < G::NV; ++v) {
-            const f32x4 x = *reinterpret_cast<const f32x4 *>(&scratch[g2 * D + ch0 + 4 * v]);
+            const f32x4 x = *reinterpret_cast<const f32x4 *>(&scratch[v2 * D + ch0 + 4 * v]);
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                tot[4 * v + u] += x[u];
-                if (g2 < grp) pre[4 * v + u] += x[u];
-            }
+            for (int u = 0; u < 4; ++u) pw[4 * v + u] += x[u];
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < E; ++c) tot[c] = pw[c];
+    for (int v2 = w; v2 < NW; ++v2) {
+#pragma unroll
+        for (int v = 0; v < G::NV; ++v) {
+            const f32x4 x = *reinterpret_cast<const f32x4 *>(&scratch[v2 * D + ch0 + 4 * v]);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) tot[4 * v + u] += x[u];
         }
     }
 #pragma unroll
     for (int j = 0; j < RPT; ++j)
 #pragma unroll
-        for (int c = 0; c < E; ++c) b[j][c] += pre[c];
+        for (int c = 0; c < E; ++c) b[j][c] += pw[c] + pre[c];
+    // the chunk's last row is its total, to the bit: factors 2^(tot - b) of that
+    // row are exactly 1 however far the chunk decays (its exponent would
+    // otherwise carry the rounding of a sum of magnitude |tot|)
+    if (tid / CB == NT / CB - 1) {
+#pragma unroll
+        for (int c = 0; c < E; ++c) b[RPT - 1][c] = tot[c];
+    }
 }
 
 // Stores tile t scaled per element by f[j][c] as a hi/lo pair of natural tiles:
@@ -161,7 +208,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     __shared__ __attribute__((aligned(16))) T sX[C * LDN];
     __shared__ __attribute__((aligned(16))) T sXl[SP ? C * LDN : 8];
     __shared__ __attribute__((aligned(16))) T sY[C * LDN];
-    __shared__ __attribute__((aligned(16))) float scratch[GT::NG * D];
+    __shared__ __attribute__((aligned(16))) float scratch[GT::SCR];
     __shared__ __attribute__((aligned(16))) float sE63[D];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
@@ -267,7 +314,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_walk_vg(SegArgs a) {
     __shared__ __attribute__((aligned(16))) T sK[C * LDN];   // K o 2^-b, plain, swizzled (hi)
     __shared__ __attribute__((aligned(16))) T sKl[SP ? C * LDN : 8];
     __shared__ __attribute__((aligned(16))) T sV[C * LDN];   // plain, swizzled
-    constexpr int AB = 2 * C * LDT * (int)sizeof(T), SB = GT::NG * D * 4;
+    constexpr int AB = 2 * C * LDT * (int)sizeof(T), SB = GT::SCR * 4;
     __shared__ __attribute__((aligned(16))) char sAraw[AB > SB ? AB : SB];  // A hi/lo, or the gate scratch
     T *sA = reinterpret_cast<T *>(sAraw), *sAl = sA + C * LDT;
     float *scratch = reinterpret_cast<float *>(sAraw);
@@ -488,7 +535,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dq_vg(SegArgs a) {
     __shared__ __attribute__((aligned(16))) T sV[C * LDN];   // plain, swizzled
     __shared__ __attribute__((aligned(16))) T sK[C * LDN];   // K o 2^-b, plain, swizzled (hi)
     __shared__ __attribute__((aligned(16))) T sKl[SP ? C * LDN : 8];
-    constexpr int AB = 2 * C * LDT * (int)sizeof(T), SB = GT::NG * D * 4;
+    constexpr int AB = 2 * C * LDT * (int)sizeof(T), SB = GT::SCR * 4;
     __shared__ __attribute__((aligned(16))) char sPraw[AB > SB ? AB : SB];  // P hi/lo, or the gate scratch
     T *sP = reinterpret_cast<T *>(sPraw), *sPl = sP + C * LDT;
     float *scratch = reinterpret_cast<float *>(sPraw);
@@ -732,7 +779,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dv_vg(SegArgs a) {
     __shared__ __attribute__((aligned(16))) T sK[C * LDN];   // K o 2^-b, nat_pos order (hi)
     __shared__ __attribute__((aligned(16))) T sKl[SP ? C * LDN : 8];
     __shared__ __attribute__((aligned(16))) T sO[C * LDN];   // dO, plain, swizzled
-    constexpr int AB = 2 * C * LDT * (int)sizeof(T), SB = GT::NG * D * 4;
+    constexpr int AB = 2 * C * LDT * (int)sizeof(T), SB = GT::SCR * 4;
     __shared__ __attribute__((aligned(16))) char sAraw[AB > SB ? AB : SB];  // A^T hi/lo, or the gate scratch
     T *sAT = reinterpret_cast<T *>(sAraw), *sATl = sAT + C * LDT;
     float *scratch = reinterpret_cast<float *>(sAraw);
@@ -961,7 +1008,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), 1) k_dk_vg(SegArgs a) {
     __shared__ __attribute__((aligned(16))) T sV[C * LDN];   // nat_pos order
     __shared__ __attribute__((aligned(16))) T sO[C * LDN];   // dO, plain, swizzled
     __shared__ __attribute__((aligned(16))) T sKr[C * LDN];  // k, plain
-    constexpr int AB = 2 * C * LDT * (int)sizeof(T), SB = GT::NG * D * 4;
+    constexpr int AB = 2 * C * LDT * (int)sizeof(T), SB = GT::SCR * 4;
     __shared__ __attribute__((aligned(16))) char sPraw[AB > SB ? AB : SB];  // P^T hi/lo, or the gate scratch
     T *sPT = reinterpret_cast<T *>(sPraw), *sPTl = sPT + C * LDT;
     float *scratch = reinterpret_cast<float *>(sPraw);
