@@ -21,6 +21,7 @@
 // then fits in half the registers and two waves share each SIMD):
 //   k_prep_vg<BWD=false>  D_J and the per-channel superchunk decay
 //   k_prep_vg<BWD=true>   E_J = sum_t diag(2^{B_t}) q_t dO_t^T
+//   k_prep_vg_bwd         the backward's replay of D_J and its E_J in one launch
 //   k_walk_vg             o (and S_out for a one-superchunk segment)
 //   k_dq_vg               dq and q o dq (into dg) by a forward walk
 //   k_dv_vg               dv by a reverse walk with G
@@ -197,22 +198,21 @@ __device__ __forceinline__ f32x4 ld4(const T *p) {
 //   E_J = sum_t diag(2^{B_t}) q_t dO_t^T  (BWD; B superchunk-local, inclusive)
 // Every factor is <= 1; the scaled key (query) tile is the shared exact-split
 // A operand, V (dO) the wave's own columns.
+// One superchunk (item) of either summary; the LDS arrays are the caller's:
+// sX, sXl (C x (D + pad) each), sY (the same), scratch (the gate cumsum's) and
+// sE63 (D floats).
 template <typename T, int D, int NCT, bool BWD>
-__global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_prep_vg(SegArgs a) {
+__device__ __forceinline__ void prep_vg_item(const SegArgs &a, int item, T *sX, T *sXl, T *sY, float *scratch,
+                                             float *sE63) {
     constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
     constexpr int LDN = D + pad<T>(), SWX = swx<T, D>();
     constexpr bool SP = kSplit<T>;
     using TT = Tile<T, D, NT>;
     using GT = GTile<T, D, NT>;
     constexpr int E = TT::E, RPT = TT::RPT;
-    __shared__ __attribute__((aligned(16))) T sX[C * LDN];
-    __shared__ __attribute__((aligned(16))) T sXl[SP ? C * LDN : 8];
-    __shared__ __attribute__((aligned(16))) T sY[C * LDN];
-    __shared__ __attribute__((aligned(16))) float scratch[GT::SCR];
-    __shared__ __attribute__((aligned(16))) float sE63[D];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
-    const Decode d = decode(a);
+    const Decode d = decode(a, item);
     const LaneOff tro = tr_off<T, LDN, SWX>(lane);
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *X = (const T *)(BWD ? a.q : a.k) + xo;
@@ -298,6 +298,32 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         for (int cc = 0; cc < E; ++cc) lg[ch0 + cc] = off[cc];
     }
 }
+
+#define SF_PREP_VG_LDS                                                           \
+    constexpr int LDN = D + pad<T>();                                          \
+    __shared__ __attribute__((aligned(16))) T sX[C * LDN];                     \
+    __shared__ __attribute__((aligned(16))) T sXl[kSplit<T> ? C * LDN : 8];    \
+    __shared__ __attribute__((aligned(16))) T sY[C * LDN];                     \
+    __shared__ __attribute__((aligned(16))) float scratch[GTile<T, D, 64 * D / (16 * NCT)>::SCR]; \
+    __shared__ __attribute__((aligned(16))) float sE63[D];
+
+template <typename T, int D, int NCT, bool BWD>
+__global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_prep_vg(SegArgs a) {
+    SF_PREP_VG_LDS
+    prep_vg_item<T, D, NCT, BWD>(a, (int)blockIdx.x, sX, sXl, sY, scratch, sE63);
+}
+
+// The backward's two summaries in one launch: workgroups [0, n) replay D_J,
+// [n, 2n) form E_J (n = B H n_super); two workgroups share a CU, so the two
+// halves overlap.
+template <typename T, int D, int NCT>
+__global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_prep_vg_bwd(SegArgs a) {
+    SF_PREP_VG_LDS
+    const int n = (int)(gridDim.x / 2), item = (int)blockIdx.x;
+    if (item < n) prep_vg_item<T, D, NCT, false>(a, item, sX, sXl, sY, scratch, sE63);
+    else prep_vg_item<T, D, NCT, true>(a, item - n, sX, sXl, sY, scratch, sE63);
+}
+#undef SF_PREP_VG_LDS
 
 // ---------------------------------------------------------------------------
 // Forward walker (vector gate): o over the chunks of one superchunk.
@@ -1289,8 +1315,7 @@ static hipError_t launch_vg_td(int kind, const SegArgs &a, hipStream_t s, hipEve
         if (a.ckpt) {
             hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, true>), grid, dim3(NT), 0, s, e0, e1, 0, a);
         } else {
-            hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, false>), grid, dim3(NT), 0, s, e0, nullptr, 0, a);
-            hipExtLaunchKernelGGL((k_prep_vg<T, D, NCT, true>), grid, dim3(NT), 0, s, nullptr, e1, 0, a);
+            hipExtLaunchKernelGGL((k_prep_vg_bwd<T, D, NCT>), dim3(2 * grid.x), dim3(NT), 0, s, e0, e1, 0, a);
         }
         break;
     case SF_K_BWD_DQ: hipExtLaunchKernelGGL((k_dq_vg<T, D, NCT>), grid, dim3(NT), 0, s, e0, e1, 0, a); break;
