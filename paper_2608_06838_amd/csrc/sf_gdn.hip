@@ -577,17 +577,24 @@ __global__ void __launch_bounds__(256) k_gdn_scan(GdnArgs a) {
     for (int i = 0; i < RTW; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[i][r] = a.S_in ? a.S_in[bh * SS + (int64_t)row(i, r) * D + col0 + n16] : 0.f;
-    f32x4 mreg[MV];
-    auto fetch = [&](int J) {
+    // M_J and N_J two steps ahead, in two register sets used alternately
+    f32x4 mA[MV], mB[MV];
+    float nA[RTW][4], nB[RTW][4];
+    auto fetch = [&](f32x4 (&mr)[MV], float (&nr)[RTW][4], int J) {
         const f32x4 *m = reinterpret_cast<const f32x4 *>(wsM + (int64_t)J * SS);
 #pragma unroll
-        for (int i = 0; i < MV; ++i) mreg[i] = m[tid + NT * i];
+        for (int i = 0; i < MV; ++i) mr[i] = m[tid + NT * i];
+#pragma unroll
+        for (int i = 0; i < RTW; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) nr[i][r] = wsN[(int64_t)J * SS + (int64_t)row(i, r) * D + col0 + n16];
     };
     const int last = a.scan_out ? nJ : nJ - 1;  // steps taken
     // S_J and S_out go out through buffer stores (32-bit lane offsets)
     const rsrc_t rS = buf_rsrc(wsS, (uint32_t)(nJ * SS * 4));
-    if (last > 0) fetch(0);
-    for (int J = 0; J < nJ; ++J) {
+    // step J: store S_J; unless J is the last, S_{J+1} = M_J S_J + N_J from
+    // (mr, nr), which then take the maps of J + 2; false after the last store
+    auto step = [&](int J, f32x4 (&mr)[MV], float (&nr)[RTW][4]) {
 #pragma unroll
         for (int i = 0; i < RTW; ++i)
 #pragma unroll
@@ -595,21 +602,16 @@ __global__ void __launch_bounds__(256) k_gdn_scan(GdnArgs a) {
                 sS[row(i, r) * LS + n16] = acc[i][r];
                 buf_st(rS, (uint32_t)((row(i, r) * D + col0 + n16) * 4), (uint32_t)(J * SS * 4), acc[i][r]);
             }
-        if (J == last) break;
-        float nv[RTW][4];
-#pragma unroll
-        for (int i = 0; i < RTW; ++i)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) nv[i][r] = wsN[(int64_t)J * SS + (int64_t)row(i, r) * D + col0 + n16];
+        if (J == last) return false;
 #pragma unroll
         for (int i = 0; i < MV; ++i) {
             const int e = 4 * (tid + NT * i);
-            *reinterpret_cast<f32x4 *>(&sM[(e / D) * LDM + e % D]) = mreg[i];
+            *reinterpret_cast<f32x4 *>(&sM[(e / D) * LDM + e % D]) = mr[i];
         }
         __syncthreads();
-        if (J + 1 < last) fetch(J + 1);
 #pragma unroll
-        for (int i = 0; i < RTW; ++i) acc[i] = f32x4{nv[i][0], nv[i][1], nv[i][2], nv[i][3]};
+        for (int i = 0; i < RTW; ++i) acc[i] = f32x4{nr[i][0], nr[i][1], nr[i][2], nr[i][3]};
+        if (J + 2 < last) fetch(mr, nr, J + 2);
 #pragma unroll 2
         for (int m = 0; m < KQ; m += 4) {
             float bv[4];
@@ -623,7 +625,12 @@ __global__ void __launch_bounds__(256) k_gdn_scan(GdnArgs a) {
             }
         }
         __syncthreads();  // every read of sM and sS is done
-    }
+        return true;
+    };
+    if (last > 0) fetch(mA, nA, 0);
+    if (last > 1) fetch(mB, nB, 1);
+    for (int J = 0;; J += 2)
+        if (!step(J, mA, nA) || !step(J + 1, mB, nB)) break;
     if (a.scan_out) {  // the state after the last superchunk
         const rsrc_t rO = buf_rsrc(a.S_out + bh * SS, (uint32_t)(SS * 4));
 #pragma unroll
@@ -905,14 +912,21 @@ __global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
     for (int i = 0; i < RTW; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[i][r] = a.dS_out ? a.dS_out[bh * SS + (int64_t)row(i, r) * D + col0 + n16] : 0.f;
-    f32x4 mreg[MV];
-    auto fetch = [&](int J) {
+    // M_J and E_{J-1} two steps ahead, in two register sets used alternately
+    f32x4 mA[MV], mB[MV];
+    float nA[RTW][4], nB[RTW][4];
+    auto fetch = [&](f32x4 (&mr)[MV], float (&nr)[RTW][4], int J) {
         const f32x4 *m = reinterpret_cast<const f32x4 *>(wsM + (int64_t)J * SS);
 #pragma unroll
-        for (int i = 0; i < MV; ++i) mreg[i] = m[tid + NT * i];
+        for (int i = 0; i < MV; ++i) mr[i] = m[tid + NT * i];
+#pragma unroll
+        for (int i = 0; i < RTW; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) nr[i][r] = wsE[(int64_t)(J - 1) * SS + (int64_t)row(i, r) * D + col0 + n16];
     };
-    if (nJ > 1) fetch(nJ - 1);
-    for (int J = nJ - 1;; --J) {
+    // step J: store dS_end(J); unless J = 0, dS_end(J-1) = M_J^T dS_end(J) +
+    // E_{J-1} from (mr, nr), which then take the maps of J - 2; false after J = 0
+    auto step = [&](int J, f32x4 (&mr)[MV], float (&nr)[RTW][4]) {
 #pragma unroll
         for (int i = 0; i < RTW; ++i)
 #pragma unroll
@@ -920,21 +934,16 @@ __global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
                 sS[row(i, r) * LS + n16] = acc[i][r];
                 wsDe[(int64_t)J * SS + (int64_t)row(i, r) * D + col0 + n16] = acc[i][r];
             }
-        if (J == 0) break;
-        float nv[RTW][4];
-#pragma unroll
-        for (int i = 0; i < RTW; ++i)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) nv[i][r] = wsE[(int64_t)(J - 1) * SS + (int64_t)row(i, r) * D + col0 + n16];
+        if (J == 0) return false;
 #pragma unroll
         for (int i = 0; i < MV; ++i) {
             const int e = 4 * (tid + NT * i);
-            *reinterpret_cast<f32x4 *>(&sM[(e / D) * LDM + e % D]) = mreg[i];
+            *reinterpret_cast<f32x4 *>(&sM[(e / D) * LDM + e % D]) = mr[i];
         }
         __syncthreads();
-        if (J - 1 >= 1) fetch(J - 1);
 #pragma unroll
-        for (int i = 0; i < RTW; ++i) acc[i] = f32x4{nv[i][0], nv[i][1], nv[i][2], nv[i][3]};
+        for (int i = 0; i < RTW; ++i) acc[i] = f32x4{nr[i][0], nr[i][1], nr[i][2], nr[i][3]};
+        if (J - 2 >= 1) fetch(mr, nr, J - 2);
 #pragma unroll 4
         for (int m = 0; m < D / 4; ++m) {
             const float bv = sS[(4 * m + q4) * LS + n16];
@@ -944,7 +953,12 @@ __global__ void __launch_bounds__(256) k_gdn_dscan(GdnArgs a) {
                                                               0, 0, 0);
         }
         __syncthreads();
-    }
+        return true;
+    };
+    if (nJ > 1) fetch(mA, nA, nJ - 1);
+    if (nJ > 2) fetch(mB, nB, nJ - 2);
+    for (int J = nJ - 1;; J -= 2)
+        if (!step(J, mA, nA) || !step(J - 1, mB, nB)) break;
 }
 
 // Parameter gradients of one chunk per item (b, h, chunk), items in a
