@@ -79,6 +79,30 @@ __device__ __forceinline__ void gdn_diag_column(const float *M, int ld, int c, c
         for (int r = s2 + 1; r < 16; ++r) acc[r] = fmaf(M[r * ld + s2], x[s2], acc[r]);
     }
 }
+// The same column, the same sums in the same order (so the same bits), row by
+// row for a kernel short of registers (ld a multiple of 4, M 16-byte aligned):
+// row r's part left of the diagonal is read with 16-byte loads that do not
+// depend on x, and the row scales are read up front, so the rows are selected
+// arithmetically (a load under the per-lane condition r > c made every row a
+// branch with its own wait).
+__device__ __forceinline__ void gdn_diag_column_rows(const float *M, int ld, int c, const float *rs, float (&x)[16]) {
+    float rv[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) rv[r] = rs ? rs[r] : 1.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        float acc = 0.f;
+#pragma unroll
+        for (int m = 0; 4 * m < r; ++m) {
+            const f32x4 mv = *reinterpret_cast<const f32x4 *>(M + r * ld + 4 * m);
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (4 * m + u < r) acc = fmaf(mv[u], x[4 * m + u], acc);
+        }
+        const float y = -rv[r] * acc;
+        x[r] = r > c ? y : (r == c ? 1.f : 0.f);
+    }
+}
 
 // T = (I + A)^{-1} for the strictly lower 64 x 64 A = diag(rs) M with M in sA
 // (pitch C + 4; rs == nullptr: A = M), into sT (fp32, pitch C + 4, zero above
@@ -95,7 +119,7 @@ __device__ __forceinline__ void gdn_tinv(int tid, const float *sA, float *sT, co
     if (tid < 64) {
         const int o = 16 * (tid >> 4), c = tid & 15;
         float x[16];
-        gdn_diag_column(sA + o * LA + o, LA, c, rs ? rs + o : nullptr, x);
+        gdn_diag_column_rows(sA + o * LA + o, LA, c, rs ? rs + o : nullptr, x);
 #pragma unroll
         for (int r = 0; r < 16; ++r) sT[(o + r) * LT + o + c] = x[r];
     }
