@@ -349,13 +349,13 @@ def study_main(args):
     inp = synth.make_inputs(w, device=dev, seed=1002)
     T = inp["q"].shape[1]
     if args.tune_ts:
-        cands = [(ts, ov) for ts in tune.ts_candidates(w["seg_lens"]) for ov in (True, False)]
+        cands = [(ts, ov) for ts in tune.ts_candidates(w["seg_lens"]) for ov in (1, 0, 2)]
 
         def time_fn(c):
             return time_steps(torch, make_chain_step(sf, torch, inp, w["seg_lens"], c[0], c[1]), 1, args.steps)
 
         best, table = tune.search(cands, time_fn)
-        sp = tune.speedups(table, (0, True))
+        sp = tune.speedups(table, (0, 1))
         rows = [dict(ts=r["candidate"][0] or "auto", overlap=r["candidate"][1], ms=r["ms"], status=r["status"],
                      speedup_vs_auto_overlap=x) for r, x in zip(table, sp)]
         out = dict(study="superchunk stride and scan overlap", workload=w["name"], steps=args.steps, table=rows,
@@ -615,7 +615,10 @@ def bench_recurrence(args):
     seg = w["seg_lens"]
     pick = tuned.choice(w["name"])  # the profiled per-shape setting (ts, overlap)
     ts = args.ts if args.ts is not None else pick["ts"]
-    overlap = (not args.no_overlap) if (args.no_overlap or args.overlap) else pick["overlap"]
+    if args.no_overlap or args.overlap or args.overlap_prep:
+        overlap = 0 if args.no_overlap else (2 if args.overlap_prep else 1)
+    else:
+        overlap = pick["overlap"]
     # inputs below ~2 GiB could sit partly in the 256 MB MALL between steps
     in_bytes = sum(inp[k].numel() * inp[k].element_size() for k in ("q", "k", "v", "g", "dO"))
     flush = Flusher(torch, dev, MALL_FLUSH_MIB if in_bytes < (2 << 30) else 0)
@@ -649,15 +652,18 @@ def bench_recurrence(args):
 
     # Split-and-overlap figures (Sec. 3.4): the same step with the scans
     # serialised on the main stream, the scans' own time there, and with them
-    # overlapped on the aux stream.
+    # overlapped on the aux stream (the scans alone, then each segment's
+    # preparation kernel with its scan).
     ov = {"default_overlap": overlap}
     if not args.no_overlap_study:
         timer.select(["scan"])
         t_serial = timed_steps(torch, lambda: step(timer, overlap=False), args.steps, flush)
         t_scan = timer.read().get("scan", (0.0, 0))[0] / args.steps
-        t_over = timed_steps(torch, lambda: step(None, overlap=True), args.steps, flush)
+        t_over = timed_steps(torch, lambda: step(None, overlap=1), args.steps, flush)
+        t_over2 = timed_steps(torch, lambda: step(None, overlap=2), args.steps, flush)
         t_intra = t_serial - t_scan
-        ov.update(t_e2e_ms=ms, t_overlapped_ms=t_over, t_serial_ms=t_serial, t_scan_serial_ms=t_scan,
+        ov.update(t_e2e_ms=ms, t_overlapped_ms=t_over, t_overlapped_prep_ms=t_over2, t_serial_ms=t_serial,
+                  t_scan_serial_ms=t_scan,
                   t_intra_only_ms=t_intra, e2e_over_intra_only=ms / t_intra if t_intra > 0 else None,
                   hidden_frac_of_scan=(t_serial - t_over) / t_scan if t_scan > 0 else None)
     # The superchunk states: replayed by the backward (the default: the paper's
@@ -717,6 +723,8 @@ def main():
     ap.add_argument("--ts", type=int, default=None, help="superchunk length (0: automatic; default: the tuned one)")
     ap.add_argument("--no-overlap", action="store_true", help="scans serialised on the main stream")
     ap.add_argument("--overlap", action="store_true", help="scans overlapped on the aux stream")
+    ap.add_argument("--overlap-prep", action="store_true",
+                    help="each segment's preparation kernel and scan on the aux stream")
     ap.add_argument("--no-overlap-study", action="store_true",
                     help="skip the serial / overlapped comparison after the timed steps")
     ap.add_argument("--keep-states", action="store_true",

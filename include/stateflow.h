@@ -143,7 +143,13 @@ typedef struct sf_tuning {
     int32_t overlap;  /* chain calls: 1 (default when aux != NULL) runs the
                          state scans on the aux stream overlapped with the
                          neighbouring segment's dense kernels (Sec. 3.4
-                         "Split and Overlap"); 0 serialises on main. */
+                         "Split and Overlap"); 2 (scalar and vector gate)
+                         also moves each segment's preparation kernel to
+                         aux, ahead of its scan, so that Pre and ST of one
+                         segment run beside the output (or gradient)
+                         kernels of its neighbour; 0 serialises on main.
+                         Other values are rejected (SF_E_SHAPE); the delta
+                         rule's chain treats 2 as 1. */
     int32_t reserved[4];
     sf_timing *timing; /* NULL: no timing (see sf_timing) */
 } sf_tuning;
@@ -238,7 +244,8 @@ size_t sf_chain_ckpt_bytes(const sf_shape *shape, int32_t n_seg, const int64_t *
  *          shape, segments and tuning.
  * With aux != NULL and overlap enabled, each segment's state scan runs on aux
  * concurrently with the next segment's preparation and the previous
- * segment's output kernels (Sec. 3.4, fwd split-and-overlap schedule); both
+ * segment's output kernels (Sec. 3.4, fwd split-and-overlap schedule; with
+ * overlap = 2 the preparation runs on aux too, ahead of the scan); both
  * streams must belong to the current device.  On return the work is
  * enqueued on main and aux, and main carries a dependency on all of it.
  */

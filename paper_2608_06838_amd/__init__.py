@@ -50,11 +50,22 @@ def _stream_handle(s):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _overlap_mode(overlap):
+    """False / True select modes 0 / 1; the integers 0, 1, 2 pass through
+    (2: the preparation kernels on the aux stream as well, see sf_tuning)."""
+    if isinstance(overlap, bool):
+        return int(overlap)
+    m = int(overlap)
+    if m not in (0, 1, 2):
+        raise ValueError(f"overlap must be a bool or 0, 1 or 2, got {overlap!r}")
+    return m
+
+
 def _tuning(ts=0, overlap=True, timing=None):
     """timing: a timing.KernelTimer whose record the call's launches use."""
     t = _lib.SfTuning()
     t.ts = int(ts)
-    t.overlap = 1 if overlap else 0
+    t.overlap = _overlap_mode(overlap)
     if timing is not None:
         t.timing = ctypes.pointer(timing.rec)
     return t
@@ -203,11 +214,11 @@ def _aux_for(device, aux_stream, overlap):
 def _pick(q, g, seg_lens, ts, overlap):
     """ts / overlap left as None take the profiled per-shape setting."""
     if ts is not None and overlap is not None:
-        return int(ts), bool(overlap)
+        return int(ts), _overlap_mode(overlap)
     B, L, H, D = q.shape
     t = tuned.lookup(B, H, D, "bf16" if q.dtype == torch.bfloat16 else "f32",
                      "vector" if g.dim() == 4 else "scalar", seg_lens)
-    return (t["ts"] if ts is None else int(ts)), (t["overlap"] if overlap is None else bool(overlap))
+    return (t["ts"] if ts is None else int(ts)), _overlap_mode(t["overlap"] if overlap is None else overlap)
 
 
 def chain_ckpt_bytes(q, g, seg_lens, ts=None, overlap=None):
@@ -233,7 +244,11 @@ def chain_fwd(q, k, v, g, seg_lens, S_init=None, *, ts=None, overlap=None, strea
     preallocated (o, S_bnd, workspace) buffers.  keep_states=True also returns
     the superchunk states (a uint8 device tensor of chain_ckpt_bytes bytes, or
     a caller's buffer given as out[3]) for chain_bwd(ckpt=...), which then
-    skips replaying them; the results are the same.
+    skips replaying them; the results are the same.  overlap: None takes the
+    profiled per-shape setting; False / 0 serialises on `stream`; True / 1
+    runs the state scans on the aux stream; 2 runs each segment's
+    preparation kernel there as well, ahead of its scan.  ts and overlap do
+    not change the results.
     """
     _same_layout(q, k, v)
     sh = _shape(q, g)

@@ -303,6 +303,8 @@ WsLayout ws_layout(const Shape &r, int64_t L, int ts, bool bwd) {
 // the begin and end timestamps of its own dispatch packets.  The library keeps
 // nothing: the pairs, the count and the kinds live in the caller's record.
 sf_status check_timing(const sf_tuning *t) {
+    if (t && (t->overlap < 0 || t->overlap > 2))
+        return fail(SF_E_SHAPE, "tuning.overlap must be 0, 1 or 2 (got %d)", t->overlap);
     const sf_timing *tm = t ? t->timing : nullptr;
     if (!tm) return SF_OK;
     if (tm->capacity < 0 || tm->count < 0 || tm->count > tm->capacity)
@@ -906,6 +908,7 @@ sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
     const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
     hipStream_t mn = (hipStream_t)main_s;
     hipStream_t ax = (aux_s && (!tuning || tuning->overlap != 0)) ? (hipStream_t)aux_s : mn;
+    const bool prep_aux = ax != mn && tuning && tuning->overlap == 2;
     hipEvent_t e0 = nullptr, e1 = nullptr, sd[2] = {nullptr, nullptr};
     if (ax != mn) TRY(events(e0, e1, sd));
     if (ax != mn) TRY(dep(mn, ax, e0));  // aux sees everything queued on main so far
@@ -942,8 +945,13 @@ sf_status sf_chain_fwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
     for (int i = 0; i < n_seg; ++i) {
         Seg &s = segs[i];
         if (s.n > 1) {
-            TRY(fwd_prep(r, s, mn));
-            TRY(dep(mn, ax, e0));  // prep(i) done (and any main-side S_bnd[i] producer)
+            if (prep_aux) {
+                TRY(dep(mn, ax, e0));  // slot i%2 free (Out(i-2) done) and any main-side S_bnd[i] producer
+                TRY(fwd_prep(r, s, ax));
+            } else {
+                TRY(fwd_prep(r, s, mn));
+                TRY(dep(mn, ax, e0));  // prep(i) done (and any main-side S_bnd[i] producer)
+            }
             TRY(fwd_scan(r, s, ax));
             if (ax != mn) TRY(record(sd[i % 2], ax));
         }
@@ -995,6 +1003,7 @@ sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
     const int64_t SSB = (int64_t)r.B * r.H * r.D * r.D;
     hipStream_t mn = (hipStream_t)main_s;
     hipStream_t ax = (aux_s && (!tuning || tuning->overlap != 0)) ? (hipStream_t)aux_s : mn;
+    const bool prep_aux = ax != mn && tuning && tuning->overlap == 2;
     hipEvent_t e0 = nullptr, e1 = nullptr, sd[2] = {nullptr, nullptr};
     if (ax != mn) TRY(events(e0, e1, sd));
     if (ax != mn) TRY(dep(mn, ax, e0));
@@ -1035,8 +1044,13 @@ sf_status sf_chain_bwd(const sf_shape *shape, int32_t n_seg, const int64_t *seg_
     for (int i = n_seg - 1; i >= 0; --i) {
         Seg &s = segs[i];
         if (s.n > 1) {
-            TRY(bwd_prep(r, s, mn));
-            TRY(dep(mn, ax, e0));
+            if (prep_aux) {
+                TRY(dep(mn, ax, e0));  // slot i%2 free (the gradients of i+2 done) and any main-side dS producer
+                TRY(bwd_prep(r, s, ax));
+            } else {
+                TRY(bwd_prep(r, s, mn));
+                TRY(dep(mn, ax, e0));
+            }
             TRY(bwd_scan(r, s, ax));
             if (ax != mn) TRY(record(sd[i % 2], ax));
         }

@@ -227,6 +227,24 @@ def test_chain_validation():
     assert rc == _lib.SF_E_NULL  # dS_init missing
 
 
+def test_overlap_mode_validation():
+    """tuning.overlap takes 0, 1 or 2; anything else is rejected before any launch."""
+    L = _lib.lib()
+    s = shape()
+    segs = (ctypes.c_int64 * 2)(512, 512)
+    for bad in (-1, 3):
+        t = _tuning()
+        t.overlap = bad
+        assert fwd(s, tun=t) == _lib.SF_E_SHAPE
+        rc = L.sf_chain_fwd(ctypes.byref(s), 2, segs, p(1), p(2), p(3), p(4), p(5), p(6), None, 0, p(7), 1 << 30,
+                            ctypes.byref(t), None, None)
+        assert rc == _lib.SF_E_SHAPE
+    import paper_2608_06838_amd as sf
+    assert sf._overlap_mode(True) == 1 and sf._overlap_mode(False) == 0 and sf._overlap_mode(2) == 2
+    with pytest.raises(ValueError):
+        sf._overlap_mode(3)
+
+
 def test_timing_validation():
     """A caller's timing record is checked before any launch."""
     tm = _lib.SfTiming()

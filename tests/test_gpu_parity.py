@@ -159,16 +159,18 @@ def check_chain(io, inp, got, seg_lens, pairs=None):
 
 @pytest.mark.parametrize("ts", [0, 64, 128])
 def test_chain_nonuniform_small(ts):
-    """Four nonuniform segments, chained; overlap on and off agree bitwise."""
+    """Four nonuniform segments, chained; every overlap mode (serial, scans on
+    the aux stream, preparation and scans there) agrees bitwise."""
     w = synth.workload("mid_bf16", B=1, H=4, D=128)
     seg_lens = [192, 64, 320, 128]
     inp = synth.make_inputs(w, device="cpu", seed=11, dS_out_std=0.1, L=sum(seg_lens))
     g = on_gpu(inp)
     say(f"[chain] small nonuniform ts={ts}")
     a = run_chain(g, seg_lens, ts=ts, overlap=True)
-    b = run_chain(g, seg_lens, ts=ts, overlap=False)
-    for key in a:
-        assert torch.equal(a[key], b[key]), key
+    for mode in (False, 2):
+        b = run_chain(g, seg_lens, ts=ts, overlap=mode)
+        for key in a:
+            assert torch.equal(a[key], b[key]), (key, mode)
     check_chain("bf16", inp, a, seg_lens)
 
 
@@ -186,7 +188,7 @@ def test_kept_states(name, D, io, ts):
     inp = synth.make_inputs(w, device="cpu", seed=53 + D + ts, dS_out_std=0.1, L=sum(seg_lens))
     g = on_gpu(inp)
     say(f"[chain] kept states {name} D={D} {io} ts={ts}")
-    for overlap in (False, True):
+    for overlap in (False, True, 2):
         a = run_chain(g, seg_lens, ts=ts, overlap=overlap)
         b = run_chain(g, seg_lens, ts=ts, overlap=overlap, keep=True)
         for key in a:
@@ -263,9 +265,10 @@ def test_vector_gate_chain_nonuniform(ts):
     g = on_gpu(inp)
     say(f"[chain] vector gate nonuniform ts={ts}")
     a = run_chain(g, seg_lens, ts=ts, overlap=True)
-    b = run_chain(g, seg_lens, ts=ts, overlap=False)
-    for key in a:
-        assert torch.equal(a[key], b[key]), key
+    for mode in (False, 2):
+        b = run_chain(g, seg_lens, ts=ts, overlap=mode)
+        for key in a:
+            assert torch.equal(a[key], b[key]), (key, mode)
     check_chain("bf16", inp, a, seg_lens)
 
 
