@@ -8,7 +8,8 @@ Default workload: B=1, H=40, d=128, L=262144 in 8 nonuniform segments
 --workload selects the other shapes (tiny_fp32, mid_bf16, vector_gate,
 scan_stress); --conv and --gdn the short convolution and the gated delta rule.
 
-Prints one JSON line ("Measurement").
+Prints one JSON line: the metric, the dominant kernel's roofline (algorithmic
+bytes or flops per launch over its HIP-event time) and the oracle's CPU baseline.
 """
 import argparse
 import hashlib
@@ -31,7 +32,7 @@ MALL_FLUSH_MIB = 512  # written between timed steps of workloads whose inputs ar
 #   bwd_prep: q, k, v, dO, g     bwd_dq: dO, v, k, q, g in; dq, dg out
 #   bwd_dkv:  q, k, v, dO, g, dg in; dk, dv, dg out
 # gb = bytes of one token-head's gate (4 scalar, 4*D per-key-channel); the
-# per-key-channel backward runs dv and dk as two walks
+# per-key-channel backward runs dv and dk as two walks, each reading its inputs
 KERNEL_BYTES = {
     "fwd_prep": lambda D, io, gb: 2 * D * io + gb,
     "fwd_out": lambda D, io, gb: 4 * D * io + gb,
@@ -43,9 +44,9 @@ RECURRENCE_KERNELS = ["fwd_prep", "scan", "fwd_out", "bwd_prep", "bwd_dq", "bwd_
 
 
 def alg_flops_per_token_head(D, C=64):
-    """Causal-tile algorithmic flops of one fwd+bwd per token and head (see
-    the design doc): fwd (C+1)(2D) + 4 D^2; bwd incl. the state replay
-    (C+1)(5D) + 10 D^2."""
+    """Causal-tile algorithmic flops of one fwd+bwd per token and head (2 per
+    multiply-add, causal score tiles at their triangular size): fwd
+    (C+1)(2D) + 4 D^2; bwd incl. the state replay (C+1)(5D) + 10 D^2."""
     return (C + 1) * 2 * D + 4 * D * D + (C + 1) * 5 * D + 10 * D * D
 
 
@@ -393,7 +394,7 @@ def gdn_dchunk_flops(D, C=64):
     """Algorithmic flops per 64-token chunk and head of the delta rule's
     per-chunk parameter gradients, given the state S entering the chunk and
     the gradient dS' of the state leaving it (2 m n k per product, triangular
-    factors at their triangular size, gated delta rule):
+    factors at their triangular size):
       five C x D x D products (K S, K dS', G_U S^T, dO S^T, U dS'^T): 10 C D^2;
       lower-triangular-with-diagonal C x C products (Q K^T, T R, P^T dO, T^T dU,
       dO U^T, (dP o Gamma) K, (dP o Gamma)^T Q): 7 C (C + 1) D;

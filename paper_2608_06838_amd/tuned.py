@@ -25,8 +25,8 @@ DEFAULT = dict(ts=0, overlap=False)
 _SEG_256K = (65536, 40960, 32768, 28672, 26624, 24576, 22528, 20480)
 
 # Profiled on MI355X (bench.py --tune-ts, fwd+bwd chain steps, best of the
-# ts x overlap grid, tuner section).  ts = 0 where the library's
-# per-segment choice beat every fixed stride.
+# ts x overlap-mode grid).  ts = 0 where the library's per-segment choice beat
+# every fixed stride.
 TABLE = {
     (1, 2, 64, "f32", "scalar", (1024,)): dict(ts=0, overlap=False),
     (1, 16, 128, "bf16", "scalar", (4096,) * 8): dict(ts=256, overlap=2),
