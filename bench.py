@@ -748,8 +748,9 @@ def main():
                     help="per-call study over heads 20/10/8 and 8K-64K tokens: superchunk length x split fraction")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the recurrence shards over "
-              "heads with no exchange, see DESIGN.md", file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); across GPUs the recurrence would "
+              "shard over heads (no exchange) or over sequence segments (boundary states passed on)",
+              file=sys.stderr)
         sys.exit(2)
     if args.conv:
         bench_conv(args)
