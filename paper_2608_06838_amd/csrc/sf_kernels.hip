@@ -434,15 +434,9 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         const float b2 = wave_scan_dpp(gl * LOG2E);
         const float b63 = lane_value(b2, 63);
         __syncthreads();
-        if constexpr (DQ) {  // q.dq of the previous chunk
-            if (w == 0 && c > 0) {
-                float r = 0.f;
-#pragma unroll
-                for (int ww = 0; ww < NW; ++ww) r += sred[ww * C + lane];
-                dgp[(int64_t)((c - 1) * C + lane) * a.sg_l] = r;
-            }
-        }
-        if (w == 0) {
+        // the decay tables and (dq walk) the previous chunk's q.dq sums come from
+        // the last wave, which forms one score tile fewer than wave 0
+        if (w == NW - 1) {
             sb[lane] = b2;
             sq[lane] = fexp2(b2);
             se[lane] = fexp2(b63 - b2);
@@ -456,6 +450,14 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
         if (c + 1 < d.nch) issue1(c + 1);
         __syncthreads();
         if (c + 1 < d.nch) issue2(c + 1);
+        if constexpr (DQ) {  // q.dq of the previous chunk, beside the scores
+            if (w == NW - 1 && c > 0) {
+                float r = 0.f;
+#pragma unroll
+                for (int ww = 0; ww < NW; ++ww) r += sred[ww * C + lane];
+                dgp[(int64_t)((c - 1) * C + lane) * a.sg_l] = r;
+            }
+        }
 
         // scores P^T[s][t] = sum_ch X2[s][ch] X1[t][ch] on the causal tiles -> A[t][s]
         for (int i = w; i < 10; i += NW) {
