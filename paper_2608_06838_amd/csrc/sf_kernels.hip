@@ -287,9 +287,15 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
 // The score tiles XOR their 16-byte blocks by bit 2 of the row and the output
 // staging tile uses a 16-byte-odd pitch: both halve the bank conflicts of the
 // 8-byte accumulator-row writes.
-template <typename T, int D, int NCT, bool DQ>
-__global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k_walk(SegArgs a) {
-    constexpr int NW = D / (16 * NCT), NT = 64 * NW, NK = D / 16;
+// CS > 1 (output walk only): the state's columns are split over CS workgroups
+// per item, each staging the whole chunk and forming the scores but keeping
+// and writing only its D / CS columns; for launches with fewer items than CUs.
+// The CS workgroups of an item lie 8 apart in dispatch order (one XCD, so the
+// second read of a tile meets L2).
+template <typename T, int D, int NCT, bool DQ, int CS = 1>
+__global__ void __launch_bounds__(64 * D / (16 * NCT * CS), sizeof(T) == 2 ? 2 : 1) k_walk(SegArgs a) {
+    static_assert(CS == 1 || (CS == 2 && !DQ), "column split: output walk, two parts");
+    constexpr int NW = D / (16 * NCT * CS), NT = 64 * NW, NK = D / 16;
     constexpr int LDN = D + pad<T>(), LDT = C + pad<T>(), SWX = swx<T, D>();
     constexpr bool SP = kSplitScores<T>, SPS = kSplitState<T>, SPD = kSplitDecay<T>;
     __shared__ __attribute__((aligned(16))) T sX1[C * LDN];
@@ -308,7 +314,11 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     __shared__ float sred[DQ ? NW * C : 1];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, q4 = lane >> 4, n16 = lane & 15;
-    const Decode d = decode(a);
+    const int blk = (int)blockIdx.x;
+    const int half = CS > 1 ? (blk >> 3) & 1 : 0, item = CS > 1 ? (blk >> 4) * 8 + (blk & 7) : blk;
+    if (CS > 1 && item >= a.B * a.H * a.n_super) return;  // the last group of 8 items is ragged
+    const int wc = w + NW * half;  // the wave's place among the D / (16 NCT) column owners
+    const Decode d = decode(a, item);
     const LaneOff tro = tr_off<T, LDN, SWX>(lane), swo = swz_off<T, LDN, SWX>(lane);
     // bf16: the state's rows are read into the update's A operands in the order
     // that puts channels 8q..8q+7 of each 32-channel block in lane row q of the
@@ -323,8 +333,8 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     // the output accumulators, so its q values and its output row segments are
     // single 16-byte accesses: column n of tile ct is channel scol(ct, n)
     constexpr bool CP = RP && NCT == 2;
-    auto scol = [&](int ct, int n) { return CP ? 32 * w + 8 * (n >> 2) + 4 * ct + (n & 3) : 16 * (NCT * w + ct) + n; };
-    const int ccol0 = CP ? 32 * w : 16 * NCT * w, ccstep = CP ? 4 : 16;  // ldfragTR column of tile ct
+    auto scol = [&](int ct, int n) { return CP ? 32 * wc + 8 * (n >> 2) + 4 * ct + (n & 3) : 16 * (NCT * wc + ct) + n; };
+    const int ccol0 = CP ? 32 * wc : 16 * NCT * wc, ccstep = CP ? 4 : 16;  // ldfragTR column of tile ct
     const LaneOff troc = CP ? tro8 : tro;
     const int64_t xo = d.b * a.sx_b + d.h * a.sx_h + d.tok0 * a.sx_l;
     const T *X1 = (const T *)(DQ ? a.dO : a.q) + xo;
@@ -367,7 +377,7 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
     uint32_t toff[Tile<T, D, NT>::RPT];
     Tile<T, D, NT>::offsets(toff, a.sx_l, tid);
     const uint32_t goff = (uint32_t)(lane * a.sg_l * 4);
-    const uint32_t aoff = (uint32_t)((n16 * a.sx_l + (CP ? 32 * w + 8 * q4 : 16 * NCT * w + 4 * q4)) * (int64_t)sizeof(T));
+    const uint32_t aoff = (uint32_t)((n16 * a.sx_l + (CP ? 32 * wc + 8 * q4 : 16 * NCT * wc + 4 * q4)) * (int64_t)sizeof(T));
     const uint32_t tstep = (uint32_t)(16 * a.sx_l * (int64_t)sizeof(T));
     // the next chunk's tiles go out in three batches (X1 and g at staging, X2 at
     // the start of the scores, X3 at the start of the output products), so the
@@ -405,20 +415,21 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT), sizeof(T) == 2 ? 2 : 1) k
             typedef T vec8T __attribute__((ext_vector_type(8)));
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
-                *reinterpret_cast<vec8T *>(&sY[(16 * tt + n16) * LDY + 32 * w + 8 * q4]) =
+                *reinterpret_cast<vec8T *>(&sY[(16 * tt + n16) * LDY + 32 * wc + 8 * q4]) =
                     __builtin_shufflevector(yo[0][tt], yo[1][tt], 0, 1, 2, 3, 4, 5, 6, 7);
         } else {
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
                 for (int tt = 0; tt < 4; ++tt)
-                    *reinterpret_cast<vec4T *>(&sY[(16 * tt + n16) * LDY + 16 * (NCT * w + ct) + 4 * q4]) = yo[ct][tt];
+                    *reinterpret_cast<vec4T *>(&sY[(16 * tt + n16) * LDY + 16 * (NCT * wc + ct) + 4 * q4]) = yo[ct][tt];
         }
     };
     auto store_y = [&](int cp) {
         typedef typename Tile<T, D, NT>::vecE vecE;
         constexpr int E = Tile<T, D, NT>::E, CB = Tile<T, D, NT>::CB, RPT = Tile<T, D, NT>::RPT;
         const int r0 = (tid / CB) * RPT, ch = (tid % CB) * E;
+        if (CS > 1 && (ch < half * (D / CS) || ch >= (half + 1) * (D / CS))) return;  // another part's columns
         const rsrc_t ry = buf_rsrc(Y + cp * cstep, cspan);
 #pragma unroll
         for (int j = 0; j < RPT; ++j) buf_st(ry, toff[j], 0, *reinterpret_cast<const vecE *>(&sY[(r0 + j) * LDY + ch]));
@@ -1233,7 +1244,17 @@ static hipError_t launch_td(int kind, const SegArgs &a, hipStream_t s, hipEvent_
     constexpr int NTW = 64 * D / (16 * SF_NCT_WALK);
     switch (kind) {
     case SF_K_FWD_PREP: hipExtLaunchKernelGGL((k_prep<T, D, SF_NCT_PREP, false>), grid, dim3(NTP), 0, s, e0, e1, 0, a); break;
-    case SF_K_FWD_OUT: hipExtLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, false>), grid, dim3(NTW), 0, s, e0, e1, 0, a); break;
+    case SF_K_FWD_OUT:
+        // a launch that would leave half the CUs idle splits the state's columns
+        // over two workgroups per item (scan-bound workload: 5.15 -> 4.98 ms per
+        // step; at one item per CU the split measured slower)
+        if (sizeof(T) == 2 && D == 128 && 2 * (int64_t)grid.x <= (int64_t)a.n_cu) {
+            hipExtLaunchKernelGGL((k_walk<T, D, 1, false, 2>), dim3((grid.x + 7) / 8 * 16), dim3(64 * D / 32), 0, s, e0,
+                                  e1, 0, a);
+        } else {
+            hipExtLaunchKernelGGL((k_walk<T, D, SF_NCT_WALK, false>), grid, dim3(NTW), 0, s, e0, e1, 0, a);
+        }
+        break;
     case SF_K_BWD_PREP:  // the replay of D_J (the forward's prep), skipped for kept states, then E_J
         if (!a.ckpt)
             hipExtLaunchKernelGGL((k_prep_bwd<T, D, SF_NCT_PREP>), dim3(2 * grid.x), dim3(NTP), 0, s, e0, e1, 0, a);
