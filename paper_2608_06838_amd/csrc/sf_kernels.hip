@@ -289,7 +289,8 @@ __global__ void __launch_bounds__(SCAN_NT) k_scan(SegArgs a, int D) {
 // 8-byte accumulator-row writes.
 // CS > 1 (output walk only): the state's columns are split over CS workgroups
 // per item, each staging the whole chunk and forming the scores but keeping
-// and writing only its D / CS columns; for launches with fewer items than CUs.
+// and writing only its D / CS columns; for launches that would leave half the
+// CUs idle.
 // The CS workgroups of an item lie 8 apart in dispatch order (one XCD, so the
 // second read of a tile meets L2).
 template <typename T, int D, int NCT, bool DQ, int CS = 1>
@@ -446,7 +447,8 @@ __global__ void __launch_bounds__(64 * D / (16 * NCT * CS), sizeof(T) == 2 ? 2 :
         const float b63 = lane_value(b2, 63);
         __syncthreads();
         // the decay tables and (dq walk) the previous chunk's q.dq sums come from
-        // the last wave, which forms one score tile fewer than wave 0
+        // the last wave, which forms no more score tiles than wave 0 (one fewer
+        // with four waves)
         if (w == NW - 1) {
             sb[lane] = b2;
             sq[lane] = fexp2(b2);
